@@ -1,0 +1,510 @@
+"""ProtoKV far-memory hot path -- plain CPU oracle.
+
+TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and the
+cpu_baseline leg of bench.py may import this module.  The product path (the
+HIP library and its Python binding) never imports, calls or links it, and it
+shares no code with that path.
+
+What it computes, in the paper's order and notation (ProtoKV, Sections
+"State representation and prototype bank", "Online update", "Residual
+Statistics and Pseudo-Token Interface"; Appendix Algorithms "ProtoKV
+Streaming Update", "DecodeTopSResidualModes" and "Pseudo-Token Decoding and
+Attention"; Equations 1 (assignment cost), pq (smoothed PQ probability) and
+attn_logit (mass-aware logit); Table tab:default_config for the defaults):
+
+* near tier: a ring of the last W frames of exact KV; appending frame t
+  evicts frame t-W (the oldest) once W frames are resident;
+* far tier: K prototype slots with (sum K, sum V, sum K^2, sum V^2, mass n,
+  PQ histograms H^K, H^V, n_res, spatial mean mu and covariance Sigma,
+  recency tau);
+* fold of one evicted frame: seed free slots, then assign the remaining
+  tokens with Eq. 1 against the post-seed bank and accumulate them in
+  eviction order;
+* synthesis: S pseudo-tokens per active prototype from the centres plus the
+  top-S PQ residual modes (Alg. DecodeTopSResidualModes), paired by rank;
+* readout: softmax attention over [near KV ; pseudo-tokens] with logit bias
+  log n_k on the pseudo-tokens of prototype k (Eq. attn_logit).
+
+Readings where the paper is silent or at odds with itself (each is listed
+in the design doc):
+
+* centres are running means c_k = sumK_k / n_k (the text's "e.g. via EMA"
+  and the merge rule's mass-weighted means), not Alg. 1's fixed-rate EMA;
+* a fold is frame-batched: all non-seed tokens of the evicted frame are
+  assigned against the bank as it stands after seeding, then accumulated in
+  eviction order (with one token per frame this is Alg. 1's per-token loop);
+* ties in the argmin of Eq. 1 go to the lowest slot; cos is 0 when either
+  vector is zero;
+* d_Mah is the (unsquared) distance sqrt(d^T (Sigma + rho I)^-1 d) with a
+  ridge rho = 1e-4; coordinates are cell centres ((col+.5)/W, (row+.5)/H);
+* tau is the stream position of the most recently absorbed source token; a
+  prototype is idle when (current frame) - (frame of tau) > T_idle frames;
+* PQ residuals are taken against the centre before this fold's updates
+  (the post-seed snapshot); PQ distance is squared Euclidean over
+  contiguous subspaces; code ties go to the lowest codeword;
+* smoothing eps = 1, so every PQ probability is (H+1)/(n_res+C); a code
+  tuple's score sum_g log P is compared exactly through the integer product
+  prod_g (H[g][z_g] + 1) (the denominator is common to all tuples); ties
+  between equal scores go to the lexicographically smaller code tuple;
+* pseudo-tokens are rounded to the KV dtype from the float32 sum c + r;
+  centres are float32(sumK / n).
+
+Precision: the bank is float32 (fp32 prototype statistics) and is updated
+with the explicit float32 operation sequences written below (one IEEE
+rounding per operation, no fused multiply-add); every cost, softmax and
+readout value is float64.
+
+Parity unpinned: eps, rho, the coordinate convention and the time unit of
+T_idle have no numeric anchor in the paper (no worked example, no code); they
+are pinned only by this reading.
+"""
+from __future__ import annotations
+
+import collections
+import dataclasses
+import itertools
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+F32 = np.float32
+
+# Table tab:default_config (Appendix "Default Hyperparameter Configuration").
+TABLE5_DEFAULTS = {
+    "near_far_split": (1, 3),
+    "S": 8,
+    "lambda_sp": 0.1,
+    "lambda_idle": 0.01,
+    "T_idle": 120,
+    "alpha": 0.05,
+    "beta": 0.05,
+    "eta": 0.05,
+    "gamma": 0.05,
+    "eps_K": 0.20,
+    "eps_V": 0.25,
+    "G": 8,
+    "C": 16,
+    "B": 32,
+}
+
+
+@dataclasses.dataclass
+class Params:
+    head_dim: int = 128
+    grid_h: int = 14
+    grid_w: int = 14
+    window_frames: int = 8
+    capacity: int = 256
+    S: int = TABLE5_DEFAULTS["S"]
+    G: int = TABLE5_DEFAULTS["G"]
+    C: int = TABLE5_DEFAULTS["C"]
+    B: int = TABLE5_DEFAULTS["B"]
+    lambda_sp: float = TABLE5_DEFAULTS["lambda_sp"]
+    lambda_idle: float = TABLE5_DEFAULTS["lambda_idle"]
+    t_idle: int = TABLE5_DEFAULTS["T_idle"]
+    eta: float = TABLE5_DEFAULTS["eta"]
+    ridge: float = 1e-4
+    kv_dtype: str = "bf16"
+    use_pq: bool = True
+    mass_bias: bool = True
+
+    @property
+    def tokens_per_frame(self) -> int:
+        return self.grid_h * self.grid_w
+
+
+# ---------------------------------------------------------------------------
+# small helpers
+# ---------------------------------------------------------------------------
+
+
+def round_kv(x32: np.ndarray, kv_dtype: str) -> np.ndarray:
+    """Round float32 values to the KV dtype (bf16: round to nearest even)."""
+    x32 = np.asarray(x32, dtype=F32)
+    if kv_dtype == "fp32":
+        return x32.copy()
+    bits = x32.view(np.uint32).astype(np.uint64)
+    lsb = (bits >> 16) & 1
+    top = ((bits + 0x7FFF + lsb) >> 16).astype(np.uint32)
+    return (top << 16).view(F32)
+
+
+def spatial_coords(grid_h: int, grid_w: int) -> np.ndarray:
+    """s_j = ((col+0.5)/grid_w, (row+0.5)/grid_h) in float32, raster order j."""
+    out = np.zeros((grid_h * grid_w, 2), dtype=F32)
+    for j in range(grid_h * grid_w):
+        row, col = divmod(j, grid_w)
+        out[j, 0] = F32(col + 0.5) / F32(grid_w)
+        out[j, 1] = F32(row + 0.5) / F32(grid_h)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# prototype bank (far tier)
+# ---------------------------------------------------------------------------
+
+
+class Bank:
+    """B_far = {Pi_k}: one (layer, kv head)'s K prototype slots."""
+
+    def __init__(self, p: Params):
+        K, D, G, C = p.capacity, p.head_dim, p.G, p.C
+        self.n = np.zeros(K, dtype=np.int64)          # mass n_k (0 = inactive)
+        self.sum_k = np.zeros((K, D), dtype=F32)       # sum of absorbed keys
+        self.sum_v = np.zeros((K, D), dtype=F32)
+        self.sq_k = np.zeros((K, D), dtype=F32)        # sum of squared keys
+        self.sq_v = np.zeros((K, D), dtype=F32)
+        self.hist_k = np.zeros((K, G, C), dtype=np.int64)   # H^K
+        self.hist_v = np.zeros((K, G, C), dtype=np.int64)   # H^V
+        self.n_res = np.zeros(K, dtype=np.int64)
+        self.mu = np.zeros((K, 2), dtype=F32)          # spatial mean (x, y)
+        self.sigma = np.zeros((K, 3), dtype=F32)       # (xx, xy, yy)
+        self.tau = np.zeros(K, dtype=np.int64)         # stream position
+
+    def copy(self) -> "Bank":
+        b = Bank.__new__(Bank)
+        for k, v in self.__dict__.items():
+            setattr(b, k, v.copy())
+        return b
+
+
+# ---------------------------------------------------------------------------
+# Eq. 1: continuity-aware assignment cost
+# ---------------------------------------------------------------------------
+
+
+def assignment_costs(keys: np.ndarray, coords: np.ndarray, bank: Bank, t_frame: int,
+                     p: Params) -> np.ndarray:
+    """cost[i, k] = -cos(K_i, c_k) + lambda_sp d_Mah(s_i; mu_k, Sigma_k)
+    + lambda_idle 1[idle(tau_k)]  (Eq. 1), float64; +inf for inactive k.
+
+    cos uses sumK_k (cos is scale invariant, so cos(K, sumK/n) = cos(K, sumK)).
+    """
+    K64 = keys.astype(np.float64)
+    C64 = bank.sum_k.astype(np.float64)
+    dots = K64 @ C64.T
+    nk = np.sqrt((K64 * K64).sum(axis=1))
+    nc = np.sqrt((C64 * C64).sum(axis=1))
+    denom = nk[:, None] * nc[None, :]
+    with np.errstate(invalid="ignore", divide="ignore"):
+        cos = np.where(denom > 0, dots / np.where(denom > 0, denom, 1.0), 0.0)
+
+    # Mahalanobis distance to the prototype's running location distribution.
+    dx = coords[:, 0].astype(np.float64)[:, None] - bank.mu[:, 0].astype(np.float64)[None, :]
+    dy = coords[:, 1].astype(np.float64)[:, None] - bank.mu[:, 1].astype(np.float64)[None, :]
+    A = bank.sigma[:, 0].astype(np.float64) + p.ridge
+    Bxy = bank.sigma[:, 1].astype(np.float64)
+    Cc = bank.sigma[:, 2].astype(np.float64) + p.ridge
+    det = A * Cc - Bxy * Bxy
+    q = (Cc[None, :] * dx * dx - 2.0 * Bxy[None, :] * dx * dy + A[None, :] * dy * dy) / det[None, :]
+    d_mah = np.sqrt(np.maximum(q, 0.0))
+
+    T = p.tokens_per_frame
+    idle = ((t_frame - bank.tau // T) > p.t_idle).astype(np.float64)
+
+    cost = -cos + p.lambda_sp * d_mah + p.lambda_idle * idle[None, :]
+    cost[:, bank.n == 0] = np.inf
+    return cost
+
+
+def argmin_lowest(cost: np.ndarray):
+    """Row argmin (ties -> lowest k) and the top-2 margin (cost2 - cost1)."""
+    idx = np.argmin(cost, axis=1)
+    if cost.shape[1] >= 2:
+        part = np.sort(cost, axis=1)
+        margin = part[:, 1] - part[:, 0]
+    else:
+        margin = np.full(cost.shape[0], np.inf)
+    return idx, margin
+
+
+# ---------------------------------------------------------------------------
+# PQ residual encoding
+# ---------------------------------------------------------------------------
+
+
+def pq_encode(residuals: np.ndarray, codebook: np.ndarray) -> np.ndarray:
+    """Nearest codeword per subspace for float32 residuals [M][D].
+
+    codebook float32 [G][C][D/G]; subspace g covers dims [g*D/G, (g+1)*D/G).
+    dist(g, c) = sum_u (r_u - C[g][c][u])^2 accumulated in float32 with u
+    ascending (one rounding per subtract, multiply and add); ties -> lowest c.
+    """
+    G, C, Dp = codebook.shape
+    M = residuals.shape[0]
+    codes = np.zeros((M, G), dtype=np.int64)
+    for g in range(G):
+        sub = residuals[:, g * Dp:(g + 1) * Dp].astype(F32)
+        acc = np.zeros((M, C), dtype=F32)
+        for u in range(Dp):
+            diff = (sub[:, u][:, None] - codebook[g][None, :, u]).astype(F32)
+            acc = (acc + (diff * diff).astype(F32)).astype(F32)
+        codes[:, g] = np.argmin(acc, axis=1)
+    return codes
+
+
+# ---------------------------------------------------------------------------
+# Alg. "ProtoKV Streaming Update", one evicted frame, frame-batched
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass
+class FoldResult:
+    assign: np.ndarray      # slot per evicted token (seeded tokens: their slot)
+    margin: np.ndarray      # top-2 cost margin (inf for seeded tokens)
+    n_seed: int
+
+
+def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
+               t_frame: int, p: Params, codebooks: np.ndarray) -> FoldResult:
+    """Absorb the evicted frame f_evicted (tokens j = 0..T-1 in raster order)
+    into `bank` (modified in place).  t_frame is the frame being appended.
+
+    codebooks float32 [2][G][C][D/G] (keys, values) of this (layer, head).
+    """
+    T = keys.shape[0]
+    coords = spatial_coords(p.grid_h, p.grid_w)
+    pos = f_evicted * T + np.arange(T)
+    one, eta = F32(1.0), F32(p.eta)
+    keep = F32(one - eta)
+
+    # Initialization: while free slots remain, an evicted token seeds the
+    # lowest free slot (c <- K, p <- V, n <- 1, mu <- s, Sigma <- I, R <- 0).
+    free = [k for k in range(p.capacity) if bank.n[k] == 0]
+    n_seed = min(T, len(free))
+    assign = np.full(T, -1, dtype=np.int64)
+    margin = np.full(T, np.inf)
+    for j in range(n_seed):
+        k = free[j]
+        kk, vv = keys[j].astype(F32), values[j].astype(F32)
+        bank.n[k] = 1
+        bank.sum_k[k] = kk
+        bank.sum_v[k] = vv
+        bank.sq_k[k] = (kk * kk).astype(F32)
+        bank.sq_v[k] = (vv * vv).astype(F32)
+        bank.hist_k[k] = 0
+        bank.hist_v[k] = 0
+        bank.n_res[k] = 0
+        bank.mu[k] = coords[j]
+        bank.sigma[k] = np.array([1.0, 0.0, 1.0], dtype=F32)
+        bank.tau[k] = pos[j]
+        assign[j] = k
+    if n_seed == T:
+        return FoldResult(assign, margin, n_seed)
+
+    # Assignment (Eq. 1) of the remaining tokens against the post-seed bank.
+    snap = bank.copy()
+    rest = np.arange(n_seed, T)
+    cost = assignment_costs(keys[rest], coords[rest], snap, t_frame, p)
+    idx, marg = argmin_lowest(cost)
+    assign[rest] = idx
+    margin[rest] = marg
+
+    # Residual codes against the snapshot centres c = f32(sumK / n).
+    if p.use_pq:
+        nf = snap.n[idx].astype(F32)[:, None]
+        c_snap = (snap.sum_k[idx] / nf).astype(F32)
+        p_snap = (snap.sum_v[idx] / nf).astype(F32)
+        r_k = (keys[rest].astype(F32) - c_snap).astype(F32)
+        r_v = (values[rest].astype(F32) - p_snap).astype(F32)
+        codes_k = pq_encode(r_k, codebooks[0])
+        codes_v = pq_encode(r_v, codebooks[1])
+
+    # Prototype update, tokens in eviction order.
+    for i, j in enumerate(rest):
+        k = idx[i]
+        kk, vv = keys[j].astype(F32), values[j].astype(F32)
+        bank.n[k] += 1
+        bank.sum_k[k] = (bank.sum_k[k] + kk).astype(F32)
+        bank.sum_v[k] = (bank.sum_v[k] + vv).astype(F32)
+        bank.sq_k[k] = (bank.sq_k[k] + (kk * kk).astype(F32)).astype(F32)
+        bank.sq_v[k] = (bank.sq_v[k] + (vv * vv).astype(F32)).astype(F32)
+        if p.use_pq:
+            for g in range(p.G):
+                bank.hist_k[k, g, codes_k[i, g]] += 1
+                bank.hist_v[k, g, codes_v[i, g]] += 1
+            bank.n_res[k] += 1
+        # spatial state: mu <- (1-eta) mu + eta s, then
+        # Sigma <- (1-eta) Sigma + eta (s - mu)(s - mu)^T with the new mu.
+        s = coords[j]
+        mx = F32(F32(keep * bank.mu[k, 0]) + F32(eta * s[0]))
+        my = F32(F32(keep * bank.mu[k, 1]) + F32(eta * s[1]))
+        bank.mu[k, 0], bank.mu[k, 1] = mx, my
+        ddx, ddy = F32(s[0] - mx), F32(s[1] - my)
+        sxx, sxy, syy = bank.sigma[k]
+        bank.sigma[k, 0] = F32(F32(keep * sxx) + F32(eta * F32(ddx * ddx)))
+        bank.sigma[k, 1] = F32(F32(keep * sxy) + F32(eta * F32(ddx * ddy)))
+        bank.sigma[k, 2] = F32(F32(keep * syy) + F32(eta * F32(ddy * ddy)))
+        bank.tau[k] = pos[j]
+    return FoldResult(assign, margin, n_seed)
+
+
+# ---------------------------------------------------------------------------
+# Eq. pq and Alg. "DecodeTopSResidualModes"
+# ---------------------------------------------------------------------------
+
+
+def _order_key(score: int, codes: Tuple[int, ...]):
+    return (-score, codes)
+
+
+def decode_top_s(hist: np.ndarray, S: int, B: int) -> List[Tuple[int, ...]]:
+    """Top-S code tuples of one PQ histogram H [G][C] by beam search (Alg. 3).
+
+    With eps = 1, log P(g, c) = log(H[g][c] + 1) - log(n_res + C); a tuple
+    scores sum_g log P(g, z_g), so the ranking equals that of the integer
+    prod_g (H[g][z_g] + 1), compared exactly.  TopB / TopS keep the highest
+    scores; equal scores keep the lexicographically smaller code tuple.
+    """
+    G, C = hist.shape
+    beam: List[Tuple[int, Tuple[int, ...]]] = [(1, ())]
+    for g in range(G):
+        expanded = []
+        for score, codes in beam:
+            for c in range(C):
+                expanded.append((score * (int(hist[g, c]) + 1), codes + (c,)))
+        expanded.sort(key=lambda e: _order_key(*e))
+        beam = expanded[:B]
+    beam.sort(key=lambda e: _order_key(*e))
+    return [codes for _, codes in beam[:S]]
+
+
+def residual_from_codes(codes: Sequence[int], codebook: np.ndarray) -> np.ndarray:
+    """r_bar = concat_g C_g[z_g]  (float32 [D])."""
+    return np.concatenate([codebook[g][c] for g, c in enumerate(codes)]).astype(F32)
+
+
+# ---------------------------------------------------------------------------
+# Alg. "Pseudo-Token Decoding and Attention": synthesis
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass
+class Pseudo:
+    keys: np.ndarray     # float32 [n_active * S][D] (values of the KV dtype)
+    values: np.ndarray
+    bias: np.ndarray     # float64 [n_active * S]: log n_k (0 if mass bias off)
+    slots: np.ndarray    # slot k of each pseudo-token
+
+
+def synthesize(bank: Bank, codebooks: np.ndarray, p: Params) -> Pseudo:
+    ks, vs, bs, sl = [], [], [], []
+    zero = np.zeros(p.head_dim, dtype=F32)
+    for k in range(p.capacity):
+        if bank.n[k] == 0:
+            continue
+        nf = F32(bank.n[k])
+        c = (bank.sum_k[k] / nf).astype(F32)
+        pv = (bank.sum_v[k] / nf).astype(F32)
+        if bank.n_res[k] == 0 or not p.use_pq:
+            rk = [zero] * p.S
+            rv = [zero] * p.S
+        else:
+            zk = decode_top_s(bank.hist_k[k], p.S, p.B)
+            zv = decode_top_s(bank.hist_v[k], p.S, p.B)
+            rk = [residual_from_codes(z, codebooks[0]) for z in zk]
+            rv = [residual_from_codes(z, codebooks[1]) for z in zv]
+        b = math.log(bank.n[k]) if p.mass_bias else 0.0
+        for s in range(p.S):
+            ks.append(round_kv((c + rk[s]).astype(F32), p.kv_dtype))
+            vs.append(round_kv((pv + rv[s]).astype(F32), p.kv_dtype))
+            bs.append(b)
+            sl.append(k)
+    D = p.head_dim
+    return Pseudo(np.array(ks, dtype=F32).reshape(-1, D), np.array(vs, dtype=F32).reshape(-1, D),
+                  np.array(bs, dtype=np.float64), np.array(sl, dtype=np.int64))
+
+
+# ---------------------------------------------------------------------------
+# Eq. attn_logit: mass-aware readout
+# ---------------------------------------------------------------------------
+
+
+def attend(q_rows: np.ndarray, k_ctx: np.ndarray, v_ctx: np.ndarray, bias: np.ndarray):
+    """softmax(Q K^T / sqrt(d) + b) V and log-sum-exp, in float64.
+
+    q_rows [R][D]; k_ctx, v_ctx [L][D]; bias [L] (0 for near tokens)."""
+    Q = q_rows.astype(np.float64)
+    Kc = k_ctx.astype(np.float64)
+    Vc = v_ctx.astype(np.float64)
+    logits = Q @ Kc.T / math.sqrt(Q.shape[1]) + bias[None, :]
+    m = logits.max(axis=1, keepdims=True)
+    w = np.exp(logits - m)
+    z = w.sum(axis=1, keepdims=True)
+    out = (w / z) @ Vc
+    lse = (m + np.log(z))[:, 0]
+    return out, lse
+
+
+# ---------------------------------------------------------------------------
+# One stream: near ring + far bank per (layer, kv head)
+# ---------------------------------------------------------------------------
+
+
+class OracleStream:
+    """Runs the hot path for a subset of (layer, kv head) units of one stream.
+
+    codebooks float32 [len(units)][2][G][C][D/G].
+    """
+
+    def __init__(self, p: Params, units: Sequence[int], codebooks: np.ndarray):
+        self.p = p
+        self.units = list(units)
+        self.codebooks = codebooks
+        self.banks = [Bank(p) for _ in self.units]
+        self.rings: List[collections.deque] = [collections.deque() for _ in self.units]
+        self.frame = 0          # frames appended so far
+        self.evicted = 0        # tokens evicted so far (per unit)
+
+    def append_frame(self, keys: np.ndarray, values: np.ndarray) -> Optional[List[FoldResult]]:
+        """Append frame t (keys/values [len(units)][T][D]); if the ring then
+        holds more than W frames, evict the oldest and fold it."""
+        t = self.frame
+        results = None
+        for u in range(len(self.units)):
+            self.rings[u].append((t, keys[u].astype(F32), values[u].astype(F32)))
+        if len(self.rings[0]) > self.p.window_frames:
+            results = []
+            for u in range(len(self.units)):
+                fe, ke, ve = self.rings[u].popleft()
+                results.append(fold_frame(self.banks[u], ke, ve, fe, t, self.p,
+                                          self.codebooks[u]))
+            self.evicted += self.p.tokens_per_frame
+        self.frame += 1
+        return results
+
+    def near(self, u: int):
+        frames = list(self.rings[u])
+        if not frames:
+            D = self.p.head_dim
+            return np.zeros((0, D), F32), np.zeros((0, D), F32)
+        return (np.concatenate([f[1] for f in frames]), np.concatenate([f[2] for f in frames]))
+
+    def synthesize(self) -> List[Pseudo]:
+        return [synthesize(self.banks[u], self.codebooks[u], self.p) for u in range(len(self.units))]
+
+    def context(self, u: int, pseudo: Pseudo):
+        kn, vn = self.near(u)
+        k_ctx = np.concatenate([kn, pseudo.keys])
+        v_ctx = np.concatenate([vn, pseudo.values])
+        bias = np.concatenate([np.zeros(len(kn)), pseudo.bias])
+        return k_ctx, v_ctx, bias
+
+    def attend(self, q: np.ndarray, num_kv_heads: int, pseudo: List[Pseudo]):
+        """q float32 [L][Tq][Hq][D] -> (O float64 [L][Tq][Hq][D], lse [L][Tq][Hq])
+        for the query heads whose kv head is in this stream's unit subset
+        (other entries are NaN).  Unit u = layer * Hkv + kv head."""
+        L, Tq, Hq, D = q.shape
+        grp = Hq // num_kv_heads
+        out = np.full((L, Tq, Hq, D), np.nan)
+        lse = np.full((L, Tq, Hq), np.nan)
+        for ui, u in enumerate(self.units):
+            l, h = divmod(u, num_kv_heads)
+            k_ctx, v_ctx, bias = self.context(ui, pseudo[ui])
+            heads = list(range(h * grp, (h + 1) * grp))
+            rows = q[l][:, heads, :].reshape(Tq * grp, D)
+            o, z = attend(rows, k_ctx, v_ctx, bias)
+            out[l][:, heads, :] = o.reshape(Tq, grp, D)
+            lse[l][:, heads] = z.reshape(Tq, grp)
+        return out, lse

@@ -1,0 +1,98 @@
+"""Planted mistakes in the oracle must fail at least one pin.
+
+Each case rewrites one expression of one oracle function (on the CPU, in
+this process only), then runs the pins named for it and expects one of them
+to fail.  This checks that the pins constrain every step of the oracle:
+a dropped term, a wrong sign or index, or a transposed operand is caught.
+"""
+import inspect
+import textwrap
+
+import numpy as np
+import pytest
+
+from oracle import protokv_oracle as O
+from tests import test_oracle_pins as P
+
+MUTATIONS = [
+    # (function, original text, planted mistake, pins expected to catch it)
+    ("assignment_costs", "cost = -cos +", "cost = cos +",
+     [P.test_cost_matches_scipy_cosine_and_mahalanobis]),
+    ("assignment_costs", "- 2.0 * Bxy[None, :]", "+ 2.0 * Bxy[None, :]",
+     [P.test_cost_matches_scipy_cosine_and_mahalanobis]),
+    ("assignment_costs", "(Cc[None, :] * dx * dx", "(A[None, :] * dx * dx",
+     [P.test_cost_matches_scipy_cosine_and_mahalanobis]),
+    ("assignment_costs", "> p.t_idle", ">= p.t_idle", [P.test_idle_term_counts_frames]),
+    ("assignment_costs", "p.lambda_sp * d_mah", "p.lambda_sp * d_mah * d_mah",
+     [P.test_cost_matches_scipy_cosine_and_mahalanobis]),
+    ("argmin_lowest", "idx = np.argmin(cost, axis=1)", "idx = np.argmax(cost, axis=1)",
+     [P.test_zero_lambdas_is_spherical_kmeans_assignment]),
+    ("spatial_coords", "F32(col + 0.5) / F32(grid_w)", "F32(row + 0.5) / F32(grid_w)",
+     [P.test_coordinates_are_cell_centres]),
+    ("pq_encode", "codes[:, g] = np.argmin(acc, axis=1)", "codes[:, g] = np.argmax(acc, axis=1)",
+     [P.test_pq_encode_matches_cdist_argmin]),
+    ("pq_encode", "sub = residuals[:, g * Dp:(g + 1) * Dp]", "sub = residuals[:, g:g + Dp]",
+     [P.test_pq_encode_matches_cdist_argmin]),
+    ("fold_frame", "bank.sum_k[k] = (bank.sum_k[k] + kk)", "bank.sum_k[k] = (bank.sum_k[k] + vv)",
+     [P.test_means_equal_sum_over_mass_from_assignment_log]),
+    ("fold_frame", "(bank.sq_v[k] + (vv * vv)", "(bank.sq_v[k] + (vv * kk)",
+     [lambda: P.test_mass_moment_hist_conservation("fp32")]),
+    ("fold_frame", "r_k = (keys[rest].astype(F32) - c_snap)", "r_k = (keys[rest].astype(F32) - p_snap)",
+     [P.test_histograms_match_nearest_codeword_of_logged_residuals]),
+    ("fold_frame", "codes_v = pq_encode(r_v, codebooks[1])", "codes_v = pq_encode(r_v, codebooks[0])",
+     [P.test_histograms_match_nearest_codeword_of_logged_residuals]),
+    ("fold_frame", "F32(eta * s[0]))", "F32(eta * s[1]))", [P.test_spatial_ema_closed_form]),
+    ("fold_frame", "F32(eta * F32(ddx * ddy))", "F32(eta * F32(ddx * ddx))", [P.test_spatial_ema_closed_form]),
+    ("fold_frame", "np.array([1.0, 0.0, 1.0], dtype=F32)", "np.array([1.0, 1.0, 1.0], dtype=F32)",
+     [P.test_spatial_ema_closed_form]),
+    ("fold_frame", "bank.tau[k] = pos[j]\n    return", "bank.tau[k] = t_frame\n    return",
+     [P.test_means_equal_sum_over_mass_from_assignment_log]),
+    ("fold_frame", "free = [k for k in range(p.capacity) if bank.n[k] == 0]",
+     "free = [k for k in range(p.capacity) if bank.n[k] == 0][::-1]",
+     [P.test_capacity_at_least_evicted_seeds_every_token]),
+    ("decode_top_s", "(int(hist[g, c]) + 1)", "(int(hist[g, c]) + 2)",
+     [lambda: P.test_beam_decode_is_exact_top_s(3, 5, 8, 3)]),
+    ("decode_top_s", "expanded.sort(key=lambda e: _order_key(*e))",
+     "expanded.sort(key=lambda e: (-e[0], e[1][::-1]))",
+     [lambda: P.test_beam_decode_is_exact_top_s(3, 5, 8, 3)]),
+    ("synthesize", "rv = [residual_from_codes(z, codebooks[1])", "rv = [residual_from_codes(z, codebooks[0])",
+     [P.test_pseudo_tokens_from_brute_force_modes]),
+    ("synthesize", "b = math.log(bank.n[k])", "b = math.log(bank.n[k] + 1)",
+     [P.test_log_mass_bias_equals_duplicated_tokens]),
+    ("attend", "/ math.sqrt(Q.shape[1])", "/ Q.shape[1]",
+     [P.test_attend_matches_torch_sdpa_with_additive_mask]),
+]
+
+
+def _mutated(fn_name, old, new):
+    src = textwrap.dedent(inspect.getsource(getattr(O, fn_name)))
+    assert src.count(old) == 1, (fn_name, old)
+    ns = dict(O.__dict__)
+    exec(compile(src.replace(old, new), f"<mutant {fn_name}>", "exec"), ns)
+    return ns[fn_name]
+
+
+@pytest.mark.parametrize("case", range(len(MUTATIONS)))
+def test_planted_mistake_is_caught(case, monkeypatch):
+    fn_name, old, new, pins = MUTATIONS[case]
+    monkeypatch.setattr(O, fn_name, _mutated(fn_name, old, new))
+    caught = False
+    for pin in pins:
+        try:
+            pin()
+        except Exception:          # AssertionError or a crash both count
+            caught = True
+            break
+    assert caught, f"mutation in {fn_name} ({new!r}) passed every pin"
+
+
+def test_stream_eviction_mutation_is_caught(monkeypatch):
+    """Evicting when the ring holds W frames (instead of more than W)."""
+    src = textwrap.dedent(inspect.getsource(O.OracleStream))
+    old = "if len(self.rings[0]) > self.p.window_frames:"
+    assert src.count(old) == 1
+    ns = dict(O.__dict__)
+    exec(compile(src.replace(old, old.replace(">", ">=")), "<mutant stream>", "exec"), ns)
+    monkeypatch.setattr(O, "OracleStream", ns["OracleStream"])
+    with pytest.raises(Exception):
+        P.test_capacity_limit_reproduces_exact_attention(1)
