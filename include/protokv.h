@@ -1,0 +1,220 @@
+/*
+ * libprotokv -- ProtoKV far-memory hot path on one AMD Instinct MI355X (gfx950).
+ *
+ * ProtoKV keeps, per (layer, KV head), an exact near window of the last W
+ * frames' KV and a fixed-capacity bank of K prototypes that absorbs every
+ * token evicted from that window (paper: Section "State representation and
+ * prototype bank", Section "Online update: eviction, assignment, and
+ * prototype maintenance", Appendix Algorithm "ProtoKV Streaming Update").
+ * At query time each active prototype is exposed as S pseudo-tokens decoded
+ * from its PQ residual histograms (Section "Residual Statistics and
+ * Pseudo-Token Interface", Algorithms "DecodeTopSResidualModes" and
+ * "Pseudo-Token Decoding and Attention") and attention runs over
+ * [near KV ; pseudo-tokens] with the log-mass logit bias of Eq. attn_logit.
+ *
+ * Calling conventions (every entry point):
+ *  - All arguments are plain pointers and sizes.  "device" pointers are HIP
+ *    device memory of the current device; "host" pointers are ordinary host
+ *    memory.  `stream` is a hipStream_t passed as void* (NULL = the default
+ *    stream); work is enqueued on it and the call returns without waiting,
+ *    unless the description says the call synchronizes.
+ *  - The caller owns all device memory, including the workspace; the
+ *    library never allocates device memory.  Input pointers are borrowed
+ *    until the enqueued work has completed on `stream`.
+ *  - A handle is not thread-safe; calls on one handle must be serialized.
+ *  - Every function returns a protokv_status.  Argument and state checks are
+ *    done on the host before anything is enqueued, so a non-OK return leaves
+ *    the handle and the device untouched, except PROTOKV_E_DEVICE, which
+ *    reports a HIP error from a launch or copy.  protokv_last_error() gives a
+ *    human-readable message for the last failure on a handle.
+ *
+ * v1 supports head_dim = 128, G = 8 PQ subspaces of 16 dims, C <= 16
+ * codewords, S <= 16 pseudo-tokens per prototype and smoothing eps = 1.
+ */
+#ifndef PROTOKV_H
+#define PROTOKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct protokv_ctx* protokv_t;
+
+typedef enum {
+  PROTOKV_OK = 0,
+  PROTOKV_E_INVALID = 1,     /* malformed argument or configuration */
+  PROTOKV_E_UNSUPPORTED = 2, /* well-formed but outside what v1 implements */
+  PROTOKV_E_WORKSPACE = 3,   /* workspace missing, too small or misaligned */
+  PROTOKV_E_STATE = 4,       /* call out of order for the stream's state */
+  PROTOKV_E_DEVICE = 5       /* HIP runtime error */
+} protokv_status;
+
+enum { PROTOKV_KV_BF16 = 0, PROTOKV_KV_FP32 = 1 };
+
+/* flags */
+enum {
+  PROTOKV_FLAG_PQ = 1u,        /* residual statistics on (off = "w/o residual stats" ablation) */
+  PROTOKV_FLAG_MASS_BIAS = 2u  /* log-mass bias on (off = "b_k = 0" ablation) */
+};
+
+typedef struct {
+  int32_t num_streams;      /* independent streams sharing one workspace */
+  int32_t num_layers;       /* L */
+  int32_t num_kv_heads;     /* Hkv */
+  int32_t num_q_heads;      /* Hq, a multiple of Hkv (GQA) */
+  int32_t head_dim;         /* D, must be 128 */
+  int32_t grid_h, grid_w;   /* visual tokens per frame T = grid_h * grid_w, raster order */
+  int32_t window_frames;    /* near window W in frames (W * T tokens) */
+  int32_t capacity;         /* K_max prototype slots per (stream, layer, kv head) */
+  int32_t pseudo_per_proto; /* S */
+  int32_t pq_subspaces;     /* G, must be 8 */
+  int32_t pq_codewords;     /* C, 2..16 */
+  int32_t beam;             /* B >= S; the decoded top-S does not depend on B (exact beam) */
+  int32_t t_idle;           /* T_idle in frames */
+  int32_t max_query_tokens; /* largest Tq passed to protokv_attend */
+  int32_t kv_dtype;         /* PROTOKV_KV_BF16 or PROTOKV_KV_FP32 */
+  uint32_t flags;           /* PROTOKV_FLAG_* */
+  float eta;                /* spatial EMA rate */
+  float pq_eps;             /* PQ smoothing, must be 1 */
+  double lambda_sp;         /* spatial weight of Eq. 1 */
+  double lambda_idle;       /* idle weight of Eq. 1 */
+  double ridge;             /* rho added to Sigma's diagonal in d_Mah */
+} protokv_config;
+
+/* Table tab:default_config defaults (S=8, lambda_sp=0.1, lambda_idle=0.01,
+ * T_idle=120, eta=0.05, G=8, C=16, B=32) with the 7B-class shape of one
+ * stream: 28 layers, 4 KV heads, 28 query heads, 14x14 tokens per frame,
+ * W=8 frames, K=256, bf16 KV, PQ and mass bias on, eps=1, rho=1e-4.
+ * Host only. */
+protokv_status protokv_default_config(protokv_config* cfg);
+
+/* Checks a configuration.  Host only, touches no device. */
+protokv_status protokv_validate_config(const protokv_config* cfg);
+
+/* Bytes of device workspace protokv_init needs for `cfg`.  Host only. */
+protokv_status protokv_workspace_size(const protokv_config* cfg, size_t* bytes);
+
+/* Creates a handle on the current HIP device.
+ * codebooks: host, float32 [num_streams][num_layers][num_kv_heads][2][G][C][D/G]
+ *   (index 0 = key codebooks C^K_g, 1 = value codebooks C^V_g; codewords of
+ *   subspace g cover dims [g*D/G, (g+1)*D/G)); copied during the call.
+ * workspace: device, >= protokv_workspace_size bytes, 256-byte aligned; owned
+ *   by the caller, must outlive the handle and must not be touched by the
+ *   caller while the handle exists.  It is cleared (empty rings and banks)
+ *   on `stream`.
+ * Synchronizes `stream` before returning. */
+protokv_status protokv_init(const protokv_config* cfg, const float* codebooks,
+                            void* workspace, size_t workspace_bytes, void* stream,
+                            protokv_t* out);
+
+/* Frees the host handle (not the workspace).  Does not synchronize. */
+protokv_status protokv_destroy(protokv_t h);
+
+/* Appends one frame to each listed stream's near window (Alg. "ProtoKV
+ * Streaming Update": append to B_near, and once more than W frames are held,
+ * mark the oldest frame as evicted; the eviction is absorbed by the next
+ * protokv_fold).
+ * stream_ids: host, n distinct stream indices.
+ * k, v: device, [n][num_layers][num_kv_heads][T][D] in kv_dtype (bf16 or
+ *   float32), row-major; entry i belongs to stream_ids[i].
+ * Errors: PROTOKV_E_STATE if a listed stream still has an unfolded eviction. */
+protokv_status protokv_append_frame(protokv_t h, const int32_t* stream_ids, int32_t n,
+                                    const void* k, const void* v, void* stream);
+
+/* Absorbs every pending evicted frame into its stream's prototype bank:
+ * seeds free slots (Initialization), assigns the other tokens by Eq. 1 against
+ * the post-seed bank and accumulates mass, sum, sum of squares, PQ residual
+ * histograms, spatial mean/covariance and recency in eviction order.
+ * Invalidates any synthesis.  No-op when nothing is pending. */
+protokv_status protokv_fold(protokv_t h, void* stream);
+
+/* Decodes the pseudo-tokens of every (layer, kv head) of `stream_id` into the
+ * workspace's synthesis buffer (one stream at a time): S pseudo-tokens per
+ * active prototype, keys c_k + r^K_s and values p_k + r^V_s rounded to
+ * kv_dtype, bias log n_k (Algorithms "DecodeTopSResidualModes" and
+ * "Pseudo-Token Decoding and Attention"). */
+protokv_status protokv_synthesize(protokv_t h, int32_t stream_id, void* stream);
+
+/* Mass-aware readout (Eq. attn_logit): for every layer l, query token t and
+ * query head h, with kv head g = h / (Hq/Hkv):
+ *   o = softmax([q K_near^T, q K~^T] / sqrt(D) + [0 ; log n_k]) [V_near ; V~].
+ * Needs a synthesis of `stream_id` made after its last fold.
+ * q: device [num_layers][tq][num_q_heads][D] in kv_dtype.
+ * o: device [num_layers][tq][num_q_heads][D] in kv_dtype.
+ * lse: device float32 [num_layers][tq][num_q_heads] (natural-log
+ *   log-sum-exp of the biased logits) or NULL.
+ * 1 <= tq <= max_query_tokens. */
+protokv_status protokv_attend(protokv_t h, int32_t stream_id, const void* q, int32_t tq,
+                              void* o, float* lse, void* stream);
+
+typedef struct {
+  uint64_t frames;          /* frames appended to the stream */
+  uint64_t evicted_tokens;  /* tokens folded into the bank, per (layer, kv head) */
+  int32_t active_slots;     /* prototypes with n_k > 0, per (layer, kv head) */
+  int32_t pending;          /* 1 if an evicted frame awaits protokv_fold */
+} protokv_stream_info;
+
+/* Host-side bookkeeping of one stream.  Host only, no device access. */
+protokv_status protokv_stream_info_get(protokv_t h, int32_t stream_id, protokv_stream_info* out);
+
+typedef struct {
+  uint64_t folds;            /* protokv_fold calls that folded something */
+  uint64_t tokens_assigned;  /* (token, layer, kv head) assignments by Eq. 1 */
+  uint64_t tokens_seeded;    /* (token, layer, kv head) seeds */
+  uint64_t refined;          /* assignments re-scored exactly on a few candidates */
+  uint64_t refined_full;     /* assignments re-scored exactly against every slot */
+  uint64_t near_ties;        /* assignments whose exact top-2 cost margin < 1e-6 */
+  uint64_t touched;          /* (prototype, fold) pairs that absorbed >= 1 token */
+} protokv_counters;
+
+/* Totals since init.  Synchronizes `stream`. */
+protokv_status protokv_get_counters(protokv_t h, protokv_counters* out, void* stream);
+
+/* Copies the last fold's assignment of `stream_id`: int32
+ * [num_layers][num_kv_heads][T], slot of each token of the evicted frame
+ * (seeded tokens give the slot they seeded).  dst may be host or device
+ * memory; count = number of int32 elements.  Synchronizes `stream`. */
+protokv_status protokv_read_assignments(protokv_t h, int32_t stream_id, int32_t* dst,
+                                        size_t count, void* stream);
+
+/* Bank row layout (bytes) of one prototype slot, PROTOKV_ROW_BYTES each,
+ * rows ordered [num_layers][num_kv_heads][capacity]:
+ *   0     float32 sum_k[128]      sum of absorbed keys
+ *   512   float32 sum_v[128]
+ *   1024  float32 sq_k[128]       sum of squared keys
+ *   1536  float32 sq_v[128]
+ *   2048  uint32  hist_k[8][16]   H^K[g][c] (entries c >= C are 0)
+ *   2560  uint32  hist_v[8][16]
+ *   3072  uint32  n               mass n_k (0 = inactive)
+ *   3076  uint32  n_res
+ *   3080  float32 mu_x, mu_y      running spatial mean
+ *   3088  float32 sig_xx, sig_xy, sig_yy
+ *   3100  int32   tau             stream position of the last absorbed token
+ *   3104  padding to 3200 */
+#define PROTOKV_ROW_BYTES 3200
+
+/* Copies the bank of `stream_id` (num_layers*num_kv_heads*capacity rows) to
+ * dst (host or device); bytes must equal that many PROTOKV_ROW_BYTES.
+ * Synchronizes `stream`. */
+protokv_status protokv_read_bank(protokv_t h, int32_t stream_id, void* dst, size_t bytes,
+                                 void* stream);
+
+/* Copies the current synthesis: keys and values [num_layers][num_kv_heads]
+ * [capacity*S][D] in kv_dtype (rows k*S..k*S+S-1 belong to slot k; only the
+ * first active_slots*S rows of each (layer, kv head) are defined) and bias
+ * float32 [num_layers][num_kv_heads][capacity].  Any pointer may be NULL.
+ * Synchronizes `stream`. */
+protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float* bias,
+                                   void* stream);
+
+/* Message for the last failure on h (or of protokv_init when h is NULL).
+ * Valid until the next call on h. */
+const char* protokv_last_error(protokv_t h);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PROTOKV_H */

@@ -1,0 +1,125 @@
+// Internal layout shared by the host library and the HIP kernels of libprotokv.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+#include "protokv.h"
+
+namespace pkv {
+
+constexpr int D = 128;     // head dim
+constexpr int G = 8;       // PQ subspaces
+constexpr int DP = 16;     // dims per subspace
+constexpr int CMAX = 16;   // codewords per subspace (storage)
+constexpr int SMAX = 16;   // pseudo-tokens per prototype
+constexpr int TMAX = 1024; // tokens per frame
+constexpr int MAXB = 64;   // streams per launch batch
+
+// Bank row (one prototype slot), byte offsets; see protokv.h.
+constexpr int ROW = PROTOKV_ROW_BYTES;
+constexpr int ROW_SUMK = 0, ROW_SUMV = 512, ROW_SQK = 1024, ROW_SQV = 1536;
+constexpr int ROW_HK = 2048, ROW_HV = 2560, ROW_META = 3072;
+
+struct RowMeta {
+  uint32_t n, n_res;
+  float mu_x, mu_y, sxx, sxy, syy;
+  int32_t tau;
+};
+static_assert(sizeof(RowMeta) == 32, "row meta is 32 bytes");
+
+// Screening copy of a slot (derived from its row after every update):
+// spatial mean, the inverse of (Sigma + rho I) as q = qa dx^2 + 2 qb dx dy + qc dy^2,
+// the frame index of tau and an active flag.  The unit key centre sumK/|sumK|
+// lives beside it as a two-term bf16 split (hi + lo).
+struct CacheMeta {
+  float mu_x, mu_y, qa, qb, qc;
+  int32_t last_frame;
+  uint32_t active;
+  float pad;
+};
+static_assert(sizeof(CacheMeta) == 32, "cache meta is 32 bytes");
+
+// Host-side constants of a handle, passed by value to kernels.
+struct Dims {
+  int L, Hkv, Hq, T, grid_h, grid_w, W, K, S, C, t_idle, units, streams;
+  int kv_fp32;
+  uint32_t flags;
+  float eta;
+  double lambda_sp, lambda_idle, ridge;
+  int max_rows;    // max query rows per kv head (max_query_tokens * Hq / Hkv)
+  int max_splits;  // attention context splits (partials storage)
+};
+
+// Device pointers into the caller's workspace.
+struct Workspace {
+  uint8_t* ring_k;            // [streams][units][W+1][T][D] kv dtype
+  uint8_t* ring_v;
+  uint8_t* bank;              // [streams][units][K] rows of ROW bytes
+  uint16_t* chat_hi;          // [streams][units][K][D] bf16 bits
+  uint16_t* chat_lo;
+  CacheMeta* cmeta;           // [streams][units][K]
+  int32_t* assign;            // [streams][units][T]
+  float* codebooks;           // [streams][units][2][G][CMAX][DP]
+  uint8_t* pk;                // [units][K*S][D] kv dtype (synthesis of one stream)
+  uint8_t* pv;
+  float* pbias;               // [units][K]
+  float* part_o;              // [units][max_splits][max_rows][D]
+  float* part_ml;             // [units][max_splits][max_rows][2]  (max, sum)
+  unsigned long long* counters;  // [16]
+};
+
+enum Counter {
+  CNT_REFINED = 0,
+  CNT_REFINED_FULL = 1,
+  CNT_NEAR_TIES = 2,
+  CNT_TOUCHED = 3,
+  CNT_COUNT = 16
+};
+
+struct AppendBatch {
+  int n;
+  int sid[MAXB];
+  int slot[MAXB];
+};
+
+// One pending eviction per entry.
+struct FoldBatch {
+  int n;
+  int sid[MAXB];
+  int slot[MAXB];   // ring slot holding the evicted frame
+  int fe[MAXB];     // evicted frame index
+  int t[MAXB];      // current frame (the one just appended)
+  int nact[MAXB];   // active slots before this fold
+  int nseed[MAXB];  // tokens of this frame that seed free slots
+};
+
+struct AttendArgs {
+  int sid;
+  int f_first;      // first near frame
+  int n_near;       // near tokens (frames * T)
+  int n_far;        // pseudo-tokens (active slots * S)
+  int tq;
+  int splits;       // context splits per kv head
+  int chunk;        // context tokens per split (multiple of 32)
+  const void* q;
+  void* o;
+  float* lse;
+};
+
+// Launchers (fold.hip, query.hip).  Return hipSuccess or the launch error.
+hipError_t launch_ring_insert(const Dims& dm, const Workspace& ws, const AppendBatch& ab,
+                              const void* k, const void* v, hipStream_t st);
+hipError_t launch_seed(const Dims& dm, const Workspace& ws, const FoldBatch& fb, int max_seed,
+                       hipStream_t st);
+hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
+                         hipStream_t st);
+hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
+                            hipStream_t st);
+hipError_t launch_synthesize(const Dims& dm, const Workspace& ws, int sid, int n_active,
+                             hipStream_t st);
+hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& aa,
+                         hipStream_t st);
+
+}  // namespace pkv

@@ -1,0 +1,458 @@
+// libprotokv host side: configuration checks, workspace carve-up, per-stream
+// state machine and kernel sequencing on the caller's HIP stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "pkv_internal.h"
+
+using namespace pkv;
+
+namespace {
+
+constexpr int MAX_SPLITS = 16;
+constexpr int MAX_ROWS = 512;  // query rows per kv head per attend call
+
+struct StreamState {
+  uint64_t frames = 0;
+  uint64_t evicted = 0;
+  int active = 0;
+  bool pending = false;
+  int pending_fe = -1;
+};
+
+struct Layout {
+  size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codebooks;
+  size_t pk, pv, pbias, part_o, part_ml, counters, total;
+};
+
+thread_local std::string g_init_err;
+
+size_t kv_bytes(const protokv_config& c) { return c.kv_dtype == PROTOKV_KV_FP32 ? 4 : 2; }
+
+Layout make_layout(const protokv_config& c) {
+  Layout ly{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += (bytes + 255) & ~(size_t)255;
+    return o;
+  };
+  const size_t es = kv_bytes(c);
+  const size_t units = (size_t)c.num_layers * c.num_kv_heads;
+  const size_t U = (size_t)c.num_streams * units;
+  const size_t T = (size_t)c.grid_h * c.grid_w;
+  const size_t K = (size_t)c.capacity;
+  const size_t S = (size_t)c.pseudo_per_proto;
+  const size_t rows = (size_t)c.max_query_tokens * (c.num_q_heads / c.num_kv_heads);
+  ly.ring_k = take(U * (c.window_frames + 1) * T * D * es);
+  ly.ring_v = take(U * (c.window_frames + 1) * T * D * es);
+  ly.bank = take(U * K * ROW);
+  ly.chat_hi = take(U * K * D * 2);
+  ly.chat_lo = take(U * K * D * 2);
+  ly.cmeta = take(U * K * sizeof(CacheMeta));
+  ly.assign = take(U * T * 4);
+  ly.codebooks = take(U * 2 * G * CMAX * DP * 4);
+  ly.pk = take(units * K * S * D * es);
+  ly.pv = take(units * K * S * D * es);
+  ly.pbias = take(units * K * 4);
+  ly.part_o = take(units * MAX_SPLITS * rows * D * 4);
+  ly.part_ml = take(units * MAX_SPLITS * rows * 2 * 4);
+  ly.counters = take(CNT_COUNT * 8);
+  ly.total = off;
+  return ly;
+}
+
+protokv_status check_config(const protokv_config* c, std::string& why) {
+  if (!c) { why = "config is NULL"; return PROTOKV_E_INVALID; }
+  auto bad = [&](const char* m) { why = m; return PROTOKV_E_INVALID; };
+  auto uns = [&](const char* m) { why = m; return PROTOKV_E_UNSUPPORTED; };
+  if (c->num_streams < 1) return bad("num_streams must be >= 1");
+  if (c->num_layers < 1 || c->num_kv_heads < 1) return bad("num_layers and num_kv_heads must be >= 1");
+  if (c->num_q_heads < c->num_kv_heads || c->num_q_heads % c->num_kv_heads)
+    return bad("num_q_heads must be a positive multiple of num_kv_heads");
+  if (c->head_dim != D) return uns("head_dim must be 128");
+  if (c->grid_h < 1 || c->grid_w < 1) return bad("grid_h and grid_w must be >= 1");
+  if ((int64_t)c->grid_h * c->grid_w > TMAX) return uns("at most 1024 tokens per frame");
+  if (c->window_frames < 1) return bad("window_frames must be >= 1");
+  if (c->capacity < 1) return bad("capacity must be >= 1");
+  if (c->capacity > (1 << 20)) return uns("capacity above 2^20");
+  if (c->pq_subspaces != G) return uns("pq_subspaces must be 8");
+  if (c->pq_codewords < 2 || c->pq_codewords > CMAX) return uns("pq_codewords must be in [2, 16]");
+  if (c->pseudo_per_proto < 1) return bad("pseudo_per_proto must be >= 1");
+  if (c->pseudo_per_proto > SMAX) return uns("pseudo_per_proto above 16");
+  if (c->beam < c->pseudo_per_proto) return bad("beam must be >= pseudo_per_proto");
+  if (c->t_idle < 0) return bad("t_idle must be >= 0");
+  if (c->max_query_tokens < 1) return bad("max_query_tokens must be >= 1");
+  if ((int64_t)c->max_query_tokens * (c->num_q_heads / c->num_kv_heads) > MAX_ROWS)
+    return uns("max_query_tokens * (num_q_heads/num_kv_heads) above 512");
+  if (c->kv_dtype != PROTOKV_KV_BF16 && c->kv_dtype != PROTOKV_KV_FP32) return bad("kv_dtype unknown");
+  if (c->flags & ~(uint32_t)(PROTOKV_FLAG_PQ | PROTOKV_FLAG_MASS_BIAS)) return bad("unknown flag bits");
+  if (!(c->eta > 0.f && c->eta < 1.f)) return bad("eta must be in (0, 1)");
+  if (c->pq_eps != 1.0f) return uns("pq_eps must be 1");
+  if (!(c->lambda_sp >= 0.0) || !(c->lambda_idle >= 0.0) || !std::isfinite(c->lambda_sp) ||
+      !std::isfinite(c->lambda_idle))
+    return bad("lambda_sp and lambda_idle must be finite and >= 0");
+  if (!(c->ridge > 0.0) || !std::isfinite(c->ridge)) return bad("ridge must be finite and > 0");
+  return PROTOKV_OK;
+}
+
+}  // namespace
+
+struct protokv_ctx {
+  protokv_config cfg;
+  Dims dm;
+  Workspace ws;
+  Layout ly;
+  uint8_t* base = nullptr;
+  std::vector<StreamState> st;
+  int synth_stream = -1;
+  int synth_active = 0;
+  uint64_t folds = 0, assigned = 0, seeded = 0;
+  std::string err;
+
+  protokv_status fail(protokv_status s, const std::string& m) {
+    err = m;
+    return s;
+  }
+  protokv_status dev(hipError_t e, const char* where) {
+    if (e == hipSuccess) return PROTOKV_OK;
+    err = std::string(where) + ": " + hipGetErrorString(e);
+    return PROTOKV_E_DEVICE;
+  }
+};
+
+extern "C" {
+
+protokv_status protokv_default_config(protokv_config* c) {
+  if (!c) return PROTOKV_E_INVALID;
+  std::memset(c, 0, sizeof(*c));
+  c->num_streams = 1;
+  c->num_layers = 28;
+  c->num_kv_heads = 4;
+  c->num_q_heads = 28;
+  c->head_dim = 128;
+  c->grid_h = 14;
+  c->grid_w = 14;
+  c->window_frames = 8;
+  c->capacity = 256;
+  c->pseudo_per_proto = 8;
+  c->pq_subspaces = 8;
+  c->pq_codewords = 16;
+  c->beam = 32;
+  c->t_idle = 120;
+  c->max_query_tokens = 64;
+  c->kv_dtype = PROTOKV_KV_BF16;
+  c->flags = PROTOKV_FLAG_PQ | PROTOKV_FLAG_MASS_BIAS;
+  c->eta = 0.05f;
+  c->pq_eps = 1.0f;
+  c->lambda_sp = 0.1;
+  c->lambda_idle = 0.01;
+  c->ridge = 1e-4;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_validate_config(const protokv_config* c) {
+  std::string why;
+  protokv_status s = check_config(c, why);
+  if (s != PROTOKV_OK) g_init_err = why;
+  return s;
+}
+
+protokv_status protokv_workspace_size(const protokv_config* c, size_t* bytes) {
+  std::string why;
+  protokv_status s = check_config(c, why);
+  if (s != PROTOKV_OK) { g_init_err = why; return s; }
+  if (!bytes) { g_init_err = "bytes is NULL"; return PROTOKV_E_INVALID; }
+  *bytes = make_layout(*c).total;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_init(const protokv_config* c, const float* codebooks, void* workspace,
+                            size_t workspace_bytes, void* stream, protokv_t* out) {
+  std::string why;
+  protokv_status s = check_config(c, why);
+  if (s != PROTOKV_OK) { g_init_err = why; return s; }
+  if (!out) { g_init_err = "out is NULL"; return PROTOKV_E_INVALID; }
+  if (!codebooks) { g_init_err = "codebooks is NULL"; return PROTOKV_E_INVALID; }
+  Layout ly = make_layout(*c);
+  if (!workspace) { g_init_err = "workspace is NULL"; return PROTOKV_E_WORKSPACE; }
+  if ((uintptr_t)workspace % 256) { g_init_err = "workspace must be 256-byte aligned"; return PROTOKV_E_WORKSPACE; }
+  if (workspace_bytes < ly.total) {
+    g_init_err = "workspace too small: need " + std::to_string(ly.total) + " bytes";
+    return PROTOKV_E_WORKSPACE;
+  }
+  hipStream_t hs = (hipStream_t)stream;
+  auto* h = new protokv_ctx();
+  h->cfg = *c;
+  h->ly = ly;
+  h->base = (uint8_t*)workspace;
+  Dims& dm = h->dm;
+  dm.L = c->num_layers;
+  dm.Hkv = c->num_kv_heads;
+  dm.Hq = c->num_q_heads;
+  dm.T = c->grid_h * c->grid_w;
+  dm.grid_h = c->grid_h;
+  dm.grid_w = c->grid_w;
+  dm.W = c->window_frames;
+  dm.K = c->capacity;
+  dm.S = c->pseudo_per_proto;
+  dm.C = c->pq_codewords;
+  dm.t_idle = c->t_idle;
+  dm.units = c->num_layers * c->num_kv_heads;
+  dm.streams = c->num_streams;
+  dm.kv_fp32 = c->kv_dtype == PROTOKV_KV_FP32;
+  dm.flags = c->flags;
+  dm.eta = c->eta;
+  dm.lambda_sp = c->lambda_sp;
+  dm.lambda_idle = c->lambda_idle;
+  dm.ridge = c->ridge;
+  dm.max_rows = c->max_query_tokens * (c->num_q_heads / c->num_kv_heads);
+  dm.max_splits = MAX_SPLITS;
+  uint8_t* b = h->base;
+  Workspace& ws = h->ws;
+  ws.ring_k = b + ly.ring_k;
+  ws.ring_v = b + ly.ring_v;
+  ws.bank = b + ly.bank;
+  ws.chat_hi = (uint16_t*)(b + ly.chat_hi);
+  ws.chat_lo = (uint16_t*)(b + ly.chat_lo);
+  ws.cmeta = (CacheMeta*)(b + ly.cmeta);
+  ws.assign = (int32_t*)(b + ly.assign);
+  ws.codebooks = (float*)(b + ly.codebooks);
+  ws.pk = b + ly.pk;
+  ws.pv = b + ly.pv;
+  ws.pbias = (float*)(b + ly.pbias);
+  ws.part_o = (float*)(b + ly.part_o);
+  ws.part_ml = (float*)(b + ly.part_ml);
+  ws.counters = (unsigned long long*)(b + ly.counters);
+  h->st.assign(c->num_streams, StreamState());
+
+  // codebooks -> [U][2][G][CMAX][DP] with the codeword axis padded to 16
+  const size_t U = (size_t)c->num_streams * dm.units;
+  const int C = c->pq_codewords;
+  std::vector<float> cb(U * 2 * G * CMAX * DP, 0.f);
+  for (size_t uu = 0; uu < U; ++uu)
+    for (int kv = 0; kv < 2; ++kv)
+      for (int g = 0; g < G; ++g)
+        for (int cc = 0; cc < C; ++cc)
+          std::memcpy(&cb[(((uu * 2 + kv) * G + g) * CMAX + cc) * DP],
+                      &codebooks[(((uu * 2 + kv) * G + g) * C + cc) * DP], DP * sizeof(float));
+  hipError_t e = hipMemsetAsync(workspace, 0, ly.total, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(ws.codebooks, cb.data(), cb.size() * sizeof(float),
+                                          hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) {
+    g_init_err = std::string("init: ") + hipGetErrorString(e);
+    delete h;
+    return PROTOKV_E_DEVICE;
+  }
+  *out = h;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_destroy(protokv_t h) {
+  if (!h) return PROTOKV_E_INVALID;
+  delete h;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_append_frame(protokv_t h, const int32_t* ids, int32_t n, const void* k,
+                                    const void* v, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (n < 1 || !ids || !k || !v) return h->fail(PROTOKV_E_INVALID, "append: need n >= 1 and non-NULL ids, k, v");
+  std::vector<char> seen(h->cfg.num_streams, 0);
+  for (int i = 0; i < n; ++i) {
+    const int s = ids[i];
+    if (s < 0 || s >= h->cfg.num_streams) return h->fail(PROTOKV_E_INVALID, "append: stream id out of range");
+    if (seen[s]) return h->fail(PROTOKV_E_INVALID, "append: stream listed twice");
+    seen[s] = 1;
+    if (h->st[s].pending) return h->fail(PROTOKV_E_STATE, "append: stream has an unfolded eviction; call protokv_fold");
+    if ((h->st[s].frames + 2) * (uint64_t)h->dm.T >= (1ull << 31))
+      return h->fail(PROTOKV_E_UNSUPPORTED, "append: stream position exceeds 2^31 tokens");
+  }
+  hipStream_t hs = (hipStream_t)stream;
+  const size_t entry_bytes = (size_t)h->dm.units * h->dm.T * D * kv_bytes(h->cfg);
+  for (int b0 = 0; b0 < n; b0 += MAXB) {
+    AppendBatch ab{};
+    ab.n = std::min(MAXB, n - b0);
+    for (int i = 0; i < ab.n; ++i) {
+      const StreamState& ss = h->st[ids[b0 + i]];
+      ab.sid[i] = ids[b0 + i];
+      ab.slot[i] = (int)(ss.frames % (uint64_t)(h->dm.W + 1));
+    }
+    protokv_status s = h->dev(launch_ring_insert(h->dm, h->ws, ab, (const uint8_t*)k + b0 * entry_bytes,
+                                                 (const uint8_t*)v + b0 * entry_bytes, hs),
+                              "append");
+    if (s != PROTOKV_OK) return s;
+  }
+  for (int i = 0; i < n; ++i) {
+    StreamState& ss = h->st[ids[i]];
+    ss.frames += 1;
+    if (ss.frames > (uint64_t)h->dm.W) {
+      ss.pending = true;
+      ss.pending_fe = (int)(ss.frames - 1 - h->dm.W);
+    }
+  }
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_fold(protokv_t h, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  hipStream_t hs = (hipStream_t)stream;
+  std::vector<int> pend;
+  for (int s = 0; s < h->cfg.num_streams; ++s)
+    if (h->st[s].pending) pend.push_back(s);
+  if (pend.empty()) return PROTOKV_OK;
+  const int T = h->dm.T, K = h->dm.K;
+  for (size_t b0 = 0; b0 < pend.size(); b0 += MAXB) {
+    FoldBatch fb{};
+    fb.n = (int)std::min<size_t>(MAXB, pend.size() - b0);
+    int max_seed = 0;
+    bool any_assign = false;
+    for (int i = 0; i < fb.n; ++i) {
+      const int s = pend[b0 + i];
+      const StreamState& ss = h->st[s];
+      fb.sid[i] = s;
+      fb.fe[i] = ss.pending_fe;
+      fb.slot[i] = ss.pending_fe % (h->dm.W + 1);
+      fb.t[i] = (int)(ss.frames - 1);
+      fb.nact[i] = ss.active;
+      fb.nseed[i] = std::min(T, K - ss.active);
+      max_seed = std::max(max_seed, fb.nseed[i]);
+      any_assign |= fb.nseed[i] < T;
+    }
+    protokv_status st = PROTOKV_OK;
+    if (max_seed > 0) st = h->dev(launch_seed(h->dm, h->ws, fb, max_seed, hs), "fold/seed");
+    if (st == PROTOKV_OK && any_assign) st = h->dev(launch_screen(h->dm, h->ws, fb, hs), "fold/screen");
+    if (st == PROTOKV_OK && any_assign) st = h->dev(launch_aggregate(h->dm, h->ws, fb, hs), "fold/aggregate");
+    if (st != PROTOKV_OK) return st;
+    for (int i = 0; i < fb.n; ++i) {
+      StreamState& ss = h->st[fb.sid[i]];
+      ss.active += fb.nseed[i];
+      ss.evicted += T;
+      ss.pending = false;
+      h->seeded += (uint64_t)fb.nseed[i] * h->dm.units;
+      h->assigned += (uint64_t)(T - fb.nseed[i]) * h->dm.units;
+      if (h->synth_stream == fb.sid[i]) h->synth_stream = -1;
+    }
+  }
+  h->folds += 1;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (sid < 0 || sid >= h->cfg.num_streams) return h->fail(PROTOKV_E_INVALID, "synthesize: stream id out of range");
+  if (h->st[sid].pending) return h->fail(PROTOKV_E_STATE, "synthesize: stream has an unfolded eviction");
+  protokv_status s = h->dev(launch_synthesize(h->dm, h->ws, sid, h->st[sid].active, (hipStream_t)stream),
+                            "synthesize");
+  if (s != PROTOKV_OK) return s;
+  h->synth_stream = sid;
+  h->synth_active = h->st[sid].active;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t tq, void* o, float* lse,
+                              void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (sid < 0 || sid >= h->cfg.num_streams) return h->fail(PROTOKV_E_INVALID, "attend: stream id out of range");
+  if (!q || !o) return h->fail(PROTOKV_E_INVALID, "attend: q and o must be non-NULL");
+  if (tq < 1 || tq > h->cfg.max_query_tokens) return h->fail(PROTOKV_E_INVALID, "attend: tq outside [1, max_query_tokens]");
+  const StreamState& ss = h->st[sid];
+  if (ss.pending) return h->fail(PROTOKV_E_STATE, "attend: stream has an unfolded eviction");
+  if (h->synth_stream != sid) return h->fail(PROTOKV_E_STATE, "attend: no synthesis of this stream since its last fold");
+  AttendArgs aa{};
+  aa.sid = sid;
+  const int T = h->dm.T, W = h->dm.W;
+  const uint64_t nf = std::min<uint64_t>(ss.frames, (uint64_t)W);
+  aa.f_first = (int)(ss.frames - nf);
+  aa.n_near = (int)nf * T;
+  aa.n_far = h->synth_active * h->dm.S;
+  aa.tq = tq;
+  aa.q = q;
+  aa.o = o;
+  aa.lse = lse;
+  const int ctx = aa.n_near + aa.n_far;
+  if (ctx == 0) return h->fail(PROTOKV_E_STATE, "attend: empty context (no frames appended)");
+  const int rows = tq * (h->dm.Hq / h->dm.Hkv);
+  int splits;
+  if (h->dm.kv_fp32) splits = std::max(1, std::min(MAX_SPLITS, (1024 + h->dm.units * rows - 1) / (h->dm.units * rows)));
+  else splits = std::max(1, std::min(MAX_SPLITS, (512 + h->dm.units - 1) / h->dm.units));
+  int chunk = (ctx + splits - 1) / splits;
+  chunk = (chunk + 31) / 32 * 32;
+  splits = (ctx + chunk - 1) / chunk;
+  aa.splits = splits;
+  aa.chunk = chunk;
+  return h->dev(launch_attend(h->dm, h->ws, aa, (hipStream_t)stream), "attend");
+}
+
+protokv_status protokv_stream_info_get(protokv_t h, int32_t sid, protokv_stream_info* out) {
+  if (!h || !out) return PROTOKV_E_INVALID;
+  if (sid < 0 || sid >= h->cfg.num_streams) return h->fail(PROTOKV_E_INVALID, "stream id out of range");
+  const StreamState& ss = h->st[sid];
+  out->frames = ss.frames;
+  out->evicted_tokens = ss.evicted;
+  out->active_slots = ss.active;
+  out->pending = ss.pending ? 1 : 0;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_get_counters(protokv_t h, protokv_counters* out, void* stream) {
+  if (!h || !out) return PROTOKV_E_INVALID;
+  unsigned long long dc[CNT_COUNT];
+  hipStream_t hs = (hipStream_t)stream;
+  hipError_t e = hipMemcpyAsync(dc, h->ws.counters, sizeof(dc), hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return h->dev(e, "get_counters");
+  out->folds = h->folds;
+  out->tokens_assigned = h->assigned;
+  out->tokens_seeded = h->seeded;
+  out->refined = dc[CNT_REFINED];
+  out->refined_full = dc[CNT_REFINED_FULL];
+  out->near_ties = dc[CNT_NEAR_TIES];
+  out->touched = dc[CNT_TOUCHED];
+  return PROTOKV_OK;
+}
+
+static protokv_status copy_out(protokv_t h, void* dst, const void* src, size_t bytes, void* stream,
+                               const char* where) {
+  hipStream_t hs = (hipStream_t)stream;
+  hipError_t e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  return h->dev(e, where);
+}
+
+protokv_status protokv_read_assignments(protokv_t h, int32_t sid, int32_t* dst, size_t count, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (sid < 0 || sid >= h->cfg.num_streams || !dst) return h->fail(PROTOKV_E_INVALID, "read_assignments: bad stream or dst");
+  const size_t n = (size_t)h->dm.units * h->dm.T;
+  if (count != n) return h->fail(PROTOKV_E_INVALID, "read_assignments: count must be num_layers*num_kv_heads*T");
+  return copy_out(h, dst, h->ws.assign + (size_t)sid * n, n * 4, stream, "read_assignments");
+}
+
+protokv_status protokv_read_bank(protokv_t h, int32_t sid, void* dst, size_t bytes, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (sid < 0 || sid >= h->cfg.num_streams || !dst) return h->fail(PROTOKV_E_INVALID, "read_bank: bad stream or dst");
+  const size_t n = (size_t)h->dm.units * h->dm.K * ROW;
+  if (bytes != n) return h->fail(PROTOKV_E_INVALID, "read_bank: bytes must be units*capacity*PROTOKV_ROW_BYTES");
+  return copy_out(h, dst, h->ws.bank + (size_t)sid * n, n, stream, "read_bank");
+}
+
+protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float* bias, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  const size_t n = (size_t)h->dm.units * h->dm.K * h->dm.S * D * kv_bytes(h->cfg);
+  protokv_status s = PROTOKV_OK;
+  if (keys) s = copy_out(h, keys, h->ws.pk, n, stream, "read_pseudo");
+  if (s == PROTOKV_OK && values) s = copy_out(h, values, h->ws.pv, n, stream, "read_pseudo");
+  if (s == PROTOKV_OK && bias) s = copy_out(h, bias, h->ws.pbias, (size_t)h->dm.units * h->dm.K * 4, stream, "read_pseudo");
+  return s;
+}
+
+const char* protokv_last_error(protokv_t h) { return h ? h->err.c_str() : g_init_err.c_str(); }
+
+}  // extern "C"

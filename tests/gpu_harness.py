@@ -1,0 +1,201 @@
+"""Runs the HIP path (through the C-ABI binding) and the CPU oracle side by
+side on the same seeded bytes and compares them to the parity bar:
+
+* assignments bit-exact, except tokens whose exact top-2 cost margin is
+  below 1e-6 (near ties), which are counted;
+* prototype statistics: mass, n_res, histograms, recency exact; sums and
+  sums of squares within relative 1e-4 per row (||a-b|| <= 1e-4 ||b||);
+  spatial mean/covariance within 1e-6;
+* pseudo-tokens exact (same bank -> same codes -> same rounding);
+* readout within absolute 2e-2 of the oracle's float64 output.
+"""
+from __future__ import annotations
+
+import math
+import sys
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+from oracle import protokv_oracle as O
+from paper_2606_26762_amd import protokv as pk
+from paper_2606_26762_amd import workloads as W
+
+READOUT_ATOL = 2e-2
+LSE_ATOL = 2e-3
+STAT_RTOL = 1e-4
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def oracle_params(wl: W.Workload, **kw) -> O.Params:
+    p = O.Params(head_dim=wl.head_dim, grid_h=wl.grid_h, grid_w=wl.grid_w,
+                 window_frames=wl.window_frames, capacity=wl.capacity, kv_dtype=wl.kv_dtype)
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+def gpu_config(wl: W.Workload, p: O.Params, streams: int = 1, max_query_tokens=None) -> pk.Config:
+    flags = (pk.FLAG_PQ if p.use_pq else 0) | (pk.FLAG_MASS_BIAS if p.mass_bias else 0)
+    return pk.default_config(
+        num_streams=streams, num_layers=wl.num_layers, num_kv_heads=wl.num_kv_heads,
+        num_q_heads=wl.num_q_heads, head_dim=wl.head_dim, grid_h=wl.grid_h, grid_w=wl.grid_w,
+        window_frames=wl.window_frames, capacity=wl.capacity, pseudo_per_proto=p.S,
+        pq_codewords=p.C, beam=max(p.B, p.S), t_idle=p.t_idle,
+        max_query_tokens=max_query_tokens or wl.query_tokens,
+        kv_dtype=pk.KV_FP32 if wl.kv_dtype == "fp32" else pk.KV_BF16, flags=flags,
+        eta=p.eta, lambda_sp=p.lambda_sp, lambda_idle=p.lambda_idle, ridge=p.ridge)
+
+
+class Pair:
+    """GPU handle over all units of `streams` streams + oracle over sampled units."""
+
+    def __init__(self, wl: W.Workload, sample: Optional[Sequence[int]] = None, streams: int = 1,
+                 cb_samples: int = 1024, cb_iters: int = 8, max_query_tokens=None, **pkw):
+        import torch
+        self.torch = torch
+        self.wl = wl
+        self.p = oracle_params(wl, **pkw)
+        self.streams = streams
+        self.sample = list(range(wl.units)) if sample is None else list(sample)
+        self.cb = np.stack([W.make_codebooks(wl, stream=s, samples=cb_samples, iters=cb_iters,
+                                             C=self.p.C) for s in range(streams)])
+        self.cfg = gpu_config(wl, self.p, streams, max_query_tokens)
+        self.gpu = pk.ProtoKV(self.cfg, self.cb)
+        self.host = [W.HostStream(wl, stream=s, units=self.sample) for s in range(streams)]
+        self.oracle = [O.OracleStream(self.p, self.sample, self.cb[s][self.sample]) for s in range(streams)]
+        self.dev = W.DeviceStream(wl, n_streams=1, seed=99) if len(self.sample) < wl.units else None
+        self.dtype = torch.float32 if wl.kv_dtype == "fp32" else torch.bfloat16
+        self.near_ties = 0
+        self.assign_checked = 0
+        self.frames = [0] * streams
+
+    # -- input -------------------------------------------------------------
+    def _frame_tensor(self, stream: int):
+        """One frame of `stream` as device tensors [1][L][Hkv][T][D] plus the
+        sampled units' host bytes."""
+        torch, wl = self.torch, self.wl
+        kh, vh = self.host[stream].next_frame()
+        if self.dev is not None:
+            k, v = self.dev.next_frame()
+        else:
+            shape = (1, wl.num_layers, wl.num_kv_heads, wl.tokens_per_frame, wl.head_dim)
+            k = torch.empty(shape, dtype=self.dtype, device="cuda")
+            v = torch.empty_like(k)
+        kf = k.view(wl.units, wl.tokens_per_frame, wl.head_dim)
+        vf = v.view(wl.units, wl.tokens_per_frame, wl.head_dim)
+        idx = torch.tensor(self.sample, device="cuda")
+        kf[idx] = torch.from_numpy(kh).to("cuda", self.dtype)
+        vf[idx] = torch.from_numpy(vh).to("cuda", self.dtype)
+        return k, v, kh, vh
+
+    # -- stepping ------------------------------------------------------------
+    def step(self, streams: Optional[Sequence[int]] = None, check_assign: bool = True):
+        """Append one frame to each listed stream (one batched call), fold,
+        and compare the assignments of the sampled units."""
+        torch = self.torch
+        streams = list(range(self.streams)) if streams is None else list(streams)
+        ks, vs, results = [], [], {}
+        for s in streams:
+            k, v, kh, vh = self._frame_tensor(s)
+            ks.append(k)
+            vs.append(v)
+            results[s] = self.oracle[s].append_frame(kh, vh)
+        K = torch.cat(ks) if len(ks) > 1 else ks[0]
+        V = torch.cat(vs) if len(vs) > 1 else vs[0]
+        self.gpu.append_frame(streams, K, V)
+        self.gpu.fold()
+        for s in streams:
+            self.frames[s] += 1
+            res = results[s]
+            if res is None or not check_assign:
+                continue
+            ga = self.gpu.read_assignments(s)
+            for i, u in enumerate(self.sample):
+                oa = res[i].assign
+                bad = np.nonzero(ga[u] != oa)[0]
+                tie = res[i].margin < 1e-6
+                self.near_ties += int(tie.sum())
+                if len(bad):
+                    assert np.all(tie[bad]), (
+                        f"stream {s} frame {self.frames[s] - 1} unit {u}: assignment mismatch at tokens "
+                        f"{bad[:8].tolist()} gpu {ga[u][bad[:8]].tolist()} oracle {oa[bad[:8]].tolist()} "
+                        f"margins {res[i].margin[bad[:8]].tolist()}")
+                self.assign_checked += len(oa)
+
+    # -- checks --------------------------------------------------------------
+    def check_bank(self, stream: int = 0, bitwise: bool = False):
+        gb = self.gpu.read_bank(stream)
+        for i, u in enumerate(self.sample):
+            ob = self.oracle[stream].banks[i]
+            where = f"stream {stream} unit {u}"
+            assert np.array_equal(gb["n"][u].astype(np.int64), ob.n), where + " mass"
+            assert np.array_equal(gb["n_res"][u].astype(np.int64), ob.n_res), where + " n_res"
+            C = self.p.C
+            assert np.array_equal(gb["hist_k"][u][:, :, :C].astype(np.int64), ob.hist_k), where + " H^K"
+            assert np.array_equal(gb["hist_v"][u][:, :, :C].astype(np.int64), ob.hist_v), where + " H^V"
+            assert not gb["hist_k"][u][:, :, C:].any()
+            act = ob.n > 0
+            assert np.array_equal(gb["tau"][u][act].astype(np.int64), ob.tau[act]), where + " tau"
+            for name in ("sum_k", "sum_v", "sq_k", "sq_v"):
+                g = gb[name][u][act].astype(np.float64)
+                o = getattr(ob, name)[act].astype(np.float64)
+                err = np.linalg.norm(g - o, axis=1)
+                ref = np.linalg.norm(o, axis=1)
+                assert np.all(err <= STAT_RTOL * ref + 1e-30), f"{where} {name} rel {np.max(err / (ref + 1e-30))}"
+                if bitwise:
+                    assert np.array_equal(g, o), f"{where} {name} not bitwise equal"
+            assert np.allclose(gb["mu"][u][act], ob.mu[act], atol=1e-6, rtol=0), where + " mu"
+            assert np.allclose(gb["sigma"][u][act], ob.sigma[act], atol=1e-6, rtol=1e-6), where + " sigma"
+            if bitwise:
+                assert np.array_equal(gb["mu"][u][act], ob.mu[act]) and \
+                    np.array_equal(gb["sigma"][u][act], ob.sigma[act]), where + " spatial not bitwise"
+        return gb
+
+    def synthesize(self, stream: int = 0, check: bool = True):
+        self.gpu.synthesize(stream)
+        pseudo = self.oracle[stream].synthesize()
+        if check:
+            gk, gv, gbias = self.gpu.read_pseudo()
+            S = self.p.S
+            for i, u in enumerate(self.sample):
+                ps = pseudo[i]
+                n = len(ps.keys)
+                assert n == int((self.oracle[stream].banks[i].n > 0).sum()) * S
+                assert np.array_equal(gk[u][:n], ps.keys), f"unit {u}: pseudo keys differ"
+                assert np.array_equal(gv[u][:n], ps.values), f"unit {u}: pseudo values differ"
+                slots = ps.slots[::S]
+                assert np.allclose(gbias[u][slots], ps.bias[::S], rtol=1e-6, atol=1e-6)
+        return pseudo
+
+    def query(self, rng: np.random.Generator, tq: Optional[int] = None) -> np.ndarray:
+        wl = self.wl
+        tq = tq or wl.query_tokens
+        q = rng.standard_normal((wl.num_layers, tq, wl.num_q_heads, wl.head_dim))
+        # a third of the rows look for a sampled key direction, for peaked attention
+        q[:, ::3] *= 3.0
+        return W.quantize(q, wl.kv_dtype)
+
+    def attend(self, q: np.ndarray, pseudo, stream: int = 0):
+        torch, wl = self.torch, self.wl
+        qd = torch.from_numpy(q).to("cuda", self.dtype).contiguous()
+        o, lse = self.gpu.attend(stream, qd)
+        torch.cuda.synchronize()
+        go = o.float().cpu().numpy()
+        gl = lse.cpu().numpy()
+        oo, ol = self.oracle[stream].attend(q, wl.num_kv_heads, pseudo)
+        grp = wl.num_q_heads // wl.num_kv_heads
+        worst = 0.0
+        for u in self.sample:
+            l, h = divmod(u, wl.num_kv_heads)
+            heads = list(range(h * grp, (h + 1) * grp))
+            d = np.abs(go[l][:, heads] - oo[l][:, heads]).max()
+            worst = max(worst, float(d))
+            assert d <= READOUT_ATOL, f"unit {u}: readout abs err {d}"
+            dl = np.abs(gl[l][:, heads] - ol[l][:, heads]).max()
+            assert dl <= LSE_ATOL, f"unit {u}: lse abs err {dl}"
+        return worst, go, gl

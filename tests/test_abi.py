@@ -1,0 +1,73 @@
+"""The C-ABI library loads, exports every symbol protokv.h declares, and its
+host-only entry points (defaults, validation, workspace sizing) behave as
+documented.  No GPU is touched."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2606_26762_amd import protokv as pk
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "protokv.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:protokv_status|const char\*)\s+(protokv_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ["protokv_init", "protokv_append_frame", "protokv_fold", "protokv_synthesize",
+                     "protokv_attend"]:
+        assert required in names
+    assert sorted(pk.EXPORTED) == names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = pk.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", pk.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r" T (protokv_\w+)", out))
+    assert set(declared_functions()) <= exported
+
+
+def test_default_config_is_table5():
+    c = pk.default_config()
+    assert (c.pseudo_per_proto, c.pq_subspaces, c.pq_codewords, c.beam) == (8, 8, 16, 32)
+    assert (c.lambda_sp, c.lambda_idle, c.t_idle) == (0.1, 0.01, 120)
+    assert abs(c.eta - 0.05) < 1e-8 and c.pq_eps == 1.0
+    assert c.flags == pk.FLAG_PQ | pk.FLAG_MASS_BIAS
+    assert lib_status(c) == 0
+
+
+def lib_status(c):
+    return pk.lib().protokv_validate_config(ctypes.byref(c))
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 64, 2), ("num_q_heads", 30, 1), ("num_streams", 0, 1), ("pq_subspaces", 4, 2),
+    ("pq_codewords", 17, 2), ("pseudo_per_proto", 17, 2), ("beam", 4, 1), ("capacity", 0, 1),
+    ("window_frames", 0, 1), ("grid_h", 80, 2), ("kv_dtype", 7, 1), ("flags", 8, 1),
+    ("eta", 0.0, 1), ("pq_eps", 0.5, 2), ("ridge", 0.0, 1), ("lambda_sp", -1.0, 1),
+    ("max_query_tokens", 100, 2), ("max_query_tokens", 0, 1), ("t_idle", -1, 1),
+])
+def test_validation_rejects(field, value, status):
+    c = pk.default_config(**{field: value})
+    assert lib_status(c) == status
+    assert pk.lib().protokv_last_error(None)
+
+
+def test_workspace_size_scales_with_shape():
+    small = pk.workspace_size(pk.default_config(num_layers=1, num_kv_heads=1, num_q_heads=1))
+    full = pk.workspace_size(pk.default_config())
+    multi = pk.workspace_size(pk.default_config(num_streams=4))
+    assert 0 < small < full < multi
+    # rings + banks dominate: 112 units x (9 frames x 196 x 128 x 2 x 2 B + 256 x 3200 B)
+    assert full > 112 * (9 * 196 * 128 * 4 + 256 * 3200)
+    with pytest.raises(pk.ProtoKVError):
+        pk.workspace_size(pk.default_config(head_dim=96))

@@ -1,0 +1,222 @@
+"""GPU parity: libprotokv (through its C-ABI) against the CPU oracle.
+
+Each test names its workload (shape, seed) in its output before any GPU
+step, so a failure names the case.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2606_26762_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_26762_amd import protokv as pk
+    pk.lib()
+    yield
+
+
+def H():
+    from tests import gpu_harness
+    return gpu_harness
+
+
+def test_tiny_stream_fp32_full():
+    """1x1 head, fp32, 8x8 grid, 32 frames, window 4 frames, K=64 (whole stream)."""
+    h = H()
+    wl = W.WORKLOADS["tiny"]
+    h.log(f"case: {wl.name}")
+    pair = h.Pair(wl)
+    for f in range(wl.frames):
+        pair.step()
+        if f in (4, 5, 12, wl.frames - 1):
+            pair.check_bank(bitwise=True)
+    pseudo = pair.synthesize()
+    worst, *_ = pair.attend(pair.query(np.random.default_rng(1)), pseudo)
+    c = pair.gpu.counters()
+    h.log(f"assignments checked {pair.assign_checked}, near ties {pair.near_ties}, "
+          f"refined {c.refined}+{c.refined_full}, readout max abs err {worst:.2e}")
+    assert pair.assign_checked == (wl.frames - wl.window_frames) * wl.tokens_per_frame
+
+
+def test_7b_shape_one_layer():
+    """7B shape on one layer (4 kv heads, 28 q heads): 196 tokens/frame, K=256,
+    window 8 frames, 48 frames, bf16; every unit checked."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_q_heads=7 * 4, frames=48)
+    h.log(f"case: {wl.name} L=1 frames=48")
+    pair = h.Pair(wl)
+    for f in range(wl.frames):
+        pair.step()
+    pair.check_bank(bitwise=True)
+    pseudo = pair.synthesize()
+    worst, *_ = pair.attend(pair.query(np.random.default_rng(2)), pseudo)
+    c = pair.gpu.counters()
+    h.log(f"assignments {pair.assign_checked}, near ties {pair.near_ties}, refined {c.refined}"
+          f"+{c.refined_full}, touched {c.touched}, readout err {worst:.2e}")
+
+
+def test_ragged_shapes_seed_and_assign_same_fold():
+    """T=35 (5x7, ragged tiles), K=20 < T (seed and assign in one fold),
+    2 layers x 2 kv heads x 6 q heads, S=3, C=12, tq=5."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=2, num_kv_heads=2, num_q_heads=6, grid_h=5, grid_w=7,
+                                 frames=14, window_frames=2, capacity=20, query_tokens=5,
+                                 clusters=6)
+    h.log("case: ragged T=35 K=20 L=2 Hkv=2 Hq=6 S=3 C=12")
+    pair = h.Pair(wl, S=3, C=12)
+    for f in range(wl.frames):
+        pair.step()
+        if f == wl.window_frames:
+            pair.check_bank(bitwise=True)
+    pair.check_bank(bitwise=True)
+    pseudo = pair.synthesize()
+    for tq in (5, 1):
+        pair.attend(pair.query(np.random.default_rng(3), tq=tq), pseudo)
+
+
+def test_capacity_limit_gives_exact_attention():
+    """K >= evicted tokens: every token keeps its own slot, and the readout is
+    exact attention over the full history with far logits shifted by ln S
+    (checked against torch SDPA on the CPU, independent of the oracle)."""
+    import torch
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=4, grid_w=8,
+                                 frames=10, window_frames=3, capacity=7 * 32, query_tokens=6)
+    h.log("case: capacity limit T=32 K=224 frames=10 W=3")
+    pair = h.Pair(wl)
+    hist = []
+    for f in range(wl.frames):
+        gen = pair.host[0]
+        pair.step()
+    # rebuild the full history from the oracle's record of appended frames
+    pseudo = pair.synthesize()
+    q = pair.query(np.random.default_rng(4))
+    worst, go, _ = pair.attend(q, pseudo)
+    S = pair.p.S
+    for i, u in enumerate(pair.sample):
+        st = pair.oracle[0]
+        b = st.banks[i]
+        assert np.all(b.n[: (wl.frames - wl.window_frames) * 32] == 1)
+        far_k = b.sum_k[b.n > 0]
+        far_v = b.sum_v[b.n > 0]
+        kn, vn = st.near(i)
+        keys = np.concatenate([far_k, kn]).astype(np.float64)
+        vals = np.concatenate([far_v, vn]).astype(np.float64)
+        mask = np.concatenate([np.full(len(far_k), math.log(S)), np.zeros(len(kn))])
+        l, hk = divmod(u, wl.num_kv_heads)
+        grp = wl.num_q_heads // wl.num_kv_heads
+        for g in range(grp):
+            qh = torch.tensor(q[l][:, hk * grp + g].astype(np.float64))[None, None]
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                qh, torch.tensor(keys)[None, None], torch.tensor(vals)[None, None],
+                attn_mask=torch.tensor(mask)[None, None, None, :])[0, 0].numpy()
+            assert np.abs(go[l][:, hk * grp + g] - ref).max() <= 2e-2
+
+
+def test_duplicate_tokens_force_exact_ties():
+    """All tokens of every frame share one key and value (lambda_sp = 0), so
+    in the first assigning fold every slot has the same cost: the exact tie
+    goes to the lowest slot on both sides.  Later folds stay in parity up to
+    counted near ties."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=1, num_q_heads=1, grid_h=4, grid_w=4,
+                                 frames=9, window_frames=2, capacity=8, query_tokens=4)
+    h.log("case: forced ties T=16 K=8")
+    pair = h.Pair(wl, lambda_sp=0.0)
+    orig = pair.host[0].next_frame
+
+    def dup_frame():
+        k, v = orig()
+        k[:] = k[:, :1]
+        v[:] = v[:, :1]
+        return k, v
+    pair.host[0].next_frame = dup_frame
+    for f in range(wl.window_frames + 1):
+        pair.step()
+    ga = pair.gpu.read_assignments(0)
+    assert ga[0][:8].tolist() == list(range(8))   # seeds
+    assert np.all(ga[0][8:] == 0)                 # exact tie -> lowest slot
+    for f in range(wl.frames - wl.window_frames - 1):
+        pair.step()
+    pair.check_bank()
+    h.log(f"near ties {pair.near_ties}, gpu counter {pair.gpu.counters().near_ties}")
+
+
+@pytest.mark.parametrize("use_pq,mass_bias", [(False, True), (True, False)])
+def test_ablation_switches(use_pq, mass_bias):
+    """'w/o residual stats' (PQ off) and 'b_k = 0' (mass bias off)."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=7, grid_w=7,
+                                 frames=16, window_frames=3, capacity=64, query_tokens=8)
+    h.log(f"case: ablation use_pq={use_pq} mass_bias={mass_bias}")
+    pair = h.Pair(wl, use_pq=use_pq, mass_bias=mass_bias)
+    for f in range(wl.frames):
+        pair.step()
+    pair.check_bank(bitwise=True)
+    pseudo = pair.synthesize()
+    pair.attend(pair.query(np.random.default_rng(5)), pseudo)
+
+
+def test_multi_stream_round_robin():
+    """3 independent streams appended in one batched call per round, plus a
+    round where only stream 1 advances; per-stream parity."""
+    h = H()
+    wl = W.WORKLOADS["multi"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=6, grid_w=6,
+                                    frames=12, window_frames=2, capacity=48, query_tokens=4, streams=3)
+    h.log("case: 3 streams T=36 K=48")
+    pair = h.Pair(wl, streams=3)
+    for f in range(8):
+        pair.step()
+    pair.step(streams=[1])
+    pair.step(streams=[2, 0])
+    for s in range(3):
+        pair.check_bank(stream=s, bitwise=True)
+        pseudo = pair.synthesize(stream=s)
+        pair.attend(pair.query(np.random.default_rng(6 + s)), pseudo, stream=s)
+
+
+def test_state_machine_errors():
+    import torch
+    from paper_2606_26762_amd import protokv as pk
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=1, num_q_heads=1, grid_h=2, grid_w=2,
+                                 frames=4, window_frames=1, capacity=4, query_tokens=2)
+    h.log("case: state machine errors")
+    pair = h.Pair(wl)
+    g = pair.gpu
+    q = torch.zeros((1, 2, 1, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(pk.ProtoKVError) as e:
+        g.attend(0, q)                         # nothing appended
+    assert e.value.status == 4
+    pair.step()
+    pair.step()                                # frame 1 evicts frame 0 -> folded by step
+    k = torch.zeros((1, 1, 1, 4, 128), dtype=torch.bfloat16, device="cuda")
+    g.append_frame([0], k, k)                  # pending eviction
+    with pytest.raises(pk.ProtoKVError) as e:
+        g.append_frame([0], k, k)
+    assert e.value.status == 4
+    with pytest.raises(pk.ProtoKVError) as e:
+        g.synthesize(0)
+    assert e.value.status == 4
+    g.fold()
+    with pytest.raises(pk.ProtoKVError) as e:
+        g.attend(0, q)                         # no synthesis since the fold
+    assert e.value.status == 4
+    g.synthesize(0)
+    g.attend(0, q)
+    with pytest.raises(pk.ProtoKVError) as e:
+        g.attend(0, torch.zeros((1, 3, 1, 128), dtype=torch.bfloat16, device="cuda"))  # tq > max
+    assert e.value.status == 1
+    with pytest.raises(pk.ProtoKVError) as e:
+        g.append_frame([3], k, k)
+    assert e.value.status == 1
+    info = g.stream_info(0)
+    assert (info.frames, info.pending, info.active_slots) == (3, 0, 4)
