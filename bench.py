@@ -1,0 +1,282 @@
+#!/usr/bin/env python3
+"""Benchmark of the ProtoKV far-memory hot path on one MI355X.
+
+Workload: one stream of a 7B-class video LLM (28 layers x 4 KV heads, 28
+query heads, head_dim 128, bf16 KV, 196 visual tokens per frame on a 14x14
+grid, near window 8 frames, K = 256 prototypes per (layer, kv head)), seeded
+synthetic frames drawn on the GPU (the paper's video datasets stand in).
+
+A step = one frame through the whole hot path's streaming side: append the
+frame to the near window of all 112 (layer, kv head) units and fold the
+evicted frame (seed / screen + assign / aggregate).  The timed region is
+`--steps` such frames followed by one 32-token query (synthesize + attend),
+so every hot-path step runs inside it.  `value` = evicted model tokens
+folded per second over the timed region (each token folded into all 112
+units).  Readout latency per query is timed separately (median of repeats).
+
+Per-kernel device times come from HIP events the library records around
+each launch on the launch stream (a second pass over further frames); the
+roofline object uses the dominant kernel's algorithmic bytes per launch.
+"""
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK = 2500.0     # dense bf16 TFLOP/s
+ROW_BYTES_USED = 3104       # bytes of a bank row that carry state
+CACHE_BYTES = 2 * 128 * 2 + 32   # hi + lo bf16 unit centre + screening meta
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=192)
+    ap.add_argument("--warmup", type=int, default=64)
+    ap.add_argument("--workload", default="7b")
+    ap.add_argument("--profile-frames", type=int, default=32)
+    ap.add_argument("--query-reps", type=int, default=20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-units", type=int, default=16)
+    ap.add_argument("--cpu-frames", type=int, default=24)
+    return ap.parse_args()
+
+
+def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0, rows=0):
+    """Bytes the method must move per launch of `kernel` (all units of one stream)."""
+    U, T, D, K, S = wl.units, wl.tokens_per_frame, wl.head_dim, wl.capacity, cfg.pseudo_per_proto
+    b = 4 if wl.kv_dtype == "fp32" else 2
+    if kernel == "ring_insert":
+        return U * T * D * b * 2 * 2                       # read frame K,V + write ring K,V
+    if kernel == "screen":
+        return U * (T * D * b + K * CACHE_BYTES + T * 4)   # evicted keys, centre cache, assignment
+    if kernel == "aggregate":
+        return (U * (2 * T * D * b + T * 4 + 2 * 8 * 16 * 16 * 4)    # evicted K,V, assignment, codebooks
+                + touched_per_launch * (2 * ROW_BYTES_USED + CACHE_BYTES))  # row RMW + cache rewrite
+    if kernel == "synthesize":
+        return U * n_active * (2 * 4 * D + 2 * 8 * 16 * 4 + 32) + U * n_active * S * D * b * 2 + U * K * 4
+    if kernel == "attend":
+        return U * (2 * ctx * D * b + (ctx // max(S, 1)) * 4 + 2 * rows * D * b)
+    return 0
+
+
+def cpu_baseline(args, wl):
+    """The oracle, untuned, on a bounded sample: --cpu-units units of the same
+    workload, bank filled untimed, then --cpu-frames timed steady-state folds;
+    scaled to model tokens/s for all units.  Readout: one unit's synthesis +
+    attention, scaled to all units."""
+    from threadpoolctl import threadpool_limits
+    from oracle import protokv_oracle as O
+    from paper_2606_26762_amd import workloads as W
+    units = list(range(args.cpu_units))
+    cb = W.make_codebooks(wl, units=units, samples=1024, iters=8)
+    p = O.Params(head_dim=wl.head_dim, grid_h=wl.grid_h, grid_w=wl.grid_w,
+                 window_frames=wl.window_frames, capacity=wl.capacity, kv_dtype=wl.kv_dtype)
+    gen = W.HostStream(wl, units=units)
+    st = O.OracleStream(p, units, cb)
+    warm = wl.window_frames + math.ceil(wl.capacity / wl.tokens_per_frame) + 1
+    with threadpool_limits(1):
+        for _ in range(warm):
+            st.append_frame(*gen.next_frame())
+        frames = [gen.next_frame() for _ in range(args.cpu_frames)]
+        t0 = time.perf_counter()
+        for k, v in frames:
+            st.append_frame(k, v)
+        t_fold = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        ps = [O.synthesize(st.banks[0], cb[0], p)]
+        q = np.random.default_rng(0).standard_normal(
+            (1, wl.query_tokens, wl.num_q_heads // wl.num_kv_heads, wl.head_dim))
+        kc, vc, bias = st.context(0, ps[0])
+        O.attend(q.reshape(-1, wl.head_dim), kc, vc, bias)
+        t_read = time.perf_counter() - t0
+    scale = wl.units / len(units)
+    tok_s = args.cpu_frames * wl.tokens_per_frame / (t_fold * scale)
+    return {"value": tok_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": (f"{len(units)} of {wl.units} units x {args.cpu_frames} steady-state frames "
+                       f"(fold {t_fold:.1f} s), readout of 1 unit ({t_read:.1f} s); scaled to all units"),
+            "readout_us_per_query": t_read * wl.units * 1e6,
+            "cpu": _cpu_model(), "nproc": os.cpu_count()}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              f"(units are independent and would shard by stream or kv head, see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_26762_amd import protokv as pk
+    from paper_2606_26762_amd import workloads as W
+
+    wl = W.WORKLOADS[args.workload]
+    frames_needed = args.warmup + args.steps + args.profile_frames
+    assert args.warmup >= wl.window_frames + math.ceil(wl.capacity / wl.tokens_per_frame), \
+        "warmup must fill the bank"
+    lib = pk.lib()
+    cfg = pk.default_config(num_streams=1, num_layers=wl.num_layers, num_kv_heads=wl.num_kv_heads,
+                            num_q_heads=wl.num_q_heads, grid_h=wl.grid_h, grid_w=wl.grid_w,
+                            window_frames=wl.window_frames, capacity=wl.capacity,
+                            max_query_tokens=wl.query_tokens,
+                            kv_dtype=pk.KV_FP32 if wl.kv_dtype == "fp32" else pk.KV_BF16)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cb = W.make_codebooks_device(wl)
+    eng = pk.ProtoKV(cfg, cb)
+    gen = W.DeviceStream(wl, n_streams=1)
+    ks, vs = [], []
+    for _ in range(frames_needed):
+        k, v = gen.next_frame()
+        ks.append(k)
+        vs.append(v)
+    q = gen.query()
+    o = torch.empty_like(q)
+    lse = torch.empty(q.shape[:3], dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    h = eng.h
+    ids = (ctypes.c_int32 * 1)(0)
+    kp = [ctypes.c_void_p(t.data_ptr()) for t in ks]
+    vp = [ctypes.c_void_p(t.data_ptr()) for t in vs]
+    qp, op, lp = ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(o.data_ptr()), ctypes.c_void_p(lse.data_ptr())
+    tq = q.shape[1]
+    append, fold = lib.protokv_append_frame, lib.protokv_fold
+    synth, attend = lib.protokv_synthesize, lib.protokv_attend
+
+    def run_frames(lo, hi):
+        for i in range(lo, hi):
+            if append(h, ids, 1, kp[i], vp[i], sp) or fold(h, sp):
+                raise RuntimeError(lib.protokv_last_error(h))
+
+    def run_query():
+        if synth(h, 0, sp) or attend(h, 0, qp, tq, op, lp, sp):
+            raise RuntimeError(lib.protokv_last_error(h))
+
+    # warm-up: fill the window and the bank, compile paths, one query
+    run_frames(0, args.warmup)
+    run_query()
+    torch.cuda.synchronize()
+
+    # timed region: --steps frames + one query
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    run_frames(args.warmup, args.warmup + args.steps)
+    e1.record(stream)
+    run_query()
+    e2.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_total = e0.elapsed_time(e2)
+    ms_fold = e0.elapsed_time(e1)
+    ms_query_in_region = e1.elapsed_time(e2)
+    T = wl.tokens_per_frame
+    value = args.steps * T / (ms_total / 1e3)
+
+    # readout latency: median over repeats, synthesize+attend and attend only
+    def median_ms(fn, reps):
+        out = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            out.append(a.elapsed_time(b))
+        return float(np.median(out))
+    readout_ms = median_ms(run_query, args.query_reps)
+    attend_ms = median_ms(lambda: attend(h, 0, qp, tq, op, lp, sp), args.query_reps)
+
+    # per-kernel device times (library-recorded HIP events), further frames
+    c0 = eng.counters()
+    eng.profile(True)
+    lo = args.warmup + args.steps
+    run_frames(lo, lo + args.profile_frames)
+    for _ in range(5):
+        run_query()
+    kt = eng.profile_read()
+    eng.profile(False)
+    c1 = eng.counters()
+    info = eng.stream_info(0)
+    n_active = info.active_slots
+    touched = (c1.touched - c0.touched) / max(1, kt.get("aggregate", {}).get("launches", 1))
+    rows = tq * (wl.num_q_heads // wl.num_kv_heads)
+    ctx = min(info.frames, wl.window_frames) * T + n_active * cfg.pseudo_per_proto
+    kernels = {}
+    for name, d in kt.items():
+        nbytes = algorithmic_bytes(name, wl, cfg, touched_per_launch=touched, n_active=n_active,
+                                   ctx=ctx, rows=rows)
+        kernels[name] = {"avg_us": round(d["avg_us"], 3), "launches": d["launches"],
+                         "alg_bytes": int(nbytes),
+                         "gbs": round(nbytes / (d["avg_us"] * 1e-6) / 1e9, 1) if nbytes else None}
+    # dominant kernel of the streaming step
+    per_frame = {n: kernels[n]["avg_us"] * kernels[n]["launches"] / args.profile_frames
+                 for n in ("ring_insert", "seed", "screen", "aggregate") if n in kernels}
+    dom = max(per_frame, key=per_frame.get)
+    dk = kernels[dom]
+    achieved = dk["gbs"]
+    roofline = {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "alg_bytes_per_launch": dk["alg_bytes"], "avg_us": dk["avg_us"]}
+    # screen MFMA work, for reference: 2 (hi, lo) x 2 N K D flops per unit
+    scr_flops = wl.units * 2 * 2 * T * wl.capacity * wl.head_dim
+    if "screen" in kernels:
+        kernels["screen"]["mfma_tflops"] = round(scr_flops / (kernels["screen"]["avg_us"] * 1e-6) / 1e12, 2)
+    att_flops = wl.units * 4 * rows * ctx * wl.head_dim
+    if "attend" in kernels:
+        kernels["attend"]["mfma_tflops"] = round(att_flops / (kernels["attend"]["avg_us"] * 1e-6) / 1e12, 2)
+
+    result = {
+        "metric": "evicted tokens folded/sec/GPU + readout µs/query; % HBM/MFMA roofline",
+        "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_total / args.steps, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded on-device Gaussian-mixture stream, 7B video-LLM shape)",
+        "config": {"workload": wl.name, "layers": wl.num_layers, "kv_heads": wl.num_kv_heads,
+                   "q_heads": wl.num_q_heads, "head_dim": wl.head_dim, "tokens_per_frame": T,
+                   "window_frames": wl.window_frames, "capacity": wl.capacity,
+                   "pseudo_per_proto": cfg.pseudo_per_proto, "query_tokens": tq,
+                   "frames_streamed": args.warmup + args.steps},
+        "fold_tokens_per_s": round(args.steps * T / (ms_fold / 1e3), 1),
+        "fold_us_per_frame": round(1e3 * ms_fold / args.steps, 2),
+        "query_us_in_region": round(1e3 * ms_query_in_region, 2),
+        "readout_us_per_query": round(1e3 * readout_ms, 2),
+        "attend_us_per_query": round(1e3 * attend_ms, 2),
+        "wall_s_timed_region": round(t_wall, 4),
+        "touched_per_fold": round(touched, 1), "active_slots": n_active,
+        "context_tokens": ctx,
+        "refined_fraction": round((c1.refined + c1.refined_full) / max(1, c1.tokens_assigned), 5),
+        "near_ties": c1.near_ties,
+        "kernels": kernels,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(args, wl)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -210,6 +210,31 @@ protokv_status protokv_read_bank(protokv_t h, int32_t stream_id, void* dst, size
 protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float* bias,
                                    void* stream);
 
+/* Kernel ids of protokv_kernel_times. */
+enum {
+  PROTOKV_K_RING_INSERT = 0,
+  PROTOKV_K_SEED = 1,
+  PROTOKV_K_SCREEN = 2,
+  PROTOKV_K_AGGREGATE = 3,
+  PROTOKV_K_SYNTHESIZE = 4,
+  PROTOKV_K_ATTEND = 5,
+  PROTOKV_K_ATTEND_MERGE = 6,
+  PROTOKV_K_COUNT = 8
+};
+
+typedef struct {
+  double ms[PROTOKV_K_COUNT];          /* summed device time per kernel */
+  uint64_t launches[PROTOKV_K_COUNT];  /* launches timed per kernel */
+} protokv_kernel_times;
+
+/* Diagnostics: enable != 0 brackets every kernel launch of this handle with
+ * a pair of HIP events recorded on the launch stream (and clears the totals);
+ * enable == 0 stops recording.  Host only; creates HIP events on first use. */
+protokv_status protokv_profile(protokv_t h, int32_t enable);
+
+/* Sums the recorded event pairs into `out` (waits for each end event). */
+protokv_status protokv_profile_read(protokv_t h, protokv_kernel_times* out);
+
 /* Message for the last failure on h (or of protokv_init when h is NULL).
  * Valid until the next call on h. */
 const char* protokv_last_error(protokv_t h);

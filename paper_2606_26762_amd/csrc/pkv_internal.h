@@ -121,5 +121,7 @@ hipError_t launch_synthesize(const Dims& dm, const Workspace& ws, int sid, int n
                              hipStream_t st);
 hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& aa,
                          hipStream_t st);
+hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa,
+                               hipStream_t st);
 
 }  // namespace pkv

@@ -115,6 +115,35 @@ struct protokv_ctx {
   int synth_active = 0;
   uint64_t folds = 0, assigned = 0, seeded = 0;
   std::string err;
+  // per-kernel event timing (diagnostics)
+  bool profiling = false;
+  std::vector<hipEvent_t> ev_pool;
+  struct Timed { int id; hipEvent_t a, b; };
+  std::vector<Timed> timed;
+  size_t ev_next = 0;
+
+  template <class F>
+  hipError_t launch(int id, hipStream_t st, F&& f) {
+    if (!profiling) return f();
+    hipEvent_t e[2];
+    for (int i = 0; i < 2; ++i) {
+      if (ev_next == ev_pool.size()) {
+        hipEvent_t ne;
+        hipError_t r = hipEventCreate(&ne);
+        if (r != hipSuccess) return r;
+        ev_pool.push_back(ne);
+      }
+      e[i] = ev_pool[ev_next++];
+    }
+    hipError_t r = hipEventRecord(e[0], st);
+    if (r == hipSuccess) r = f();
+    if (r == hipSuccess) r = hipEventRecord(e[1], st);
+    if (r == hipSuccess) timed.push_back({id, e[0], e[1]});
+    return r;
+  }
+  ~protokv_ctx() {
+    for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
+  }
 
   protokv_status fail(protokv_status s, const std::string& m) {
     err = m;
@@ -285,8 +314,10 @@ protokv_status protokv_append_frame(protokv_t h, const int32_t* ids, int32_t n, 
       ab.sid[i] = ids[b0 + i];
       ab.slot[i] = (int)(ss.frames % (uint64_t)(h->dm.W + 1));
     }
-    protokv_status s = h->dev(launch_ring_insert(h->dm, h->ws, ab, (const uint8_t*)k + b0 * entry_bytes,
-                                                 (const uint8_t*)v + b0 * entry_bytes, hs),
+    protokv_status s = h->dev(h->launch(PROTOKV_K_RING_INSERT, hs, [&] {
+                                return launch_ring_insert(h->dm, h->ws, ab, (const uint8_t*)k + b0 * entry_bytes,
+                                                          (const uint8_t*)v + b0 * entry_bytes, hs);
+                              }),
                               "append");
     if (s != PROTOKV_OK) return s;
   }
@@ -327,9 +358,15 @@ protokv_status protokv_fold(protokv_t h, void* stream) {
       any_assign |= fb.nseed[i] < T;
     }
     protokv_status st = PROTOKV_OK;
-    if (max_seed > 0) st = h->dev(launch_seed(h->dm, h->ws, fb, max_seed, hs), "fold/seed");
-    if (st == PROTOKV_OK && any_assign) st = h->dev(launch_screen(h->dm, h->ws, fb, hs), "fold/screen");
-    if (st == PROTOKV_OK && any_assign) st = h->dev(launch_aggregate(h->dm, h->ws, fb, hs), "fold/aggregate");
+    if (max_seed > 0)
+      st = h->dev(h->launch(PROTOKV_K_SEED, hs, [&] { return launch_seed(h->dm, h->ws, fb, max_seed, hs); }),
+                  "fold/seed");
+    if (st == PROTOKV_OK && any_assign)
+      st = h->dev(h->launch(PROTOKV_K_SCREEN, hs, [&] { return launch_screen(h->dm, h->ws, fb, hs); }),
+                  "fold/screen");
+    if (st == PROTOKV_OK && any_assign)
+      st = h->dev(h->launch(PROTOKV_K_AGGREGATE, hs, [&] { return launch_aggregate(h->dm, h->ws, fb, hs); }),
+                  "fold/aggregate");
     if (st != PROTOKV_OK) return st;
     for (int i = 0; i < fb.n; ++i) {
       StreamState& ss = h->st[fb.sid[i]];
@@ -349,7 +386,10 @@ protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
   if (!h) return PROTOKV_E_INVALID;
   if (sid < 0 || sid >= h->cfg.num_streams) return h->fail(PROTOKV_E_INVALID, "synthesize: stream id out of range");
   if (h->st[sid].pending) return h->fail(PROTOKV_E_STATE, "synthesize: stream has an unfolded eviction");
-  protokv_status s = h->dev(launch_synthesize(h->dm, h->ws, sid, h->st[sid].active, (hipStream_t)stream),
+  hipStream_t hs = (hipStream_t)stream;
+  protokv_status s = h->dev(h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] {
+                              return launch_synthesize(h->dm, h->ws, sid, h->st[sid].active, hs);
+                            }),
                             "synthesize");
   if (s != PROTOKV_OK) return s;
   h->synth_stream = sid;
@@ -388,7 +428,12 @@ protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t t
   splits = (ctx + chunk - 1) / chunk;
   aa.splits = splits;
   aa.chunk = chunk;
-  return h->dev(launch_attend(h->dm, h->ws, aa, (hipStream_t)stream), "attend");
+  hipStream_t hs = (hipStream_t)stream;
+  protokv_status s = h->dev(h->launch(PROTOKV_K_ATTEND, hs, [&] { return launch_attend(h->dm, h->ws, aa, hs); }),
+                            "attend");
+  if (s != PROTOKV_OK) return s;
+  return h->dev(h->launch(PROTOKV_K_ATTEND_MERGE, hs, [&] { return launch_attend_merge(h->dm, h->ws, aa, hs); }),
+                "attend/merge");
 }
 
 protokv_status protokv_stream_info_get(protokv_t h, int32_t sid, protokv_stream_info* out) {
@@ -451,6 +496,30 @@ protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float*
   if (s == PROTOKV_OK && values) s = copy_out(h, values, h->ws.pv, n, stream, "read_pseudo");
   if (s == PROTOKV_OK && bias) s = copy_out(h, bias, h->ws.pbias, (size_t)h->dm.units * h->dm.K * 4, stream, "read_pseudo");
   return s;
+}
+
+protokv_status protokv_profile(protokv_t h, int32_t enable) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (enable) {
+    h->timed.clear();
+    h->ev_next = 0;
+  }
+  h->profiling = enable != 0;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_profile_read(protokv_t h, protokv_kernel_times* out) {
+  if (!h || !out) return PROTOKV_E_INVALID;
+  std::memset(out, 0, sizeof(*out));
+  for (const auto& t : h->timed) {
+    hipError_t e = hipEventSynchronize(t.b);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, t.a, t.b);
+    if (e != hipSuccess) return h->dev(e, "profile_read");
+    out->ms[t.id] += ms;
+    out->launches[t.id] += 1;
+  }
+  return PROTOKV_OK;
 }
 
 const char* protokv_last_error(protokv_t h) { return h ? h->err.c_str() : g_init_err.c_str(); }

@@ -504,16 +504,19 @@ hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& 
   const int rows = aa.tq * grp;
   if (dm.kv_fp32) {
     hipLaunchKernelGGL(k_attend_f32, dim3(dm.units * rows * aa.splits), dim3(64), 0, st, dm, ws, aa, rows);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_attend_merge<1>, dim3(dm.units * rows), dim3(64), 0, st, dm, ws, aa, rows);
   } else {
     const int waves = (rows + 31) / 32;
     hipLaunchKernelGGL(k_attend_bf16, dim3(dm.units * aa.splits), dim3(waves * 64), 0, st, dm, ws, aa, rows);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_attend_merge<0>, dim3(dm.units * rows), dim3(64), 0, st, dm, ws, aa, rows);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa, hipStream_t st) {
+  const int rows = aa.tq * (dm.Hq / dm.Hkv);
+  if (dm.kv_fp32)
+    hipLaunchKernelGGL(k_attend_merge<1>, dim3(dm.units * rows), dim3(64), 0, st, dm, ws, aa, rows);
+  else
+    hipLaunchKernelGGL(k_attend_merge<0>, dim3(dm.units * rows), dim3(64), 0, st, dm, ws, aa, rows);
   return hipGetLastError();
 }
 

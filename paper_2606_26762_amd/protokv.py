@@ -26,8 +26,10 @@ EXPORTED = [
     "protokv_default_config", "protokv_validate_config", "protokv_workspace_size", "protokv_init",
     "protokv_destroy", "protokv_append_frame", "protokv_fold", "protokv_synthesize", "protokv_attend",
     "protokv_stream_info_get", "protokv_get_counters", "protokv_read_assignments", "protokv_read_bank",
-    "protokv_read_pseudo", "protokv_last_error",
+    "protokv_read_pseudo", "protokv_profile", "protokv_profile_read", "protokv_last_error",
 ]
+
+KERNELS = ["ring_insert", "seed", "screen", "aggregate", "synthesize", "attend", "attend_merge"]
 
 
 class ProtoKVError(RuntimeError):
@@ -62,6 +64,10 @@ class Counters(ctypes.Structure):
                 ("touched", ctypes.c_uint64)]
 
 
+class KernelTimes(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double * 8), ("launches", ctypes.c_uint64 * 8)]
+
+
 _lib = None
 
 
@@ -87,6 +93,8 @@ def lib() -> ctypes.CDLL:
         L.protokv_read_assignments.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_read_bank.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_read_pseudo.argtypes = [vp, vp, vp, vp, vp]
+        L.protokv_profile.argtypes = [vp, i32]
+        L.protokv_profile_read.argtypes = [vp, P(KernelTimes)]
         L.protokv_last_error.argtypes = [vp]
         L.protokv_last_error.restype = ctypes.c_char_p
         for name in EXPORTED:
@@ -236,6 +244,20 @@ class ProtoKV:
             (lambda r: (r.astype(np.uint32) << 16).view(np.float32))
         shape = (self.units, self.cfg.capacity * self.cfg.pseudo_per_proto, self.cfg.head_dim)
         return conv(raw_k).reshape(shape), conv(raw_v).reshape(shape), bias.reshape(self.units, -1)
+
+    def profile(self, enable: bool):
+        _check(lib().protokv_profile(self.h, 1 if enable else 0), self.h)
+
+    def profile_read(self) -> Dict[str, dict]:
+        """-> {kernel: {"ms": total, "launches": n, "avg_us": mean}} for timed kernels."""
+        kt = KernelTimes()
+        _check(lib().protokv_profile_read(self.h, ctypes.byref(kt)), self.h)
+        out = {}
+        for i, name in enumerate(KERNELS):
+            n = int(kt.launches[i])
+            if n:
+                out[name] = {"ms": kt.ms[i], "launches": n, "avg_us": 1000.0 * kt.ms[i] / n}
+        return out
 
     def _check_tensor(self, t, shape):
         if tuple(t.shape) != tuple(shape):

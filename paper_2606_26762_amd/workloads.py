@@ -372,3 +372,26 @@ class DeviceStream:
         q[:, half:] += 4.0 * math.sqrt(D) * mu
         dt = torch.bfloat16 if wl.kv_dtype == "bf16" else torch.float32
         return q.to(dt).contiguous()
+
+
+def make_codebooks_device(wl: Workload, n_streams: int = 1, samples: int = 2048, iters: int = 12,
+                          G: int = 8, C: int = 16, device="cuda", seed: int = 0):
+    """Same recipe as ``make_codebooks`` (Lloyd k-means per subspace on seeded
+    warm-up residuals), batched over every unit on the GPU.  Returns a numpy
+    float32 array [n_streams][units][2][G][C][D/G]."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(wl.seed_base * 7919 + seed)
+    U = n_streams * wl.units
+    Dp = wl.head_dim // G
+    scale = torch.tensor([wl.sigma, 1.0], device=device).view(1, 2, 1, 1, 1)
+    x = torch.randn(U, 2, G, samples, Dp, generator=gen, device=device) * scale
+    x = x.reshape(U * 2 * G, samples, Dp)
+    cen = x[:, :C].clone()
+    for _ in range(iters):
+        lab = torch.cdist(x, cen).argmin(dim=-1)                       # [B][samples]
+        onehot = torch.nn.functional.one_hot(lab, C).to(x.dtype)       # [B][samples][C]
+        cnt = onehot.sum(1)                                            # [B][C]
+        tot = torch.einsum("bsc,bsd->bcd", onehot, x)
+        cen = torch.where(cnt[..., None] > 0, tot / cnt.clamp_min(1)[..., None], cen)
+    return cen.reshape(n_streams, wl.units, 2, G, C, Dp).float().cpu().numpy()
