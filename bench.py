@@ -59,8 +59,11 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
         return U * T * D * b * 2 * 2                       # read frame K,V + write ring K,V
     if kernel == "screen":
         return U * (T * D * b + K * CACHE_BYTES + T * 4)   # evicted keys, centre cache, assignment
+    if kernel == "pq_encode":
+        # evicted K,V, assignment, codebooks, the assigned slots' sums (K and V), codes written
+        return U * (2 * T * D * b + T * 4 + 2 * 8 * 16 * 16 * 4 + T * 2 * D * 4 + T * 16)
     if kernel == "aggregate":
-        return (U * (2 * T * D * b + T * 4 + 2 * 8 * 16 * 16 * 4)    # evicted K,V, assignment, codebooks
+        return (U * (2 * T * D * b + T * 4 + T * 16)                   # evicted K,V, assignment, codes
                 + touched_per_launch * (2 * ROW_BYTES_USED + CACHE_BYTES))  # row RMW + cache rewrite
     if kernel == "synthesize":
         return U * n_active * (2 * 4 * D + 2 * 8 * 16 * 4 + 32) + U * n_active * S * D * b * 2 + U * K * 4
@@ -234,7 +237,7 @@ def main():
                          "gbs": round(nbytes / (d["avg_us"] * 1e-6) / 1e9, 1) if nbytes else None}
     # dominant kernel of the streaming step
     per_frame = {n: kernels[n]["avg_us"] * kernels[n]["launches"] / args.profile_frames
-                 for n in ("ring_insert", "seed", "screen", "aggregate") if n in kernels}
+                 for n in ("ring_insert", "seed", "screen", "pq_encode", "aggregate") if n in kernels}
     dom = max(per_frame, key=per_frame.get)
     dk = kernels[dom]
     achieved = dk["gbs"]

@@ -219,6 +219,7 @@ enum {
   PROTOKV_K_SYNTHESIZE = 4,
   PROTOKV_K_ATTEND = 5,
   PROTOKV_K_ATTEND_MERGE = 6,
+  PROTOKV_K_PQ_ENCODE = 7,
   PROTOKV_K_COUNT = 8
 };
 

@@ -179,6 +179,23 @@ hipError_t launch_seed(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
 // Exact cost of Eq. 1 in float64, same formula and operation order as the
 // oracle: cos from sumK, unsquared Mahalanobis with ridge, idle indicator.
 // ---------------------------------------------------------------------------
+// Eq. 1 from a float64 dot product K.sumK, |K| and |sumK|^2 (oracle formula and
+// operation order for the spatial and idle terms).
+__device__ double cost_from_dot(const Dims& dm, double dot, double knorm, double n2, double kx, double ky,
+                                const uint8_t* row, int t_frame) {
+  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  double denom = knorm * sqrt(n2);
+  double cosv = denom > 0.0 ? dot / denom : 0.0;
+  double dx = kx - (double)m.mu_x, dy = ky - (double)m.mu_y;
+  double A = (double)m.sxx + dm.ridge, B = (double)m.sxy, Cc = (double)m.syy + dm.ridge;
+  double det = A * Cc - B * B;
+  double q = (Cc * dx * dx - 2.0 * B * dx * dy + A * dy * dy) / det;
+  double dm_ = sqrt(q > 0.0 ? q : 0.0);
+  double idle = (t_frame - m.tau / dm.T) > dm.t_idle ? 1.0 : 0.0;
+  return -cosv + dm.lambda_sp * dm_ + dm.lambda_idle * idle;
+}
+
+// Exact cost of Eq. 1 in float64 for one (token, slot), serial over dimensions.
 template <int FP32>
 __device__ double exact_cost(const Dims& dm, const uint8_t* keyrow, double knorm, double kx, double ky,
                              const uint8_t* row, int t_frame) {
@@ -193,16 +210,7 @@ __device__ double exact_cost(const Dims& dm, const uint8_t* keyrow, double knorm
     n2 = n2 + (double)sv.x * (double)sv.x;
     n2 = n2 + (double)sv.y * (double)sv.y;
   }
-  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
-  double denom = knorm * sqrt(n2);
-  double cosv = denom > 0.0 ? dot / denom : 0.0;
-  double dx = kx - (double)m.mu_x, dy = ky - (double)m.mu_y;
-  double A = (double)m.sxx + dm.ridge, B = (double)m.sxy, Cc = (double)m.syy + dm.ridge;
-  double det = A * Cc - B * B;
-  double q = (Cc * dx * dx - 2.0 * B * dx * dy + A * dy * dy) / det;
-  double dm_ = sqrt(q > 0.0 ? q : 0.0);
-  double idle = (t_frame - m.tau / dm.T) > dm.t_idle ? 1.0 : 0.0;
-  return -cosv + dm.lambda_sp * dm_ + dm.lambda_idle * idle;
+  return cost_from_dot(dm, dot, knorm, n2, kx, ky, row, t_frame);
 }
 
 // Element n of a 4-entry register list (INFINITY / -1 past the end).
@@ -219,22 +227,47 @@ __device__ __forceinline__ bool better(double c1, int k1, double c2, int k2) {
 }
 
 // ---------------------------------------------------------------------------
-// Screen + argmin.  Workgroup = 4 waves x 32 tokens; each wave scores its 32
-// tokens against every active slot with v_mfma_f32_32x32x16_bf16
-// (slots = rows, tokens = columns), slot tiles of 32 staged in LDS.
-// Per token it keeps the 4 smallest lower bounds and the smallest upper
-// bound of the cost; a token whose bound interval admits a single slot is
-// assigned directly, otherwise the candidate slots (or all slots, when more
+// Screen + argmin.  Workgroup = one tile of 32 evicted tokens of one unit;
+// its 4 waves split the active slots (slot tiles t = wave, wave + 4, ...)
+// and score them against the 32 tokens with v_mfma_f32_32x32x16_bf16
+// (slots = rows, tokens = columns, unit centres as a hi + lo bf16 split read
+// straight from global memory).  Per token each lane keeps the 4 smallest
+// lower bounds and the smallest upper bound of the cost; the waves' lists are
+// merged through LDS.  A token whose bound interval admits a single slot is
+// assigned directly; otherwise the candidate slots (or all slots, when more
 // than 3 qualify) are re-scored exactly in float64.
 // ---------------------------------------------------------------------------
-constexpr int SCREEN_TOK = 128;
-constexpr int LDS_ROW = 136;  // bf16 per staged row (128 + 8 padding)
+constexpr int SCREEN_TOK = 32;
+
+struct Top4 {
+  float lb[4];
+  int id[4];
+  float ub;
+};
+
+__device__ __forceinline__ void top4_merge(Top4& a, const Top4& b) {
+  float mlb[4];
+  int mid[4];
+  int na = 0, nb = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float ha = pick4(a.lb, na), hb = pick4(b.lb, nb);
+    const int ia = pick4i(a.id, na), ib = pick4i(b.id, nb);
+    const bool takeA = (ha < hb) || (ha == hb && (unsigned)ia <= (unsigned)ib);
+    mlb[i] = takeA ? ha : hb;
+    mid[i] = takeA ? ia : ib;
+    na += takeA ? 1 : 0;
+    nb += takeA ? 0 : 1;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { a.lb[i] = mlb[i]; a.id[i] = mid[i]; }
+  a.ub = fminf(a.ub, b.ub);
+}
 
 template <int FP32>
 __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
-  __shared__ __attribute__((aligned(16))) uint16_t s_hi[2][32 * LDS_ROW];
-  __shared__ __attribute__((aligned(16))) uint16_t s_lo[2][32 * LDS_ROW];
-  __shared__ CacheMeta s_meta[2][32];
+  __shared__ CacheMeta s_meta[4][32];
+  __shared__ Top4 s_top[4][32];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int tile = blockIdx.x % tiles_per_unit;
@@ -251,7 +284,7 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
   const uint8_t* kframe = ws.ring_k + fbase * es;
 
   const int col = lane & 31, half = lane >> 5;
-  const int j = tile * SCREEN_TOK + wave * 32 + col;
+  const int j = tile * SCREEN_TOK + col;
   const bool valid = (j >= nseed) && (j < N);
   const int jc = valid ? j : 0;  // any in-bounds row for lanes without a token
 
@@ -297,128 +330,111 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
   token_xy(valid ? j : 0, dm.grid_w, dm.grid_h, tx, ty);
 
   const float lsp = (float)dm.lambda_sp, lid = (float)dm.lambda_idle;
-  float lb[4] = {INFINITY, INFINITY, INFINITY, INFINITY};
-  int id[4] = {-1, -1, -1, -1};
-  float ubmin = INFINITY;
+  Top4 top;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { top.lb[i] = INFINITY; top.id[i] = -1; }
+  top.ub = INFINITY;
 
   const int ntiles = (kact + 31) / 32;
   const uint16_t* ghi = ws.chat_hi + unit * dm.K * D;
   const uint16_t* glo = ws.chat_lo + unit * dm.K * D;
   const CacheMeta* gmeta = ws.cmeta + unit * dm.K;
 
-  auto stage = [&](int t, int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i;         // 0..1023 chunks of 16 B
-      const int which = c >> 9;            // 0 = hi, 1 = lo
-      const int r = (c & 511) >> 4;        // row 0..31
-      const int c16 = c & 15;              // 16-byte column chunk
-      const int k = t * 32 + r;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (k < kact) val = *reinterpret_cast<const uint4*>((which ? glo : ghi) + (size_t)k * D + c16 * 8);
-      *reinterpret_cast<uint4*>((which ? s_lo[buf] : s_hi[buf]) + r * LDS_ROW + c16 * 8) = val;
-    }
-    if (tid < 32) {
-      const int k = t * 32 + tid;
+  for (int t = wave; t < ntiles; t += 4) {
+    const int krow = t * 32 + col;
+    const bool rok = krow < kact;
+    // per-wave slot metadata through LDS (lanes 0..31 load one slot each)
+    if (half == 0) {
       CacheMeta cm;
-      if (k < kact) cm = gmeta[k];
+      if (rok) cm = gmeta[krow];
       else { cm.mu_x = cm.mu_y = cm.qa = cm.qb = cm.qc = cm.pad = 0.f; cm.last_frame = 0; cm.active = 0; }
-      s_meta[buf][tid] = cm;
+      s_meta[wave][col] = cm;
     }
-  };
-
-  stage(0, 0);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) stage(t + 1, buf ^ 1);
     f32x16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    const uint16_t* rh = s_hi[buf] + col * LDS_ROW + half * 8;
-    const uint16_t* rl = s_lo[buf] + col * LDS_ROW + half * 8;
+    const uint16_t* rh = ghi + (size_t)(rok ? krow : 0) * D + half * 8;
+    const uint16_t* rl = glo + (size_t)(rok ? krow : 0) * D + half * 8;
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
-      const bf16x8 ah = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(rh + kk * 16));
-      const bf16x8 al = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(rl + kk * 16));
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bk[kk], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bk[kk], acc, 0, 0, 0);
-      if (FP32) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bkl[kk], acc, 0, 0, 0);
+      u16x8 vh = *reinterpret_cast<const u16x8*>(rh + kk * 16);
+      u16x8 vl = *reinterpret_cast<const u16x8*>(rl + kk * 16);
+      if (!rok) { vh = (u16x8)0; vl = (u16x8)0; }
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vh), bk[kk], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vl), bk[kk], acc, 0, 0, 0);
+      if (FP32) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vh), bkl[kk], acc, 0, 0, 0);
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (valid) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = (r >> 2) * 8 + half * 4 + (r & 3);
         const int k = t * 32 + m;
         if (k < kact) {
-          const CacheMeta cm = s_meta[buf][m];
+          const CacheMeta cm = s_meta[wave][m];
           const float cosv = acc[r] * invn;
           const float dx = tx - cm.mu_x, dy = ty - cm.mu_y;
-          const float t1 = cm.qa * dx * dx;
+          // q = qa dx^2 + 2 qb dx dy + qc dy^2 (qa, qc > 0), computed in float32;
+          // |q - q_exact| <= 16 u (qa dx^2 + 2|qb dx dy| + qc dy^2) =: eq
+          const float t13 = cm.qa * dx * dx + cm.qc * dy * dy;
           const float t2 = (2.0f * cm.qb) * dx * dy;
-          const float t3 = cm.qc * dy * dy;
-          const float q = t1 + t2 + t3;
-          const float qabs = fabsf(t1) + fabsf(t2) + fabsf(t3);
+          const float q = t13 + t2;
+          const float eq = 16.0f * U32 * (t13 + fabsf(t2)) + 1e-30f;
+          // one reciprocal square root: d = q * rsq(q) and |d - d_exact| <= eq * rsq(max(q, eq))
+          // (|sqrt a - sqrt b| <= |a - b| / sqrt(max(a, b)) and <= sqrt|a - b|)
           const float qp = q > 0.f ? q : 0.f;
-          const float dd = sqrtf(qp);
-          const float eq = 16.0f * U32 * qabs + 1e-30f;
-          float ed = qp > eq ? 1.01f * eq * rsqrtf(qp) : sqrtf(eq);
-          ed += 2.5e-7f * dd;
+          const float rq = rsqrtf(fmaxf(qp, eq));
+          const float dd = qp * rq;
+          const float ed = 1.01f * eq * rq + 2.5e-7f * dd;
           const float idle = (t_frame - cm.last_frame) > dm.t_idle ? 1.f : 0.f;
           const float cost = -cosv + lsp * dd + lid * idle;
           const float e = ECOS + lsp * ed + 4e-7f * (fabsf(cost) + 1.0f);
           const float lo = cost - e, hi = cost + e;
-          ubmin = fminf(ubmin, hi);
-          if (lo < lb[3]) {
-            if (lo < lb[2]) {
-              lb[3] = lb[2]; id[3] = id[2];
-              if (lo < lb[1]) {
-                lb[2] = lb[1]; id[2] = id[1];
-                if (lo < lb[0]) { lb[1] = lb[0]; id[1] = id[0]; lb[0] = lo; id[0] = k; }
-                else { lb[1] = lo; id[1] = k; }
-              } else { lb[2] = lo; id[2] = k; }
-            } else { lb[3] = lo; id[3] = k; }
+          top.ub = fminf(top.ub, hi);
+          if (lo < top.lb[3]) {
+            if (lo < top.lb[2]) {
+              top.lb[3] = top.lb[2]; top.id[3] = top.id[2];
+              if (lo < top.lb[1]) {
+                top.lb[2] = top.lb[1]; top.id[2] = top.id[1];
+                if (lo < top.lb[0]) { top.lb[1] = top.lb[0]; top.id[1] = top.id[0]; top.lb[0] = lo; top.id[0] = k; }
+                else { top.lb[1] = lo; top.id[1] = k; }
+              } else { top.lb[2] = lo; top.id[2] = k; }
+            } else { top.lb[3] = lo; top.id[3] = k; }
           }
         }
       }
     }
-    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 
-  // Merge with the partner lane holding the other 16 rows of each slot tile.
+  // merge with the partner lane (other 16 rows of each slot tile), then across waves
   {
-    float plb[4];
-    int pid[4];
+    Top4 o;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      plb[i] = __shfl_xor(lb[i], 32, 64);
-      pid[i] = __shfl_xor(id[i], 32, 64);
+      o.lb[i] = __shfl_xor(top.lb[i], 32, 64);
+      o.id[i] = __shfl_xor(top.id[i], 32, 64);
     }
-    ubmin = fminf(ubmin, __shfl_xor(ubmin, 32, 64));
-    float mlb[4];
-    int mid[4];
-    int na = 0, nb = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float ha = pick4(lb, na), hb = pick4(plb, nb);
-      const int ia = pick4i(id, na), ib = pick4i(pid, nb);
-      const bool takeA = (ha < hb) || (ha == hb && (unsigned)ia <= (unsigned)ib);
-      mlb[i] = takeA ? ha : hb;
-      mid[i] = takeA ? ia : ib;
-      na += takeA ? 1 : 0;
-      nb += takeA ? 0 : 1;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) { lb[i] = mlb[i]; id[i] = mid[i]; }
+    o.ub = __shfl_xor(top.ub, 32, 64);
+    top4_merge(top, o);
   }
+  if (half == 0) s_top[wave][col] = top;
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+  for (int w = 1; w < 4; ++w) top4_merge(top, s_top[w][col]);
 
-  const float thr = ubmin + 2e-6f;
+  const float thr = top.ub + 2e-6f;
   int nc = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) nc += (lb[i] <= thr) ? 1 : 0;
+  for (int i = 0; i < 4; ++i) nc += (top.lb[i] <= thr) ? 1 : 0;
   const bool mine = valid && half == 0;
-  if (mine && nc <= 1) ws.assign[unit * N + j] = id[0];
+  if (mine && nc <= 1) ws.assign[unit * N + j] = top.id[0];
   const bool flag = mine && nc >= 2;
 
-  // Exact refine of flagged tokens, one token at a time per wave.
+  // Exact refine of flagged tokens, one token at a time.
   unsigned long long fm = __ballot(flag);
   int n_ref = 0, n_full = 0, n_tie = 0;
   while (fm) {
@@ -428,39 +444,64 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
     const int ncc = __shfl(nc, src, 64);
     int cand[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) cand[i] = __shfl(id[i], src, 64);
+    for (int i = 0; i < 4; ++i) cand[i] = __shfl(top.id[i], src, 64);
     const uint8_t* kr = kframe + (size_t)jj * D * es;
     float kxf, kyf;
     token_xy(jj, dm.grid_w, dm.grid_h, kxf, kyf);
-    double kn2 = 0.0;
-    for (int d = 0; d < D; d += 2) {
-      float2 kv = load2<FP32>(kr, d);
-      kn2 = kn2 + (double)kv.x * (double)kv.x;
-      kn2 = kn2 + (double)kv.y * (double)kv.y;
-    }
-    const double knorm = sqrt(kn2);
     double c1 = INFINITY, c2 = INFINITY;
     int k1 = 0x7fffffff;
     if (ncc <= 3) {
-      if (lane < ncc) {
-        const int k = cand[lane == 0 ? 0 : lane == 1 ? 1 : 2];
-        c1 = exact_cost<FP32>(dm, kr, knorm, kxf, kyf, ws.bank + (unit * dm.K + k) * ROW, t_frame);
-        k1 = k;
+      // lanes over dimensions: one float64 dot product and norm per candidate
+      const float2 kv = load2<FP32>(kr, 2 * lane);
+      double kn2 = (double)kv.x * (double)kv.x + (double)kv.y * (double)kv.y;
+      double dots[3], n2s[3];
+#pragma unroll
+      for (int i = 0; i < 3; ++i) {
+        const int k = cand[i] >= 0 ? cand[i] : 0;
+        const float2 sv = reinterpret_cast<const float2*>(ws.bank + (unit * dm.K + k) * ROW + ROW_SUMK)[lane];
+        dots[i] = (double)kv.x * (double)sv.x + (double)kv.y * (double)sv.y;
+        n2s[i] = (double)sv.x * (double)sv.x + (double)sv.y * (double)sv.y;
+      }
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) {
+        kn2 += __shfl_xor(kn2, o, 64);
+#pragma unroll
+        for (int i = 0; i < 3; ++i) {
+          dots[i] += __shfl_xor(dots[i], o, 64);
+          n2s[i] += __shfl_xor(n2s[i], o, 64);
+        }
+      }
+      const double knorm = sqrt(kn2);
+#pragma unroll
+      for (int i = 0; i < 3; ++i) {
+        if (i < ncc) {
+          const int k = cand[i];
+          const double c = cost_from_dot(dm, dots[i], knorm, n2s[i], kxf, kyf,
+                                         ws.bank + (unit * dm.K + k) * ROW, t_frame);
+          if (better(c, k, c1, k1)) { c2 = c1; c1 = c; k1 = k; }
+          else if (c < c2) c2 = c;
+        }
       }
     } else {
+      double kn2 = 0.0;
+      for (int d = 0; d < D; d += 2) {
+        float2 kv = load2<FP32>(kr, d);
+        kn2 = kn2 + (double)kv.x * (double)kv.x;
+        kn2 = kn2 + (double)kv.y * (double)kv.y;
+      }
+      const double knorm = sqrt(kn2);
       for (int k = lane; k < kact; k += 64) {
         double c = exact_cost<FP32>(dm, kr, knorm, kxf, kyf, ws.bank + (unit * dm.K + k) * ROW, t_frame);
         if (better(c, k, c1, k1)) { c2 = c1; c1 = c; k1 = k; }
         else if (c < c2) c2 = c;
       }
-    }
-    // wave reduction of (best, second) with the (cost, slot) order
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      double oc1 = __shfl_xor(c1, o, 64), oc2 = __shfl_xor(c2, o, 64);
-      int ok1 = __shfl_xor(k1, o, 64);
-      if (better(oc1, ok1, c1, k1)) { c2 = fmin(c1, oc2); c1 = oc1; k1 = ok1; }
-      else { c2 = fmin(c2, oc1); }
+      for (int o = 32; o >= 1; o >>= 1) {
+        double oc1 = __shfl_xor(c1, o, 64), oc2 = __shfl_xor(c2, o, 64);
+        int ok1 = __shfl_xor(k1, o, 64);
+        if (better(oc1, ok1, c1, k1)) { c2 = fmin(c1, oc2); c1 = oc1; k1 = ok1; }
+        else { c2 = fmin(c2, oc1); }
+      }
     }
     if (lane == 0) {
       ws.assign[unit * N + jj] = k1;
@@ -474,6 +515,7 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
     if (n_full) atomicAdd(&ws.counters[CNT_REFINED_FULL], (unsigned long long)n_full);
     if (n_tie) atomicAdd(&ws.counters[CNT_NEAR_TIES], (unsigned long long)n_tie);
   }
+  }  // wave 0
 }
 
 hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
@@ -487,55 +529,101 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
 }
 
 // ---------------------------------------------------------------------------
-// Aggregation.  Workgroup = 4 waves over a chunk of AGG_KC slots; each wave
-// owns whole slots, finds their tokens with ballots over the assignment
-// vector (ascending token order) and updates the slot's row in registers:
-// lane l holds components 2l, 2l+1 of the sums and histogram bins 2l, 2l+1
-// (subspace l/8, codewords 2(l%8), 2(l%8)+1).
+// PQ residual encoding of the assigned tokens.  Workgroup = 32 tokens of one
+// unit, one thread per (token, K/V, subspace): residual to the slot's centre
+// before this fold (float32 sum / n), then the nearest codeword,
+// dist(c) = sum_u (r_u - C[c][u])^2 accumulated in float32 with u ascending
+// (16 codewords side by side); ties go to the lower codeword.  Codebooks are
+// staged in LDS with each (K/V, subspace) block padded by 4 floats so the
+// 16 blocks a wave reads at once fall in different banks.
 // ---------------------------------------------------------------------------
-constexpr int AGG_KC = 16;
-
-// Nearest codeword of subspace g = lane/8 for a residual held two components
-// per lane.  dist(c) = sum_u (r_u - C[g][c][u])^2 accumulated in float32
-// with u ascending; ties go to the lower codeword.
-__device__ __forceinline__ int pq_code(float2 r, const float* cb /* [G][CMAX][DP] */, int lane, int C) {
-  const int g = lane >> 3;
-  float rv[16];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    rv[2 * i] = __shfl(r.x, g * 8 + i, 64);
-    rv[2 * i + 1] = __shfl(r.y, g * 8 + i, 64);
-  }
-  const int c0 = 2 * (lane & 7);
-  float best = INFINITY;
-  int bc = CMAX;
-#pragma unroll
-  for (int cc = 0; cc < 2; ++cc) {
-    const int c = c0 + cc;
-    if (c < C) {
-      const float* w = cb + (g * CMAX + c) * DP;
-      float acc = 0.f;
-#pragma unroll
-      for (int uu = 0; uu < DP; ++uu) {
-        float dlt = rv[uu] - w[uu];
-        float sq = dlt * dlt;
-        acc = acc + sq;
-      }
-      if (acc < best) { best = acc; bc = c; }
-    }
-  }
-#pragma unroll
-  for (int o = 1; o <= 4; o <<= 1) {
-    float ob = __shfl_xor(best, o, 64);
-    int oc = __shfl_xor(bc, o, 64);
-    if (ob < best || (ob == best && oc < bc)) { best = ob; bc = oc; }
-  }
-  return bc;
-}
+constexpr int PQ_TOK = 32;
+constexpr int CB_BLOCK = CMAX * DP + 4;
 
 template <int FP32>
+__global__ __launch_bounds__(512) void k_pq_encode(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
+  __shared__ __attribute__((aligned(16))) float s_cb[2 * G * CB_BLOCK];
+  const int tid = threadIdx.x;
+  const int tile = blockIdx.x % tiles_per_unit;
+  const int bu = blockIdx.x / tiles_per_unit;
+  const int b = bu / dm.units, u = bu % dm.units;
+  const int N = dm.T;
+  const int nseed = fb.nseed[b];
+  const int jlo = max(nseed, tile * PQ_TOK), jhi = min(N, tile * PQ_TOK + PQ_TOK);
+  if (jlo >= jhi) return;  // uniform
+  const size_t unit = (size_t)fb.sid[b] * dm.units + u;
+  {
+    const float4* src = reinterpret_cast<const float4*>(ws.codebooks + unit * (2 * G * CMAX * DP));
+    for (int i = tid; i < 2 * G * CMAX * DP / 4; i += 512) {
+      const int blk = i / (CMAX * DP / 4), within = i % (CMAX * DP / 4);
+      *reinterpret_cast<float4*>(s_cb + blk * CB_BLOCK + within * 4) = src[i];
+    }
+  }
+  __syncthreads();
+  const int jj = tile * PQ_TOK + (tid >> 4), kvg = tid & 15, kv = kvg >> 3, g = kvg & 7;
+  if (jj < jlo || jj >= jhi) return;
+  const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
+  const int k = ws.assign[unit * N + jj];
+  const uint8_t* row = ws.bank + (unit * dm.K + k) * ROW;
+  const float nf = (float)reinterpret_cast<const RowMeta*>(row + ROW_META)->n;
+  const float* sums = reinterpret_cast<const float*>(row + (kv ? ROW_SUMV : ROW_SUMK)) + g * DP;
+  const uint8_t* xb = kv ? ws.ring_v : ws.ring_k;
+  float r[DP];
+#pragma unroll
+  for (int q = 0; q < DP; q += 2) {
+    const float2 x = load2<FP32>(xb, fbase + (size_t)jj * D + g * DP + q);
+    const float2 sm = *reinterpret_cast<const float2*>(sums + q);
+    r[q] = x.x - sm.x / nf;
+    r[q + 1] = x.y - sm.y / nf;
+  }
+  const float* cb = s_cb + kvg * CB_BLOCK;   // [c][u]
+  float acc[CMAX];
+#pragma unroll
+  for (int c = 0; c < CMAX; ++c) acc[c] = 0.f;
+#pragma unroll
+  for (int q = 0; q < DP; q += 4) {
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) {
+      const float4 w = *reinterpret_cast<const float4*>(cb + c * DP + q);
+      float d0 = r[q] - w.x;
+      acc[c] = acc[c] + d0 * d0;
+      float d1 = r[q + 1] - w.y;
+      acc[c] = acc[c] + d1 * d1;
+      float d2 = r[q + 2] - w.z;
+      acc[c] = acc[c] + d2 * d2;
+      float d3 = r[q + 3] - w.w;
+      acc[c] = acc[c] + d3 * d3;
+    }
+  }
+  int bc = 0;
+  float best = acc[0];
+#pragma unroll
+  for (int c = 1; c < CMAX; ++c)
+    if (c < dm.C && acc[c] < best) { best = acc[c]; bc = c; }
+  ws.codes[(unit * N + jj) * (2 * G) + kvg] = (uint8_t)bc;
+}
+
+hipError_t launch_pq_encode(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
+  int tpu = (dm.T + PQ_TOK - 1) / PQ_TOK;
+  dim3 grid(fb.n * dm.units * tpu);
+  if (dm.kv_fp32)
+    hipLaunchKernelGGL(k_pq_encode<1>, grid, dim3(512), 0, st, dm, ws, fb, tpu);
+  else
+    hipLaunchKernelGGL(k_pq_encode<0>, grid, dim3(512), 0, st, dm, ws, fb, tpu);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Aggregation.  One wave per slot; the four waves of a workgroup are
+// independent (no LDS, no barriers).  A wave finds its slot's tokens with
+// ballots over the assignment vector and, if any, updates the slot's row in
+// registers with the tokens in eviction order: lane l holds components
+// 2l, 2l+1 of the four sums and histogram bins 2l, 2l+1 (subspace l/8,
+// codewords 2(l%8), 2(l%8)+1).  Then it writes the row back and refreshes the
+// slot's screening copy.
+// ---------------------------------------------------------------------------
+template <int FP32>
 __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int chunks_per_unit) {
-  __shared__ float s_cb[2 * G * CMAX * DP];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int chunk = blockIdx.x % chunks_per_unit;
   const int bu = blockIdx.x / chunks_per_unit;
@@ -543,106 +631,87 @@ __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBa
   const int N = dm.T;
   const int nseed = fb.nseed[b];
   const int kact = fb.nact[b] + nseed;
-  const int k0 = chunk * AGG_KC;
-  if (nseed >= N || k0 >= kact) return;  // uniform
+  const int k = chunk * 4 + wave;
+  if (nseed >= N || k >= kact) return;  // uniform per wave
   const size_t unit = (size_t)fb.sid[b] * dm.units + u;
   const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
-  if (pq) {
-    const float4* src = reinterpret_cast<const float4*>(ws.codebooks + unit * (2 * G * CMAX * DP));
-    for (int i = tid; i < 2 * G * CMAX * DP / 4; i += 256) reinterpret_cast<float4*>(s_cb)[i] = src[i];
-  }
-  __syncthreads();
-
   const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
-  const size_t es = FP32 ? 4 : 2;
-  (void)es;
-  // assignment of the non-seed tokens, 64 per register
-  int areg[TMAX / 64];
+
+  unsigned long long masks[TMAX / 64];
+  bool any = false;
 #pragma unroll
   for (int c = 0; c < TMAX / 64; ++c) {
-    const int jj = c * 64 + lane;
-    areg[c] = (jj < N && jj >= nseed) ? ws.assign[unit * N + jj] : -1;
-  }
-  const float eta = dm.eta, keep = 1.0f - dm.eta;
-  int touched = 0;
-  for (int i = 0; i < AGG_KC / 4; ++i) {
-    const int k = k0 + wave * (AGG_KC / 4) + i;
-    if (k >= kact) break;
-    unsigned long long masks[TMAX / 64];
-    bool any = false;
-#pragma unroll
-    for (int c = 0; c < TMAX / 64; ++c) {
-      masks[c] = (c * 64 < N) ? __ballot(areg[c] == k) : 0ull;
+    masks[c] = 0ull;
+    if (c * 64 < N) {
+      const int jj = c * 64 + lane;
+      const int a = (jj < N && jj >= nseed) ? ws.assign[unit * N + jj] : -1;
+      masks[c] = __ballot(a == k);
       any |= masks[c] != 0ull;
     }
-    if (!any) continue;
-    ++touched;
-    const size_t si = unit * dm.K + k;
-    uint8_t* row = ws.bank + si * ROW;
-    float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
-    float2 sv = reinterpret_cast<const float2*>(row + ROW_SUMV)[lane];
-    float2 qk = reinterpret_cast<const float2*>(row + ROW_SQK)[lane];
-    float2 qv = reinterpret_cast<const float2*>(row + ROW_SQV)[lane];
-    uint2 hk = reinterpret_cast<const uint2*>(row + ROW_HK)[lane];
-    uint2 hv = reinterpret_cast<const uint2*>(row + ROW_HV)[lane];
-    RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
-    // snapshot centres for the residuals
-    const float nf = (float)m.n;
-    const float2 cs = make_float2(sk.x / nf, sk.y / nf);
-    const float2 ps = make_float2(sv.x / nf, sv.y / nf);
-#pragma unroll
-    for (int c = 0; c < TMAX / 64; ++c) {
-      unsigned long long mk = masks[c];
-      while (mk) {
-        const int bit = __ffsll((long long)mk) - 1;
-        mk &= mk - 1;
-        const int jj = c * 64 + bit;
-        const float2 kk = load2<FP32>(ws.ring_k, fbase + (size_t)jj * D + 2 * lane);
-        const float2 vv = load2<FP32>(ws.ring_v, fbase + (size_t)jj * D + 2 * lane);
-        sk.x = sk.x + kk.x; sk.y = sk.y + kk.y;
-        sv.x = sv.x + vv.x; sv.y = sv.y + vv.y;
-        qk.x = qk.x + kk.x * kk.x; qk.y = qk.y + kk.y * kk.y;
-        qv.x = qv.x + vv.x * vv.x; qv.y = qv.y + vv.y * vv.y;
-        if (pq) {
-          const float2 rk = make_float2(kk.x - cs.x, kk.y - cs.y);
-          const float2 rv = make_float2(vv.x - ps.x, vv.y - ps.y);
-          const int zk = pq_code(rk, s_cb, lane, dm.C);
-          const int zv = pq_code(rv, s_cb + G * CMAX * DP, lane, dm.C);
-          const int c0 = 2 * (lane & 7);
-          hk.x += (zk == c0) ? 1u : 0u;
-          hk.y += (zk == c0 + 1) ? 1u : 0u;
-          hv.x += (zv == c0) ? 1u : 0u;
-          hv.y += (zv == c0 + 1) ? 1u : 0u;
-          m.n_res += 1;
-        }
-        float sx, sy;
-        token_xy(jj, dm.grid_w, dm.grid_h, sx, sy);
-        const float mx = keep * m.mu_x + eta * sx;
-        const float my = keep * m.mu_y + eta * sy;
-        m.mu_x = mx;
-        m.mu_y = my;
-        const float ddx = sx - mx, ddy = sy - my;
-        m.sxx = keep * m.sxx + eta * (ddx * ddx);
-        m.sxy = keep * m.sxy + eta * (ddx * ddy);
-        m.syy = keep * m.syy + eta * (ddy * ddy);
-        m.tau = fb.fe[b] * N + jj;
-        m.n += 1;
-      }
-    }
-    reinterpret_cast<float2*>(row + ROW_SUMK)[lane] = sk;
-    reinterpret_cast<float2*>(row + ROW_SUMV)[lane] = sv;
-    reinterpret_cast<float2*>(row + ROW_SQK)[lane] = qk;
-    reinterpret_cast<float2*>(row + ROW_SQV)[lane] = qv;
-    reinterpret_cast<uint2*>(row + ROW_HK)[lane] = hk;
-    reinterpret_cast<uint2*>(row + ROW_HV)[lane] = hv;
-    if (lane == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
-    refresh_cache(dm, sk, m, si, ws, lane);
   }
-  if (lane == 0 && touched) atomicAdd(&ws.counters[CNT_TOUCHED], (unsigned long long)touched);
+  if (!any) return;  // untouched slot
+
+  const size_t si = unit * dm.K + k;
+  uint8_t* row = ws.bank + si * ROW;
+  float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
+  float2 sv = reinterpret_cast<const float2*>(row + ROW_SUMV)[lane];
+  float2 qk = reinterpret_cast<const float2*>(row + ROW_SQK)[lane];
+  float2 qv = reinterpret_cast<const float2*>(row + ROW_SQV)[lane];
+  uint2 hk = reinterpret_cast<const uint2*>(row + ROW_HK)[lane];
+  uint2 hv = reinterpret_cast<const uint2*>(row + ROW_HV)[lane];
+  RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  const float eta = dm.eta, keep = 1.0f - dm.eta;
+  const int gl = lane >> 3, c0 = 2 * (lane & 7);
+#pragma unroll
+  for (int c = 0; c < TMAX / 64; ++c) {
+    unsigned long long mk = masks[c];
+    while (mk) {
+      const int bit = __ffsll((long long)mk) - 1;
+      mk &= mk - 1;
+      const int jj = c * 64 + bit;
+      const float2 kk = load2<FP32>(ws.ring_k, fbase + (size_t)jj * D + 2 * lane);
+      const float2 vv = load2<FP32>(ws.ring_v, fbase + (size_t)jj * D + 2 * lane);
+      sk.x = sk.x + kk.x; sk.y = sk.y + kk.y;
+      sv.x = sv.x + vv.x; sv.y = sv.y + vv.y;
+      qk.x = qk.x + kk.x * kk.x; qk.y = qk.y + kk.y * kk.y;
+      qv.x = qv.x + vv.x * vv.x; qv.y = qv.y + vv.y * vv.y;
+      if (pq) {
+        const uint8_t* cz = ws.codes + (unit * N + jj) * (2 * G);
+        const int zk = cz[gl], zv = cz[G + gl];
+        hk.x += (zk == c0) ? 1u : 0u;
+        hk.y += (zk == c0 + 1) ? 1u : 0u;
+        hv.x += (zv == c0) ? 1u : 0u;
+        hv.y += (zv == c0 + 1) ? 1u : 0u;
+        m.n_res += 1;
+      }
+      float sx, sy;
+      token_xy(jj, dm.grid_w, dm.grid_h, sx, sy);
+      const float mx = keep * m.mu_x + eta * sx;
+      const float my = keep * m.mu_y + eta * sy;
+      m.mu_x = mx;
+      m.mu_y = my;
+      const float ddx = sx - mx, ddy = sy - my;
+      m.sxx = keep * m.sxx + eta * (ddx * ddx);
+      m.sxy = keep * m.sxy + eta * (ddx * ddy);
+      m.syy = keep * m.syy + eta * (ddy * ddy);
+      m.tau = fb.fe[b] * N + jj;
+      m.n += 1;
+    }
+  }
+  reinterpret_cast<float2*>(row + ROW_SUMK)[lane] = sk;
+  reinterpret_cast<float2*>(row + ROW_SUMV)[lane] = sv;
+  reinterpret_cast<float2*>(row + ROW_SQK)[lane] = qk;
+  reinterpret_cast<float2*>(row + ROW_SQV)[lane] = qv;
+  reinterpret_cast<uint2*>(row + ROW_HK)[lane] = hk;
+  reinterpret_cast<uint2*>(row + ROW_HV)[lane] = hv;
+  if (lane == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
+  refresh_cache(dm, sk, m, si, ws, lane);
+  // per-slot count of folds that touched it (owned by this wave: no atomics)
+  if (lane == 0) ws.touched[si] += 1u;
 }
 
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
-  int cpu = (dm.K + AGG_KC - 1) / AGG_KC;
+  int cpu = (dm.K + 3) / 4;
   dim3 grid(fb.n * dm.units * cpu);
   if (dm.kv_fp32)
     hipLaunchKernelGGL(k_aggregate<1>, grid, dim3(256), 0, st, dm, ws, fb, cpu);

@@ -61,6 +61,7 @@ struct Workspace {
   uint16_t* chat_lo;
   CacheMeta* cmeta;           // [streams][units][K]
   int32_t* assign;            // [streams][units][T]
+  uint8_t* codes;             // [streams][units][T][2][G]: PQ codes of the last fold's tokens
   float* codebooks;           // [streams][units][2][G][CMAX][DP]
   uint8_t* pk;                // [units][K*S][D] kv dtype (synthesis of one stream)
   uint8_t* pv;
@@ -68,6 +69,7 @@ struct Workspace {
   float* part_o;              // [units][max_splits][max_rows][D]
   float* part_ml;             // [units][max_splits][max_rows][2]  (max, sum)
   unsigned long long* counters;  // [16]
+  uint32_t* touched;             // [streams][units][K]: folds in which the slot absorbed >= 1 token
 };
 
 enum Counter {
@@ -115,6 +117,8 @@ hipError_t launch_seed(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                        hipStream_t st);
 hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                          hipStream_t st);
+hipError_t launch_pq_encode(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
+                            hipStream_t st);
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                             hipStream_t st);
 hipError_t launch_synthesize(const Dims& dm, const Workspace& ws, int sid, int n_active,

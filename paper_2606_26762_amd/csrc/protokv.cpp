@@ -27,8 +27,8 @@ struct StreamState {
 };
 
 struct Layout {
-  size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codebooks;
-  size_t pk, pv, pbias, part_o, part_ml, counters, total;
+  size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codes, codebooks;
+  size_t pk, pv, pbias, part_o, part_ml, counters, touched, total;
 };
 
 thread_local std::string g_init_err;
@@ -57,6 +57,7 @@ Layout make_layout(const protokv_config& c) {
   ly.chat_lo = take(U * K * D * 2);
   ly.cmeta = take(U * K * sizeof(CacheMeta));
   ly.assign = take(U * T * 4);
+  ly.codes = take(U * T * 2 * G);
   ly.codebooks = take(U * 2 * G * CMAX * DP * 4);
   ly.pk = take(units * K * S * D * es);
   ly.pv = take(units * K * S * D * es);
@@ -64,6 +65,7 @@ Layout make_layout(const protokv_config& c) {
   ly.part_o = take(units * MAX_SPLITS * rows * D * 4);
   ly.part_ml = take(units * MAX_SPLITS * rows * 2 * 4);
   ly.counters = take(CNT_COUNT * 8);
+  ly.touched = take(U * K * 4);
   ly.total = off;
   return ly;
 }
@@ -252,6 +254,7 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.chat_lo = (uint16_t*)(b + ly.chat_lo);
   ws.cmeta = (CacheMeta*)(b + ly.cmeta);
   ws.assign = (int32_t*)(b + ly.assign);
+  ws.codes = b + ly.codes;
   ws.codebooks = (float*)(b + ly.codebooks);
   ws.pk = b + ly.pk;
   ws.pv = b + ly.pv;
@@ -259,6 +262,7 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.part_o = (float*)(b + ly.part_o);
   ws.part_ml = (float*)(b + ly.part_ml);
   ws.counters = (unsigned long long*)(b + ly.counters);
+  ws.touched = (uint32_t*)(b + ly.touched);
   h->st.assign(c->num_streams, StreamState());
 
   // codebooks -> [U][2][G][CMAX][DP] with the codeword axis padded to 16
@@ -364,6 +368,9 @@ protokv_status protokv_fold(protokv_t h, void* stream) {
     if (st == PROTOKV_OK && any_assign)
       st = h->dev(h->launch(PROTOKV_K_SCREEN, hs, [&] { return launch_screen(h->dm, h->ws, fb, hs); }),
                   "fold/screen");
+    if (st == PROTOKV_OK && any_assign && (h->dm.flags & PROTOKV_FLAG_PQ))
+      st = h->dev(h->launch(PROTOKV_K_PQ_ENCODE, hs, [&] { return launch_pq_encode(h->dm, h->ws, fb, hs); }),
+                  "fold/pq_encode");
     if (st == PROTOKV_OK && any_assign)
       st = h->dev(h->launch(PROTOKV_K_AGGREGATE, hs, [&] { return launch_aggregate(h->dm, h->ws, fb, hs); }),
                   "fold/aggregate");
@@ -452,15 +459,20 @@ protokv_status protokv_get_counters(protokv_t h, protokv_counters* out, void* st
   unsigned long long dc[CNT_COUNT];
   hipStream_t hs = (hipStream_t)stream;
   hipError_t e = hipMemcpyAsync(dc, h->ws.counters, sizeof(dc), hipMemcpyDeviceToHost, hs);
+  const size_t nt = (size_t)h->cfg.num_streams * h->dm.units * h->dm.K;
+  std::vector<uint32_t> tv(nt);
+  if (e == hipSuccess) e = hipMemcpyAsync(tv.data(), h->ws.touched, nt * 4, hipMemcpyDeviceToHost, hs);
   if (e == hipSuccess) e = hipStreamSynchronize(hs);
   if (e != hipSuccess) return h->dev(e, "get_counters");
+  uint64_t touched = 0;
+  for (uint32_t x : tv) touched += x;
   out->folds = h->folds;
   out->tokens_assigned = h->assigned;
   out->tokens_seeded = h->seeded;
   out->refined = dc[CNT_REFINED];
   out->refined_full = dc[CNT_REFINED_FULL];
   out->near_ties = dc[CNT_NEAR_TIES];
-  out->touched = dc[CNT_TOUCHED];
+  out->touched = touched;
   return PROTOKV_OK;
 }
 

@@ -29,7 +29,7 @@ EXPORTED = [
     "protokv_read_pseudo", "protokv_profile", "protokv_profile_read", "protokv_last_error",
 ]
 
-KERNELS = ["ring_insert", "seed", "screen", "aggregate", "synthesize", "attend", "attend_merge"]
+KERNELS = ["ring_insert", "seed", "screen", "aggregate", "synthesize", "attend", "attend_merge", "pq_encode"]
 
 
 class ProtoKVError(RuntimeError):
