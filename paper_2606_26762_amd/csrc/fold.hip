@@ -231,43 +231,69 @@ __device__ __forceinline__ bool better(double c1, int k1, double c2, int k2) {
 // its 4 waves split the active slots (slot tiles t = wave, wave + 4, ...)
 // and score them against the 32 tokens with v_mfma_f32_32x32x16_bf16
 // (slots = rows, tokens = columns, unit centres as a hi + lo bf16 split read
-// straight from global memory).  Per token each lane keeps the 4 smallest
-// lower bounds and the smallest upper bound of the cost; the waves' lists are
-// merged through LDS.  A token whose bound interval admits a single slot is
-// assigned directly; otherwise the candidate slots (or all slots, when more
-// than 3 qualify) are re-scored exactly in float64.
+// straight from global memory).  Each lane keeps, for its token, the three
+// smallest lower bounds of the cost (slot ids of the first two) and the
+// smallest upper bound; the lists are merged across the partner lane and the
+// waves.  A token whose bound interval admits a single slot is assigned
+// directly; two candidates are re-scored exactly in float64; three or more
+// send the token to an exact float64 pass over every slot.
 // ---------------------------------------------------------------------------
-constexpr int SCREEN_TOK = 32;
+constexpr int SCREEN_TOK = 64;
 
-struct Top4 {
-  float lb[4];
-  int id[4];
+struct Top3 {
+  float lb1, lb2, lb3;
+  int id1, id2;
   float ub;
 };
 
-__device__ __forceinline__ void top4_merge(Top4& a, const Top4& b) {
-  float mlb[4];
-  int mid[4];
-  int na = 0, nb = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float ha = pick4(a.lb, na), hb = pick4(b.lb, nb);
-    const int ia = pick4i(a.id, na), ib = pick4i(b.id, nb);
-    const bool takeA = (ha < hb) || (ha == hb && (unsigned)ia <= (unsigned)ib);
-    mlb[i] = takeA ? ha : hb;
-    mid[i] = takeA ? ia : ib;
-    na += takeA ? 1 : 0;
-    nb += takeA ? 0 : 1;
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { a.lb[i] = mlb[i]; a.id[i] = mid[i]; }
+__device__ __forceinline__ void top3_push(Top3& a, float lo, int k) {
+  const bool c1 = lo < a.lb1, c2 = lo < a.lb2, c3 = lo < a.lb3;
+  a.lb3 = c2 ? a.lb2 : (c3 ? lo : a.lb3);
+  a.lb2 = c1 ? a.lb1 : (c2 ? lo : a.lb2);
+  a.id2 = c1 ? a.id1 : (c2 ? k : a.id2);
+  a.lb1 = c1 ? lo : a.lb1;
+  a.id1 = c1 ? k : a.id1;
+}
+
+__device__ __forceinline__ void top3_merge(Top3& a, const Top3& b) {
+  top3_push(a, b.lb1, b.id1);
+  top3_push(a, b.lb2, b.id2);
+  a.lb3 = fminf(a.lb3, fmaxf(b.lb3, a.lb2));  // b.lb3 can only be a third smallest
   a.ub = fminf(a.ub, b.ub);
+}
+
+// Scores one slot row against one token column and folds it into the token's
+// running bounds.  The float32 arithmetic only approximates the cost; E0 and
+// the spatial error term bound the distance to the exact value.
+__device__ __forceinline__ void screen_pair(float dot, float invn, float tx, float ty, const float4& a,
+                                            const float2& c, int k, bool kok, float lsp, float lsp101,
+                                            float lsp65, float E0, Top3& top) {
+  const float dx = tx - a.x, dy = ty - a.y;
+  // q = qa dx^2 + 2 qb dx dy + qc dy^2 (qa, qc > 0);
+  // |q - q_exact| <= 16 u (qa dx^2 + |2 qb dx dy| + qc dy^2) =: eq
+  const float t13 = fmaf(a.z * dx, dx, (c.x * dy) * dy);
+  const float t2 = (a.w * dx) * dy;
+  const float q = t13 + t2;
+  const float eq = fmaf(16.0f * U32, t13 + fabsf(t2), 1e-30f);
+  // d = q rsq(max(q, eq)), |d - d_exact| <= eq rsq(max(q, eq)) + 2.5e-7 d
+  // (|sqrt a - sqrt b| <= |a - b| / sqrt(max(a, b)) and <= sqrt|a - b|; raw
+  // v_rsq_f32 is accurate to ~1 ulp for the normal arguments >= 1e-30 used here)
+  const float qp = fmaxf(q, 0.f);
+  const float rq = __builtin_amdgcn_rsqf(fmaxf(qp, eq));
+  const float dd = qp * rq;
+  const float cost = fmaf(lsp, dd, fmaf(-dot, invn, c.y));
+  const float e = fmaf(lsp65, dd, fmaf(lsp101, eq * rq, E0));
+  const float lo = kok ? cost - e : INFINITY;
+  const float hi = kok ? cost + e : INFINITY;
+  top.ub = fminf(top.ub, hi);
+  top3_push(top, lo, k);
 }
 
 template <int FP32>
 __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
-  __shared__ CacheMeta s_meta[4][32];
-  __shared__ Top4 s_top[4][32];
+  __shared__ float4 s_ma[4][32];   // mu_x, mu_y, qa, 2 qb
+  __shared__ float2 s_mb[4][32];   // qc, lambda_idle * idle
+  __shared__ Top3 s_top[4][SCREEN_TOK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int tile = blockIdx.x % tiles_per_unit;
@@ -284,16 +310,20 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
   const uint8_t* kframe = ws.ring_k + fbase * es;
 
   const int col = lane & 31, half = lane >> 5;
-  const int j = tile * SCREEN_TOK + col;
-  const bool valid = (j >= nseed) && (j < N);
-  const int jc = valid ? j : 0;  // any in-bounds row for lanes without a token
-
-  // B operand: K^T (dims x tokens).  Lane holds dims kk*16 + half*8 + 0..7 of token col.
-  bf16x8 bk[8];
-  bf16x8 bkl[8];
-  float nsq = 0.f;
-  {
-    const uint8_t* kr = kframe + (size_t)jc * D * es;
+  // two token columns per lane: tokens tile*64 + col and tile*64 + 32 + col
+  int jt[2];
+  bool vt[2];
+  float invn[2], tx[2], ty[2];
+  bf16x8 bk[2][8];
+  bf16x8 bkl[2][8];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int j = tile * SCREEN_TOK + h * 32 + col;
+    const bool valid = (j >= nseed) && (j < N);
+    jt[h] = j;
+    vt[h] = valid;
+    const uint8_t* kr = kframe + (size_t)(valid ? j : 0) * D * es;
+    float nsq = 0.f;
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
       const int d0 = kk * 16 + half * 8;
@@ -301,39 +331,46 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
         const float4 a0 = *reinterpret_cast<const float4*>(kr + (size_t)d0 * 4);
         const float4 a1 = *reinterpret_cast<const float4*>(kr + (size_t)(d0 + 4) * 4);
         float f[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-        u16x8 h, l;
+        u16x8 hh, ll;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           float x = valid ? f[i] : 0.f;
           nsq += x * x;
           uint16_t hb = to_bf16(x);
-          h[i] = hb;
-          l[i] = to_bf16(x - from_bf16(hb));
+          hh[i] = hb;
+          ll[i] = to_bf16(x - from_bf16(hb));
         }
-        bk[kk] = __builtin_bit_cast(bf16x8, h);
-        bkl[kk] = __builtin_bit_cast(bf16x8, l);
+        bk[h][kk] = __builtin_bit_cast(bf16x8, hh);
+        bkl[h][kk] = __builtin_bit_cast(bf16x8, ll);
       } else {
-        u16x8 h = *reinterpret_cast<const u16x8*>(kr + (size_t)d0 * 2);
-        if (!valid) h = (u16x8)0;
+        u16x8 hh = *reinterpret_cast<const u16x8*>(kr + (size_t)d0 * 2);
+        if (!valid) hh = (u16x8)0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          float x = from_bf16(h[i]);
+          float x = from_bf16(hh[i]);
           nsq += x * x;
         }
-        bk[kk] = __builtin_bit_cast(bf16x8, h);
+        bk[h][kk] = __builtin_bit_cast(bf16x8, hh);
       }
     }
+    nsq += __shfl_xor(nsq, 32, 64);
+    invn[h] = nsq > 0.f ? 1.0f / sqrtf(nsq) : 0.f;
+    token_xy(valid ? j : 0, dm.grid_w, dm.grid_h, tx[h], ty[h]);
   }
-  nsq += __shfl_xor(nsq, 32, 64);
-  const float invn = nsq > 0.f ? 1.0f / sqrtf(nsq) : 0.f;
-  float tx, ty;
-  token_xy(valid ? j : 0, dm.grid_w, dm.grid_h, tx, ty);
 
-  const float lsp = (float)dm.lambda_sp, lid = (float)dm.lambda_idle;
-  Top4 top;
+  const float lsp = (float)dm.lambda_sp;
+  const float lidle = (float)dm.lambda_idle;
+  // |cost - cost_exact| <= E0 + lsp (1.01 eq rq + 6.5e-7 d): ECOS for the dot product,
+  // 4e-7 (|cost| + 1) for rounding the assembly, |cost| <= 1 + lsp d + lambda_idle.
+  const float E0 = ECOS + 4e-7f * (2.0f + lidle);
+  const float lsp101 = 1.01f * lsp, lsp65 = 6.5e-7f * lsp;
+  Top3 top[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) { top.lb[i] = INFINITY; top.id[i] = -1; }
-  top.ub = INFINITY;
+  for (int h = 0; h < 2; ++h) {
+    top[h].lb1 = top[h].lb2 = top[h].lb3 = INFINITY;
+    top[h].id1 = top[h].id2 = -1;
+    top[h].ub = INFINITY;
+  }
 
   const int ntiles = (kact + 31) / 32;
   const uint16_t* ghi = ws.chat_hi + unit * dm.K * D;
@@ -343,14 +380,19 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
   for (int t = wave; t < ntiles; t += 4) {
     const int krow = t * 32 + col;
     const bool rok = krow < kact;
-    // per-wave slot metadata through LDS (lanes 0..31 load one slot each)
     if (half == 0) {
-      CacheMeta cm;
-      if (rok) cm = gmeta[krow];
-      else { cm.mu_x = cm.mu_y = cm.qa = cm.qb = cm.qc = cm.pad = 0.f; cm.last_frame = 0; cm.active = 0; }
-      s_meta[wave][col] = cm;
+      float4 ma = make_float4(0.f, 0.f, 0.f, 0.f);
+      float2 mb = make_float2(0.f, 0.f);
+      if (rok) {
+        const CacheMeta cm = gmeta[krow];
+        ma = make_float4(cm.mu_x, cm.mu_y, cm.qa, 2.0f * cm.qb);
+        mb = make_float2(cm.qc, (t_frame - cm.last_frame) > dm.t_idle ? lidle : 0.f);
+      }
+      s_ma[wave][col] = ma;
+      s_mb[wave][col] = mb;
     }
-    f32x16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    f32x16 acc0 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    f32x16 acc1 = acc0;
     const uint16_t* rh = ghi + (size_t)(rok ? krow : 0) * D + half * 8;
     const uint16_t* rl = glo + (size_t)(rok ? krow : 0) * D + half * 8;
 #pragma unroll
@@ -358,51 +400,28 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
       u16x8 vh = *reinterpret_cast<const u16x8*>(rh + kk * 16);
       u16x8 vl = *reinterpret_cast<const u16x8*>(rl + kk * 16);
       if (!rok) { vh = (u16x8)0; vl = (u16x8)0; }
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vh), bk[kk], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vl), bk[kk], acc, 0, 0, 0);
-      if (FP32) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vh), bkl[kk], acc, 0, 0, 0);
+      const bf16x8 ah = __builtin_bit_cast(bf16x8, vh), al = __builtin_bit_cast(bf16x8, vl);
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bk[0][kk], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bk[1][kk], acc1, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bk[0][kk], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bk[1][kk], acc1, 0, 0, 0);
+      if (FP32) {
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bkl[0][kk], acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bkl[1][kk], acc1, 0, 0, 0);
+      }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    if (valid) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = (r >> 2) * 8 + half * 4 + (r & 3);
-        const int k = t * 32 + m;
-        if (k < kact) {
-          const CacheMeta cm = s_meta[wave][m];
-          const float cosv = acc[r] * invn;
-          const float dx = tx - cm.mu_x, dy = ty - cm.mu_y;
-          // q = qa dx^2 + 2 qb dx dy + qc dy^2 (qa, qc > 0), computed in float32;
-          // |q - q_exact| <= 16 u (qa dx^2 + 2|qb dx dy| + qc dy^2) =: eq
-          const float t13 = cm.qa * dx * dx + cm.qc * dy * dy;
-          const float t2 = (2.0f * cm.qb) * dx * dy;
-          const float q = t13 + t2;
-          const float eq = 16.0f * U32 * (t13 + fabsf(t2)) + 1e-30f;
-          // one reciprocal square root: d = q * rsq(q) and |d - d_exact| <= eq * rsq(max(q, eq))
-          // (|sqrt a - sqrt b| <= |a - b| / sqrt(max(a, b)) and <= sqrt|a - b|)
-          const float qp = q > 0.f ? q : 0.f;
-          const float rq = rsqrtf(fmaxf(qp, eq));
-          const float dd = qp * rq;
-          const float ed = 1.01f * eq * rq + 2.5e-7f * dd;
-          const float idle = (t_frame - cm.last_frame) > dm.t_idle ? 1.f : 0.f;
-          const float cost = -cosv + lsp * dd + lid * idle;
-          const float e = ECOS + lsp * ed + 4e-7f * (fabsf(cost) + 1.0f);
-          const float lo = cost - e, hi = cost + e;
-          top.ub = fminf(top.ub, hi);
-          if (lo < top.lb[3]) {
-            if (lo < top.lb[2]) {
-              top.lb[3] = top.lb[2]; top.id[3] = top.id[2];
-              if (lo < top.lb[1]) {
-                top.lb[2] = top.lb[1]; top.id[2] = top.id[1];
-                if (lo < top.lb[0]) { top.lb[1] = top.lb[0]; top.id[1] = top.id[0]; top.lb[0] = lo; top.id[0] = k; }
-                else { top.lb[1] = lo; top.id[1] = k; }
-              } else { top.lb[2] = lo; top.id[2] = k; }
-            } else { top.lb[3] = lo; top.id[3] = k; }
-          }
-        }
-      }
+#pragma unroll 4
+    for (int r = 0; r < 16; ++r) {
+      const int m = (r >> 2) * 8 + half * 4 + (r & 3);
+      const float4 a = s_ma[wave][m];
+      const float2 c = s_mb[wave][m];
+      const int k = t * 32 + m;
+      const bool kok = k < kact;
+      screen_pair(acc0[r], invn[0], tx[0], ty[0], a, c, k, kok, lsp, lsp101, lsp65, E0, top[0]);
+      screen_pair(acc1[r], invn[1], tx[1], ty[1], a, c, k, kok, lsp, lsp101, lsp65, E0, top[1]);
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -410,28 +429,32 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
   }
 
   // merge with the partner lane (other 16 rows of each slot tile), then across waves
-  {
-    Top4 o;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      o.lb[i] = __shfl_xor(top.lb[i], 32, 64);
-      o.id[i] = __shfl_xor(top.id[i], 32, 64);
-    }
-    o.ub = __shfl_xor(top.ub, 32, 64);
-    top4_merge(top, o);
+  for (int h = 0; h < 2; ++h) {
+    Top3 o;
+    o.lb1 = __shfl_xor(top[h].lb1, 32, 64);
+    o.lb2 = __shfl_xor(top[h].lb2, 32, 64);
+    o.lb3 = __shfl_xor(top[h].lb3, 32, 64);
+    o.id1 = __shfl_xor(top[h].id1, 32, 64);
+    o.id2 = __shfl_xor(top[h].id2, 32, 64);
+    o.ub = __shfl_xor(top[h].ub, 32, 64);
+    top3_merge(top[h], o);
+    if (half == 0) s_top[wave][h * 32 + col] = top[h];
   }
-  if (half == 0) s_top[wave][col] = top;
   __syncthreads();
-  if (wave == 0) {
+  // waves 0 and 1 decide for token columns 0..31 and 32..63
+  if (wave >= 2) return;
+  const int hsel = wave;
+  Top3 tp = s_top[0][hsel * 32 + col];
 #pragma unroll
-  for (int w = 1; w < 4; ++w) top4_merge(top, s_top[w][col]);
+  for (int w = 1; w < 4; ++w) top3_merge(tp, s_top[w][hsel * 32 + col]);
+  const int j = hsel ? jt[1] : jt[0];
+  const bool valid = hsel ? vt[1] : vt[0];
 
-  const float thr = top.ub + 2e-6f;
-  int nc = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) nc += (top.lb[i] <= thr) ? 1 : 0;
+  const float thr = tp.ub + 2e-6f;
+  const int nc = (tp.lb1 <= thr) + (tp.lb2 <= thr) + (tp.lb3 <= thr);
   const bool mine = valid && half == 0;
-  if (mine && nc <= 1) ws.assign[unit * N + j] = top.id[0];
+  if (mine && nc <= 1) ws.assign[unit * N + j] = tp.id1;
   const bool flag = mine && nc >= 2;
 
   // Exact refine of flagged tokens, one token at a time.
@@ -442,46 +465,35 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
     fm &= fm - 1;
     const int jj = __shfl(j, src, 64);
     const int ncc = __shfl(nc, src, 64);
-    int cand[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) cand[i] = __shfl(top.id[i], src, 64);
+    const int cand0 = __shfl(tp.id1, src, 64), cand1 = __shfl(tp.id2, src, 64);
     const uint8_t* kr = kframe + (size_t)jj * D * es;
     float kxf, kyf;
     token_xy(jj, dm.grid_w, dm.grid_h, kxf, kyf);
     double c1 = INFINITY, c2 = INFINITY;
     int k1 = 0x7fffffff;
-    if (ncc <= 3) {
-      // lanes over dimensions: one float64 dot product and norm per candidate
+    if (ncc == 2) {
+      // lanes over dimensions: float64 dot products and norms of the two candidates
       const float2 kv = load2<FP32>(kr, 2 * lane);
+      const float2 s0 = reinterpret_cast<const float2*>(ws.bank + (unit * dm.K + cand0) * ROW + ROW_SUMK)[lane];
+      const float2 s1 = reinterpret_cast<const float2*>(ws.bank + (unit * dm.K + cand1) * ROW + ROW_SUMK)[lane];
       double kn2 = (double)kv.x * (double)kv.x + (double)kv.y * (double)kv.y;
-      double dots[3], n2s[3];
-#pragma unroll
-      for (int i = 0; i < 3; ++i) {
-        const int k = cand[i] >= 0 ? cand[i] : 0;
-        const float2 sv = reinterpret_cast<const float2*>(ws.bank + (unit * dm.K + k) * ROW + ROW_SUMK)[lane];
-        dots[i] = (double)kv.x * (double)sv.x + (double)kv.y * (double)sv.y;
-        n2s[i] = (double)sv.x * (double)sv.x + (double)sv.y * (double)sv.y;
-      }
+      double d0 = (double)kv.x * (double)s0.x + (double)kv.y * (double)s0.y;
+      double d1 = (double)kv.x * (double)s1.x + (double)kv.y * (double)s1.y;
+      double n0 = (double)s0.x * (double)s0.x + (double)s0.y * (double)s0.y;
+      double n1 = (double)s1.x * (double)s1.x + (double)s1.y * (double)s1.y;
 #pragma unroll
       for (int o = 32; o >= 1; o >>= 1) {
         kn2 += __shfl_xor(kn2, o, 64);
-#pragma unroll
-        for (int i = 0; i < 3; ++i) {
-          dots[i] += __shfl_xor(dots[i], o, 64);
-          n2s[i] += __shfl_xor(n2s[i], o, 64);
-        }
+        d0 += __shfl_xor(d0, o, 64);
+        d1 += __shfl_xor(d1, o, 64);
+        n0 += __shfl_xor(n0, o, 64);
+        n1 += __shfl_xor(n1, o, 64);
       }
       const double knorm = sqrt(kn2);
-#pragma unroll
-      for (int i = 0; i < 3; ++i) {
-        if (i < ncc) {
-          const int k = cand[i];
-          const double c = cost_from_dot(dm, dots[i], knorm, n2s[i], kxf, kyf,
-                                         ws.bank + (unit * dm.K + k) * ROW, t_frame);
-          if (better(c, k, c1, k1)) { c2 = c1; c1 = c; k1 = k; }
-          else if (c < c2) c2 = c;
-        }
-      }
+      const double e0 = cost_from_dot(dm, d0, knorm, n0, kxf, kyf, ws.bank + (unit * dm.K + cand0) * ROW, t_frame);
+      const double e1 = cost_from_dot(dm, d1, knorm, n1, kxf, kyf, ws.bank + (unit * dm.K + cand1) * ROW, t_frame);
+      if (better(e0, cand0, e1, cand1)) { c1 = e0; k1 = cand0; c2 = e1; }
+      else { c1 = e1; k1 = cand1; c2 = e0; }
     } else {
       double kn2 = 0.0;
       for (int d = 0; d < D; d += 2) {
@@ -506,7 +518,7 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
     if (lane == 0) {
       ws.assign[unit * N + jj] = k1;
       n_ref += 1;
-      n_full += ncc > 3 ? 1 : 0;
+      n_full += ncc > 2 ? 1 : 0;
       n_tie += (c2 - c1) < NEAR_TIE ? 1 : 0;
     }
   }
@@ -515,7 +527,6 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
     if (n_full) atomicAdd(&ws.counters[CNT_REFINED_FULL], (unsigned long long)n_full);
     if (n_tie) atomicAdd(&ws.counters[CNT_NEAR_TIES], (unsigned long long)n_tie);
   }
-  }  // wave 0
 }
 
 hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
