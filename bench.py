@@ -65,8 +65,12 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     if kernel == "aggregate":
         return (U * (2 * T * D * b + T * 4 + T * 16)                   # evicted K,V, assignment, codes
                 + touched_per_launch * (2 * ROW_BYTES_USED + CACHE_BYTES))  # row RMW + cache rewrite
-    if kernel == "synthesize":
-        return U * n_active * (2 * 4 * D + 2 * 8 * 16 * 4 + 32) + U * n_active * S * D * b * 2 + U * K * 4
+    if kernel == "decode":
+        return U * n_active * (2 * 8 * 16 * 4 + 32 + 2 * (S + 1) * 4)       # histograms, meta, codes out
+    if kernel == "materialize":
+        # sums, meta, codes, codebooks per unit, pseudo-token rows out, bias out
+        return (U * n_active * (2 * 4 * D + 32 + 2 * (S + 1) * 4 + S * D * b * 2 + 4)
+                + U * 2 * 8 * 16 * 16 * 4)
     if kernel == "attend":
         return U * (2 * ctx * D * b + (ctx // max(S, 1)) * 4 + 2 * rows * D * b)
     return 0

@@ -216,11 +216,12 @@ enum {
   PROTOKV_K_SEED = 1,
   PROTOKV_K_SCREEN = 2,
   PROTOKV_K_AGGREGATE = 3,
-  PROTOKV_K_SYNTHESIZE = 4,
+  PROTOKV_K_SYNTHESIZE = 4,      /* top-S decoding of the histograms */
   PROTOKV_K_ATTEND = 5,
   PROTOKV_K_ATTEND_MERGE = 6,
   PROTOKV_K_PQ_ENCODE = 7,
-  PROTOKV_K_COUNT = 8
+  PROTOKV_K_MATERIALIZE = 8,     /* pseudo-token rows and biases */
+  PROTOKV_K_COUNT = 12
 };
 
 typedef struct {

@@ -16,6 +16,7 @@ constexpr int CMAX = 16;   // codewords per subspace (storage)
 constexpr int SMAX = 16;   // pseudo-tokens per prototype
 constexpr int TMAX = 1024; // tokens per frame
 constexpr int MAXB = 64;   // streams per launch batch
+constexpr int MAX_RBLOCKS = 2;  // query-row blocks of 256 per kv head
 
 // Bank row (one prototype slot), byte offsets; see protokv.h.
 constexpr int ROW = PROTOKV_ROW_BYTES;
@@ -66,6 +67,7 @@ struct Workspace {
   uint8_t* pk;                // [units][K*S][D] kv dtype (synthesis of one stream)
   uint8_t* pv;
   float* pbias;               // [units][K]
+  uint32_t* pcodes;           // [units][K][2][SMAX + 1]: decoded top-S code tuples + no-residual flag
   float* part_o;              // [units][max_splits][max_rows][D]
   float* part_ml;             // [units][max_splits][max_rows][2]  (max, sum)
   unsigned long long* counters;  // [16]
@@ -121,8 +123,8 @@ hipError_t launch_pq_encode(const Dims& dm, const Workspace& ws, const FoldBatch
                             hipStream_t st);
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                             hipStream_t st);
-hipError_t launch_synthesize(const Dims& dm, const Workspace& ws, int sid, int n_active,
-                             hipStream_t st);
+hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st);
+hipError_t launch_materialize(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st);
 hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& aa,
                          hipStream_t st);
 hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa,

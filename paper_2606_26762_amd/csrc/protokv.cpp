@@ -28,7 +28,7 @@ struct StreamState {
 
 struct Layout {
   size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codes, codebooks;
-  size_t pk, pv, pbias, part_o, part_ml, counters, touched, total;
+  size_t pk, pv, pbias, pcodes, part_o, part_ml, counters, touched, total;
 };
 
 thread_local std::string g_init_err;
@@ -62,6 +62,7 @@ Layout make_layout(const protokv_config& c) {
   ly.pk = take(units * K * S * D * es);
   ly.pv = take(units * K * S * D * es);
   ly.pbias = take(units * K * 4);
+  ly.pcodes = take(units * K * 2 * (SMAX + 1) * 4);
   ly.part_o = take(units * MAX_SPLITS * rows * D * 4);
   ly.part_ml = take(units * MAX_SPLITS * rows * 2 * 4);
   ly.counters = take(CNT_COUNT * 8);
@@ -259,6 +260,7 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.pk = b + ly.pk;
   ws.pv = b + ly.pv;
   ws.pbias = (float*)(b + ly.pbias);
+  ws.pcodes = (uint32_t*)(b + ly.pcodes);
   ws.part_o = (float*)(b + ly.part_o);
   ws.part_ml = (float*)(b + ly.part_ml);
   ws.counters = (unsigned long long*)(b + ly.counters);
@@ -394,10 +396,12 @@ protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
   if (sid < 0 || sid >= h->cfg.num_streams) return h->fail(PROTOKV_E_INVALID, "synthesize: stream id out of range");
   if (h->st[sid].pending) return h->fail(PROTOKV_E_STATE, "synthesize: stream has an unfolded eviction");
   hipStream_t hs = (hipStream_t)stream;
-  protokv_status s = h->dev(h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] {
-                              return launch_synthesize(h->dm, h->ws, sid, h->st[sid].active, hs);
-                            }),
-                            "synthesize");
+  const int na = h->st[sid].active;
+  protokv_status s = h->dev(h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] { return launch_decode(h->dm, h->ws, sid, na, hs); }),
+                            "synthesize/decode");
+  if (s == PROTOKV_OK)
+    s = h->dev(h->launch(PROTOKV_K_MATERIALIZE, hs, [&] { return launch_materialize(h->dm, h->ws, sid, na, hs); }),
+               "synthesize/materialize");
   if (s != PROTOKV_OK) return s;
   h->synth_stream = sid;
   h->synth_active = h->st[sid].active;
@@ -429,9 +433,13 @@ protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t t
   const int rows = tq * (h->dm.Hq / h->dm.Hkv);
   int splits;
   if (h->dm.kv_fp32) splits = std::max(1, std::min(MAX_SPLITS, (1024 + h->dm.units * rows - 1) / (h->dm.units * rows)));
-  else splits = std::max(1, std::min(MAX_SPLITS, (512 + h->dm.units - 1) / h->dm.units));
+  else {
+    const int rblocks = (rows + 255) / 256;
+    // about one workgroup per compute unit (256 on MI355X)
+    splits = std::max(1, std::min(MAX_SPLITS, (256 + h->dm.units * rblocks / 2) / (h->dm.units * rblocks)));
+  }
   int chunk = (ctx + splits - 1) / splits;
-  chunk = (chunk + 31) / 32 * 32;
+  chunk = (chunk + 63) / 64 * 64;
   splits = (ctx + chunk - 1) / chunk;
   aa.splits = splits;
   aa.chunk = chunk;

@@ -140,95 +140,214 @@ __device__ void decode_top_s(const uint32_t* hist /* [G][CMAX] */, int C, int S,
   for (int s = 0; s < S; ++s) out_codes[s] = s < nb ? bv.code[bv.at(cur, s, tl)] : 0u;
 }
 
-// One wave per workgroup over 32 prototypes of one (layer, kv head): lanes
-// 0-31 decode the key histograms, lanes 32-63 the value histograms, then the
-// wave writes the pseudo-tokens row by row (lane l writes components 2l, 2l+1).
-template <int FP32>
-__global__ __launch_bounds__(64) void k_synthesize(Dims dm, Workspace ws, int sid, int n_active,
-                                                   int blocks_per_unit) {
+// Register-resident exact top-S for prototypes whose residual count is at
+// most 65534: every factor H+1 is below 2^16, so a product of 8 factors fits
+// in 128 bits.  Same beam (width S) and merge order as decode_top_s.
+struct U128 {
+  uint64_t lo, hi;
+};
+
+__device__ __forceinline__ U128 mul_u128_u32(const U128& a, uint32_t f) {
+  U128 r;
+  const unsigned __int128 t0 = (unsigned __int128)a.lo * f;
+  r.lo = (uint64_t)t0;
+  r.hi = a.hi * (uint64_t)f + (uint64_t)(t0 >> 64);
+  return r;
+}
+
+// (pa, ca) ranks before (pb, cb): larger product, then smaller packed code.
+__device__ __forceinline__ bool before128(const U128& pa, uint32_t ca, const U128& pb, uint32_t cb) {
+  return pa.hi != pb.hi ? pa.hi > pb.hi : (pa.lo != pb.lo ? pa.lo > pb.lo : ca < cb);
+}
+
+template <int SM>
+__device__ void decode_top_s_small(const uint32_t* hist /* [G][CMAX] */, int C, int S, uint32_t* out) {
+  U128 bp[SM];
+  uint32_t bc[SM];
+#pragma unroll
+  for (int i = 0; i < SM; ++i) { bp[i].lo = 0; bp[i].hi = 0; bc[i] = 0; }
+  bp[0].lo = 1;
+  int nb = 1;
+  const int R = S < C ? S : C;
+  for (int g = 0; g < G; ++g) {
+    // ranks of subspace g: key = (count << 4 | (15 - code)) + 1, larger = better
+    uint32_t key[CMAX];
+    const uint4* h4 = reinterpret_cast<const uint4*>(hist + g * CMAX);
+#pragma unroll
+    for (int q = 0; q < CMAX / 4; ++q) {
+      const uint4 v = h4[q];
+      const uint32_t hv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = q * 4 + i;
+        key[c] = c < C ? ((hv[i] << 4) | (uint32_t)(15 - c)) + 1u : 0u;
+      }
+    }
+    uint32_t rf[SM], rc[SM];
+#pragma unroll
+    for (int r = 0; r < SM; ++r) {
+      uint32_t m = 0;
+#pragma unroll
+      for (int c = 0; c < CMAX; ++c) m = key[c] > m ? key[c] : m;
+#pragma unroll
+      for (int c = 0; c < CMAX; ++c) key[c] = key[c] == m ? 0u : key[c];
+      rf[r] = ((m - 1u) >> 4) + 1u;          // count + 1
+      rc[r] = 15u - ((m - 1u) & 15u);        // code
+    }
+    // merge the nb prefixes with the R ranks: S pops over the row heads
+    const int shift = 4 * (G - 1 - g);
+    int ptr[SM];
+    U128 hp[SM];
+#pragma unroll
+    for (int i = 0; i < SM; ++i) {
+      ptr[i] = 0;
+      hp[i] = mul_u128_u32(bp[i], rf[0]);
+    }
+    U128 np[SM];
+    uint32_t nc[SM];
+    const int total = nb * R;
+    const int nout = S < total ? S : total;
+#pragma unroll
+    for (int o = 0; o < SM; ++o) {
+      if (o < nout) {
+        int bi = -1;
+        U128 best = {0, 0};
+        uint32_t bcode = 0;
+#pragma unroll
+        for (int i = 0; i < SM; ++i) {
+          if (i < nb && ptr[i] < R) {
+            uint32_t rci = rc[0];
+#pragma unroll
+            for (int r = 1; r < SM; ++r) rci = ptr[i] == r ? rc[r] : rci;
+            const uint32_t code = bc[i] | (rci << shift);
+            if (bi < 0 || before128(hp[i], code, best, bcode)) { bi = i; best = hp[i]; bcode = code; }
+          }
+        }
+        np[o] = best;
+        nc[o] = bcode;
+#pragma unroll
+        for (int i = 0; i < SM; ++i) {
+          if (i == bi) {
+            ptr[i] += 1;
+            uint32_t f = rf[0];
+#pragma unroll
+            for (int r = 1; r < SM; ++r) f = ptr[i] == r ? rf[r] : f;
+            hp[i] = mul_u128_u32(bp[i], f);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < SM; ++i) { bp[i] = np[i]; bc[i] = nc[i]; }
+    nb = nout;
+  }
+  for (int sidx = 0; sidx < S; ++sidx) out[sidx] = sidx < nb ? bc[sidx] : 0u;
+}
+
+// Decoding: one thread per (slot, K/V) of one (layer, kv head), 32 slots per
+// workgroup (lanes 0-31 keys, 32-63 values).  Codes go to ws.pcodes
+// [units][K][2][SMAX] (packed tuples, subspace 0 in the top nibble) and a flag
+// word per (slot, K/V): 1 if the slot has no residual statistics.
+template <int SM>
+__global__ __launch_bounds__(64) void k_decode(Dims dm, Workspace ws, int sid, int n_active, int blocks_per_unit) {
   extern __shared__ __attribute__((aligned(16))) uint8_t s_dyn[];
-  __shared__ uint32_t s_codes[2][SYN_P][SMAX];
-  __shared__ uint32_t s_nores[2][SYN_P];  // 1: no residual statistics, S copies of the centre
   const int lane = threadIdx.x;
   const int u = blockIdx.x / blocks_per_unit;
-  const int p0 = (blockIdx.x % blocks_per_unit) * SYN_P;
+  const int p = (blockIdx.x % blocks_per_unit) * SYN_P + (lane & 31);
+  const int kv = lane >> 5;
+  if (p >= n_active) return;
   const size_t unit = (size_t)sid * dm.units + u;
   const int S = dm.S;
+  const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
+  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * (SMAX + 1);
   const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
-  BeamView bv;
-  bv.S = S;
-  bv.w0 = reinterpret_cast<uint64_t*>(s_dyn);
-  bv.w1 = bv.w0 + 2 * S * 64;
-  bv.w2 = bv.w1 + 2 * S * 64;
-  bv.code = reinterpret_cast<uint32_t*>(bv.w2 + 2 * S * 64);
-  const float* cbk = ws.codebooks + unit * (2 * G * CMAX * DP);
-
-  const int pl = lane & 31, kv = lane >> 5;
-  const int p = p0 + pl;
-  if (p < n_active) {
-    const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
-    const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
-    if (pq && m.n_res > 0) {
-      const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
-      uint32_t codes[SMAX];
-      decode_top_s(hist, dm.C, S, bv, lane, codes);
-      for (int s = 0; s < S; ++s) s_codes[kv][pl][s] = codes[s];
-      s_nores[kv][pl] = 0u;
-    } else {
-      s_nores[kv][pl] = 1u;
-    }
-    if (kv == 0) {
-      const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
-      ws.pbias[(size_t)u * dm.K + p] = mb ? logf((float)m.n) : 0.f;
-    }
+  if (!pq || m.n_res == 0) {
+    out[SMAX] = 1u;
+    return;
   }
-  __syncthreads();
+  out[SMAX] = 0u;
+  const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
+  uint32_t codes[SMAX];
+  if (m.n_res <= 65534u && S <= SM) {
+    decode_top_s_small<SM>(hist, dm.C, S, codes);
+  } else {
+    BeamView bv;
+    bv.S = S;
+    bv.w0 = reinterpret_cast<uint64_t*>(s_dyn);
+    bv.w1 = bv.w0 + 2 * S * 64;
+    bv.w2 = bv.w1 + 2 * S * 64;
+    bv.code = reinterpret_cast<uint32_t*>(bv.w2 + 2 * S * 64);
+    decode_top_s(hist, dm.C, S, bv, lane, codes);
+  }
+  for (int s2 = 0; s2 < S; ++s2) out[s2] = codes[s2];
+}
 
+// Pseudo-tokens: one wave per slot, lane l writes components 2l, 2l+1 of each
+// of the 2S rows: k~_s = kv_dtype(float32(c + r^K_s)), v~_s likewise, with
+// c = float32(sum / n) and r_s = concatenated codewords; bias = log n.
+template <int FP32>
+__global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int sid, int n_active) {
+  const int lane = threadIdx.x & 63;
+  const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int u = gw / dm.K, p = gw % dm.K;
+  if (u >= dm.units || p >= n_active) return;
+  const size_t unit = (size_t)sid * dm.units + u;
+  const int S = dm.S;
   const size_t es = FP32 ? 4 : 2;
+  const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
+  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  const float nf = (float)m.n;
+  const float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
+  const float2 sv = reinterpret_cast<const float2*>(row + ROW_SUMV)[lane];
+  const float* cbk = ws.codebooks + unit * (2 * G * CMAX * DP);
   const int g = lane >> 3, u16 = (2 * lane) & 15;
-  for (int q = 0; q < SYN_P; ++q) {
-    const int pp = p0 + q;
-    if (pp >= n_active) break;
-    const uint8_t* row = ws.bank + (unit * dm.K + pp) * ROW;
-    const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
-    const float nf = (float)m.n;
-    const float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
-    const float2 sv = reinterpret_cast<const float2*>(row + ROW_SUMV)[lane];
-    const float2 ck = make_float2(sk.x / nf, sk.y / nf);
-    const float2 cv = make_float2(sv.x / nf, sv.y / nf);
-    for (int w = 0; w < 2; ++w) {
-      const float2 c = w ? cv : ck;
-      uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * S + (size_t)pp * S) * D * es;
-      const bool nores = s_nores[w][q] != 0u;
-      for (int s = 0; s < S; ++s) {
-        const uint32_t code = s_codes[w][q][s];
-        float2 val = c;
-        if (!nores) {
-          const int z = (code >> (4 * (G - 1 - g))) & 15;
-          const float2 cw = *reinterpret_cast<const float2*>(cbk + ((w * G + g) * CMAX + z) * DP + u16);
-          val.x = c.x + cw.x;
-          val.y = c.y + cw.y;
-        }
-        if (FP32) {
-          reinterpret_cast<float2*>(out + (size_t)s * D * 4)[lane] = val;
-        } else {
-          const uint32_t packed = (uint32_t)q_to_bf16(val.x) | ((uint32_t)q_to_bf16(val.y) << 16);
-          reinterpret_cast<uint32_t*>(out + (size_t)s * D * 2)[lane] = packed;
-        }
+  if (lane == 0) {
+    const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
+    ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
+  }
+#pragma unroll
+  for (int w = 0; w < 2; ++w) {
+    const float2 c = w ? make_float2(sv.x / nf, sv.y / nf) : make_float2(sk.x / nf, sk.y / nf);
+    const uint32_t* codes = ws.pcodes + (((size_t)u * dm.K + p) * 2 + w) * (SMAX + 1);
+    const bool nores = codes[SMAX] != 0u;
+    uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * S + (size_t)p * S) * D * es;
+    for (int s2 = 0; s2 < S; ++s2) {
+      float2 val = c;
+      if (!nores) {
+        const int z = (codes[s2] >> (4 * (G - 1 - g))) & 15;
+        const float2 cw = *reinterpret_cast<const float2*>(cbk + ((w * G + g) * CMAX + z) * DP + u16);
+        val.x = c.x + cw.x;
+        val.y = c.y + cw.y;
+      }
+      if (FP32) {
+        reinterpret_cast<float2*>(out + (size_t)s2 * D * 4)[lane] = val;
+      } else {
+        const uint32_t packed = (uint32_t)q_to_bf16(val.x) | ((uint32_t)q_to_bf16(val.y) << 16);
+        reinterpret_cast<uint32_t*>(out + (size_t)s2 * D * 2)[lane] = packed;
       }
     }
   }
 }
 
-hipError_t launch_synthesize(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st) {
+hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st) {
   if (n_active <= 0) return hipSuccess;
-  int bpu = (n_active + SYN_P - 1) / SYN_P;
-  dim3 grid(dm.units * bpu);
-  size_t lds = (size_t)2 * dm.S * 64 * (3 * sizeof(uint64_t) + sizeof(uint32_t));
-  if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_synthesize<1>, grid, dim3(64), lds, st, dm, ws, sid, n_active, bpu);
+  const int bpu = (n_active + SYN_P - 1) / SYN_P;
+  const size_t lds = (size_t)2 * dm.S * 64 * (3 * sizeof(uint64_t) + sizeof(uint32_t));
+  if (dm.S <= 8)
+    hipLaunchKernelGGL(k_decode<8>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
   else
-    hipLaunchKernelGGL(k_synthesize<0>, grid, dim3(64), lds, st, dm, ws, sid, n_active, bpu);
+    hipLaunchKernelGGL(k_decode<16>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
+  return hipGetLastError();
+}
+
+hipError_t launch_materialize(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st) {
+  if (n_active <= 0) return hipSuccess;
+  const int waves = dm.units * dm.K;
+  if (dm.kv_fp32)
+    hipLaunchKernelGGL(k_materialize<1>, dim3((waves + 3) / 4), dim3(256), 0, st, dm, ws, sid, n_active);
+  else
+    hipLaunchKernelGGL(k_materialize<0>, dim3((waves + 3) / 4), dim3(256), 0, st, dm, ws, sid, n_active);
   return hipGetLastError();
 }
 
@@ -240,8 +359,6 @@ hipError_t launch_synthesize(const Dims& dm, const Workspace& ws, int sid, int n
 // ---------------------------------------------------------------------------
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
-constexpr int KROW = 136;  // staged key row (bf16), 128 + 8 padding
-constexpr int VCOL = 40;   // staged transposed value row (bf16), 32 keys + 8 padding
 
 struct CtxRef {
   const uint8_t* base;
@@ -269,31 +386,51 @@ __device__ __forceinline__ CtxRef ctx_key(const Dims& dm, const Workspace& ws, c
   return r;
 }
 
-// bf16 path: workgroup = one (kv head, context split), one wave per 32 query
-// rows.  S^T = K Q^T and O^T = V^T P with v_mfma_f32_32x32x16_bf16; each lane
-// holds one query column, so the online softmax needs only lane-local work
-// plus one exchange with the partner lane (the other 16 key rows).
-__global__ __launch_bounds__(1024) void k_attend_bf16(Dims dm, Workspace ws, AttendArgs aa, int rows) {
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[2][32 * KROW];
-  __shared__ __attribute__((aligned(16))) uint16_t s_vt[2][D * VCOL];
-  __shared__ float s_bias[2][32];
+// bf16 path.  Workgroup = one (kv head, context split, block of up to 256
+// query rows), one wave per 32 rows (at least 4 waves).  Context tiles of 64
+// keys go straight from global memory into double-buffered LDS
+// (global_load_lds_dwordx4, row-major, 16-byte chunks XOR-swizzled by row so
+// the operand reads do not conflict); the next tile loads while the current
+// one is computed.  S^T = K Q^T and O^T = V^T P with v_mfma_f32_32x32x16_bf16;
+// the V^T operand comes from the row-major tile through ds_read_b64_tr_b16.
+// Each lane holds one query column, so the online softmax is lane-local plus
+// one exchange with the partner lane.  With several splits, every workgroup
+// writes its partial (unnormalised O, running max, sum) for k_attend_merge.
+constexpr int AT_KEYS = 64;
+constexpr int AT_ROWS = 256;  // query rows per workgroup
+constexpr int AT_TILE_BYTES = AT_KEYS * D * 2;   // one K or V tile, 16 KB
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void gbl_void;
+
+// byte offset of 16-byte chunk c of tile row r
+__device__ __forceinline__ int at_chunk(int r, int c) { return r * (D * 2) + ((c ^ (r & 15)) << 4); }
+
+__global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, AttendArgs aa, int rows, int rblocks) {
+  __shared__ __attribute__((aligned(16))) uint8_t s_kv[2][2][AT_TILE_BYTES];   // [buffer][K,V]
+  __shared__ float s_bias[2][AT_KEYS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nthr = blockDim.x;
-  const int split = blockIdx.x % aa.splits;
-  const int u = blockIdx.x / aa.splits;
+  const int nwave = blockDim.x >> 6;
+  // blocks of one kv head land on one XCD (dispatch is round-robin over 8)
+  const int nblk = gridDim.x, per = nblk / 8;
+  const int lbid = (int)blockIdx.x < per * 8 ? ((int)blockIdx.x % 8) * per + (int)blockIdx.x / 8 : (int)blockIdx.x;
+  const int split = lbid % aa.splits;
+  const int rb = (lbid / aa.splits) % rblocks;
+  const int u = lbid / (aa.splits * rblocks);
   const size_t unit = (size_t)aa.sid * dm.units + u;
   const int grp = dm.Hq / dm.Hkv;
   const int l = u / dm.Hkv, kvh = u % dm.Hkv;
   const int ctx = aa.n_near + aa.n_far;
   const int c0 = split * aa.chunk;
   const int c1 = min(ctx, c0 + aa.chunk);
-  const int ntiles = c1 > c0 ? (c1 - c0 + 31) / 32 : 0;
+  const int ntiles = c1 > c0 ? (c1 - c0 + AT_KEYS - 1) / AT_KEYS : 0;
 
   const int col = lane & 31, half = lane >> 5;
-  const int r = wave * 32 + col;  // query row of this lane
+  const int r = rb * AT_ROWS + wave * 32 + col;  // query row of this lane
   const bool rvalid = r < rows;
-  // Q^T operand: dims kk*16 + half*8 + 0..7 of row r.
   bf16x8 bq[8];
   {
     const int t = rvalid ? r / grp : 0, gg = rvalid ? r % grp : 0;
@@ -306,80 +443,86 @@ __global__ __launch_bounds__(1024) void k_attend_bf16(Dims dm, Workspace ws, Att
       bq[kk] = __builtin_bit_cast(bf16x8, v);
     }
   }
+
+  // Async load of tile t into buffer buf: 2 x 16 wave-instructions (4 rows of
+  // 16 chunks each); wave w issues instructions w, w + nwave, ...  Lane L of
+  // instruction i lands at byte (i*64 + L)*16 of the tile = row 4i + L/16,
+  // physical chunk L%16, so it fetches logical chunk (L%16) ^ (row & 15).
+  float bias_reg = -INFINITY;
+  auto issue = [&](int t, int buf) {
+    const int base = c0 + t * AT_KEYS;
+    for (int i = wave; i < 32; i += nwave) {
+      const int kv = i >> 4, ii = i & 15;
+      const int row = ii * 4 + (lane >> 4);
+      const int cl = (lane & 15) ^ (row & 15);
+      const int idx = base + row;
+      // rows past the context read row c0 (any valid row; masked by the bias)
+      const CtxRef ref = ctx_key<2>(dm, ws, aa, unit, u, idx < c1 ? idx : c0, kv == 1);
+      __builtin_amdgcn_global_load_lds((gbl_void*)(ref.base + cl * 16),
+                                       (lds_void*)(&s_kv[buf][kv][ii * 1024]), 16, 0, 0);
+    }
+    if (wave == 0) {
+      const int idx = base + lane;
+      bias_reg = idx < c1 ? ctx_key<2>(dm, ws, aa, unit, u, idx, false).bias : -INFINITY;
+    }
+  };
+
   const float scale = LOG2E / sqrtf((float)D);
   f32x16 oacc[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) oacc[b] = (f32x16){0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.f;
 
-  auto stage = [&](int t, int buf) {
-    const int base = c0 + t * 32;
-    // keys: 32 rows x 16 chunks of 16 B
-    for (int c = tid; c < 32 * 16; c += nthr) {
-      const int rr = c >> 4, cc = c & 15;
-      const int idx = base + rr;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (idx < c1) {
-        CtxRef kr = ctx_key<2>(dm, ws, aa, unit, u, idx, false);
-        val = *reinterpret_cast<const uint4*>(kr.base + cc * 16);
-      }
-      *reinterpret_cast<uint4*>(s_k[buf] + rr * KROW + cc * 8) = val;
-    }
-    // values, transposed into [dim][key]
-    for (int c = tid; c < 32 * 16; c += nthr) {
-      const int rr = c >> 4, cc = c & 15;
-      const int idx = base + rr;
-      u16x8 val = (u16x8)0;
-      if (idx < c1) {
-        CtxRef vr = ctx_key<2>(dm, ws, aa, unit, u, idx, true);
-        val = *reinterpret_cast<const u16x8*>(vr.base + cc * 16);
-      }
-#pragma unroll
-      for (int i = 0; i < 8; ++i) s_vt[buf][(cc * 8 + i) * VCOL + rr] = val[i];
-    }
-    if (tid < 32) {
-      const int idx = base + tid;
-      float bval = -INFINITY;
-      if (idx < c1) bval = ctx_key<2>(dm, ws, aa, unit, u, idx, false).bias;
-      s_bias[buf][tid] = bval;
-    }
-  };
-
-  if (ntiles > 0) stage(0, 0);
-  __syncthreads();
+  if (ntiles > 0) issue(0, 0);
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
-    if (t + 1 < ntiles) stage(t + 1, buf ^ 1);
-    // S^T = K Q^T: rows = keys (m), columns = query rows
-    f32x16 sacc = (f32x16){0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    const uint16_t* kr = s_k[buf] + col * KROW + half * 8;
+    __builtin_amdgcn_s_waitcnt(0);          // this wave's loads of tile t have landed
+    if (wave == 0) s_bias[buf][lane] = bias_reg;
+    __syncthreads();
+    if (t + 1 < ntiles) issue(t + 1, buf ^ 1);
+    const uint8_t* kt = s_kv[buf][0];
+    const uint8_t* vt = s_kv[buf][1];
+    // S^T for the two 32-key halves of the tile
+    f32x16 sacc[2];
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const bf16x8 ak = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(kr + kk * 16));
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bq[kk], sacc, 0, 0, 0);
+    for (int h = 0; h < 2; ++h) {
+      sacc[h] = (f32x16){0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      const int krow = h * 32 + col;
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) {
+        const bf16x8 ak = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(kt + at_chunk(krow, 2 * kk + half)));
+        sacc[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bq[kk], sacc[h], 0, 0, 0);
+      }
     }
-    // logits in log2 units, masked beyond the context
     float tmax = -INFINITY;
-    float sv[16];
+    float sv[2][16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int m = (i >> 2) * 8 + half * 4 + (i & 3);
-      const float bsv = s_bias[buf][m];
-      const float x = bsv == -INFINITY ? -INFINITY : sacc[i] * scale + bsv * LOG2E;
-      sv[i] = x;
-      tmax = fmaxf(tmax, x);
-    }
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int m = h * 32 + (i >> 2) * 8 + half * 4 + (i & 3);
+        const float bsv = s_bias[buf][m];
+        const float x = bsv == -INFINITY ? -INFINITY : fmaf(sacc[h][i], scale, bsv * LOG2E);
+        sv[h][i] = x;
+        tmax = fmaxf(tmax, x);
+      }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
     const float mnew = fmaxf(mrun, tmax);
-    const float alpha = mnew == -INFINITY ? 1.f : exp2f(mrun - mnew);
+    const float alpha = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(mrun - mnew);
     float psum = 0.f;
-    u16x8 pb0, pb1;
+    bf16x8 pb[4];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float pv = sv[i] == -INFINITY ? 0.f : exp2f(sv[i] - mnew);
-      psum += pv;
-      const uint16_t hb = q_to_bf16(pv);
-      if (i < 8) pb0[i] = hb; else pb1[i - 8] = hb;
+    for (int h = 0; h < 2; ++h) {
+      u16x8 p0, p1;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float pv = sv[h][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sv[h][i] - mnew);
+        psum += pv;
+        const uint16_t hb = q_to_bf16(pv);
+        if (i < 8) p0[i] = hb; else p1[i - 8] = hb;
+      }
+      pb[2 * h] = __builtin_bit_cast(bf16x8, p0);
+      pb[2 * h + 1] = __builtin_bit_cast(bf16x8, p1);
     }
     psum += __shfl_xor(psum, 32, 64);
     lrun = lrun * alpha + psum;
@@ -388,34 +531,51 @@ __global__ __launch_bounds__(1024) void k_attend_bf16(Dims dm, Workspace ws, Att
     for (int b = 0; b < 4; ++b)
 #pragma unroll
       for (int i = 0; i < 16; ++i) oacc[b][i] *= alpha;
-    const bf16x8 bp0 = __builtin_bit_cast(bf16x8, pb0), bp1 = __builtin_bit_cast(bf16x8, pb1);
-    // O^T = V^T P: A = V^T rows (dims), k positions half*8 + i <-> keys
-    // {4 half + 0..3, 8 + 4 half + 0..3} (+16 for the second step).
+    // O^T = V^T P.  k positions half*8 + i of step st <-> keys 16 st + 4 half + {0..3}
+    // (i < 4) and 16 st + 8 + 4 half + {0..3} (i >= 4), matching P's layout.  Each
+    // 4-key part is one ds_read_b64_tr_b16 per 16-lane group: source lane s reads
+    // key key0 + s/4, dims d0 + 4(s%4) .. +3; lane i then holds dim d0 + i of the 4 keys.
+    const int grp16 = lane >> 4, s16 = lane & 15;
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
-      const uint16_t* vr = s_vt[buf] + (b * 32 + col) * VCOL + 4 * half;
+      const int d0 = b * 32 + (grp16 & 1) * 16;
+      const int dsrc = d0 + 4 * (s16 & 3);
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        const u16x4 lo = *reinterpret_cast<const u16x4*>(vr + st * 16);
-        const u16x4 hi = *reinterpret_cast<const u16x4*>(vr + st * 16 + 8);
-        const u16x8 a = (u16x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                          st ? bp1 : bp0, oacc[b], 0, 0, 0);
+      for (int st = 0; st < 4; ++st) {
+        const int ka = st * 16 + 4 * half + (s16 >> 2);
+        const int kb = ka + 8;
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_v4i16*)(vt + at_chunk(ka, dsrc >> 3) + (dsrc & 7) * 2));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_v4i16*)(vt + at_chunk(kb, dsrc >> 3) + (dsrc & 7) * 2));
+        const u16x8 a = (u16x8){(uint16_t)lo[0], (uint16_t)lo[1], (uint16_t)lo[2], (uint16_t)lo[3],
+                                (uint16_t)hi[0], (uint16_t)hi[1], (uint16_t)hi[2], (uint16_t)hi[3]};
+        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), pb[st], oacc[b], 0, 0, 0);
       }
     }
-    __syncthreads();
   }
 
-  // partial (unnormalised O, running max in log2 units, sum)
+  const size_t orow_t = rvalid ? (size_t)(r / grp) : 0;
+  const int ogg = rvalid ? r % grp : 0;
+  const size_t orow = (((size_t)l * aa.tq + orow_t) * dm.Hq + kvh * grp + ogg) * D;
+  if (aa.splits == 1) {
+    if (rvalid) {
+      const float inv = lrun > 0.f ? 1.0f / lrun : 0.f;
+      uint16_t* o = reinterpret_cast<uint16_t*>(aa.o) + orow;
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[b * 32 + (i >> 2) * 8 + half * 4 + (i & 3)] = q_to_bf16(oacc[b][i] * inv);
+      if (half == 0 && aa.lse) aa.lse[((size_t)l * aa.tq + orow_t) * dm.Hq + kvh * grp + ogg] = (mrun + log2f(lrun)) * LN2;
+    }
+    return;
+  }
   if (rvalid) {
     float* po = ws.part_o + (((size_t)u * dm.max_splits + split) * dm.max_rows + r) * D;
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int dim = b * 32 + (i >> 2) * 8 + half * 4 + (i & 3);
-        po[dim] = oacc[b][i];
-      }
+      for (int i = 0; i < 16; ++i) po[b * 32 + (i >> 2) * 8 + half * 4 + (i & 3)] = oacc[b][i];
     if (half == 0) {
       float* pml = ws.part_ml + (((size_t)u * dm.max_splits + split) * dm.max_rows + r) * 2;
       pml[0] = mrun;
@@ -426,10 +586,12 @@ __global__ __launch_bounds__(1024) void k_attend_bf16(Dims dm, Workspace ws, Att
 
 // Combines the splits of each query row: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
 template <int FP32>
-__global__ __launch_bounds__(64) void k_attend_merge(Dims dm, Workspace ws, AttendArgs aa, int rows) {
-  const int lane = threadIdx.x;
-  const int r = blockIdx.x % rows;
-  const int u = blockIdx.x / rows;
+__global__ __launch_bounds__(256) void k_attend_merge(Dims dm, Workspace ws, AttendArgs aa, int rows) {
+  const int lane = threadIdx.x & 63;
+  const int gr = blockIdx.x * 4 + (threadIdx.x >> 6);   // (kv head, row) pair
+  if (gr >= dm.units * rows) return;
+  const int r = gr % rows;
+  const int u = gr / rows;
   const int grp = dm.Hq / dm.Hkv;
   const int l = u / dm.Hkv, kvh = u % dm.Hkv;
   float M = -INFINITY;
@@ -505,18 +667,22 @@ hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& 
   if (dm.kv_fp32) {
     hipLaunchKernelGGL(k_attend_f32, dim3(dm.units * rows * aa.splits), dim3(64), 0, st, dm, ws, aa, rows);
   } else {
-    const int waves = (rows + 31) / 32;
-    hipLaunchKernelGGL(k_attend_bf16, dim3(dm.units * aa.splits), dim3(waves * 64), 0, st, dm, ws, aa, rows);
+    const int rblocks = (rows + AT_ROWS - 1) / AT_ROWS;
+    const int waves = std::max(4, (std::min(rows, AT_ROWS) + 31) / 32);
+    hipLaunchKernelGGL(k_attend_bf16, dim3(dm.units * aa.splits * rblocks), dim3(waves * 64), 0, st, dm, ws, aa,
+                       rows, rblocks);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa, hipStream_t st) {
+  if (!dm.kv_fp32 && aa.splits == 1) return hipSuccess;  // the bf16 readout wrote O directly
   const int rows = aa.tq * (dm.Hq / dm.Hkv);
+  const int nb = (dm.units * rows + 3) / 4;
   if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_attend_merge<1>, dim3(dm.units * rows), dim3(64), 0, st, dm, ws, aa, rows);
+    hipLaunchKernelGGL(k_attend_merge<1>, dim3(nb), dim3(256), 0, st, dm, ws, aa, rows);
   else
-    hipLaunchKernelGGL(k_attend_merge<0>, dim3(dm.units * rows), dim3(64), 0, st, dm, ws, aa, rows);
+    hipLaunchKernelGGL(k_attend_merge<0>, dim3(nb), dim3(256), 0, st, dm, ws, aa, rows);
   return hipGetLastError();
 }
 

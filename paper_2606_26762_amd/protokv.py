@@ -29,7 +29,8 @@ EXPORTED = [
     "protokv_read_pseudo", "protokv_profile", "protokv_profile_read", "protokv_last_error",
 ]
 
-KERNELS = ["ring_insert", "seed", "screen", "aggregate", "synthesize", "attend", "attend_merge", "pq_encode"]
+KERNELS = ["ring_insert", "seed", "screen", "aggregate", "decode", "attend", "attend_merge", "pq_encode",
+           "materialize"]
 
 
 class ProtoKVError(RuntimeError):
@@ -65,7 +66,7 @@ class Counters(ctypes.Structure):
 
 
 class KernelTimes(ctypes.Structure):
-    _fields_ = [("ms", ctypes.c_double * 8), ("launches", ctypes.c_uint64 * 8)]
+    _fields_ = [("ms", ctypes.c_double * 12), ("launches", ctypes.c_uint64 * 12)]
 
 
 _lib = None
