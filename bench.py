@@ -15,8 +15,13 @@ folded per second over the timed region (each token folded into all 112
 units).  Readout latency per query is timed separately (median of repeats).
 
 Per-kernel device times come from HIP events the library records around
-each launch on the launch stream (a second pass over further frames); the
-roofline object uses the dominant kernel's algorithmic bytes per launch.
+each launch on the launch stream: first around every launch over
+--profile-frames frames (to find the fold's dominant kernel), then, inside
+the timed region, around that kernel's launches only.  The roofline object
+divides that kernel's algorithmic bytes per launch by its live average
+duration; `traffic` is the HBM bytes per launch from the committed
+FETCH_SIZE/WRITE_SIZE summary under profiles/, null when the kernel's source
+has changed since.
 """
 import argparse
 import ctypes
@@ -74,6 +79,44 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     if kernel == "attend":
         return U * (2 * ctx * D * b + (ctx // max(S, 1)) * 4 + 2 * rows * D * b)
     return 0
+
+
+FOLD_KERNELS = ("ring_insert", "seed", "screen", "pq_encode", "aggregate")
+KERNEL_SOURCES = {k: "fold.hip" for k in FOLD_KERNELS}
+KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "attend", "attend_merge")})
+
+
+def kernel_source_hash(kernel):
+    """sha256 over the HIP source file holding `kernel` and the shared header."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2606_26762_amd", "csrc")
+    hs = hashlib.sha256()
+    for f in (KERNEL_SOURCES[kernel], "pkv_internal.h"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            hs.update(fh.read())
+    return hs.hexdigest()
+
+
+def recorded_traffic(kernel, wl):
+    """HBM bytes per launch from a committed FETCH_SIZE/WRITE_SIZE summary under
+    profiles/ (a fenced json block), or None when there is none for this kernel
+    and workload or the kernel's source has changed since the counters were taken."""
+    import glob
+    import re
+    want = kernel_source_hash(kernel)
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        text = open(path).read()
+        for block in re.findall(r"```json\n(.*?)\n```", text, re.S):
+            try:
+                rec = json.loads(block)
+            except ValueError:
+                continue
+            if (isinstance(rec, dict) and rec.get("kernel") == kernel and rec.get("workload") == wl.name
+                    and rec.get("source_sha256") == want and "traffic_bytes_per_launch" in rec):
+                rec = dict(rec)
+                rec["file"] = os.path.relpath(path, ROOT)
+                return rec
+    return None
 
 
 def cpu_baseline(args, wl):
@@ -137,7 +180,7 @@ def main():
     from paper_2606_26762_amd import workloads as W
 
     wl = W.WORKLOADS[args.workload]
-    frames_needed = args.warmup + args.steps + args.profile_frames
+    frames_needed = args.warmup + args.profile_frames + args.steps
     assert args.warmup >= wl.window_frames + math.ceil(wl.capacity / wl.tokens_per_frame), \
         "warmup must fill the bank"
     lib = pk.lib()
@@ -186,41 +229,11 @@ def main():
     run_query()
     torch.cuda.synchronize()
 
-    # timed region: --steps frames + one query
-    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    e0.record(stream)
-    run_frames(args.warmup, args.warmup + args.steps)
-    e1.record(stream)
-    run_query()
-    e2.record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_total = e0.elapsed_time(e2)
-    ms_fold = e0.elapsed_time(e1)
-    ms_query_in_region = e1.elapsed_time(e2)
-    T = wl.tokens_per_frame
-    value = args.steps * T / (ms_total / 1e3)
-
-    # readout latency: median over repeats, synthesize+attend and attend only
-    def median_ms(fn, reps):
-        out = []
-        for _ in range(reps):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            fn()
-            b.record(stream)
-            torch.cuda.synchronize()
-            out.append(a.elapsed_time(b))
-        return float(np.median(out))
-    readout_ms = median_ms(run_query, args.query_reps)
-    attend_ms = median_ms(lambda: attend(h, 0, qp, tq, op, lp, sp), args.query_reps)
-
-    # per-kernel device times (library-recorded HIP events), further frames
+    # per-kernel device times: library-recorded HIP events around every launch,
+    # over --profile-frames frames and 5 queries, to find the dominant kernel
+    lo = args.warmup
     c0 = eng.counters()
     eng.profile(True)
-    lo = args.warmup + args.steps
     run_frames(lo, lo + args.profile_frames)
     for _ in range(5):
         run_query()
@@ -239,15 +252,59 @@ def main():
         kernels[name] = {"avg_us": round(d["avg_us"], 3), "launches": d["launches"],
                          "alg_bytes": int(nbytes),
                          "gbs": round(nbytes / (d["avg_us"] * 1e-6) / 1e9, 1) if nbytes else None}
-    # dominant kernel of the streaming step
+    # dominant kernel of the streaming step (device time per frame)
     per_frame = {n: kernels[n]["avg_us"] * kernels[n]["launches"] / args.profile_frames
-                 for n in ("ring_insert", "seed", "screen", "pq_encode", "aggregate") if n in kernels}
+                 for n in FOLD_KERNELS if n in kernels}
     dom = max(per_frame, key=per_frame.get)
-    dk = kernels[dom]
-    achieved = dk["gbs"]
-    roofline = {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                "alg_bytes_per_launch": dk["alg_bytes"], "avg_us": dk["avg_us"]}
+
+    # timed region: --steps frames + one query; only the dominant kernel's
+    # launches are bracketed by the library's events (on the launch stream)
+    lo += args.profile_frames
+    c2 = eng.counters()
+    eng.profile(True, [dom])
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    run_frames(lo, lo + args.steps)
+    e1.record(stream)
+    run_query()
+    e2.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    live = eng.profile_read()[dom]
+    eng.profile(False)
+    c3 = eng.counters()
+    ms_total = e0.elapsed_time(e2)
+    ms_fold = e0.elapsed_time(e1)
+    ms_query_in_region = e1.elapsed_time(e2)
+    value = args.steps * T / (ms_total / 1e3)
+    touched_live = (c3.touched - c2.touched) / args.steps
+
+    # readout latency: median over repeats, synthesize+attend and attend only
+    def median_ms(fn, reps):
+        out = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            out.append(a.elapsed_time(b))
+        return float(np.median(out))
+    readout_ms = median_ms(run_query, args.query_reps)
+    attend_ms = median_ms(lambda: attend(h, 0, qp, tq, op, lp, sp), args.query_reps)
+
+    dom_bytes = algorithmic_bytes(dom, wl, cfg, touched_per_launch=touched_live, n_active=n_active,
+                                  ctx=ctx, rows=rows)
+    achieved = dom_bytes / (live["avg_us"] * 1e-6) / 1e9
+    traffic = recorded_traffic(dom, wl)
+    roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic["traffic_bytes_per_launch"] if traffic else None,
+                "alg_bytes_per_launch": int(dom_bytes), "avg_us": round(live["avg_us"], 3),
+                "launches_timed": live["launches"],
+                "traffic_source": traffic["file"] if traffic else None}
     # screen MFMA work, for reference: 2 (hi, lo) x 2 N K D flops per unit
     scr_flops = wl.units * 2 * 2 * T * wl.capacity * wl.head_dim
     if "screen" in kernels:
@@ -266,17 +323,17 @@ def main():
                    "q_heads": wl.num_q_heads, "head_dim": wl.head_dim, "tokens_per_frame": T,
                    "window_frames": wl.window_frames, "capacity": wl.capacity,
                    "pseudo_per_proto": cfg.pseudo_per_proto, "query_tokens": tq,
-                   "frames_streamed": args.warmup + args.steps},
+                   "frames_streamed": lo + args.steps},
         "fold_tokens_per_s": round(args.steps * T / (ms_fold / 1e3), 1),
         "fold_us_per_frame": round(1e3 * ms_fold / args.steps, 2),
         "query_us_in_region": round(1e3 * ms_query_in_region, 2),
         "readout_us_per_query": round(1e3 * readout_ms, 2),
         "attend_us_per_query": round(1e3 * attend_ms, 2),
         "wall_s_timed_region": round(t_wall, 4),
-        "touched_per_fold": round(touched, 1), "active_slots": n_active,
+        "touched_per_fold": round(touched_live, 1), "active_slots": n_active,
         "context_tokens": ctx,
-        "refined_fraction": round((c1.refined + c1.refined_full) / max(1, c1.tokens_assigned), 5),
-        "near_ties": c1.near_ties,
+        "refined_fraction": round((c3.refined + c3.refined_full) / max(1, c3.tokens_assigned), 5),
+        "refined_full": c3.refined_full, "near_ties": c3.near_ties,
         "kernels": kernels,
         "roofline": roofline,
     }

@@ -229,10 +229,13 @@ typedef struct {
   uint64_t launches[PROTOKV_K_COUNT];  /* launches timed per kernel */
 } protokv_kernel_times;
 
-/* Diagnostics: enable != 0 brackets every kernel launch of this handle with
- * a pair of HIP events recorded on the launch stream (and clears the totals);
- * enable == 0 stops recording.  Host only; creates HIP events on first use. */
-protokv_status protokv_profile(protokv_t h, int32_t enable);
+/* Diagnostics: a nonzero kernel_mask (bit i = protokv_kernel_id i) brackets
+ * every launch of the selected kernels on this handle with a pair of HIP
+ * events recorded on the launch stream, and clears the totals; 0 stops
+ * recording.  The events are created without a system-scope fence, so they
+ * add no cache writeback to the timed work.  Host only; creates HIP events on
+ * first use. */
+protokv_status protokv_profile(protokv_t h, uint32_t kernel_mask);
 
 /* Sums the recorded event pairs into `out` (waits for each end event). */
 protokv_status protokv_profile_read(protokv_t h, protokv_kernel_times* out);

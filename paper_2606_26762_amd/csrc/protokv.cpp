@@ -119,7 +119,7 @@ struct protokv_ctx {
   uint64_t folds = 0, assigned = 0, seeded = 0;
   std::string err;
   // per-kernel event timing (diagnostics)
-  bool profiling = false;
+  uint32_t profile_mask = 0;
   std::vector<hipEvent_t> ev_pool;
   struct Timed { int id; hipEvent_t a, b; };
   std::vector<Timed> timed;
@@ -127,12 +127,12 @@ struct protokv_ctx {
 
   template <class F>
   hipError_t launch(int id, hipStream_t st, F&& f) {
-    if (!profiling) return f();
+    if (!(profile_mask >> id & 1u)) return f();
     hipEvent_t e[2];
     for (int i = 0; i < 2; ++i) {
       if (ev_next == ev_pool.size()) {
         hipEvent_t ne;
-        hipError_t r = hipEventCreate(&ne);
+        hipError_t r = hipEventCreateWithFlags(&ne, hipEventDisableSystemFence);
         if (r != hipSuccess) return r;
         ev_pool.push_back(ne);
       }
@@ -518,13 +518,13 @@ protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float*
   return s;
 }
 
-protokv_status protokv_profile(protokv_t h, int32_t enable) {
+protokv_status protokv_profile(protokv_t h, uint32_t kernel_mask) {
   if (!h) return PROTOKV_E_INVALID;
-  if (enable) {
+  if (kernel_mask) {
     h->timed.clear();
     h->ev_next = 0;
   }
-  h->profiling = enable != 0;
+  h->profile_mask = kernel_mask;
   return PROTOKV_OK;
 }
 

@@ -94,7 +94,7 @@ def lib() -> ctypes.CDLL:
         L.protokv_read_assignments.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_read_bank.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_read_pseudo.argtypes = [vp, vp, vp, vp, vp]
-        L.protokv_profile.argtypes = [vp, i32]
+        L.protokv_profile.argtypes = [vp, ctypes.c_uint32]
         L.protokv_profile_read.argtypes = [vp, P(KernelTimes)]
         L.protokv_last_error.argtypes = [vp]
         L.protokv_last_error.restype = ctypes.c_char_p
@@ -246,8 +246,12 @@ class ProtoKV:
         shape = (self.units, self.cfg.capacity * self.cfg.pseudo_per_proto, self.cfg.head_dim)
         return conv(raw_k).reshape(shape), conv(raw_v).reshape(shape), bias.reshape(self.units, -1)
 
-    def profile(self, enable: bool):
-        _check(lib().protokv_profile(self.h, 1 if enable else 0), self.h)
+    def profile(self, enable, kernels=None):
+        """Time every launch (enable=True), only the named kernels, or stop (False)."""
+        mask = 0
+        if enable:
+            mask = 0xFFFFFFFF if kernels is None else sum(1 << KERNELS.index(k) for k in kernels)
+        _check(lib().protokv_profile(self.h, mask), self.h)
 
     def profile_read(self) -> Dict[str, dict]:
         """-> {kernel: {"ms": total, "launches": n, "avg_us": mean}} for timed kernels."""
