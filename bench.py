@@ -212,6 +212,7 @@ def main():
     vp = [ctypes.c_void_p(t.data_ptr()) for t in vs]
     qp, op, lp = ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(o.data_ptr()), ctypes.c_void_p(lse.data_ptr())
     tq = q.shape[1]
+    T = wl.tokens_per_frame
     append, fold = lib.protokv_append_frame, lib.protokv_fold
     synth, attend = lib.protokv_synthesize, lib.protokv_attend
 

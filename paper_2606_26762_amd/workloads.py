@@ -319,6 +319,13 @@ class DeviceStream:
                 self.labels = coarse[:, r[:, None], c[None, :]].reshape(U, T)
             else:
                 self.labels = torch.randint(lo, C, (U, T), generator=self.gen, device=device)
+                # one seeded CUE_PATCH x CUE_PATCH patch per unit shows cluster 0 in CUE_FRAMES
+                pr = torch.randint(0, wl.grid_h - CUE_PATCH + 1, (U, 1), generator=self.gen, device=device)
+                pc = torch.randint(0, wl.grid_w - CUE_PATCH + 1, (U, 1), generator=self.gen, device=device)
+                pos = torch.arange(T, device=device)[None, :]
+                rows, cols = pos // wl.grid_w, pos % wl.grid_w
+                self.cue_mask = ((rows >= pr) & (rows < pr + CUE_PATCH)
+                                 & (cols >= pc) & (cols < pc + CUE_PATCH))
         else:
             self.labels = None
         if wl.structure == "spatial":
@@ -349,6 +356,8 @@ class DeviceStream:
                 m = self.means + wl.drift * xi / math.sqrt(D)
                 self.means = m / m.norm(dim=-1, keepdim=True)
             lab = self.labels
+            if wl.structure == "cue" and self.frame in CUE_FRAMES:
+                lab = torch.where(self.cue_mask, torch.zeros_like(lab), lab)
         k = torch.gather(self.means, 1, lab[..., None].expand(self.U, T, D))
         k = k + wl.sigma * torch.randn(self.U, T, D, generator=self.gen, device=self.device)
         v = torch.randn(self.U, T, D, generator=self.gen, device=self.device)

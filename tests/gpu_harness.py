@@ -51,6 +51,157 @@ def gpu_config(wl: W.Workload, p: O.Params, streams: int = 1, max_query_tokens=N
         eta=p.eta, lambda_sp=p.lambda_sp, lambda_idle=p.lambda_idle, ridge=p.ridge)
 
 
+def assert_bank_equal(gb, u: int, ob: O.Bank, C: int, where: str, bitwise: bool):
+    """GPU bank rows of unit u (decoded dict) against an oracle Bank."""
+    assert np.array_equal(gb["n"][u].astype(np.int64), ob.n), where + " mass"
+    assert np.array_equal(gb["n_res"][u].astype(np.int64), ob.n_res), where + " n_res"
+    assert np.array_equal(gb["hist_k"][u][:, :, :C].astype(np.int64), ob.hist_k), where + " H^K"
+    assert np.array_equal(gb["hist_v"][u][:, :, :C].astype(np.int64), ob.hist_v), where + " H^V"
+    assert not gb["hist_k"][u][:, :, C:].any()
+    act = ob.n > 0
+    assert np.array_equal(gb["tau"][u][act].astype(np.int64), ob.tau[act]), where + " tau"
+    for name in ("sum_k", "sum_v", "sq_k", "sq_v"):
+        g = gb[name][u][act].astype(np.float64)
+        o = getattr(ob, name)[act].astype(np.float64)
+        err = np.linalg.norm(g - o, axis=1)
+        ref = np.linalg.norm(o, axis=1)
+        assert np.all(err <= STAT_RTOL * ref + 1e-30), f"{where} {name} rel {np.max(err / (ref + 1e-30))}"
+        if bitwise:
+            assert np.array_equal(g, o), f"{where} {name} not bitwise equal"
+    assert np.allclose(gb["mu"][u][act], ob.mu[act], atol=1e-6, rtol=0), where + " mu"
+    assert np.allclose(gb["sigma"][u][act], ob.sigma[act], atol=1e-6, rtol=1e-6), where + " sigma"
+    if bitwise:
+        assert np.array_equal(gb["mu"][u][act], ob.mu[act]) and \
+            np.array_equal(gb["sigma"][u][act], ob.sigma[act]), where + " spatial not bitwise"
+
+
+def bank_from_gpu(gb, u: int, p: O.Params) -> O.Bank:
+    """Oracle Bank holding the GPU's rows of unit u (to re-sync the oracle)."""
+    b = O.Bank(p)
+    b.n = gb["n"][u].astype(np.int64)
+    b.n_res = gb["n_res"][u].astype(np.int64)
+    for name in ("sum_k", "sum_v", "sq_k", "sq_v"):
+        setattr(b, name, gb[name][u].astype(np.float32).copy())
+    b.hist_k = gb["hist_k"][u][:, :, :p.C].astype(np.int64)
+    b.hist_v = gb["hist_v"][u][:, :, :p.C].astype(np.int64)
+    b.mu = gb["mu"][u].astype(np.float32).copy()
+    b.sigma = gb["sigma"][u].astype(np.float32).copy()
+    b.tau = gb["tau"][u].astype(np.int64)
+    return b
+
+
+def check_assign(ga: np.ndarray, res: "O.FoldResult", where: str) -> int:
+    """Assignments equal except near ties; returns the near-tie count."""
+    bad = np.nonzero(ga != res.assign)[0]
+    tie = res.margin < 1e-6
+    if len(bad):
+        assert np.all(tie[bad]), (
+            f"{where}: assignment mismatch at tokens {bad[:8].tolist()} gpu {ga[bad[:8]].tolist()} "
+            f"oracle {res.assign[bad[:8]].tolist()} margins {res.margin[bad[:8]].tolist()}")
+    return int(tie.sum())
+
+
+class Resync:
+    """Full-size run: every unit of every stream on the GPU, frames drawn on
+    the device.  At chosen frames the oracle folds the sampled (stream, unit)
+    pairs starting from the GPU's own pre-fold bank and the evicted frame's
+    bytes, and the result must match the GPU's fold exactly (assignments
+    except near ties; rows bitwise).  The readout check synthesizes from the
+    GPU's bank in the oracle and attends over the sampled units' near window."""
+
+    def __init__(self, wl: W.Workload, sample: Sequence, streams: int = 1, seed: int = 5,
+                 cb_samples: int = 1024, **pkw):
+        import collections
+        import torch
+        self.torch = torch
+        self.wl = wl
+        self.p = oracle_params(wl, **pkw)
+        self.streams = streams
+        self.sample = [tuple(x) for x in sample]          # (stream, unit)
+        self.cb = W.make_codebooks_device(wl, n_streams=streams, samples=cb_samples, iters=8)
+        self.cfg = gpu_config(wl, self.p, streams)
+        self.gpu = pk.ProtoKV(self.cfg, self.cb.reshape(-1, *self.cb.shape[2:]))
+        self.dev = W.DeviceStream(wl, n_streams=streams, seed=seed)
+        self.ring = collections.deque(maxlen=wl.window_frames + 1)
+        self.t = 0
+        self.folds_checked = 0
+        self.near_ties = 0
+        self._sidx = torch.tensor([s for s, _ in self.sample], device="cuda")
+        self._uidx = torch.tensor([u for _, u in self.sample], device="cuda")
+
+    def _sampled(self, x):
+        wl = self.wl
+        xf = x.view(self.streams, wl.units, wl.tokens_per_frame, wl.head_dim)
+        return xf[self._sidx, self._uidx].float().cpu().numpy()
+
+    def step(self, check: bool = False):
+        wl = self.wl
+        k, v = self.dev.next_frame()
+        self.ring.append((self.t, self._sampled(k), self._sampled(v)))
+        evict = self.t >= wl.window_frames
+        streams = sorted({s for s, _ in self.sample})
+        if check and evict:
+            before = {s: self.gpu.read_bank(s) for s in streams}
+        self.gpu.append_frame(list(range(self.streams)), k, v)
+        self.gpu.fold()
+        if check and evict:
+            fe, ke, ve = self.ring[0]
+            assert fe == self.t - wl.window_frames
+            after = {s: self.gpu.read_bank(s) for s in streams}
+            assign = {s: self.gpu.read_assignments(s) for s in streams}
+            for i, (s, u) in enumerate(self.sample):
+                where = f"frame {self.t} stream {s} unit {u}"
+                ob = bank_from_gpu(before[s], u, self.p)
+                res = O.fold_frame(ob, ke[i], ve[i], fe, self.t, self.p, self.cb[s][u])
+                ties = check_assign(assign[s][u], res, where)
+                self.near_ties += ties
+                if np.array_equal(assign[s][u], res.assign):
+                    assert_bank_equal(after[s], u, ob, self.p.C, where, bitwise=True)
+                self.folds_checked += 1
+        self.t += 1
+
+    def check_readout(self, stream: int):
+        """Synthesis (exact rows) and attention (abs 2e-2) of the sampled units of `stream`."""
+        torch, wl = self.torch, self.wl
+        self.gpu.synthesize(stream)
+        gk, gv, gbias = self.gpu.read_pseudo()
+        gb = self.gpu.read_bank(stream)
+        q = self.dev.query()
+        o, lse = self.gpu.attend(stream, q)
+        torch.cuda.synchronize()
+        go, gl = o.float().cpu().numpy(), lse.cpu().numpy()
+        qh = q.float().cpu().numpy()
+        grp = wl.num_q_heads // wl.num_kv_heads
+        near = list(self.ring)[-min(self.t, wl.window_frames):]
+        worst = 0.0
+        for i, (s, u) in enumerate(self.sample):
+            if s != stream:
+                continue
+            ob = bank_from_gpu(gb, u, self.p)
+            ps = O.synthesize(ob, self.cb[s][u], self.p)
+            n = len(ps.keys)
+            assert n == int((ob.n > 0).sum()) * self.p.S
+            assert np.array_equal(gk[u][:n], ps.keys), f"stream {s} unit {u}: pseudo keys differ"
+            assert np.array_equal(gv[u][:n], ps.values), f"stream {s} unit {u}: pseudo values differ"
+            slots = ps.slots[::self.p.S]
+            assert np.allclose(gbias[u][slots], ps.bias[::self.p.S], rtol=1e-6, atol=1e-6)
+            kn = np.concatenate([f[1][i] for f in near])
+            vn = np.concatenate([f[2][i] for f in near])
+            k_ctx = np.concatenate([kn, ps.keys])
+            v_ctx = np.concatenate([vn, ps.values])
+            bias = np.concatenate([np.zeros(len(kn)), ps.bias])
+            l, h = divmod(u, wl.num_kv_heads)
+            heads = list(range(h * grp, (h + 1) * grp))
+            rows = qh[l][:, heads, :].reshape(-1, wl.head_dim)
+            oo, ol = O.attend(rows, k_ctx, v_ctx, bias)
+            d = np.abs(go[l][:, heads].reshape(-1, wl.head_dim) - oo).max()
+            dl = np.abs(gl[l][:, heads].reshape(-1) - ol).max()
+            assert d <= READOUT_ATOL, f"stream {s} unit {u}: readout abs err {d}"
+            assert dl <= LSE_ATOL, f"stream {s} unit {u}: lse abs err {dl}"
+            worst = max(worst, float(d))
+        return worst
+
+
 class Pair:
     """GPU handle over all units of `streams` streams + oracle over sampled units."""
 
@@ -131,29 +282,8 @@ class Pair:
     def check_bank(self, stream: int = 0, bitwise: bool = False):
         gb = self.gpu.read_bank(stream)
         for i, u in enumerate(self.sample):
-            ob = self.oracle[stream].banks[i]
-            where = f"stream {stream} unit {u}"
-            assert np.array_equal(gb["n"][u].astype(np.int64), ob.n), where + " mass"
-            assert np.array_equal(gb["n_res"][u].astype(np.int64), ob.n_res), where + " n_res"
-            C = self.p.C
-            assert np.array_equal(gb["hist_k"][u][:, :, :C].astype(np.int64), ob.hist_k), where + " H^K"
-            assert np.array_equal(gb["hist_v"][u][:, :, :C].astype(np.int64), ob.hist_v), where + " H^V"
-            assert not gb["hist_k"][u][:, :, C:].any()
-            act = ob.n > 0
-            assert np.array_equal(gb["tau"][u][act].astype(np.int64), ob.tau[act]), where + " tau"
-            for name in ("sum_k", "sum_v", "sq_k", "sq_v"):
-                g = gb[name][u][act].astype(np.float64)
-                o = getattr(ob, name)[act].astype(np.float64)
-                err = np.linalg.norm(g - o, axis=1)
-                ref = np.linalg.norm(o, axis=1)
-                assert np.all(err <= STAT_RTOL * ref + 1e-30), f"{where} {name} rel {np.max(err / (ref + 1e-30))}"
-                if bitwise:
-                    assert np.array_equal(g, o), f"{where} {name} not bitwise equal"
-            assert np.allclose(gb["mu"][u][act], ob.mu[act], atol=1e-6, rtol=0), where + " mu"
-            assert np.allclose(gb["sigma"][u][act], ob.sigma[act], atol=1e-6, rtol=1e-6), where + " sigma"
-            if bitwise:
-                assert np.array_equal(gb["mu"][u][act], ob.mu[act]) and \
-                    np.array_equal(gb["sigma"][u][act], ob.sigma[act]), where + " spatial not bitwise"
+            assert_bank_equal(gb, u, self.oracle[stream].banks[i], self.p.C,
+                              f"stream {stream} unit {u}", bitwise)
         return gb
 
     def synthesize(self, stream: int = 0, check: bool = True):
