@@ -65,15 +65,18 @@ __device__ __forceinline__ void token_xy(int j, int gw, int gh, float& x, float&
 
 // Rewrites the screening copy of one slot from its (updated) statistics.
 // sk = this lane's two components (2*lane, 2*lane+1) of sum_k.
-__device__ void refresh_cache(const Dims& dm, float2 sk, const RowMeta& m, size_t slot_index,
+__device__ void refresh_cache(const Dims& dm, float2 sk, const RowMeta& m, size_t unit, int k,
                               const Workspace& ws, int lane) {
+  const size_t slot_index = unit * dm.K + k;
   float nsq = wave_sum(sk.x * sk.x + sk.y * sk.y);
   float inv = nsq > 0.f ? 1.0f / sqrtf(nsq) : 0.f;
   float cx = sk.x * inv, cy = sk.y * inv;
   uint16_t hx = to_bf16(cx), hy = to_bf16(cy);
   uint16_t lx = to_bf16(cx - from_bf16(hx)), ly = to_bf16(cy - from_bf16(hy));
-  reinterpret_cast<uint32_t*>(ws.chat_hi + slot_index * D)[lane] = (uint32_t)hx | ((uint32_t)hy << 16);
-  reinterpret_cast<uint32_t*>(ws.chat_lo + slot_index * D)[lane] = (uint32_t)lx | ((uint32_t)ly << 16);
+  // components 2*lane and 2*lane + 1 are adjacent in the swizzled layout
+  const size_t off = unit * (size_t)cap32(dm.K) * D + chat_offset(k, 2 * lane);
+  *reinterpret_cast<uint32_t*>(ws.chat_hi + off) = (uint32_t)hx | ((uint32_t)hy << 16);
+  *reinterpret_cast<uint32_t*>(ws.chat_lo + off) = (uint32_t)lx | ((uint32_t)ly << 16);
   if (lane == 0) {
     double A = (double)m.sxx + dm.ridge, B = (double)m.sxy, Cc = (double)m.syy + dm.ridge;
     double det = A * Cc - B * B;
@@ -161,7 +164,7 @@ __global__ __launch_bounds__(256) void k_seed(Dims dm, Workspace ws, FoldBatch f
     *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
     ws.assign[unit * dm.T + j] = slot;
   }
-  refresh_cache(dm, kk, m, si, ws, lane);
+  refresh_cache(dm, kk, m, unit, slot, ws, lane);
 }
 
 hipError_t launch_seed(const Dims& dm, const Workspace& ws, const FoldBatch& fb, int max_seed,
@@ -213,68 +216,69 @@ __device__ double exact_cost(const Dims& dm, const uint8_t* keyrow, double knorm
   return cost_from_dot(dm, dot, knorm, n2, kx, ky, row, t_frame);
 }
 
-// Element n of a 4-entry register list (INFINITY / -1 past the end).
-__device__ __forceinline__ float pick4(const float* a, int n) {
-  return n == 0 ? a[0] : n == 1 ? a[1] : n == 2 ? a[2] : n == 3 ? a[3] : INFINITY;
-}
-__device__ __forceinline__ int pick4i(const int* a, int n) {
-  return n == 0 ? a[0] : n == 1 ? a[1] : n == 2 ? a[2] : n == 3 ? a[3] : -1;
-}
-
 // (cost, slot) lexicographic minimum: lower cost, then lower slot.
 __device__ __forceinline__ bool better(double c1, int k1, double c2, int k2) {
   return c1 < c2 || (c1 == c2 && k1 < k2);
 }
 
 // ---------------------------------------------------------------------------
-// Screen + argmin.  Workgroup = one tile of 32 evicted tokens of one unit;
-// its 4 waves split the active slots (slot tiles t = wave, wave + 4, ...)
-// and score them against the 32 tokens with v_mfma_f32_32x32x16_bf16
-// (slots = rows, tokens = columns, unit centres as a hi + lo bf16 split read
-// straight from global memory).  Each lane keeps, for its token, the three
-// smallest lower bounds of the cost (slot ids of the first two) and the
-// smallest upper bound; the lists are merged across the partner lane and the
-// waves.  A token whose bound interval admits a single slot is assigned
-// directly; two candidates are re-scored exactly in float64; three or more
-// send the token to an exact float64 pass over every slot.
+// Screen + argmin.  Workgroup = 64 evicted tokens of one unit (two 32-token
+// columns per lane, keys staged once in LDS); its 4 waves split the slot
+// tiles (t = wave, wave + 4, ...) and score them with v_mfma_f32_32x32x16_bf16 (slots = rows, tokens =
+// columns; unit centres as a hi + lo bf16 split read in MFMA operand order,
+// so each k-step is one contiguous 1 KiB load per wave, and the next tile's
+// loads are in flight during this tile's epilogue).  The float32 epilogue
+// approximates Eq. 1 per (token, slot) with a rigorous bound on its error;
+// each lane keeps, per token, the three smallest approximate costs (slots of
+// the first two) and the largest spatial error term.  A token whose interval
+// admits one slot is assigned directly; two candidates are re-scored exactly
+// in float64; three or more send the token to an exact float64 pass over
+// every slot.  Workgroups are placed so that the tiles of one unit run on the
+// same XCD and share its L2 copy of the centres.
 // ---------------------------------------------------------------------------
 constexpr int SCREEN_TOK = 64;
 
 struct Top3 {
-  float lb1, lb2, lb3;
-  int id1, id2;
-  float ub;
+  float c1, c2, c3;  // three smallest approximate costs
+  int i1, i2;        // slots of c1 and c2
+  float emax;        // largest spatial error term (in units of d_Mah)
 };
 
-__device__ __forceinline__ void top3_push(Top3& a, float lo, int k) {
-  const bool c1 = lo < a.lb1, c2 = lo < a.lb2, c3 = lo < a.lb3;
-  a.lb3 = c2 ? a.lb2 : (c3 ? lo : a.lb3);
-  a.lb2 = c1 ? a.lb1 : (c2 ? lo : a.lb2);
-  a.id2 = c1 ? a.id1 : (c2 ? k : a.id2);
-  a.lb1 = c1 ? lo : a.lb1;
-  a.id1 = c1 ? k : a.id1;
+__device__ __forceinline__ void top3_push(Top3& a, float c, int k) {
+  // slot ids by mask arithmetic (nested selects are otherwise lowered to
+  // divergent branches)
+  const bool lt1 = c < a.c1, lt2 = c < a.c2;
+  const int m1 = -(int)lt1, m2 = -(int)lt2;
+  const int s2 = (k & m2) | (a.i2 & ~m2);
+  a.i2 = (a.i1 & m1) | (s2 & ~m1);
+  a.i1 = (k & m1) | (a.i1 & ~m1);
+  a.c3 = __builtin_amdgcn_fmed3f(c, a.c2, a.c3);
+  a.c2 = __builtin_amdgcn_fmed3f(c, a.c1, a.c2);
+  a.c1 = fminf(a.c1, c);
 }
 
+// b's third cost can only be the union's third smallest (it has two smaller
+// entries of its own, which the pushes already placed).
 __device__ __forceinline__ void top3_merge(Top3& a, const Top3& b) {
-  top3_push(a, b.lb1, b.id1);
-  top3_push(a, b.lb2, b.id2);
-  a.lb3 = fminf(a.lb3, fmaxf(b.lb3, a.lb2));  // b.lb3 can only be a third smallest
-  a.ub = fminf(a.ub, b.ub);
+  top3_push(a, b.c1, b.i1);
+  top3_push(a, b.c2, b.i2);
+  a.c3 = fminf(a.c3, b.c3);
+  a.emax = fmaxf(a.emax, b.emax);
 }
 
-// Scores one slot row against one token column and folds it into the token's
-// running bounds.  The float32 arithmetic only approximates the cost; E0 and
-// the spatial error term bound the distance to the exact value.
+// Approximate cost of one (token, slot) pair folded into the token's running
+// top-3.  a = (mu_x, mu_y, qa, 2 qb), c = (qc, lambda_idle * idle), with c.y =
+// +inf for rows past the active slots.
 __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, float ty, const float4& a,
-                                            const float2& c, int k, bool kok, float lsp, float lsp101,
-                                            float lsp65, float E0, Top3& top) {
+                                            const float2& c, int k, float lsp, Top3& top) {
   const float dx = tx - a.x, dy = ty - a.y;
-  // q = qa dx^2 + 2 qb dx dy + qc dy^2 (qa, qc > 0);
-  // |q - q_exact| <= 16 u (qa dx^2 + |2 qb dx dy| + qc dy^2) =: eq
+  // q = qa dx^2 + 2 qb dx dy + qc dy^2; Sigma + rho I is positive definite,
+  // so |2 qb dx dy| <= qa dx^2 + qc dy^2 = t13 and
+  // |q - q_exact| <= 16 u (t13 + |t2|) <= 33 u t13 =: eq
   const float t13 = fmaf(a.z * dx, dx, (c.x * dy) * dy);
   const float t2 = (a.w * dx) * dy;
   const float q = t13 + t2;
-  const float eq = fmaf(16.0f * U32, t13 + fabsf(t2), 1e-30f);
+  const float eq = fmaf(33.0f * U32, t13, 1e-30f);
   // d = q rsq(max(q, eq)), |d - d_exact| <= eq rsq(max(q, eq)) + 2.5e-7 d
   // (|sqrt a - sqrt b| <= |a - b| / sqrt(max(a, b)) and <= sqrt|a - b|; raw
   // v_rsq_f32 is accurate to ~1 ulp for the normal arguments >= 1e-30 used here)
@@ -282,22 +286,30 @@ __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, flo
   const float rq = __builtin_amdgcn_rsqf(fmaxf(qp, eq));
   const float dd = qp * rq;
   const float cost = fmaf(lsp, dd, fmaf(-dot, invn, c.y));
-  const float e = fmaf(lsp65, dd, fmaf(lsp101, eq * rq, E0));
-  const float lo = kok ? cost - e : INFINITY;
-  const float hi = kok ? cost + e : INFINITY;
-  top.ub = fminf(top.ub, hi);
-  top3_push(top, lo, k);
+  top.emax = fmaxf(top.emax, fmaf(eq, rq, 6.5e-7f * dd));
+  top3_push(top, cost, k);
 }
 
+constexpr int SCREEN_WAVES = 4;
+
 template <int FP32>
-__global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
-  __shared__ float4 s_ma[4][32];   // mu_x, mu_y, qa, 2 qb
-  __shared__ float2 s_mb[4][32];   // qc, lambda_idle * idle
-  __shared__ Top3 s_top[4][SCREEN_TOK];
+__global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
+  // token operands of the workgroup in MFMA B order [token half][k-step][lane]
+  __shared__ bf16x8 s_bk[2][8][64];
+  __shared__ bf16x8 s_bkl[FP32 ? 2 : 1][FP32 ? 8 : 1][64];  // low part of float32 keys
+  __shared__ float s_nsq[SCREEN_WAVES][2][64];                // partial squared key norms
+  __shared__ float4 s_ma[SCREEN_WAVES][32];                   // mu_x, mu_y, qa, 2 qb
+  __shared__ float2 s_mb[SCREEN_WAVES][32];                   // qc, lambda_idle * idle (+inf past the active slots)
+  __shared__ Top3 s_top[SCREEN_WAVES][SCREEN_TOK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int tile = blockIdx.x % tiles_per_unit;
-  const int bu = blockIdx.x / tiles_per_unit;
+  // Workgroups are dealt to the 8 XCDs round-robin; logical block lb runs on
+  // XCD lb / per, so consecutive logical blocks (the tiles of one unit) share
+  // an L2.
+  const int nblk = (int)gridDim.x, per = nblk >> 3, bid = (int)blockIdx.x;
+  const int lb = bid < per * 8 ? (bid & 7) * per + (bid >> 3) : bid;
+  const int tile = lb % tiles_per_unit;
+  const int bu = lb / tiles_per_unit;
   const int b = bu / dm.units, u = bu % dm.units;
   const int N = dm.T;
   const int nseed = fb.nseed[b];
@@ -308,14 +320,42 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
   const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
   const size_t es = FP32 ? 4 : 2;
   const uint8_t* kframe = ws.ring_k + fbase * es;
-
   const int col = lane & 31, half = lane >> 5;
-  // two token columns per lane: tokens tile*64 + col and tile*64 + 32 + col
+  const float lsp = (float)dm.lambda_sp;
+  const float lidle = (float)dm.lambda_idle;
+
+  const int ntiles = (kact + 31) / 32;
+  const size_t K32 = (size_t)cap32(dm.K);
+  const uint16_t* ghi = ws.chat_hi + unit * K32 * D + lane * 8;
+  const uint16_t* glo = ws.chat_lo + unit * K32 * D + lane * 8;
+  const CacheMeta* gmeta = ws.cmeta + unit * dm.K;
+
+  // operands of slot tile t: k-step kk of lane l is 16 contiguous bytes at
+  // ((t * 8 + kk) * 64 + l) * 8 elements; half-0 lanes also fetch their row's meta
+  u16x8 ah[8], al[8];
+  float4 ma = make_float4(0.f, 0.f, 0.f, 0.f);
+  float2 mb = make_float2(0.f, INFINITY);
+  auto load_tile = [&](int t) {
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      ah[kk] = *reinterpret_cast<const u16x8*>(ghi + ((size_t)t * 8 + kk) * 512);
+      al[kk] = *reinterpret_cast<const u16x8*>(glo + ((size_t)t * 8 + kk) * 512);
+    }
+    const int krow = t * 32 + col;
+    ma = make_float4(0.f, 0.f, 0.f, 0.f);
+    mb = make_float2(0.f, INFINITY);
+    if (half == 0 && krow < kact) {
+      const CacheMeta cm = gmeta[krow];
+      ma = make_float4(cm.mu_x, cm.mu_y, cm.qa, 2.0f * cm.qb);
+      mb = make_float2(cm.qc, (t_frame - cm.last_frame) > dm.t_idle ? lidle : 0.f);
+    }
+  };
+  if (wave < ntiles) load_tile(wave);  // in flight while the keys are staged
+
+  // Stage the keys: wave w loads k-steps w, w + 4 of both 32-token halves
+  // (tokens tile*64 + h*32 + col, dims 16 kk + 8 half .. + 8) and its partial norms.
   int jt[2];
   bool vt[2];
-  float invn[2], tx[2], ty[2];
-  bf16x8 bk[2][8];
-  bf16x8 bkl[2][8];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int j = tile * SCREEN_TOK + h * 32 + col;
@@ -325,103 +365,90 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
     const uint8_t* kr = kframe + (size_t)(valid ? j : 0) * D * es;
     float nsq = 0.f;
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const int d0 = kk * 16 + half * 8;
-      if (FP32) {
-        const float4 a0 = *reinterpret_cast<const float4*>(kr + (size_t)d0 * 4);
-        const float4 a1 = *reinterpret_cast<const float4*>(kr + (size_t)(d0 + 4) * 4);
-        float f[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-        u16x8 hh, ll;
+    for (int kk = wave; kk < 8; kk += SCREEN_WAVES) {
+    const int d0 = kk * 16 + half * 8;
+    if (FP32) {
+      const float4 a0 = *reinterpret_cast<const float4*>(kr + (size_t)d0 * 4);
+      const float4 a1 = *reinterpret_cast<const float4*>(kr + (size_t)(d0 + 4) * 4);
+      float f[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      u16x8 hh, ll;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          float x = valid ? f[i] : 0.f;
-          nsq += x * x;
-          uint16_t hb = to_bf16(x);
-          hh[i] = hb;
-          ll[i] = to_bf16(x - from_bf16(hb));
-        }
-        bk[h][kk] = __builtin_bit_cast(bf16x8, hh);
-        bkl[h][kk] = __builtin_bit_cast(bf16x8, ll);
-      } else {
-        u16x8 hh = *reinterpret_cast<const u16x8*>(kr + (size_t)d0 * 2);
-        if (!valid) hh = (u16x8)0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          float x = from_bf16(hh[i]);
-          nsq += x * x;
-        }
-        bk[h][kk] = __builtin_bit_cast(bf16x8, hh);
+      for (int i = 0; i < 8; ++i) {
+        float x = valid ? f[i] : 0.f;
+        nsq += x * x;
+        uint16_t hb = to_bf16(x);
+        hh[i] = hb;
+        ll[i] = to_bf16(x - from_bf16(hb));
       }
+      s_bk[h][kk][lane] = __builtin_bit_cast(bf16x8, hh);
+      s_bkl[FP32 ? h : 0][FP32 ? kk : 0][lane] = __builtin_bit_cast(bf16x8, ll);
+    } else {
+      u16x8 hh = *reinterpret_cast<const u16x8*>(kr + (size_t)d0 * 2);
+      if (!valid) hh = (u16x8)0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        float x = from_bf16(hh[i]);
+        nsq += x * x;
+      }
+      s_bk[h][kk][lane] = __builtin_bit_cast(bf16x8, hh);
     }
-    nsq += __shfl_xor(nsq, 32, 64);
+    }
+    s_nsq[wave][h][lane] = nsq;
+  }
+  __syncthreads();
+  float invn[2], tx[2], ty[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    float nsq = 0.f;
+#pragma unroll
+    for (int w = 0; w < SCREEN_WAVES; ++w) nsq += s_nsq[w][h][col] + s_nsq[w][h][col + 32];
     invn[h] = nsq > 0.f ? 1.0f / sqrtf(nsq) : 0.f;
-    token_xy(valid ? j : 0, dm.grid_w, dm.grid_h, tx[h], ty[h]);
+    token_xy(vt[h] ? jt[h] : 0, dm.grid_w, dm.grid_h, tx[h], ty[h]);
   }
 
-  const float lsp = (float)dm.lambda_sp;
-  const float lidle = (float)dm.lambda_idle;
-  // |cost - cost_exact| <= E0 + lsp (1.01 eq rq + 6.5e-7 d): ECOS for the dot product,
-  // 4e-7 (|cost| + 1) for rounding the assembly, |cost| <= 1 + lsp d + lambda_idle.
-  const float E0 = ECOS + 4e-7f * (2.0f + lidle);
-  const float lsp101 = 1.01f * lsp, lsp65 = 6.5e-7f * lsp;
   Top3 top[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    top[h].lb1 = top[h].lb2 = top[h].lb3 = INFINITY;
-    top[h].id1 = top[h].id2 = -1;
-    top[h].ub = INFINITY;
+    top[h].c1 = top[h].c2 = top[h].c3 = INFINITY;
+    top[h].i1 = top[h].i2 = -1;
+    top[h].emax = 0.f;
   }
 
-  const int ntiles = (kact + 31) / 32;
-  const uint16_t* ghi = ws.chat_hi + unit * dm.K * D;
-  const uint16_t* glo = ws.chat_lo + unit * dm.K * D;
-  const CacheMeta* gmeta = ws.cmeta + unit * dm.K;
-
-  for (int t = wave; t < ntiles; t += 4) {
-    const int krow = t * 32 + col;
-    const bool rok = krow < kact;
+  for (int t = wave; t < ntiles; t += SCREEN_WAVES) {
     if (half == 0) {
-      float4 ma = make_float4(0.f, 0.f, 0.f, 0.f);
-      float2 mb = make_float2(0.f, 0.f);
-      if (rok) {
-        const CacheMeta cm = gmeta[krow];
-        ma = make_float4(cm.mu_x, cm.mu_y, cm.qa, 2.0f * cm.qb);
-        mb = make_float2(cm.qc, (t_frame - cm.last_frame) > dm.t_idle ? lidle : 0.f);
-      }
       s_ma[wave][col] = ma;
       s_mb[wave][col] = mb;
     }
     f32x16 acc0 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     f32x16 acc1 = acc0;
-    const uint16_t* rh = ghi + (size_t)(rok ? krow : 0) * D + half * 8;
-    const uint16_t* rl = glo + (size_t)(rok ? krow : 0) * D + half * 8;
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
-      u16x8 vh = *reinterpret_cast<const u16x8*>(rh + kk * 16);
-      u16x8 vl = *reinterpret_cast<const u16x8*>(rl + kk * 16);
-      if (!rok) { vh = (u16x8)0; vl = (u16x8)0; }
-      const bf16x8 ah = __builtin_bit_cast(bf16x8, vh), al = __builtin_bit_cast(bf16x8, vl);
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bk[0][kk], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bk[1][kk], acc1, 0, 0, 0);
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bk[0][kk], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bk[1][kk], acc1, 0, 0, 0);
+      const bf16x8 xh = __builtin_bit_cast(bf16x8, ah[kk]), xl = __builtin_bit_cast(bf16x8, al[kk]);
+      const bf16x8 b0 = s_bk[0][kk][lane], b1 = s_bk[1][kk][lane];
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, b0, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, b1, acc1, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xl, b0, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xl, b1, acc1, 0, 0, 0);
       if (FP32) {
-        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bkl[0][kk], acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bkl[1][kk], acc1, 0, 0, 0);
+        const bf16x8 c0 = s_bkl[FP32 ? 0 : 0][FP32 ? kk : 0][lane];
+        const bf16x8 c1 = s_bkl[FP32 ? 1 : 0][FP32 ? kk : 0][lane];
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, c0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, c1, acc1, 0, 0, 0);
       }
     }
+    if (t + SCREEN_WAVES < ntiles) load_tile(t + SCREEN_WAVES);  // in flight during the epilogue
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll 4
+#pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int m = (r >> 2) * 8 + half * 4 + (r & 3);
       const float4 a = s_ma[wave][m];
       const float2 c = s_mb[wave][m];
       const int k = t * 32 + m;
-      const bool kok = k < kact;
-      screen_pair(acc0[r], invn[0], tx[0], ty[0], a, c, k, kok, lsp, lsp101, lsp65, E0, top[0]);
-      screen_pair(acc1[r], invn[1], tx[1], ty[1], a, c, k, kok, lsp, lsp101, lsp65, E0, top[1]);
+      screen_pair(acc0[r], invn[0], tx[0], ty[0], a, c, k, lsp, top[0]);
+      screen_pair(acc1[r], invn[1], tx[1], ty[1], a, c, k, lsp, top[1]);
+      if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -432,12 +459,12 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     Top3 o;
-    o.lb1 = __shfl_xor(top[h].lb1, 32, 64);
-    o.lb2 = __shfl_xor(top[h].lb2, 32, 64);
-    o.lb3 = __shfl_xor(top[h].lb3, 32, 64);
-    o.id1 = __shfl_xor(top[h].id1, 32, 64);
-    o.id2 = __shfl_xor(top[h].id2, 32, 64);
-    o.ub = __shfl_xor(top[h].ub, 32, 64);
+    o.c1 = __shfl_xor(top[h].c1, 32, 64);
+    o.c2 = __shfl_xor(top[h].c2, 32, 64);
+    o.c3 = __shfl_xor(top[h].c3, 32, 64);
+    o.i1 = __shfl_xor(top[h].i1, 32, 64);
+    o.i2 = __shfl_xor(top[h].i2, 32, 64);
+    o.emax = __shfl_xor(top[h].emax, 32, 64);
     top3_merge(top[h], o);
     if (half == 0) s_top[wave][h * 32 + col] = top[h];
   }
@@ -447,14 +474,19 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
   const int hsel = wave;
   Top3 tp = s_top[0][hsel * 32 + col];
 #pragma unroll
-  for (int w = 1; w < 4; ++w) top3_merge(tp, s_top[w][hsel * 32 + col]);
+  for (int w = 1; w < SCREEN_WAVES; ++w) top3_merge(tp, s_top[w][hsel * 32 + col]);
   const int j = hsel ? jt[1] : jt[0];
   const bool valid = hsel ? vt[1] : vt[0];
 
-  const float thr = tp.ub + 2e-6f;
-  const int nc = (tp.lb1 <= thr) + (tp.lb2 <= thr) + (tp.lb3 <= thr);
+  // |cost - cost_exact| <= E for every slot: ECOS for the dot product,
+  // 4e-7 (|cost| + 1) for rounding the assembly (|cost| <= 1 + lsp d +
+  // lambda_idle), and lsp * 1.01 * emax for the spatial term.  Slot k can
+  // be the exact argmin only if cost_k - E <= c1 + E.
+  const float E = ECOS + 4e-7f * (2.0f + lidle) + 1.01f * lsp * tp.emax;
+  const float thr = tp.c1 + 2.0f * E + 2e-6f;
+  const int nc = 1 + (tp.c2 <= thr) + (tp.c3 <= thr);
   const bool mine = valid && half == 0;
-  if (mine && nc <= 1) ws.assign[unit * N + j] = tp.id1;
+  if (mine && nc <= 1) ws.assign[unit * N + j] = tp.i1;
   const bool flag = mine && nc >= 2;
 
   // Exact refine of flagged tokens, one token at a time.
@@ -465,7 +497,7 @@ __global__ __launch_bounds__(256) void k_screen(Dims dm, Workspace ws, FoldBatch
     fm &= fm - 1;
     const int jj = __shfl(j, src, 64);
     const int ncc = __shfl(nc, src, 64);
-    const int cand0 = __shfl(tp.id1, src, 64), cand1 = __shfl(tp.id2, src, 64);
+    const int cand0 = __shfl(tp.i1, src, 64), cand1 = __shfl(tp.i2, src, 64);
     const uint8_t* kr = kframe + (size_t)jj * D * es;
     float kxf, kyf;
     token_xy(jj, dm.grid_w, dm.grid_h, kxf, kyf);
@@ -533,9 +565,9 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
   int tpu = (dm.T + SCREEN_TOK - 1) / SCREEN_TOK;
   dim3 grid(fb.n * dm.units * tpu);
   if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_screen<1>, grid, dim3(256), 0, st, dm, ws, fb, tpu);
+    hipLaunchKernelGGL(k_screen<1>, grid, dim3(64 * SCREEN_WAVES), 0, st, dm, ws, fb, tpu);
   else
-    hipLaunchKernelGGL(k_screen<0>, grid, dim3(256), 0, st, dm, ws, fb, tpu);
+    hipLaunchKernelGGL(k_screen<0>, grid, dim3(64 * SCREEN_WAVES), 0, st, dm, ws, fb, tpu);
   return hipGetLastError();
 }
 
@@ -626,15 +658,19 @@ hipError_t launch_pq_encode(const Dims& dm, const Workspace& ws, const FoldBatch
 
 // ---------------------------------------------------------------------------
 // Aggregation.  One wave per slot; the four waves of a workgroup are
-// independent (no LDS, no barriers).  A wave finds its slot's tokens with
-// ballots over the assignment vector and, if any, updates the slot's row in
-// registers with the tokens in eviction order: lane l holds components
-// 2l, 2l+1 of the four sums and histogram bins 2l, 2l+1 (subspace l/8,
-// codewords 2(l%8), 2(l%8)+1).  Then it writes the row back and refreshes the
-// slot's screening copy.
+// independent (no barriers across waves).  A wave finds its slot's tokens with
+// ballots over the assignment vector, compacts them (eviction order) into its
+// LDS list and, if any, updates the slot's row in registers: tokens are taken
+// in batches of 8 whose K, V and codes are loaded together, then absorbed
+// one by one in order.  Lane l holds components 2l, 2l+1 of the four sums and
+// histogram bins 2l, 2l+1 (subspace l/8, codewords 2(l%8), 2(l%8)+1).  Then
+// it writes the row back and refreshes the slot's screening copy.
 // ---------------------------------------------------------------------------
+constexpr int AGG_BATCH = 8;
+
 template <int FP32>
 __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int chunks_per_unit) {
+  __shared__ uint16_t s_tok[4][TMAX];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int chunk = blockIdx.x % chunks_per_unit;
   const int bu = blockIdx.x / chunks_per_unit;
@@ -648,19 +684,23 @@ __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBa
   const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
   const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
 
-  unsigned long long masks[TMAX / 64];
-  bool any = false;
+  // this slot's tokens, in eviction order
+  const unsigned long long below = (1ull << lane) - 1ull;
+  int ntok = 0;
 #pragma unroll
   for (int c = 0; c < TMAX / 64; ++c) {
-    masks[c] = 0ull;
     if (c * 64 < N) {
       const int jj = c * 64 + lane;
       const int a = (jj < N && jj >= nseed) ? ws.assign[unit * N + jj] : -1;
-      masks[c] = __ballot(a == k);
-      any |= masks[c] != 0ull;
+      const unsigned long long mk = __ballot(a == k);
+      if (a == k) s_tok[wave][ntok + __popcll(mk & below)] = (uint16_t)jj;
+      ntok += __popcll(mk);
     }
   }
-  if (!any) return;  // untouched slot
+  if (ntok == 0) return;  // untouched slot
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
   const size_t si = unit * dm.K + k;
   uint8_t* row = ws.bank + si * ROW;
@@ -673,26 +713,39 @@ __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBa
   RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
   const float eta = dm.eta, keep = 1.0f - dm.eta;
   const int gl = lane >> 3, c0 = 2 * (lane & 7);
+  for (int i0 = 0; i0 < ntok; i0 += AGG_BATCH) {
+    int jb[AGG_BATCH];
+    float2 kb[AGG_BATCH], vb[AGG_BATCH];
+    int zk[AGG_BATCH], zv[AGG_BATCH];
 #pragma unroll
-  for (int c = 0; c < TMAX / 64; ++c) {
-    unsigned long long mk = masks[c];
-    while (mk) {
-      const int bit = __ffsll((long long)mk) - 1;
-      mk &= mk - 1;
-      const int jj = c * 64 + bit;
-      const float2 kk = load2<FP32>(ws.ring_k, fbase + (size_t)jj * D + 2 * lane);
-      const float2 vv = load2<FP32>(ws.ring_v, fbase + (size_t)jj * D + 2 * lane);
+    for (int q = 0; q < AGG_BATCH; ++q) {
+      jb[q] = i0 + q < ntok ? (int)s_tok[wave][i0 + q] : -1;  // uniform
+      kb[q] = vb[q] = make_float2(0.f, 0.f);
+      zk[q] = zv[q] = 0;
+      if (jb[q] >= 0) {
+        kb[q] = load2<FP32>(ws.ring_k, fbase + (size_t)jb[q] * D + 2 * lane);
+        vb[q] = load2<FP32>(ws.ring_v, fbase + (size_t)jb[q] * D + 2 * lane);
+        if (pq) {
+          const uint8_t* cz = ws.codes + (unit * N + jb[q]) * (2 * G);
+          zk[q] = cz[gl];
+          zv[q] = cz[G + gl];
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < AGG_BATCH; ++q) {
+      if (jb[q] < 0) break;
+      const int jj = jb[q];
+      const float2 kk = kb[q], vv = vb[q];
       sk.x = sk.x + kk.x; sk.y = sk.y + kk.y;
       sv.x = sv.x + vv.x; sv.y = sv.y + vv.y;
       qk.x = qk.x + kk.x * kk.x; qk.y = qk.y + kk.y * kk.y;
       qv.x = qv.x + vv.x * vv.x; qv.y = qv.y + vv.y * vv.y;
       if (pq) {
-        const uint8_t* cz = ws.codes + (unit * N + jj) * (2 * G);
-        const int zk = cz[gl], zv = cz[G + gl];
-        hk.x += (zk == c0) ? 1u : 0u;
-        hk.y += (zk == c0 + 1) ? 1u : 0u;
-        hv.x += (zv == c0) ? 1u : 0u;
-        hv.y += (zv == c0 + 1) ? 1u : 0u;
+        hk.x += (zk[q] == c0) ? 1u : 0u;
+        hk.y += (zk[q] == c0 + 1) ? 1u : 0u;
+        hv.x += (zv[q] == c0) ? 1u : 0u;
+        hv.y += (zv[q] == c0 + 1) ? 1u : 0u;
         m.n_res += 1;
       }
       float sx, sy;
@@ -716,7 +769,7 @@ __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBa
   reinterpret_cast<uint2*>(row + ROW_HK)[lane] = hk;
   reinterpret_cast<uint2*>(row + ROW_HV)[lane] = hv;
   if (lane == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
-  refresh_cache(dm, sk, m, si, ws, lane);
+  refresh_cache(dm, sk, m, unit, k, ws, lane);
   // per-slot count of folds that touched it (owned by this wave: no atomics)
   if (lane == 0) ws.touched[si] += 1u;
 }

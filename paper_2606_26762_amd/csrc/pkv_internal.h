@@ -53,12 +53,22 @@ struct Dims {
   int max_splits;  // attention context splits (partials storage)
 };
 
+// Screening copy of the unit centres, stored in the operand order of
+// v_mfma_f32_32x32x16_bf16 so that one wave reads 1 KiB contiguous per
+// k-step: slot k of a unit sits in slot tile k / 32 at column k % 32; element
+// d in k-step d / 16, lane (d / 8 % 2) * 32 + k % 32, position d % 8.
+// Capacity is padded to K32 = 32 * ceil(K / 32) slots per unit.
+__host__ __device__ inline int cap32(int K) { return (K + 31) & ~31; }
+__host__ __device__ inline size_t chat_offset(int k, int d) {
+  return ((((size_t)(k >> 5) * 8 + (d >> 4)) * 64 + ((d >> 3) & 1) * 32 + (k & 31)) * 8) + (d & 7);
+}
+
 // Device pointers into the caller's workspace.
 struct Workspace {
   uint8_t* ring_k;            // [streams][units][W+1][T][D] kv dtype
   uint8_t* ring_v;
   uint8_t* bank;              // [streams][units][K] rows of ROW bytes
-  uint16_t* chat_hi;          // [streams][units][K][D] bf16 bits
+  uint16_t* chat_hi;          // [streams][units][K32 / 32][8][64][8] bf16 bits (chat_offset)
   uint16_t* chat_lo;
   CacheMeta* cmeta;           // [streams][units][K]
   int32_t* assign;            // [streams][units][T]

@@ -53,8 +53,9 @@ Layout make_layout(const protokv_config& c) {
   ly.ring_k = take(U * (c.window_frames + 1) * T * D * es);
   ly.ring_v = take(U * (c.window_frames + 1) * T * D * es);
   ly.bank = take(U * K * ROW);
-  ly.chat_hi = take(U * K * D * 2);
-  ly.chat_lo = take(U * K * D * 2);
+  const size_t K32 = (size_t)cap32(c.capacity);
+  ly.chat_hi = take(U * K32 * D * 2);
+  ly.chat_lo = take(U * K32 * D * 2);
   ly.cmeta = take(U * K * sizeof(CacheMeta));
   ly.assign = take(U * T * 4);
   ly.codes = take(U * T * 2 * G);
