@@ -95,32 +95,45 @@ __device__ void refresh_cache(const Dims& dm, float2 sk, const RowMeta& m, size_
 
 // ---------------------------------------------------------------------------
 // Near ring insert: frame -> ring slot (f mod (W+1)) of each listed stream.
+// Workgroup = one quarter of one (batch entry, unit): its frame of K and of V
+// is one contiguous block on both sides, copied 16 bytes per thread with eight
+// loads in flight before the stores.
+constexpr int RING_PARTS = 4;
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_ring_insert(Dims dm, Workspace ws, AppendBatch ab,
                                                      const uint8_t* k, const uint8_t* v,
-                                                     size_t unit_bytes, size_t chunks_per_entry) {
-  const size_t total = chunks_per_entry * (size_t)ab.n;
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total;
-       i += (size_t)gridDim.x * blockDim.x) {
-    int e = (int)(i / chunks_per_entry);
-    size_t off = (i % chunks_per_entry) * 16;
-    size_t unit = off / unit_bytes, within = off % unit_bytes;
-    size_t dst = (((size_t)ab.sid[e] * dm.units + unit) * (dm.W + 1) + ab.slot[e]) * unit_bytes + within;
-    size_t src = (size_t)e * chunks_per_entry * 16 + off;
-    *reinterpret_cast<uint4*>(ws.ring_k + dst) = *reinterpret_cast<const uint4*>(k + src);
-    *reinterpret_cast<uint4*>(ws.ring_v + dst) = *reinterpret_cast<const uint4*>(v + src);
+                                                     size_t unit_bytes) {
+  const int part = blockIdx.x % RING_PARTS, eu = blockIdx.x / RING_PARTS;
+  const int e = eu / dm.units, unit = eu % dm.units;
+  const size_t dst = (((size_t)ab.sid[e] * dm.units + unit) * (dm.W + 1) + ab.slot[e]) * unit_bytes;
+  const size_t src = ((size_t)e * dm.units + unit) * unit_bytes;
+  const uint4* ks = reinterpret_cast<const uint4*>(k + src);
+  const uint4* vs = reinterpret_cast<const uint4*>(v + src);
+  uint4* kd = reinterpret_cast<uint4*>(ws.ring_k + dst);
+  uint4* vd = reinterpret_cast<uint4*>(ws.ring_v + dst);
+  const int n16 = (int)(unit_bytes / 16);
+  const int per = (n16 + RING_PARTS - 1) / RING_PARTS;
+  const int lo = part * per, n = min(n16, lo + per);
+  int i = lo + threadIdx.x;
+  for (; i + 3 * 256 < n; i += 4 * 256) {
+    const uint4 a0 = ks[i], a1 = ks[i + 256], a2 = ks[i + 512], a3 = ks[i + 768];
+    const uint4 c0 = vs[i], c1 = vs[i + 256], c2 = vs[i + 512], c3 = vs[i + 768];
+    kd[i] = a0; kd[i + 256] = a1; kd[i + 512] = a2; kd[i + 768] = a3;
+    vd[i] = c0; vd[i + 256] = c1; vd[i + 512] = c2; vd[i + 768] = c3;
+  }
+  for (; i < n; i += 256) {
+    const uint4 a0 = ks[i], c0 = vs[i];
+    kd[i] = a0;
+    vd[i] = c0;
   }
 }
 
 hipError_t launch_ring_insert(const Dims& dm, const Workspace& ws, const AppendBatch& ab,
                               const void* k, const void* v, hipStream_t st) {
   size_t es = dm.kv_fp32 ? 4 : 2;
-  size_t unit_bytes = (size_t)dm.T * D * es;
-  size_t chunks = unit_bytes * dm.units / 16;
-  size_t total = chunks * ab.n;
-  int blocks = (int)std::min<size_t>((total + 255) / 256, 8192);
-  hipLaunchKernelGGL(k_ring_insert, dim3(blocks), dim3(256), 0, st, dm, ws, ab,
-                     (const uint8_t*)k, (const uint8_t*)v, unit_bytes, chunks);
+  size_t unit_bytes = (size_t)dm.T * D * es;   // a multiple of 256
+  hipLaunchKernelGGL(k_ring_insert, dim3(ab.n * dm.units * RING_PARTS), dim3(256), 0, st, dm, ws, ab,
+                     (const uint8_t*)k, (const uint8_t*)v, unit_bytes);
   return hipGetLastError();
 }
 
@@ -152,6 +165,9 @@ __global__ __launch_bounds__(256) void k_seed(Dims dm, Workspace ws, FoldBatch f
   reinterpret_cast<float2*>(row + ROW_SQV)[lane] = make_float2(vv.x * vv.x, vv.y * vv.y);
   reinterpret_cast<uint2*>(row + ROW_HK)[lane] = make_uint2(0, 0);
   reinterpret_cast<uint2*>(row + ROW_HV)[lane] = make_uint2(0, 0);
+  // centres sum / 1 of the seeded slot
+  reinterpret_cast<float2*>(ws.cent + si * 2 * D)[lane] = kk;
+  reinterpret_cast<float2*>(ws.cent + (si * 2 + 1) * D)[lane] = vv;
   RowMeta m;
   m.n = 1;
   m.n_res = 0;
@@ -486,7 +502,11 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
   const float thr = tp.c1 + 2.0f * E + 2e-6f;
   const int nc = 1 + (tp.c2 <= thr) + (tp.c3 <= thr);
   const bool mine = valid && half == 0;
-  if (mine && nc <= 1) ws.assign[unit * N + j] = tp.i1;
+  const uint32_t tag = (uint32_t)fb.fe[b] + 1u;
+  if (mine && nc <= 1) {
+    ws.assign[unit * N + j] = tp.i1;
+    ws.tgen[unit * dm.K + tp.i1] = tag;  // same value from every writer
+  }
   const bool flag = mine && nc >= 2;
 
   // Exact refine of flagged tokens, one token at a time.
@@ -549,6 +569,7 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
     }
     if (lane == 0) {
       ws.assign[unit * N + jj] = k1;
+      ws.tgen[unit * dm.K + k1] = tag;
       n_ref += 1;
       n_full += ncc > 2 ? 1 : 0;
       n_tie += (c2 - c1) < NEAR_TIE ? 1 : 0;
@@ -572,102 +593,226 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
 }
 
 // ---------------------------------------------------------------------------
-// PQ residual encoding of the assigned tokens.  Workgroup = 32 tokens of one
-// unit, one thread per (token, K/V, subspace): residual to the slot's centre
-// before this fold (float32 sum / n), then the nearest codeword,
-// dist(c) = sum_u (r_u - C[c][u])^2 accumulated in float32 with u ascending
-// (16 codewords side by side); ties go to the lower codeword.  Codebooks are
-// staged in LDS with each (K/V, subspace) block padded by 4 floats so the
-// 16 blocks a wave reads at once fall in different banks.
+// PQ residual encoding of the assigned tokens.  The code of subspace g is the
+// nearest codeword to r = x - c (c = float32(sum / n) before this fold,
+// stored by the previous fold), defined by the float32 sequential distance
+// dist(c) = sum_u (r_u - C[c][u])^2 (u ascending, one rounding per subtract,
+// multiply and add; ties to the lower codeword).  It is found as
+// argmax_c (r . C_c - |C_c|^2 / 2) on MFMA with a rigorous error bound; a
+// subspace whose best two scores are not separated by the bound is decided by
+// the sequential float32 distances themselves.
+//
+// Workgroup = 64 tokens of one unit; wave w takes the 32-token block w / 2 of
+// K (w even) or V, with every load issued up front (no LDS, no barriers;
+// |C|^2 / 2 and max |C| per codebook come precomputed from init).  For subspaces g0 = 2p, g1 = 2p + 1, v_mfma_f32_32x32x16_bf16
+// multiplies A = codebook rows (rows 0-15: C[g0], rows 16-31: C[g1]; block
+// diagonal over two k-steps) by B = residual dims (k-step 0: g0, 1: g1), both
+// split into hi + lo bf16 (hi*hi + hi*lo + lo*hi), starting from -|C|^2 / 2.
 // ---------------------------------------------------------------------------
-constexpr int PQ_TOK = 32;
-constexpr int CB_BLOCK = CMAX * DP + 4;
+constexpr int PQ_TOK = 64;
+constexpr int CBW = CMAX * DP;  // floats per (K/V, subspace) codebook block
+
+// v -> hi + lo with hi = bf16(v), lo = bf16(v - hi), both round to nearest even
+__device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const __bf16 h = (__bf16)v[i];
+    hi[i] = h;
+    lo[i] = (__bf16)(v[i] - (float)h);
+  }
+}
 
 template <int FP32>
-__global__ __launch_bounds__(512) void k_pq_encode(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
-  __shared__ __attribute__((aligned(16))) float s_cb[2 * G * CB_BLOCK];
-  const int tid = threadIdx.x;
+__global__ __launch_bounds__(256) void k_pq_encode(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int tile = blockIdx.x % tiles_per_unit;
   const int bu = blockIdx.x / tiles_per_unit;
   const int b = bu / dm.units, u = bu % dm.units;
   const int N = dm.T;
   const int nseed = fb.nseed[b];
   const int jlo = max(nseed, tile * PQ_TOK), jhi = min(N, tile * PQ_TOK + PQ_TOK);
-  if (jlo >= jhi) return;  // uniform
+  const int blk = wave >> 1, kv = wave & 1;
+  const int jb0 = tile * PQ_TOK + blk * 32;
+  if (jb0 >= jhi || jb0 + 32 <= jlo) return;  // uniform per wave
   const size_t unit = (size_t)fb.sid[b] * dm.units + u;
-  {
-    const float4* src = reinterpret_cast<const float4*>(ws.codebooks + unit * (2 * G * CMAX * DP));
-    for (int i = tid; i < 2 * G * CMAX * DP / 4; i += 512) {
-      const int blk = i / (CMAX * DP / 4), within = i % (CMAX * DP / 4);
-      *reinterpret_cast<float4*>(s_cb + blk * CB_BLOCK + within * 4) = src[i];
+  const int col = lane & 31, half = lane >> 5;
+  const int j = jb0 + col;
+  const bool valid = j >= jlo && j < jhi;
+  const size_t ub = unit * 2 + kv;
+  const float* cbk = ws.codebooks + ub * G * CBW;
+  const float* hnp = ws.cbhn + ub * G * CMAX;
+  const float* cmx = ws.cbmax + ub * G;
+  const int slot = valid ? ws.assign[unit * N + j] : 0;
+  const size_t es = FP32 ? 4 : 2;
+  const uint8_t* xr = (kv ? ws.ring_v : ws.ring_k) +
+                      ((((unit * (dm.W + 1) + fb.slot[b]) * N) + (size_t)(valid ? j : 0)) * D) * es;
+  uint8_t* codes = ws.codes + (unit * N + (valid ? j : 0)) * (2 * G) + kv * G;
+
+  // this lane's half (dims g*16 + half*8 .. +7) of every subspace of its token
+  float r[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int d0 = g * DP + half * 8;
+    if (FP32) {
+      *reinterpret_cast<float4*>(&r[g][0]) = *reinterpret_cast<const float4*>(xr + (size_t)d0 * 4);
+      *reinterpret_cast<float4*>(&r[g][4]) = *reinterpret_cast<const float4*>(xr + (size_t)(d0 + 4) * 4);
+    } else {
+      const u16x8 h = *reinterpret_cast<const u16x8*>(xr + (size_t)d0 * 2);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) r[g][i] = from_bf16(h[i]);
     }
   }
-  __syncthreads();
-  const int jj = tile * PQ_TOK + (tid >> 4), kvg = tid & 15, kv = kvg >> 3, g = kvg & 7;
-  if (jj < jlo || jj >= jhi) return;
-  const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
-  const int k = ws.assign[unit * N + jj];
-  const uint8_t* row = ws.bank + (unit * dm.K + k) * ROW;
-  const float nf = (float)reinterpret_cast<const RowMeta*>(row + ROW_META)->n;
-  const float* sums = reinterpret_cast<const float*>(row + (kv ? ROW_SUMV : ROW_SUMK)) + g * DP;
-  const uint8_t* xb = kv ? ws.ring_v : ws.ring_k;
-  float r[DP];
+  // A operand rows: row col < 16 holds C[2p][col][half*8 ..] (k-step 0 of pair p),
+  // row >= 16 holds C[2p+1][col-16][half*8 ..] (k-step 1)
+  float w[G / 2][8];
 #pragma unroll
-  for (int q = 0; q < DP; q += 2) {
-    const float2 x = load2<FP32>(xb, fbase + (size_t)jj * D + g * DP + q);
-    const float2 sm = *reinterpret_cast<const float2*>(sums + q);
-    r[q] = x.x - sm.x / nf;
-    r[q + 1] = x.y - sm.y / nf;
+  for (int p = 0; p < G / 2; ++p) {
+    const float* wa = cbk + (2 * p + (col < 16 ? 0 : 1)) * CBW + (col & 15) * DP + half * 8;
+    *reinterpret_cast<float4*>(&w[p][0]) = *reinterpret_cast<const float4*>(wa);
+    *reinterpret_cast<float4*>(&w[p][4]) = *reinterpret_cast<const float4*>(wa + 4);
   }
-  const float* cb = s_cb + kvg * CB_BLOCK;   // [c][u]
-  float acc[CMAX];
+  const float* cen = ws.cent + ((unit * dm.K + slot) * 2 + kv) * D;
 #pragma unroll
-  for (int c = 0; c < CMAX; ++c) acc[c] = 0.f;
+  for (int g = 0; g < G; ++g) {
+    const int d0 = g * DP + half * 8;
+    const float4 c0 = *reinterpret_cast<const float4*>(cen + d0);
+    const float4 c1 = *reinterpret_cast<const float4*>(cen + d0 + 4);
+    const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
 #pragma unroll
-  for (int q = 0; q < DP; q += 4) {
+    for (int i = 0; i < 8; ++i) r[g][i] = valid ? r[g][i] - cc[i] : 0.f;
+  }
+  const bf16x8 zero8 = {};
+  const bool lowrows = col < 16;
+
 #pragma unroll
-    for (int c = 0; c < CMAX; ++c) {
-      const float4 w = *reinterpret_cast<const float4*>(cb + c * DP + q);
-      float d0 = r[q] - w.x;
-      acc[c] = acc[c] + d0 * d0;
-      float d1 = r[q + 1] - w.y;
-      acc[c] = acc[c] + d1 * d1;
-      float d2 = r[q + 2] - w.z;
-      acc[c] = acc[c] + d2 * d2;
-      float d3 = r[q + 3] - w.w;
-      acc[c] = acc[c] + d3 * d3;
+  for (int p = 0; p < G / 2; ++p) {
+    const int g0 = 2 * p, g1 = 2 * p + 1;
+    bf16x8 ah, al, b0h, b0l, b1h, b1l;
+    split8(w[p], ah, al);
+    split8(r[g0], b0h, b0l);
+    split8(r[g1], b1h, b1l);
+    const bf16x8 a0h = lowrows ? ah : zero8, a0l = lowrows ? al : zero8;
+    const bf16x8 a1h = lowrows ? zero8 : ah, a1l = lowrows ? zero8 : al;
+    float n0 = 0.f, n1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      n0 = fmaf(r[g0][i], r[g0][i], n0);
+      n1 = fmaf(r[g1][i], r[g1][i], n1);
     }
-  }
-  int bc = 0;
-  float best = acc[0];
+    // accumulator rows (rr / 4) * 8 + half * 4 + rr % 4: rr < 8 -> codeword of g0, else of g1
+    f32x16 acc;
 #pragma unroll
-  for (int c = 1; c < CMAX; ++c)
-    if (c < dm.C && acc[c] < best) { best = acc[c]; bc = c; }
-  ws.codes[(unit * N + jj) * (2 * G) + kvg] = (uint8_t)bc;
+    for (int q = 0; q < 4; ++q) {
+      const float4 h = *reinterpret_cast<const float4*>(hnp + (q < 2 ? g0 : g1) * CMAX + (q & 1) * 8 + half * 4);
+      acc[4 * q + 0] = -h.x;
+      acc[4 * q + 1] = -h.y;
+      acc[4 * q + 2] = -h.z;
+      acc[4 * q + 3] = -h.w;
+    }
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0h, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0l, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0l, b0h, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1h, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1l, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1l, b1h, acc, 0, 0, 0);
+
+    // best two scores per subspace: 8 codewords here, 8 in the partner lane
+    float bst1[2], bst2[2];
+    int bid[2];
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      float v1 = -INFINITY, v2 = -INFINITY;
+      int i1 = 0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float v = acc[sub * 8 + q];
+        const int cw = (q >> 2) * 8 + half * 4 + (q & 3);
+        const int mk = -(int)(v > v1);
+        v2 = __builtin_amdgcn_fmed3f(v, v1, v2);
+        v1 = fmaxf(v1, v);
+        i1 = (cw & mk) | (i1 & ~mk);
+      }
+      const float o1 = __shfl_xor(v1, 32, 64), o2 = __shfl_xor(v2, 32, 64);
+      const int oi = __shfl_xor(i1, 32, 64);
+      const bool take = o1 > v1 || (o1 == v1 && oi < i1);
+      bst2[sub] = fmaxf(fminf(v1, o1), fmaxf(v2, o2));
+      bst1[sub] = fmaxf(v1, o1);
+      bid[sub] = take ? oi : i1;
+    }
+    // lane half 0 settles g0, half 1 settles g1
+    const int g = half ? g1 : g0;
+    const float v1 = half ? bst1[1] : bst1[0], v2 = half ? bst2[1] : bst2[0];
+    float rn2 = half ? n1 : n0;
+    rn2 += __shfl_xor(half ? n0 : n1, 32, 64);  // the partner's half of subspace g
+    // |score - exact| <= F for every codeword: split error of the MFMA dot
+    // (3 * 2^-18 |r| |C|), its float32 accumulation over three MFMAs
+    // (<= 51 u (|C|^2 / 2 + |r| |C|)) and the rounding of the sequential
+    // float32 distance of the two leading codewords (<= 18 u D / 2 with
+    // D = |r|^2 - 2 score), each taken with margin
+    const float rn = sqrtf(rn2) * 1.0001f, cm = cmx[g];
+    const float dlead = fmaxf(rn * rn - 2.0f * v2, 0.f) + 1e-30f;
+    const float F = fmaf(1.6e-5f * rn, cm, fmaf(2.5e-6f, cm * cm, 1e-6f * dlead));
+    int z = half ? bid[1] : bid[0];
+    // not separated: the float32 sequential distances decide, one flagged
+    // (token, subspace) at a time for the whole wave (lane % 16 = codeword)
+    unsigned long long fm = __ballot(valid && !(v1 - v2 > 2.0f * F));
+    while (fm) {
+      const int src = __ffsll((long long)fm) - 1;
+      fm &= fm - 1;
+      const int gs = (src >> 5) ? g1 : g0;   // uniform
+      const int tc = src & 31;
+      float rr[DP];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float mine = (gs == g0) ? r[g0][i] : r[g1][i];
+        rr[i] = __shfl(mine, tc, 64);
+        rr[8 + i] = __shfl(mine, tc + 32, 64);
+      }
+      const int cw = lane & 15;
+      const float* wc = cbk + gs * CBW + cw * DP;
+      float a = 0.f;
+#pragma unroll
+      for (int q = 0; q < DP; ++q) {
+        const float d = rr[q] - wc[q];
+        a = a + d * d;
+      }
+      if (cw >= dm.C) a = INFINITY;
+      int ai = cw;
+#pragma unroll
+      for (int o = 8; o >= 1; o >>= 1) {
+        const float oa = __shfl_xor(a, o, 64);
+        const int oi = __shfl_xor(ai, o, 64);
+        const bool take = oa < a || (oa == a && oi < ai);
+        a = take ? oa : a;
+        ai = take ? oi : ai;
+      }
+      if (lane == src) z = ai;
+    }
+    if (valid) codes[g] = (uint8_t)z;
+  }
 }
 
 hipError_t launch_pq_encode(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
   int tpu = (dm.T + PQ_TOK - 1) / PQ_TOK;
   dim3 grid(fb.n * dm.units * tpu);
   if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_pq_encode<1>, grid, dim3(512), 0, st, dm, ws, fb, tpu);
+    hipLaunchKernelGGL(k_pq_encode<1>, grid, dim3(256), 0, st, dm, ws, fb, tpu);
   else
-    hipLaunchKernelGGL(k_pq_encode<0>, grid, dim3(512), 0, st, dm, ws, fb, tpu);
+    hipLaunchKernelGGL(k_pq_encode<0>, grid, dim3(256), 0, st, dm, ws, fb, tpu);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // Aggregation.  One wave per slot; the four waves of a workgroup are
-// independent (no barriers across waves).  A wave finds its slot's tokens with
-// ballots over the assignment vector, compacts them (eviction order) into its
-// LDS list and, if any, updates the slot's row in registers: tokens are taken
-// in batches of 8 whose K, V and codes are loaded together, then absorbed
-// one by one in order.  Lane l holds components 2l, 2l+1 of the four sums and
+// independent.  A slot the screen did not tag in this fold exits after one
+// load.  Otherwise the wave compacts its tokens (eviction order) into its LDS
+// list with ballots over the assignment vector and updates the row in
+// registers, loading the next token's K, V and codes while it absorbs the
+// current one.  Lane l holds components 2l, 2l+1 of the four sums and
 // histogram bins 2l, 2l+1 (subspace l/8, codewords 2(l%8), 2(l%8)+1).  Then
-// it writes the row back and refreshes the slot's screening copy.
+// it writes the row back, stores the new centres and refreshes the slot's
+// screening copy.
 // ---------------------------------------------------------------------------
-constexpr int AGG_BATCH = 8;
-
 template <int FP32>
 __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int chunks_per_unit) {
   __shared__ uint16_t s_tok[4][TMAX];
@@ -681,28 +826,26 @@ __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBa
   const int k = chunk * 4 + wave;
   if (nseed >= N || k >= kact) return;  // uniform per wave
   const size_t unit = (size_t)fb.sid[b] * dm.units + u;
+  const size_t si = unit * dm.K + k;
+  if (ws.tgen[si] != (uint32_t)fb.fe[b] + 1u) return;  // no token this fold
   const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
   const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
 
   // this slot's tokens, in eviction order
   const unsigned long long below = (1ull << lane) - 1ull;
   int ntok = 0;
-#pragma unroll
-  for (int c = 0; c < TMAX / 64; ++c) {
-    if (c * 64 < N) {
-      const int jj = c * 64 + lane;
-      const int a = (jj < N && jj >= nseed) ? ws.assign[unit * N + jj] : -1;
-      const unsigned long long mk = __ballot(a == k);
-      if (a == k) s_tok[wave][ntok + __popcll(mk & below)] = (uint16_t)jj;
-      ntok += __popcll(mk);
-    }
+  for (int c = 0; c * 64 < N; ++c) {
+    const int jj = c * 64 + lane;
+    const int a = (jj < N && jj >= nseed) ? ws.assign[unit * N + jj] : -1;
+    const unsigned long long mk = __ballot(a == k);
+    if (a == k) s_tok[wave][ntok + __popcll(mk & below)] = (uint16_t)jj;
+    ntok += __popcll(mk);
   }
-  if (ntok == 0) return;  // untouched slot
+  if (ntok == 0) return;  // uniform; a tagged slot always has a token
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-  const size_t si = unit * dm.K + k;
   uint8_t* row = ws.bank + si * ROW;
   float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
   float2 sv = reinterpret_cast<const float2*>(row + ROW_SUMV)[lane];
@@ -713,54 +856,51 @@ __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBa
   RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
   const float eta = dm.eta, keep = 1.0f - dm.eta;
   const int gl = lane >> 3, c0 = 2 * (lane & 7);
-  for (int i0 = 0; i0 < ntok; i0 += AGG_BATCH) {
-    int jb[AGG_BATCH];
-    float2 kb[AGG_BATCH], vb[AGG_BATCH];
-    int zk[AGG_BATCH], zv[AGG_BATCH];
-#pragma unroll
-    for (int q = 0; q < AGG_BATCH; ++q) {
-      jb[q] = i0 + q < ntok ? (int)s_tok[wave][i0 + q] : -1;  // uniform
-      kb[q] = vb[q] = make_float2(0.f, 0.f);
-      zk[q] = zv[q] = 0;
-      if (jb[q] >= 0) {
-        kb[q] = load2<FP32>(ws.ring_k, fbase + (size_t)jb[q] * D + 2 * lane);
-        vb[q] = load2<FP32>(ws.ring_v, fbase + (size_t)jb[q] * D + 2 * lane);
-        if (pq) {
-          const uint8_t* cz = ws.codes + (unit * N + jb[q]) * (2 * G);
-          zk[q] = cz[gl];
-          zv[q] = cz[G + gl];
-        }
-      }
+  auto fetch = [&](int jj, float2& kk, float2& vv, int& zk, int& zv) {
+    kk = load2<FP32>(ws.ring_k, fbase + (size_t)jj * D + 2 * lane);
+    vv = load2<FP32>(ws.ring_v, fbase + (size_t)jj * D + 2 * lane);
+    zk = zv = 0;
+    if (pq) {
+      const uint8_t* cz = ws.codes + (unit * N + jj) * (2 * G);
+      zk = cz[gl];
+      zv = cz[G + gl];
     }
-#pragma unroll
-    for (int q = 0; q < AGG_BATCH; ++q) {
-      if (jb[q] < 0) break;
-      const int jj = jb[q];
-      const float2 kk = kb[q], vv = vb[q];
-      sk.x = sk.x + kk.x; sk.y = sk.y + kk.y;
-      sv.x = sv.x + vv.x; sv.y = sv.y + vv.y;
-      qk.x = qk.x + kk.x * kk.x; qk.y = qk.y + kk.y * kk.y;
-      qv.x = qv.x + vv.x * vv.x; qv.y = qv.y + vv.y * vv.y;
-      if (pq) {
-        hk.x += (zk[q] == c0) ? 1u : 0u;
-        hk.y += (zk[q] == c0 + 1) ? 1u : 0u;
-        hv.x += (zv[q] == c0) ? 1u : 0u;
-        hv.y += (zv[q] == c0 + 1) ? 1u : 0u;
-        m.n_res += 1;
-      }
-      float sx, sy;
-      token_xy(jj, dm.grid_w, dm.grid_h, sx, sy);
-      const float mx = keep * m.mu_x + eta * sx;
-      const float my = keep * m.mu_y + eta * sy;
-      m.mu_x = mx;
-      m.mu_y = my;
-      const float ddx = sx - mx, ddy = sy - my;
-      m.sxx = keep * m.sxx + eta * (ddx * ddx);
-      m.sxy = keep * m.sxy + eta * (ddx * ddy);
-      m.syy = keep * m.syy + eta * (ddy * ddy);
-      m.tau = fb.fe[b] * N + jj;
-      m.n += 1;
+  };
+  int jn = s_tok[wave][0];
+  float2 kn, vn;
+  int zkn, zvn;
+  fetch(jn, kn, vn, zkn, zvn);
+  for (int i = 0; i < ntok; ++i) {
+    const int jj = jn;
+    const float2 kk = kn, vv = vn;
+    const int zk = zkn, zv = zvn;
+    if (i + 1 < ntok) {  // uniform: next token's loads in flight while this one is absorbed
+      jn = s_tok[wave][i + 1];
+      fetch(jn, kn, vn, zkn, zvn);
     }
+    sk.x = sk.x + kk.x; sk.y = sk.y + kk.y;
+    sv.x = sv.x + vv.x; sv.y = sv.y + vv.y;
+    qk.x = qk.x + kk.x * kk.x; qk.y = qk.y + kk.y * kk.y;
+    qv.x = qv.x + vv.x * vv.x; qv.y = qv.y + vv.y * vv.y;
+    if (pq) {
+      hk.x += (zk == c0) ? 1u : 0u;
+      hk.y += (zk == c0 + 1) ? 1u : 0u;
+      hv.x += (zv == c0) ? 1u : 0u;
+      hv.y += (zv == c0 + 1) ? 1u : 0u;
+      m.n_res += 1;
+    }
+    float sx, sy;
+    token_xy(jj, dm.grid_w, dm.grid_h, sx, sy);
+    const float mx = keep * m.mu_x + eta * sx;
+    const float my = keep * m.mu_y + eta * sy;
+    m.mu_x = mx;
+    m.mu_y = my;
+    const float ddx = sx - mx, ddy = sy - my;
+    m.sxx = keep * m.sxx + eta * (ddx * ddx);
+    m.sxy = keep * m.sxy + eta * (ddx * ddy);
+    m.syy = keep * m.syy + eta * (ddy * ddy);
+    m.tau = fb.fe[b] * N + jj;
+    m.n += 1;
   }
   reinterpret_cast<float2*>(row + ROW_SUMK)[lane] = sk;
   reinterpret_cast<float2*>(row + ROW_SUMV)[lane] = sv;
@@ -769,6 +909,10 @@ __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBa
   reinterpret_cast<uint2*>(row + ROW_HK)[lane] = hk;
   reinterpret_cast<uint2*>(row + ROW_HV)[lane] = hv;
   if (lane == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
+  // centres float32(sum / n) for the next fold's residuals (IEEE division)
+  const float nf = (float)m.n;
+  reinterpret_cast<float2*>(ws.cent + si * 2 * D)[lane] = make_float2(sk.x / nf, sk.y / nf);
+  reinterpret_cast<float2*>(ws.cent + (si * 2 + 1) * D)[lane] = make_float2(sv.x / nf, sv.y / nf);
   refresh_cache(dm, sk, m, unit, k, ws, lane);
   // per-slot count of folds that touched it (owned by this wave: no atomics)
   if (lane == 0) ws.touched[si] += 1u;
@@ -783,5 +927,6 @@ hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch
     hipLaunchKernelGGL(k_aggregate<0>, grid, dim3(256), 0, st, dm, ws, fb, cpu);
   return hipGetLastError();
 }
+
 
 }  // namespace pkv

@@ -73,7 +73,10 @@ struct Workspace {
   CacheMeta* cmeta;           // [streams][units][K]
   int32_t* assign;            // [streams][units][T]
   uint8_t* codes;             // [streams][units][T][2][G]: PQ codes of the last fold's tokens
+  float* cent;                // [streams][units][K][2][D]: centres float32(sum / n) of K and V
   float* codebooks;           // [streams][units][2][G][CMAX][DP]
+  float* cbhn;                // [streams][units][2][G][CMAX]: |C|^2 / 2 (+inf for codewords >= C)
+  float* cbmax;               // [streams][units][2][G]: an upper bound of max_c |C|
   uint8_t* pk;                // [units][K*S][D] kv dtype (synthesis of one stream)
   uint8_t* pv;
   float* pbias;               // [units][K]
@@ -82,6 +85,7 @@ struct Workspace {
   float* part_ml;             // [units][max_splits][max_rows][2]  (max, sum)
   unsigned long long* counters;  // [16]
   uint32_t* touched;             // [streams][units][K]: folds in which the slot absorbed >= 1 token
+  uint32_t* tgen;                // [streams][units][K]: tag (evicted frame + 1) of the last fold that assigned the slot a token
 };
 
 enum Counter {

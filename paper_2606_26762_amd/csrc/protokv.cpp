@@ -27,8 +27,8 @@ struct StreamState {
 };
 
 struct Layout {
-  size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codes, codebooks;
-  size_t pk, pv, pbias, pcodes, part_o, part_ml, counters, touched, total;
+  size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codes, cent, codebooks, cbhn, cbmax;
+  size_t pk, pv, pbias, pcodes, part_o, part_ml, counters, touched, tgen, total;
 };
 
 thread_local std::string g_init_err;
@@ -59,7 +59,10 @@ Layout make_layout(const protokv_config& c) {
   ly.cmeta = take(U * K * sizeof(CacheMeta));
   ly.assign = take(U * T * 4);
   ly.codes = take(U * T * 2 * G);
+  ly.cent = take(U * K * 2 * D * 4);
   ly.codebooks = take(U * 2 * G * CMAX * DP * 4);
+  ly.cbhn = take(U * 2 * G * CMAX * 4);
+  ly.cbmax = take(U * 2 * G * 4);
   ly.pk = take(units * K * S * D * es);
   ly.pv = take(units * K * S * D * es);
   ly.pbias = take(units * K * 4);
@@ -68,6 +71,7 @@ Layout make_layout(const protokv_config& c) {
   ly.part_ml = take(units * MAX_SPLITS * rows * 2 * 4);
   ly.counters = take(CNT_COUNT * 8);
   ly.touched = take(U * K * 4);
+  ly.tgen = take(U * K * 4);
   ly.total = off;
   return ly;
 }
@@ -257,7 +261,10 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.cmeta = (CacheMeta*)(b + ly.cmeta);
   ws.assign = (int32_t*)(b + ly.assign);
   ws.codes = b + ly.codes;
+  ws.cent = (float*)(b + ly.cent);
   ws.codebooks = (float*)(b + ly.codebooks);
+  ws.cbhn = (float*)(b + ly.cbhn);
+  ws.cbmax = (float*)(b + ly.cbmax);
   ws.pk = b + ly.pk;
   ws.pv = b + ly.pv;
   ws.pbias = (float*)(b + ly.pbias);
@@ -266,6 +273,7 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.part_ml = (float*)(b + ly.part_ml);
   ws.counters = (unsigned long long*)(b + ly.counters);
   ws.touched = (uint32_t*)(b + ly.touched);
+  ws.tgen = (uint32_t*)(b + ly.tgen);
   h->st.assign(c->num_streams, StreamState());
 
   // codebooks -> [U][2][G][CMAX][DP] with the codeword axis padded to 16
@@ -278,8 +286,25 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
         for (int cc = 0; cc < C; ++cc)
           std::memcpy(&cb[(((uu * 2 + kv) * G + g) * CMAX + cc) * DP],
                       &codebooks[(((uu * 2 + kv) * G + g) * C + cc) * DP], DP * sizeof(float));
+  // per codeword |C|^2 / 2 and per (K/V, subspace) a bound on max |C|, for the
+  // PQ encoder's error bound (float32, sequential fused multiply-add)
+  std::vector<float> hn(U * 2 * G * CMAX), cmax(U * 2 * G);
+  for (size_t blk = 0; blk < U * 2 * G; ++blk) {
+    float m = 0.f;
+    for (int cc = 0; cc < CMAX; ++cc) {
+      float n2 = 0.f;
+      for (int q = 0; q < DP; ++q) n2 = std::fma(cb[(blk * CMAX + cc) * DP + q], cb[(blk * CMAX + cc) * DP + q], n2);
+      hn[blk * CMAX + cc] = cc < C ? 0.5f * n2 : INFINITY;
+      if (cc < C) m = std::max(m, n2);
+    }
+    cmax[blk] = std::sqrt(m) * 1.0001f;
+  }
   hipError_t e = hipMemsetAsync(workspace, 0, ly.total, hs);
   if (e == hipSuccess) e = hipMemcpyAsync(ws.codebooks, cb.data(), cb.size() * sizeof(float),
+                                          hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(ws.cbhn, hn.data(), hn.size() * sizeof(float),
+                                          hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(ws.cbmax, cmax.data(), cmax.size() * sizeof(float),
                                           hipMemcpyHostToDevice, hs);
   if (e == hipSuccess) e = hipStreamSynchronize(hs);
   if (e != hipSuccess) {

@@ -401,6 +401,7 @@ constexpr int AT_ROWS = 256;  // query rows per workgroup
 constexpr int AT_TILE_BYTES = AT_KEYS * D * 2;   // one K or V tile, 16 KB
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_void;
@@ -410,7 +411,8 @@ __device__ __forceinline__ int at_chunk(int r, int c) { return r * (D * 2) + ((c
 
 __global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, AttendArgs aa, int rows, int rblocks) {
   __shared__ __attribute__((aligned(16))) uint8_t s_kv[2][2][AT_TILE_BYTES];   // [buffer][K,V]
-  __shared__ float s_bias[2][AT_KEYS];
+  __shared__ __attribute__((aligned(16))) float s_bias[3][AT_KEYS];          // log2(e) * bias, -inf past the context
+  __shared__ const uint8_t* s_rowp[3][2][AT_KEYS];                            // K and V address of each tile row
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nwave = blockDim.x >> 6;
@@ -444,26 +446,44 @@ __global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, Atte
     }
   }
 
-  // Async load of tile t into buffer buf: 2 x 16 wave-instructions (4 rows of
-  // 16 chunks each); wave w issues instructions w, w + nwave, ...  Lane L of
-  // instruction i lands at byte (i*64 + L)*16 of the tile = row 4i + L/16,
-  // physical chunk L%16, so it fetches logical chunk (L%16) ^ (row & 15).
-  float bias_reg = -INFINITY;
+  // Per-tile row table: wave 0 resolves each tile row (one lane per row) to its
+  // K and V addresses and its bias once; it is triple-buffered so wave 0 can
+  // fill the next tile's entry while other waves still read the previous one.
+  // Rows past the context read row c0 and carry bias -inf.
+  const float invS = 1.0f / (float)dm.S;
+  auto resolve = [&](int t, const uint8_t*& kp, const uint8_t*& vp, float& bv) {
+    const int idx = c0 + t * AT_KEYS + lane;
+    const int pos = idx < c1 ? idx : c0;
+    bv = idx < c1 ? 0.f : -INFINITY;
+    if (pos < aa.n_near) {
+      const int fo = pos / dm.T;
+      const int slot = (aa.f_first + fo) % (dm.W + 1);
+      const size_t off = (((unit * (dm.W + 1) + slot) * dm.T + (pos - fo * dm.T)) * (size_t)D) * 2;
+      kp = ws.ring_k + off;
+      vp = ws.ring_v + off;
+    } else {
+      const int prow = pos - aa.n_near;
+      const size_t off = (((size_t)u * dm.K * dm.S + prow) * (size_t)D) * 2;
+      kp = ws.pk + off;
+      vp = ws.pv + off;
+      int k = (int)((float)prow * invS);
+      k -= k * dm.S > prow ? 1 : 0;
+      k += (k + 1) * dm.S <= prow ? 1 : 0;
+      if (idx < c1) bv = ws.pbias[(size_t)u * dm.K + k] * LOG2E;
+    }
+  };
+  // Loads of tile t: instruction i = wave, wave + nwave, ... (< 32) moves tile
+  // row 4 (i & 15) + lane / 16 of K (i < 16) or V, 16-byte chunk (lane & 15) ^
+  // (row & 15) (XOR swizzle), straight into LDS.
   auto issue = [&](int t, int buf) {
-    const int base = c0 + t * AT_KEYS;
+    const int tb = t % 3;
     for (int i = wave; i < 32; i += nwave) {
       const int kv = i >> 4, ii = i & 15;
       const int row = ii * 4 + (lane >> 4);
       const int cl = (lane & 15) ^ (row & 15);
-      const int idx = base + row;
-      // rows past the context read row c0 (any valid row; masked by the bias)
-      const CtxRef ref = ctx_key<2>(dm, ws, aa, unit, u, idx < c1 ? idx : c0, kv == 1);
-      __builtin_amdgcn_global_load_lds((gbl_void*)(ref.base + cl * 16),
+      const uint8_t* base = s_rowp[tb][kv][row];
+      __builtin_amdgcn_global_load_lds((gbl_void*)(base + cl * 16),
                                        (lds_void*)(&s_kv[buf][kv][ii * 1024]), 16, 0, 0);
-    }
-    if (wave == 0) {
-      const int idx = base + lane;
-      bias_reg = idx < c1 ? ctx_key<2>(dm, ws, aa, unit, u, idx, false).bias : -INFINITY;
     }
   };
 
@@ -471,15 +491,35 @@ __global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, Atte
   f32x16 oacc[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) oacc[b] = (f32x16){0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  float mrun = -INFINITY, lrun = 0.f;
+  // Reference max (log2 units) with a finite floor: masked keys score -inf and
+  // give exp2(-inf) = 0 without special cases.  The reference is raised only
+  // when a row's max exceeds it by more than 8, so p <= 2^8 and the output
+  // accumulators are rescaled rarely.
+  float mref = -1e30f, lrun = 0.f;
 
+  const uint8_t *nk = nullptr, *nv = nullptr;
+  float nb = -INFINITY;
+  if (wave == 0 && ntiles > 0) {
+    resolve(0, nk, nv, nb);
+    s_rowp[0][0][lane] = nk;
+    s_rowp[0][1][lane] = nv;
+    s_bias[0][lane] = nb;
+    if (ntiles > 1) resolve(1, nk, nv, nb);
+  }
+  __syncthreads();
   if (ntiles > 0) issue(0, 0);
   for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
+    const int buf = t & 1, tb = t % 3;
     __builtin_amdgcn_s_waitcnt(0);          // this wave's loads of tile t have landed
-    if (wave == 0) s_bias[buf][lane] = bias_reg;
+    if (wave == 0 && t + 1 < ntiles) {      // entry (t + 1) % 3 was last read for tile t - 2
+      const int nb3 = (t + 1) % 3;
+      s_rowp[nb3][0][lane] = nk;
+      s_rowp[nb3][1][lane] = nv;
+      s_bias[nb3][lane] = nb;
+    }
     __syncthreads();
     if (t + 1 < ntiles) issue(t + 1, buf ^ 1);
+    if (wave == 0 && t + 2 < ntiles) resolve(t + 2, nk, nv, nb);
     const uint8_t* kt = s_kv[buf][0];
     const uint8_t* vt = s_kv[buf][1];
     // S^T for the two 32-key halves of the tile
@@ -494,43 +534,45 @@ __global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, Atte
         sacc[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bq[kk], sacc[h], 0, 0, 0);
       }
     }
-    float tmax = -INFINITY;
-    float sv[2][16];
+    // scores x = s * scale + bias (key m = h*32 + (i/4)*8 + half*4 + i%4)
+    float tmax = -1e30f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const float4 bb = *reinterpret_cast<const float4*>(&s_bias[tb][h * 32 + i4 * 8 + half * 4]);
+        const float bv[4] = {bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float x = fmaf(sacc[h][i4 * 4 + e], scale, bv[e]);
+          sacc[h][i4 * 4 + e] = x;
+          tmax = fmaxf(tmax, x);
+        }
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const bool grow = tmax > mref + 8.0f;
+    if (__ballot(grow)) {  // uniform
+      const float mnew = grow ? tmax : mref;
+      const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
+      lrun *= alpha;
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[b][i] *= alpha;
+      mref = mnew;
+    }
+    float psum = 0.f;
+    bf16x8 pb[4];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int m = h * 32 + (i >> 2) * 8 + half * 4 + (i & 3);
-        const float bsv = s_bias[buf][m];
-        const float x = bsv == -INFINITY ? -INFINITY : fmaf(sacc[h][i], scale, bsv * LOG2E);
-        sv[h][i] = x;
-        tmax = fmaxf(tmax, x);
-      }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(mrun, tmax);
-    const float alpha = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(mrun - mnew);
-    float psum = 0.f;
-    bf16x8 pb[4];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      u16x8 p0, p1;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float pv = sv[h][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sv[h][i] - mnew);
+        const float pv = __builtin_amdgcn_exp2f(sacc[h][i] - mref);
         psum += pv;
-        const uint16_t hb = q_to_bf16(pv);
-        if (i < 8) p0[i] = hb; else p1[i - 8] = hb;
+        pb[2 * h + (i >> 3)][i & 7] = (__bf16)pv;
       }
-      pb[2 * h] = __builtin_bit_cast(bf16x8, p0);
-      pb[2 * h + 1] = __builtin_bit_cast(bf16x8, p1);
-    }
     psum += __shfl_xor(psum, 32, 64);
-    lrun = lrun * alpha + psum;
-    mrun = mnew;
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[b][i] *= alpha;
+    lrun += psum;
     // O^T = V^T P.  k positions half*8 + i of step st <-> keys 16 st + 4 half + {0..3}
     // (i < 4) and 16 st + 8 + 4 half + {0..3} (i >= 4), matching P's layout.  Each
     // 4-key part is one ds_read_b64_tr_b16 per 16-lane group: source lane s reads
@@ -548,12 +590,12 @@ __global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, Atte
             (lds_v4i16*)(vt + at_chunk(ka, dsrc >> 3) + (dsrc & 7) * 2));
         const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (lds_v4i16*)(vt + at_chunk(kb, dsrc >> 3) + (dsrc & 7) * 2));
-        const u16x8 a = (u16x8){(uint16_t)lo[0], (uint16_t)lo[1], (uint16_t)lo[2], (uint16_t)lo[3],
-                                (uint16_t)hi[0], (uint16_t)hi[1], (uint16_t)hi[2], (uint16_t)hi[3]};
+        const v8i16 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), pb[st], oacc[b], 0, 0, 0);
       }
     }
   }
+  const float mrun = mref;
 
   const size_t orow_t = rvalid ? (size_t)(r / grp) : 0;
   const int ogg = rvalid ? r % grp : 0;
