@@ -5,6 +5,8 @@
 // tokens, mass-aware bias, Eq. attn_logit), Eq. pq and Appendix Algorithms
 // "DecodeTopSResidualModes" and "ProtoKV Query-Time Pseudo-Token Decoding
 // and Attention".
+#include <type_traits>
+
 #include "pkv_internal.h"
 
 namespace pkv {
@@ -244,7 +246,156 @@ __device__ void decode_top_s_small(const uint32_t* hist /* [G][CMAX] */, int C, 
   for (int sidx = 0; sidx < S; ++sidx) out[sidx] = sidx < nb ? bc[sidx] : 0u;
 }
 
-// Decoding: one thread per (slot, K/V) of one (layer, kv head), 32 slots per
+// Decoding, register path: four lanes per (slot, K/V) beam, 16 beams per
+// wave, for prototypes whose residual count is at most 65534 (every factor
+// H+1 is below 2^16, so a product of the 8 factors fits in 128 bits) and
+// S <= SM.  Lane q of a beam owns the prefixes e = q, q + 4, ...  For each
+// subspace the four lanes rank the codewords (count desc, code asc) by
+// counting, publish the top R = min(S, C) in order through LDS, and merge:
+// S pops of the best row head (product desc, packed tuple asc), the best
+// found with two shuffle steps across the four lanes; only the winning row
+// advances.  Same beam (width S) and order as decode_top_s.
+constexpr int DEC_BEAMS = 16;  // beams per wave
+
+template <int SM>
+__global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid, int n_active) {
+  constexpr int E = SM / 4;  // prefixes per lane
+  __shared__ uint32_t s_rank[4][DEC_BEAMS][CMAX];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane & 3, bq = lane >> 2;
+  const int beam = (blockIdx.x * 4 + wave) * DEC_BEAMS + bq;  // ((unit * n_active + slot) * 2 + K/V)
+  const bool bvalid = beam < dm.units * n_active * 2;
+  const int kv = beam & 1, up = bvalid ? beam >> 1 : 0;
+  const int u = up / n_active, p = up % n_active;
+  const size_t unit = (size_t)sid * dm.units + u;
+  const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
+  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * (SMAX + 1);
+  const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
+  const int S = dm.S, C = dm.C;
+  const bool nores = !pq || m.n_res == 0;
+  if (bvalid && q == 0 && nores) out[SMAX] = 1u;
+  // this path decodes the beam (uniform within the four lanes)
+  const bool mine = bvalid && !nores && m.n_res <= 65534u && S <= SM;
+  const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
+  const int R = S < C ? S : C;
+  const int gbase = lane & ~3;
+
+  U128 pp[E];
+  uint32_t pc[E];
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+    pp[j].lo = (q == 0 && j == 0) ? 1u : 0u;
+    pp[j].hi = 0;
+    pc[j] = 0;
+  }
+  int nb = 1;
+  for (int g = 0; g < G; ++g) {
+    // keys of codewords 4q .. 4q+3: (count << 4 | (15 - c)) + 1, larger = better, 0 = absent
+    uint4 h4 = make_uint4(0, 0, 0, 0);
+    if (mine) h4 = reinterpret_cast<const uint4*>(hist + g * CMAX)[q];
+    const uint32_t hv[4] = {h4.x, h4.y, h4.z, h4.w};
+    uint32_t key[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = 4 * q + i;
+      key[i] = c < C ? ((hv[i] << 4) | (uint32_t)(15 - c)) + 1u : 0u;
+    }
+    int rk[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int src = 0; src < 4; ++src)
+#pragma unroll
+      for (int i2 = 0; i2 < 4; ++i2) {
+        const uint32_t other = __shfl(key[i2], gbase + src, 64);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rk[i] += other > key[i] ? 1 : 0;
+      }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (key[i] != 0u && rk[i] < R) s_rank[wave][bq][rk[i]] = key[i];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const uint32_t k0 = s_rank[wave][bq][0];
+    const int shift = 4 * (G - 1 - g);
+    // row heads: prefix e = q + 4j times rank ptr[j]
+    int ptr[E];
+    U128 hp[E];
+    uint32_t hc[E];
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      ptr[j] = 0;
+      const bool ok = q + 4 * j < nb;
+      hp[j] = ok ? mul_u128_u32(pp[j], ((k0 - 1u) >> 4) + 1u) : U128{0, 0};
+      hc[j] = ok ? (pc[j] | ((15u - ((k0 - 1u) & 15u)) << shift)) : 0xFFFFFFFFu;
+    }
+    const int nout = S < nb * R ? S : nb * R;
+    U128 np[E];
+    uint32_t nc[E];
+#pragma unroll
+    for (int j = 0; j < E; ++j) { np[j] = U128{0, 0}; nc[j] = 0; }
+#pragma unroll
+    for (int o = 0; o < SM; ++o) {
+      if (o < nout) {
+        // best head of this lane (product 0 = exhausted row)
+        U128 bv = hp[0];
+        uint32_t bc = hc[0];
+        int bj = 0;
+#pragma unroll
+        for (int j = 1; j < E; ++j)
+          if (before128(hp[j], hc[j], bv, bc)) { bv = hp[j]; bc = hc[j]; bj = j; }
+        int who = q * E + bj;
+        // best of the four lanes
+#pragma unroll
+        for (int x = 1; x <= 2; x <<= 1) {
+          U128 ov;
+          ov.lo = __shfl_xor(bv.lo, x, 64);
+          ov.hi = __shfl_xor(bv.hi, x, 64);
+          const uint32_t oc = __shfl_xor(bc, x, 64);
+          const int ow = __shfl_xor(who, x, 64);
+          if (before128(ov, oc, bv, bc)) { bv = ov; bc = oc; who = ow; }
+        }
+        if ((o & 3) == q) { np[o >> 2] = bv; nc[o >> 2] = bc; }
+        // the winning row moves to its next rank
+        if (who / E == q) {
+          const int j = who % E;
+#pragma unroll
+          for (int jj = 0; jj < E; ++jj) {
+            if (jj == j) {
+              ptr[jj] += 1;
+              if (ptr[jj] < R) {
+                const uint32_t kk = s_rank[wave][bq][ptr[jj]];
+                hp[jj] = mul_u128_u32(pp[jj], ((kk - 1u) >> 4) + 1u);
+                hc[jj] = pc[jj] | ((15u - ((kk - 1u) & 15u)) << shift);
+              } else {
+                hp[jj] = U128{0, 0};
+                hc[jj] = 0xFFFFFFFFu;
+              }
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < E; ++j) { pp[j] = np[j]; pc[j] = nc[j]; }
+    nb = nout;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  if (mine) {
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int o = q + 4 * j;
+      if (o < S) out[o] = o < nb ? pc[j] : 0u;
+    }
+    if (q == 0) out[SMAX] = 0u;
+  }
+}
+
+// Decoding, wide path (prototypes with more than 65534 residuals, whose
+// products need 192 bits): one thread per (slot, K/V) of one (layer, kv
+// head), 32 slots per
 // workgroup (lanes 0-31 keys, 32-63 values).  Codes go to ws.pcodes
 // [units][K][2][SMAX] (packed tuples, subspace 0 in the top nibble) and a flag
 // word per (slot, K/V): 1 if the slot has no residual statistics.
@@ -262,16 +413,12 @@ __global__ __launch_bounds__(64) void k_decode(Dims dm, Workspace ws, int sid, i
   const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
   uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * (SMAX + 1);
   const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
-  if (!pq || m.n_res == 0) {
-    out[SMAX] = 1u;
-    return;
-  }
+  if (!pq || m.n_res == 0) return;             // flagged by k_decode4
+  if (m.n_res <= 65534u && S <= SM) return;    // decoded by k_decode4
   out[SMAX] = 0u;
   const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
   uint32_t codes[SMAX];
-  if (m.n_res <= 65534u && S <= SM) {
-    decode_top_s_small<SM>(hist, dm.C, S, codes);
-  } else {
+  {
     BeamView bv;
     bv.S = S;
     bv.w0 = reinterpret_cast<uint64_t*>(s_dyn);
@@ -334,10 +481,15 @@ hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_act
   if (n_active <= 0) return hipSuccess;
   const int bpu = (n_active + SYN_P - 1) / SYN_P;
   const size_t lds = (size_t)2 * dm.S * 64 * (3 * sizeof(uint64_t) + sizeof(uint32_t));
-  if (dm.S <= 8)
+  const int nbeams = dm.units * n_active * 2;
+  const int nblk4 = (nbeams + 4 * DEC_BEAMS - 1) / (4 * DEC_BEAMS);
+  if (dm.S <= 8) {
+    hipLaunchKernelGGL(k_decode4<8>, dim3(nblk4), dim3(256), 0, st, dm, ws, sid, n_active);
     hipLaunchKernelGGL(k_decode<8>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
-  else
+  } else {
+    hipLaunchKernelGGL(k_decode4<16>, dim3(nblk4), dim3(256), 0, st, dm, ws, sid, n_active);
     hipLaunchKernelGGL(k_decode<16>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
+  }
   return hipGetLastError();
 }
 
@@ -409,13 +561,42 @@ typedef __attribute__((address_space(1))) const void gbl_void;
 // byte offset of 16-byte chunk c of tile row r
 __device__ __forceinline__ int at_chunk(int r, int c) { return r * (D * 2) + ((c ^ (r & 15)) << 4); }
 
-__global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, AttendArgs aa, int rows, int rblocks) {
-  __shared__ __attribute__((aligned(16))) uint8_t s_kv[2][2][AT_TILE_BYTES];   // [buffer][K,V]
-  __shared__ __attribute__((aligned(16))) float s_bias[3][AT_KEYS];          // log2(e) * bias, -inf past the context
-  __shared__ const uint8_t* s_rowp[3][2][AT_KEYS];                            // K and V address of each tile row
+// Barrier for LDS traffic only: waits for this wave's LDS operations, not
+// for its outstanding global loads (the tiles in flight).  The asm memory
+// clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  asm volatile("s_barrier" ::: "memory");
+}
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane
+// (global_load_lds_dwordx4; M0 holds the wave-uniform LDS byte address).
+// Issued as inline asm so the compiler does not treat later LDS reads of
+// other buffers as dependent on it: completion is awaited explicitly with
+// wait_vm before the barrier that publishes a tile.
+__device__ __forceinline__ void lds_dma16(const void* g, void* lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0) : "memory", "m0");
+}
+// s_waitcnt vmcnt(n) (expcnt / lgkmcnt not waited for)
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+constexpr int AT_NBUF = 4;        // tile buffers: tile t computes while t+1..t+3 load
+constexpr int AT_NTAB = 5;        // row-table entries (written 3 tiles ahead)
+constexpr int AT_PB_MAX = 4096;   // pseudo-token biases staged in LDS up to this capacity
+
+template <int NW>
+__global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims dm, Workspace ws, AttendArgs aa, int rows, int rblocks) {
+  constexpr int LPT = 32 / NW;  // load instructions per wave per tile
+  __shared__ __attribute__((aligned(16))) uint8_t s_kv[AT_NBUF][2][AT_TILE_BYTES];   // [buffer][K,V]
+  __shared__ __attribute__((aligned(16))) float s_bias[AT_NTAB][AT_KEYS];           // log2(e) * bias, -inf past the context
+  __shared__ const uint8_t* s_rowp[AT_NTAB][2][AT_KEYS];                             // K and V address of each tile row
+  __shared__ float s_pb[AT_PB_MAX];                                                  // log2(e) * ln n_k of this unit
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nwave = blockDim.x >> 6;
   // blocks of one kv head land on one XCD (dispatch is round-robin over 8)
   const int nblk = gridDim.x, per = nblk / 8;
   const int lbid = (int)blockIdx.x < per * 8 ? ((int)blockIdx.x % 8) * per + (int)blockIdx.x / 8 : (int)blockIdx.x;
@@ -429,10 +610,14 @@ __global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, Atte
   const int c0 = split * aa.chunk;
   const int c1 = min(ctx, c0 + aa.chunk);
   const int ntiles = c1 > c0 ? (c1 - c0 + AT_KEYS - 1) / AT_KEYS : 0;
+  const bool pb_lds = dm.K <= AT_PB_MAX;
+  if (pb_lds)
+    for (int k = tid; k < dm.K; k += NW * 64) s_pb[k] = ws.pbias[(size_t)u * dm.K + k] * LOG2E;
 
   const int col = lane & 31, half = lane >> 5;
-  const int r = rb * AT_ROWS + wave * 32 + col;  // query row of this lane
+  const int r = rb * (NW * 32) + wave * 32 + col;  // query row of this lane
   const bool rvalid = r < rows;
+  const bool wvalid = rb * (NW * 32) + wave * 32 < rows;  // uniform: the wave has query rows
   bf16x8 bq[8];
   {
     const int t = rvalid ? r / grp : 0, gg = rvalid ? r % grp : 0;
@@ -445,11 +630,11 @@ __global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, Atte
       bq[kk] = __builtin_bit_cast(bf16x8, v);
     }
   }
+  __syncthreads();  // s_pb staged (and the query loads complete)
 
   // Per-tile row table: wave 0 resolves each tile row (one lane per row) to its
-  // K and V addresses and its bias once; it is triple-buffered so wave 0 can
-  // fill the next tile's entry while other waves still read the previous one.
-  // Rows past the context read row c0 and carry bias -inf.
+  // K and V addresses and its bias once, three tiles ahead.  Rows past the
+  // context read row c0 and carry bias -inf.
   const float invS = 1.0f / (float)dm.S;
   auto resolve = [&](int t, const uint8_t*& kp, const uint8_t*& vp, float& bv) {
     const int idx = c0 + t * AT_KEYS + lane;
@@ -469,21 +654,28 @@ __global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, Atte
       int k = (int)((float)prow * invS);
       k -= k * dm.S > prow ? 1 : 0;
       k += (k + 1) * dm.S <= prow ? 1 : 0;
-      if (idx < c1) bv = ws.pbias[(size_t)u * dm.K + k] * LOG2E;
+      if (idx < c1) bv = pb_lds ? s_pb[k] : ws.pbias[(size_t)u * dm.K + k] * LOG2E;
     }
   };
-  // Loads of tile t: instruction i = wave, wave + nwave, ... (< 32) moves tile
-  // row 4 (i & 15) + lane / 16 of K (i < 16) or V, 16-byte chunk (lane & 15) ^
-  // (row & 15) (XOR swizzle), straight into LDS.
-  auto issue = [&](int t, int buf) {
-    const int tb = t % 3;
-    for (int i = wave; i < 32; i += nwave) {
+  auto publish = [&](int t, const uint8_t* kp, const uint8_t* vp, float bv) {
+    const int e = t % AT_NTAB;
+    s_rowp[e][0][lane] = kp;
+    s_rowp[e][1][lane] = vp;
+    s_bias[e][lane] = bv;
+  };
+  // Loads of tile t: instruction i = wave + q * NW (q < LPT) moves tile row
+  // 4 (i & 15) + lane / 16 of K (i < 16) or V, 16-byte chunk (lane & 15) ^
+  // (row & 15) (XOR swizzle), straight into LDS buffer t % AT_NBUF.
+  auto issue = [&](int t) {
+    const int e = t % AT_NTAB, buf = t % AT_NBUF;
+#pragma unroll
+    for (int q = 0; q < LPT; ++q) {
+      const int i = wave + q * NW;
       const int kv = i >> 4, ii = i & 15;
       const int row = ii * 4 + (lane >> 4);
       const int cl = (lane & 15) ^ (row & 15);
-      const uint8_t* base = s_rowp[tb][kv][row];
-      __builtin_amdgcn_global_load_lds((gbl_void*)(base + cl * 16),
-                                       (lds_void*)(&s_kv[buf][kv][ii * 1024]), 16, 0, 0);
+      const uint8_t* base = s_rowp[e][kv][row];
+      lds_dma16(base + cl * 16, &s_kv[buf][kv][ii * 1024]);
     }
   };
 
@@ -497,29 +689,33 @@ __global__ __launch_bounds__(512) void k_attend_bf16(Dims dm, Workspace ws, Atte
   // accumulators are rescaled rarely.
   float mref = -1e30f, lrun = 0.f;
 
+  // prologue: rows of tiles 0..2 published, their loads issued; tile 3 resolved
   const uint8_t *nk = nullptr, *nv = nullptr;
   float nb = -INFINITY;
-  if (wave == 0 && ntiles > 0) {
-    resolve(0, nk, nv, nb);
-    s_rowp[0][0][lane] = nk;
-    s_rowp[0][1][lane] = nv;
-    s_bias[0][lane] = nb;
-    if (ntiles > 1) resolve(1, nk, nv, nb);
-  }
-  __syncthreads();
-  if (ntiles > 0) issue(0, 0);
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1, tb = t % 3;
-    __builtin_amdgcn_s_waitcnt(0);          // this wave's loads of tile t have landed
-    if (wave == 0 && t + 1 < ntiles) {      // entry (t + 1) % 3 was last read for tile t - 2
-      const int nb3 = (t + 1) % 3;
-      s_rowp[nb3][0][lane] = nk;
-      s_rowp[nb3][1][lane] = nv;
-      s_bias[nb3][lane] = nb;
+  if (wave == 0) {
+    for (int t = 0; t < 3 && t < ntiles; ++t) {
+      resolve(t, nk, nv, nb);
+      publish(t, nk, nv, nb);
     }
-    __syncthreads();
-    if (t + 1 < ntiles) issue(t + 1, buf ^ 1);
-    if (wave == 0 && t + 2 < ntiles) resolve(t + 2, nk, nv, nb);
+    if (ntiles > 3) resolve(3, nk, nv, nb);
+  }
+  wait_vm<0>();  // the query operands are in registers before any tile is in flight
+  lds_barrier();
+  for (int t = 0; t < 3 && t < ntiles; ++t) issue(t);
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int buf = t % AT_NBUF, tb = t % AT_NTAB;
+    // this wave's loads of tile t have landed; tiles t+1, t+2 may still be in flight
+    if (t + 2 < ntiles) wait_vm<2 * LPT>();
+    else if (t + 1 < ntiles) wait_vm<LPT>();
+    else wait_vm<0>();
+    // entry (t + 3) % 5 was last read for tile t - 2 (before the previous barrier)
+    if (wave == 0 && t + 3 < ntiles) publish(t + 3, nk, nv, nb);
+    lds_barrier();
+    // buffer (t + 3) % 4 held tile t - 1, finished by every wave before this barrier
+    if (t + 3 < ntiles) issue(t + 3);
+    if (wave == 0 && t + 4 < ntiles) resolve(t + 4, nk, nv, nb);
+    if (!wvalid) continue;  // uniform: a loader-only wave
     const uint8_t* kt = s_kv[buf][0];
     const uint8_t* vt = s_kv[buf][1];
     // S^T for the two 32-key halves of the tile
@@ -709,10 +905,14 @@ hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& 
   if (dm.kv_fp32) {
     hipLaunchKernelGGL(k_attend_f32, dim3(dm.units * rows * aa.splits), dim3(64), 0, st, dm, ws, aa, rows);
   } else {
+    // 8 waves (256 query rows) per workgroup, or 4 waves for at most 128 rows:
+    // every wave issues 32 / waves loads per tile
     const int rblocks = (rows + AT_ROWS - 1) / AT_ROWS;
-    const int waves = std::max(4, (std::min(rows, AT_ROWS) + 31) / 32);
-    hipLaunchKernelGGL(k_attend_bf16, dim3(dm.units * aa.splits * rblocks), dim3(waves * 64), 0, st, dm, ws, aa,
-                       rows, rblocks);
+    if (rows > 128)
+      hipLaunchKernelGGL(k_attend_bf16<8>, dim3(dm.units * aa.splits * rblocks), dim3(512), 0, st, dm, ws, aa,
+                         rows, rblocks);
+    else
+      hipLaunchKernelGGL(k_attend_bf16<4>, dim3(dm.units * aa.splits), dim3(256), 0, st, dm, ws, aa, rows, 1);
   }
   return hipGetLastError();
 }
