@@ -63,13 +63,15 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     if kernel == "ring_insert":
         return U * T * D * b * 2 * 2                       # read frame K,V + write ring K,V
     if kernel == "screen":
-        return U * (T * D * b + K * CACHE_BYTES + T * 4)   # evicted keys, centre cache, assignment
-    if kernel == "pq_encode":
-        # evicted K,V, assignment, codebooks, the assigned slots' sums (K and V), codes written
-        return U * (2 * T * D * b + T * 4 + 2 * 8 * 16 * 16 * 4 + T * 2 * D * 4 + T * 16)
+        # assignment: evicted keys, centre cache, assignment written;
+        # PQ encoding: evicted values, the touched slots' centres (K and V),
+        # codebooks, codes written
+        return (U * (2 * T * D * b + K * CACHE_BYTES + T * 4 + 2 * 8 * 16 * 16 * 4 + T * 16)
+                + touched_per_launch * 2 * D * 4)
     if kernel == "aggregate":
         return (U * (2 * T * D * b + T * 4 + T * 16)                   # evicted K,V, assignment, codes
-                + touched_per_launch * (2 * ROW_BYTES_USED + CACHE_BYTES))  # row RMW + cache rewrite
+                + touched_per_launch * (2 * ROW_BYTES_USED + CACHE_BYTES   # row RMW + cache rewrite
+                                        + 2 * D * 4))                   # + the new K and V centres
     if kernel == "decode":
         return U * n_active * (2 * 8 * 16 * 4 + 32 + 2 * (S + 1) * 4)       # histograms, meta, codes out
     if kernel == "materialize":

@@ -214,12 +214,12 @@ protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float*
 enum {
   PROTOKV_K_RING_INSERT = 0,
   PROTOKV_K_SEED = 1,
-  PROTOKV_K_SCREEN = 2,
+  PROTOKV_K_SCREEN = 2,          /* assignment and PQ encoding of the evicted tokens */
   PROTOKV_K_AGGREGATE = 3,
   PROTOKV_K_SYNTHESIZE = 4,      /* top-S decoding of the histograms */
   PROTOKV_K_ATTEND = 5,
   PROTOKV_K_ATTEND_MERGE = 6,
-  PROTOKV_K_PQ_ENCODE = 7,
+  PROTOKV_K_PQ_ENCODE = 7,       /* reserved: PQ encoding runs inside the screen kernel */
   PROTOKV_K_MATERIALIZE = 8,     /* pseudo-token rows and biases */
   PROTOKV_K_COUNT = 12
 };

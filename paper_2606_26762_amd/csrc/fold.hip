@@ -238,6 +238,199 @@ __device__ __forceinline__ bool better(double c1, int k1, double c2, int k2) {
 }
 
 // ---------------------------------------------------------------------------
+// PQ residual encoding of the assigned tokens.  The code of subspace g is the
+// nearest codeword to r = x - c (c = float32(sum / n) before this fold,
+// stored by the previous fold), defined by the float32 sequential distance
+// dist(c) = sum_u (r_u - C[c][u])^2 (u ascending, one rounding per subtract,
+// multiply and add; ties to the lower codeword).  It is found as
+// argmax_c (r . C_c - |C_c|^2 / 2) on MFMA with a rigorous error bound; a
+// subspace whose best two scores are not separated by the bound is decided by
+// the sequential float32 distances themselves.
+//
+// Four waves per 64 screened tokens: wave w takes the 32-token block w / 2 of
+// K (w even) or V, with every load issued up front (|C|^2 / 2 and max |C|
+// per codebook come precomputed from init).  For subspaces g0 = 2p, g1 = 2p + 1, v_mfma_f32_32x32x16_bf16
+// multiplies A = codebook rows (rows 0-15: C[g0], rows 16-31: C[g1]; block
+// diagonal over two k-steps) by B = residual dims (k-step 0: g0, 1: g1), both
+// split into hi + lo bf16 (hi*hi + hi*lo + lo*hi), starting from -|C|^2 / 2.
+// ---------------------------------------------------------------------------
+constexpr int CBW = CMAX * DP;  // floats per (K/V, subspace) codebook block
+
+// v -> hi + lo with hi = bf16(v), lo = bf16(v - hi), both round to nearest even
+__device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const __bf16 h = (__bf16)v[i];
+    hi[i] = h;
+    lo[i] = (__bf16)(v[i] - (float)h);
+  }
+}
+
+// Encodes the residuals of one 32-token block of one unit for K (kv = 0) or
+// V: token jb0 + (lane % 32), assigned to `slot`; tokens outside [jlo, jhi)
+// are skipped.  Called by the four waves of a screen workgroup once the
+// workgroup's assignments are final.
+template <int FP32>
+__device__ __forceinline__ void pq_block(const Dims& dm, const Workspace& ws, const FoldBatch& fb, int b,
+                                         size_t unit, int jb0, int jlo, int jhi, int kv, int lane, int slot) {
+  const int N = dm.T;
+  const int col = lane & 31, half = lane >> 5;
+  const int j = jb0 + col;
+  const bool valid = j >= jlo && j < jhi;
+  const size_t ub = unit * 2 + kv;
+  const float* cbk = ws.codebooks + ub * G * CBW;
+  const float* hnp = ws.cbhn + ub * G * CMAX;
+  const float* cmx = ws.cbmax + ub * G;
+  const size_t es = FP32 ? 4 : 2;
+  const uint8_t* xr = (kv ? ws.ring_v : ws.ring_k) +
+                      ((((unit * (dm.W + 1) + fb.slot[b]) * N) + (size_t)(valid ? j : 0)) * D) * es;
+  uint8_t* codes = ws.codes + (unit * N + (valid ? j : 0)) * (2 * G) + kv * G;
+
+  // this lane's half (dims g*16 + half*8 .. +7) of every subspace of its token
+  float r[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int d0 = g * DP + half * 8;
+    if (FP32) {
+      *reinterpret_cast<float4*>(&r[g][0]) = *reinterpret_cast<const float4*>(xr + (size_t)d0 * 4);
+      *reinterpret_cast<float4*>(&r[g][4]) = *reinterpret_cast<const float4*>(xr + (size_t)(d0 + 4) * 4);
+    } else {
+      const u16x8 h = *reinterpret_cast<const u16x8*>(xr + (size_t)d0 * 2);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) r[g][i] = from_bf16(h[i]);
+    }
+  }
+  // A operand rows: row col < 16 holds C[2p][col][half*8 ..] (k-step 0 of pair p),
+  // row >= 16 holds C[2p+1][col-16][half*8 ..] (k-step 1)
+  float w[G / 2][8];
+#pragma unroll
+  for (int p = 0; p < G / 2; ++p) {
+    const float* wa = cbk + (2 * p + (col < 16 ? 0 : 1)) * CBW + (col & 15) * DP + half * 8;
+    *reinterpret_cast<float4*>(&w[p][0]) = *reinterpret_cast<const float4*>(wa);
+    *reinterpret_cast<float4*>(&w[p][4]) = *reinterpret_cast<const float4*>(wa + 4);
+  }
+  const float* cen = ws.cent + ((unit * dm.K + slot) * 2 + kv) * D;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int d0 = g * DP + half * 8;
+    const float4 c0 = *reinterpret_cast<const float4*>(cen + d0);
+    const float4 c1 = *reinterpret_cast<const float4*>(cen + d0 + 4);
+    const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[g][i] = valid ? r[g][i] - cc[i] : 0.f;
+  }
+  const bf16x8 zero8 = {};
+  const bool lowrows = col < 16;
+
+#pragma unroll
+  for (int p = 0; p < G / 2; ++p) {
+    const int g0 = 2 * p, g1 = 2 * p + 1;
+    bf16x8 ah, al, b0h, b0l, b1h, b1l;
+    split8(w[p], ah, al);
+    split8(r[g0], b0h, b0l);
+    split8(r[g1], b1h, b1l);
+    const bf16x8 a0h = lowrows ? ah : zero8, a0l = lowrows ? al : zero8;
+    const bf16x8 a1h = lowrows ? zero8 : ah, a1l = lowrows ? zero8 : al;
+    float n0 = 0.f, n1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      n0 = fmaf(r[g0][i], r[g0][i], n0);
+      n1 = fmaf(r[g1][i], r[g1][i], n1);
+    }
+    // accumulator rows (rr / 4) * 8 + half * 4 + rr % 4: rr < 8 -> codeword of g0, else of g1
+    f32x16 acc;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 h = *reinterpret_cast<const float4*>(hnp + (q < 2 ? g0 : g1) * CMAX + (q & 1) * 8 + half * 4);
+      acc[4 * q + 0] = -h.x;
+      acc[4 * q + 1] = -h.y;
+      acc[4 * q + 2] = -h.z;
+      acc[4 * q + 3] = -h.w;
+    }
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0h, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0l, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0l, b0h, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1h, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1l, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1l, b1h, acc, 0, 0, 0);
+
+    // best two scores per subspace: 8 codewords here, 8 in the partner lane
+    float bst1[2], bst2[2];
+    int bid[2];
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      float v1 = -INFINITY, v2 = -INFINITY;
+      int i1 = 0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float v = acc[sub * 8 + q];
+        const int cw = (q >> 2) * 8 + half * 4 + (q & 3);
+        const int mk = -(int)(v > v1);
+        v2 = __builtin_amdgcn_fmed3f(v, v1, v2);
+        v1 = fmaxf(v1, v);
+        i1 = (cw & mk) | (i1 & ~mk);
+      }
+      const float o1 = __shfl_xor(v1, 32, 64), o2 = __shfl_xor(v2, 32, 64);
+      const int oi = __shfl_xor(i1, 32, 64);
+      const bool take = o1 > v1 || (o1 == v1 && oi < i1);
+      bst2[sub] = fmaxf(fminf(v1, o1), fmaxf(v2, o2));
+      bst1[sub] = fmaxf(v1, o1);
+      bid[sub] = take ? oi : i1;
+    }
+    // lane half 0 settles g0, half 1 settles g1
+    const int g = half ? g1 : g0;
+    const float v1 = half ? bst1[1] : bst1[0], v2 = half ? bst2[1] : bst2[0];
+    float rn2 = half ? n1 : n0;
+    rn2 += __shfl_xor(half ? n0 : n1, 32, 64);  // the partner's half of subspace g
+    // |score - exact| <= F for every codeword: split error of the MFMA dot
+    // (3 * 2^-18 |r| |C|), its float32 accumulation over three MFMAs
+    // (<= 51 u (|C|^2 / 2 + |r| |C|)) and the rounding of the sequential
+    // float32 distance of the two leading codewords (<= 18 u D / 2 with
+    // D = |r|^2 - 2 score), each taken with margin
+    const float rn = sqrtf(rn2) * 1.0001f, cm = cmx[g];
+    const float dlead = fmaxf(rn * rn - 2.0f * v2, 0.f) + 1e-30f;
+    const float F = fmaf(1.6e-5f * rn, cm, fmaf(2.5e-6f, cm * cm, 1e-6f * dlead));
+    int z = half ? bid[1] : bid[0];
+    // not separated: the float32 sequential distances decide, one flagged
+    // (token, subspace) at a time for the whole wave (lane % 16 = codeword)
+    unsigned long long fm = __ballot(valid && !(v1 - v2 > 2.0f * F));
+    while (fm) {
+      const int src = __ffsll((long long)fm) - 1;
+      fm &= fm - 1;
+      const int gs = (src >> 5) ? g1 : g0;   // uniform
+      const int tc = src & 31;
+      float rr[DP];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float mine = (gs == g0) ? r[g0][i] : r[g1][i];
+        rr[i] = __shfl(mine, tc, 64);
+        rr[8 + i] = __shfl(mine, tc + 32, 64);
+      }
+      const int cw = lane & 15;
+      const float* wc = cbk + gs * CBW + cw * DP;
+      float a = 0.f;
+#pragma unroll
+      for (int q = 0; q < DP; ++q) {
+        const float d = rr[q] - wc[q];
+        a = a + d * d;
+      }
+      if (cw >= dm.C) a = INFINITY;
+      int ai = cw;
+#pragma unroll
+      for (int o = 8; o >= 1; o >>= 1) {
+        const float oa = __shfl_xor(a, o, 64);
+        const int oi = __shfl_xor(ai, o, 64);
+        const bool take = oa < a || (oa == a && oi < ai);
+        a = take ? oa : a;
+        ai = take ? oi : ai;
+      }
+      if (lane == src) z = ai;
+    }
+    if (valid) codes[g] = (uint8_t)z;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Screen + argmin.  Workgroup = 64 evicted tokens of one unit (two 32-token
 // columns per lane, keys staged once in LDS); its 4 waves split the slot
 // tiles (t = wave, wave + 4, ...) and score them with v_mfma_f32_32x32x16_bf16 (slots = rows, tokens =
@@ -317,6 +510,7 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
   __shared__ float4 s_ma[SCREEN_WAVES][32];                   // mu_x, mu_y, qa, 2 qb
   __shared__ float2 s_mb[SCREEN_WAVES][32];                   // qc, lambda_idle * idle (+inf past the active slots)
   __shared__ Top3 s_top[SCREEN_WAVES][SCREEN_TOK];
+  __shared__ int s_asg[SCREEN_TOK];                           // final slot of each token of the tile
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // Workgroups are dealt to the 8 XCDs round-robin; logical block lb runs on
@@ -486,7 +680,7 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
   }
   __syncthreads();
   // waves 0 and 1 decide for token columns 0..31 and 32..63
-  if (wave >= 2) return;
+  if (wave < 2) {
   const int hsel = wave;
   Top3 tp = s_top[0][hsel * 32 + col];
 #pragma unroll
@@ -506,6 +700,7 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
   if (mine && nc <= 1) {
     ws.assign[unit * N + j] = tp.i1;
     ws.tgen[unit * dm.K + tp.i1] = tag;  // same value from every writer
+    s_asg[hsel * 32 + col] = tp.i1;
   }
   const bool flag = mine && nc >= 2;
 
@@ -570,6 +765,7 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
     if (lane == 0) {
       ws.assign[unit * N + jj] = k1;
       ws.tgen[unit * dm.K + k1] = tag;
+      s_asg[jj - tile * SCREEN_TOK] = k1;
       n_ref += 1;
       n_full += ncc > 2 ? 1 : 0;
       n_tie += (c2 - c1) < NEAR_TIE ? 1 : 0;
@@ -580,6 +776,21 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
     if (n_full) atomicAdd(&ws.counters[CNT_REFINED_FULL], (unsigned long long)n_full);
     if (n_tie) atomicAdd(&ws.counters[CNT_NEAR_TIES], (unsigned long long)n_tie);
   }
+  }  // waves 0 and 1
+
+  // PQ codes of the tile's assigned tokens (residuals against the centres
+  // before this fold): wave w encodes block w / 2 of K (w even) or V
+  if (dm.flags & PROTOKV_FLAG_PQ) {
+    __syncthreads();
+    const int blk = wave >> 1, kv = wave & 1;
+    const int jlo = max(nseed, tile * SCREEN_TOK), jhi = min(N, tile * SCREEN_TOK + SCREEN_TOK);
+    const int jb0 = tile * SCREEN_TOK + blk * 32;
+    if (!(jb0 >= jhi || jb0 + 32 <= jlo)) {  // uniform per wave
+      const int jj = jb0 + col;
+      const int slot = (jj >= jlo && jj < jhi) ? s_asg[blk * 32 + col] : 0;
+      pq_block<FP32>(dm, ws, fb, b, unit, jb0, jlo, jhi, kv, lane, slot);
+    }
+  }
 }
 
 hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
@@ -589,216 +800,6 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
     hipLaunchKernelGGL(k_screen<1>, grid, dim3(64 * SCREEN_WAVES), 0, st, dm, ws, fb, tpu);
   else
     hipLaunchKernelGGL(k_screen<0>, grid, dim3(64 * SCREEN_WAVES), 0, st, dm, ws, fb, tpu);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// PQ residual encoding of the assigned tokens.  The code of subspace g is the
-// nearest codeword to r = x - c (c = float32(sum / n) before this fold,
-// stored by the previous fold), defined by the float32 sequential distance
-// dist(c) = sum_u (r_u - C[c][u])^2 (u ascending, one rounding per subtract,
-// multiply and add; ties to the lower codeword).  It is found as
-// argmax_c (r . C_c - |C_c|^2 / 2) on MFMA with a rigorous error bound; a
-// subspace whose best two scores are not separated by the bound is decided by
-// the sequential float32 distances themselves.
-//
-// Workgroup = 64 tokens of one unit; wave w takes the 32-token block w / 2 of
-// K (w even) or V, with every load issued up front (no LDS, no barriers;
-// |C|^2 / 2 and max |C| per codebook come precomputed from init).  For subspaces g0 = 2p, g1 = 2p + 1, v_mfma_f32_32x32x16_bf16
-// multiplies A = codebook rows (rows 0-15: C[g0], rows 16-31: C[g1]; block
-// diagonal over two k-steps) by B = residual dims (k-step 0: g0, 1: g1), both
-// split into hi + lo bf16 (hi*hi + hi*lo + lo*hi), starting from -|C|^2 / 2.
-// ---------------------------------------------------------------------------
-constexpr int PQ_TOK = 64;
-constexpr int CBW = CMAX * DP;  // floats per (K/V, subspace) codebook block
-
-// v -> hi + lo with hi = bf16(v), lo = bf16(v - hi), both round to nearest even
-__device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const __bf16 h = (__bf16)v[i];
-    hi[i] = h;
-    lo[i] = (__bf16)(v[i] - (float)h);
-  }
-}
-
-template <int FP32>
-__global__ __launch_bounds__(256) void k_pq_encode(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int tile = blockIdx.x % tiles_per_unit;
-  const int bu = blockIdx.x / tiles_per_unit;
-  const int b = bu / dm.units, u = bu % dm.units;
-  const int N = dm.T;
-  const int nseed = fb.nseed[b];
-  const int jlo = max(nseed, tile * PQ_TOK), jhi = min(N, tile * PQ_TOK + PQ_TOK);
-  const int blk = wave >> 1, kv = wave & 1;
-  const int jb0 = tile * PQ_TOK + blk * 32;
-  if (jb0 >= jhi || jb0 + 32 <= jlo) return;  // uniform per wave
-  const size_t unit = (size_t)fb.sid[b] * dm.units + u;
-  const int col = lane & 31, half = lane >> 5;
-  const int j = jb0 + col;
-  const bool valid = j >= jlo && j < jhi;
-  const size_t ub = unit * 2 + kv;
-  const float* cbk = ws.codebooks + ub * G * CBW;
-  const float* hnp = ws.cbhn + ub * G * CMAX;
-  const float* cmx = ws.cbmax + ub * G;
-  const int slot = valid ? ws.assign[unit * N + j] : 0;
-  const size_t es = FP32 ? 4 : 2;
-  const uint8_t* xr = (kv ? ws.ring_v : ws.ring_k) +
-                      ((((unit * (dm.W + 1) + fb.slot[b]) * N) + (size_t)(valid ? j : 0)) * D) * es;
-  uint8_t* codes = ws.codes + (unit * N + (valid ? j : 0)) * (2 * G) + kv * G;
-
-  // this lane's half (dims g*16 + half*8 .. +7) of every subspace of its token
-  float r[G][8];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const int d0 = g * DP + half * 8;
-    if (FP32) {
-      *reinterpret_cast<float4*>(&r[g][0]) = *reinterpret_cast<const float4*>(xr + (size_t)d0 * 4);
-      *reinterpret_cast<float4*>(&r[g][4]) = *reinterpret_cast<const float4*>(xr + (size_t)(d0 + 4) * 4);
-    } else {
-      const u16x8 h = *reinterpret_cast<const u16x8*>(xr + (size_t)d0 * 2);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) r[g][i] = from_bf16(h[i]);
-    }
-  }
-  // A operand rows: row col < 16 holds C[2p][col][half*8 ..] (k-step 0 of pair p),
-  // row >= 16 holds C[2p+1][col-16][half*8 ..] (k-step 1)
-  float w[G / 2][8];
-#pragma unroll
-  for (int p = 0; p < G / 2; ++p) {
-    const float* wa = cbk + (2 * p + (col < 16 ? 0 : 1)) * CBW + (col & 15) * DP + half * 8;
-    *reinterpret_cast<float4*>(&w[p][0]) = *reinterpret_cast<const float4*>(wa);
-    *reinterpret_cast<float4*>(&w[p][4]) = *reinterpret_cast<const float4*>(wa + 4);
-  }
-  const float* cen = ws.cent + ((unit * dm.K + slot) * 2 + kv) * D;
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const int d0 = g * DP + half * 8;
-    const float4 c0 = *reinterpret_cast<const float4*>(cen + d0);
-    const float4 c1 = *reinterpret_cast<const float4*>(cen + d0 + 4);
-    const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) r[g][i] = valid ? r[g][i] - cc[i] : 0.f;
-  }
-  const bf16x8 zero8 = {};
-  const bool lowrows = col < 16;
-
-#pragma unroll
-  for (int p = 0; p < G / 2; ++p) {
-    const int g0 = 2 * p, g1 = 2 * p + 1;
-    bf16x8 ah, al, b0h, b0l, b1h, b1l;
-    split8(w[p], ah, al);
-    split8(r[g0], b0h, b0l);
-    split8(r[g1], b1h, b1l);
-    const bf16x8 a0h = lowrows ? ah : zero8, a0l = lowrows ? al : zero8;
-    const bf16x8 a1h = lowrows ? zero8 : ah, a1l = lowrows ? zero8 : al;
-    float n0 = 0.f, n1 = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      n0 = fmaf(r[g0][i], r[g0][i], n0);
-      n1 = fmaf(r[g1][i], r[g1][i], n1);
-    }
-    // accumulator rows (rr / 4) * 8 + half * 4 + rr % 4: rr < 8 -> codeword of g0, else of g1
-    f32x16 acc;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float4 h = *reinterpret_cast<const float4*>(hnp + (q < 2 ? g0 : g1) * CMAX + (q & 1) * 8 + half * 4);
-      acc[4 * q + 0] = -h.x;
-      acc[4 * q + 1] = -h.y;
-      acc[4 * q + 2] = -h.z;
-      acc[4 * q + 3] = -h.w;
-    }
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0h, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0l, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0l, b0h, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1h, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1l, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1l, b1h, acc, 0, 0, 0);
-
-    // best two scores per subspace: 8 codewords here, 8 in the partner lane
-    float bst1[2], bst2[2];
-    int bid[2];
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      float v1 = -INFINITY, v2 = -INFINITY;
-      int i1 = 0;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const float v = acc[sub * 8 + q];
-        const int cw = (q >> 2) * 8 + half * 4 + (q & 3);
-        const int mk = -(int)(v > v1);
-        v2 = __builtin_amdgcn_fmed3f(v, v1, v2);
-        v1 = fmaxf(v1, v);
-        i1 = (cw & mk) | (i1 & ~mk);
-      }
-      const float o1 = __shfl_xor(v1, 32, 64), o2 = __shfl_xor(v2, 32, 64);
-      const int oi = __shfl_xor(i1, 32, 64);
-      const bool take = o1 > v1 || (o1 == v1 && oi < i1);
-      bst2[sub] = fmaxf(fminf(v1, o1), fmaxf(v2, o2));
-      bst1[sub] = fmaxf(v1, o1);
-      bid[sub] = take ? oi : i1;
-    }
-    // lane half 0 settles g0, half 1 settles g1
-    const int g = half ? g1 : g0;
-    const float v1 = half ? bst1[1] : bst1[0], v2 = half ? bst2[1] : bst2[0];
-    float rn2 = half ? n1 : n0;
-    rn2 += __shfl_xor(half ? n0 : n1, 32, 64);  // the partner's half of subspace g
-    // |score - exact| <= F for every codeword: split error of the MFMA dot
-    // (3 * 2^-18 |r| |C|), its float32 accumulation over three MFMAs
-    // (<= 51 u (|C|^2 / 2 + |r| |C|)) and the rounding of the sequential
-    // float32 distance of the two leading codewords (<= 18 u D / 2 with
-    // D = |r|^2 - 2 score), each taken with margin
-    const float rn = sqrtf(rn2) * 1.0001f, cm = cmx[g];
-    const float dlead = fmaxf(rn * rn - 2.0f * v2, 0.f) + 1e-30f;
-    const float F = fmaf(1.6e-5f * rn, cm, fmaf(2.5e-6f, cm * cm, 1e-6f * dlead));
-    int z = half ? bid[1] : bid[0];
-    // not separated: the float32 sequential distances decide, one flagged
-    // (token, subspace) at a time for the whole wave (lane % 16 = codeword)
-    unsigned long long fm = __ballot(valid && !(v1 - v2 > 2.0f * F));
-    while (fm) {
-      const int src = __ffsll((long long)fm) - 1;
-      fm &= fm - 1;
-      const int gs = (src >> 5) ? g1 : g0;   // uniform
-      const int tc = src & 31;
-      float rr[DP];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float mine = (gs == g0) ? r[g0][i] : r[g1][i];
-        rr[i] = __shfl(mine, tc, 64);
-        rr[8 + i] = __shfl(mine, tc + 32, 64);
-      }
-      const int cw = lane & 15;
-      const float* wc = cbk + gs * CBW + cw * DP;
-      float a = 0.f;
-#pragma unroll
-      for (int q = 0; q < DP; ++q) {
-        const float d = rr[q] - wc[q];
-        a = a + d * d;
-      }
-      if (cw >= dm.C) a = INFINITY;
-      int ai = cw;
-#pragma unroll
-      for (int o = 8; o >= 1; o >>= 1) {
-        const float oa = __shfl_xor(a, o, 64);
-        const int oi = __shfl_xor(ai, o, 64);
-        const bool take = oa < a || (oa == a && oi < ai);
-        a = take ? oa : a;
-        ai = take ? oi : ai;
-      }
-      if (lane == src) z = ai;
-    }
-    if (valid) codes[g] = (uint8_t)z;
-  }
-}
-
-hipError_t launch_pq_encode(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
-  int tpu = (dm.T + PQ_TOK - 1) / PQ_TOK;
-  dim3 grid(fb.n * dm.units * tpu);
-  if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_pq_encode<1>, grid, dim3(256), 0, st, dm, ws, fb, tpu);
-  else
-    hipLaunchKernelGGL(k_pq_encode<0>, grid, dim3(256), 0, st, dm, ws, fb, tpu);
   return hipGetLastError();
 }
 
@@ -827,16 +828,29 @@ __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBa
   if (nseed >= N || k >= kact) return;  // uniform per wave
   const size_t unit = (size_t)fb.sid[b] * dm.units + u;
   const size_t si = unit * dm.K + k;
-  if (ws.tgen[si] != (uint32_t)fb.fe[b] + 1u) return;  // no token this fold
   const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
   const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
+  // the tag and the first chunk of the (small, cached) assignment vector are
+  // loaded together; a slot without this fold's tag leaves after that round
+  // trip, a tagged one loads its row while it compacts its token list
+  const uint32_t tag = ws.tgen[si];
+  const int a0 = (lane < N && lane >= nseed) ? ws.assign[unit * N + lane] : -1;
+  if (tag != (uint32_t)fb.fe[b] + 1u) return;  // no token this fold
+  uint8_t* row = ws.bank + si * ROW;
+  float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
+  float2 sv = reinterpret_cast<const float2*>(row + ROW_SUMV)[lane];
+  float2 qk = reinterpret_cast<const float2*>(row + ROW_SQK)[lane];
+  float2 qv = reinterpret_cast<const float2*>(row + ROW_SQV)[lane];
+  uint2 hk = reinterpret_cast<const uint2*>(row + ROW_HK)[lane];
+  uint2 hv = reinterpret_cast<const uint2*>(row + ROW_HV)[lane];
+  RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
 
   // this slot's tokens, in eviction order
   const unsigned long long below = (1ull << lane) - 1ull;
   int ntok = 0;
   for (int c = 0; c * 64 < N; ++c) {
     const int jj = c * 64 + lane;
-    const int a = (jj < N && jj >= nseed) ? ws.assign[unit * N + jj] : -1;
+    const int a = c == 0 ? a0 : ((jj < N && jj >= nseed) ? ws.assign[unit * N + jj] : -1);
     const unsigned long long mk = __ballot(a == k);
     if (a == k) s_tok[wave][ntok + __popcll(mk & below)] = (uint16_t)jj;
     ntok += __popcll(mk);
@@ -846,14 +860,6 @@ __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBa
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-  uint8_t* row = ws.bank + si * ROW;
-  float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
-  float2 sv = reinterpret_cast<const float2*>(row + ROW_SUMV)[lane];
-  float2 qk = reinterpret_cast<const float2*>(row + ROW_SQK)[lane];
-  float2 qv = reinterpret_cast<const float2*>(row + ROW_SQV)[lane];
-  uint2 hk = reinterpret_cast<const uint2*>(row + ROW_HK)[lane];
-  uint2 hv = reinterpret_cast<const uint2*>(row + ROW_HV)[lane];
-  RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
   const float eta = dm.eta, keep = 1.0f - dm.eta;
   const int gl = lane >> 3, c0 = 2 * (lane & 7);
   auto fetch = [&](int jj, float2& kk, float2& vv, int& zk, int& zv) {

@@ -133,8 +133,6 @@ hipError_t launch_seed(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                        hipStream_t st);
 hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                          hipStream_t st);
-hipError_t launch_pq_encode(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
-                            hipStream_t st);
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                             hipStream_t st);
 hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st);

@@ -396,9 +396,6 @@ protokv_status protokv_fold(protokv_t h, void* stream) {
     if (st == PROTOKV_OK && any_assign)
       st = h->dev(h->launch(PROTOKV_K_SCREEN, hs, [&] { return launch_screen(h->dm, h->ws, fb, hs); }),
                   "fold/screen");
-    if (st == PROTOKV_OK && any_assign && (h->dm.flags & PROTOKV_FLAG_PQ))
-      st = h->dev(h->launch(PROTOKV_K_PQ_ENCODE, hs, [&] { return launch_pq_encode(h->dm, h->ws, fb, hs); }),
-                  "fold/pq_encode");
     if (st == PROTOKV_OK && any_assign)
       st = h->dev(h->launch(PROTOKV_K_AGGREGATE, hs, [&] { return launch_aggregate(h->dm, h->ws, fb, hs); }),
                   "fold/aggregate");

@@ -257,6 +257,32 @@ __device__ void decode_top_s_small(const uint32_t* hist /* [G][CMAX] */, int C, 
 // advances.  Same beam (width S) and order as decode_top_s.
 constexpr int DEC_BEAMS = 16;  // beams per wave
 
+// Exchanges within a quad of lanes (DPP quad_perm, no LDS round trip).
+template <int CTRL>
+__device__ __forceinline__ uint32_t qperm(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ uint64_t qperm64(uint64_t x) {
+  return (uint64_t)qperm<CTRL>((uint32_t)x) | ((uint64_t)qperm<CTRL>((uint32_t)(x >> 32)) << 32);
+}
+constexpr int QP_XOR1 = 0xB1;  // lanes (1, 0, 3, 2)
+constexpr int QP_XOR2 = 0x4E;  // lanes (2, 3, 0, 1)
+
+// (pa, ca) ranks before (pb, cb), without branches
+__device__ __forceinline__ bool before128b(const U128& pa, uint32_t ca, const U128& pb, uint32_t cb) {
+  const bool gh = pa.hi > pb.hi, eh = pa.hi == pb.hi, gl = pa.lo > pb.lo, el = pa.lo == pb.lo;
+  return gh | (eh & (gl | (el & (ca < cb))));
+}
+__device__ __forceinline__ uint64_t sel64(bool t, uint64_t a, uint64_t b) {
+  const uint64_t m = 0ull - (uint64_t)t;
+  return (a & m) | (b & ~m);
+}
+__device__ __forceinline__ uint32_t sel32(bool t, uint32_t a, uint32_t b) {
+  const uint32_t m = 0u - (uint32_t)t;
+  return (a & m) | (b & ~m);
+}
+
 template <int SM>
 __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid, int n_active) {
   constexpr int E = SM / 4;  // prefixes per lane
@@ -279,7 +305,6 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
   const bool mine = bvalid && !nores && m.n_res <= 65534u && S <= SM;
   const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
   const int R = S < C ? S : C;
-  const int gbase = lane & ~3;
 
   U128 pp[E];
   uint32_t pc[E];
@@ -303,13 +328,14 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
     }
     int rk[4] = {0, 0, 0, 0};
 #pragma unroll
-    for (int src = 0; src < 4; ++src)
+    for (int i2 = 0; i2 < 4; ++i2) {
+      const uint32_t others[4] = {qperm<0x00>(key[i2]), qperm<0x55>(key[i2]), qperm<0xAA>(key[i2]),
+                                  qperm<0xFF>(key[i2])};
 #pragma unroll
-      for (int i2 = 0; i2 < 4; ++i2) {
-        const uint32_t other = __shfl(key[i2], gbase + src, 64);
+      for (int src = 0; src < 4; ++src)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) rk[i] += other > key[i] ? 1 : 0;
-      }
+        for (int i = 0; i < 4; ++i) rk[i] += others[src] > key[i] ? 1 : 0;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       if (key[i] != 0u && rk[i] < R) s_rank[wave][bq][rk[i]] = key[i];
@@ -342,37 +368,66 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
         uint32_t bc = hc[0];
         int bj = 0;
 #pragma unroll
-        for (int j = 1; j < E; ++j)
-          if (before128(hp[j], hc[j], bv, bc)) { bv = hp[j]; bc = hc[j]; bj = j; }
-        int who = q * E + bj;
+        for (int j = 1; j < E; ++j) {
+          const bool t = before128b(hp[j], hc[j], bv, bc);
+          bv.lo = sel64(t, hp[j].lo, bv.lo);
+          bv.hi = sel64(t, hp[j].hi, bv.hi);
+          bc = sel32(t, hc[j], bc);
+          bj = t ? j : bj;
+        }
+        uint32_t who = (uint32_t)(q * E + bj);
         // best of the four lanes
 #pragma unroll
-        for (int x = 1; x <= 2; x <<= 1) {
+        for (int x = 0; x < 2; ++x) {
           U128 ov;
-          ov.lo = __shfl_xor(bv.lo, x, 64);
-          ov.hi = __shfl_xor(bv.hi, x, 64);
-          const uint32_t oc = __shfl_xor(bc, x, 64);
-          const int ow = __shfl_xor(who, x, 64);
-          if (before128(ov, oc, bv, bc)) { bv = ov; bc = oc; who = ow; }
-        }
-        if ((o & 3) == q) { np[o >> 2] = bv; nc[o >> 2] = bc; }
-        // the winning row moves to its next rank
-        if (who / E == q) {
-          const int j = who % E;
-#pragma unroll
-          for (int jj = 0; jj < E; ++jj) {
-            if (jj == j) {
-              ptr[jj] += 1;
-              if (ptr[jj] < R) {
-                const uint32_t kk = s_rank[wave][bq][ptr[jj]];
-                hp[jj] = mul_u128_u32(pp[jj], ((kk - 1u) >> 4) + 1u);
-                hc[jj] = pc[jj] | ((15u - ((kk - 1u) & 15u)) << shift);
-              } else {
-                hp[jj] = U128{0, 0};
-                hc[jj] = 0xFFFFFFFFu;
-              }
-            }
+          uint32_t oc, ow;
+          if (x == 0) {
+            ov.lo = qperm64<QP_XOR1>(bv.lo); ov.hi = qperm64<QP_XOR1>(bv.hi);
+            oc = qperm<QP_XOR1>(bc); ow = qperm<QP_XOR1>(who);
+          } else {
+            ov.lo = qperm64<QP_XOR2>(bv.lo); ov.hi = qperm64<QP_XOR2>(bv.hi);
+            oc = qperm<QP_XOR2>(bc); ow = qperm<QP_XOR2>(who);
           }
+          const bool t = before128b(ov, oc, bv, bc);
+          bv.lo = sel64(t, ov.lo, bv.lo);
+          bv.hi = sel64(t, ov.hi, bv.hi);
+          bc = sel32(t, oc, bc);
+          who = sel32(t, ow, who);
+        }
+        {
+          const bool rec = (o & 3) == q;
+          np[o >> 2].lo = sel64(rec, bv.lo, np[o >> 2].lo);
+          np[o >> 2].hi = sel64(rec, bv.hi, np[o >> 2].hi);
+          nc[o >> 2] = sel32(rec, bc, nc[o >> 2]);
+        }
+        // the winning row moves to its next rank: one product, then selects
+        const bool iwin = (int)(who / E) == q;
+        const int j = (int)(who % E);
+        int pj = ptr[0];
+        U128 base = pp[0];
+        uint32_t bcode = pc[0];
+#pragma unroll
+        for (int jj = 1; jj < E; ++jj) {
+          const bool t = jj == j;
+          pj = t ? ptr[jj] : pj;
+          base.lo = sel64(t, pp[jj].lo, base.lo);
+          base.hi = sel64(t, pp[jj].hi, base.hi);
+          bcode = sel32(t, pc[jj], bcode);
+        }
+        pj += 1;
+        const bool more = pj < R;
+        const uint32_t kk = s_rank[wave][bq][more ? pj : 0];
+        U128 nh = mul_u128_u32(base, ((kk - 1u) >> 4) + 1u);
+        nh.lo = more ? nh.lo : 0ull;
+        nh.hi = more ? nh.hi : 0ull;
+        const uint32_t ncode = more ? (bcode | ((15u - ((kk - 1u) & 15u)) << shift)) : 0xFFFFFFFFu;
+#pragma unroll
+        for (int jj = 0; jj < E; ++jj) {
+          const bool t = iwin && jj == j;
+          ptr[jj] = t ? pj : ptr[jj];
+          hp[jj].lo = sel64(t, nh.lo, hp[jj].lo);
+          hp[jj].hi = sel64(t, nh.hi, hp[jj].hi);
+          hc[jj] = sel32(t, ncode, hc[jj]);
         }
       }
     }
@@ -453,25 +508,39 @@ __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int 
     const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
     ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
   }
+  // the decoded tuples of K and V first (all loads in flight together)
+  const uint32_t* codes_k = ws.pcodes + (((size_t)u * dm.K + p) * 2) * (SMAX + 1);
+  const uint32_t* codes_v = codes_k + (SMAX + 1);
+  uint32_t ck[SMAX], cv[SMAX];
+#pragma unroll
+  for (int s2 = 0; s2 < SMAX; ++s2) {
+    ck[s2] = s2 < S ? codes_k[s2] : 0u;
+    cv[s2] = s2 < S ? codes_v[s2] : 0u;
+  }
+  const bool nores_k = codes_k[SMAX] != 0u, nores_v = codes_v[SMAX] != 0u;
+  const int sh = 4 * (G - 1 - g);
 #pragma unroll
   for (int w = 0; w < 2; ++w) {
     const float2 c = w ? make_float2(sv.x / nf, sv.y / nf) : make_float2(sk.x / nf, sk.y / nf);
-    const uint32_t* codes = ws.pcodes + (((size_t)u * dm.K + p) * 2 + w) * (SMAX + 1);
-    const bool nores = codes[SMAX] != 0u;
+    const bool nores = w ? nores_v : nores_k;
+    const float* cbw = cbk + ((size_t)w * G + g) * CMAX * DP + u16;
     uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * S + (size_t)p * S) * D * es;
-    for (int s2 = 0; s2 < S; ++s2) {
-      float2 val = c;
-      if (!nores) {
-        const int z = (codes[s2] >> (4 * (G - 1 - g))) & 15;
-        const float2 cw = *reinterpret_cast<const float2*>(cbk + ((w * G + g) * CMAX + z) * DP + u16);
-        val.x = c.x + cw.x;
-        val.y = c.y + cw.y;
-      }
-      if (FP32) {
-        reinterpret_cast<float2*>(out + (size_t)s2 * D * 4)[lane] = val;
-      } else {
-        const uint32_t packed = (uint32_t)q_to_bf16(val.x) | ((uint32_t)q_to_bf16(val.y) << 16);
-        reinterpret_cast<uint32_t*>(out + (size_t)s2 * D * 2)[lane] = packed;
+#pragma unroll
+    for (int s2 = 0; s2 < SMAX; ++s2) {
+      if (s2 < S) {
+        float2 val = c;
+        if (!nores) {
+          const int z = ((w ? cv[s2] : ck[s2]) >> sh) & 15;
+          const float2 cw = *reinterpret_cast<const float2*>(cbw + z * DP);
+          val.x = c.x + cw.x;
+          val.y = c.y + cw.y;
+        }
+        if (FP32) {
+          reinterpret_cast<float2*>(out + (size_t)s2 * D * 4)[lane] = val;
+        } else {
+          const uint32_t packed = (uint32_t)q_to_bf16(val.x) | ((uint32_t)q_to_bf16(val.y) << 16);
+          reinterpret_cast<uint32_t*>(out + (size_t)s2 * D * 2)[lane] = packed;
+        }
       }
     }
   }
