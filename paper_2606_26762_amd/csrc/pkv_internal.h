@@ -16,6 +16,7 @@ constexpr int CMAX = 16;   // codewords per subspace (storage)
 constexpr int SMAX = 16;   // pseudo-tokens per prototype
 constexpr int TMAX = 1024; // tokens per frame
 constexpr int MAXB = 64;   // streams per launch batch
+constexpr int MAX_SPLITS = 16;  // attention context splits (partials storage)
 constexpr int MAX_RBLOCKS = 2;  // query-row blocks of 256 per kv head
 
 // Bank row (one prototype slot), byte offsets; see protokv.h.

@@ -15,7 +15,6 @@ using namespace pkv;
 
 namespace {
 
-constexpr int MAX_SPLITS = 16;
 constexpr int MAX_ROWS = 512;  // query rows per kv head per attend call
 
 struct StreamState {

@@ -894,36 +894,53 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
 // Combines the splits of each query row: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
 template <int FP32>
 __global__ __launch_bounds__(256) void k_attend_merge(Dims dm, Workspace ws, AttendArgs aa, int rows) {
-  const int lane = threadIdx.x & 63;
-  const int gr = blockIdx.x * 4 + (threadIdx.x >> 6);   // (kv head, row) pair
-  if (gr >= dm.units * rows) return;
-  const int r = gr % rows;
-  const int u = gr / rows;
+  // thread = (kv head, query row, 4 output dims); every split's (m, l) and
+  // partial O are loaded together
+  const size_t gt = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (gt >= (size_t)dm.units * rows * (D / 4)) return;
+  const int d4 = (int)(gt % (D / 4));
+  const int r = (int)((gt / (D / 4)) % rows);
+  const int u = (int)(gt / ((size_t)(D / 4) * rows));
   const int grp = dm.Hq / dm.Hkv;
   const int l = u / dm.Hkv, kvh = u % dm.Hkv;
+  float ms[MAX_SPLITS], ls[MAX_SPLITS];
+  float4 ov[MAX_SPLITS];
   float M = -INFINITY;
-  for (int s = 0; s < aa.splits; ++s)
-    M = fmaxf(M, ws.part_ml[(((size_t)u * dm.max_splits + s) * dm.max_rows + r) * 2]);
-  float Lsum = 0.f, o0 = 0.f, o1 = 0.f;
-  for (int s = 0; s < aa.splits; ++s) {
-    const size_t pr = ((size_t)u * dm.max_splits + s) * dm.max_rows + r;
-    const float ms = ws.part_ml[pr * 2], ls = ws.part_ml[pr * 2 + 1];
-    const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
-    Lsum += w * ls;
-    const float2 ov = reinterpret_cast<const float2*>(ws.part_o + pr * D)[lane];
-    o0 += w * ov.x;
-    o1 += w * ov.y;
+#pragma unroll
+  for (int s2 = 0; s2 < MAX_SPLITS; ++s2) {
+    if (s2 < aa.splits) {
+      const size_t pr = ((size_t)u * dm.max_splits + s2) * dm.max_rows + r;
+      ms[s2] = ws.part_ml[pr * 2];
+      ls[s2] = ws.part_ml[pr * 2 + 1];
+      ov[s2] = reinterpret_cast<const float4*>(ws.part_o + pr * D)[d4];
+      M = fmaxf(M, ms[s2]);
+    }
+  }
+  float Lsum = 0.f;
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int s2 = 0; s2 < MAX_SPLITS; ++s2) {
+    if (s2 < aa.splits) {
+      const float w = ms[s2] == -INFINITY ? 0.f : exp2f(ms[s2] - M);
+      Lsum += w * ls[s2];
+      o.x += w * ov[s2].x;
+      o.y += w * ov[s2].y;
+      o.z += w * ov[s2].z;
+      o.w += w * ov[s2].w;
+    }
   }
   const float inv = Lsum > 0.f ? 1.0f / Lsum : 0.f;
   const int t = r / grp, gg = r % grp;
   const size_t orow = (((size_t)l * aa.tq + t) * dm.Hq + kvh * grp + gg) * D;
   if (FP32) {
-    reinterpret_cast<float2*>(reinterpret_cast<float*>(aa.o) + orow)[lane] = make_float2(o0 * inv, o1 * inv);
+    reinterpret_cast<float4*>(reinterpret_cast<float*>(aa.o) + orow)[d4] =
+        make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv);
   } else {
-    reinterpret_cast<uint32_t*>(reinterpret_cast<uint16_t*>(aa.o) + orow)[lane] =
-        (uint32_t)q_to_bf16(o0 * inv) | ((uint32_t)q_to_bf16(o1 * inv) << 16);
+    const uint2 packed = make_uint2((uint32_t)q_to_bf16(o.x * inv) | ((uint32_t)q_to_bf16(o.y * inv) << 16),
+                                    (uint32_t)q_to_bf16(o.z * inv) | ((uint32_t)q_to_bf16(o.w * inv) << 16));
+    reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(aa.o) + orow)[d4] = packed;
   }
-  if (lane == 0 && aa.lse) aa.lse[((size_t)l * aa.tq + t) * dm.Hq + kvh * grp + gg] = (M + log2f(Lsum)) * LN2;
+  if (d4 == 0 && aa.lse) aa.lse[((size_t)l * aa.tq + t) * dm.Hq + kvh * grp + gg] = (M + log2f(Lsum)) * LN2;
 }
 
 // float32 path (small fp32 streams): one wave per (kv head, query row, split),
@@ -989,7 +1006,7 @@ hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& 
 hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa, hipStream_t st) {
   if (!dm.kv_fp32 && aa.splits == 1) return hipSuccess;  // the bf16 readout wrote O directly
   const int rows = aa.tq * (dm.Hq / dm.Hkv);
-  const int nb = (dm.units * rows + 3) / 4;
+  const int nb = (int)(((size_t)dm.units * rows * (D / 4) + 255) / 256);
   if (dm.kv_fp32)
     hipLaunchKernelGGL(k_attend_merge<1>, dim3(nb), dim3(256), 0, st, dm, ws, aa, rows);
   else
