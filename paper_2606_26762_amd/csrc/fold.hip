@@ -818,8 +818,13 @@ template <int FP32>
 __global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int chunks_per_unit) {
   __shared__ uint16_t s_tok[4][TMAX];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int chunk = blockIdx.x % chunks_per_unit;
-  const int bu = blockIdx.x / chunks_per_unit;
+  // same XCD placement as the screen (consecutive logical blocks share an
+  // XCD), so a unit's assignments, tags and evicted tokens are read from the
+  // L2 the screen left them in
+  const int nblk = (int)gridDim.x, per = nblk >> 3, bid = (int)blockIdx.x;
+  const int lb = bid < per * 8 ? (bid & 7) * per + (bid >> 3) : bid;
+  const int chunk = lb % chunks_per_unit;
+  const int bu = lb / chunks_per_unit;
   const int b = bu / dm.units, u = bu % dm.units;
   const int N = dm.T;
   const int nseed = fb.nseed[b];
