@@ -38,8 +38,10 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK = 2500.0     # dense bf16 TFLOP/s
-ROW_BYTES_USED = 3104       # bytes of a bank row that carry state
-CACHE_BYTES = 2 * 128 * 2 + 32   # hi + lo bf16 unit centre + screening meta
+ROW_STATS_BYTES = 4 * 128 * 4 + 32   # a bank row's four sums and its meta
+HIST_BYTES = 2 * 8 * 16 * 4          # a bank row's K and V histograms
+CACHE_BYTES = 2 * 128 * 2 + 32       # hi + lo bf16 unit centre + screening meta
+CODEBOOK_BYTES = 2 * 8 * 16 * 16 * 4  # a unit's K and V codebooks
 
 
 def parse():
@@ -51,8 +53,8 @@ def parse():
     ap.add_argument("--profile-frames", type=int, default=32)
     ap.add_argument("--query-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=16)
-    ap.add_argument("--cpu-frames", type=int, default=24)
+    ap.add_argument("--cpu-units", type=int, default=32)
+    ap.add_argument("--cpu-frames", type=int, default=64)
     return ap.parse_args()
 
 
@@ -63,15 +65,16 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     if kernel == "ring_insert":
         return U * T * D * b * 2 * 2                       # read frame K,V + write ring K,V
     if kernel == "screen":
-        # assignment: evicted keys, centre cache, assignment written;
-        # PQ encoding: evicted values, the touched slots' centres (K and V),
-        # codebooks, codes written
-        return (U * (2 * T * D * b + K * CACHE_BYTES + T * 4 + 2 * 8 * 16 * 16 * 4 + T * 16)
-                + touched_per_launch * 2 * D * 4)
+        # assignment: evicted keys, the unit's centre cache, assignments
+        # written; PQ encoding: evicted values, codebooks, per touched slot
+        # its K and V sums (centres) and its two histograms read and written
+        return (U * (2 * T * D * b + K * CACHE_BYTES + T * 4 + CODEBOOK_BYTES)
+                + touched_per_launch * (2 * D * 4 + 2 * HIST_BYTES))
     if kernel == "aggregate":
-        return (U * (2 * T * D * b + T * 4 + T * 16)                   # evicted K,V, assignment, codes
-                + touched_per_launch * (2 * ROW_BYTES_USED + CACHE_BYTES   # row RMW + cache rewrite
-                                        + 2 * D * 4))                   # + the new K and V centres
+        # evicted K and V, assignments; per touched slot its sums, sums of
+        # squares and meta read and written and its screening copy rewritten
+        return (U * (2 * T * D * b + T * 4)
+                + touched_per_launch * (2 * ROW_STATS_BYTES + CACHE_BYTES))
     if kernel == "decode":
         return U * n_active * (2 * 8 * 16 * 4 + 32 + 2 * (S + 1) * 4)       # histograms, meta, codes out
     if kernel == "materialize":
@@ -83,7 +86,7 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     return 0
 
 
-FOLD_KERNELS = ("ring_insert", "seed", "screen", "pq_encode", "aggregate")
+FOLD_KERNELS = ("ring_insert", "seed", "screen", "aggregate")
 KERNEL_SOURCES = {k: "fold.hip" for k in FOLD_KERNELS}
 KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "attend", "attend_merge")})
 

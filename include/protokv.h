@@ -68,7 +68,7 @@ typedef struct {
   int32_t head_dim;         /* D, must be 128 */
   int32_t grid_h, grid_w;   /* visual tokens per frame T = grid_h * grid_w, raster order */
   int32_t window_frames;    /* near window W in frames (W * T tokens) */
-  int32_t capacity;         /* K_max prototype slots per (stream, layer, kv head) */
+  int32_t capacity;         /* K_max prototype slots per (stream, layer, kv head), 1..65535 */
   int32_t pseudo_per_proto; /* S */
   int32_t pq_subspaces;     /* G, must be 8 */
   int32_t pq_codewords;     /* C, 2..16 */

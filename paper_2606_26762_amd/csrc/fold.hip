@@ -11,6 +11,8 @@
 // Every state update below is written as an explicit float32 operation
 // sequence (the library is compiled with -ffp-contract=off), so the bank is
 // reproducible bit for bit.
+#include <algorithm>
+
 #include "pkv_internal.h"
 
 namespace pkv {
@@ -56,6 +58,27 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// The lane id as a value the compiler cannot see through: per-lane index
+// arithmetic derived from it is recomputed where it is used instead of being
+// hoisted out of loops and held in registers for the whole kernel.
+__device__ __forceinline__ int opaque_lane() {
+  int l = (int)(threadIdx.x & 63);
+  asm volatile("" : "+v"(l));
+  return l;
+}
+
+// Sum over the 16 lanes of a lane group (lanes 16m .. 16m+15).
+__device__ __forceinline__ float group16_sum(float v) {
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ int group16_sum_i(int v) {
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
 // Cell-centre coordinates of token j (float32, same operations as the oracle).
 __device__ __forceinline__ void token_xy(int j, int gw, int gh, float& x, float& y) {
   int row = j / gw, col = j - row * gw;
@@ -93,17 +116,56 @@ __device__ void refresh_cache(const Dims& dm, float2 sk, const RowMeta& m, size_
   }
 }
 
+// As refresh_cache, for a slot owned by a 16-lane group: s = this lane's
+// components [8 il, 8 il + 8) of sum_k.
+__device__ void refresh_cache16(const Dims& dm, const float (&s)[8], const RowMeta& m, size_t unit, int k,
+                                const Workspace& ws, int il) {
+  float part = 0.f;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) part += s[q] * s[q];
+  const float nsq = group16_sum(part);
+  const float inv = nsq > 0.f ? 1.0f / sqrtf(nsq) : 0.f;
+  u16x8 hi, lo;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const float c = s[q] * inv;
+    const uint16_t h = to_bf16(c);
+    hi[q] = h;
+    lo[q] = to_bf16(c - from_bf16(h));
+  }
+  // components 8 il .. 8 il + 7 are contiguous in the swizzled layout
+  const size_t off = unit * (size_t)cap32(dm.K) * D + chat_offset(k, 8 * il);
+  *reinterpret_cast<u16x8*>(ws.chat_hi + off) = hi;
+  *reinterpret_cast<u16x8*>(ws.chat_lo + off) = lo;
+  if (il == 0) {
+    double A = (double)m.sxx + dm.ridge, B = (double)m.sxy, Cc = (double)m.syy + dm.ridge;
+    double det = A * Cc - B * B;
+    CacheMeta c;
+    c.mu_x = m.mu_x;
+    c.mu_y = m.mu_y;
+    c.qa = (float)(Cc / det);
+    c.qb = (float)(-B / det);
+    c.qc = (float)(A / det);
+    c.last_frame = m.tau / dm.T;
+    c.active = m.n > 0 ? 1u : 0u;
+    c.pad = 0.f;
+    ws.cmeta[unit * dm.K + k] = c;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Near ring insert: frame -> ring slot (f mod (W+1)) of each listed stream.
-// Workgroup = one quarter of one (batch entry, unit): its frame of K and of V
-// is one contiguous block on both sides, copied 16 bytes per thread with eight
-// loads in flight before the stores.
-constexpr int RING_PARTS = 4;
+// Workgroup = one part of one (batch entry, unit): its frame of K and of V is
+// one contiguous block on both sides, split into parts of at most 1024
+// 16-byte chunks so that every thread issues all of its (up to 4 + 4) loads
+// before its first store.
 // ---------------------------------------------------------------------------
+constexpr int RING_CHUNKS = 1024;  // 16-byte chunks of K (and of V) per workgroup
+
 __global__ __launch_bounds__(256) void k_ring_insert(Dims dm, Workspace ws, AppendBatch ab,
                                                      const uint8_t* k, const uint8_t* v,
-                                                     size_t unit_bytes) {
-  const int part = blockIdx.x % RING_PARTS, eu = blockIdx.x / RING_PARTS;
+                                                     size_t unit_bytes, int parts) {
+  const int part = blockIdx.x % parts, eu = blockIdx.x / parts;
   const int e = eu / dm.units, unit = eu % dm.units;
   const size_t dst = (((size_t)ab.sid[e] * dm.units + unit) * (dm.W + 1) + ab.slot[e]) * unit_bytes;
   const size_t src = ((size_t)e * dm.units + unit) * unit_bytes;
@@ -112,28 +174,26 @@ __global__ __launch_bounds__(256) void k_ring_insert(Dims dm, Workspace ws, Appe
   uint4* kd = reinterpret_cast<uint4*>(ws.ring_k + dst);
   uint4* vd = reinterpret_cast<uint4*>(ws.ring_v + dst);
   const int n16 = (int)(unit_bytes / 16);
-  const int per = (n16 + RING_PARTS - 1) / RING_PARTS;
-  const int lo = part * per, n = min(n16, lo + per);
-  int i = lo + threadIdx.x;
-  for (; i + 3 * 256 < n; i += 4 * 256) {
-    const uint4 a0 = ks[i], a1 = ks[i + 256], a2 = ks[i + 512], a3 = ks[i + 768];
-    const uint4 c0 = vs[i], c1 = vs[i + 256], c2 = vs[i + 512], c3 = vs[i + 768];
-    kd[i] = a0; kd[i + 256] = a1; kd[i + 512] = a2; kd[i + 768] = a3;
-    vd[i] = c0; vd[i + 256] = c1; vd[i + 512] = c2; vd[i + 768] = c3;
-  }
-  for (; i < n; i += 256) {
-    const uint4 a0 = ks[i], c0 = vs[i];
-    kd[i] = a0;
-    vd[i] = c0;
-  }
+  const int lo = part * RING_CHUNKS, hi = min(n16, lo + RING_CHUNKS);
+  // loads unconditional (index clamped into the part, which is never empty)
+  // so that all eight are in flight together; stores predicated
+  // (named registers, not an array: a private array here gets promoted to LDS)
+  const int i0 = lo + (int)threadIdx.x, i1 = i0 + 256, i2 = i0 + 512, i3 = i0 + 768;
+  const uint4 a0 = ks[min(i0, hi - 1)], a1 = ks[min(i1, hi - 1)], a2 = ks[min(i2, hi - 1)], a3 = ks[min(i3, hi - 1)];
+  const uint4 c0 = vs[min(i0, hi - 1)], c1 = vs[min(i1, hi - 1)], c2 = vs[min(i2, hi - 1)], c3 = vs[min(i3, hi - 1)];
+  if (i0 < hi) { kd[i0] = a0; vd[i0] = c0; }
+  if (i1 < hi) { kd[i1] = a1; vd[i1] = c1; }
+  if (i2 < hi) { kd[i2] = a2; vd[i2] = c2; }
+  if (i3 < hi) { kd[i3] = a3; vd[i3] = c3; }
 }
 
 hipError_t launch_ring_insert(const Dims& dm, const Workspace& ws, const AppendBatch& ab,
                               const void* k, const void* v, hipStream_t st) {
   size_t es = dm.kv_fp32 ? 4 : 2;
   size_t unit_bytes = (size_t)dm.T * D * es;   // a multiple of 256
-  hipLaunchKernelGGL(k_ring_insert, dim3(ab.n * dm.units * RING_PARTS), dim3(256), 0, st, dm, ws, ab,
-                     (const uint8_t*)k, (const uint8_t*)v, unit_bytes);
+  const int parts = (int)((unit_bytes / 16 + RING_CHUNKS - 1) / RING_CHUNKS);
+  hipLaunchKernelGGL(k_ring_insert, dim3(ab.n * dm.units * parts), dim3(256), 0, st, dm, ws, ab,
+                     (const uint8_t*)k, (const uint8_t*)v, unit_bytes, parts);
   return hipGetLastError();
 }
 
@@ -165,9 +225,6 @@ __global__ __launch_bounds__(256) void k_seed(Dims dm, Workspace ws, FoldBatch f
   reinterpret_cast<float2*>(row + ROW_SQV)[lane] = make_float2(vv.x * vv.x, vv.y * vv.y);
   reinterpret_cast<uint2*>(row + ROW_HK)[lane] = make_uint2(0, 0);
   reinterpret_cast<uint2*>(row + ROW_HV)[lane] = make_uint2(0, 0);
-  // centres sum / 1 of the seeded slot
-  reinterpret_cast<float2*>(ws.cent + si * 2 * D)[lane] = kk;
-  reinterpret_cast<float2*>(ws.cent + (si * 2 + 1) * D)[lane] = vv;
   RowMeta m;
   m.n = 1;
   m.n_res = 0;
@@ -238,18 +295,19 @@ __device__ __forceinline__ bool better(double c1, int k1, double c2, int k2) {
 }
 
 // ---------------------------------------------------------------------------
-// PQ residual encoding of the assigned tokens.  The code of subspace g is the
-// nearest codeword to r = x - c (c = float32(sum / n) before this fold,
-// stored by the previous fold), defined by the float32 sequential distance
+// PQ residual codes (used by the screen once its tokens are assigned).  The
+// code of subspace g is the nearest codeword to the residual r = x - c, with
+// c = float32(sum / n) the centre of the token's slot before this fold (IEEE
+// division, from the slot's row, which the aggregation rewrites only
+// afterwards), under the float32 sequential distance
 // dist(c) = sum_u (r_u - C[c][u])^2 (u ascending, one rounding per subtract,
 // multiply and add; ties to the lower codeword).  It is found as
 // argmax_c (r . C_c - |C_c|^2 / 2) on MFMA with a rigorous error bound; a
-// subspace whose best two scores are not separated by the bound is decided by
-// the sequential float32 distances themselves.
+// subspace whose best two scores are not separated by the bound is decided
+// by the sequential float32 distances themselves.
 //
-// Four waves per 64 screened tokens: wave w takes the 32-token block w / 2 of
-// K (w even) or V, with every load issued up front (|C|^2 / 2 and max |C|
-// per codebook come precomputed from init).  For subspaces g0 = 2p, g1 = 2p + 1, v_mfma_f32_32x32x16_bf16
+// Lane = (token column col = lane % 32, half = lane / 32 of each subspace's 16
+// dims).  For subspaces g0 = 2p, g1 = 2p + 1, v_mfma_f32_32x32x16_bf16
 // multiplies A = codebook rows (rows 0-15: C[g0], rows 16-31: C[g1]; block
 // diagonal over two k-steps) by B = residual dims (k-step 0: g0, 1: g1), both
 // split into hi + lo bf16 (hi*hi + hi*lo + lo*hi), starting from -|C|^2 / 2.
@@ -266,169 +324,117 @@ __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
   }
 }
 
-// Encodes the residuals of one 32-token block of one unit for K (kv = 0) or
-// V: token jb0 + (lane % 32), assigned to `slot`; tokens outside [jlo, jhi)
-// are skipped.  Called by the four waves of a screen workgroup once the
-// workgroup's assignments are final.
-template <int FP32>
-__device__ __forceinline__ void pq_block(const Dims& dm, const Workspace& ws, const FoldBatch& fb, int b,
-                                         size_t unit, int jb0, int jlo, int jhi, int kv, int lane, int slot) {
-  const int N = dm.T;
+// Codes of subspaces g0 = 2p, g1 = 2p + 1 for this lane's token from its
+// residual halves r[0] (g0) and r[1] (g1) and A-operand codebook row w;
+// returns the code of subspace g0 (half 0) or g1 (half 1).
+__device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const float* hnp, const float* cmx,
+                                       const float (&r)[2][8], const float (&w)[8], int p, bool valid,
+                                       int lane) {
   const int col = lane & 31, half = lane >> 5;
-  const int j = jb0 + col;
-  const bool valid = j >= jlo && j < jhi;
-  const size_t ub = unit * 2 + kv;
-  const float* cbk = ws.codebooks + ub * G * CBW;
-  const float* hnp = ws.cbhn + ub * G * CMAX;
-  const float* cmx = ws.cbmax + ub * G;
-  const size_t es = FP32 ? 4 : 2;
-  const uint8_t* xr = (kv ? ws.ring_v : ws.ring_k) +
-                      ((((unit * (dm.W + 1) + fb.slot[b]) * N) + (size_t)(valid ? j : 0)) * D) * es;
-  uint8_t* codes = ws.codes + (unit * N + (valid ? j : 0)) * (2 * G) + kv * G;
-
-  // this lane's half (dims g*16 + half*8 .. +7) of every subspace of its token
-  float r[G][8];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const int d0 = g * DP + half * 8;
-    if (FP32) {
-      *reinterpret_cast<float4*>(&r[g][0]) = *reinterpret_cast<const float4*>(xr + (size_t)d0 * 4);
-      *reinterpret_cast<float4*>(&r[g][4]) = *reinterpret_cast<const float4*>(xr + (size_t)(d0 + 4) * 4);
-    } else {
-      const u16x8 h = *reinterpret_cast<const u16x8*>(xr + (size_t)d0 * 2);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) r[g][i] = from_bf16(h[i]);
-    }
-  }
-  // A operand rows: row col < 16 holds C[2p][col][half*8 ..] (k-step 0 of pair p),
-  // row >= 16 holds C[2p+1][col-16][half*8 ..] (k-step 1)
-  float w[G / 2][8];
-#pragma unroll
-  for (int p = 0; p < G / 2; ++p) {
-    const float* wa = cbk + (2 * p + (col < 16 ? 0 : 1)) * CBW + (col & 15) * DP + half * 8;
-    *reinterpret_cast<float4*>(&w[p][0]) = *reinterpret_cast<const float4*>(wa);
-    *reinterpret_cast<float4*>(&w[p][4]) = *reinterpret_cast<const float4*>(wa + 4);
-  }
-  const float* cen = ws.cent + ((unit * dm.K + slot) * 2 + kv) * D;
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const int d0 = g * DP + half * 8;
-    const float4 c0 = *reinterpret_cast<const float4*>(cen + d0);
-    const float4 c1 = *reinterpret_cast<const float4*>(cen + d0 + 4);
-    const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) r[g][i] = valid ? r[g][i] - cc[i] : 0.f;
-  }
+  const int g0 = 2 * p, g1 = 2 * p + 1;
   const bf16x8 zero8 = {};
   const bool lowrows = col < 16;
-
+  bf16x8 ah, al, b0h, b0l, b1h, b1l;
+  split8(w, ah, al);
+  split8(r[0], b0h, b0l);
+  split8(r[1], b1h, b1l);
+  const bf16x8 a0h = lowrows ? ah : zero8, a0l = lowrows ? al : zero8;
+  const bf16x8 a1h = lowrows ? zero8 : ah, a1l = lowrows ? zero8 : al;
+  float n0 = 0.f, n1 = 0.f;
 #pragma unroll
-  for (int p = 0; p < G / 2; ++p) {
-    const int g0 = 2 * p, g1 = 2 * p + 1;
-    bf16x8 ah, al, b0h, b0l, b1h, b1l;
-    split8(w[p], ah, al);
-    split8(r[g0], b0h, b0l);
-    split8(r[g1], b1h, b1l);
-    const bf16x8 a0h = lowrows ? ah : zero8, a0l = lowrows ? al : zero8;
-    const bf16x8 a1h = lowrows ? zero8 : ah, a1l = lowrows ? zero8 : al;
-    float n0 = 0.f, n1 = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      n0 = fmaf(r[g0][i], r[g0][i], n0);
-      n1 = fmaf(r[g1][i], r[g1][i], n1);
-    }
-    // accumulator rows (rr / 4) * 8 + half * 4 + rr % 4: rr < 8 -> codeword of g0, else of g1
-    f32x16 acc;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float4 h = *reinterpret_cast<const float4*>(hnp + (q < 2 ? g0 : g1) * CMAX + (q & 1) * 8 + half * 4);
-      acc[4 * q + 0] = -h.x;
-      acc[4 * q + 1] = -h.y;
-      acc[4 * q + 2] = -h.z;
-      acc[4 * q + 3] = -h.w;
-    }
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0h, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0l, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0l, b0h, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1h, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1l, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1l, b1h, acc, 0, 0, 0);
-
-    // best two scores per subspace: 8 codewords here, 8 in the partner lane
-    float bst1[2], bst2[2];
-    int bid[2];
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      float v1 = -INFINITY, v2 = -INFINITY;
-      int i1 = 0;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const float v = acc[sub * 8 + q];
-        const int cw = (q >> 2) * 8 + half * 4 + (q & 3);
-        const int mk = -(int)(v > v1);
-        v2 = __builtin_amdgcn_fmed3f(v, v1, v2);
-        v1 = fmaxf(v1, v);
-        i1 = (cw & mk) | (i1 & ~mk);
-      }
-      const float o1 = __shfl_xor(v1, 32, 64), o2 = __shfl_xor(v2, 32, 64);
-      const int oi = __shfl_xor(i1, 32, 64);
-      const bool take = o1 > v1 || (o1 == v1 && oi < i1);
-      bst2[sub] = fmaxf(fminf(v1, o1), fmaxf(v2, o2));
-      bst1[sub] = fmaxf(v1, o1);
-      bid[sub] = take ? oi : i1;
-    }
-    // lane half 0 settles g0, half 1 settles g1
-    const int g = half ? g1 : g0;
-    const float v1 = half ? bst1[1] : bst1[0], v2 = half ? bst2[1] : bst2[0];
-    float rn2 = half ? n1 : n0;
-    rn2 += __shfl_xor(half ? n0 : n1, 32, 64);  // the partner's half of subspace g
-    // |score - exact| <= F for every codeword: split error of the MFMA dot
-    // (3 * 2^-18 |r| |C|), its float32 accumulation over three MFMAs
-    // (<= 51 u (|C|^2 / 2 + |r| |C|)) and the rounding of the sequential
-    // float32 distance of the two leading codewords (<= 18 u D / 2 with
-    // D = |r|^2 - 2 score), each taken with margin
-    const float rn = sqrtf(rn2) * 1.0001f, cm = cmx[g];
-    const float dlead = fmaxf(rn * rn - 2.0f * v2, 0.f) + 1e-30f;
-    const float F = fmaf(1.6e-5f * rn, cm, fmaf(2.5e-6f, cm * cm, 1e-6f * dlead));
-    int z = half ? bid[1] : bid[0];
-    // not separated: the float32 sequential distances decide, one flagged
-    // (token, subspace) at a time for the whole wave (lane % 16 = codeword)
-    unsigned long long fm = __ballot(valid && !(v1 - v2 > 2.0f * F));
-    while (fm) {
-      const int src = __ffsll((long long)fm) - 1;
-      fm &= fm - 1;
-      const int gs = (src >> 5) ? g1 : g0;   // uniform
-      const int tc = src & 31;
-      float rr[DP];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float mine = (gs == g0) ? r[g0][i] : r[g1][i];
-        rr[i] = __shfl(mine, tc, 64);
-        rr[8 + i] = __shfl(mine, tc + 32, 64);
-      }
-      const int cw = lane & 15;
-      const float* wc = cbk + gs * CBW + cw * DP;
-      float a = 0.f;
-#pragma unroll
-      for (int q = 0; q < DP; ++q) {
-        const float d = rr[q] - wc[q];
-        a = a + d * d;
-      }
-      if (cw >= dm.C) a = INFINITY;
-      int ai = cw;
-#pragma unroll
-      for (int o = 8; o >= 1; o >>= 1) {
-        const float oa = __shfl_xor(a, o, 64);
-        const int oi = __shfl_xor(ai, o, 64);
-        const bool take = oa < a || (oa == a && oi < ai);
-        a = take ? oa : a;
-        ai = take ? oi : ai;
-      }
-      if (lane == src) z = ai;
-    }
-    if (valid) codes[g] = (uint8_t)z;
+  for (int i = 0; i < 8; ++i) {
+    n0 = fmaf(r[0][i], r[0][i], n0);
+    n1 = fmaf(r[1][i], r[1][i], n1);
   }
+  // accumulator rows (rr / 4) * 8 + half * 4 + rr % 4: rr < 8 -> codeword of g0, else of g1
+  f32x16 acc;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 h = *reinterpret_cast<const float4*>(hnp + (q < 2 ? g0 : g1) * CMAX + (q & 1) * 8 + half * 4);
+    acc[4 * q + 0] = -h.x;
+    acc[4 * q + 1] = -h.y;
+    acc[4 * q + 2] = -h.z;
+    acc[4 * q + 3] = -h.w;
+  }
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0h, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0h, b0l, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0l, b0h, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1h, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1l, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1l, b1h, acc, 0, 0, 0);
+
+  // best two scores per subspace: 8 codewords here, 8 in the partner lane
+  float bst1[2], bst2[2];
+  int bid[2];
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    float v1 = -INFINITY, v2 = -INFINITY;
+    int i1 = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const float v = acc[sub * 8 + q];
+      const int cw = (q >> 2) * 8 + half * 4 + (q & 3);
+      const int mk = -(int)(v > v1);
+      v2 = __builtin_amdgcn_fmed3f(v, v1, v2);
+      v1 = fmaxf(v1, v);
+      i1 = (cw & mk) | (i1 & ~mk);
+    }
+    const float o1 = __shfl_xor(v1, 32, 64), o2 = __shfl_xor(v2, 32, 64);
+    const int oi = __shfl_xor(i1, 32, 64);
+    const bool take = o1 > v1 || (o1 == v1 && oi < i1);
+    bst2[sub] = fmaxf(fminf(v1, o1), fmaxf(v2, o2));
+    bst1[sub] = fmaxf(v1, o1);
+    bid[sub] = take ? oi : i1;
+  }
+  // lane half 0 settles g0, half 1 settles g1
+  const int g = half ? g1 : g0;
+  const float v1 = half ? bst1[1] : bst1[0], v2 = half ? bst2[1] : bst2[0];
+  float rn2 = half ? n1 : n0;
+  rn2 += __shfl_xor(half ? n0 : n1, 32, 64);  // the partner's half of subspace g
+  // |score - exact| <= F for every codeword: the hi + lo split of both
+  // operands leaves <= 3 * 2^-16 |r_u| |C_u| per product (the dropped
+  // lo * lo and the two split remainders), summed <= 4.6e-5 |r| |C|; the
+  // float32 accumulation over three MFMAs adds <= 51 u (|C|^2 / 2 +
+  // |r| |C|), the rounded |C|^2 / 2 <= 9 u |C|^2.  The float32 sequential
+  // distances of the codewords differ from the exact ones by <= 19 u D,
+  // D <= |r|^2 - 2 score of the runner-up (dlead).  Each term is taken with
+  // margin.
+  const float rn = sqrtf(rn2) * 1.0001f, cm = cmx[g];
+  const float dlead = fmaxf(rn * rn - 2.0f * v2, 0.f) + 1e-30f;
+  const float F = fmaf(5.2e-5f * rn, cm, fmaf(2.5e-6f, cm * cm, 1.2e-6f * dlead));
+  int z = half ? bid[1] : bid[0];
+  // not separated: the float32 sequential distances decide, one flagged
+  // (token, subspace) at a time for the whole wave (lane % 16 = codeword)
+  unsigned long long fm = __ballot(valid && !(v1 - v2 > 2.0f * F));
+  while (fm) {
+    const int src = __ffsll((long long)fm) - 1;
+    fm &= fm - 1;
+    const int gs = (src >> 5) ? g1 : g0;   // uniform
+    const int tc = src & 31;
+    const int cw = lane & 15;
+    const float* wc = cbk + gs * CBW + cw * DP;
+    float a = 0.f;
+#pragma unroll
+    for (int q = 0; q < DP; ++q) {
+      const float mine = (gs == g0) ? r[0][q & 7] : r[1][q & 7];
+      const float d = __shfl(mine, q < 8 ? tc : tc + 32, 64) - wc[q];
+      a = a + d * d;
+    }
+    if (cw >= dm.C) a = INFINITY;
+    int ai = cw;
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) {
+      const float oa = __shfl_xor(a, o, 64);
+      const int oi = __shfl_xor(ai, o, 64);
+      const bool take = oa < a || (oa == a && oi < ai);
+      a = take ? oa : a;
+      ai = take ? oi : ai;
+    }
+    if (lane == src) z = ai;
+  }
+  return z;
 }
+
 
 // ---------------------------------------------------------------------------
 // Screen + argmin.  Workgroup = 64 evicted tokens of one unit (two 32-token
@@ -502,7 +508,7 @@ __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, flo
 constexpr int SCREEN_WAVES = 4;
 
 template <int FP32>
-__global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
+__global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
   // token operands of the workgroup in MFMA B order [token half][k-step][lane]
   __shared__ bf16x8 s_bk[2][8][64];
   __shared__ bf16x8 s_bkl[FP32 ? 2 : 1][FP32 ? 8 : 1][64];  // low part of float32 keys
@@ -562,7 +568,7 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
   };
   if (wave < ntiles) load_tile(wave);  // in flight while the keys are staged
 
-  // Stage the keys: wave w loads k-steps w, w + 4 of both 32-token halves
+  // Stage the keys: wave w loads k-steps w, w + SCREEN_WAVES, ... of both 32-token halves
   // (tokens tile*64 + h*32 + col, dims 16 kk + 8 half .. + 8) and its partial norms.
   int jt[2];
   bool vt[2];
@@ -696,10 +702,8 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
   const float thr = tp.c1 + 2.0f * E + 2e-6f;
   const int nc = 1 + (tp.c2 <= thr) + (tp.c3 <= thr);
   const bool mine = valid && half == 0;
-  const uint32_t tag = (uint32_t)fb.fe[b] + 1u;
   if (mine && nc <= 1) {
     ws.assign[unit * N + j] = tp.i1;
-    ws.tgen[unit * dm.K + tp.i1] = tag;  // same value from every writer
     s_asg[hsel * 32 + col] = tp.i1;
   }
   const bool flag = mine && nc >= 2;
@@ -764,7 +768,6 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
     }
     if (lane == 0) {
       ws.assign[unit * N + jj] = k1;
-      ws.tgen[unit * dm.K + k1] = tag;
       s_asg[jj - tile * SCREEN_TOK] = k1;
       n_ref += 1;
       n_full += ncc > 2 ? 1 : 0;
@@ -778,17 +781,81 @@ __global__ __launch_bounds__(256, 2) void k_screen(Dims dm, Workspace ws, FoldBa
   }
   }  // waves 0 and 1
 
-  // PQ codes of the tile's assigned tokens (residuals against the centres
-  // before this fold): wave w encodes block w / 2 of K (w even) or V
+  // PQ codes of the tile's assigned tokens: wave w encodes the 32-token block
+  // w / 2 of K (w even) or V; each code bumps its bin of the slot's
+  // histogram (integer counts: the order of the increments does not matter)
   if (dm.flags & PROTOKV_FLAG_PQ) {
     __syncthreads();
     const int blk = wave >> 1, kv = wave & 1;
-    const int jlo = max(nseed, tile * SCREEN_TOK), jhi = min(N, tile * SCREEN_TOK + SCREEN_TOK);
-    const int jb0 = tile * SCREEN_TOK + blk * 32;
-    if (!(jb0 >= jhi || jb0 + 32 <= jlo)) {  // uniform per wave
-      const int jj = jb0 + col;
-      const int slot = (jj >= jlo && jj < jhi) ? s_asg[blk * 32 + col] : 0;
-      pq_block<FP32>(dm, ws, fb, b, unit, jb0, jlo, jhi, kv, lane, slot);
+    const int jq = tile * SCREEN_TOK + blk * 32 + col;
+    const bool qv = jq >= nseed && jq < N;
+    if (__ballot(qv)) {  // uniform per wave
+      const int slot = qv ? s_asg[blk * 32 + col] : 0;
+      const uint8_t* srow = ws.bank + (unit * dm.K + slot) * ROW;
+      const float* sums = reinterpret_cast<const float*>(srow + (kv ? ROW_SUMV : ROW_SUMK));
+      const size_t ub = unit * 2 + kv;
+      const float* cbk = ws.codebooks + ub * G * CBW;
+      // every load of the four subspace pairs up front: the token's dims
+      // (half of each subspace), the slot's sums of the same dims, n and the
+      // A-operand codebook rows
+      uint4 xr[G][FP32 ? 2 : 1];
+      if (kv == 0 && !FP32) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) xr[g][0] = __builtin_bit_cast(uint4, s_bk[blk][g][half * 32 + col]);
+      } else {
+        const uint8_t* xrow = (kv ? ws.ring_v : ws.ring_k) + (fbase + (size_t)(qv ? jq : 0) * D) * es;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const uint4* px = reinterpret_cast<const uint4*>(xrow + (size_t)(g * DP + half * 8) * es);
+#pragma unroll
+          for (int e = 0; e < (FP32 ? 2 : 1); ++e) xr[g][e] = px[e];
+        }
+      }
+      float4 sr[G][2], wr[G / 2][2];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        sr[g][0] = *reinterpret_cast<const float4*>(sums + g * DP + half * 8);
+        sr[g][1] = *reinterpret_cast<const float4*>(sums + g * DP + half * 8 + 4);
+      }
+#pragma unroll
+      for (int p = 0; p < G / 2; ++p) {
+        const float* wa = cbk + (2 * p + (col < 16 ? 0 : 1)) * CBW + (col & 15) * DP + half * 8;
+        wr[p][0] = *reinterpret_cast<const float4*>(wa);
+        wr[p][1] = *reinterpret_cast<const float4*>(wa + 4);
+      }
+      const float nf = (float)*reinterpret_cast<const uint32_t*>(srow + ROW_META);
+      uint32_t* hist = reinterpret_cast<uint32_t*>(ws.bank + (unit * dm.K + slot) * ROW + (kv ? ROW_HV : ROW_HK));
+#pragma unroll
+      for (int p = 0; p < G / 2; ++p) {
+        float r[2][8], w[8];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int g = 2 * p + q;
+          float x[8];
+          if (FP32) {
+            const uint4 a = xr[g][0], c = xr[g][FP32 ? 1 : 0];
+            const uint32_t xw[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
+#pragma unroll
+            for (int i = 0; i < 8; ++i) x[i] = __uint_as_float(xw[i]);
+          } else {
+            const uint4 a = xr[g][0];
+            const uint32_t xw[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              x[2 * i] = __uint_as_float(xw[i] << 16);
+              x[2 * i + 1] = __uint_as_float(xw[i] & 0xFFFF0000u);
+            }
+          }
+          const float sv[8] = {sr[g][0].x, sr[g][0].y, sr[g][0].z, sr[g][0].w,
+                               sr[g][1].x, sr[g][1].y, sr[g][1].z, sr[g][1].w};
+#pragma unroll
+          for (int i = 0; i < 8; ++i) r[q][i] = qv ? x[i] - sv[i] / nf : 0.f;
+        }
+        w[0] = wr[p][0].x; w[1] = wr[p][0].y; w[2] = wr[p][0].z; w[3] = wr[p][0].w;
+        w[4] = wr[p][1].x; w[5] = wr[p][1].y; w[6] = wr[p][1].z; w[7] = wr[p][1].w;
+        const int z = pq_pair(dm, cbk, ws.cbhn + ub * G * CMAX, ws.cbmax + ub * G, r, w, p, qv, lane);
+        if (qv) atomicAdd(hist + (2 * p + half) * CMAX + z, 1u);
+      }
     }
   }
 }
@@ -804,138 +871,199 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
 }
 
 // ---------------------------------------------------------------------------
-// Aggregation.  One wave per slot; the four waves of a workgroup are
-// independent.  A slot the screen did not tag in this fold exits after one
-// load.  Otherwise the wave compacts its tokens (eviction order) into its LDS
-// list with ballots over the assignment vector and updates the row in
-// registers, loading the next token's K, V and codes while it absorbs the
-// current one.  Lane l holds components 2l, 2l+1 of the four sums and
-// histogram bins 2l, 2l+1 (subspace l/8, codewords 2(l%8), 2(l%8)+1).  Then
-// it writes the row back, stores the new centres and refreshes the slot's
-// screening copy.
+// Aggregation.  Workgroup = 32 consecutive slots of one unit, two per 16-lane
+// group (absorbed one after the other); lane il of a group holds dims
+// [8 il, 8 il + 8) of the slot's four sums.  The unit's assignment vector
+// is staged in LDS; wave w sweeps it with ballots for its eight slots, once
+// to count their tokens and once to list them in eviction order.  A workgroup whose slots drew no token
+// exits there.  Each group then loads its slot's row, absorbs the slot's
+// tokens in order, TOK_BATCH at a time with all of a batch's loads in flight
+// (mass, sums, sums of squares, residual count, spatial EMA, recency; the
+// screen already counted the PQ codes into the histograms), writes the row
+// back and refreshes the slot's screening copy.
 // ---------------------------------------------------------------------------
+constexpr int AGG_SLOTS = 32;  // slots per workgroup: two per 16-lane group (k0 + g, k0 + g + 16)
+constexpr int TOK_BATCH = 2;
+constexpr uint16_t NO_SLOT = 0xFFFF;
+
+// Eight consecutive KV elements (index e, a multiple of 8) as raw words
+// (bf16 pairs or float32 bits), and element q of them as float.
 template <int FP32>
-__global__ __launch_bounds__(256) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int chunks_per_unit) {
-  __shared__ uint16_t s_tok[4][TMAX];
+struct Raw8 {
+  uint4 w[FP32 ? 2 : 1];
+};
+template <int FP32>
+__device__ __forceinline__ void load8(const uint8_t* base, size_t e, Raw8<FP32>& x) {
+  const uint4* p = reinterpret_cast<const uint4*>(base + e * (FP32 ? 4 : 2));
+#pragma unroll
+  for (int q = 0; q < (FP32 ? 2 : 1); ++q) x.w[q] = p[q];
+}
+template <int FP32>
+__device__ __forceinline__ float raw_at(const Raw8<FP32>& x, int q) {
+  const uint4& v = x.w[FP32 ? q >> 2 : 0];
+  const int e = FP32 ? (q & 3) : (q >> 1);
+  const uint32_t word = e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w;
+  if (FP32) return __uint_as_float(word);
+  return __uint_as_float((q & 1) ? (word & 0xFFFF0000u) : (word << 16));
+}
+
+__device__ __forceinline__ void ld8f(const uint8_t* p, float (&x)[8]) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+__device__ __forceinline__ void st8f(uint8_t* p, const float (&x)[8]) {
+  reinterpret_cast<float4*>(p)[0] = make_float4(x[0], x[1], x[2], x[3]);
+  reinterpret_cast<float4*>(p)[1] = make_float4(x[4], x[5], x[6], x[7]);
+}
+
+template <int FP32>
+__global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int wg_per_unit) {
+  __shared__ uint16_t s_asg[TMAX];         // slot of each token (NO_SLOT: seeded / padding)
+  __shared__ uint16_t s_tok[TMAX];         // tokens of this workgroup's slots, grouped, eviction order
+  __shared__ int s_cnt[AGG_SLOTS];
+  __shared__ int s_off[AGG_SLOTS + 1];       // local slot q = group + 16 * pass
+
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // same XCD placement as the screen (consecutive logical blocks share an
-  // XCD), so a unit's assignments, tags and evicted tokens are read from the
-  // L2 the screen left them in
+  // XCD), so the unit's assignments and evicted tokens come from its L2
   const int nblk = (int)gridDim.x, per = nblk >> 3, bid = (int)blockIdx.x;
   const int lb = bid < per * 8 ? (bid & 7) * per + (bid >> 3) : bid;
-  const int chunk = lb % chunks_per_unit;
-  const int bu = lb / chunks_per_unit;
+  const int wgi = lb % wg_per_unit;
+  const int bu = lb / wg_per_unit;
   const int b = bu / dm.units, u = bu % dm.units;
   const int N = dm.T;
   const int nseed = fb.nseed[b];
   const int kact = fb.nact[b] + nseed;
-  const int k = chunk * 4 + wave;
-  if (nseed >= N || k >= kact) return;  // uniform per wave
+  const int k0 = wgi * AGG_SLOTS;
+  if (nseed >= N || k0 >= kact) return;  // uniform
   const size_t unit = (size_t)fb.sid[b] * dm.units + u;
-  const size_t si = unit * dm.K + k;
   const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
   const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
-  // the tag and the first chunk of the (small, cached) assignment vector are
-  // loaded together; a slot without this fold's tag leaves after that round
-  // trip, a tagged one loads its row while it compacts its token list
-  const uint32_t tag = ws.tgen[si];
-  const int a0 = (lane < N && lane >= nseed) ? ws.assign[unit * N + lane] : -1;
-  if (tag != (uint32_t)fb.fe[b] + 1u) return;  // no token this fold
-  uint8_t* row = ws.bank + si * ROW;
-  float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
-  float2 sv = reinterpret_cast<const float2*>(row + ROW_SUMV)[lane];
-  float2 qk = reinterpret_cast<const float2*>(row + ROW_SQK)[lane];
-  float2 qv = reinterpret_cast<const float2*>(row + ROW_SQV)[lane];
-  uint2 hk = reinterpret_cast<const uint2*>(row + ROW_HK)[lane];
-  uint2 hv = reinterpret_cast<const uint2*>(row + ROW_HV)[lane];
-  RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
-
-  // this slot's tokens, in eviction order
   const unsigned long long below = (1ull << lane) - 1ull;
-  int ntok = 0;
-  for (int c = 0; c * 64 < N; ++c) {
-    const int jj = c * 64 + lane;
-    const int a = c == 0 ? a0 : ((jj < N && jj >= nseed) ? ws.assign[unit * N + jj] : -1);
-    const unsigned long long mk = __ballot(a == k);
-    if (a == k) s_tok[wave][ntok + __popcll(mk & below)] = (uint16_t)jj;
-    ntok += __popcll(mk);
-  }
-  if (ntok == 0) return;  // uniform; a tagged slot always has a token
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int N64 = (N + 63) & ~63;
 
-  const float eta = dm.eta, keep = 1.0f - dm.eta;
-  const int gl = lane >> 3, c0 = 2 * (lane & 7);
-  auto fetch = [&](int jj, float2& kk, float2& vv, int& zk, int& zv) {
-    kk = load2<FP32>(ws.ring_k, fbase + (size_t)jj * D + 2 * lane);
-    vv = load2<FP32>(ws.ring_v, fbase + (size_t)jj * D + 2 * lane);
-    zk = zv = 0;
-    if (pq) {
-      const uint8_t* cz = ws.codes + (unit * N + jj) * (2 * G);
-      zk = cz[gl];
-      zv = cz[G + gl];
-    }
-  };
-  int jn = s_tok[wave][0];
-  float2 kn, vn;
-  int zkn, zvn;
-  fetch(jn, kn, vn, zkn, zvn);
-  for (int i = 0; i < ntok; ++i) {
-    const int jj = jn;
-    const float2 kk = kn, vv = vn;
-    const int zk = zkn, zv = zvn;
-    if (i + 1 < ntok) {  // uniform: next token's loads in flight while this one is absorbed
-      jn = s_tok[wave][i + 1];
-      fetch(jn, kn, vn, zkn, zvn);
-    }
-    sk.x = sk.x + kk.x; sk.y = sk.y + kk.y;
-    sv.x = sv.x + vv.x; sv.y = sv.y + vv.y;
-    qk.x = qk.x + kk.x * kk.x; qk.y = qk.y + kk.y * kk.y;
-    qv.x = qv.x + vv.x * vv.x; qv.y = qv.y + vv.y * vv.y;
-    if (pq) {
-      hk.x += (zk == c0) ? 1u : 0u;
-      hk.y += (zk == c0 + 1) ? 1u : 0u;
-      hv.x += (zv == c0) ? 1u : 0u;
-      hv.y += (zv == c0 + 1) ? 1u : 0u;
-      m.n_res += 1;
-    }
-    float sx, sy;
-    token_xy(jj, dm.grid_w, dm.grid_h, sx, sy);
-    const float mx = keep * m.mu_x + eta * sx;
-    const float my = keep * m.mu_y + eta * sy;
-    m.mu_x = mx;
-    m.mu_y = my;
-    const float ddx = sx - mx, ddy = sy - my;
-    m.sxx = keep * m.sxx + eta * (ddx * ddx);
-    m.sxy = keep * m.sxy + eta * (ddx * ddy);
-    m.syy = keep * m.syy + eta * (ddy * ddy);
-    m.tau = fb.fe[b] * N + jj;
-    m.n += 1;
+  for (int j = tid; j < N64; j += 256)
+    s_asg[j] = (j >= nseed && j < N) ? (uint16_t)ws.assign[unit * N + j] : NO_SLOT;
+  __syncthreads();
+  // wave w sweeps for the local slots of its lane groups: q = 4 w + g and
+  // q + 16 (slot k0 + q), g = 0..3
+  int kw[8];
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    const int q = 4 * wave + (g & 3) + 16 * (g >> 2);
+    kw[g] = (k0 + q < kact) ? k0 + q : -1;
   }
-  reinterpret_cast<float2*>(row + ROW_SUMK)[lane] = sk;
-  reinterpret_cast<float2*>(row + ROW_SUMV)[lane] = sv;
-  reinterpret_cast<float2*>(row + ROW_SQK)[lane] = qk;
-  reinterpret_cast<float2*>(row + ROW_SQV)[lane] = qv;
-  reinterpret_cast<uint2*>(row + ROW_HK)[lane] = hk;
-  reinterpret_cast<uint2*>(row + ROW_HV)[lane] = hv;
-  if (lane == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
-  // centres float32(sum / n) for the next fold's residuals (IEEE division)
-  const float nf = (float)m.n;
-  reinterpret_cast<float2*>(ws.cent + si * 2 * D)[lane] = make_float2(sk.x / nf, sk.y / nf);
-  reinterpret_cast<float2*>(ws.cent + (si * 2 + 1) * D)[lane] = make_float2(sv.x / nf, sv.y / nf);
-  refresh_cache(dm, sk, m, unit, k, ws, lane);
-  // per-slot count of folds that touched it (owned by this wave: no atomics)
-  if (lane == 0) ws.touched[si] += 1u;
+  int cw[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int c = 0; c < N64; c += 64) {
+    const int a = s_asg[c + lane];
+#pragma unroll
+    for (int g = 0; g < 8; ++g) cw[g] += __popcll(__ballot(a == kw[g]));
+  }
+  if (lane < 8) {
+    int v = cw[0];
+#pragma unroll
+    for (int g = 1; g < 8; ++g) v = lane == g ? cw[g] : v;
+    s_cnt[4 * wave + (lane & 3) + 16 * (lane >> 2)] = v;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    const int v = lane < AGG_SLOTS ? s_cnt[lane] : 0;
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < AGG_SLOTS; o <<= 1) {
+      const int y = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += y;
+    }
+    if (lane < AGG_SLOTS) s_off[lane + 1] = incl;
+    if (lane == 0) s_off[0] = 0;
+  }
+  __syncthreads();
+  if (s_off[AGG_SLOTS] == 0) return;  // uniform: none of these slots drew a token
+  int ow[8];
+#pragma unroll
+  for (int g = 0; g < 8; ++g) ow[g] = s_off[4 * wave + (g & 3) + 16 * (g >> 2)];
+  for (int c = 0; c < N64; c += 64) {
+    const int a = s_asg[c + lane];
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      const unsigned long long mk = __ballot(a == kw[g]);
+      if (a == kw[g]) s_tok[ow[g] + __popcll(mk & below)] = (uint16_t)(c + lane);
+      ow[g] += __popcll(mk);
+    }
+  }
+  __syncthreads();
+
+  const int gi = tid >> 4, il = tid & 15;
+  const float eta = dm.eta, keep = 1.0f - dm.eta;
+  for (int pass = 0; pass < 2; ++pass) {  // uniform per lane group; no barrier below
+    const int q = gi + 16 * pass;
+    const int t0 = s_off[q], t1 = s_off[q + 1];
+    if (t1 == t0) continue;
+    const int k = k0 + q;
+    const size_t si = unit * dm.K + k;
+    uint8_t* row = ws.bank + si * ROW;
+    float sk[8], sv[8], qk[8], qv[8];
+    ld8f(row + ROW_SUMK + il * 32, sk);
+    ld8f(row + ROW_SUMV + il * 32, sv);
+    ld8f(row + ROW_SQK + il * 32, qk);
+    ld8f(row + ROW_SQV + il * 32, qv);
+    RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+    for (int tb = t0; tb < t1; tb += TOK_BATCH) {  // uniform per lane group
+      // a batch's loads all in flight together (indices clamped into the list)
+      int jb[TOK_BATCH];
+      Raw8<FP32> kb[TOK_BATCH], vb[TOK_BATCH];
+#pragma unroll
+      for (int e = 0; e < TOK_BATCH; ++e) {
+        jb[e] = s_tok[min(tb + e, t1 - 1)];
+        load8<FP32>(ws.ring_k, fbase + (size_t)jb[e] * D + 8 * il, kb[e]);
+        load8<FP32>(ws.ring_v, fbase + (size_t)jb[e] * D + 8 * il, vb[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < TOK_BATCH; ++e) {
+        if (tb + e < t1) {
+          const int jj = jb[e];
+#pragma unroll
+          for (int d = 0; d < 8; ++d) {
+            const float xk = raw_at<FP32>(kb[e], d), xv = raw_at<FP32>(vb[e], d);
+            sk[d] = sk[d] + xk;
+            sv[d] = sv[d] + xv;
+            qk[d] = qk[d] + xk * xk;
+            qv[d] = qv[d] + xv * xv;
+          }
+          if (pq) m.n_res += 1;
+          float sx, sy;
+          token_xy(jj, dm.grid_w, dm.grid_h, sx, sy);
+          const float mx = keep * m.mu_x + eta * sx;
+          const float my = keep * m.mu_y + eta * sy;
+          m.mu_x = mx;
+          m.mu_y = my;
+          const float ddx = sx - mx, ddy = sy - my;
+          m.sxx = keep * m.sxx + eta * (ddx * ddx);
+          m.sxy = keep * m.sxy + eta * (ddx * ddy);
+          m.syy = keep * m.syy + eta * (ddy * ddy);
+          m.tau = fb.fe[b] * N + jj;
+          m.n += 1;
+        }
+      }
+    }
+    st8f(row + ROW_SUMK + il * 32, sk);
+    st8f(row + ROW_SUMV + il * 32, sv);
+    st8f(row + ROW_SQK + il * 32, qk);
+    st8f(row + ROW_SQV + il * 32, qv);
+    if (il == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
+    refresh_cache16(dm, sk, m, unit, k, ws, il);
+    // per-slot count of folds that touched it (owned by this lane group: no atomics)
+    if (il == 0) ws.touched[si] += 1u;
+  }
 }
 
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
-  int cpu = (dm.K + 3) / 4;
-  dim3 grid(fb.n * dm.units * cpu);
+  const int wpu = (dm.K + AGG_SLOTS - 1) / AGG_SLOTS;
+  dim3 grid(fb.n * dm.units * wpu);
   if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_aggregate<1>, grid, dim3(256), 0, st, dm, ws, fb, cpu);
+    hipLaunchKernelGGL(k_aggregate<1>, grid, dim3(256), 0, st, dm, ws, fb, wpu);
   else
-    hipLaunchKernelGGL(k_aggregate<0>, grid, dim3(256), 0, st, dm, ws, fb, cpu);
+    hipLaunchKernelGGL(k_aggregate<0>, grid, dim3(256), 0, st, dm, ws, fb, wpu);
   return hipGetLastError();
 }
 

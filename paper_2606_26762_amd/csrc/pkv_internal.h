@@ -18,6 +18,7 @@ constexpr int TMAX = 1024; // tokens per frame
 constexpr int MAXB = 64;   // streams per launch batch
 constexpr int MAX_SPLITS = 16;  // attention context splits (partials storage)
 constexpr int MAX_RBLOCKS = 2;  // query-row blocks of 256 per kv head
+constexpr int KMAX = 65535;     // prototype slots per unit (slot ids fit 16 bits)
 
 // Bank row (one prototype slot), byte offsets; see protokv.h.
 constexpr int ROW = PROTOKV_ROW_BYTES;
@@ -73,8 +74,6 @@ struct Workspace {
   uint16_t* chat_lo;
   CacheMeta* cmeta;           // [streams][units][K]
   int32_t* assign;            // [streams][units][T]
-  uint8_t* codes;             // [streams][units][T][2][G]: PQ codes of the last fold's tokens
-  float* cent;                // [streams][units][K][2][D]: centres float32(sum / n) of K and V
   float* codebooks;           // [streams][units][2][G][CMAX][DP]
   float* cbhn;                // [streams][units][2][G][CMAX]: |C|^2 / 2 (+inf for codewords >= C)
   float* cbmax;               // [streams][units][2][G]: an upper bound of max_c |C|
@@ -86,7 +85,6 @@ struct Workspace {
   float* part_ml;             // [units][max_splits][max_rows][2]  (max, sum)
   unsigned long long* counters;  // [16]
   uint32_t* touched;             // [streams][units][K]: folds in which the slot absorbed >= 1 token
-  uint32_t* tgen;                // [streams][units][K]: tag (evicted frame + 1) of the last fold that assigned the slot a token
 };
 
 enum Counter {

@@ -26,8 +26,8 @@ struct StreamState {
 };
 
 struct Layout {
-  size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codes, cent, codebooks, cbhn, cbmax;
-  size_t pk, pv, pbias, pcodes, part_o, part_ml, counters, touched, tgen, total;
+  size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codebooks, cbhn, cbmax;
+  size_t pk, pv, pbias, pcodes, part_o, part_ml, counters, touched, total;
 };
 
 thread_local std::string g_init_err;
@@ -57,8 +57,6 @@ Layout make_layout(const protokv_config& c) {
   ly.chat_lo = take(U * K32 * D * 2);
   ly.cmeta = take(U * K * sizeof(CacheMeta));
   ly.assign = take(U * T * 4);
-  ly.codes = take(U * T * 2 * G);
-  ly.cent = take(U * K * 2 * D * 4);
   ly.codebooks = take(U * 2 * G * CMAX * DP * 4);
   ly.cbhn = take(U * 2 * G * CMAX * 4);
   ly.cbmax = take(U * 2 * G * 4);
@@ -70,7 +68,6 @@ Layout make_layout(const protokv_config& c) {
   ly.part_ml = take(units * MAX_SPLITS * rows * 2 * 4);
   ly.counters = take(CNT_COUNT * 8);
   ly.touched = take(U * K * 4);
-  ly.tgen = take(U * K * 4);
   ly.total = off;
   return ly;
 }
@@ -88,7 +85,7 @@ protokv_status check_config(const protokv_config* c, std::string& why) {
   if ((int64_t)c->grid_h * c->grid_w > TMAX) return uns("at most 1024 tokens per frame");
   if (c->window_frames < 1) return bad("window_frames must be >= 1");
   if (c->capacity < 1) return bad("capacity must be >= 1");
-  if (c->capacity > (1 << 20)) return uns("capacity above 2^20");
+  if (c->capacity > KMAX) return uns("capacity above 65535");
   if (c->pq_subspaces != G) return uns("pq_subspaces must be 8");
   if (c->pq_codewords < 2 || c->pq_codewords > CMAX) return uns("pq_codewords must be in [2, 16]");
   if (c->pseudo_per_proto < 1) return bad("pseudo_per_proto must be >= 1");
@@ -259,8 +256,6 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.chat_lo = (uint16_t*)(b + ly.chat_lo);
   ws.cmeta = (CacheMeta*)(b + ly.cmeta);
   ws.assign = (int32_t*)(b + ly.assign);
-  ws.codes = b + ly.codes;
-  ws.cent = (float*)(b + ly.cent);
   ws.codebooks = (float*)(b + ly.codebooks);
   ws.cbhn = (float*)(b + ly.cbhn);
   ws.cbmax = (float*)(b + ly.cbmax);
@@ -272,7 +267,6 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.part_ml = (float*)(b + ly.part_ml);
   ws.counters = (unsigned long long*)(b + ly.counters);
   ws.touched = (uint32_t*)(b + ly.touched);
-  ws.tgen = (uint32_t*)(b + ly.tgen);
   h->st.assign(c->num_streams, StreamState());
 
   // codebooks -> [U][2][G][CMAX][DP] with the codeword axis padded to 16
