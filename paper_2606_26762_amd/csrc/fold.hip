@@ -257,9 +257,8 @@ hipError_t launch_seed(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
 // ---------------------------------------------------------------------------
 // Eq. 1 from a float64 dot product K.sumK, |K| and |sumK|^2 (oracle formula and
 // operation order for the spatial and idle terms).
-__device__ double cost_from_dot(const Dims& dm, double dot, double knorm, double n2, double kx, double ky,
-                                const uint8_t* row, int t_frame) {
-  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+__device__ double cost_from_meta(const Dims& dm, double dot, double knorm, double n2, double kx, double ky,
+                                 const RowMeta& m, int t_frame) {
   double denom = knorm * sqrt(n2);
   double cosv = denom > 0.0 ? dot / denom : 0.0;
   double dx = kx - (double)m.mu_x, dy = ky - (double)m.mu_y;
@@ -269,6 +268,10 @@ __device__ double cost_from_dot(const Dims& dm, double dot, double knorm, double
   double dm_ = sqrt(q > 0.0 ? q : 0.0);
   double idle = (t_frame - m.tau / dm.T) > dm.t_idle ? 1.0 : 0.0;
   return -cosv + dm.lambda_sp * dm_ + dm.lambda_idle * idle;
+}
+__device__ double cost_from_dot(const Dims& dm, double dot, double knorm, double n2, double kx, double ky,
+                                const uint8_t* row, int t_frame) {
+  return cost_from_meta(dm, dot, knorm, n2, kx, ky, *reinterpret_cast<const RowMeta*>(row + ROW_META), t_frame);
 }
 
 // Exact cost of Eq. 1 in float64 for one (token, slot), serial over dimensions.
@@ -723,10 +726,24 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
     double c1 = INFINITY, c2 = INFINITY;
     int k1 = 0x7fffffff;
     if (ncc == 2) {
-      // lanes over dimensions: float64 dot products and norms of the two candidates
-      const float2 kv = load2<FP32>(kr, 2 * lane);
-      const float2 s0 = reinterpret_cast<const float2*>(ws.bank + (unit * dm.K + cand0) * ROW + ROW_SUMK)[lane];
-      const float2 s1 = reinterpret_cast<const float2*>(ws.bank + (unit * dm.K + cand1) * ROW + ROW_SUMK)[lane];
+      // lanes over dimensions: float64 dot products and norms of the two
+      // candidates; the key (bf16: from its LDS copy), both sums and both
+      // metas in one round trip
+      const uint8_t* r0 = ws.bank + (unit * dm.K + cand0) * ROW;
+      const uint8_t* r1 = ws.bank + (unit * dm.K + cand1) * ROW;
+      const float2 s0 = reinterpret_cast<const float2*>(r0 + ROW_SUMK)[lane];
+      const float2 s1 = reinterpret_cast<const float2*>(r1 + ROW_SUMK)[lane];
+      const RowMeta m0 = *reinterpret_cast<const RowMeta*>(r0 + ROW_META);
+      const RowMeta m1 = *reinterpret_cast<const RowMeta*>(r1 + ROW_META);
+      float2 kv;
+      if (FP32) {
+        kv = load2<FP32>(kr, 2 * lane);
+      } else {
+        // dims 2l, 2l+1 sit in k-step l / 8, lane half (l / 4) % 2, pair (l % 4)
+        const int tl = jj - tile * SCREEN_TOK;
+        const uint32_t w = reinterpret_cast<const uint32_t*>(&s_bk[tl >> 5][lane >> 3][((lane >> 2) & 1) * 32 + (tl & 31)])[lane & 3];
+        kv = make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+      }
       double kn2 = (double)kv.x * (double)kv.x + (double)kv.y * (double)kv.y;
       double d0 = (double)kv.x * (double)s0.x + (double)kv.y * (double)s0.y;
       double d1 = (double)kv.x * (double)s1.x + (double)kv.y * (double)s1.y;
@@ -741,8 +758,8 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
         n1 += __shfl_xor(n1, o, 64);
       }
       const double knorm = sqrt(kn2);
-      const double e0 = cost_from_dot(dm, d0, knorm, n0, kxf, kyf, ws.bank + (unit * dm.K + cand0) * ROW, t_frame);
-      const double e1 = cost_from_dot(dm, d1, knorm, n1, kxf, kyf, ws.bank + (unit * dm.K + cand1) * ROW, t_frame);
+      const double e0 = cost_from_meta(dm, d0, knorm, n0, kxf, kyf, m0, t_frame);
+      const double e1 = cost_from_meta(dm, d1, knorm, n1, kxf, kyf, m1, t_frame);
       if (better(e0, cand0, e1, cand1)) { c1 = e0; k1 = cand0; c2 = e1; }
       else { c1 = e1; k1 = cand1; c2 = e0; }
     } else {
