@@ -58,8 +58,11 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0, rows=0):
-    """Bytes the method must move per launch of `kernel` (all units of one stream)."""
+def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0, rows=0, formed=False):
+    """Bytes the method must move per launch of `kernel` (all units of one stream).
+
+    `formed`: the readout forms the pseudo-token rows from the centres, code
+    tuples and codebooks as it loads them (no rows in memory)."""
     U, T, D, K, S = wl.units, wl.tokens_per_frame, wl.head_dim, wl.capacity, cfg.pseudo_per_proto
     b = 4 if wl.kv_dtype == "fp32" else 2
     if kernel == "ring_insert":
@@ -81,14 +84,23 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
         # sums, meta, codes, codebooks per unit, pseudo-token rows out, bias out
         return (U * n_active * (2 * 4 * D + 32 + 2 * (S + 1) * 4 + S * D * b * 2 + 4)
                 + U * 2 * 8 * 16 * 16 * 4)
+    if kernel == "centres":
+        # sums and meta in, float32 centres and bias out
+        return U * n_active * (2 * D * 4 + 32 + 2 * D * 4 + 4)
     if kernel == "attend":
+        if formed:
+            # near-window K, V; per active slot its centres, code tuples and
+            # bias; the unit's codebooks; queries in, outputs out
+            n_near = ctx - n_active * S
+            return U * (2 * n_near * D * b + n_active * (2 * D * 4 + 2 * (S + 1) * 4 + 4)
+                        + CODEBOOK_BYTES + 2 * rows * D * b)
         return U * (2 * ctx * D * b + (ctx // max(S, 1)) * 4 + 2 * rows * D * b)
     return 0
 
 
 FOLD_KERNELS = ("ring_insert", "seed", "screen", "aggregate")
 KERNEL_SOURCES = {k: "fold.hip" for k in FOLD_KERNELS}
-KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "attend", "attend_merge")})
+KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "centres", "attend", "attend_merge")})
 
 
 def kernel_source_hash(kernel):
@@ -251,10 +263,11 @@ def main():
     touched = (c1.touched - c0.touched) / max(1, kt.get("aggregate", {}).get("launches", 1))
     rows = tq * (wl.num_q_heads // wl.num_kv_heads)
     ctx = min(info.frames, wl.window_frames) * T + n_active * cfg.pseudo_per_proto
+    formed = "centres" in kt
     kernels = {}
     for name, d in kt.items():
         nbytes = algorithmic_bytes(name, wl, cfg, touched_per_launch=touched, n_active=n_active,
-                                   ctx=ctx, rows=rows)
+                                   ctx=ctx, rows=rows, formed=formed)
         kernels[name] = {"avg_us": round(d["avg_us"], 3), "launches": d["launches"],
                          "alg_bytes": int(nbytes),
                          "gbs": round(nbytes / (d["avg_us"] * 1e-6) / 1e9, 1) if nbytes else None}
@@ -302,7 +315,7 @@ def main():
     attend_ms = median_ms(lambda: attend(h, 0, qp, tq, op, lp, sp), args.query_reps)
 
     dom_bytes = algorithmic_bytes(dom, wl, cfg, touched_per_launch=touched_live, n_active=n_active,
-                                  ctx=ctx, rows=rows)
+                                  ctx=ctx, rows=rows, formed=formed)
     achieved = dom_bytes / (live["avg_us"] * 1e-6) / 1e9
     traffic = recorded_traffic(dom, wl)
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,

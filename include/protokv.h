@@ -135,7 +135,10 @@ protokv_status protokv_fold(protokv_t h, void* stream);
  * workspace's synthesis buffer (one stream at a time): S pseudo-tokens per
  * active prototype, keys c_k + r^K_s and values p_k + r^V_s rounded to
  * kv_dtype, bias log n_k (Algorithms "DecodeTopSResidualModes" and
- * "Pseudo-Token Decoding and Attention"). */
+ * "Pseudo-Token Decoding and Attention").  The buffer holds the top-S code
+ * tuples, the biases and the rows themselves, except for bf16 KV with S >= 5:
+ * there it holds the float32 centres c_k, p_k instead and protokv_attend
+ * forms each row, with the same rounding, as it reads it. */
 protokv_status protokv_synthesize(protokv_t h, int32_t stream_id, void* stream);
 
 /* Mass-aware readout (Eq. attn_logit): for every layer l, query token t and
@@ -206,6 +209,8 @@ protokv_status protokv_read_bank(protokv_t h, int32_t stream_id, void* dst, size
  * [capacity*S][D] in kv_dtype (rows k*S..k*S+S-1 belong to slot k; only the
  * first active_slots*S rows of each (layer, kv head) are defined) and bias
  * float32 [num_layers][num_kv_heads][capacity].  Any pointer may be NULL.
+ * Rows the synthesis did not write (bf16 KV) are formed first, on `stream`.
+ * Errors: PROTOKV_E_STATE when no synthesis was made since the last fold.
  * Synchronizes `stream`. */
 protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float* bias,
                                    void* stream);
@@ -220,7 +225,8 @@ enum {
   PROTOKV_K_ATTEND = 5,
   PROTOKV_K_ATTEND_MERGE = 6,
   PROTOKV_K_PQ_ENCODE = 7,       /* reserved: PQ encoding runs inside the screen kernel */
-  PROTOKV_K_MATERIALIZE = 8,     /* pseudo-token rows and biases */
+  PROTOKV_K_MATERIALIZE = 8,     /* pseudo-token rows and biases (float32 KV) */
+  PROTOKV_K_CENTRES = 9,         /* float32 centres and biases the bf16 readout expands */
   PROTOKV_K_COUNT = 12
 };
 

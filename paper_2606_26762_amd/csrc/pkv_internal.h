@@ -19,6 +19,12 @@ constexpr int MAXB = 64;   // streams per launch batch
 constexpr int MAX_SPLITS = 16;  // attention context splits (partials storage)
 constexpr int MAX_RBLOCKS = 2;  // query-row blocks of 256 per kv head
 constexpr int KMAX = 65535;     // prototype slots per unit (slot ids fit 16 bits)
+constexpr int PCW = SMAX + 2;   // words per (slot, K/V) decode record: S tuples, no-residual flag, pad
+// The bf16 readout forms pseudo-token rows in LDS from at most PS_SLOTS slots
+// per 64-row tile, which holds for S >= PS_MIN_S (64 consecutive rows span
+// floor(63 / S) + 2 slots at most); below that the synthesis writes the rows.
+constexpr int PS_SLOTS = 14;
+constexpr int PS_MIN_S = 5;
 
 // Bank row (one prototype slot), byte offsets; see protokv.h.
 constexpr int ROW = PROTOKV_ROW_BYTES;
@@ -80,7 +86,8 @@ struct Workspace {
   uint8_t* pk;                // [units][K*S][D] kv dtype (synthesis of one stream)
   uint8_t* pv;
   float* pbias;               // [units][K]
-  uint32_t* pcodes;           // [units][K][2][SMAX + 1]: decoded top-S code tuples + no-residual flag
+  float* pcen;                // [units][K][2][D]: float32 centres (sum / n) of K and V (synthesis, bf16 path)
+  uint32_t* pcodes;           // [units][K][2][PCW]: decoded top-S code tuples, no-residual flag (word SMAX), pad
   float* part_o;              // [units][max_splits][max_rows][D]
   float* part_ml;             // [units][max_splits][max_rows][2]  (max, sum)
   unsigned long long* counters;  // [16]
@@ -120,6 +127,7 @@ struct AttendArgs {
   int tq;
   int splits;       // context splits per kv head
   int chunk;        // context tokens per split (multiple of 32)
+  int gen;          // bf16: pseudo-token rows are formed from centres, codes and codebooks (else read from pk, pv)
   const void* q;
   void* o;
   float* lse;
@@ -136,6 +144,7 @@ hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch
                             hipStream_t st);
 hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st);
 hipError_t launch_materialize(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st);
+hipError_t launch_centres(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st);
 hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& aa,
                          hipStream_t st);
 hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa,

@@ -27,7 +27,7 @@ struct StreamState {
 
 struct Layout {
   size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codebooks, cbhn, cbmax;
-  size_t pk, pv, pbias, pcodes, part_o, part_ml, counters, touched, total;
+  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, total;
 };
 
 thread_local std::string g_init_err;
@@ -63,7 +63,8 @@ Layout make_layout(const protokv_config& c) {
   ly.pk = take(units * K * S * D * es);
   ly.pv = take(units * K * S * D * es);
   ly.pbias = take(units * K * 4);
-  ly.pcodes = take(units * K * 2 * (SMAX + 1) * 4);
+  ly.pcen = take(units * K * 2 * D * 4);
+  ly.pcodes = take(units * K * 2 * PCW * 4);
   ly.part_o = take(units * MAX_SPLITS * rows * D * 4);
   ly.part_ml = take(units * MAX_SPLITS * rows * 2 * 4);
   ly.counters = take(CNT_COUNT * 8);
@@ -117,6 +118,7 @@ struct protokv_ctx {
   std::vector<StreamState> st;
   int synth_stream = -1;
   int synth_active = 0;
+  bool synth_rows = false;  // pseudo-token rows written (else only centres, biases, codes)
   uint64_t folds = 0, assigned = 0, seeded = 0;
   std::string err;
   // per-kernel event timing (diagnostics)
@@ -262,6 +264,7 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.pk = b + ly.pk;
   ws.pv = b + ly.pv;
   ws.pbias = (float*)(b + ly.pbias);
+  ws.pcen = (float*)(b + ly.pcen);
   ws.pcodes = (uint32_t*)(b + ly.pcodes);
   ws.part_o = (float*)(b + ly.part_o);
   ws.part_ml = (float*)(b + ly.part_ml);
@@ -415,12 +418,19 @@ protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
   const int na = h->st[sid].active;
   protokv_status s = h->dev(h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] { return launch_decode(h->dm, h->ws, sid, na, hs); }),
                             "synthesize/decode");
-  if (s == PROTOKV_OK)
+  // bf16 with S >= PS_MIN_S: the readout forms the rows from the centres as
+  // it loads them; otherwise the rows are written here
+  const bool rows = h->dm.kv_fp32 != 0 || h->dm.S < PS_MIN_S;
+  if (s == PROTOKV_OK && rows)
     s = h->dev(h->launch(PROTOKV_K_MATERIALIZE, hs, [&] { return launch_materialize(h->dm, h->ws, sid, na, hs); }),
                "synthesize/materialize");
+  if (s == PROTOKV_OK && !rows)
+    s = h->dev(h->launch(PROTOKV_K_CENTRES, hs, [&] { return launch_centres(h->dm, h->ws, sid, na, hs); }),
+               "synthesize/centres");
   if (s != PROTOKV_OK) return s;
   h->synth_stream = sid;
   h->synth_active = h->st[sid].active;
+  h->synth_rows = rows;
   return PROTOKV_OK;
 }
 
@@ -440,6 +450,7 @@ protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t t
   aa.f_first = (int)(ss.frames - nf);
   aa.n_near = (int)nf * T;
   aa.n_far = h->synth_active * h->dm.S;
+  aa.gen = h->synth_rows ? 0 : 1;
   aa.tq = tq;
   aa.q = q;
   aa.o = o;
@@ -456,6 +467,29 @@ protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t t
   }
   int chunk = (ctx + splits - 1) / splits;
   chunk = (chunk + 63) / 64 * 64;
+  if (!h->dm.kv_fp32 && splits > 1) {
+    // Split i covers context rows [i * chunk, min(ctx, (i + 1) * chunk)).
+    // Pseudo-token tiles formed in LDS cost more than near-window tiles, so
+    // the chunk is the multiple of 64 (>= ctx / splits) that minimises the
+    // largest split's cost in tiles, a formed tile weighing kFormed.
+    const double kFormed = aa.gen ? 1.4 : 1.0;
+    auto tiles = [](int n) { return (n + 63) / 64; };
+    double best = 1e300;
+    int best_chunk = chunk;
+    for (int ch = chunk; ch < ctx + 64; ch += 64) {
+      double worst = 0.0;
+      for (int lo = 0; lo < ctx; lo += ch) {
+        const int hi = std::min(ctx, lo + ch);
+        const int nn = std::max(0, std::min(hi, aa.n_near) - lo);
+        worst = std::max(worst, tiles(nn) + kFormed * tiles(hi - lo - nn));
+      }
+      if (worst < best) {
+        best = worst;
+        best_chunk = ch;
+      }
+    }
+    chunk = best_chunk;
+  }
   splits = (ctx + chunk - 1) / chunk;
   aa.splits = splits;
   aa.chunk = chunk;
@@ -526,8 +560,16 @@ protokv_status protokv_read_bank(protokv_t h, int32_t sid, void* dst, size_t byt
 
 protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float* bias, void* stream) {
   if (!h) return PROTOKV_E_INVALID;
+  if (h->synth_stream < 0) return h->fail(PROTOKV_E_STATE, "read_pseudo: no synthesis since the last fold");
   const size_t n = (size_t)h->dm.units * h->dm.K * h->dm.S * D * kv_bytes(h->cfg);
   protokv_status s = PROTOKV_OK;
+  if (!h->synth_rows && (keys || values)) {
+    hipStream_t hs = (hipStream_t)stream;
+    const int sid = h->synth_stream, na = h->synth_active;
+    s = h->dev(launch_materialize(h->dm, h->ws, sid, na, hs), "read_pseudo/materialize");
+    if (s != PROTOKV_OK) return s;
+    h->synth_rows = true;
+  }
   if (keys) s = copy_out(h, keys, h->ws.pk, n, stream, "read_pseudo");
   if (s == PROTOKV_OK && values) s = copy_out(h, values, h->ws.pv, n, stream, "read_pseudo");
   if (s == PROTOKV_OK && bias) s = copy_out(h, bias, h->ws.pbias, (size_t)h->dm.units * h->dm.K * 4, stream, "read_pseudo");

@@ -12,6 +12,7 @@
 namespace pkv {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
@@ -296,7 +297,7 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
   const size_t unit = (size_t)sid * dm.units + u;
   const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
   const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
-  uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * (SMAX + 1);
+  uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * PCW;
   const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
   const int S = dm.S, C = dm.C;
   const bool nores = !pq || m.n_res == 0;
@@ -466,7 +467,7 @@ __global__ __launch_bounds__(64) void k_decode(Dims dm, Workspace ws, int sid, i
   const int S = dm.S;
   const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
   const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
-  uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * (SMAX + 1);
+  uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * PCW;
   const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
   if (!pq || m.n_res == 0) return;             // flagged by k_decode4
   if (m.n_res <= 65534u && S <= SM) return;    // decoded by k_decode4
@@ -509,8 +510,8 @@ __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int 
     ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
   }
   // the decoded tuples of K and V first (all loads in flight together)
-  const uint32_t* codes_k = ws.pcodes + (((size_t)u * dm.K + p) * 2) * (SMAX + 1);
-  const uint32_t* codes_v = codes_k + (SMAX + 1);
+  const uint32_t* codes_k = ws.pcodes + (((size_t)u * dm.K + p) * 2) * PCW;
+  const uint32_t* codes_v = codes_k + PCW;
   uint32_t ck[SMAX], cv[SMAX];
 #pragma unroll
   for (int s2 = 0; s2 < SMAX; ++s2) {
@@ -546,6 +547,106 @@ __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int 
   }
 }
 
+// bf16 pseudo-tokens, one wave per slot with 16-byte stores: lane l writes
+// dims [8 (l % 16), 8 (l % 16) + 8) of rows s = l / 16 + 4 i (i = 0, 1, ...)
+// of K and of V, so each store instruction covers four whole rows.  The
+// values and their rounding are those of k_materialize.
+__global__ __launch_bounds__(256) void k_materialize16(Dims dm, Workspace ws, int sid, int n_active) {
+  const int lane = threadIdx.x & 63;
+  const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int u = gw / dm.K, p = gw % dm.K;
+  if (u >= dm.units || p >= n_active) return;
+  const size_t unit = (size_t)sid * dm.units + u;
+  const int S = dm.S;
+  const int dq = lane & 15, r0 = lane >> 4;
+  const int g = dq >> 1, hsub = (dq & 1) * 8;  // subspace of these 8 dims, offset inside it
+  const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
+  const float nf = (float)reinterpret_cast<const RowMeta*>(row + ROW_META)->n;
+  const uint32_t* codes = ws.pcodes + (((size_t)u * dm.K + p) * 2) * PCW;
+  const float* cbk = ws.codebooks + unit * (2 * G * CMAX * DP);
+  if (lane == 0) {
+    const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
+    ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
+  }
+  // everything this lane needs first: its 8 dims of both sums, the no-residual
+  // flags and the tuples of its rows
+  float4 sr[2][2];
+  uint32_t tup[2][SMAX / 4];
+  bool nores[2];
+#pragma unroll
+  for (int w = 0; w < 2; ++w) {
+    const float* sums = reinterpret_cast<const float*>(row + (w ? ROW_SUMV : ROW_SUMK)) + 8 * dq;
+    sr[w][0] = reinterpret_cast<const float4*>(sums)[0];
+    sr[w][1] = reinterpret_cast<const float4*>(sums)[1];
+    const uint32_t* cw = codes + w * PCW;
+    nores[w] = cw[SMAX] != 0u;
+#pragma unroll
+    for (int i = 0; i < SMAX / 4; ++i) {
+      const int s2 = r0 + 4 * i;
+      tup[w][i] = s2 < S ? cw[s2] : 0u;
+    }
+  }
+  const int sh = 4 * (G - 1 - g);
+#pragma unroll
+  for (int w = 0; w < 2; ++w) {
+    const float c[8] = {sr[w][0].x / nf, sr[w][0].y / nf, sr[w][0].z / nf, sr[w][0].w / nf,
+                        sr[w][1].x / nf, sr[w][1].y / nf, sr[w][1].z / nf, sr[w][1].w / nf};
+    const float* cbw = cbk + ((size_t)w * G + g) * CMAX * DP + hsub;
+    uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * S + (size_t)p * S) * D * 2 + dq * 16;
+#pragma unroll
+    for (int i = 0; i < SMAX / 4; ++i) {
+      const int s2 = r0 + 4 * i;
+      if (s2 < S) {
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = c[e];
+        if (!nores[w]) {
+          const int z = (tup[w][i] >> sh) & 15;
+          const float4 a = reinterpret_cast<const float4*>(cbw + z * DP)[0];
+          const float4 b = reinterpret_cast<const float4*>(cbw + z * DP)[1];
+          v[0] = c[0] + a.x; v[1] = c[1] + a.y; v[2] = c[2] + a.z; v[3] = c[3] + a.w;
+          v[4] = c[4] + b.x; v[5] = c[5] + b.y; v[6] = c[6] + b.z; v[7] = c[7] + b.w;
+        }
+        uint4 o;
+        o.x = (uint32_t)q_to_bf16(v[0]) | ((uint32_t)q_to_bf16(v[1]) << 16);
+        o.y = (uint32_t)q_to_bf16(v[2]) | ((uint32_t)q_to_bf16(v[3]) << 16);
+        o.z = (uint32_t)q_to_bf16(v[4]) | ((uint32_t)q_to_bf16(v[5]) << 16);
+        o.w = (uint32_t)q_to_bf16(v[6]) | ((uint32_t)q_to_bf16(v[7]) << 16);
+        *reinterpret_cast<uint4*>(out + (size_t)s2 * D * 2) = o;
+      }
+    }
+  }
+}
+
+// Synthesis without rows: the float32 centres c = float32(sum / n) of K and V
+// of every active slot (IEEE division) and the bias log n, which the bf16
+// readout turns into pseudo-token rows as it loads them.  Thread = (slot,
+// K/V, 4 dims).
+__global__ __launch_bounds__(256) void k_centres(Dims dm, Workspace ws, int sid, int n_active) {
+  const size_t gt = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int d4 = (int)(gt & 31), kv = (int)((gt >> 5) & 1);
+  const size_t up = gt >> 6;
+  const int u = (int)(up / n_active), p = (int)(up % n_active);
+  if (u >= dm.units) return;
+  const size_t unit = (size_t)sid * dm.units + u;
+  const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
+  const float nf = (float)reinterpret_cast<const RowMeta*>(row + ROW_META)->n;
+  const float4 sm = reinterpret_cast<const float4*>(row + (kv ? ROW_SUMV : ROW_SUMK))[d4];
+  reinterpret_cast<float4*>(ws.pcen + (((size_t)u * dm.K + p) * 2 + kv) * D)[d4] =
+      make_float4(sm.x / nf, sm.y / nf, sm.z / nf, sm.w / nf);
+  if (d4 == 0 && kv == 0) {
+    const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
+    ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
+  }
+}
+
+hipError_t launch_centres(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st) {
+  if (n_active <= 0) return hipSuccess;
+  const size_t threads = (size_t)dm.units * n_active * 64;
+  hipLaunchKernelGGL(k_centres, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, dm, ws, sid, n_active);
+  return hipGetLastError();
+}
+
 hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st) {
   if (n_active <= 0) return hipSuccess;
   const int bpu = (n_active + SYN_P - 1) / SYN_P;
@@ -568,7 +669,7 @@ hipError_t launch_materialize(const Dims& dm, const Workspace& ws, int sid, int 
   if (dm.kv_fp32)
     hipLaunchKernelGGL(k_materialize<1>, dim3((waves + 3) / 4), dim3(256), 0, st, dm, ws, sid, n_active);
   else
-    hipLaunchKernelGGL(k_materialize<0>, dim3((waves + 3) / 4), dim3(256), 0, st, dm, ws, sid, n_active);
+    hipLaunchKernelGGL(k_materialize16, dim3((waves + 3) / 4), dim3(256), 0, st, dm, ws, sid, n_active);
   return hipGetLastError();
 }
 
@@ -608,15 +709,18 @@ __device__ __forceinline__ CtxRef ctx_key(const Dims& dm, const Workspace& ws, c
 }
 
 // bf16 path.  Workgroup = one (kv head, context split, block of up to 256
-// query rows), one wave per 32 rows (at least 4 waves).  Context tiles of 64
-// keys go straight from global memory into double-buffered LDS
-// (global_load_lds_dwordx4, row-major, 16-byte chunks XOR-swizzled by row so
-// the operand reads do not conflict); the next tile loads while the current
-// one is computed.  S^T = K Q^T and O^T = V^T P with v_mfma_f32_32x32x16_bf16;
-// the V^T operand comes from the row-major tile through ds_read_b64_tr_b16.
-// Each lane holds one query column, so the online softmax is lane-local plus
-// one exchange with the partner lane.  With several splits, every workgroup
-// writes its partial (unnormalised O, running max, sum) for k_attend_merge.
+// query rows), one wave per 32 rows (at least 4 waves).  A context tile of 64
+// keys sits in LDS in two layouts under which every operand read is a per-lane
+// base plus compile-time offsets and touches distinct banks:
+//   K chunk-major: 16-byte chunk c (dims 8c .. 8c+7) of row r at c * 1024 + r * 16;
+//   V by 32-dim block: dims 32b .. 32b+31 of row r at b * 4096 + r * 64.
+// Near-window tiles go straight from global memory into these layouts
+// (global_load_lds_dwordx4), three tiles ahead of the one computed.
+// S^T = K Q^T and O^T = V^T P with v_mfma_f32_32x32x16_bf16; the V^T operand
+// comes through ds_read_b64_tr_b16.  Each lane holds one query column, so the
+// online softmax is lane-local plus one exchange with the partner lane.  With
+// several splits, every workgroup writes its partial (unnormalised O, running
+// max, sum) for k_attend_merge.
 constexpr int AT_KEYS = 64;
 constexpr int AT_ROWS = 256;  // query rows per workgroup
 constexpr int AT_TILE_BYTES = AT_KEYS * D * 2;   // one K or V tile, 16 KB
@@ -626,9 +730,6 @@ typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_void;
-
-// byte offset of 16-byte chunk c of tile row r
-__device__ __forceinline__ int at_chunk(int r, int c) { return r * (D * 2) + ((c ^ (r & 15)) << 4); }
 
 // Barrier for LDS traffic only: waits for this wave's LDS operations, not
 // for its outstanding global loads (the tiles in flight).  The asm memory
@@ -678,7 +779,12 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
   const int ctx = aa.n_near + aa.n_far;
   const int c0 = split * aa.chunk;
   const int c1 = min(ctx, c0 + aa.chunk);
-  const int ntiles = c1 > c0 ? (c1 - c0 + AT_KEYS - 1) / AT_KEYS : 0;
+  // rows [c0, c1n) stream through LDS by DMA (near-window rows, and the
+  // written pseudo-token rows when aa.gen is 0); with aa.gen the pseudo-token
+  // rows [max(c0, n_near), c1) are formed in LDS from the synthesized centres,
+  // decode records and codebooks
+  const int c1n = aa.gen ? min(c1, aa.n_near) : c1;
+  const int ntiles = c1n > c0 ? (c1n - c0 + AT_KEYS - 1) / AT_KEYS : 0;
   const bool pb_lds = dm.K <= AT_PB_MAX;
   if (pb_lds)
     for (int k = tid; k < dm.K; k += NW * 64) s_pb[k] = ws.pbias[(size_t)u * dm.K + k] * LOG2E;
@@ -707,8 +813,8 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
   const float invS = 1.0f / (float)dm.S;
   auto resolve = [&](int t, const uint8_t*& kp, const uint8_t*& vp, float& bv) {
     const int idx = c0 + t * AT_KEYS + lane;
-    const int pos = idx < c1 ? idx : c0;
-    bv = idx < c1 ? 0.f : -INFINITY;
+    const int pos = idx < c1n ? idx : c0;
+    bv = idx < c1n ? 0.f : -INFINITY;
     if (pos < aa.n_near) {
       const int fo = pos / dm.T;
       const int slot = (aa.f_first + fo) % (dm.W + 1);
@@ -723,7 +829,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
       int k = (int)((float)prow * invS);
       k -= k * dm.S > prow ? 1 : 0;
       k += (k + 1) * dm.S <= prow ? 1 : 0;
-      if (idx < c1) bv = pb_lds ? s_pb[k] : ws.pbias[(size_t)u * dm.K + k] * LOG2E;
+      if (idx < c1n) bv = pb_lds ? s_pb[k] : ws.pbias[(size_t)u * dm.K + k] * LOG2E;
     }
   };
   auto publish = [&](int t, const uint8_t* kp, const uint8_t* vp, float bv) {
@@ -732,19 +838,23 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
     s_rowp[e][1][lane] = vp;
     s_bias[e][lane] = bv;
   };
-  // Loads of tile t: instruction i = wave + q * NW (q < LPT) moves tile row
-  // 4 (i & 15) + lane / 16 of K (i < 16) or V, 16-byte chunk (lane & 15) ^
-  // (row & 15) (XOR swizzle), straight into LDS buffer t % AT_NBUF.
+  // Loads of tile t into LDS buffer t % AT_NBUF: instruction i = wave + q * NW
+  // (q < LPT) moves 1 KiB, K chunk i of all 64 rows (lane = row) for i < 16,
+  // else V block j = i - 16: dims 32 (j / 4) .. +31 of rows 16 (j % 4) ..
+  // +15 (lane / 4 = row, lane % 4 = 16-byte part).
   auto issue = [&](int t) {
     const int e = t % AT_NTAB, buf = t % AT_NBUF;
 #pragma unroll
     for (int q = 0; q < LPT; ++q) {
-      const int i = wave + q * NW;
-      const int kv = i >> 4, ii = i & 15;
-      const int row = ii * 4 + (lane >> 4);
-      const int cl = (lane & 15) ^ (row & 15);
-      const uint8_t* base = s_rowp[e][kv][row];
-      lds_dma16(base + cl * 16, &s_kv[buf][kv][ii * 1024]);
+      const int i = wave + q * NW;  // uniform
+      const uint8_t* src;
+      if (i < 16) {
+        src = s_rowp[e][0][lane] + i * 16;
+      } else {
+        const int j = i - 16;
+        src = s_rowp[e][1][(j & 3) * 16 + (lane >> 2)] + ((j >> 2) * 4 + (lane & 3)) * 16;
+      }
+      lds_dma16(src, &s_kv[buf][i >> 4][(i & 15) * 1024]);
     }
   };
 
@@ -757,6 +867,125 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
   // when a row's max exceeds it by more than 8, so p <= 2^8 and the output
   // accumulators are rescaled rarely.
   float mref = -1e30f, lrun = 0.f;
+
+  // per-lane operand bases: K row h*32 + col, chunk 2 kk + half at
+  // koff + kk * 2048 + h * 512; V (transposed reads, see below) at
+  // voff + b * 4096 + st * 1024 (+ 512 for keys 8 .. 15 of the step)
+  const int grp16 = lane >> 4, s16 = lane & 15;
+  const int koff = half * 1024 + col * 16;
+  const int voff = (4 * half + (s16 >> 2)) * 64 + (grp16 & 1) * 32 + (s16 & 3) * 8;
+  const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
+
+  // one 64-key tile in LDS (K at kt, V at vt): S^T = K Q^T, scores with the
+  // tile's biases, online softmax, O^T += V^T P.  Without BIAS (a full tile of
+  // near-window keys after the first tile, all biases 0) the scores are taken
+  // relative to the running reference in the same multiply-add.
+  auto compute_tile = [&](const uint8_t* kt, const uint8_t* vt, int tb, auto bias_tag) {
+    constexpr bool BIAS = decltype(bias_tag)::value;
+    const uint8_t* kl = kt + koff;
+    const uint8_t* vl = vt + voff;
+    // S^T for the two 32-key halves of the tile
+    f32x16 sacc[2];
+  #pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      sacc[h] = (f32x16){0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  #pragma unroll
+      for (int kk = 0; kk < 8; ++kk) {
+        const bf16x8 ak = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(kl + kk * 2048 + h * 512));
+        sacc[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bq[kk], sacc[h], 0, 0, 0);
+      }
+    }
+    // scores x = s * scale + bias (key m = h*32 + (i/4)*8 + half*4 + i%4),
+    // without BIAS x = s * scale - mref
+    float tmax = -1e30f;
+    if constexpr (BIAS) {
+  #pragma unroll
+      for (int h = 0; h < 2; ++h)
+  #pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const float4 bb = *reinterpret_cast<const float4*>(&s_bias[tb][h * 32 + i4 * 8 + half * 4]);
+          const float bv[4] = {bb.x, bb.y, bb.z, bb.w};
+  #pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float x = fmaf(sacc[h][i4 * 4 + e], scale, bv[e]);
+            sacc[h][i4 * 4 + e] = x;
+            tmax = fmaxf(tmax, x);
+          }
+        }
+    } else {
+      const float nm = -mref;
+  #pragma unroll
+      for (int h = 0; h < 2; ++h)
+  #pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float x = fmaf(sacc[h][i], scale, nm);
+          sacc[h][i] = x;
+          tmax = fmaxf(tmax, x);
+        }
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    // the reference moves up only when a row's max exceeds it by more than 8
+    const bool grow = BIAS ? tmax > mref + 8.0f : tmax > 8.0f;
+    if (__ballot(grow)) {  // uniform
+      if constexpr (BIAS) {
+        const float mnew = grow ? tmax : mref;
+        const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
+        lrun *= alpha;
+  #pragma unroll
+        for (int b = 0; b < 4; ++b)
+  #pragma unroll
+          for (int i = 0; i < 16; ++i) oacc[b][i] *= alpha;
+        mref = mnew;
+      } else {
+        const float mnew = grow ? mref + tmax : mref;
+        const float delta = mnew - mref;
+        const float alpha = __builtin_amdgcn_exp2f(-delta);
+        lrun *= alpha;
+  #pragma unroll
+        for (int b = 0; b < 4; ++b)
+  #pragma unroll
+          for (int i = 0; i < 16; ++i) oacc[b][i] *= alpha;
+  #pragma unroll
+        for (int h = 0; h < 2; ++h)
+  #pragma unroll
+          for (int i = 0; i < 16; ++i) sacc[h][i] -= delta;
+        mref = mnew;
+      }
+    }
+    // P in bf16; the row sum is taken over the rounded values the products use
+    bf16x8 pb[4];
+  #pragma unroll
+    for (int h = 0; h < 2; ++h)
+  #pragma unroll
+      for (int i = 0; i < 16; ++i)
+        pb[2 * h + (i >> 3)][i & 7] = (__bf16)__builtin_amdgcn_exp2f(BIAS ? sacc[h][i] - mref : sacc[h][i]);
+    float sum0 = 0.f, sum1 = 0.f;
+  #pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      sum0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 0, 1), ones2, sum0, false);
+      sum1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 2, 3), ones2, sum1, false);
+      sum0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 4, 5), ones2, sum0, false);
+      sum1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 6, 7), ones2, sum1, false);
+    }
+    float psum = sum0 + sum1;
+    psum += __shfl_xor(psum, 32, 64);
+    lrun += psum;
+    // O^T = V^T P.  k positions half*8 + i of step st <-> keys 16 st + 4 half + {0..3}
+    // (i < 4) and 16 st + 8 + 4 half + {0..3} (i >= 4), matching P's layout.  Each
+    // 4-key part is one ds_read_b64_tr_b16 per 16-lane group: source lane s reads
+    // key key0 + s/4, dims d0 + 4(s%4) .. +3 (d0 = 32 b + 16 (lane/16 % 2)); lane i
+    // then holds dim d0 + i of the 4 keys.
+  #pragma unroll
+    for (int b = 0; b < 4; ++b) {
+  #pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vl + b * 4096 + st * 1024));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vl + b * 4096 + st * 1024 + 512));
+        const v8i16 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), pb[st], oacc[b], 0, 0, 0);
+      }
+    }
+  };
 
   // prologue: rows of tiles 0..2 published, their loads issued; tile 3 resolved
   const uint8_t *nk = nullptr, *nv = nullptr;
@@ -785,79 +1014,153 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
     if (t + 3 < ntiles) issue(t + 3);
     if (wave == 0 && t + 4 < ntiles) resolve(t + 4, nk, nv, nb);
     if (!wvalid) continue;  // uniform: a loader-only wave
-    const uint8_t* kt = s_kv[buf][0];
-    const uint8_t* vt = s_kv[buf][1];
-    // S^T for the two 32-key halves of the tile
-    f32x16 sacc[2];
+    // a full tile of near-window keys past the first has all biases 0
+    if (t > 0 && c0 + (t + 1) * AT_KEYS <= min(c1n, aa.n_near))
+      compute_tile(s_kv[buf][0], s_kv[buf][1], tb, std::false_type{});
+    else
+      compute_tile(s_kv[buf][0], s_kv[buf][1], tb, std::true_type{});
+  }
+
+  // Pseudo-token tiles formed in LDS (aa.gen): row (k, s) of K is
+  // bf16(c_k + concat_g C^K_g[z_{s,g}]) (c_k alone when the slot has no
+  // residual), the values k_materialize writes; likewise V.  The inputs of a
+  // tile (float32 centres, 1 KiB per slot, and decode records of its <=
+  // PS_SLOTS slots) go by DMA into one of three 16 KiB staging buffers three
+  // tiles ahead, with PS_INSTR load instructions per tile spread evenly over
+  // the waves (unused ones repeat a valid slot), so every wave's outstanding
+  // count is known.  Iteration t: wait for tile t+1's inputs, barrier, issue
+  // tile t+3's, form tile t+1 into buffer (t+1) % 2, compute tile t: the
+  // forming of the next tile overlaps the MFMA work of the current one.
+  // LDS: buffers 0, 1 the formed tiles, s_kv[2][0] the unit's codebooks (16
+  // KiB), s_kv[2][1] .. s_kv[3][1] the staging buffers.
+  const int ps0 = max(c0, aa.n_near) - aa.n_near, ps1 = c1 - aa.n_near;
+  const int npt = aa.gen && ps1 > ps0 ? (ps1 - ps0 + AT_KEYS - 1) / AT_KEYS : 0;
+  if (npt > 0) {  // uniform
+    constexpr int PS_INSTR = 16;                        // PS_SLOTS centre loads + 2 record loads
+    constexpr int PS_STAGE = AT_TILE_BYTES;             // 16 KiB
+    constexpr int PS_REC = PS_SLOTS * 1024;             // records at this offset of a stage
+    constexpr int IPW = PS_INSTR / NW;                  // load instructions per wave per tile
+    constexpr int CPT = 2 * AT_KEYS * 16 / (NW * 64);   // 16-byte chunks formed per thread per tile
+    static_assert(PS_REC + 2 * 1024 <= PS_STAGE && 2 * PCW * 4 * PS_SLOTS <= 2 * 1024, "stage layout");
+    static_assert(1024 % (NW * 64) == 0, "a thread's chunks of one pass are all K or all V");
+    const int S = dm.S;
+    const float invS2 = 1.0f / (float)S;
+    auto divS = [&](int x) {
+      int k = (int)((float)x * invS2);
+      k -= k * S > x ? 1 : 0;
+      k += (k + 1) * S <= x ? 1 : 0;
+      return k;
+    };
+    uint8_t* s_cbb = s_kv[2][0];
+    uint8_t* s_stage = s_kv[2][1];
+    const size_t ubase = (size_t)u * dm.K;
+    // Staged centre of the slot at stage position i: 16-byte unit (K/V half
+    // kvh, part 2 cl + e) at kvh * 32 + (2 cl + e + 2 i) % 32, so that rows of
+    // different slots reading one chunk fall on different banks.
+    auto stage = [&](int t) {
+      const int r0 = ps0 + t * AT_KEYS;
+      const int kA = divS(r0), kB = divS(min(r0 + AT_KEYS, ps1) - 1);
+      const int nk = kB - kA + 1;
+      uint8_t* sb = s_stage + (t % 3) * PS_STAGE;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      sacc[h] = (f32x16){0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      const int krow = h * 32 + col;
-#pragma unroll
-      for (int kk = 0; kk < 8; ++kk) {
-        const bf16x8 ak = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(kt + at_chunk(krow, 2 * kk + half)));
-        sacc[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bq[kk], sacc[h], 0, 0, 0);
-      }
-    }
-    // scores x = s * scale + bias (key m = h*32 + (i/4)*8 + half*4 + i%4)
-    float tmax = -1e30f;
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int i4 = 0; i4 < 4; ++i4) {
-        const float4 bb = *reinterpret_cast<const float4*>(&s_bias[tb][h * 32 + i4 * 8 + half * 4]);
-        const float bv[4] = {bb.x, bb.y, bb.z, bb.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float x = fmaf(sacc[h][i4 * 4 + e], scale, bv[e]);
-          sacc[h][i4 * 4 + e] = x;
-          tmax = fmaxf(tmax, x);
+      for (int q = 0; q < IPW; ++q) {
+        const int i = wave + q * NW;  // uniform
+        const uint8_t* src;
+        uint8_t* dst;
+        if (i < PS_SLOTS) {
+          const int part = (lane & 32) + (((lane & 31) - 2 * i) & 31);
+          src = reinterpret_cast<const uint8_t*>(ws.pcen + (ubase + kA + min(i, nk - 1)) * 2 * D) + part * 16;
+          dst = sb + i * 1024;
+        } else {
+          const int ch = min((i - PS_SLOTS) * 64 + lane, nk * (2 * PCW / 4) - 1);
+          src = reinterpret_cast<const uint8_t*>(ws.pcodes + (ubase + kA) * 2 * PCW) + ch * 16;
+          dst = sb + PS_REC + (i - PS_SLOTS) * 1024;
         }
+        lds_dma16(src, dst);
       }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const bool grow = tmax > mref + 8.0f;
-    if (__ballot(grow)) {  // uniform
-      const float mnew = grow ? tmax : mref;
-      const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
-      lrun *= alpha;
+    };
+    // Tile t from stage t % 3 into buffer t % 2, in the layouts of the near
+    // tiles.  A thread forms the 16-byte store units q = tid + e * NW * 64 of
+    // K (row q % 64, chunk q / 64) and of V (row q / 4 % 64, chunk
+    // 4 (q / 256) + q % 4): one K row and one V row per thread, and each
+    // store instruction writes 1 KiB contiguous.
+    auto form = [&](int t) {
+      constexpr int UPT = 1024 / (NW * 64);  // units per thread of K (and of V)
+      const int r0 = ps0 + t * AT_KEYS;
+      const int kA = divS(r0);
+      const uint8_t* sb = s_stage + (t % 3) * PS_STAGE;
+      const int pb = t & 1;
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
+      for (int kv = 0; kv < 2; ++kv) {
+        const int row = kv ? (tid >> 2) & 63 : tid & 63;
+        const bool valid = r0 + row < ps1;
+        const int prow = valid ? r0 + row : r0;  // rows past the context repeat a valid row (bias -inf)
+        const int k = divS(prow);
+        const int j = k - kA, s2 = prow - k * S;
+        const uint32_t* rec = reinterpret_cast<const uint32_t*>(sb + PS_REC) + (j * 2 + kv) * PCW;
+        const uint32_t tup = rec[s2];
+        const float m = rec[SMAX] != 0u ? 0.f : 1.f;  // no residual: the centre alone
+        const float4* cen = reinterpret_cast<const float4*>(sb + j * 1024 + kv * 512);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[b][i] *= alpha;
-      mref = mnew;
+        for (int e = 0; e < UPT; ++e) {
+          const int q = tid + e * NW * 64;
+          const int cl = kv ? (q >> 8) * 4 + (q & 3) : q >> 6;
+          const float4 ca = cen[(2 * cl + 2 * j) & 31], cb = cen[(2 * cl + 1 + 2 * j) & 31];
+          const int g = cl >> 1;
+          const int z = (tup >> (4 * (G - 1 - g))) & 15;
+          const float4* cw = reinterpret_cast<const float4*>(s_cbb) + ((kv * G + g) * CMAX + z) * 4;
+          const int zr = z >> 2;
+          const float4 wa = cw[(2 * (cl & 1) + zr) & 3], wb = cw[(2 * (cl & 1) + 1 + zr) & 3];
+          // w * m + c is exactly c + w (m = 1) or c (m = 0)
+          const bf16x2 o0 = {(__bf16)fmaf(wa.x, m, ca.x), (__bf16)fmaf(wa.y, m, ca.y)};
+          const bf16x2 o1 = {(__bf16)fmaf(wa.z, m, ca.z), (__bf16)fmaf(wa.w, m, ca.w)};
+          const bf16x2 o2 = {(__bf16)fmaf(wb.x, m, cb.x), (__bf16)fmaf(wb.y, m, cb.y)};
+          const bf16x2 o3 = {(__bf16)fmaf(wb.z, m, cb.z), (__bf16)fmaf(wb.w, m, cb.w)};
+          *reinterpret_cast<uint4*>(s_kv[pb][kv] + q * 16) =
+              make_uint4(__builtin_bit_cast(uint32_t, o0), __builtin_bit_cast(uint32_t, o1),
+                         __builtin_bit_cast(uint32_t, o2), __builtin_bit_cast(uint32_t, o3));
+        }
+        if (kv == 0 && tid < AT_KEYS)  // row == tid
+          s_bias[pb][row] = valid ? (pb_lds ? s_pb[k] : ws.pbias[ubase + k] * LOG2E) : -INFINITY;
+      }
+    };
+
+    lds_barrier();  // every wave is done with the near tiles (buffers and bias entries are reused)
+    // codebooks as [K/V][subspace][codeword][4 parts of 16 bytes], part s of
+    // codeword z at position (s + z / 4) % 4: rows reading one chunk of
+    // different codewords fall on different banks
+#pragma unroll
+    for (int q = 0; q < 16 / NW; ++q) {
+      const int i = wave + q * NW;
+      const int pos = i * 64 + lane;
+      const int z = (pos >> 2) & 15;
+      const int part = (pos & ~3) + (((pos & 3) - (z >> 2)) & 3);
+      lds_dma16(reinterpret_cast<const uint8_t*>(ws.codebooks + unit * (2 * G * CMAX * DP)) + part * 16,
+                s_cbb + i * 1024);
     }
-    float psum = 0.f;
-    bf16x8 pb[4];
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float pv = __builtin_amdgcn_exp2f(sacc[h][i] - mref);
-        psum += pv;
-        pb[2 * h + (i >> 3)][i & 7] = (__bf16)pv;
-      }
-    psum += __shfl_xor(psum, 32, 64);
-    lrun += psum;
-    // O^T = V^T P.  k positions half*8 + i of step st <-> keys 16 st + 4 half + {0..3}
-    // (i < 4) and 16 st + 8 + 4 half + {0..3} (i >= 4), matching P's layout.  Each
-    // 4-key part is one ds_read_b64_tr_b16 per 16-lane group: source lane s reads
-    // key key0 + s/4, dims d0 + 4(s%4) .. +3; lane i then holds dim d0 + i of the 4 keys.
-    const int grp16 = lane >> 4, s16 = lane & 15;
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int d0 = b * 32 + (grp16 & 1) * 16;
-      const int dsrc = d0 + 4 * (s16 & 3);
-#pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        const int ka = st * 16 + 4 * half + (s16 >> 2);
-        const int kb = ka + 8;
-        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_v4i16*)(vt + at_chunk(ka, dsrc >> 3) + (dsrc & 7) * 2));
-        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_v4i16*)(vt + at_chunk(kb, dsrc >> 3) + (dsrc & 7) * 2));
-        const v8i16 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), pb[st], oacc[b], 0, 0, 0);
-      }
+    stage(0);
+    if (npt > 1) stage(1);
+    if (npt > 2) stage(2);
+    // codebooks and tile 0's inputs have landed (tiles 1, 2 may be in flight)
+    if (npt > 2) wait_vm<2 * IPW>();
+    else if (npt > 1) wait_vm<IPW>();
+    else wait_vm<0>();
+    lds_barrier();
+    form(0);
+    for (int t = 0; t < npt; ++t) {
+      // this wave's loads of tile t+1's inputs have landed (tile t+2's may be in flight)
+      if (t + 2 < npt) wait_vm<IPW>();
+      else wait_vm<0>();
+      // tile t formed everywhere; stage t % 3 (read by form(t)) and formed
+      // buffer (t+1) % 2 (read by compute(t-1)) are free
+      lds_barrier();
+      if (t + 3 < npt) stage(t + 3);
+      // waves w and w + 4 share a SIMD: one forms before computing, the other
+      // after, so the forming overlaps the partner's matrix work
+      const bool form_first = wave < 4 || !wvalid;  // uniform
+      if (form_first && t + 1 < npt) form(t + 1);
+      if (wvalid) compute_tile(s_kv[t & 1][0], s_kv[t & 1][1], t & 1, std::true_type{});
+      if (!form_first && t + 1 < npt) form(t + 1);
     }
   }
   const float mrun = mref;
