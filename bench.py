@@ -79,14 +79,14 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
         return (U * (2 * T * D * b + T * 4)
                 + touched_per_launch * (2 * ROW_STATS_BYTES + CACHE_BYTES))
     if kernel == "decode":
-        return U * n_active * (2 * 8 * 16 * 4 + 32 + 2 * (S + 1) * 4)       # histograms, meta, codes out
+        # histograms, meta, codes out; with formed rows also the sums in and
+        # the float32 centres and bias out
+        extra = (2 * D * 4 + 2 * D * 4 + 4) if formed else 0
+        return U * n_active * (2 * 8 * 16 * 4 + 32 + 2 * (S + 1) * 4 + extra)
     if kernel == "materialize":
         # sums, meta, codes, codebooks per unit, pseudo-token rows out, bias out
         return (U * n_active * (2 * 4 * D + 32 + 2 * (S + 1) * 4 + S * D * b * 2 + 4)
                 + U * 2 * 8 * 16 * 16 * 4)
-    if kernel == "centres":
-        # sums and meta in, float32 centres and bias out
-        return U * n_active * (2 * D * 4 + 32 + 2 * D * 4 + 4)
     if kernel == "attend":
         if formed:
             # near-window K, V; per active slot its centres, code tuples and
@@ -100,7 +100,7 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
 
 FOLD_KERNELS = ("ring_insert", "seed", "screen", "aggregate")
 KERNEL_SOURCES = {k: "fold.hip" for k in FOLD_KERNELS}
-KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "centres", "attend", "attend_merge")})
+KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "attend", "attend_merge")})
 
 
 def kernel_source_hash(kernel):
@@ -263,7 +263,7 @@ def main():
     touched = (c1.touched - c0.touched) / max(1, kt.get("aggregate", {}).get("launches", 1))
     rows = tq * (wl.num_q_heads // wl.num_kv_heads)
     ctx = min(info.frames, wl.window_frames) * T + n_active * cfg.pseudo_per_proto
-    formed = "centres" in kt
+    formed = "materialize" not in kt  # bf16 readout forms the pseudo-token rows itself
     kernels = {}
     for name, d in kt.items():
         nbytes = algorithmic_bytes(name, wl, cfg, touched_per_launch=touched, n_active=n_active,

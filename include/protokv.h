@@ -226,7 +226,6 @@ enum {
   PROTOKV_K_ATTEND_MERGE = 6,
   PROTOKV_K_PQ_ENCODE = 7,       /* reserved: PQ encoding runs inside the screen kernel */
   PROTOKV_K_MATERIALIZE = 8,     /* pseudo-token rows and biases (float32 KV) */
-  PROTOKV_K_CENTRES = 9,         /* float32 centres and biases the bf16 readout expands */
   PROTOKV_K_COUNT = 12
 };
 

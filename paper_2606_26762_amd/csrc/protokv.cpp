@@ -416,17 +416,16 @@ protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
   if (h->st[sid].pending) return h->fail(PROTOKV_E_STATE, "synthesize: stream has an unfolded eviction");
   hipStream_t hs = (hipStream_t)stream;
   const int na = h->st[sid].active;
-  protokv_status s = h->dev(h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] { return launch_decode(h->dm, h->ws, sid, na, hs); }),
-                            "synthesize/decode");
-  // bf16 with S >= PS_MIN_S: the readout forms the rows from the centres as
-  // it loads them; otherwise the rows are written here
+  // bf16 with S >= PS_MIN_S: the decode also writes the float32 centres and
+  // the readout forms the rows from them as it loads them; otherwise the rows
+  // are written here
   const bool rows = h->dm.kv_fp32 != 0 || h->dm.S < PS_MIN_S;
+  protokv_status s = h->dev(
+      h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] { return launch_decode(h->dm, h->ws, sid, na, !rows, hs); }),
+      "synthesize/decode");
   if (s == PROTOKV_OK && rows)
     s = h->dev(h->launch(PROTOKV_K_MATERIALIZE, hs, [&] { return launch_materialize(h->dm, h->ws, sid, na, hs); }),
                "synthesize/materialize");
-  if (s == PROTOKV_OK && !rows)
-    s = h->dev(h->launch(PROTOKV_K_CENTRES, hs, [&] { return launch_centres(h->dm, h->ws, sid, na, hs); }),
-               "synthesize/centres");
   if (s != PROTOKV_OK) return s;
   h->synth_stream = sid;
   h->synth_active = h->st[sid].active;

@@ -285,7 +285,7 @@ __device__ __forceinline__ uint32_t sel32(bool t, uint32_t a, uint32_t b) {
 }
 
 template <int SM>
-__global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid, int n_active) {
+__global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid, int n_active, int centres) {
   constexpr int E = SM / 4;  // prefixes per lane
   __shared__ uint32_t s_rank[4][DEC_BEAMS][CMAX];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -302,6 +302,22 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
   const int S = dm.S, C = dm.C;
   const bool nores = !pq || m.n_res == 0;
   if (bvalid && q == 0 && nores) out[SMAX] = 1u;
+  if (bvalid && centres) {
+    // the float32 centre sum / n of this (slot, K/V) (IEEE division) for the
+    // readout's row forming, lane q taking float4s q, q + 4, ...; and the bias
+    const float nf = (float)m.n;
+    const float4* sums = reinterpret_cast<const float4*>(row + (kv ? ROW_SUMV : ROW_SUMK));
+    float4* cen = reinterpret_cast<float4*>(ws.pcen + (((size_t)u * dm.K + p) * 2 + kv) * D);
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) {
+      const float4 v = sums[q + 4 * i];
+      cen[q + 4 * i] = make_float4(v.x / nf, v.y / nf, v.z / nf, v.w / nf);
+    }
+    if (kv == 0 && q == 0) {
+      const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
+      ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
+    }
+  }
   // this path decodes the beam (uniform within the four lanes)
   const bool mine = bvalid && !nores && m.n_res <= 65534u && S <= SM;
   const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
@@ -618,46 +634,17 @@ __global__ __launch_bounds__(256) void k_materialize16(Dims dm, Workspace ws, in
   }
 }
 
-// Synthesis without rows: the float32 centres c = float32(sum / n) of K and V
-// of every active slot (IEEE division) and the bias log n, which the bf16
-// readout turns into pseudo-token rows as it loads them.  Thread = (slot,
-// K/V, 4 dims).
-__global__ __launch_bounds__(256) void k_centres(Dims dm, Workspace ws, int sid, int n_active) {
-  const size_t gt = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const int d4 = (int)(gt & 31), kv = (int)((gt >> 5) & 1);
-  const size_t up = gt >> 6;
-  const int u = (int)(up / n_active), p = (int)(up % n_active);
-  if (u >= dm.units) return;
-  const size_t unit = (size_t)sid * dm.units + u;
-  const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
-  const float nf = (float)reinterpret_cast<const RowMeta*>(row + ROW_META)->n;
-  const float4 sm = reinterpret_cast<const float4*>(row + (kv ? ROW_SUMV : ROW_SUMK))[d4];
-  reinterpret_cast<float4*>(ws.pcen + (((size_t)u * dm.K + p) * 2 + kv) * D)[d4] =
-      make_float4(sm.x / nf, sm.y / nf, sm.z / nf, sm.w / nf);
-  if (d4 == 0 && kv == 0) {
-    const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
-    ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
-  }
-}
-
-hipError_t launch_centres(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st) {
-  if (n_active <= 0) return hipSuccess;
-  const size_t threads = (size_t)dm.units * n_active * 64;
-  hipLaunchKernelGGL(k_centres, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, dm, ws, sid, n_active);
-  return hipGetLastError();
-}
-
-hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st) {
+hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, bool centres, hipStream_t st) {
   if (n_active <= 0) return hipSuccess;
   const int bpu = (n_active + SYN_P - 1) / SYN_P;
   const size_t lds = (size_t)2 * dm.S * 64 * (3 * sizeof(uint64_t) + sizeof(uint32_t));
   const int nbeams = dm.units * n_active * 2;
   const int nblk4 = (nbeams + 4 * DEC_BEAMS - 1) / (4 * DEC_BEAMS);
   if (dm.S <= 8) {
-    hipLaunchKernelGGL(k_decode4<8>, dim3(nblk4), dim3(256), 0, st, dm, ws, sid, n_active);
+    hipLaunchKernelGGL(k_decode4<8>, dim3(nblk4), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
     hipLaunchKernelGGL(k_decode<8>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
   } else {
-    hipLaunchKernelGGL(k_decode4<16>, dim3(nblk4), dim3(256), 0, st, dm, ws, sid, n_active);
+    hipLaunchKernelGGL(k_decode4<16>, dim3(nblk4), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
     hipLaunchKernelGGL(k_decode<16>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
   }
   return hipGetLastError();
@@ -1195,15 +1182,11 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
 }
 
 // Combines the splits of each query row: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
+// Combines the splits' partials of output row r, dims 4 d4 .. 4 d4 + 3, of
+// kv head u: O = sum_s w_s O_s / sum_s w_s l_s with w_s = 2^(m_s - max m).
 template <int FP32>
-__global__ __launch_bounds__(256) void k_attend_merge(Dims dm, Workspace ws, AttendArgs aa, int rows) {
-  // thread = (kv head, query row, 4 output dims); every split's (m, l) and
-  // partial O are loaded together
-  const size_t gt = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (gt >= (size_t)dm.units * rows * (D / 4)) return;
-  const int d4 = (int)(gt % (D / 4));
-  const int r = (int)((gt / (D / 4)) % rows);
-  const int u = (int)(gt / ((size_t)(D / 4) * rows));
+__device__ __forceinline__ void merge_row4(const Dims& dm, const Workspace& ws, const AttendArgs& aa, int u, int r,
+                                           int d4) {
   const int grp = dm.Hq / dm.Hkv;
   const int l = u / dm.Hkv, kvh = u % dm.Hkv;
   float ms[MAX_SPLITS], ls[MAX_SPLITS];
@@ -1244,6 +1227,18 @@ __global__ __launch_bounds__(256) void k_attend_merge(Dims dm, Workspace ws, Att
     reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(aa.o) + orow)[d4] = packed;
   }
   if (d4 == 0 && aa.lse) aa.lse[((size_t)l * aa.tq + t) * dm.Hq + kvh * grp + gg] = (M + log2f(Lsum)) * LN2;
+}
+
+template <int FP32>
+__global__ __launch_bounds__(256) void k_attend_merge(Dims dm, Workspace ws, AttendArgs aa, int rows) {
+  // thread = (kv head, query row, 4 output dims); every split's (m, l) and
+  // partial O are loaded together
+  const size_t gt = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (gt >= (size_t)dm.units * rows * (D / 4)) return;
+  const int d4 = (int)(gt % (D / 4));
+  const int r = (int)((gt / (D / 4)) % rows);
+  const int u = (int)(gt / ((size_t)(D / 4) * rows));
+  merge_row4<FP32>(dm, ws, aa, u, r, d4);
 }
 
 // float32 path (small fp32 streams): one wave per (kv head, query row, split),

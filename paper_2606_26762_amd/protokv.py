@@ -30,7 +30,7 @@ EXPORTED = [
 ]
 
 KERNELS = ["ring_insert", "seed", "screen", "aggregate", "decode", "attend", "attend_merge", "pq_encode",
-           "materialize", "centres"]
+           "materialize"]
 
 
 class ProtoKVError(RuntimeError):
