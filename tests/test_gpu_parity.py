@@ -82,6 +82,27 @@ def test_ragged_shapes_seed_and_assign_same_fold():
         pair.attend(pair.query(np.random.default_rng(3), tq=tq), pseudo)
 
 
+@pytest.mark.parametrize("S", [5, 7, 16])
+def test_formed_rows_across_s(S):
+    """bf16 readout forming pseudo-token rows in LDS, S in {5, 7, 16}: T=49,
+    W=3 (147 near rows, the near/pseudo boundary inside a 64-row tile), K=40,
+    2 kv heads (several context splits, some holding one tile); readout with
+    formed rows, then with the rows written back, both against the oracle."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=7, grid_w=7,
+                                 frames=12, window_frames=3, capacity=40, query_tokens=6)
+    h.log(f"case: formed rows S={S} T=49 W=3 K=40")
+    pair = h.Pair(wl, S=S, B=max(32, S))
+    for f in range(wl.frames):
+        pair.step()
+    pseudo = pair.synthesize()
+    rng = np.random.default_rng(40 + S)
+    q = pair.query(rng)
+    w1, o1, _ = pair.attend(q, pseudo)      # formed rows
+    w2, o2, _ = pair.attend(q, pseudo)      # rows written by read_pseudo
+    h.log(f"readout err formed {w1:.2e} written {w2:.2e}, max diff {np.abs(o1 - o2).max():.2e}")
+
+
 def test_capacity_limit_gives_exact_attention():
     """K >= evicted tokens: every token keeps its own slot, and the readout is
     exact attention over the full history with far logits shifted by ln S
