@@ -247,16 +247,19 @@ __device__ void decode_top_s_small(const uint32_t* hist /* [G][CMAX] */, int C, 
   for (int sidx = 0; sidx < S; ++sidx) out[sidx] = sidx < nb ? bc[sidx] : 0u;
 }
 
-// Decoding, register path: four lanes per (slot, K/V) beam, 16 beams per
-// wave, for prototypes whose residual count is at most 65534 (every factor
-// H+1 is below 2^16, so a product of the 8 factors fits in 128 bits) and
-// S <= SM.  Lane q of a beam owns the prefixes e = q, q + 4, ...  For each
-// subspace the four lanes rank the codewords (count desc, code asc) by
-// counting, publish the top R = min(S, C) in order through LDS, and merge:
-// S pops of the best row head (product desc, packed tuple asc), the best
-// found with two shuffle steps across the four lanes; only the winning row
-// advances.  Same beam (width S) and order as decode_top_s.
-constexpr int DEC_BEAMS = 16;  // beams per wave
+// Decoding, register path: LPB lanes (2 or 4) per (slot, K/V) beam,
+// 64 / LPB beams per wave, for prototypes whose residual count is at most
+// 65534 (every factor H+1 is below 2^16, so a product of the 8 factors fits
+// in 128 bits) and S <= SM.  Lane q of a beam owns the prefixes e = q,
+// q + LPB, ...  For each subspace the lanes rank the codewords (count desc,
+// code asc) by counting, publish the top R = min(S, C) in order through LDS,
+// and merge: S pops of the best row head (product desc, packed tuple asc),
+// the best found in-lane and then with log2(LPB) DPP exchange steps across
+// the beam's lanes; only the winning row advances.  Same beam (width S) and
+// order as decode_top_s.
+//
+// With `centres` it also writes the float32 centre sum / n of the (slot,
+// K/V) (IEEE division) and the slot's bias, for the readout's row forming.
 
 // Exchanges within a quad of lanes (DPP quad_perm, no LDS round trip).
 template <int CTRL>
@@ -269,6 +272,12 @@ __device__ __forceinline__ uint64_t qperm64(uint64_t x) {
 }
 constexpr int QP_XOR1 = 0xB1;  // lanes (1, 0, 3, 2)
 constexpr int QP_XOR2 = 0x4E;  // lanes (2, 3, 0, 1)
+// value of lane SRC of this lane's quad
+template <int LPB, int SRC>
+__device__ __forceinline__ uint32_t group_bcast(uint32_t x) {
+  static_assert(LPB == 4, "quad broadcast");
+  return qperm<SRC * 0x55>(x);
+}
 
 // (pa, ca) ranks before (pb, cb), without branches
 __device__ __forceinline__ bool before128b(const U128& pa, uint32_t ca, const U128& pb, uint32_t cb) {
@@ -284,13 +293,16 @@ __device__ __forceinline__ uint32_t sel32(bool t, uint32_t a, uint32_t b) {
   return (a & m) | (b & ~m);
 }
 
-template <int SM>
+template <int SM, int LPB>
 __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid, int n_active, int centres) {
-  constexpr int E = SM / 4;  // prefixes per lane
-  __shared__ uint32_t s_rank[4][DEC_BEAMS][CMAX];
+  static_assert(LPB == 2 || LPB == 4, "lanes per beam");
+  constexpr int E = SM / LPB;        // prefixes per lane
+  constexpr int BPW = 64 / LPB;      // beams per wave
+  constexpr int KPL = CMAX / LPB;    // codewords per lane
+  __shared__ uint32_t s_rank[4][BPW][CMAX];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int q = lane & 3, bq = lane >> 2;
-  const int beam = (blockIdx.x * 4 + wave) * DEC_BEAMS + bq;  // ((unit * n_active + slot) * 2 + K/V)
+  const int q = lane & (LPB - 1), bq = lane / LPB;
+  const int beam = (blockIdx.x * 4 + wave) * BPW + bq;  // ((unit * n_active + slot) * 2 + K/V)
   const bool bvalid = beam < dm.units * n_active * 2;
   const int kv = beam & 1, up = bvalid ? beam >> 1 : 0;
   const int u = up / n_active, p = up % n_active;
@@ -303,22 +315,24 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
   const bool nores = !pq || m.n_res == 0;
   if (bvalid && q == 0 && nores) out[SMAX] = 1u;
   if (bvalid && centres) {
-    // the float32 centre sum / n of this (slot, K/V) (IEEE division) for the
-    // readout's row forming, lane q taking float4s q, q + 4, ...; and the bias
+    // lane q takes float4s q, q + LPB, ...
     const float nf = (float)m.n;
     const float4* sums = reinterpret_cast<const float4*>(row + (kv ? ROW_SUMV : ROW_SUMK));
     float4* cen = reinterpret_cast<float4*>(ws.pcen + (((size_t)u * dm.K + p) * 2 + kv) * D);
+    // every load issued before the first store (the stores may alias them
+    // as far as the compiler knows)
+    float4 v[D / 4 / LPB];
 #pragma unroll
-    for (int i = 0; i < D / 16; ++i) {
-      const float4 v = sums[q + 4 * i];
-      cen[q + 4 * i] = make_float4(v.x / nf, v.y / nf, v.z / nf, v.w / nf);
-    }
+    for (int i = 0; i < D / 4 / LPB; ++i) v[i] = sums[q + LPB * i];
+#pragma unroll
+    for (int i = 0; i < D / 4 / LPB; ++i)
+      cen[q + LPB * i] = make_float4(v[i].x / nf, v[i].y / nf, v[i].z / nf, v[i].w / nf);
     if (kv == 0 && q == 0) {
       const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
       ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
     }
   }
-  // this path decodes the beam (uniform within the four lanes)
+  // this path decodes the beam (uniform within the beam's lanes)
   const bool mine = bvalid && !nores && m.n_res <= 65534u && S <= SM;
   const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
   const int R = S < C ? S : C;
@@ -332,43 +346,98 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
     pc[j] = 0;
   }
   int nb = 1;
+  // this lane's counts of subspace g, loaded one subspace ahead
+  uint4 hnext[KPL / 4];
+#pragma unroll
+  for (int v4 = 0; v4 < KPL / 4; ++v4)
+    hnext[v4] = mine ? reinterpret_cast<const uint4*>(hist)[q * (KPL / 4) + v4] : make_uint4(0, 0, 0, 0);
   for (int g = 0; g < G; ++g) {
-    // keys of codewords 4q .. 4q+3: (count << 4 | (15 - c)) + 1, larger = better, 0 = absent
-    uint4 h4 = make_uint4(0, 0, 0, 0);
-    if (mine) h4 = reinterpret_cast<const uint4*>(hist + g * CMAX)[q];
-    const uint32_t hv[4] = {h4.x, h4.y, h4.z, h4.w};
-    uint32_t key[4];
+    uint4 hcur[KPL / 4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = 4 * q + i;
-      key[i] = c < C ? ((hv[i] << 4) | (uint32_t)(15 - c)) + 1u : 0u;
+    for (int v4 = 0; v4 < KPL / 4; ++v4) {
+      hcur[v4] = hnext[v4];
+      hnext[v4] = mine && g + 1 < G ? reinterpret_cast<const uint4*>(hist + (g + 1) * CMAX)[q * (KPL / 4) + v4]
+                                    : make_uint4(0, 0, 0, 0);
     }
-    int rk[4] = {0, 0, 0, 0};
+    // keys of codewords KPL q .. KPL q + KPL - 1: (count << 4 | (15 - c)) + 1,
+    // larger = better, 0 = absent
+    uint32_t key[KPL];
 #pragma unroll
-    for (int i2 = 0; i2 < 4; ++i2) {
-      const uint32_t others[4] = {qperm<0x00>(key[i2]), qperm<0x55>(key[i2]), qperm<0xAA>(key[i2]),
-                                  qperm<0xFF>(key[i2])};
+    for (int v4 = 0; v4 < KPL / 4; ++v4) {
+      const uint4 h4 = hcur[v4];
+      const uint32_t hv[4] = {h4.x, h4.y, h4.z, h4.w};
 #pragma unroll
-      for (int src = 0; src < 4; ++src)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) rk[i] += others[src] > key[i] ? 1 : 0;
+      for (int i = 0; i < 4; ++i) {
+        const int c = KPL * q + 4 * v4 + i;
+        key[4 * v4 + i] = c < C ? ((hv[i] << 4) | (uint32_t)(15 - c)) + 1u : 0u;
+      }
     }
+    // ranks of the 16 keys (unique: the code is in the low bits)
+    if constexpr (LPB == 2) {
+      // each lane sorts its 8 keys descending (bitonic network), then one
+      // bitonic half-cleaner across the pair (lane 0 keeps the larger of
+      // key[k] and the partner's key[7 - k], lane 1 the smaller) and a
+      // bitonic merge of 8 leave lane 0 with ranks 0..7 and lane 1 with
+      // ranks 8..15, both in order
+      auto cx = [&](int a, int b, bool desc) {
+        const uint32_t x = key[a], y = key[b];
+        const uint32_t hi = x > y ? x : y, lo = x > y ? y : x;
+        key[a] = desc ? hi : lo;
+        key[b] = desc ? lo : hi;
+      };
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (key[i] != 0u && rk[i] < R) s_rank[wave][bq][rk[i]] = key[i];
+      for (int k = 2; k <= KPL; k <<= 1)
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+          for (int i = 0; i < KPL; ++i)
+            if ((i ^ j) > i) cx(i, i ^ j, (i & k) == 0);
+      uint32_t t[KPL];
+#pragma unroll
+      for (int k = 0; k < KPL; ++k) t[k] = qperm<QP_XOR1>(key[KPL - 1 - k]);
+#pragma unroll
+      for (int k = 0; k < KPL; ++k) {
+        const uint32_t hi = key[k] > t[k] ? key[k] : t[k], lo = key[k] > t[k] ? t[k] : key[k];
+        key[k] = q == 0 ? hi : lo;
+      }
+#pragma unroll
+      for (int j = KPL >> 1; j > 0; j >>= 1)
+#pragma unroll
+        for (int i = 0; i < KPL; ++i)
+          if ((i ^ j) > i) cx(i, i ^ j, true);
+#pragma unroll
+      for (int i = 0; i < KPL; ++i)
+        if (key[i] != 0u && q * KPL + i < R) s_rank[wave][bq][q * KPL + i] = key[i];
+    } else {
+      int rk[KPL];
+#pragma unroll
+      for (int i = 0; i < KPL; ++i) rk[i] = 0;
+#pragma unroll
+      for (int i2 = 0; i2 < KPL; ++i2) {
+        const uint32_t others[4] = {group_bcast<LPB, 0>(key[i2]), group_bcast<LPB, 1>(key[i2]),
+                                    group_bcast<LPB, 2>(key[i2]), group_bcast<LPB, 3>(key[i2])};
+#pragma unroll
+        for (int src = 0; src < LPB; ++src)
+#pragma unroll
+          for (int i = 0; i < KPL; ++i) rk[i] += others[src] > key[i] ? 1 : 0;
+      }
+#pragma unroll
+      for (int i = 0; i < KPL; ++i)
+        if (key[i] != 0u && rk[i] < R) s_rank[wave][bq][rk[i]] = key[i];
+    }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     const uint32_t k0 = s_rank[wave][bq][0];
     const int shift = 4 * (G - 1 - g);
-    // row heads: prefix e = q + 4j times rank ptr[j]
+    // row heads: prefix e = q + LPB j times rank ptr[j]
     int ptr[E];
     U128 hp[E];
     uint32_t hc[E];
 #pragma unroll
     for (int j = 0; j < E; ++j) {
       ptr[j] = 0;
-      const bool ok = q + 4 * j < nb;
+      const bool ok = q + LPB * j < nb;
       hp[j] = ok ? mul_u128_u32(pp[j], ((k0 - 1u) >> 4) + 1u) : U128{0, 0};
       hc[j] = ok ? (pc[j] | ((15u - ((k0 - 1u) & 15u)) << shift)) : 0xFFFFFFFFu;
     }
@@ -393,9 +462,9 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
           bj = t ? j : bj;
         }
         uint32_t who = (uint32_t)(q * E + bj);
-        // best of the four lanes
+        // best of the beam's lanes
 #pragma unroll
-        for (int x = 0; x < 2; ++x) {
+        for (int x = 0; x < (LPB == 4 ? 2 : 1); ++x) {
           U128 ov;
           uint32_t oc, ow;
           if (x == 0) {
@@ -412,10 +481,10 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
           who = sel32(t, ow, who);
         }
         {
-          const bool rec = (o & 3) == q;
-          np[o >> 2].lo = sel64(rec, bv.lo, np[o >> 2].lo);
-          np[o >> 2].hi = sel64(rec, bv.hi, np[o >> 2].hi);
-          nc[o >> 2] = sel32(rec, bc, nc[o >> 2]);
+          const bool rec = (o % LPB) == q;
+          np[o / LPB].lo = sel64(rec, bv.lo, np[o / LPB].lo);
+          np[o / LPB].hi = sel64(rec, bv.hi, np[o / LPB].hi);
+          nc[o / LPB] = sel32(rec, bc, nc[o / LPB]);
         }
         // the winning row moves to its next rank: one product, then selects
         const bool iwin = (int)(who / E) == q;
@@ -458,7 +527,7 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
   if (mine) {
 #pragma unroll
     for (int j = 0; j < E; ++j) {
-      const int o = q + 4 * j;
+      const int o = q + LPB * j;
       if (o < S) out[o] = o < nb ? pc[j] : 0u;
     }
     if (q == 0) out[SMAX] = 0u;
@@ -639,12 +708,13 @@ hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_act
   const int bpu = (n_active + SYN_P - 1) / SYN_P;
   const size_t lds = (size_t)2 * dm.S * 64 * (3 * sizeof(uint64_t) + sizeof(uint32_t));
   const int nbeams = dm.units * n_active * 2;
-  const int nblk4 = (nbeams + 4 * DEC_BEAMS - 1) / (4 * DEC_BEAMS);
+  constexpr int LPB = 2;  // lanes per beam
+  const int nblk = (nbeams + 4 * (64 / LPB) - 1) / (4 * (64 / LPB));
   if (dm.S <= 8) {
-    hipLaunchKernelGGL(k_decode4<8>, dim3(nblk4), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
+    hipLaunchKernelGGL((k_decode4<8, LPB>), dim3(nblk), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
     hipLaunchKernelGGL(k_decode<8>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
   } else {
-    hipLaunchKernelGGL(k_decode4<16>, dim3(nblk4), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
+    hipLaunchKernelGGL((k_decode4<16, LPB>), dim3(nblk), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
     hipLaunchKernelGGL(k_decode<16>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
   }
   return hipGetLastError();
