@@ -142,8 +142,11 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
                          hipStream_t st);
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                             hipStream_t st);
-// centres: also write the float32 centres (pcen) and biases for the readout's row forming
-hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, bool centres, hipStream_t st);
+// centres: also write the float32 centres (pcen) and biases for the readout's
+// row forming; wide: some slot may hold more than 65534 residuals (the
+// 192-bit path runs too)
+hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, bool centres, bool wide,
+                         hipStream_t st);
 hipError_t launch_materialize(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st);
 hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& aa,
                          hipStream_t st);

@@ -420,8 +420,10 @@ protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
   // the readout forms the rows from them as it loads them; otherwise the rows
   // are written here
   const bool rows = h->dm.kv_fp32 != 0 || h->dm.S < PS_MIN_S;
+  // a slot's residual count is at most the tokens its stream has evicted
+  const bool wide = h->st[sid].evicted > 65534u;
   protokv_status s = h->dev(
-      h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] { return launch_decode(h->dm, h->ws, sid, na, !rows, hs); }),
+      h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] { return launch_decode(h->dm, h->ws, sid, na, !rows, wide, hs); }),
       "synthesize/decode");
   if (s == PROTOKV_OK && rows)
     s = h->dev(h->launch(PROTOKV_K_MATERIALIZE, hs, [&] { return launch_materialize(h->dm, h->ws, sid, na, hs); }),

@@ -703,7 +703,8 @@ __global__ __launch_bounds__(256) void k_materialize16(Dims dm, Workspace ws, in
   }
 }
 
-hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, bool centres, hipStream_t st) {
+hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, bool centres, bool wide,
+                         hipStream_t st) {
   if (n_active <= 0) return hipSuccess;
   const int bpu = (n_active + SYN_P - 1) / SYN_P;
   const size_t lds = (size_t)2 * dm.S * 64 * (3 * sizeof(uint64_t) + sizeof(uint32_t));
@@ -712,10 +713,10 @@ hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_act
   const int nblk = (nbeams + 4 * (64 / LPB) - 1) / (4 * (64 / LPB));
   if (dm.S <= 8) {
     hipLaunchKernelGGL((k_decode4<8, LPB>), dim3(nblk), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
-    hipLaunchKernelGGL(k_decode<8>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
+    if (wide) hipLaunchKernelGGL(k_decode<8>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
   } else {
     hipLaunchKernelGGL((k_decode4<16, LPB>), dim3(nblk), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
-    hipLaunchKernelGGL(k_decode<16>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
+    if (wide) hipLaunchKernelGGL(k_decode<16>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
   }
   return hipGetLastError();
 }
