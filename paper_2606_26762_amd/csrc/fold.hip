@@ -329,10 +329,16 @@ __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
 
 // Codes of subspaces g0 = 2p, g1 = 2p + 1 for this lane's token from its
 // residual halves r[0] (g0) and r[1] (g1) and A-operand codebook row w;
-// returns the code of subspace g0 (half 0) or g1 (half 1).
+// returns the code of subspace g0 (half 0) or g1 (half 1).  r is formed
+// with the centre c' = sum * (1 / n) (a correctly rounded reciprocal, then
+// a multiply: |c' - c| <= 3.01 u |c| against c = float32(sum / n)); the
+// bound carries that difference through cn (the norm of c' over the
+// subspace, from both halves), and the exact fallback forms its residual
+// from x, the sums s and n with the IEEE division.
 __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const float* hnp, const float* cmx,
-                                       const float (&r)[2][8], const float (&w)[8], int p, bool valid,
-                                       int lane) {
+                                       const float (&r)[2][8], const float (&w)[8], const float (&x)[2][8],
+                                       const float (&sv)[2][8], float nf, float cn2h0, float cn2h1, int p,
+                                       bool valid, int lane) {
   const int col = lane & 31, half = lane >> 5;
   const int g0 = 2 * p, g1 = 2 * p + 1;
   const bf16x8 zero8 = {};
@@ -402,9 +408,13 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
   // distances of the codewords differ from the exact ones by <= 19 u D,
   // D <= |r|^2 - 2 score of the runner-up (dlead).  Each term is taken with
   // margin.
+  float cn2 = half ? cn2h1 : cn2h0;
+  cn2 += __shfl_xor(half ? cn2h0 : cn2h1, 32, 64);
   const float rn = sqrtf(rn2) * 1.0001f, cm = cmx[g];
   const float dlead = fmaxf(rn * rn - 2.0f * v2, 0.f) + 1e-30f;
-  const float F = fmaf(5.2e-5f * rn, cm, fmaf(2.5e-6f, cm * cm, 1.2e-6f * dlead));
+  // ... and <= 3.1 u |c| |C| from the centre c' (taken as 2e-7 |c'| |C|)
+  const float F = fmaf(fmaf(5.2e-5f, rn, 2e-7f * sqrtf(cn2) * 1.0001f), cm,
+                       fmaf(2.5e-6f, cm * cm, 1.2e-6f * dlead));
   int z = half ? bid[1] : bid[0];
   // not separated: the float32 sequential distances decide, one flagged
   // (token, subspace) at a time for the whole wave (lane % 16 = codeword)
@@ -416,11 +426,14 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
     const int tc = src & 31;
     const int cw = lane & 15;
     const float* wc = cbk + gs * CBW + cw * DP;
+    // the exact residual x - float32(s / n) of subspace gs, this lane's half
+    float rex[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) rex[i] = (gs == g0) ? x[0][i] - sv[0][i] / nf : x[1][i] - sv[1][i] / nf;
     float a = 0.f;
 #pragma unroll
     for (int q = 0; q < DP; ++q) {
-      const float mine = (gs == g0) ? r[0][q & 7] : r[1][q & 7];
-      const float d = __shfl(mine, q < 8 ? tc : tc + 32, 64) - wc[q];
+      const float d = __shfl(rex[q & 7], q < 8 ? tc : tc + 32, 64) - wc[q];
       a = a + d * d;
     }
     if (cw >= dm.C) a = INFINITY;
@@ -841,10 +854,11 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
         wr[p][1] = *reinterpret_cast<const float4*>(wa + 4);
       }
       const float nf = (float)*reinterpret_cast<const uint32_t*>(srow + ROW_META);
+      const float inv = 1.0f / nf;
       uint32_t* hist = reinterpret_cast<uint32_t*>(ws.bank + (unit * dm.K + slot) * ROW + (kv ? ROW_HV : ROW_HK));
 #pragma unroll
       for (int p = 0; p < G / 2; ++p) {
-        float r[2][8], w[8];
+        float r[2][8], w[8], xs[2][8], ss[2][8], cn2[2];
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
           const int g = 2 * p + q;
@@ -865,12 +879,21 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
           }
           const float sv[8] = {sr[g][0].x, sr[g][0].y, sr[g][0].z, sr[g][0].w,
                                sr[g][1].x, sr[g][1].y, sr[g][1].z, sr[g][1].w};
+          float c2 = 0.f;
 #pragma unroll
-          for (int i = 0; i < 8; ++i) r[q][i] = qv ? x[i] - sv[i] / nf : 0.f;
+          for (int i = 0; i < 8; ++i) {
+            const float c = sv[i] * inv;
+            c2 = fmaf(c, c, c2);
+            r[q][i] = qv ? x[i] - c : 0.f;
+            xs[q][i] = x[i];
+            ss[q][i] = sv[i];
+          }
+          cn2[q] = qv ? c2 : 0.f;
         }
         w[0] = wr[p][0].x; w[1] = wr[p][0].y; w[2] = wr[p][0].z; w[3] = wr[p][0].w;
         w[4] = wr[p][1].x; w[5] = wr[p][1].y; w[6] = wr[p][1].z; w[7] = wr[p][1].w;
-        const int z = pq_pair(dm, cbk, ws.cbhn + ub * G * CMAX, ws.cbmax + ub * G, r, w, p, qv, lane);
+        const int z = pq_pair(dm, cbk, ws.cbhn + ub * G * CMAX, ws.cbmax + ub * G, r, w, xs, ss, nf, cn2[0], cn2[1],
+                              p, qv, lane);
         if (qv) atomicAdd(hist + (2 * p + half) * CMAX + z, 1u);
       }
     }

@@ -133,6 +133,22 @@ struct AttendArgs {
   float* lse;
 };
 
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane
+// (global_load_lds_dwordx4; M0 holds the wave-uniform LDS byte address).
+// Issued as inline asm so the compiler does not treat later LDS reads of
+// other buffers as dependent on it: completion is awaited explicitly with
+// wait_vm before the barrier that publishes a tile.
+__device__ __forceinline__ void lds_dma16(const void* g, void* lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0) : "memory", "m0");
+}
+// s_waitcnt vmcnt(n) (expcnt / lgkmcnt not waited for)
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // Launchers (fold.hip, query.hip).  Return hipSuccess or the launch error.
 hipError_t launch_ring_insert(const Dims& dm, const Workspace& ws, const AppendBatch& ab,
                               const void* k, const void* v, hipStream_t st);

@@ -796,22 +796,6 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
   asm volatile("s_barrier" ::: "memory");
 }
-// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane
-// (global_load_lds_dwordx4; M0 holds the wave-uniform LDS byte address).
-// Issued as inline asm so the compiler does not treat later LDS reads of
-// other buffers as dependent on it: completion is awaited explicitly with
-// wait_vm before the barrier that publishes a tile.
-__device__ __forceinline__ void lds_dma16(const void* g, void* lds) {
-  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0) : "memory", "m0");
-}
-// s_waitcnt vmcnt(n) (expcnt / lgkmcnt not waited for)
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 constexpr int AT_NBUF = 4;        // tile buffers: tile t computes while t+1..t+3 load
 constexpr int AT_NTAB = 5;        // row-table entries (written 3 tiles ahead)
 constexpr int AT_PB_MAX = 4096;   // pseudo-token biases staged in LDS up to this capacity
