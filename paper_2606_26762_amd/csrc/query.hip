@@ -158,95 +158,6 @@ __device__ __forceinline__ U128 mul_u128_u32(const U128& a, uint32_t f) {
   return r;
 }
 
-// (pa, ca) ranks before (pb, cb): larger product, then smaller packed code.
-__device__ __forceinline__ bool before128(const U128& pa, uint32_t ca, const U128& pb, uint32_t cb) {
-  return pa.hi != pb.hi ? pa.hi > pb.hi : (pa.lo != pb.lo ? pa.lo > pb.lo : ca < cb);
-}
-
-template <int SM>
-__device__ void decode_top_s_small(const uint32_t* hist /* [G][CMAX] */, int C, int S, uint32_t* out) {
-  U128 bp[SM];
-  uint32_t bc[SM];
-#pragma unroll
-  for (int i = 0; i < SM; ++i) { bp[i].lo = 0; bp[i].hi = 0; bc[i] = 0; }
-  bp[0].lo = 1;
-  int nb = 1;
-  const int R = S < C ? S : C;
-  for (int g = 0; g < G; ++g) {
-    // ranks of subspace g: key = (count << 4 | (15 - code)) + 1, larger = better
-    uint32_t key[CMAX];
-    const uint4* h4 = reinterpret_cast<const uint4*>(hist + g * CMAX);
-#pragma unroll
-    for (int q = 0; q < CMAX / 4; ++q) {
-      const uint4 v = h4[q];
-      const uint32_t hv[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c = q * 4 + i;
-        key[c] = c < C ? ((hv[i] << 4) | (uint32_t)(15 - c)) + 1u : 0u;
-      }
-    }
-    uint32_t rf[SM], rc[SM];
-#pragma unroll
-    for (int r = 0; r < SM; ++r) {
-      uint32_t m = 0;
-#pragma unroll
-      for (int c = 0; c < CMAX; ++c) m = key[c] > m ? key[c] : m;
-#pragma unroll
-      for (int c = 0; c < CMAX; ++c) key[c] = key[c] == m ? 0u : key[c];
-      rf[r] = ((m - 1u) >> 4) + 1u;          // count + 1
-      rc[r] = 15u - ((m - 1u) & 15u);        // code
-    }
-    // merge the nb prefixes with the R ranks: S pops over the row heads
-    const int shift = 4 * (G - 1 - g);
-    int ptr[SM];
-    U128 hp[SM];
-#pragma unroll
-    for (int i = 0; i < SM; ++i) {
-      ptr[i] = 0;
-      hp[i] = mul_u128_u32(bp[i], rf[0]);
-    }
-    U128 np[SM];
-    uint32_t nc[SM];
-    const int total = nb * R;
-    const int nout = S < total ? S : total;
-#pragma unroll
-    for (int o = 0; o < SM; ++o) {
-      if (o < nout) {
-        int bi = -1;
-        U128 best = {0, 0};
-        uint32_t bcode = 0;
-#pragma unroll
-        for (int i = 0; i < SM; ++i) {
-          if (i < nb && ptr[i] < R) {
-            uint32_t rci = rc[0];
-#pragma unroll
-            for (int r = 1; r < SM; ++r) rci = ptr[i] == r ? rc[r] : rci;
-            const uint32_t code = bc[i] | (rci << shift);
-            if (bi < 0 || before128(hp[i], code, best, bcode)) { bi = i; best = hp[i]; bcode = code; }
-          }
-        }
-        np[o] = best;
-        nc[o] = bcode;
-#pragma unroll
-        for (int i = 0; i < SM; ++i) {
-          if (i == bi) {
-            ptr[i] += 1;
-            uint32_t f = rf[0];
-#pragma unroll
-            for (int r = 1; r < SM; ++r) f = ptr[i] == r ? rf[r] : f;
-            hp[i] = mul_u128_u32(bp[i], f);
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < SM; ++i) { bp[i] = np[i]; bc[i] = nc[i]; }
-    nb = nout;
-  }
-  for (int sidx = 0; sidx < S; ++sidx) out[sidx] = sidx < nb ? bc[sidx] : 0u;
-}
-
 // Decoding, register path: LPB lanes (2 or 4) per (slot, K/V) beam,
 // 64 / LPB beams per wave, for prototypes whose residual count is at most
 // 65534 (every factor H+1 is below 2^16, so a product of the 8 factors fits
