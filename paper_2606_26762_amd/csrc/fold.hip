@@ -923,6 +923,7 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
 // back and refreshes the slot's screening copy.
 // ---------------------------------------------------------------------------
 constexpr int AGG_SLOTS = 32;  // slots per workgroup: two per 16-lane group (k0 + g, k0 + g + 16)
+constexpr int AGG_TOK_BYTES = 32768;  // LDS for the workgroup's tokens (64 bf16 or 32 float32 tokens)
 constexpr int TOK_BATCH = 2;
 constexpr uint16_t NO_SLOT = 0xFFFF;
 
@@ -962,6 +963,8 @@ __global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, Fol
   __shared__ uint16_t s_tok[TMAX];         // tokens of this workgroup's slots, grouped, eviction order
   __shared__ int s_cnt[AGG_SLOTS];
   __shared__ int s_off[AGG_SLOTS + 1];       // local slot q = group + 16 * pass
+  // the workgroup's tokens in list order, [position][K, V][D] KV dtype, when they fit
+  __shared__ __attribute__((aligned(16))) uint8_t s_tk[AGG_TOK_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // same XCD placement as the screen (consecutive logical blocks share an
@@ -1035,6 +1038,42 @@ __global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, Fol
 
   const int gi = tid >> 4, il = tid & 15;
   const float eta = dm.eta, keep = 1.0f - dm.eta;
+  constexpr int ES = FP32 ? 4 : 2;
+  constexpr int TOKB = 2 * D * ES;             // bytes of one token's K and V
+  constexpr int TPI = 1024 / TOKB;             // tokens per 1 KiB DMA instruction
+  constexpr int CAP = AGG_TOK_BYTES / TOKB;
+  // All of the workgroup's tokens go into LDS in one round of DMA loads
+  // (instruction i moves list positions TPI i ..: lane = (position, K/V,
+  // 16-byte part)), beside the first slot's row loads; a workgroup with more
+  // tokens than fit reads them from global memory TOK_BATCH at a time.
+  const int ntok = s_off[AGG_SLOTS];
+  const bool staged = ntok <= CAP;  // uniform
+  if (staged) {
+    const int ninstr = (ntok + TPI - 1) / TPI;
+    for (int i = wave; i < ninstr; i += 4) {
+      const int pos = min(TPI * i + (FP32 ? 0 : (lane >> 5)), ntok - 1);
+      const int kvs = FP32 ? (lane >> 5) : ((lane >> 4) & 1);
+      const int part = FP32 ? (lane & 31) : (lane & 15);
+      const uint8_t* src = (kvs ? ws.ring_v : ws.ring_k) + (fbase + (size_t)s_tok[pos] * D) * ES + part * 16;
+      lds_dma16(src, s_tk + i * 1024);
+    }
+  }
+  // the first slot's row (loads in flight with the tokens')
+  float sk[8], sv[8], qk[8], qv[8];
+  RowMeta m;
+  auto load_row = [&](int q) {
+    const uint8_t* row = ws.bank + (unit * dm.K + k0 + q) * ROW;
+    ld8f(row + ROW_SUMK + il * 32, sk);
+    ld8f(row + ROW_SUMV + il * 32, sv);
+    ld8f(row + ROW_SQK + il * 32, qk);
+    ld8f(row + ROW_SQV + il * 32, qv);
+    m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  };
+  if (s_off[gi + 1] > s_off[gi]) load_row(gi);
+  if (staged) {
+    wait_vm<0>();  // this wave's token loads (and its row loads) have landed
+    __syncthreads();
+  }
   for (int pass = 0; pass < 2; ++pass) {  // uniform per lane group; no barrier below
     const int q = gi + 16 * pass;
     const int t0 = s_off[q], t1 = s_off[q + 1];
@@ -1042,21 +1081,27 @@ __global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, Fol
     const int k = k0 + q;
     const size_t si = unit * dm.K + k;
     uint8_t* row = ws.bank + si * ROW;
-    float sk[8], sv[8], qk[8], qv[8];
-    ld8f(row + ROW_SUMK + il * 32, sk);
-    ld8f(row + ROW_SUMV + il * 32, sv);
-    ld8f(row + ROW_SQK + il * 32, qk);
-    ld8f(row + ROW_SQV + il * 32, qv);
-    RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+    if (pass == 1) load_row(q);
     for (int tb = t0; tb < t1; tb += TOK_BATCH) {  // uniform per lane group
       // a batch's loads all in flight together (indices clamped into the list)
       int jb[TOK_BATCH];
       Raw8<FP32> kb[TOK_BATCH], vb[TOK_BATCH];
 #pragma unroll
       for (int e = 0; e < TOK_BATCH; ++e) {
-        jb[e] = s_tok[min(tb + e, t1 - 1)];
-        load8<FP32>(ws.ring_k, fbase + (size_t)jb[e] * D + 8 * il, kb[e]);
-        load8<FP32>(ws.ring_v, fbase + (size_t)jb[e] * D + 8 * il, vb[e]);
+        const int pos = min(tb + e, t1 - 1);
+        jb[e] = s_tok[pos];
+        if (staged) {
+          const uint4* pk = reinterpret_cast<const uint4*>(s_tk + pos * TOKB + il * 8 * ES);
+          const uint4* pv = reinterpret_cast<const uint4*>(s_tk + pos * TOKB + D * ES + il * 8 * ES);
+#pragma unroll
+          for (int w = 0; w < (FP32 ? 2 : 1); ++w) {
+            kb[e].w[w] = pk[w];
+            vb[e].w[w] = pv[w];
+          }
+        } else {
+          load8<FP32>(ws.ring_k, fbase + (size_t)jb[e] * D + 8 * il, kb[e]);
+          load8<FP32>(ws.ring_v, fbase + (size_t)jb[e] * D + 8 * il, vb[e]);
+        }
       }
 #pragma unroll
       for (int e = 0; e < TOK_BATCH; ++e) {
