@@ -339,8 +339,23 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const uint32_t k0 = s_rank[wave][bq][0];
     const int shift = 4 * (G - 1 - g);
+    if (g == 0) {
+      // one prefix (the empty tuple): the beam is the ranks themselves
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        const int e = q + LPB * j;
+        const uint32_t ke = s_rank[wave][bq][e < R ? e : 0];
+        pp[j] = e < R ? U128{((ke - 1u) >> 4) + 1u, 0ull} : U128{0ull, 0ull};
+        pc[j] = e < R ? (15u - ((ke - 1u) & 15u)) << shift : 0u;
+      }
+      nb = S < R ? S : R;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      continue;
+    }
+    const uint32_t k0 = s_rank[wave][bq][0];
     // row heads: prefix e = q + LPB j times rank ptr[j]
     int ptr[E];
     U128 hp[E];
