@@ -47,7 +47,22 @@ in DESIGN.md):
   prod_g (H[g][z_g] + 1) (the denominator is common to all tuples); ties
   between equal scores go to the lexicographically smaller code tuple;
 * pseudo-tokens are rounded to the KV dtype from the float32 sum c + r;
-  centres are float32(sumK / n).
+  centres are float32(sumK / n);
+* maintenance (Alg. "Prototype Maintenance", when enabled) runs once per
+  fold, after the evicted frame is absorbed, at the current frame t, over
+  the active prefix of A slots (the slots seeded so far).  Aging: an idle
+  slot (the idle rule above) gets n' = floor((1 - gamma) n) in float64, and
+  its sums and squared sums are scaled by float32(n') / float32(n), so its
+  centre stays (histograms, n_res, mu, Sigma and tau stay).  Merging: pairs
+  (i, j), i < j, in ascending order; i absorbs j when
+  ||c_i - c_j||^2 < eps_K^2 and ||p_i - p_j||^2 < eps_V^2, each a float64
+  sum over d ascending of (c_i[d] - c_j[d])^2 with c = float32(sum / n),
+  using i's centre as updated by its earlier merges; sums, squared sums,
+  histograms, n and n_res add, mu becomes the mass-weighted mean, Sigma and
+  tau of i stay, j becomes empty.  Recycling: the empty slots of the prefix,
+  in ascending order, are seeded like evicted tokens from the near window's
+  tokens taken newest frame first, raster order within a frame (wrapping
+  around when there are more empty slots than near tokens).
 
 Precision: the bank is float32 (fp32 prototype statistics) and is updated
 with the explicit float32 operation sequences written below (one IEEE
@@ -108,6 +123,13 @@ class Params:
     kv_dtype: str = "bf16"
     use_pq: bool = True
     mass_bias: bool = True
+    # Alg. "Prototype Maintenance" (off unless asked for); gamma and the
+    # thresholds are float64, so (1 - 0.05) n lands on the integers the paper
+    # means (a float32 gamma = 0.0500000007 would floor 0.95 * 40 to 37)
+    maintenance: bool = False
+    gamma: float = TABLE5_DEFAULTS["gamma"]
+    eps_k: float = TABLE5_DEFAULTS["eps_K"]
+    eps_v: float = TABLE5_DEFAULTS["eps_V"]
 
     @property
     def tokens_per_frame(self) -> int:
@@ -341,6 +363,105 @@ def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
 
 
 # ---------------------------------------------------------------------------
+# Alg. "Prototype Maintenance": aging, merging, recycling
+# ---------------------------------------------------------------------------
+
+
+def _seed_slot(bank: Bank, k: int, kk: np.ndarray, vv: np.ndarray, coord: np.ndarray, pos: int) -> None:
+    """(Re)initialise slot k from one token: c <- K, p <- V, n <- 1, mu <- s,
+    Sigma <- I, tau <- its position, R <- 0."""
+    kk, vv = kk.astype(F32), vv.astype(F32)
+    bank.n[k] = 1
+    bank.sum_k[k] = kk
+    bank.sum_v[k] = vv
+    bank.sq_k[k] = (kk * kk).astype(F32)
+    bank.sq_v[k] = (vv * vv).astype(F32)
+    bank.hist_k[k] = 0
+    bank.hist_v[k] = 0
+    bank.n_res[k] = 0
+    bank.mu[k] = coord
+    bank.sigma[k] = np.array([1.0, 0.0, 1.0], dtype=F32)
+    bank.tau[k] = pos
+
+
+def _dist2(a: np.ndarray, b: np.ndarray) -> float:
+    """float64 sum over d ascending of (a[d] - b[d])^2 (a, b float32)."""
+    acc = 0.0
+    for x, y in zip(a.tolist(), b.tolist()):
+        t = x - y
+        acc = acc + t * t
+    return acc
+
+
+def maintain(bank: Bank, near: Sequence[Tuple[int, np.ndarray, np.ndarray]], t_frame: int,
+             p: Params) -> Dict[str, int]:
+    """One maintenance pass over `bank` (modified in place) at frame t_frame.
+
+    near: the near window's frames (frame index, K [T][D], V [T][D]), oldest
+    first.  Returns counts of aged, merged and recycled slots.
+    """
+    T = p.tokens_per_frame
+    A = int((bank.n > 0).sum())
+    assert np.all(bank.n[:A] > 0), "active slots form a prefix"
+    stats = {"aged": 0, "merged": 0, "recycled": 0}
+
+    # aging: mass decay of idle prototypes, sums scaled with it
+    for k in range(A):
+        if (t_frame - int(bank.tau[k]) // T) > p.t_idle:
+            n_old = int(bank.n[k])
+            n_new = int(math.floor((1.0 - p.gamma) * float(n_old)))
+            r = F32(F32(n_new) / F32(n_old))
+            bank.sum_k[k] = (bank.sum_k[k] * r).astype(F32)
+            bank.sum_v[k] = (bank.sum_v[k] * r).astype(F32)
+            bank.sq_k[k] = (bank.sq_k[k] * r).astype(F32)
+            bank.sq_v[k] = (bank.sq_v[k] * r).astype(F32)
+            bank.n[k] = n_new
+            stats["aged"] += 1
+
+    # merging: i absorbs every later j whose key and value centres are close
+    ek2 = float(p.eps_k) * float(p.eps_k)
+    ev2 = float(p.eps_v) * float(p.eps_v)
+    for i in range(A):
+        if bank.n[i] == 0:
+            continue
+        for j in range(i + 1, A):
+            if bank.n[j] == 0:
+                continue
+            ni, nj = F32(bank.n[i]), F32(bank.n[j])
+            ci, cj = (bank.sum_k[i] / ni).astype(F32), (bank.sum_k[j] / nj).astype(F32)
+            if not _dist2(ci, cj) < ek2:
+                continue
+            pi, pj = (bank.sum_v[i] / ni).astype(F32), (bank.sum_v[j] / nj).astype(F32)
+            if not _dist2(pi, pj) < ev2:
+                continue
+            wsum = F32(ni + nj)
+            for a in range(2):
+                bank.mu[i, a] = F32(F32(F32(ni * bank.mu[i, a]) + F32(nj * bank.mu[j, a])) / wsum)
+            bank.sum_k[i] = (bank.sum_k[i] + bank.sum_k[j]).astype(F32)
+            bank.sum_v[i] = (bank.sum_v[i] + bank.sum_v[j]).astype(F32)
+            bank.sq_k[i] = (bank.sq_k[i] + bank.sq_k[j]).astype(F32)
+            bank.sq_v[i] = (bank.sq_v[i] + bank.sq_v[j]).astype(F32)
+            bank.hist_k[i] += bank.hist_k[j]
+            bank.hist_v[i] += bank.hist_v[j]
+            bank.n[i] += bank.n[j]
+            bank.n_res[i] += bank.n_res[j]
+            bank.n[j] = 0
+            stats["merged"] += 1
+
+    # recycling: empty slots of the prefix take the most recent near tokens
+    coords = spatial_coords(p.grid_h, p.grid_w)
+    tokens = [(f, kf, vf, j) for (f, kf, vf) in reversed(list(near)) for j in range(T)]
+    e = 0
+    for k in range(A):
+        if bank.n[k] == 0:
+            f, kf, vf, j = tokens[e % len(tokens)]
+            _seed_slot(bank, k, kf[j], vf[j], coords[j], f * T + j)
+            e += 1
+    stats["recycled"] = e
+    return stats
+
+
+# ---------------------------------------------------------------------------
 # Eq. pq and Alg. "DecodeTopSResidualModes"
 # ---------------------------------------------------------------------------
 
@@ -470,6 +591,8 @@ class OracleStream:
                 fe, ke, ve = self.rings[u].popleft()
                 results.append(fold_frame(self.banks[u], ke, ve, fe, t, self.p,
                                           self.codebooks[u]))
+                if self.p.maintenance:
+                    maintain(self.banks[u], self.rings[u], t, self.p)
             self.evicted += self.p.tokens_per_frame
         self.frame += 1
         return results

@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 from oracle import protokv_oracle as O
+from tests import test_oracle_maintenance as M
 from tests import test_oracle_pins as P
 
 MUTATIONS = [
@@ -61,6 +62,26 @@ MUTATIONS = [
      [P.test_log_mass_bias_equals_duplicated_tokens]),
     ("attend", "/ math.sqrt(Q.shape[1])", "/ Q.shape[1]",
      [P.test_attend_matches_torch_sdpa_with_additive_mask]),
+    ("maintain", "bank.sum_k[k] = (bank.sum_k[k] * r)", "bank.sum_k[k] = (bank.sum_k[k] * F32(1))",
+     [M.test_aging_floors_the_mass_and_keeps_the_centre]),
+    ("maintain", "(1.0 - p.gamma)", "(1.0 + p.gamma)", [M.test_aging_floors_the_mass_and_keeps_the_centre]),
+    ("maintain", "> p.t_idle", ">= p.t_idle", [M.test_aging_floors_the_mass_and_keeps_the_centre]),
+    ("maintain", "ci, cj = (bank.sum_k[i] / ni)", "ci, cj = (bank.sum_k[i] / F32(1))",
+     [lambda: M.test_merge_uses_the_centre_updated_by_earlier_merges(0.3, 1)]),
+    ("maintain", "if not _dist2(ci, cj) < ek2", "if not _dist2(ci, cj) <= ek2",
+     [M.test_merge_thresholds_are_strict_and_need_both_centres]),
+    ("maintain", "if not _dist2(pi, pj) < ev2", "if False",
+     [M.test_merge_thresholds_are_strict_and_need_both_centres]),
+    ("maintain", "F32(ni * bank.mu[i, a])", "F32(nj * bank.mu[i, a])",
+     [M.test_merge_adds_statistics_and_weights_the_spatial_mean]),
+    ("maintain", "bank.sq_v[i] = (bank.sq_v[i] + bank.sq_v[j])", "bank.sq_v[i] = (bank.sq_v[i] + bank.sum_v[j])",
+     [M.test_merge_adds_statistics_and_weights_the_spatial_mean]),
+    ("maintain", "bank.hist_v[i] += bank.hist_v[j]", "bank.hist_v[i] += bank.hist_k[j]",
+     [M.test_merge_adds_statistics_and_weights_the_spatial_mean]),
+    ("maintain", "reversed(list(near))", "list(near)",
+     [M.test_recycling_takes_near_tokens_newest_frame_first_in_raster_order]),
+    ("maintain", "bank.n[j] = 0", "bank.n[j] = bank.n[j]",
+     [M.test_merge_adds_statistics_and_weights_the_spatial_mean]),
 ]
 
 
