@@ -56,7 +56,8 @@ in DESIGN.md):
   centre stays (histograms, n_res, mu, Sigma and tau stay).  Merging: pairs
   (i, j), i < j, in ascending order; i absorbs j when
   ||c_i - c_j||^2 < eps_K^2 and ||p_i - p_j||^2 < eps_V^2, each a float64
-  sum over d ascending of (c_i[d] - c_j[d])^2 with c = float32(sum / n),
+  sum of the terms (c_i[d] - c_j[d])^2 (c = float32(sum / n)) taken as
+  pairs of consecutive dims, then halves of the partial sums,
   using i's centre as updated by its earlier merges; sums, squared sums,
   histograms, n and n_res add, mu becomes the mass-weighted mean, Sigma and
   tau of i stay, j becomes empty.  Recycling: the empty slots of the prefix,
@@ -385,12 +386,16 @@ def _seed_slot(bank: Bank, k: int, kk: np.ndarray, vv: np.ndarray, coord: np.nda
 
 
 def _dist2(a: np.ndarray, b: np.ndarray) -> float:
-    """float64 sum over d ascending of (a[d] - b[d])^2 (a, b float32)."""
-    acc = 0.0
-    for x, y in zip(a.tolist(), b.tolist()):
-        t = x - y
-        acc = acc + t * t
-    return acc
+    """sum_d (a[d] - b[d])^2 for float32 a, b of length 2^m, in float64:
+    each term a rounded difference, then a rounded square; the terms are
+    added as pairs of consecutive dims, then the first half of the partial
+    sums plus the second half, until one is left."""
+    t = (a.astype(np.float64) - b.astype(np.float64)) ** 2
+    s = [t[2 * i] + t[2 * i + 1] for i in range(len(t) // 2)]
+    while len(s) > 1:
+        h = len(s) // 2
+        s = [s[i] + s[i + h] for i in range(h)]
+    return float(s[0])
 
 
 def maintain(bank: Bank, near: Sequence[Tuple[int, np.ndarray, np.ndarray]], t_frame: int,
