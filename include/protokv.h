@@ -57,7 +57,8 @@ enum { PROTOKV_KV_BF16 = 0, PROTOKV_KV_FP32 = 1 };
 /* flags */
 enum {
   PROTOKV_FLAG_PQ = 1u,        /* residual statistics on (off = "w/o residual stats" ablation) */
-  PROTOKV_FLAG_MASS_BIAS = 2u  /* log-mass bias on (off = "b_k = 0" ablation) */
+  PROTOKV_FLAG_MASS_BIAS = 2u, /* log-mass bias on (off = "b_k = 0" ablation) */
+  PROTOKV_FLAG_MAINTENANCE = 4u /* Alg. "Prototype Maintenance" after every fold (capacity <= 2048) */
 };
 
 typedef struct {
@@ -82,10 +83,13 @@ typedef struct {
   double lambda_sp;         /* spatial weight of Eq. 1 */
   double lambda_idle;       /* idle weight of Eq. 1 */
   double ridge;             /* rho added to Sigma's diagonal in d_Mah */
+  double gamma;             /* maintenance: idle mass decay, n <- floor((1 - gamma) n), in [0, 1) */
+  double eps_k, eps_v;      /* maintenance: key / value centre merge thresholds (>= 0) */
 } protokv_config;
 
 /* Table tab:default_config defaults (S=8, lambda_sp=0.1, lambda_idle=0.01,
- * T_idle=120, eta=0.05, G=8, C=16, B=32) with the 7B-class shape of one
+ * T_idle=120, eta=0.05, G=8, C=16, B=32, gamma=0.05, eps_K=0.20,
+ * eps_V=0.25; maintenance off) with the 7B-class shape of one
  * stream: 28 layers, 4 KV heads, 28 query heads, 14x14 tokens per frame,
  * W=8 frames, K=256, bf16 KV, PQ and mass bias on, eps=1, rho=1e-4.
  * Host only. */
@@ -127,7 +131,13 @@ protokv_status protokv_append_frame(protokv_t h, const int32_t* stream_ids, int3
 /* Absorbs every pending evicted frame into its stream's prototype bank:
  * seeds free slots (Initialization), assigns the other tokens by Eq. 1 against
  * the post-seed bank and accumulates mass, sum, sum of squares, PQ residual
- * histograms, spatial mean/covariance and recency in eviction order.
+ * histograms, spatial mean/covariance and recency in eviction order.  With
+ * PROTOKV_FLAG_MAINTENANCE each fold then runs Alg. "Prototype Maintenance"
+ * on the seeded slots: idle mass decay n <- floor((1 - gamma) n) (sums and
+ * squared sums scaled to keep the centre), merging of slot pairs whose key
+ * and value centres are closer than eps_k, eps_v (the lower slot absorbs the
+ * higher, pairs in ascending order, each merge moving the absorbing centre),
+ * and reseeding of emptied slots from the near window's newest tokens.
  * Invalidates any synthesis.  No-op when nothing is pending. */
 protokv_status protokv_fold(protokv_t h, void* stream);
 
@@ -171,6 +181,9 @@ typedef struct {
   uint64_t refined_full;     /* assignments re-scored exactly against every slot */
   uint64_t near_ties;        /* assignments whose exact top-2 cost margin < 1e-6 */
   uint64_t touched;          /* (prototype, fold) pairs that absorbed >= 1 token */
+  uint64_t aged;             /* maintenance: (prototype, fold) mass decays */
+  uint64_t merged;           /* maintenance: prototypes merged into a lower slot */
+  uint64_t recycled;         /* maintenance: slots reseeded from the near window */
 } protokv_counters;
 
 /* Totals since init.  Synchronizes `stream`. */
@@ -226,6 +239,7 @@ enum {
   PROTOKV_K_ATTEND_MERGE = 6,
   PROTOKV_K_PQ_ENCODE = 7,       /* reserved: PQ encoding runs inside the screen kernel */
   PROTOKV_K_MATERIALIZE = 8,     /* pseudo-token rows and biases (float32 KV) */
+  PROTOKV_K_MAINTAIN = 9,        /* prototype maintenance (PROTOKV_FLAG_MAINTENANCE) */
   PROTOKV_K_COUNT = 12
 };
 

@@ -1153,4 +1153,254 @@ hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch
 }
 
 
+// ---------------------------------------------------------------------------
+// Prototype maintenance (Alg. "Prototype Maintenance") after a fold, over the
+// A = nact + nseed seeded slots of one (stream, unit); workgroup of 4 waves.
+//  1. Aging (waves over slots): an idle slot gets n' = floor((1 - gamma) n)
+//     in float64 and its sums and squared sums are scaled by float32(n') /
+//     float32(n); every slot's first MT_FD key-centre dims float32(sumK / n)
+//     go to LDS.
+//  2. Merging (wave 0): i ascending; the candidates j > i are found 64 at a
+//     time by a float32 filter on the LDS dims (a partial sum of squares is
+//     a lower bound of the full one; the filter keeps every pair whose float32
+//     partial is within 1e-4 relative of eps_k^2, far more than its rounding)
+//     and tested exactly: float64 terms (c_i[d] - c_j[d])^2, lane l adding
+//     dims 2l and 2l+1, then a butterfly over the lanes; i absorbs j (sums,
+//     squared sums, histograms, n, n_res add; mu the mass-weighted mean), and
+//     i's centre (registers and LDS) moves before the scan goes on.
+//  3. Recycling (waves over slots): the empty slots, in ascending order, take
+//     the near window's tokens, newest frame first, raster order.
+//  4. The screening copies of aged and absorbing slots are rewritten
+//     (recycled slots are rewritten as they are seeded).
+// ---------------------------------------------------------------------------
+constexpr int MT_FD = 16;  // leading key dims of each centre in the LDS filter
+
+// dynamic LDS of k_maintain for capacity K
+__host__ __device__ inline size_t mt_lds_bytes(int K) {
+  return (((size_t)K * (MT_FD * 4 + 4 + 2 + 1)) + 15) & ~(size_t)15;
+}
+
+template <int FP32>
+__global__ __launch_bounds__(256) void k_maintain(Dims dm, Workspace ws, FoldBatch fb) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t s_dyn[];
+  __shared__ int s_cnt[3];  // aged, merged, recycled
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int b = blockIdx.x / dm.units, u = blockIdx.x % dm.units;
+  const int A = fb.nact[b] + fb.nseed[b];
+  if (A <= 0) return;  // uniform
+  const int t = fb.t[b];
+  const int T = dm.T;
+  const size_t unit = (size_t)fb.sid[b] * dm.units + u;
+  uint8_t* rows = ws.bank + unit * dm.K * ROW;
+  float* s_c16 = reinterpret_cast<float*>(s_dyn);                                // [A][MT_FD]
+  uint32_t* s_n = reinterpret_cast<uint32_t*>(s_dyn + (size_t)dm.K * MT_FD * 4);  // [A] current mass
+  uint16_t* s_rk = reinterpret_cast<uint16_t*>(s_n + dm.K);                      // [A] recycling rank
+  uint8_t* s_dirty = reinterpret_cast<uint8_t*>(s_rk + dm.K);                    // [A] screening copy stale
+  if (tid < 3) s_cnt[tid] = 0;
+  __syncthreads();
+
+  // 1. aging; lane l holds floats 8l .. 8l+7 of the row's sums and squared
+  // sums (lanes 0 and 1: key dims 0 .. 15)
+  for (int k = wave; k < A; k += 4) {  // uniform per wave
+    uint8_t* row = rows + (size_t)k * ROW;
+    const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+    float4* pf = reinterpret_cast<float4*>(row + ROW_SUMK) + 2 * lane;
+    float4 f0 = pf[0], f1 = pf[1];
+    uint32_t n = m.n;
+    const bool idle = (t - m.tau / T) > dm.t_idle;
+    if (idle) {
+      const uint32_t n2 = (uint32_t)floor((1.0 - dm.gamma) * (double)n);
+      const float r = (float)n2 / (float)n;
+      f0 = make_float4(f0.x * r, f0.y * r, f0.z * r, f0.w * r);
+      f1 = make_float4(f1.x * r, f1.y * r, f1.z * r, f1.w * r);
+      pf[0] = f0;
+      pf[1] = f1;
+      if (lane == 0) *reinterpret_cast<uint32_t*>(row + ROW_META) = n2;  // RowMeta::n
+      n = n2;
+    }
+    if (lane < 2) {
+      const float nf = (float)n;
+      const float fv[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+#pragma unroll
+      for (int q = 0; q < 8; ++q) s_c16[k * MT_FD + 8 * lane + q] = n > 0 ? fv[q] / nf : 0.f;
+    }
+    if (lane == 0) {
+      s_n[k] = n;
+      s_dirty[k] = idle ? 1 : 0;
+      if (idle) atomicAdd(&s_cnt[0], 1);
+    }
+  }
+  __syncthreads();
+
+  // 2. merging (wave 0)
+  if (wave == 0) {
+    const double ek2 = dm.eps_k * dm.eps_k, ev2 = dm.eps_v * dm.eps_v;
+    const float fk2 = (float)(ek2 * (1.0 + 1e-4));
+    int nmerged = 0;
+    for (int i = 0; i < A; ++i) {
+      if (s_n[i] == 0) continue;  // uniform
+      uint8_t* rowi = rows + (size_t)i * ROW;
+      bool have_ci = false;
+      float2 cik = make_float2(0.f, 0.f), civ = make_float2(0.f, 0.f);  // dims 2l, 2l+1 of c_i, p_i
+      int j0 = i + 1;
+      while (j0 < A) {  // uniform
+        const int j = j0 + lane;
+        bool pass = false;
+        if (j < A && s_n[j] != 0) {
+          float part = 0.f;
+#pragma unroll
+          for (int d = 0; d < MT_FD; ++d) {
+            const float df = s_c16[i * MT_FD + d] - s_c16[j * MT_FD + d];
+            part = part + df * df;
+          }
+          pass = !(part > fk2);
+        }
+        const unsigned long long bal = __ballot(pass);
+        if (bal == 0ull) {
+          j0 += 64;
+          continue;
+        }
+        const int jj = j0 + __ffsll((long long)bal) - 1;
+        const uint8_t* rowj = rows + (size_t)jj * ROW;
+        if (!have_ci) {
+          const float ni = (float)s_n[i];
+          const float2 sk = reinterpret_cast<const float2*>(rowi + ROW_SUMK)[lane];
+          const float2 sv = reinterpret_cast<const float2*>(rowi + ROW_SUMV)[lane];
+          cik = make_float2(sk.x / ni, sk.y / ni);
+          civ = make_float2(sv.x / ni, sv.y / ni);
+          have_ci = true;
+        }
+        const float nj = (float)s_n[jj];
+        const float2 tk = reinterpret_cast<const float2*>(rowj + ROW_SUMK)[lane];
+        const float2 tv = reinterpret_cast<const float2*>(rowj + ROW_SUMV)[lane];
+        const float2 cjk = make_float2(tk.x / nj, tk.y / nj), cjv = make_float2(tv.x / nj, tv.y / nj);
+        double dk, dv;
+        {
+          const double ax = (double)cik.x - (double)cjk.x, ay = (double)cik.y - (double)cjk.y;
+          const double bx = (double)civ.x - (double)cjv.x, by = (double)civ.y - (double)cjv.y;
+          dk = ax * ax + ay * ay;
+          dv = bx * bx + by * by;
+#pragma unroll
+          for (int o = 32; o >= 1; o >>= 1) {
+            dk = dk + __shfl_xor(dk, o, 64);
+            dv = dv + __shfl_xor(dv, o, 64);
+          }
+        }
+        if (dk < ek2 && dv < ev2) {  // uniform
+          // i absorbs jj: lane l adds dims 2l, 2l+1 of the four sums and
+          // histogram words 4l .. 4l+3 (H^K then H^V)
+          float2 x[4];
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            float2* pi = reinterpret_cast<float2*>(rowi + a * 512) + lane;
+            const float2 xi = *pi, xj = reinterpret_cast<const float2*>(rowj + a * 512)[lane];
+            x[a] = make_float2(xi.x + xj.x, xi.y + xj.y);
+            *pi = x[a];
+          }
+          {
+            uint4* hi = reinterpret_cast<uint4*>(rowi + ROW_HK) + lane;
+            const uint4 h1 = *hi, h2 = reinterpret_cast<const uint4*>(rowj + ROW_HK)[lane];
+            *hi = make_uint4(h1.x + h2.x, h1.y + h2.y, h1.z + h2.z, h1.w + h2.w);
+          }
+          const RowMeta mi = *reinterpret_cast<const RowMeta*>(rowi + ROW_META);
+          const RowMeta mj = *reinterpret_cast<const RowMeta*>(rowj + ROW_META);
+          const float wi = (float)mi.n, wj = (float)mj.n, wsum = wi + wj;
+          RowMeta mn = mi;
+          mn.mu_x = ((wi * mi.mu_x) + (wj * mj.mu_x)) / wsum;
+          mn.mu_y = ((wi * mi.mu_y) + (wj * mj.mu_y)) / wsum;
+          mn.n = mi.n + mj.n;
+          mn.n_res = mi.n_res + mj.n_res;
+          if (lane == 0) {
+            *reinterpret_cast<RowMeta*>(rowi + ROW_META) = mn;
+            *reinterpret_cast<uint32_t*>(const_cast<uint8_t*>(rowj) + ROW_META) = 0u;  // RowMeta::n
+            s_n[i] = mn.n;
+            s_n[jj] = 0u;
+            s_dirty[i] = 1;
+          }
+          // i's centre moves
+          const float nn = (float)mn.n;
+          cik = make_float2(x[0].x / nn, x[0].y / nn);
+          civ = make_float2(x[1].x / nn, x[1].y / nn);
+          if (lane < MT_FD / 2) {
+            s_c16[i * MT_FD + 2 * lane] = cik.x;
+            s_c16[i * MT_FD + 2 * lane + 1] = cik.y;
+          }
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+          ++nmerged;
+        }
+        j0 = jj + 1;
+      }
+    }
+    if (lane == 0) s_cnt[1] = nmerged;
+    // recycling ranks: e-th empty slot in ascending order
+    const unsigned long long below = (1ull << lane) - 1ull;
+    int run = 0;
+    for (int k0 = 0; k0 < A; k0 += 64) {
+      const int k = k0 + lane;
+      const bool empty = k < A && s_n[k] == 0;
+      const unsigned long long bal = __ballot(empty);
+      if (empty) s_rk[k] = (uint16_t)(run + __popcll(bal & below));
+      run += __popcll(bal);
+    }
+    if (lane == 0) s_cnt[2] = run;
+  }
+  __syncthreads();
+
+  // 3. recycling and 4. screening copies
+  const int ntok = dm.W * T;
+  for (int k = wave; k < A; k += 4) {  // uniform per wave
+    uint8_t* row = rows + (size_t)k * ROW;
+    if (s_n[k] == 0) {
+      const int e = (int)s_rk[k] % ntok;
+      const int f = t - e / T, j = e % T;
+      const int rs = f % (dm.W + 1);
+      const size_t tb = ((unit * (dm.W + 1) + rs) * (size_t)T + j) * D;
+      const float2 kk = load2<FP32>(ws.ring_k, tb + 2 * lane);
+      const float2 vv = load2<FP32>(ws.ring_v, tb + 2 * lane);
+      reinterpret_cast<float2*>(row + ROW_SUMK)[lane] = kk;
+      reinterpret_cast<float2*>(row + ROW_SUMV)[lane] = vv;
+      reinterpret_cast<float2*>(row + ROW_SQK)[lane] = make_float2(kk.x * kk.x, kk.y * kk.y);
+      reinterpret_cast<float2*>(row + ROW_SQV)[lane] = make_float2(vv.x * vv.x, vv.y * vv.y);
+      reinterpret_cast<uint2*>(row + ROW_HK)[lane] = make_uint2(0, 0);
+      reinterpret_cast<uint2*>(row + ROW_HV)[lane] = make_uint2(0, 0);
+      RowMeta m;
+      m.n = 1;
+      m.n_res = 0;
+      token_xy(j, dm.grid_w, dm.grid_h, m.mu_x, m.mu_y);
+      m.sxx = 1.f;
+      m.sxy = 0.f;
+      m.syy = 1.f;
+      m.tau = f * T + j;
+      if (lane == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
+      refresh_cache(dm, kk, m, unit, k, ws, lane);
+    } else if (s_dirty[k]) {
+      const float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
+      const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+      refresh_cache(dm, sk, m, unit, k, ws, lane);
+    }
+  }
+  if (tid == 0) {
+    if (s_cnt[0]) atomicAdd(&ws.counters[CNT_AGED], (unsigned long long)s_cnt[0]);
+    if (s_cnt[1]) atomicAdd(&ws.counters[CNT_MERGED], (unsigned long long)s_cnt[1]);
+    if (s_cnt[2]) atomicAdd(&ws.counters[CNT_RECYCLED], (unsigned long long)s_cnt[2]);
+  }
+}
+
+hipError_t launch_maintain(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
+  const size_t lds = mt_lds_bytes(dm.K);  // <= 145 KiB for K <= MT_KMAX
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(dm.kv_fp32 ? k_maintain<1> : k_maintain<0>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  dim3 grid(fb.n * dm.units);
+  if (dm.kv_fp32)
+    hipLaunchKernelGGL(k_maintain<1>, grid, dim3(256), lds, st, dm, ws, fb);
+  else
+    hipLaunchKernelGGL(k_maintain<0>, grid, dim3(256), lds, st, dm, ws, fb);
+  return hipGetLastError();
+}
+
 }  // namespace pkv

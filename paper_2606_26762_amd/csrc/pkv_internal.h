@@ -25,6 +25,7 @@ constexpr int PCW = SMAX + 2;   // words per (slot, K/V) decode record: S tuples
 // floor(63 / S) + 2 slots at most); below that the synthesis writes the rows.
 constexpr int PS_SLOTS = 14;
 constexpr int PS_MIN_S = 5;
+constexpr int MT_KMAX = 2048;   // largest capacity the maintenance pass supports (its LDS)
 
 // Bank row (one prototype slot), byte offsets; see protokv.h.
 constexpr int ROW = PROTOKV_ROW_BYTES;
@@ -57,6 +58,7 @@ struct Dims {
   uint32_t flags;
   float eta;
   double lambda_sp, lambda_idle, ridge;
+  double gamma, eps_k, eps_v;  // maintenance (PROTOKV_FLAG_MAINTENANCE)
   int max_rows;    // max query rows per kv head (max_query_tokens * Hq / Hkv)
   int max_splits;  // attention context splits (partials storage)
 };
@@ -99,6 +101,9 @@ enum Counter {
   CNT_REFINED_FULL = 1,
   CNT_NEAR_TIES = 2,
   CNT_TOUCHED = 3,
+  CNT_AGED = 4,
+  CNT_MERGED = 5,
+  CNT_RECYCLED = 6,
   CNT_COUNT = 16
 };
 
@@ -158,6 +163,7 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
                          hipStream_t st);
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                             hipStream_t st);
+hipError_t launch_maintain(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st);
 // centres: also write the float32 centres (pcen) and biases for the readout's
 // row forming; wide: some slot may hold more than 65534 residuals (the
 // 192-bit path runs too)

@@ -97,13 +97,20 @@ protokv_status check_config(const protokv_config* c, std::string& why) {
   if ((int64_t)c->max_query_tokens * (c->num_q_heads / c->num_kv_heads) > MAX_ROWS)
     return uns("max_query_tokens * (num_q_heads/num_kv_heads) above 512");
   if (c->kv_dtype != PROTOKV_KV_BF16 && c->kv_dtype != PROTOKV_KV_FP32) return bad("kv_dtype unknown");
-  if (c->flags & ~(uint32_t)(PROTOKV_FLAG_PQ | PROTOKV_FLAG_MASS_BIAS)) return bad("unknown flag bits");
+  if (c->flags & ~(uint32_t)(PROTOKV_FLAG_PQ | PROTOKV_FLAG_MASS_BIAS | PROTOKV_FLAG_MAINTENANCE))
+    return bad("unknown flag bits");
   if (!(c->eta > 0.f && c->eta < 1.f)) return bad("eta must be in (0, 1)");
   if (c->pq_eps != 1.0f) return uns("pq_eps must be 1");
   if (!(c->lambda_sp >= 0.0) || !(c->lambda_idle >= 0.0) || !std::isfinite(c->lambda_sp) ||
       !std::isfinite(c->lambda_idle))
     return bad("lambda_sp and lambda_idle must be finite and >= 0");
   if (!(c->ridge > 0.0) || !std::isfinite(c->ridge)) return bad("ridge must be finite and > 0");
+  if (c->flags & PROTOKV_FLAG_MAINTENANCE) {
+    if (!(c->gamma >= 0.0 && c->gamma < 1.0)) return bad("gamma must be in [0, 1)");
+    if (!(c->eps_k >= 0.0) || !(c->eps_v >= 0.0) || !std::isfinite(c->eps_k) || !std::isfinite(c->eps_v))
+      return bad("eps_k and eps_v must be finite and >= 0");
+    if (c->capacity > MT_KMAX) return uns("maintenance supports capacity up to 2048");
+  }
   return PROTOKV_OK;
 }
 
@@ -189,6 +196,9 @@ protokv_status protokv_default_config(protokv_config* c) {
   c->lambda_sp = 0.1;
   c->lambda_idle = 0.01;
   c->ridge = 1e-4;
+  c->gamma = 0.05;
+  c->eps_k = 0.20;
+  c->eps_v = 0.25;
   return PROTOKV_OK;
 }
 
@@ -247,6 +257,9 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   dm.lambda_sp = c->lambda_sp;
   dm.lambda_idle = c->lambda_idle;
   dm.ridge = c->ridge;
+  dm.gamma = c->gamma;
+  dm.eps_k = c->eps_k;
+  dm.eps_v = c->eps_v;
   dm.max_rows = c->max_query_tokens * (c->num_q_heads / c->num_kv_heads);
   dm.max_splits = MAX_SPLITS;
   uint8_t* b = h->base;
@@ -395,6 +408,9 @@ protokv_status protokv_fold(protokv_t h, void* stream) {
     if (st == PROTOKV_OK && any_assign)
       st = h->dev(h->launch(PROTOKV_K_AGGREGATE, hs, [&] { return launch_aggregate(h->dm, h->ws, fb, hs); }),
                   "fold/aggregate");
+    if (st == PROTOKV_OK && (h->dm.flags & PROTOKV_FLAG_MAINTENANCE))
+      st = h->dev(h->launch(PROTOKV_K_MAINTAIN, hs, [&] { return launch_maintain(h->dm, h->ws, fb, hs); }),
+                  "fold/maintain");
     if (st != PROTOKV_OK) return st;
     for (int i = 0; i < fb.n; ++i) {
       StreamState& ss = h->st[fb.sid[i]];
@@ -532,6 +548,9 @@ protokv_status protokv_get_counters(protokv_t h, protokv_counters* out, void* st
   out->refined_full = dc[CNT_REFINED_FULL];
   out->near_ties = dc[CNT_NEAR_TIES];
   out->touched = touched;
+  out->aged = dc[CNT_AGED];
+  out->merged = dc[CNT_MERGED];
+  out->recycled = dc[CNT_RECYCLED];
   return PROTOKV_OK;
 }
 

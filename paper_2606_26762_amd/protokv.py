@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "libprotokv.so")
 
 ROW_BYTES = 3200
 KV_BF16, KV_FP32 = 0, 1
-FLAG_PQ, FLAG_MASS_BIAS = 1, 2
+FLAG_PQ, FLAG_MASS_BIAS, FLAG_MAINTENANCE = 1, 2, 4
 
 STATUS = {0: "OK", 1: "E_INVALID", 2: "E_UNSUPPORTED", 3: "E_WORKSPACE", 4: "E_STATE", 5: "E_DEVICE"}
 
@@ -30,7 +30,7 @@ EXPORTED = [
 ]
 
 KERNELS = ["ring_insert", "seed", "screen", "aggregate", "decode", "attend", "attend_merge", "pq_encode",
-           "materialize"]
+           "materialize", "maintain"]
 
 
 class ProtoKVError(RuntimeError):
@@ -50,6 +50,7 @@ class Config(ctypes.Structure):
         ("max_query_tokens", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
         ("flags", ctypes.c_uint32), ("eta", ctypes.c_float), ("pq_eps", ctypes.c_float),
         ("lambda_sp", ctypes.c_double), ("lambda_idle", ctypes.c_double), ("ridge", ctypes.c_double),
+        ("gamma", ctypes.c_double), ("eps_k", ctypes.c_double), ("eps_v", ctypes.c_double),
     ]
 
 
@@ -62,7 +63,8 @@ class Counters(ctypes.Structure):
     _fields_ = [("folds", ctypes.c_uint64), ("tokens_assigned", ctypes.c_uint64),
                 ("tokens_seeded", ctypes.c_uint64), ("refined", ctypes.c_uint64),
                 ("refined_full", ctypes.c_uint64), ("near_ties", ctypes.c_uint64),
-                ("touched", ctypes.c_uint64)]
+                ("touched", ctypes.c_uint64), ("aged", ctypes.c_uint64), ("merged", ctypes.c_uint64),
+                ("recycled", ctypes.c_uint64)]
 
 
 class KernelTimes(ctypes.Structure):

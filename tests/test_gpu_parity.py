@@ -103,6 +103,27 @@ def test_formed_rows_across_s(S):
     h.log(f"readout err formed {w1:.2e} written {w2:.2e}, max diff {np.abs(o1 - o2).max():.2e}")
 
 
+@pytest.mark.parametrize("eps_k,eps_v", [(1.0, 12.0), (1.5, 14.0)])
+def test_maintenance_aging_merging_recycling(eps_k, eps_v):
+    """Prototype maintenance after every fold (T_idle = 2 frames, gamma =
+    0.3, merge thresholds that let same-cluster prototypes merge): banks
+    bitwise equal to the oracle's after every fold, then the readout."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=6, grid_w=6,
+                                 frames=14, window_frames=2, capacity=48, query_tokens=4)
+    h.log(f"case: maintenance eps_k={eps_k} eps_v={eps_v} T=36 K=48 W=2")
+    pair = h.Pair(wl, maintenance=True, t_idle=2, gamma=0.3, eps_k=eps_k, eps_v=eps_v)
+    for f in range(wl.frames):
+        pair.step()
+        if f >= wl.window_frames:
+            pair.check_bank(bitwise=True)
+    c = pair.gpu.counters()
+    h.log(f"aged {c.aged} merged {c.merged} recycled {c.recycled}, near ties {pair.near_ties}")
+    assert c.aged > 0 and c.merged > 0 and c.recycled > 0
+    pseudo = pair.synthesize()
+    pair.attend(pair.query(np.random.default_rng(11)), pseudo)
+
+
 def test_capacity_limit_gives_exact_attention():
     """K >= evicted tokens: every token keeps its own slot, and the readout is
     exact attention over the full history with far logits shifted by ln S
