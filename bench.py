@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=64)
     ap.add_argument("--workload", default="7b")
     ap.add_argument("--profile-frames", type=int, default=32)
+    ap.add_argument("--maintenance", action="store_true",
+                    help="fold with prototype maintenance (aging, merging, recycling) after every frame")
     ap.add_argument("--query-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=32)
@@ -58,11 +60,13 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0, rows=0, formed=False):
+def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0, rows=0, formed=False,
+                      maint=None):
     """Bytes the method must move per launch of `kernel` (all units of one stream).
 
     `formed`: the readout forms the pseudo-token rows from the centres, code
-    tuples and codebooks as it loads them (no rows in memory)."""
+    tuples and codebooks as it loads them (no rows in memory).  `maint`: aged,
+    merged and recycled slots per maintenance launch."""
     U, T, D, K, S = wl.units, wl.tokens_per_frame, wl.head_dim, wl.capacity, cfg.pseudo_per_proto
     b = 4 if wl.kv_dtype == "fp32" else 2
     if kernel == "ring_insert":
@@ -78,6 +82,17 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
         # squares and meta read and written and its screening copy rewritten
         return (U * (2 * T * D * b + T * 4)
                 + touched_per_launch * (2 * ROW_STATS_BYTES + CACHE_BYTES))
+    if kernel == "maintain":
+        # every slot's mass, tau and leading fd key and value dims (the LDS
+        # filter: 16, 8 or 4 dims as K grows); an aged slot's sums and squares
+        # read and written; a merge reads two rows and writes one; a recycled
+        # slot reads its token and writes its row; rewritten screening copies
+        m = maint or {}
+        fd = 16 if K <= 512 else (8 if K <= 1024 else 4)
+        row = 4 * D * 4 + 2 * 8 * 16 * 4 + 32
+        return (U * n_active * (8 + 2 * fd * 4) + m.get("aged", 0) * (2 * 4 * D * 4 + CACHE_BYTES)
+                + m.get("merged", 0) * (3 * row + CACHE_BYTES)
+                + m.get("recycled", 0) * (2 * D * b + row + CACHE_BYTES))
     if kernel == "decode":
         # histograms, meta, codes out; with formed rows also the sums in and
         # the float32 centres and bias out
@@ -98,8 +113,8 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     return 0
 
 
-FOLD_KERNELS = ("ring_insert", "seed", "screen", "aggregate")
-KERNEL_SOURCES = {k: "fold.hip" for k in FOLD_KERNELS}
+FOLD_KERNELS = ("ring_insert", "seed", "screen", "aggregate", "maintain")
+KERNEL_SOURCES = {k: "fold.hip" for k in FOLD_KERNELS}  # maintain too
 KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "attend", "attend_merge")})
 
 
@@ -206,6 +221,8 @@ def main():
                             window_frames=wl.window_frames, capacity=wl.capacity,
                             max_query_tokens=wl.query_tokens,
                             kv_dtype=pk.KV_FP32 if wl.kv_dtype == "fp32" else pk.KV_BF16)
+    if args.maintenance:
+        cfg.flags |= pk.FLAG_MAINTENANCE
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cb = W.make_codebooks_device(wl)
@@ -264,10 +281,12 @@ def main():
     rows = tq * (wl.num_q_heads // wl.num_kv_heads)
     ctx = min(info.frames, wl.window_frames) * T + n_active * cfg.pseudo_per_proto
     formed = "materialize" not in kt  # bf16 readout forms the pseudo-token rows itself
+    nm = max(1, kt.get("maintain", {}).get("launches", 1))
+    maint = {k: (getattr(c1, k) - getattr(c0, k)) / nm for k in ("aged", "merged", "recycled")}
     kernels = {}
     for name, d in kt.items():
         nbytes = algorithmic_bytes(name, wl, cfg, touched_per_launch=touched, n_active=n_active,
-                                   ctx=ctx, rows=rows, formed=formed)
+                                   ctx=ctx, rows=rows, formed=formed, maint=maint)
         kernels[name] = {"avg_us": round(d["avg_us"], 3), "launches": d["launches"],
                          "alg_bytes": int(nbytes),
                          "gbs": round(nbytes / (d["avg_us"] * 1e-6) / 1e9, 1) if nbytes else None}
@@ -315,7 +334,7 @@ def main():
     attend_ms = median_ms(lambda: attend(h, 0, qp, tq, op, lp, sp), args.query_reps)
 
     dom_bytes = algorithmic_bytes(dom, wl, cfg, touched_per_launch=touched_live, n_active=n_active,
-                                  ctx=ctx, rows=rows, formed=formed)
+                                  ctx=ctx, rows=rows, formed=formed, maint=maint)
     achieved = dom_bytes / (live["avg_us"] * 1e-6) / 1e9
     traffic = recorded_traffic(dom, wl)
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -342,7 +361,7 @@ def main():
                    "q_heads": wl.num_q_heads, "head_dim": wl.head_dim, "tokens_per_frame": T,
                    "window_frames": wl.window_frames, "capacity": wl.capacity,
                    "pseudo_per_proto": cfg.pseudo_per_proto, "query_tokens": tq,
-                   "frames_streamed": lo + args.steps},
+                   "frames_streamed": lo + args.steps, "maintenance": bool(args.maintenance)},
         "fold_tokens_per_s": round(args.steps * T / (ms_fold / 1e3), 1),
         "fold_us_per_frame": round(1e3 * ms_fold / args.steps, 2),
         "query_us_in_region": round(1e3 * ms_query_in_region, 2),
@@ -353,6 +372,7 @@ def main():
         "context_tokens": ctx,
         "refined_fraction": round((c3.refined + c3.refined_full) / max(1, c3.tokens_assigned), 5),
         "refined_full": c3.refined_full, "near_ties": c3.near_ties,
+        "maintenance_per_fold": ({k: round(v, 1) for k, v in maint.items()} if args.maintenance else None),
         "kernels": kernels,
         "roofline": roofline,
     }

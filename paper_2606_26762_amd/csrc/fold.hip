@@ -1155,36 +1155,102 @@ hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch
 
 // ---------------------------------------------------------------------------
 // Prototype maintenance (Alg. "Prototype Maintenance") after a fold, over the
-// A = nact + nseed seeded slots of one (stream, unit); workgroup of 4 waves.
-//  1. Aging (waves over slots): an idle slot gets n' = floor((1 - gamma) n)
-//     in float64 and its sums and squared sums are scaled by float32(n') /
-//     float32(n); every slot's first MT_FD key-centre dims float32(sumK / n)
-//     go to LDS.
-//  2. Merging (wave 0): i ascending; the candidates j > i are found 64 at a
-//     time by a float32 filter on the LDS dims (a partial sum of squares is
-//     a lower bound of the full one; the filter keeps every pair whose float32
-//     partial is within 1e-4 relative of eps_k^2, far more than its rounding)
-//     and tested exactly: float64 terms (c_i[d] - c_j[d])^2, lane l adding
-//     dims 2l and 2l+1, then a butterfly over the lanes; i absorbs j (sums,
-//     squared sums, histograms, n, n_res add; mu the mass-weighted mean), and
-//     i's centre (registers and LDS) moves before the scan goes on.
-//  3. Recycling (waves over slots): the empty slots, in ascending order, take
-//     the near window's tokens, newest frame first, raster order.
+// A = nact + nseed seeded slots of one (stream, unit); workgroup of MT_WAVES
+// waves.
+//  1. Aging (threads over slots, then over 16-byte pieces): an idle slot gets
+//     n' = floor((1 - gamma) n) in float64 and its sums and squared sums are
+//     scaled by float32(n') / float32(n); the first FD dims of every slot's
+//     key and value centres float32(sum / n) go to LDS (FD = 16, 8 or 4 as
+//     K grows).
+//  2. Merging, i ascending: i absorbs every later j whose key and value
+//     centres are closer than eps_k and eps_v.  A squared distance is the
+//     float64 terms (c_i[d] - c_j[d])^2 summed in a fixed tree: dims 2L and
+//     2L + 1 first, then the 64 pair sums by halves of L (bit 5 first, bit 0
+//     last).  Rows go in blocks of mt_block(K); per block:
+//     a. a filter on the LDS dims over every pair i < j with i in the block:
+//        the partial sum of squares over the filter dims is a lower bound of
+//        the full one; the waves form it for 32 x 32 pair tiles in the Gram
+//        form on MFMA (bound below) and list the pairs whose key and value
+//        partials may be below eps_k^2 and eps_v^2 (1e-4 relative slack for
+//        the float64 rounding of the exact sums, plus the Gram bound);
+//     b. groups of 16 lanes test the listed pairs exactly and mark those
+//        that merge in a bitmask [block rows][K];
+//     c. wave 0 walks the marked rows: while i's centre has not moved, its
+//        partners are the marked j still holding mass (neither centre has
+//        changed since: a later slot only loses its mass to an earlier row);
+//        after i's first merge, and for rows whose pairs overflowed the
+//        list, it runs the filter as float32 sums of squares, 64 candidates
+//        at a time, and tests each candidate exactly (64 lanes, same tree).
+//     i absorbs j: sums, squared sums, histograms, n and n_res add, mu the
+//     mass-weighted mean; i's centre (registers and LDS) moves at once.
+//  3. Recycling (waves over a worklist): the empty slots, in ascending
+//     order, take the near window's tokens, newest frame first, raster order.
 //  4. The screening copies of aged and absorbing slots are rewritten
 //     (recycled slots are rewritten as they are seeded).
 // ---------------------------------------------------------------------------
-constexpr int MT_FD = 16;  // leading key dims of each centre in the LDS filter
+constexpr int MT_PAIRS = 4096;  // filter pairs listed per block
+constexpr int MT_THREADS = 512, MT_WAVES = MT_THREADS / 64;
+// Gram form of the filter: P = |a|^2 + |b|^2 - 2 a.b over the filter dims of
+// two float32 centres, a.b on MFMA from hi + lo bf16 splits (hi*hi + hi*lo +
+// lo*hi, float32 accumulation).  The split leaves at most 2^-16 |x| per
+// component, the dropped lo*lo term and the accumulation add at most 2^-17.4
+// sum |a_d b_d|, so |a.b - computed| <= 2^-14.1 |a| |b|; with the float32
+// norms, |P - (|a|^2 + |b|^2 - 2 computed)| <= 2^-13.9 S, S = |a|^2 + |b|^2.
+// A pair is kept when rho_i + (rho_j + thr) - 2 computed <= 0 with the row
+// terms rho = (1 - M) |x|^2 - thr (M = MT_GRAM_MARGIN): the test's own
+// roundings stay below 2^-20 S + 2^-21 thr, so every pair with P below thr
+// is kept.
+constexpr float MT_GRAM_MARGIN = 0x1p-12f;
 
-// dynamic LDS of k_maintain for capacity K
+__host__ __device__ inline int mt_fd(int K) { return K <= 512 ? 16 : (K <= 1024 ? 8 : 4); }
+__host__ __device__ inline int mt_w32(int K) { return (K + 31) / 32; }
+// rows per block (a multiple of 32 below K): the bitmask holds at most 32 KiB
+__host__ __device__ inline int mt_block(int K) {
+  const int r = 8192 / mt_w32(K);
+  return r < K ? (r & ~31) : K;
+}
+__host__ __device__ inline size_t mt_base_bytes(int K) {
+  return (((size_t)K * (2 * mt_fd(K) * 4 + 4 + 4 + 2 + 1) + (size_t)cap32(K) * 8) + 15) & ~(size_t)15;
+}
+// dynamic LDS of k_maintain for capacity K: filter dims, masses, aging
+// ratios, Gram row terms (key, value; K32 entries each), idle list /
+// recycling ranks, stale flags | bitmask, marked-row flags, overflow flags |
+// pair list (then the recycling and refresh worklist)
 __host__ __device__ inline size_t mt_lds_bytes(int K) {
-  return (((size_t)K * (MT_FD * 4 + 4 + 2 + 1)) + 15) & ~(size_t)15;
+  const size_t R = (size_t)mt_block(K);
+  return mt_base_bytes(K) + (R * mt_w32(K) + 2 * ((R + 31) / 32)) * 4 + (size_t)MT_PAIRS * 4;
 }
 
-template <int FP32>
-__global__ __launch_bounds__(256) void k_maintain(Dims dm, Workspace ws, FoldBatch fb) {
+// Squared key and value distances of two slots by a 16-lane group: lane m
+// holds dims 2L, 2L + 1 for L = m + 16 r (r = 0 .. 3), so the first two tree
+// levels (bits 5 and 4 of L) are in registers and the last four are lane
+// exchanges within the group.
+__device__ __forceinline__ void mt_dist16(const float2 (&ak)[4], const float2 (&av)[4], const float2 (&bk)[4],
+                                          const float2 (&bv)[4], double& dk, double& dv) {
+  double sk[4], sv[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const double ax = (double)ak[r].x - (double)bk[r].x, ay = (double)ak[r].y - (double)bk[r].y;
+    const double bx = (double)av[r].x - (double)bv[r].x, by = (double)av[r].y - (double)bv[r].y;
+    sk[r] = ax * ax + ay * ay;
+    sv[r] = bx * bx + by * by;
+  }
+  dk = (sk[0] + sk[2]) + (sk[1] + sk[3]);
+  dv = (sv[0] + sv[2]) + (sv[1] + sv[3]);
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) {
+    dk = dk + __shfl_xor(dk, o, 64);
+    dv = dv + __shfl_xor(dv, o, 64);
+  }
+}
+
+template <int FP32, int FD>
+__global__ __launch_bounds__(MT_THREADS) void k_maintain(Dims dm, Workspace ws, FoldBatch fb) {
   extern __shared__ __attribute__((aligned(16))) uint8_t s_dyn[];
   __shared__ int s_cnt[3];  // aged, merged, recycled
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ int s_np;      // pairs that passed the filter in this block
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int b = blockIdx.x / dm.units, u = blockIdx.x % dm.units;
   const int A = fb.nact[b] + fb.nseed[b];
   if (A <= 0) return;  // uniform
@@ -1192,165 +1258,407 @@ __global__ __launch_bounds__(256) void k_maintain(Dims dm, Workspace ws, FoldBat
   const int T = dm.T;
   const size_t unit = (size_t)fb.sid[b] * dm.units + u;
   uint8_t* rows = ws.bank + unit * dm.K * ROW;
-  float* s_c16 = reinterpret_cast<float*>(s_dyn);                                // [A][MT_FD]
-  uint32_t* s_n = reinterpret_cast<uint32_t*>(s_dyn + (size_t)dm.K * MT_FD * 4);  // [A] current mass
-  uint16_t* s_rk = reinterpret_cast<uint16_t*>(s_n + dm.K);                      // [A] recycling rank
-  uint8_t* s_dirty = reinterpret_cast<uint8_t*>(s_rk + dm.K);                    // [A] screening copy stale
+  float* s_c16 = reinterpret_cast<float*>(s_dyn);  // [2 FD][K]: key dims, then value dims, dim-major
+  // Gram row terms (1 - M) |filter dims|^2 - thr of key and value, +inf for
+  // empty slots and from A up to K32 (16-byte aligned for b128 reads)
+  float* s_rhk = s_c16 + (size_t)dm.K * 2 * FD;
+  float* s_rhv = s_rhk + cap32(dm.K);
+  uint32_t* s_n = reinterpret_cast<uint32_t*>(s_rhv + cap32(dm.K));  // [A] current mass
+  float* s_r = reinterpret_cast<float*>(s_n + dm.K);                  // [A] aging ratio
+  uint16_t* s_rk = reinterpret_cast<uint16_t*>(s_r + dm.K);          // [A] idle slots, later recycling ranks
+  uint8_t* s_dirty = reinterpret_cast<uint8_t*>(s_rk + dm.K);        // [A] screening copy stale
+  const int W32 = mt_w32(dm.K), R = mt_block(dm.K), RW = (R + 31) / 32;
+  uint32_t* s_adj = reinterpret_cast<uint32_t*>(s_dyn + mt_base_bytes(dm.K));  // [R][W32]: (i, j) merges
+  uint32_t* s_rf = s_adj + (size_t)R * W32;                                    // [RW]: row has a mark
+  uint32_t* s_ov = s_rf + RW;                                                  // [RW]: row's pairs overflowed
+  uint32_t* s_pairs = s_ov + RW;                                               // [MT_PAIRS]: i << 16 | j
+  const unsigned long long below = (1ull << lane) - 1ull;
   if (tid < 3) s_cnt[tid] = 0;
   __syncthreads();
 
-  // 1. aging; lane l holds floats 8l .. 8l+7 of the row's sums and squared
-  // sums (lanes 0 and 1: key dims 0 .. 15)
-  for (int k = wave; k < A; k += 4) {  // uniform per wave
-    uint8_t* row = rows + (size_t)k * ROW;
-    const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
-    float4* pf = reinterpret_cast<float4*>(row + ROW_SUMK) + 2 * lane;
-    float4 f0 = pf[0], f1 = pf[1];
-    uint32_t n = m.n;
-    const bool idle = (t - m.tau / T) > dm.t_idle;
-    if (idle) {
-      const uint32_t n2 = (uint32_t)floor((1.0 - dm.gamma) * (double)n);
-      const float r = (float)n2 / (float)n;
-      f0 = make_float4(f0.x * r, f0.y * r, f0.z * r, f0.w * r);
-      f1 = make_float4(f1.x * r, f1.y * r, f1.z * r, f1.w * r);
-      pf[0] = f0;
-      pf[1] = f1;
-      if (lane == 0) *reinterpret_cast<uint32_t*>(row + ROW_META) = n2;  // RowMeta::n
-      n = n2;
-    }
-    if (lane < 2) {
-      const float nf = (float)n;
-      const float fv[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+  const double ek2 = dm.eps_k * dm.eps_k, ev2 = dm.eps_v * dm.eps_v;
+  const float fk2 = (float)(ek2 * (1.0 + 1e-4)), fv2 = (float)(ev2 * (1.0 + 1e-4));
+  // 1a. aging, one thread per slot (its mass, tau and leading FD key and
+  // value sums loaded together): mass after aging, idle slots listed, the
+  // filter dims of the centres after aging and the Gram row terms
+  // (1 - M) |filter dims|^2 - thr, +inf for empty slots and past A
+  {
+    constexpr int QC = FD / 4;  // 16-byte chunks per side
+    for (int k = tid; k < cap32(dm.K); k += MT_THREADS) {
+      float rk = INFINITY, rv = INFINITY;
+      if (k < A) {
+        uint8_t* row = rows + (size_t)k * ROW;
+        uint32_t* mp = reinterpret_cast<uint32_t*>(row + ROW_META);
+        float4 f[2][QC];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) s_c16[k * MT_FD + 8 * lane + q] = n > 0 ? fv[q] / nf : 0.f;
-    }
-    if (lane == 0) {
-      s_n[k] = n;
-      s_dirty[k] = idle ? 1 : 0;
-      if (idle) atomicAdd(&s_cnt[0], 1);
+        for (int q = 0; q < QC; ++q) {
+          f[0][q] = *reinterpret_cast<const float4*>(row + ROW_SUMK + 16 * q);
+          f[1][q] = *reinterpret_cast<const float4*>(row + ROW_SUMV + 16 * q);
+        }
+        const uint32_t n = mp[0];                         // RowMeta::n
+        const int32_t tau = static_cast<int32_t>(mp[7]);  // RowMeta::tau
+        const bool idle = (t - tau / T) > dm.t_idle;
+        uint32_t n2 = n;
+        float r = 1.f;
+        if (idle) {
+          n2 = (uint32_t)floor((1.0 - dm.gamma) * (double)n);
+          r = (float)n2 / (float)n;
+          mp[0] = n2;
+          s_rk[atomicAdd(&s_cnt[0], 1)] = (uint16_t)k;
+        }
+        s_n[k] = n2;
+        s_r[k] = r;
+        s_dirty[k] = idle ? 1 : 0;
+        const float nf = (float)n2;
+        float nrm[2] = {0.f, 0.f};
+#pragma unroll
+        for (int side = 0; side < 2; ++side)
+#pragma unroll
+          for (int q = 0; q < QC; ++q) {
+            const float fv[4] = {f[side][q].x, f[side][q].y, f[side][q].z, f[side][q].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float y = idle ? fv[e] * r : fv[e];
+              const float c = n2 > 0 ? y / nf : 0.f;
+              s_c16[(side * FD + 4 * q + e) * dm.K + k] = c;
+              nrm[side] = fmaf(c, c, nrm[side]);
+            }
+          }
+        if (n2 > 0) {
+          rk = (1.f - MT_GRAM_MARGIN) * nrm[0] - fk2;
+          rv = (1.f - MT_GRAM_MARGIN) * nrm[1] - fv2;
+        }
+      }
+      s_rhk[k] = rk;
+      s_rhv[k] = rv;
     }
   }
   __syncthreads();
+  const int nidle = s_cnt[0];
+  // 1c. idle slots: sums and squared sums scaled by float32(n') / float32(n),
+  // one thread per 16 bytes
+  for (int x = tid; x < nidle * 128; x += MT_THREADS) {
+    const int k = s_rk[x >> 7];
+    float4* pf = reinterpret_cast<float4*>(rows + (size_t)k * ROW + ROW_SUMK) + (x & 127);
+    const float r = s_r[k];
+    const float4 f = *pf;
+    *pf = make_float4(f.x * r, f.y * r, f.z * r, f.w * r);
+  }
 
-  // 2. merging (wave 0)
-  if (wave == 0) {
-    const double ek2 = dm.eps_k * dm.eps_k, ev2 = dm.eps_v * dm.eps_v;
-    const float fk2 = (float)(ek2 * (1.0 + 1e-4));
-    int nmerged = 0;
-    for (int i = 0; i < A; ++i) {
-      if (s_n[i] == 0) continue;  // uniform
-      uint8_t* rowi = rows + (size_t)i * ROW;
-      bool have_ci = false;
-      float2 cik = make_float2(0.f, 0.f), civ = make_float2(0.f, 0.f);  // dims 2l, 2l+1 of c_i, p_i
-      int j0 = i + 1;
-      while (j0 < A) {  // uniform
-        const int j = j0 + lane;
-        bool pass = false;
-        if (j < A && s_n[j] != 0) {
-          float part = 0.f;
+  int nmerged = 0;  // wave 0
+  for (int r0 = 0; r0 < A; r0 += R) {  // uniform
+    const int r1 = min(A, r0 + R);
+    for (int x = tid; x < R * W32 + 2 * RW; x += MT_THREADS) s_adj[x] = 0u;
+    if (tid == 0) s_np = 0;
+    __syncthreads();
+
+    // 2a. filter on MFMA: 32 x 32 tiles (rows ib of the block, columns jb >=
+    // ib) of the Gram matrices of the filter dims, tiles t = wave, wave + W,
+    // ... in row-major order; the pairs that pass are listed
+    {
+      const int col = lane & 31, half = lane >> 5;
+      const int nb = (A + 31) >> 5;
+      // operand of slot s: dims 8 half .. 8 half + 7 of one side, hi + lo
+      auto operand = [&](int s, int side, bf16x8& h, bf16x8& l) {
+        float v[8];
 #pragma unroll
-          for (int d = 0; d < MT_FD; ++d) {
-            const float df = s_c16[i * MT_FD + d] - s_c16[j * MT_FD + d];
-            part = part + df * df;
-          }
-          pass = !(part > fk2);
+        for (int e = 0; e < 8; ++e) {
+          const int d = 8 * half + e;
+          v[e] = d < FD ? s_c16[(side * FD + d) * dm.K + s] : 0.f;
         }
-        const unsigned long long bal = __ballot(pass);
-        if (bal == 0ull) {
-          j0 += 64;
-          continue;
-        }
-        const int jj = j0 + __ffsll((long long)bal) - 1;
-        const uint8_t* rowj = rows + (size_t)jj * ROW;
-        if (!have_ci) {
-          const float ni = (float)s_n[i];
-          const float2 sk = reinterpret_cast<const float2*>(rowi + ROW_SUMK)[lane];
-          const float2 sv = reinterpret_cast<const float2*>(rowi + ROW_SUMV)[lane];
-          cik = make_float2(sk.x / ni, sk.y / ni);
-          civ = make_float2(sv.x / ni, sv.y / ni);
-          have_ci = true;
-        }
-        const float nj = (float)s_n[jj];
-        const float2 tk = reinterpret_cast<const float2*>(rowj + ROW_SUMK)[lane];
-        const float2 tv = reinterpret_cast<const float2*>(rowj + ROW_SUMV)[lane];
-        const float2 cjk = make_float2(tk.x / nj, tk.y / nj), cjv = make_float2(tv.x / nj, tv.y / nj);
-        double dk, dv;
+        split8(v, h, l);
+      };
+      int tc = 0;
+      for (int ib = r0 >> 5; ib < ((r1 + 31) >> 5); ++ib) {  // uniform
+        const int jb0 = ib + ((wave - tc) % MT_WAVES + MT_WAVES) % MT_WAVES;
+        tc += nb - ib;
+        if (jb0 >= nb) continue;
+        bf16x8 akh, akl, avh, avl;
         {
-          const double ax = (double)cik.x - (double)cjk.x, ay = (double)cik.y - (double)cjk.y;
-          const double bx = (double)civ.x - (double)cjv.x, by = (double)civ.y - (double)cjv.y;
-          dk = ax * ax + ay * ay;
-          dv = bx * bx + by * by;
+          const int si = min(ib * 32 + col, A - 1);
+          operand(si, 0, akh, akl);
+          operand(si, 1, avh, avl);
+        }
+        // accumulator element rr is row (rr / 4) * 8 + half * 4 + rr % 4:
+        // its row terms, +inf past the block
+        float rhk[16], rhv[16];
 #pragma unroll
-          for (int o = 32; o >= 1; o >>= 1) {
-            dk = dk + __shfl_xor(dk, o, 64);
-            dv = dv + __shfl_xor(dv, o, 64);
+        for (int q = 0; q < 4; ++q) {
+          const int i0 = ib * 32 + q * 8 + half * 4;
+          const float4 xk = *reinterpret_cast<const float4*>(s_rhk + i0);
+          const float4 xv = *reinterpret_cast<const float4*>(s_rhv + i0);
+          const float ek[4] = {xk.x, xk.y, xk.z, xk.w}, ev[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            rhk[4 * q + r] = i0 + r < r1 ? ek[r] : INFINITY;
+            rhv[4 * q + r] = i0 + r < r1 ? ev[r] : INFINITY;
           }
         }
-        if (dk < ek2 && dv < ev2) {  // uniform
-          // i absorbs jj: lane l adds dims 2l, 2l+1 of the four sums and
-          // histogram words 4l .. 4l+3 (H^K then H^V)
-          float2 x[4];
+        for (int jb = jb0; jb < nb; jb += MT_WAVES) {  // uniform
+          const int j = jb * 32 + col, jc = min(j, A - 1);
+          bf16x8 bkh, bkl, bvh, bvl;
+          operand(jc, 0, bkh, bkl);
+          operand(jc, 1, bvh, bvl);
+          // column terms (1 - M) |b|^2 = row term + thr (+inf past A or empty)
+          const float gck = s_rhk[j] + fk2, gcv = s_rhv[j] + fv2;
+          const bool diag = jb == ib;
+          f32x16 gk = {}, gv = {};
+          gk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(akh, bkh, gk, 0, 0, 0);
+          gv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(avh, bvh, gv, 0, 0, 0);
+          gk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(akh, bkl, gk, 0, 0, 0);
+          gv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(avh, bvl, gv, 0, 0, 0);
+          gk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(akl, bkh, gk, 0, 0, 0);
+          gv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(avl, bvh, gv, 0, 0, 0);
+          // pair (i, j) passes when max(row + column - 2 G) over key and
+          // value is <= 0 (and i < j on the diagonal tile)
+          float e[16], emin = INFINITY;
 #pragma unroll
-          for (int a = 0; a < 4; ++a) {
-            float2* pi = reinterpret_cast<float2*>(rowi + a * 512) + lane;
-            const float2 xi = *pi, xj = reinterpret_cast<const float2*>(rowj + a * 512)[lane];
-            x[a] = make_float2(xi.x + xj.x, xi.y + xj.y);
-            *pi = x[a];
+          for (int rr = 0; rr < 16; ++rr) {
+            const int m = (rr >> 2) * 8 + half * 4 + (rr & 3);
+            const float tk = fmaf(-2.f, gk[rr], rhk[rr] + gck);
+            const float tv = fmaf(-2.f, gv[rr], rhv[rr] + gcv);
+            e[rr] = (diag && m >= col) ? INFINITY : fmaxf(tk, tv);
+            emin = fminf(emin, e[rr]);
           }
-          {
-            uint4* hi = reinterpret_cast<uint4*>(rowi + ROW_HK) + lane;
-            const uint4 h1 = *hi, h2 = reinterpret_cast<const uint4*>(rowj + ROW_HK)[lane];
-            *hi = make_uint4(h1.x + h2.x, h1.y + h2.y, h1.z + h2.z, h1.w + h2.w);
+          if (__ballot(emin <= 0.f) == 0ull) continue;  // uniform
+#pragma unroll
+          for (int rr = 0; rr < 16; ++rr) {
+            const bool pass = e[rr] <= 0.f;
+            const unsigned long long bal = __ballot(pass);
+            if (bal == 0ull) continue;  // uniform
+            int base = 0;
+            if (lane == 0) base = atomicAdd(&s_np, __popcll(bal));
+            base = __shfl(base, 0, 64);
+            const int pos = base + __popcll(bal & below);
+            if (pass) {
+              const int i = ib * 32 + (rr >> 2) * 8 + half * 4 + (rr & 3);
+              if (pos < MT_PAIRS)
+                s_pairs[pos] = ((uint32_t)i << 16) | (uint32_t)j;
+              else
+                atomicOr(&s_ov[(i - r0) >> 5], 1u << ((i - r0) & 31));
+            }
           }
-          const RowMeta mi = *reinterpret_cast<const RowMeta*>(rowi + ROW_META);
-          const RowMeta mj = *reinterpret_cast<const RowMeta*>(rowj + ROW_META);
-          const float wi = (float)mi.n, wj = (float)mj.n, wsum = wi + wj;
-          RowMeta mn = mi;
-          mn.mu_x = ((wi * mi.mu_x) + (wj * mj.mu_x)) / wsum;
-          mn.mu_y = ((wi * mi.mu_y) + (wj * mj.mu_y)) / wsum;
-          mn.n = mi.n + mj.n;
-          mn.n_res = mi.n_res + mj.n_res;
-          if (lane == 0) {
-            *reinterpret_cast<RowMeta*>(rowi + ROW_META) = mn;
-            *reinterpret_cast<uint32_t*>(const_cast<uint8_t*>(rowj) + ROW_META) = 0u;  // RowMeta::n
-            s_n[i] = mn.n;
-            s_n[jj] = 0u;
-            s_dirty[i] = 1;
-          }
-          // i's centre moves
-          const float nn = (float)mn.n;
-          cik = make_float2(x[0].x / nn, x[0].y / nn);
-          civ = make_float2(x[1].x / nn, x[1].y / nn);
-          if (lane < MT_FD / 2) {
-            s_c16[i * MT_FD + 2 * lane] = cik.x;
-            s_c16[i * MT_FD + 2 * lane + 1] = cik.y;
-          }
-          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-          __builtin_amdgcn_wave_barrier();
-          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-          ++nmerged;
         }
-        j0 = jj + 1;
       }
     }
+    __syncthreads();
+
+    // 2b. exact test of the listed pairs: groups of 16 lanes, two pairs
+    // per group in flight
+    {
+      const int np = min(s_np, MT_PAIRS);
+      constexpr int NG = MT_THREADS / 16;  // groups
+      const int grp = tid >> 4, m = tid & 15;
+      for (int p0 = grp; p0 < np; p0 += 2 * NG) {
+        int pi[2], pj[2];
+        bool ok[2];
+        float2 ak[2][4], av[2][4], bk[2][4], bv[2][4];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int p = p0 + NG * h;
+          const uint32_t e = p < np ? s_pairs[p] : 0u;
+          pi[h] = (int)(e >> 16);
+          pj[h] = (int)(e & 0xffffu);
+          ok[h] = p < np;
+          if (ok[h]) ok[h] = !((s_ov[(pi[h] - r0) >> 5] >> ((pi[h] - r0) & 31)) & 1u);  // overflowed: scanned
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            ak[h][r] = av[h][r] = bk[h][r] = bv[h][r] = make_float2(0.f, 0.f);
+          }
+          if (ok[h]) {
+            const float2* xi = reinterpret_cast<const float2*>(rows + (size_t)pi[h] * ROW) + m;
+            const float2* xj = reinterpret_cast<const float2*>(rows + (size_t)pj[h] * ROW) + m;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              ak[h][r] = xi[16 * r];
+              av[h][r] = xi[64 + 16 * r];  // ROW_SUMV = 64 float2
+              bk[h][r] = xj[16 * r];
+              bv[h][r] = xj[64 + 16 * r];
+            }
+          }
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const float ni = ok[h] ? (float)s_n[pi[h]] : 1.f, nj = ok[h] ? (float)s_n[pj[h]] : 1.f;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            ak[h][r] = make_float2(ak[h][r].x / ni, ak[h][r].y / ni);
+            av[h][r] = make_float2(av[h][r].x / ni, av[h][r].y / ni);
+            bk[h][r] = make_float2(bk[h][r].x / nj, bk[h][r].y / nj);
+            bv[h][r] = make_float2(bv[h][r].x / nj, bv[h][r].y / nj);
+          }
+          double dk, dv;
+          mt_dist16(ak[h], av[h], bk[h], bv[h], dk, dv);
+          if (ok[h] && m == 0 && dk < ek2 && dv < ev2) {
+            const int li = pi[h] - r0;
+            atomicOr(&s_adj[li * W32 + (pj[h] >> 5)], 1u << (pj[h] & 31));
+            atomicOr(&s_rf[li >> 5], 1u << (li & 31));
+          }
+        }
+      }
+    }
+    __syncthreads();
+
+    // 2c. merging (wave 0), marked rows ascending
+    if (wave == 0) {
+      for (int w = 0; w < (r1 - r0 + 31) / 32; ++w) {
+        const uint32_t ovw = s_ov[w];
+        uint32_t rword = s_rf[w] | ovw;
+        while (rword != 0u) {  // uniform
+          const int li = w * 32 + __ffs(rword) - 1;
+          rword &= rword - 1u;
+          const int i = r0 + li;
+          if (s_n[i] == 0) continue;  // uniform
+          uint8_t* rowi = rows + (size_t)i * ROW;
+          // scan: pick candidates with the filter (after a merge, or when the
+          // row's pairs overflowed the list); else from the bitmask
+          bool scan = (ovw >> li) & 1u, have_ci = false;
+          float2 cik = make_float2(0.f, 0.f), civ = make_float2(0.f, 0.f);  // dims 2l, 2l+1 of c_i, p_i
+          int j0 = i + 1;
+          while (j0 < A) {  // uniform
+            int jj;
+            if (!scan) {
+              // lowest mark >= j0 of row i (lane l < W32 holds word l)
+              uint32_t wv = lane < W32 ? s_adj[li * W32 + lane] : 0u;
+              const int lo = j0 - lane * 32;
+              if (lo > 0) wv = lo >= 32 ? 0u : (wv & ~((1u << lo) - 1u));
+              const unsigned long long nz = __ballot(wv != 0u);
+              if (nz == 0ull) break;
+              const int wl = __ffsll((long long)nz) - 1;
+              const uint32_t wsel = __shfl(wv, wl, 64);
+              jj = wl * 32 + __ffs(wsel) - 1;
+              if (s_n[jj] == 0) {  // merged away meanwhile
+                j0 = jj + 1;
+                continue;
+              }
+            } else {
+              const int j = j0 + lane;
+              bool pass = false;
+              if (j < A && s_n[j] != 0) {
+                float pk = 0.f, pv = 0.f;
+#pragma unroll
+                for (int d = 0; d < FD; ++d) {
+                  const float dk = s_c16[d * dm.K + i] - s_c16[d * dm.K + j];
+                  const float dv = s_c16[(FD + d) * dm.K + i] - s_c16[(FD + d) * dm.K + j];
+                  pk = pk + dk * dk;
+                  pv = pv + dv * dv;
+                }
+                pass = !(pk > fk2) && !(pv > fv2);
+              }
+              const unsigned long long bal = __ballot(pass);
+              if (bal == 0ull) {
+                j0 += 64;
+                continue;
+              }
+              jj = j0 + __ffsll((long long)bal) - 1;
+            }
+            const uint8_t* rowj = rows + (size_t)jj * ROW;
+            if (!have_ci) {
+              const float ni = (float)s_n[i];
+              const float2 sk = reinterpret_cast<const float2*>(rowi + ROW_SUMK)[lane];
+              const float2 sv = reinterpret_cast<const float2*>(rowi + ROW_SUMV)[lane];
+              cik = make_float2(sk.x / ni, sk.y / ni);
+              civ = make_float2(sv.x / ni, sv.y / ni);
+              have_ci = true;
+            }
+            const float nj = (float)s_n[jj];
+            const float2 tk = reinterpret_cast<const float2*>(rowj + ROW_SUMK)[lane];
+            const float2 tv = reinterpret_cast<const float2*>(rowj + ROW_SUMV)[lane];
+            const float2 cjk = make_float2(tk.x / nj, tk.y / nj), cjv = make_float2(tv.x / nj, tv.y / nj);
+            double dk, dv;
+            {
+              const double ax = (double)cik.x - (double)cjk.x, ay = (double)cik.y - (double)cjk.y;
+              const double bx = (double)civ.x - (double)cjv.x, by = (double)civ.y - (double)cjv.y;
+              dk = ax * ax + ay * ay;
+              dv = bx * bx + by * by;
+#pragma unroll
+              for (int o = 32; o >= 1; o >>= 1) {
+                dk = dk + __shfl_xor(dk, o, 64);
+                dv = dv + __shfl_xor(dv, o, 64);
+              }
+            }
+            if (dk < ek2 && dv < ev2) {  // uniform
+              // i absorbs jj: lane l adds dims 2l, 2l+1 of the four sums and
+              // histogram words 4l .. 4l+3 (H^K then H^V)
+              float2 x[4];
+#pragma unroll
+              for (int a = 0; a < 4; ++a) {
+                float2* pi = reinterpret_cast<float2*>(rowi + a * 512) + lane;
+                const float2 xi = *pi, xj = reinterpret_cast<const float2*>(rowj + a * 512)[lane];
+                x[a] = make_float2(xi.x + xj.x, xi.y + xj.y);
+                *pi = x[a];
+              }
+              {
+                uint4* hi = reinterpret_cast<uint4*>(rowi + ROW_HK) + lane;
+                const uint4 h1 = *hi, h2 = reinterpret_cast<const uint4*>(rowj + ROW_HK)[lane];
+                *hi = make_uint4(h1.x + h2.x, h1.y + h2.y, h1.z + h2.z, h1.w + h2.w);
+              }
+              const RowMeta mi = *reinterpret_cast<const RowMeta*>(rowi + ROW_META);
+              const RowMeta mj = *reinterpret_cast<const RowMeta*>(rowj + ROW_META);
+              const float wi = (float)mi.n, wj = (float)mj.n, wsum = wi + wj;
+              RowMeta mn = mi;
+              mn.mu_x = ((wi * mi.mu_x) + (wj * mj.mu_x)) / wsum;
+              mn.mu_y = ((wi * mi.mu_y) + (wj * mj.mu_y)) / wsum;
+              mn.n = mi.n + mj.n;
+              mn.n_res = mi.n_res + mj.n_res;
+              if (lane == 0) {
+                *reinterpret_cast<RowMeta*>(rowi + ROW_META) = mn;
+                *reinterpret_cast<uint32_t*>(const_cast<uint8_t*>(rowj) + ROW_META) = 0u;  // RowMeta::n
+                s_n[i] = mn.n;
+                s_n[jj] = 0u;
+                s_dirty[i] = 1;
+              }
+              // i's centre moves
+              const float nn = (float)mn.n;
+              cik = make_float2(x[0].x / nn, x[0].y / nn);
+              civ = make_float2(x[1].x / nn, x[1].y / nn);
+              if (lane < FD / 2) {
+                s_c16[(2 * lane) * dm.K + i] = cik.x;
+                s_c16[(2 * lane + 1) * dm.K + i] = cik.y;
+                s_c16[(FD + 2 * lane) * dm.K + i] = civ.x;
+                s_c16[(FD + 2 * lane + 1) * dm.K + i] = civ.y;
+              }
+              __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+              __builtin_amdgcn_wave_barrier();
+              __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+              ++nmerged;
+              scan = true;
+            }
+            j0 = jj + 1;
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // recycling ranks: e-th empty slot in ascending order
+  if (wave == 0) {
     if (lane == 0) s_cnt[1] = nmerged;
-    // recycling ranks: e-th empty slot in ascending order
-    const unsigned long long below = (1ull << lane) - 1ull;
-    int run = 0;
+    // and the worklist of slots to recycle or refresh (in the pair list)
+    int run = 0, nw = 0;
     for (int k0 = 0; k0 < A; k0 += 64) {
       const int k = k0 + lane;
       const bool empty = k < A && s_n[k] == 0;
-      const unsigned long long bal = __ballot(empty);
+      const bool work = k < A && (empty || s_dirty[k] != 0);
+      const unsigned long long bal = __ballot(empty), bw = __ballot(work);
       if (empty) s_rk[k] = (uint16_t)(run + __popcll(bal & below));
+      if (work) s_pairs[nw + __popcll(bw & below)] = (uint32_t)k;
       run += __popcll(bal);
+      nw += __popcll(bw);
     }
-    if (lane == 0) s_cnt[2] = run;
+    if (lane == 0) {
+      s_cnt[2] = run;
+      s_np = nw;
+    }
   }
   __syncthreads();
+  const int nwork = s_np;
 
   // 3. recycling and 4. screening copies
   const int ntok = dm.W * T;
-  for (int k = wave; k < A; k += 4) {  // uniform per wave
+  for (int x = wave; x < nwork; x += MT_WAVES) {  // uniform
+    const int k = __builtin_amdgcn_readfirstlane((int)s_pairs[x]);
     uint8_t* row = rows + (size_t)k * ROW;
     if (s_n[k] == 0) {
       const int e = (int)s_rk[k] % ntok;
@@ -1389,17 +1697,17 @@ __global__ __launch_bounds__(256) void k_maintain(Dims dm, Workspace ws, FoldBat
 }
 
 hipError_t launch_maintain(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
-  const size_t lds = mt_lds_bytes(dm.K);  // <= 145 KiB for K <= MT_KMAX
+  const size_t lds = mt_lds_bytes(dm.K);  // <= 142 KiB for K <= MT_KMAX
+  using KFn = void (*)(Dims, Workspace, FoldBatch);
+  const int fd = mt_fd(dm.K);
+  const KFn fn = dm.kv_fp32 ? (fd == 16 ? k_maintain<1, 16> : fd == 8 ? k_maintain<1, 8> : k_maintain<1, 4>)
+                            : (fd == 16 ? k_maintain<0, 16> : fd == 8 ? k_maintain<0, 8> : k_maintain<0, 4>);
   if (lds > 65536) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(dm.kv_fp32 ? k_maintain<1> : k_maintain<0>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  dim3 grid(fb.n * dm.units);
-  if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_maintain<1>, grid, dim3(256), lds, st, dm, ws, fb);
-  else
-    hipLaunchKernelGGL(k_maintain<0>, grid, dim3(256), lds, st, dm, ws, fb);
+  hipLaunchKernelGGL(fn, dim3(fb.n * dm.units), dim3(MT_THREADS), lds, st, dm, ws, fb);
   return hipGetLastError();
 }
 

@@ -103,15 +103,20 @@ def test_formed_rows_across_s(S):
     h.log(f"readout err formed {w1:.2e} written {w2:.2e}, max diff {np.abs(o1 - o2).max():.2e}")
 
 
-@pytest.mark.parametrize("eps_k,eps_v", [(1.0, 12.0), (1.5, 14.0)])
-def test_maintenance_aging_merging_recycling(eps_k, eps_v):
+# K = 48: one row block, the exactly tested pairs all listed, 16-dim filter;
+# K = 600: 8-dim filter, more filter pairs than the list holds (rows scanned);
+# K = 1100: 4-dim filter, two row blocks (the first overflows, the second
+# merges from its bitmask)
+@pytest.mark.parametrize("eps_k,eps_v,grid,cap", [(1.0, 12.0, 6, 48), (1.5, 14.0, 6, 48),
+                                                  (1.0, 12.0, 4, 600), (1.5, 14.0, 5, 1100)])
+def test_maintenance_aging_merging_recycling(eps_k, eps_v, grid, cap):
     """Prototype maintenance after every fold (T_idle = 2 frames, gamma =
     0.3, merge thresholds that let same-cluster prototypes merge): banks
     bitwise equal to the oracle's after every fold, then the readout."""
     h = H()
-    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=6, grid_w=6,
-                                 frames=14, window_frames=2, capacity=48, query_tokens=4)
-    h.log(f"case: maintenance eps_k={eps_k} eps_v={eps_v} T=36 K=48 W=2")
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=grid, grid_w=grid,
+                                 frames=14, window_frames=2, capacity=cap, query_tokens=4)
+    h.log(f"case: maintenance eps_k={eps_k} eps_v={eps_v} T={grid * grid} K={cap} W=2")
     pair = h.Pair(wl, maintenance=True, t_idle=2, gamma=0.3, eps_k=eps_k, eps_v=eps_v)
     for f in range(wl.frames):
         pair.step()
