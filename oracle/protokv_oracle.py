@@ -30,6 +30,14 @@ in DESIGN.md):
 
 * centres are running means c_k = sumK_k / n_k (the text's "e.g. via EMA"
   and the merge rule's mass-weighted means), not Alg. 1's fixed-rate EMA;
+  with Params.ema the fixed-rate EMA of Alg. 1 is followed instead: the
+  sumK / sumV fields hold the centres c, p themselves, and every absorbed
+  token, in eviction order, sets c <- (1 - alpha) c + alpha K and
+  p <- (1 - beta) p + beta V (float32: one rounding per product and per
+  add, 1 - alpha rounded to float32 first), then codes its residuals
+  K - c, V - p against those updated centres (Alg. 1 updates the centres
+  before R); the screen's cos is unchanged (scale invariant) and synthesis
+  uses c, p directly.  Maintenance is not defined for this mode here;
 * a fold is frame-batched: all non-seed tokens of the evicted frame are
   assigned against the bank as it stands after seeding, then accumulated in
   eviction order (with one token per frame this is Alg. 1's per-token loop);
@@ -131,6 +139,11 @@ class Params:
     gamma: float = TABLE5_DEFAULTS["gamma"]
     eps_k: float = TABLE5_DEFAULTS["eps_K"]
     eps_v: float = TABLE5_DEFAULTS["eps_V"]
+    # Alg. "ProtoKV Streaming Update" literally: fixed-rate EMA centres
+    # (rates used as float32), residuals against the updated centres
+    ema: bool = False
+    alpha: float = TABLE5_DEFAULTS["alpha"]
+    beta: float = TABLE5_DEFAULTS["beta"]
 
     @property
     def tokens_per_frame(self) -> int:
@@ -174,7 +187,7 @@ class Bank:
     def __init__(self, p: Params):
         K, D, G, C = p.capacity, p.head_dim, p.G, p.C
         self.n = np.zeros(K, dtype=np.int64)          # mass n_k (0 = inactive)
-        self.sum_k = np.zeros((K, D), dtype=F32)       # sum of absorbed keys
+        self.sum_k = np.zeros((K, D), dtype=F32)       # sum of absorbed keys (EMA: the centre c)
         self.sum_v = np.zeros((K, D), dtype=F32)
         self.sq_k = np.zeros((K, D), dtype=F32)        # sum of squared keys
         self.sq_v = np.zeros((K, D), dtype=F32)
@@ -324,8 +337,9 @@ def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
     assign[rest] = idx
     margin[rest] = marg
 
-    # Residual codes against the snapshot centres c = f32(sumK / n).
-    if p.use_pq:
+    # Residual codes against the snapshot centres c = f32(sumK / n) (running
+    # means; with EMA centres each token is coded after its own update).
+    if p.use_pq and not p.ema:
         nf = snap.n[idx].astype(F32)[:, None]
         c_snap = (snap.sum_k[idx] / nf).astype(F32)
         p_snap = (snap.sum_v[idx] / nf).astype(F32)
@@ -335,18 +349,31 @@ def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
         codes_v = pq_encode(r_v, codebooks[1])
 
     # Prototype update, tokens in eviction order.
+    al, be = F32(p.alpha), F32(p.beta)
+    ka, kb = F32(one - al), F32(one - be)
     for i, j in enumerate(rest):
         k = idx[i]
         kk, vv = keys[j].astype(F32), values[j].astype(F32)
         bank.n[k] += 1
-        bank.sum_k[k] = (bank.sum_k[k] + kk).astype(F32)
-        bank.sum_v[k] = (bank.sum_v[k] + vv).astype(F32)
+        if p.ema:
+            # c <- (1 - alpha) c + alpha K, p <- (1 - beta) p + beta V
+            bank.sum_k[k] = ((ka * bank.sum_k[k]).astype(F32) + (al * kk).astype(F32)).astype(F32)
+            bank.sum_v[k] = ((kb * bank.sum_v[k]).astype(F32) + (be * vv).astype(F32)).astype(F32)
+        else:
+            bank.sum_k[k] = (bank.sum_k[k] + kk).astype(F32)
+            bank.sum_v[k] = (bank.sum_v[k] + vv).astype(F32)
         bank.sq_k[k] = (bank.sq_k[k] + (kk * kk).astype(F32)).astype(F32)
         bank.sq_v[k] = (bank.sq_v[k] + (vv * vv).astype(F32)).astype(F32)
         if p.use_pq:
+            if p.ema:
+                # residuals against the centres just updated
+                zk = pq_encode((kk - bank.sum_k[k]).astype(F32)[None, :], codebooks[0])[0]
+                zv = pq_encode((vv - bank.sum_v[k]).astype(F32)[None, :], codebooks[1])[0]
+            else:
+                zk, zv = codes_k[i], codes_v[i]
             for g in range(p.G):
-                bank.hist_k[k, g, codes_k[i, g]] += 1
-                bank.hist_v[k, g, codes_v[i, g]] += 1
+                bank.hist_k[k, g, zk[g]] += 1
+                bank.hist_v[k, g, zv[g]] += 1
             bank.n_res[k] += 1
         # spatial state: mu <- (1-eta) mu + eta s, then
         # Sigma <- (1-eta) Sigma + eta (s - mu)(s - mu)^T with the new mu.
@@ -405,6 +432,8 @@ def maintain(bank: Bank, near: Sequence[Tuple[int, np.ndarray, np.ndarray]], t_f
     near: the near window's frames (frame index, K [T][D], V [T][D]), oldest
     first.  Returns counts of aged, merged and recycled slots.
     """
+    if p.ema:
+        raise ValueError("maintenance is defined for running-mean centres only")
     T = p.tokens_per_frame
     A = int((bank.n > 0).sum())
     assert np.all(bank.n[:A] > 0), "active slots form a prefix"
@@ -520,9 +549,12 @@ def synthesize(bank: Bank, codebooks: np.ndarray, p: Params) -> Pseudo:
     for k in range(p.capacity):
         if bank.n[k] == 0:
             continue
-        nf = F32(bank.n[k])
-        c = (bank.sum_k[k] / nf).astype(F32)
-        pv = (bank.sum_v[k] / nf).astype(F32)
+        if p.ema:  # the fields hold the centres
+            c, pv = bank.sum_k[k].copy(), bank.sum_v[k].copy()
+        else:
+            nf = F32(bank.n[k])
+            c = (bank.sum_k[k] / nf).astype(F32)
+            pv = (bank.sum_v[k] / nf).astype(F32)
         if bank.n_res[k] == 0 or not p.use_pq:
             rk = [zero] * p.S
             rv = [zero] * p.S
@@ -575,6 +607,8 @@ class OracleStream:
     """
 
     def __init__(self, p: Params, units: Sequence[int], codebooks: np.ndarray):
+        if p.ema and p.maintenance:
+            raise ValueError("maintenance is defined for running-mean centres only")
         self.p = p
         self.units = list(units)
         self.codebooks = codebooks

@@ -12,11 +12,26 @@ import numpy as np
 import pytest
 
 from oracle import protokv_oracle as O
+from tests import test_oracle_ema as E
 from tests import test_oracle_maintenance as M
 from tests import test_oracle_pins as P
 
 MUTATIONS = [
     # (function, original text, planted mistake, pins expected to catch it)
+    ("fold_frame", "ka, kb = F32(one - al), F32(one - be)", "ka, kb = F32(one - al), F32(one - al)",
+     [E.test_repeated_token_follows_the_geometric_closed_form]),
+    ("fold_frame", "(al * kk).astype(F32)).astype(F32)", "(al * vv).astype(F32)).astype(F32)",
+     [E.test_repeated_token_follows_the_geometric_closed_form]),
+    ("fold_frame", "(kb * bank.sum_v[k]).astype(F32) + (be * vv)", "(kb * bank.sum_v[k]).astype(F32) + (al * vv)",
+     [E.test_repeated_token_follows_the_geometric_closed_form]),
+    ("fold_frame", "zk = pq_encode((kk - bank.sum_k[k])", "zk = pq_encode((kk - F32(0) * bank.sum_k[k])",
+     [E.test_residual_is_taken_after_the_centre_update]),
+    ("fold_frame", "zv = pq_encode((vv - bank.sum_v[k]).astype(F32)[None, :], codebooks[1])",
+     "zv = pq_encode((vv - bank.sum_v[k]).astype(F32)[None, :], codebooks[0])",
+     [E.test_residual_is_taken_after_the_centre_update]),
+    ("synthesize", "c, pv = bank.sum_k[k].copy(), bank.sum_v[k].copy()",
+     "c, pv = (bank.sum_k[k] / F32(bank.n[k])).astype(F32), bank.sum_v[k].copy()",
+     [E.test_synthesis_uses_the_stored_centres]),
     ("assignment_costs", "cost = -cos +", "cost = cos +",
      [P.test_cost_matches_scipy_cosine_and_mahalanobis]),
     ("assignment_costs", "- 2.0 * Bxy[None, :]", "+ 2.0 * Bxy[None, :]",
