@@ -53,6 +53,8 @@ def parse():
     ap.add_argument("--profile-frames", type=int, default=32)
     ap.add_argument("--maintenance", action="store_true",
                     help="fold with prototype maintenance (aging, merging, recycling) after every frame")
+    ap.add_argument("--ema", action="store_true",
+                    help="fixed-rate EMA centres (alpha = beta = 0.05) instead of running means")
     ap.add_argument("--query-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=32)
@@ -61,12 +63,13 @@ def parse():
 
 
 def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0, rows=0, formed=False,
-                      maint=None):
+                      maint=None, ema=False):
     """Bytes the method must move per launch of `kernel` (all units of one stream).
 
     `formed`: the readout forms the pseudo-token rows from the centres, code
     tuples and codebooks as it loads them (no rows in memory).  `maint`: aged,
-    merged and recycled slots per maintenance launch."""
+    merged and recycled slots per maintenance launch.  `ema`: EMA centres, whose
+    residual codes the aggregation computes (the screen only assigns)."""
     U, T, D, K, S = wl.units, wl.tokens_per_frame, wl.head_dim, wl.capacity, cfg.pseudo_per_proto
     b = 4 if wl.kv_dtype == "fp32" else 2
     if kernel == "ring_insert":
@@ -75,13 +78,16 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
         # assignment: evicted keys, the unit's centre cache, assignments
         # written; PQ encoding: evicted values, codebooks, per touched slot
         # its K and V sums (centres) and its two histograms read and written
+        if ema:
+            return U * (T * D * b + K * CACHE_BYTES + T * 4)
         return (U * (2 * T * D * b + K * CACHE_BYTES + T * 4 + CODEBOOK_BYTES)
                 + touched_per_launch * (2 * D * 4 + 2 * HIST_BYTES))
     if kernel == "aggregate":
         # evicted K and V, assignments; per touched slot its sums, sums of
         # squares and meta read and written and its screening copy rewritten
-        return (U * (2 * T * D * b + T * 4)
-                + touched_per_launch * (2 * ROW_STATS_BYTES + CACHE_BYTES))
+        # (EMA centres: also the unit's codebooks and the slot's histograms)
+        return (U * (2 * T * D * b + T * 4 + (CODEBOOK_BYTES if ema else 0))
+                + touched_per_launch * (2 * ROW_STATS_BYTES + CACHE_BYTES + (2 * HIST_BYTES if ema else 0)))
     if kernel == "maintain":
         # every slot's mass, tau and leading fd key and value dims (the LDS
         # filter: 16, 8 or 4 dims as K grows); an aged slot's sums and squares
@@ -223,6 +229,8 @@ def main():
                             kv_dtype=pk.KV_FP32 if wl.kv_dtype == "fp32" else pk.KV_BF16)
     if args.maintenance:
         cfg.flags |= pk.FLAG_MAINTENANCE
+    if args.ema:
+        cfg.flags |= pk.FLAG_EMA_CENTRES
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cb = W.make_codebooks_device(wl)
@@ -286,7 +294,7 @@ def main():
     kernels = {}
     for name, d in kt.items():
         nbytes = algorithmic_bytes(name, wl, cfg, touched_per_launch=touched, n_active=n_active,
-                                   ctx=ctx, rows=rows, formed=formed, maint=maint)
+                                   ctx=ctx, rows=rows, formed=formed, maint=maint, ema=args.ema)
         kernels[name] = {"avg_us": round(d["avg_us"], 3), "launches": d["launches"],
                          "alg_bytes": int(nbytes),
                          "gbs": round(nbytes / (d["avg_us"] * 1e-6) / 1e9, 1) if nbytes else None}
@@ -334,7 +342,7 @@ def main():
     attend_ms = median_ms(lambda: attend(h, 0, qp, tq, op, lp, sp), args.query_reps)
 
     dom_bytes = algorithmic_bytes(dom, wl, cfg, touched_per_launch=touched_live, n_active=n_active,
-                                  ctx=ctx, rows=rows, formed=formed, maint=maint)
+                                  ctx=ctx, rows=rows, formed=formed, maint=maint, ema=args.ema)
     achieved = dom_bytes / (live["avg_us"] * 1e-6) / 1e9
     traffic = recorded_traffic(dom, wl)
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -361,7 +369,8 @@ def main():
                    "q_heads": wl.num_q_heads, "head_dim": wl.head_dim, "tokens_per_frame": T,
                    "window_frames": wl.window_frames, "capacity": wl.capacity,
                    "pseudo_per_proto": cfg.pseudo_per_proto, "query_tokens": tq,
-                   "frames_streamed": lo + args.steps, "maintenance": bool(args.maintenance)},
+                   "frames_streamed": lo + args.steps, "maintenance": bool(args.maintenance),
+                   "centres": "ema" if args.ema else "mean"},
         "fold_tokens_per_s": round(args.steps * T / (ms_fold / 1e3), 1),
         "fold_us_per_frame": round(1e3 * ms_fold / args.steps, 2),
         "query_us_in_region": round(1e3 * ms_query_in_region, 2),

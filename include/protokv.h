@@ -58,7 +58,8 @@ enum { PROTOKV_KV_BF16 = 0, PROTOKV_KV_FP32 = 1 };
 enum {
   PROTOKV_FLAG_PQ = 1u,        /* residual statistics on (off = "w/o residual stats" ablation) */
   PROTOKV_FLAG_MASS_BIAS = 2u, /* log-mass bias on (off = "b_k = 0" ablation) */
-  PROTOKV_FLAG_MAINTENANCE = 4u /* Alg. "Prototype Maintenance" after every fold (capacity <= 2048) */
+  PROTOKV_FLAG_MAINTENANCE = 4u, /* Alg. "Prototype Maintenance" after every fold (capacity <= 2048) */
+  PROTOKV_FLAG_EMA_CENTRES = 8u  /* Alg. "ProtoKV Streaming Update" fixed-rate EMA centres (not with maintenance) */
 };
 
 typedef struct {
@@ -85,11 +86,12 @@ typedef struct {
   double ridge;             /* rho added to Sigma's diagonal in d_Mah */
   double gamma;             /* maintenance: idle mass decay, n <- floor((1 - gamma) n), in [0, 1) */
   double eps_k, eps_v;      /* maintenance: key / value centre merge thresholds (>= 0) */
+  float alpha, beta;        /* PROTOKV_FLAG_EMA_CENTRES: key / value centre EMA rates, in [0, 1] */
 } protokv_config;
 
 /* Table tab:default_config defaults (S=8, lambda_sp=0.1, lambda_idle=0.01,
- * T_idle=120, eta=0.05, G=8, C=16, B=32, gamma=0.05, eps_K=0.20,
- * eps_V=0.25; maintenance off) with the 7B-class shape of one
+ * T_idle=120, eta=0.05, alpha=beta=0.05, G=8, C=16, B=32, gamma=0.05,
+ * eps_K=0.20, eps_V=0.25; maintenance and EMA centres off) with the 7B-class shape of one
  * stream: 28 layers, 4 KV heads, 28 query heads, 14x14 tokens per frame,
  * W=8 frames, K=256, bf16 KV, PQ and mass bias on, eps=1, rho=1e-4.
  * Host only. */
@@ -138,6 +140,13 @@ protokv_status protokv_append_frame(protokv_t h, const int32_t* stream_ids, int3
  * and value centres are closer than eps_k, eps_v (the lower slot absorbs the
  * higher, pairs in ascending order, each merge moving the absorbing centre),
  * and reseeding of emptied slots from the near window's newest tokens.
+ * With PROTOKV_FLAG_EMA_CENTRES the centres follow the fixed-rate EMA of
+ * Alg. "ProtoKV Streaming Update" instead of running means: the bank's key
+ * and value sum fields hold the centres c, p; each absorbed token, in
+ * eviction order, sets c <- (1 - alpha) c + alpha K and p <- (1 - beta) p +
+ * beta V in float32 (one rounding per product and per add, 1 - alpha
+ * rounded first), then its PQ residual codes are taken against the updated
+ * centres (the screen's cosine is unchanged; synthesis uses c, p directly).
  * Invalidates any synthesis.  No-op when nothing is pending. */
 protokv_status protokv_fold(protokv_t h, void* stream);
 
@@ -198,8 +207,8 @@ protokv_status protokv_read_assignments(protokv_t h, int32_t stream_id, int32_t*
 
 /* Bank row layout (bytes) of one prototype slot, PROTOKV_ROW_BYTES each,
  * rows ordered [num_layers][num_kv_heads][capacity]:
- *   0     float32 sum_k[128]      sum of absorbed keys
- *   512   float32 sum_v[128]
+ *   0     float32 sum_k[128]      sum of absorbed keys (EMA centres: the centre c)
+ *   512   float32 sum_v[128]      (EMA centres: the centre p)
  *   1024  float32 sq_k[128]       sum of squared keys
  *   1536  float32 sq_v[128]
  *   2048  uint32  hist_k[8][16]   H^K[g][c] (entries c >= C are 0)

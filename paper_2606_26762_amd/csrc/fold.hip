@@ -813,8 +813,10 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
 
   // PQ codes of the tile's assigned tokens: wave w encodes the 32-token block
   // w / 2 of K (w even) or V; each code bumps its bin of the slot's
-  // histogram (integer counts: the order of the increments does not matter)
-  if (dm.flags & PROTOKV_FLAG_PQ) {
+  // histogram (integer counts: the order of the increments does not matter).
+  // With EMA centres the residuals follow each token's own centre update and
+  // the aggregation codes them.
+  if ((dm.flags & (PROTOKV_FLAG_PQ | PROTOKV_FLAG_EMA_CENTRES)) == PROTOKV_FLAG_PQ) {
     __syncthreads();
     const int blk = wave >> 1, kv = wave & 1;
     const int jq = tile * SCREEN_TOK + blk * 32 + col;
@@ -920,7 +922,10 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
 // tokens in order, TOK_BATCH at a time with all of a batch's loads in flight
 // (mass, sums, sums of squares, residual count, spatial EMA, recency; the
 // screen already counted the PQ codes into the histograms), writes the row
-// back and refreshes the slot's screening copy.
+// back and refreshes the slot's screening copy.  With EMA centres (EMA = 1)
+// the sums are the centres, updated per token at rates alpha, beta, and each
+// token's residuals against its updated centres are coded here (pq_code16)
+// into the slot's histograms, held by the group (two lanes per subspace).
 // ---------------------------------------------------------------------------
 constexpr int AGG_SLOTS = 32;  // slots per workgroup: two per 16-lane group (k0 + g, k0 + g + 16)
 constexpr int AGG_TOK_BYTES = 32768;  // LDS for the workgroup's tokens (64 bf16 or 32 float32 tokens)
@@ -957,14 +962,52 @@ __device__ __forceinline__ void st8f(uint8_t* p, const float (&x)[8]) {
   reinterpret_cast<float4*>(p)[1] = make_float4(x[4], x[5], x[6], x[7]);
 }
 
-template <int FP32>
-__global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int wg_per_unit) {
+// Nearest codeword (ties to the lower index) of one subspace of a residual
+// held by two lanes of a 16-lane group: lane 2g has dims 0..7 of subspace g,
+// lane 2g + 1 dims 8..15.  The float32 distance sum_u (r_u - C[c][u])^2 is
+// accumulated with u ascending, one rounding per operation: lane 2g sums its
+// eight terms, lane 2g + 1 continues from that partial with its own.  cb is
+// the side's codebook [G][CMAX][DP] in LDS.  Returns the code in both lanes.
+__device__ __forceinline__ int pq_code16(const float (&r)[8], const float* cb, int il, int C) {
+  const float* cw = cb + (il >> 1) * CMAX * DP + (il & 1) * 8;
+  float best = INFINITY;
+  int code = 0;
+#pragma unroll 4
+  for (int c = 0; c < CMAX; ++c) {
+    const float4 w0 = *reinterpret_cast<const float4*>(cw + c * DP);
+    const float4 w1 = *reinterpret_cast<const float4*>(cw + c * DP + 4);
+    const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+    float t[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float df = r[e] - w[e];
+      t[e] = df * df;
+    }
+    float acc = t[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) acc = acc + t[e];
+    float full = __shfl_xor(acc, 1, 64);  // lane 2g + 1: the partial of dims 0..7
+#pragma unroll
+    for (int e = 0; e < 8; ++e) full = full + t[e];
+    if (c < C && full < best) {
+      best = full;
+      code = c;
+    }
+  }
+  const int other = __shfl_xor(code, 1, 64);
+  return (il & 1) ? code : other;
+}
+
+template <int FP32, int EMA>
+__global__ __launch_bounds__(256, EMA ? 3 : 4) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int wg_per_unit) {
   __shared__ uint16_t s_asg[TMAX];         // slot of each token (NO_SLOT: seeded / padding)
   __shared__ uint16_t s_tok[TMAX];         // tokens of this workgroup's slots, grouped, eviction order
   __shared__ int s_cnt[AGG_SLOTS];
   __shared__ int s_off[AGG_SLOTS + 1];       // local slot q = group + 16 * pass
   // the workgroup's tokens in list order, [position][K, V][D] KV dtype, when they fit
   __shared__ __attribute__((aligned(16))) uint8_t s_tk[AGG_TOK_BYTES];
+  // EMA centres: the unit's codebooks [K, V][G][CMAX][DP] for the residual codes
+  __shared__ __attribute__((aligned(16))) float s_cb[EMA ? 2 * G * CMAX * DP : 4];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // same XCD placement as the screen (consecutive logical blocks share an
@@ -1022,6 +1065,10 @@ __global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, Fol
   }
   __syncthreads();
   if (s_off[AGG_SLOTS] == 0) return;  // uniform: none of these slots drew a token
+  if (EMA && pq) {
+    const float4* src = reinterpret_cast<const float4*>(ws.codebooks + unit * (2 * G * CMAX * DP));
+    for (int x = tid; x < 2 * G * CMAX * DP / 4; x += 256) reinterpret_cast<float4*>(s_cb)[x] = src[x];
+  }
   int ow[8];
 #pragma unroll
   for (int g = 0; g < 8; ++g) ow[g] = s_off[4 * wave + (g & 3) + 16 * (g >> 2)];
@@ -1060,6 +1107,8 @@ __global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, Fol
   }
   // the first slot's row (loads in flight with the tokens')
   float sk[8], sv[8], qk[8], qv[8];
+  // EMA centres: this lane's histogram bins H[il / 2][8 (il % 2) ..] (K, V)
+  uint4 hk[2], hv[2];
   RowMeta m;
   auto load_row = [&](int q) {
     const uint8_t* row = ws.bank + (unit * dm.K + k0 + q) * ROW;
@@ -1067,8 +1116,15 @@ __global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, Fol
     ld8f(row + ROW_SUMV + il * 32, sv);
     ld8f(row + ROW_SQK + il * 32, qk);
     ld8f(row + ROW_SQV + il * 32, qv);
+    if (EMA && pq) {
+      hk[0] = reinterpret_cast<const uint4*>(row + ROW_HK + il * 32)[0];
+      hk[1] = reinterpret_cast<const uint4*>(row + ROW_HK + il * 32)[1];
+      hv[0] = reinterpret_cast<const uint4*>(row + ROW_HV + il * 32)[0];
+      hv[1] = reinterpret_cast<const uint4*>(row + ROW_HV + il * 32)[1];
+    }
     m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
   };
+  const float ak = dm.alpha, av = dm.beta, a1k = 1.0f - dm.alpha, a1v = 1.0f - dm.beta;
   if (s_off[gi + 1] > s_off[gi]) load_row(gi);
   if (staged) {
     wait_vm<0>();  // this wave's token loads (and its row loads) have landed
@@ -1107,15 +1163,40 @@ __global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, Fol
       for (int e = 0; e < TOK_BATCH; ++e) {
         if (tb + e < t1) {
           const int jj = jb[e];
+          if (EMA) {
+            // c <- (1 - alpha) c + alpha K, p likewise with beta; residuals
+            // against the updated centres, coded into this lane's bins
+            float rk[8], rv[8];
 #pragma unroll
-          for (int d = 0; d < 8; ++d) {
-            const float xk = raw_at<FP32>(kb[e], d), xv = raw_at<FP32>(vb[e], d);
-            sk[d] = sk[d] + xk;
-            sv[d] = sv[d] + xv;
-            qk[d] = qk[d] + xk * xk;
-            qv[d] = qv[d] + xv * xv;
+            for (int d = 0; d < 8; ++d) {
+              const float xk = raw_at<FP32>(kb[e], d), xv = raw_at<FP32>(vb[e], d);
+              sk[d] = a1k * sk[d] + ak * xk;
+              sv[d] = a1v * sv[d] + av * xv;
+              qk[d] = qk[d] + xk * xk;
+              qv[d] = qv[d] + xv * xv;
+              rk[d] = xk - sk[d];
+              rv[d] = xv - sv[d];
+            }
+            if (pq) {
+              const int zk = pq_code16(rk, s_cb, il, dm.C) - 8 * (il & 1);
+              const int zv = pq_code16(rv, s_cb + G * CMAX * DP, il, dm.C) - 8 * (il & 1);
+              hk[0].x += zk == 0; hk[0].y += zk == 1; hk[0].z += zk == 2; hk[0].w += zk == 3;
+              hk[1].x += zk == 4; hk[1].y += zk == 5; hk[1].z += zk == 6; hk[1].w += zk == 7;
+              hv[0].x += zv == 0; hv[0].y += zv == 1; hv[0].z += zv == 2; hv[0].w += zv == 3;
+              hv[1].x += zv == 4; hv[1].y += zv == 5; hv[1].z += zv == 6; hv[1].w += zv == 7;
+              m.n_res += 1;
+            }
+          } else {
+#pragma unroll
+            for (int d = 0; d < 8; ++d) {
+              const float xk = raw_at<FP32>(kb[e], d), xv = raw_at<FP32>(vb[e], d);
+              sk[d] = sk[d] + xk;
+              sv[d] = sv[d] + xv;
+              qk[d] = qk[d] + xk * xk;
+              qv[d] = qv[d] + xv * xv;
+            }
+            if (pq) m.n_res += 1;
           }
-          if (pq) m.n_res += 1;
           float sx, sy;
           token_xy(jj, dm.grid_w, dm.grid_h, sx, sy);
           const float mx = keep * m.mu_x + eta * sx;
@@ -1135,6 +1216,12 @@ __global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, Fol
     st8f(row + ROW_SUMV + il * 32, sv);
     st8f(row + ROW_SQK + il * 32, qk);
     st8f(row + ROW_SQV + il * 32, qv);
+    if (EMA && pq) {
+      reinterpret_cast<uint4*>(row + ROW_HK + il * 32)[0] = hk[0];
+      reinterpret_cast<uint4*>(row + ROW_HK + il * 32)[1] = hk[1];
+      reinterpret_cast<uint4*>(row + ROW_HV + il * 32)[0] = hv[0];
+      reinterpret_cast<uint4*>(row + ROW_HV + il * 32)[1] = hv[1];
+    }
     if (il == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
     refresh_cache16(dm, sk, m, unit, k, ws, il);
     // per-slot count of folds that touched it (owned by this lane group: no atomics)
@@ -1145,10 +1232,11 @@ __global__ __launch_bounds__(256, 4) void k_aggregate(Dims dm, Workspace ws, Fol
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
   const int wpu = (dm.K + AGG_SLOTS - 1) / AGG_SLOTS;
   dim3 grid(fb.n * dm.units * wpu);
-  if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_aggregate<1>, grid, dim3(256), 0, st, dm, ws, fb, wpu);
-  else
-    hipLaunchKernelGGL(k_aggregate<0>, grid, dim3(256), 0, st, dm, ws, fb, wpu);
+  const bool ema = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) != 0;
+  using KFn = void (*)(Dims, Workspace, FoldBatch, int);
+  const KFn fn = dm.kv_fp32 ? (ema ? k_aggregate<1, 1> : k_aggregate<1, 0>)
+                            : (ema ? k_aggregate<0, 1> : k_aggregate<0, 0>);
+  hipLaunchKernelGGL(fn, grid, dim3(256), 0, st, dm, ws, fb, wpu);
   return hipGetLastError();
 }
 

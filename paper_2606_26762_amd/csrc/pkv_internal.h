@@ -59,6 +59,7 @@ struct Dims {
   float eta;
   double lambda_sp, lambda_idle, ridge;
   double gamma, eps_k, eps_v;  // maintenance (PROTOKV_FLAG_MAINTENANCE)
+  float alpha, beta;           // centre EMA rates (PROTOKV_FLAG_EMA_CENTRES)
   int max_rows;    // max query rows per kv head (max_query_tokens * Hq / Hkv)
   int max_splits;  // attention context splits (partials storage)
 };

@@ -97,8 +97,14 @@ protokv_status check_config(const protokv_config* c, std::string& why) {
   if ((int64_t)c->max_query_tokens * (c->num_q_heads / c->num_kv_heads) > MAX_ROWS)
     return uns("max_query_tokens * (num_q_heads/num_kv_heads) above 512");
   if (c->kv_dtype != PROTOKV_KV_BF16 && c->kv_dtype != PROTOKV_KV_FP32) return bad("kv_dtype unknown");
-  if (c->flags & ~(uint32_t)(PROTOKV_FLAG_PQ | PROTOKV_FLAG_MASS_BIAS | PROTOKV_FLAG_MAINTENANCE))
+  if (c->flags & ~(uint32_t)(PROTOKV_FLAG_PQ | PROTOKV_FLAG_MASS_BIAS | PROTOKV_FLAG_MAINTENANCE |
+                             PROTOKV_FLAG_EMA_CENTRES))
     return bad("unknown flag bits");
+  if (c->flags & PROTOKV_FLAG_EMA_CENTRES) {
+    if (!(c->alpha >= 0.f && c->alpha <= 1.f) || !(c->beta >= 0.f && c->beta <= 1.f))
+      return bad("alpha and beta must be in [0, 1]");
+    if (c->flags & PROTOKV_FLAG_MAINTENANCE) return uns("maintenance with EMA centres");
+  }
   if (!(c->eta > 0.f && c->eta < 1.f)) return bad("eta must be in (0, 1)");
   if (c->pq_eps != 1.0f) return uns("pq_eps must be 1");
   if (!(c->lambda_sp >= 0.0) || !(c->lambda_idle >= 0.0) || !std::isfinite(c->lambda_sp) ||
@@ -199,6 +205,8 @@ protokv_status protokv_default_config(protokv_config* c) {
   c->gamma = 0.05;
   c->eps_k = 0.20;
   c->eps_v = 0.25;
+  c->alpha = 0.05f;
+  c->beta = 0.05f;
   return PROTOKV_OK;
 }
 
@@ -260,6 +268,8 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   dm.gamma = c->gamma;
   dm.eps_k = c->eps_k;
   dm.eps_v = c->eps_v;
+  dm.alpha = c->alpha;
+  dm.beta = c->beta;
   dm.max_rows = c->max_query_tokens * (c->num_q_heads / c->num_kv_heads);
   dm.max_splits = MAX_SPLITS;
   uint8_t* b = h->base;

@@ -227,7 +227,8 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
   if (bvalid && q == 0 && nores) out[SMAX] = 1u;
   if (bvalid && centres) {
     // lane q takes float4s q, q + LPB, ...
-    const float nf = (float)m.n;
+    // centre = sum / n (EMA centres: the stored centre, divided by 1)
+    const float nf = (float)m.n, cd = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) ? 1.f : nf;
     const float4* sums = reinterpret_cast<const float4*>(row + (kv ? ROW_SUMV : ROW_SUMK));
     float4* cen = reinterpret_cast<float4*>(ws.pcen + (((size_t)u * dm.K + p) * 2 + kv) * D);
     // every load issued before the first store (the stores may alias them
@@ -237,7 +238,7 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
     for (int i = 0; i < D / 4 / LPB; ++i) v[i] = sums[q + LPB * i];
 #pragma unroll
     for (int i = 0; i < D / 4 / LPB; ++i)
-      cen[q + LPB * i] = make_float4(v[i].x / nf, v[i].y / nf, v[i].z / nf, v[i].w / nf);
+      cen[q + LPB * i] = make_float4(v[i].x / cd, v[i].y / cd, v[i].z / cd, v[i].w / cd);
     if (kv == 0 && q == 0) {
       const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
       ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
@@ -499,7 +500,8 @@ __global__ __launch_bounds__(64) void k_decode(Dims dm, Workspace ws, int sid, i
 
 // Pseudo-tokens: one wave per slot, lane l writes components 2l, 2l+1 of each
 // of the 2S rows: k~_s = kv_dtype(float32(c + r^K_s)), v~_s likewise, with
-// c = float32(sum / n) and r_s = concatenated codewords; bias = log n.
+// c = float32(sum / n) (EMA centres: the stored c) and r_s = concatenated
+// codewords; bias = log n.
 template <int FP32>
 __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int sid, int n_active) {
   const int lane = threadIdx.x & 63;
@@ -533,7 +535,8 @@ __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int 
   const int sh = 4 * (G - 1 - g);
 #pragma unroll
   for (int w = 0; w < 2; ++w) {
-    const float2 c = w ? make_float2(sv.x / nf, sv.y / nf) : make_float2(sk.x / nf, sk.y / nf);
+    const float cd = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) ? 1.f : nf;  // EMA centres are stored
+    const float2 c = w ? make_float2(sv.x / cd, sv.y / cd) : make_float2(sk.x / cd, sk.y / cd);
     const bool nores = w ? nores_v : nores_k;
     const float* cbw = cbk + ((size_t)w * G + g) * CMAX * DP + u16;
     uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * S + (size_t)p * S) * D * es;
@@ -600,8 +603,9 @@ __global__ __launch_bounds__(256) void k_materialize16(Dims dm, Workspace ws, in
   const int sh = 4 * (G - 1 - g);
 #pragma unroll
   for (int w = 0; w < 2; ++w) {
-    const float c[8] = {sr[w][0].x / nf, sr[w][0].y / nf, sr[w][0].z / nf, sr[w][0].w / nf,
-                        sr[w][1].x / nf, sr[w][1].y / nf, sr[w][1].z / nf, sr[w][1].w / nf};
+    const float cd = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) ? 1.f : nf;  // EMA centres are stored
+    const float c[8] = {sr[w][0].x / cd, sr[w][0].y / cd, sr[w][0].z / cd, sr[w][0].w / cd,
+                        sr[w][1].x / cd, sr[w][1].y / cd, sr[w][1].z / cd, sr[w][1].w / cd};
     const float* cbw = cbk + ((size_t)w * G + g) * CMAX * DP + hsub;
     uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * S + (size_t)p * S) * D * 2 + dq * 16;
 #pragma unroll

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "libprotokv.so")
 
 ROW_BYTES = 3200
 KV_BF16, KV_FP32 = 0, 1
-FLAG_PQ, FLAG_MASS_BIAS, FLAG_MAINTENANCE = 1, 2, 4
+FLAG_PQ, FLAG_MASS_BIAS, FLAG_MAINTENANCE, FLAG_EMA_CENTRES = 1, 2, 4, 8
 
 STATUS = {0: "OK", 1: "E_INVALID", 2: "E_UNSUPPORTED", 3: "E_WORKSPACE", 4: "E_STATE", 5: "E_DEVICE"}
 
@@ -51,6 +51,7 @@ class Config(ctypes.Structure):
         ("flags", ctypes.c_uint32), ("eta", ctypes.c_float), ("pq_eps", ctypes.c_float),
         ("lambda_sp", ctypes.c_double), ("lambda_idle", ctypes.c_double), ("ridge", ctypes.c_double),
         ("gamma", ctypes.c_double), ("eps_k", ctypes.c_double), ("eps_v", ctypes.c_double),
+        ("alpha", ctypes.c_float), ("beta", ctypes.c_float),
     ]
 
 

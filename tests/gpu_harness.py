@@ -41,7 +41,7 @@ def oracle_params(wl: W.Workload, **kw) -> O.Params:
 
 def gpu_config(wl: W.Workload, p: O.Params, streams: int = 1, max_query_tokens=None) -> pk.Config:
     flags = ((pk.FLAG_PQ if p.use_pq else 0) | (pk.FLAG_MASS_BIAS if p.mass_bias else 0)
-             | (pk.FLAG_MAINTENANCE if p.maintenance else 0))
+             | (pk.FLAG_MAINTENANCE if p.maintenance else 0) | (pk.FLAG_EMA_CENTRES if p.ema else 0))
     return pk.default_config(
         num_streams=streams, num_layers=wl.num_layers, num_kv_heads=wl.num_kv_heads,
         num_q_heads=wl.num_q_heads, head_dim=wl.head_dim, grid_h=wl.grid_h, grid_w=wl.grid_w,
@@ -50,7 +50,7 @@ def gpu_config(wl: W.Workload, p: O.Params, streams: int = 1, max_query_tokens=N
         max_query_tokens=max_query_tokens or wl.query_tokens,
         kv_dtype=pk.KV_FP32 if wl.kv_dtype == "fp32" else pk.KV_BF16, flags=flags,
         eta=p.eta, lambda_sp=p.lambda_sp, lambda_idle=p.lambda_idle, ridge=p.ridge,
-        gamma=p.gamma, eps_k=p.eps_k, eps_v=p.eps_v)
+        gamma=p.gamma, eps_k=p.eps_k, eps_v=p.eps_v, alpha=p.alpha, beta=p.beta)
 
 
 def assert_bank_equal(gb, u: int, ob: O.Bank, C: int, where: str, bitwise: bool):

@@ -41,6 +41,7 @@ def test_default_config_is_table5():
     assert (c.pseudo_per_proto, c.pq_subspaces, c.pq_codewords, c.beam) == (8, 8, 16, 32)
     assert (c.lambda_sp, c.lambda_idle, c.t_idle) == (0.1, 0.01, 120)
     assert abs(c.eta - 0.05) < 1e-8 and c.pq_eps == 1.0
+    assert abs(c.alpha - 0.05) < 1e-8 and abs(c.beta - 0.05) < 1e-8
     assert c.flags == pk.FLAG_PQ | pk.FLAG_MASS_BIAS
     assert lib_status(c) == 0
 
@@ -52,7 +53,7 @@ def lib_status(c):
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 64, 2), ("num_q_heads", 30, 1), ("num_streams", 0, 1), ("pq_subspaces", 4, 2),
     ("pq_codewords", 17, 2), ("pseudo_per_proto", 17, 2), ("beam", 4, 1), ("capacity", 0, 1),
-    ("window_frames", 0, 1), ("grid_h", 80, 2), ("kv_dtype", 7, 1), ("flags", 8, 1),
+    ("window_frames", 0, 1), ("grid_h", 80, 2), ("kv_dtype", 7, 1), ("flags", 16, 1),
     ("eta", 0.0, 1), ("pq_eps", 0.5, 2), ("ridge", 0.0, 1), ("lambda_sp", -1.0, 1),
     ("max_query_tokens", 100, 2), ("max_query_tokens", 0, 1), ("t_idle", -1, 1),
 ])
@@ -60,6 +61,16 @@ def test_validation_rejects(field, value, status):
     c = pk.default_config(**{field: value})
     assert lib_status(c) == status
     assert pk.lib().protokv_last_error(None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(alpha=1.5), 1), (dict(beta=-0.1), 1), (dict(flags=pk.FLAG_MAINTENANCE), 2), ({}, 0),
+])
+def test_ema_centre_validation(kw, status):
+    """EMA rates must lie in [0, 1]; EMA centres with maintenance are not
+    supported."""
+    flags = pk.FLAG_PQ | pk.FLAG_MASS_BIAS | pk.FLAG_EMA_CENTRES | kw.pop("flags", 0)
+    assert lib_status(pk.default_config(flags=flags, **kw)) == status
 
 
 def test_workspace_size_scales_with_shape():

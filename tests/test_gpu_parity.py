@@ -129,6 +129,28 @@ def test_maintenance_aging_merging_recycling(eps_k, eps_v, grid, cap):
     pair.attend(pair.query(np.random.default_rng(11)), pseudo)
 
 
+@pytest.mark.parametrize("wl_name,alpha,beta", [("7b", 0.05, 0.05), ("tiny", 0.3, 0.7)])
+def test_ema_centres(wl_name, alpha, beta):
+    """Fixed-rate EMA centres (Alg. "ProtoKV Streaming Update" literally):
+    banks bitwise equal to the oracle's after every fold (centres, squared
+    sums, histograms of the residuals coded after each token's update,
+    masses, spatial state), then the synthesized rows and the readout."""
+    h = H()
+    if wl_name == "7b":
+        wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=6, grid_w=6,
+                                     frames=14, window_frames=2, capacity=48, query_tokens=4)
+    else:
+        wl = W.WORKLOADS["tiny"].with_(frames=12)
+    h.log(f"case: EMA centres {wl.name} alpha={alpha} beta={beta} T={wl.tokens_per_frame} K={wl.capacity}")
+    pair = h.Pair(wl, ema=True, alpha=alpha, beta=beta)
+    for f in range(wl.frames):
+        pair.step()
+        if f >= wl.window_frames:
+            pair.check_bank(bitwise=True)
+    pseudo = pair.synthesize()
+    pair.attend(pair.query(np.random.default_rng(13)), pseudo)
+
+
 def test_capacity_limit_gives_exact_attention():
     """K >= evicted tokens: every token keeps its own slot, and the readout is
     exact attention over the full history with far logits shifted by ln S
