@@ -38,6 +38,15 @@ in DESIGN.md):
   K - c, V - p against those updated centres (Alg. 1 updates the centres
   before R); the screen's cos is unchanged (scale invariant) and synthesis
   uses c, p directly.  Maintenance is not defined for this mode here;
+* with Params.rope_theta > 0 the readout applies rotary position
+  embeddings (Sec. 3.3, appendix on the RoPE anchor): keys and queries
+  arrive unrotated; a near token is rotated at its own stream position
+  f * T + j, the S pseudo-keys of prototype k at tau_k, and query token t at
+  P + t with P = (frames appended) * T (the query follows the last frame).
+  The rotation is the rotate-half form: for i < D/2 the pair
+  (x_i, x_(i + D/2)) turns by pos * theta^(-2 i / D), in float64 from the
+  stored values (the prototypes aggregate unrotated keys; values are not
+  rotated);
 * a fold is frame-batched: all non-seed tokens of the evicted frame are
   assigned against the bank as it stands after seeding, then accumulated in
   eviction order (with one token per frame this is Alg. 1's per-token loop);
@@ -144,6 +153,8 @@ class Params:
     ema: bool = False
     alpha: float = TABLE5_DEFAULTS["alpha"]
     beta: float = TABLE5_DEFAULTS["beta"]
+    # rotary positions in the readout (0 = keys and queries used as given)
+    rope_theta: float = 0.0
 
     @property
     def tokens_per_frame(self) -> int:
@@ -164,6 +175,20 @@ def round_kv(x32: np.ndarray, kv_dtype: str) -> np.ndarray:
     lsb = (bits >> 16) & 1
     top = ((bits + 0x7FFF + lsb) >> 16).astype(np.uint32)
     return (top << 16).view(F32)
+
+
+def rope_rotate(x: np.ndarray, pos, theta: float) -> np.ndarray:
+    """Rotary position embedding, rotate-half form, in float64: for i < D/2
+    the pair (x_i, x_(i + D/2)) is turned by the angle pos * theta^(-2 i / D).
+    x [..., D]; pos broadcasts against x's leading axes."""
+    x = np.asarray(x, dtype=np.float64)
+    D = x.shape[-1]
+    h = D // 2
+    inv = float(theta) ** (-2.0 * np.arange(h, dtype=np.float64) / D)
+    ang = np.asarray(pos, dtype=np.float64)[..., None] * inv
+    c, s = np.cos(ang), np.sin(ang)
+    x1, x2 = x[..., :h], x[..., h:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
 def spatial_coords(grid_h: int, grid_w: int) -> np.ndarray:
@@ -646,8 +671,21 @@ class OracleStream:
     def synthesize(self) -> List[Pseudo]:
         return [synthesize(self.banks[u], self.codebooks[u], self.p) for u in range(len(self.units))]
 
+    def near_positions(self, u: int) -> np.ndarray:
+        """Stream positions f * T + j of the near window's tokens, in order."""
+        T = self.p.tokens_per_frame
+        fr = [f for f, _, _ in self.rings[u]]
+        return np.array([f * T + j for f in fr for j in range(T)], dtype=np.int64)
+
     def context(self, u: int, pseudo: Pseudo):
         kn, vn = self.near(u)
+        if self.p.rope_theta > 0:
+            kn = rope_rotate(kn, self.near_positions(u), self.p.rope_theta)
+            pk = rope_rotate(pseudo.keys, self.banks[u].tau[pseudo.slots], self.p.rope_theta)
+            k_ctx = np.concatenate([kn, pk])
+            v_ctx = np.concatenate([vn, pseudo.values])
+            bias = np.concatenate([np.zeros(len(kn)), pseudo.bias])
+            return k_ctx, v_ctx, bias
         k_ctx = np.concatenate([kn, pseudo.keys])
         v_ctx = np.concatenate([vn, pseudo.values])
         bias = np.concatenate([np.zeros(len(kn)), pseudo.bias])
@@ -666,6 +704,9 @@ class OracleStream:
             k_ctx, v_ctx, bias = self.context(ui, pseudo[ui])
             heads = list(range(h * grp, (h + 1) * grp))
             rows = q[l][:, heads, :].reshape(Tq * grp, D)
+            if self.p.rope_theta > 0:
+                P = self.frame * self.p.tokens_per_frame
+                rows = rope_rotate(rows, P + np.repeat(np.arange(Tq), grp), self.p.rope_theta)
             o, z = attend(rows, k_ctx, v_ctx, bias)
             out[l][:, heads, :] = o.reshape(Tq, grp, D)
             lse[l][:, heads] = z.reshape(Tq, grp)

@@ -15,9 +15,16 @@ from oracle import protokv_oracle as O
 from tests import test_oracle_ema as E
 from tests import test_oracle_maintenance as M
 from tests import test_oracle_pins as P
+from tests import test_oracle_rope as R
 
 MUTATIONS = [
     # (function, original text, planted mistake, pins expected to catch it)
+    ("rope_rotate", "x1 * c - x2 * s", "x1 * c + x2 * s",
+     [R.test_rotation_is_complex_multiplication_and_a_block_rotation_matrix]),
+    ("rope_rotate", "(-2.0 * np.arange(h, dtype=np.float64) / D)", "(-1.0 * np.arange(h, dtype=np.float64) / D)",
+     [R.test_rotation_is_complex_multiplication_and_a_block_rotation_matrix]),
+    ("rope_rotate", "x1, x2 = x[..., :h], x[..., h:]", "x1, x2 = x[..., 0::2], x[..., 1::2]",
+     [R.test_rotation_is_complex_multiplication_and_a_block_rotation_matrix]),
     ("fold_frame", "ka, kb = F32(one - al), F32(one - be)", "ka, kb = F32(one - al), F32(one - al)",
      [E.test_repeated_token_follows_the_geometric_closed_form]),
     ("fold_frame", "(al * kk).astype(F32)).astype(F32)", "(al * vv).astype(F32)).astype(F32)",
@@ -132,3 +139,28 @@ def test_stream_eviction_mutation_is_caught(monkeypatch):
     monkeypatch.setattr(O, "OracleStream", ns["OracleStream"])
     with pytest.raises(Exception):
         P.test_capacity_limit_reproduces_exact_attention(1)
+
+
+STREAM_MUTATIONS = [
+    # (original text in OracleStream, planted mistake, pin expected to catch it)
+    ("P + np.repeat(np.arange(Tq), grp)", "np.repeat(np.arange(Tq), grp)",
+     lambda: R.test_capacity_limit_with_rope_is_exact_positional_attention(1)),
+    ("self.banks[u].tau[pseudo.slots]", "self.banks[u].n[pseudo.slots]",
+     lambda: R.test_capacity_limit_with_rope_is_exact_positional_attention(8)),
+    ("f * T + j for f in fr", "f * T for f in fr",
+     lambda: R.test_capacity_limit_with_rope_is_exact_positional_attention(1)),
+]
+
+
+@pytest.mark.parametrize("case", range(len(STREAM_MUTATIONS)))
+def test_stream_readout_mutation_is_caught(case, monkeypatch):
+    """Planted mistakes in the stream's rotary positions (query, pseudo-token
+    anchor, near tokens)."""
+    old, new, pin = STREAM_MUTATIONS[case]
+    src = textwrap.dedent(inspect.getsource(O.OracleStream))
+    assert src.count(old) == 1, old
+    ns = dict(O.__dict__)
+    exec(compile(src.replace(old, new), "<mutant stream>", "exec"), ns)
+    monkeypatch.setattr(O, "OracleStream", ns["OracleStream"])
+    with pytest.raises(Exception):
+        pin()
