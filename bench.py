@@ -55,6 +55,8 @@ def parse():
                     help="fold with prototype maintenance (aging, merging, recycling) after every frame")
     ap.add_argument("--ema", action="store_true",
                     help="fixed-rate EMA centres (alpha = beta = 0.05) instead of running means")
+    ap.add_argument("--rope-theta", type=float, default=0.0,
+                    help="rotary positions in the readout with this base (0 = off)")
     ap.add_argument("--query-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=32)
@@ -99,6 +101,12 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
         return (U * n_active * (8 + 2 * fd * 4) + m.get("aged", 0) * (2 * 4 * D * 4 + CACHE_BYTES)
                 + m.get("merged", 0) * (3 * row + CACHE_BYTES)
                 + m.get("recycled", 0) * (2 * D * b + row + CACHE_BYTES))
+    if kernel == "rope_ring":
+        # the appended frame's keys read and written rotated
+        return U * T * D * b * 2
+    if kernel == "rope_q":
+        # the query read and written rotated
+        return wl.num_layers * wl.query_tokens * wl.num_q_heads * D * b * 2
     if kernel == "decode":
         # histograms, meta, codes out; with formed rows also the sums in and
         # the float32 centres and bias out
@@ -119,9 +127,10 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     return 0
 
 
-FOLD_KERNELS = ("ring_insert", "seed", "screen", "aggregate", "maintain")
+FOLD_KERNELS = ("ring_insert", "seed", "screen", "aggregate", "maintain", "rope_ring")
 KERNEL_SOURCES = {k: "fold.hip" for k in FOLD_KERNELS}  # maintain too
-KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "attend", "attend_merge")})
+KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "attend", "attend_merge", "rope_ring",
+                                                 "rope_q")})
 
 
 def kernel_source_hash(kernel):
@@ -231,6 +240,7 @@ def main():
         cfg.flags |= pk.FLAG_MAINTENANCE
     if args.ema:
         cfg.flags |= pk.FLAG_EMA_CENTRES
+    cfg.rope_theta = args.rope_theta
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cb = W.make_codebooks_device(wl)
@@ -370,7 +380,7 @@ def main():
                    "window_frames": wl.window_frames, "capacity": wl.capacity,
                    "pseudo_per_proto": cfg.pseudo_per_proto, "query_tokens": tq,
                    "frames_streamed": lo + args.steps, "maintenance": bool(args.maintenance),
-                   "centres": "ema" if args.ema else "mean"},
+                   "centres": "ema" if args.ema else "mean", "rope_theta": args.rope_theta},
         "fold_tokens_per_s": round(args.steps * T / (ms_fold / 1e3), 1),
         "fold_us_per_frame": round(1e3 * ms_fold / args.steps, 2),
         "query_us_in_region": round(1e3 * ms_query_in_region, 2),

@@ -87,6 +87,7 @@ typedef struct {
   double gamma;             /* maintenance: idle mass decay, n <- floor((1 - gamma) n), in [0, 1) */
   double eps_k, eps_v;      /* maintenance: key / value centre merge thresholds (>= 0) */
   float alpha, beta;        /* PROTOKV_FLAG_EMA_CENTRES: key / value centre EMA rates, in [0, 1] */
+  double rope_theta;        /* rotary positions in the readout: 0 = off, else the base (> 1) */
 } protokv_config;
 
 /* Table tab:default_config defaults (S=8, lambda_sp=0.1, lambda_idle=0.01,
@@ -125,7 +126,10 @@ protokv_status protokv_destroy(protokv_t h);
  * protokv_fold).
  * stream_ids: host, n distinct stream indices.
  * k, v: device, [n][num_layers][num_kv_heads][T][D] in kv_dtype (bf16 or
- *   float32), row-major; entry i belongs to stream_ids[i].
+ *   float32), row-major; entry i belongs to stream_ids[i].  Keys are
+ *   unrotated; with rope_theta > 0 a copy rotated at each token's stream
+ *   position f * T + j (f = the frame's index in its stream) is kept for
+ *   the readout (the fold uses the unrotated keys).
  * Errors: PROTOKV_E_STATE if a listed stream still has an unfolded eviction. */
 protokv_status protokv_append_frame(protokv_t h, const int32_t* stream_ids, int32_t n,
                                     const void* k, const void* v, void* stream);
@@ -157,7 +161,11 @@ protokv_status protokv_fold(protokv_t h, void* stream);
  * "Pseudo-Token Decoding and Attention").  The buffer holds the top-S code
  * tuples, the biases and the rows themselves, except for bf16 KV with S >= 5:
  * there it holds the float32 centres c_k, p_k instead and protokv_attend
- * forms each row, with the same rounding, as it reads it. */
+ * forms each row, with the same rounding, as it reads it.  With
+ * rope_theta > 0 (Sec. 3.3: the S pseudo-tokens of prototype k share the
+ * rotary position tau_k) the rows are always written, and each pseudo-key,
+ * rounded to kv_dtype, is rotated at tau_k in float32 (angle reduced in
+ * float64) and rounded again. */
 protokv_status protokv_synthesize(protokv_t h, int32_t stream_id, void* stream);
 
 /* Mass-aware readout (Eq. attn_logit): for every layer l, query token t and
@@ -168,7 +176,13 @@ protokv_status protokv_synthesize(protokv_t h, int32_t stream_id, void* stream);
  * o: device [num_layers][tq][num_q_heads][D] in kv_dtype.
  * lse: device float32 [num_layers][tq][num_q_heads] (natural-log
  *   log-sum-exp of the biased logits) or NULL.
- * 1 <= tq <= max_query_tokens. */
+ * 1 <= tq <= max_query_tokens.
+ * With rope_theta > 0 (Sec. 3.3 and the appendix on the RoPE anchor) q is
+ * unrotated and query token t is rotated at stream position P + t, P =
+ * frames appended * T (the query follows the last frame); near keys sit at
+ * their own positions and the pseudo-keys of prototype k at tau_k.  The
+ * rotation is the rotate-half form: for i < D/2 the pair (x_i, x_(i+D/2))
+ * turns by pos * rope_theta^(-2i/D). */
 protokv_status protokv_attend(protokv_t h, int32_t stream_id, const void* q, int32_t tq,
                               void* o, float* lse, void* stream);
 
@@ -249,6 +263,8 @@ enum {
   PROTOKV_K_PQ_ENCODE = 7,       /* reserved: PQ encoding runs inside the screen kernel */
   PROTOKV_K_MATERIALIZE = 8,     /* pseudo-token rows and biases (float32 KV) */
   PROTOKV_K_MAINTAIN = 9,        /* prototype maintenance (PROTOKV_FLAG_MAINTENANCE) */
+  PROTOKV_K_ROPE_RING = 10,      /* rotated copy of appended keys (rope_theta > 0) */
+  PROTOKV_K_ROPE_Q = 11,         /* rotated query (rope_theta > 0) */
   PROTOKV_K_COUNT = 12
 };
 

@@ -60,6 +60,7 @@ struct Dims {
   double lambda_sp, lambda_idle, ridge;
   double gamma, eps_k, eps_v;  // maintenance (PROTOKV_FLAG_MAINTENANCE)
   float alpha, beta;           // centre EMA rates (PROTOKV_FLAG_EMA_CENTRES)
+  double rope_theta;           // rotary positions in the readout (0 = off)
   int max_rows;    // max query rows per kv head (max_query_tokens * Hq / Hkv)
   int max_splits;  // attention context splits (partials storage)
 };
@@ -95,6 +96,10 @@ struct Workspace {
   float* part_ml;             // [units][max_splits][max_rows][2]  (max, sum)
   unsigned long long* counters;  // [16]
   uint32_t* touched;             // [streams][units][K]: folds in which the slot absorbed >= 1 token
+  // rotary positions (rope_theta > 0; otherwise null)
+  uint8_t* ring_kr;              // [streams][units][W+1][T][D] kv dtype: ring_k rotated at f * T + j
+  uint8_t* qrot;                 // [L][max_query_tokens][Hq][D] kv dtype: the query rotated at P + t
+  const double* rope_inv;        // [D/2]: theta^(-2i/D)
 };
 
 enum Counter {
@@ -112,6 +117,7 @@ struct AppendBatch {
   int n;
   int sid[MAXB];
   int slot[MAXB];
+  int frame[MAXB];  // index of the appended frame in its stream
 };
 
 // One pending eviction per entry.
@@ -134,6 +140,7 @@ struct AttendArgs {
   int splits;       // context splits per kv head
   int chunk;        // context tokens per split (multiple of 32)
   int gen;          // bf16: pseudo-token rows are formed from centres, codes and codebooks (else read from pk, pv)
+  const uint8_t* near_k;  // near-window keys: ring_k, or ring_kr with rotary positions
   const void* q;
   void* o;
   float* lse;
@@ -175,5 +182,10 @@ hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& 
                          hipStream_t st);
 hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa,
                                hipStream_t st);
+// rotary positions: the appended frames' keys into ring_kr; the query
+// (tq tokens from q, first position p0) into qrot
+hipError_t launch_rope_ring(const Dims& dm, const Workspace& ws, const AppendBatch& ab, hipStream_t st);
+hipError_t launch_rope_q(const Dims& dm, const Workspace& ws, const void* q, int tq, long long p0,
+                         hipStream_t st);
 
 }  // namespace pkv

@@ -27,7 +27,7 @@ struct StreamState {
 
 struct Layout {
   size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codebooks, cbhn, cbmax;
-  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, total;
+  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, ring_kr, qrot, rope_inv, total;
 };
 
 thread_local std::string g_init_err;
@@ -69,6 +69,10 @@ Layout make_layout(const protokv_config& c) {
   ly.part_ml = take(units * MAX_SPLITS * rows * 2 * 4);
   ly.counters = take(CNT_COUNT * 8);
   ly.touched = take(U * K * 4);
+  const bool rope = c.rope_theta > 0.0;
+  ly.ring_kr = take(rope ? U * (c.window_frames + 1) * T * D * es : 0);
+  ly.qrot = take(rope ? (size_t)c.num_layers * c.max_query_tokens * c.num_q_heads * D * es : 0);
+  ly.rope_inv = take(rope ? (D / 2) * sizeof(double) : 0);
   ly.total = off;
   return ly;
 }
@@ -105,6 +109,8 @@ protokv_status check_config(const protokv_config* c, std::string& why) {
       return bad("alpha and beta must be in [0, 1]");
     if (c->flags & PROTOKV_FLAG_MAINTENANCE) return uns("maintenance with EMA centres");
   }
+  if (!(c->rope_theta == 0.0 || (c->rope_theta > 1.0 && std::isfinite(c->rope_theta))))
+    return bad("rope_theta must be 0 (off) or a finite base > 1");
   if (!(c->eta > 0.f && c->eta < 1.f)) return bad("eta must be in (0, 1)");
   if (c->pq_eps != 1.0f) return uns("pq_eps must be 1");
   if (!(c->lambda_sp >= 0.0) || !(c->lambda_idle >= 0.0) || !std::isfinite(c->lambda_sp) ||
@@ -270,6 +276,7 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   dm.eps_v = c->eps_v;
   dm.alpha = c->alpha;
   dm.beta = c->beta;
+  dm.rope_theta = c->rope_theta;
   dm.max_rows = c->max_query_tokens * (c->num_q_heads / c->num_kv_heads);
   dm.max_splits = MAX_SPLITS;
   uint8_t* b = h->base;
@@ -293,6 +300,10 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.part_ml = (float*)(b + ly.part_ml);
   ws.counters = (unsigned long long*)(b + ly.counters);
   ws.touched = (uint32_t*)(b + ly.touched);
+  const bool rope = c->rope_theta > 0.0;
+  ws.ring_kr = rope ? b + ly.ring_kr : nullptr;
+  ws.qrot = rope ? b + ly.qrot : nullptr;
+  ws.rope_inv = rope ? (const double*)(b + ly.rope_inv) : nullptr;
   h->st.assign(c->num_streams, StreamState());
 
   // codebooks -> [U][2][G][CMAX][DP] with the codeword axis padded to 16
@@ -325,6 +336,12 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
                                           hipMemcpyHostToDevice, hs);
   if (e == hipSuccess) e = hipMemcpyAsync(ws.cbmax, cmax.data(), cmax.size() * sizeof(float),
                                           hipMemcpyHostToDevice, hs);
+  // rotary frequencies theta^(-2i/D) in float64
+  std::vector<double> inv(D / 2);
+  for (int i = 0; i < D / 2; ++i) inv[i] = std::pow(c->rope_theta, -2.0 * i / D);
+  if (e == hipSuccess && ws.rope_inv)
+    e = hipMemcpyAsync(const_cast<double*>(ws.rope_inv), inv.data(), inv.size() * sizeof(double),
+                       hipMemcpyHostToDevice, hs);
   if (e == hipSuccess) e = hipStreamSynchronize(hs);
   if (e != hipSuccess) {
     g_init_err = std::string("init: ") + hipGetErrorString(e);
@@ -364,12 +381,16 @@ protokv_status protokv_append_frame(protokv_t h, const int32_t* ids, int32_t n, 
       const StreamState& ss = h->st[ids[b0 + i]];
       ab.sid[i] = ids[b0 + i];
       ab.slot[i] = (int)(ss.frames % (uint64_t)(h->dm.W + 1));
+      ab.frame[i] = (int)ss.frames;
     }
     protokv_status s = h->dev(h->launch(PROTOKV_K_RING_INSERT, hs, [&] {
                                 return launch_ring_insert(h->dm, h->ws, ab, (const uint8_t*)k + b0 * entry_bytes,
                                                           (const uint8_t*)v + b0 * entry_bytes, hs);
                               }),
                               "append");
+    if (s == PROTOKV_OK && h->ws.ring_kr)
+      s = h->dev(h->launch(PROTOKV_K_ROPE_RING, hs, [&] { return launch_rope_ring(h->dm, h->ws, ab, hs); }),
+                 "append/rope");
     if (s != PROTOKV_OK) return s;
   }
   for (int i = 0; i < n; ++i) {
@@ -445,7 +466,8 @@ protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
   // bf16 with S >= PS_MIN_S: the decode also writes the float32 centres and
   // the readout forms the rows from them as it loads them; otherwise the rows
   // are written here
-  const bool rows = h->dm.kv_fp32 != 0 || h->dm.S < PS_MIN_S;
+  // (with rotary positions the rows are written, pseudo-keys rotated at tau_k)
+  const bool rows = h->dm.kv_fp32 != 0 || h->dm.S < PS_MIN_S || h->ws.ring_kr != nullptr;
   // a slot's residual count is at most the tokens its stream has evicted
   const bool wide = h->st[sid].evicted > 65534u;
   protokv_status s = h->dev(
@@ -480,6 +502,19 @@ protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t t
   aa.gen = h->synth_rows ? 0 : 1;
   aa.tq = tq;
   aa.q = q;
+  aa.near_k = h->ws.ring_k;
+  if (h->ws.ring_kr) {
+    // rotary positions: near keys from the rotated ring, the query rotated
+    // at P + t with P = frames appended * T
+    aa.near_k = h->ws.ring_kr;
+    aa.q = h->ws.qrot;
+    const long long p0 = (long long)ss.frames * T;
+    protokv_status sr = h->dev(
+        h->launch(PROTOKV_K_ROPE_Q, (hipStream_t)stream,
+                  [&] { return launch_rope_q(h->dm, h->ws, q, tq, p0, (hipStream_t)stream); }),
+        "attend/rope");
+    if (sr != PROTOKV_OK) return sr;
+  }
   aa.o = o;
   aa.lse = lse;
   const int ctx = aa.n_near + aa.n_far;

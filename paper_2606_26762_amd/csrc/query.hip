@@ -24,6 +24,24 @@ __device__ __forceinline__ uint16_t q_to_bf16(float x) {
 }
 __device__ __forceinline__ float q_from_bf16(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
+// cos and sin of the rotary angle pos * inv (inv = theta^(-2i/D)): the angle
+// in float64, whole turns taken off in float64, the rest (|r| <= pi) to
+// float32 sincos.  Stream positions reach 10^6 and more, where a float32
+// angle would already be off by tenths of a radian.
+__device__ __forceinline__ void rope_cs(double pos, double inv, float& c, float& s) {
+  const double a = pos * inv;
+  const double turns = rint(a * 0.15915494309189535);  // 1 / (2 pi)
+  const float r = (float)fma(-turns, 6.283185307179586, a);
+  sincosf(r, &s, &c);
+}
+
+// Rotate-half rotation of the pair (x1 = dim i, x2 = dim i + D/2):
+// lo = x1 c - x2 s, hi = x2 c + x1 s (float32, one rounding per operation).
+__device__ __forceinline__ void rope_pair(float x1, float x2, float c, float s, float& lo, float& hi) {
+  lo = x1 * c - x2 * s;
+  hi = x2 * c + x1 * s;
+}
+
 // ---------------------------------------------------------------------------
 // Exact top-S decoding of one PQ histogram.
 //
@@ -518,6 +536,12 @@ __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int 
   const float2 sv = reinterpret_cast<const float2*>(row + ROW_SUMV)[lane];
   const float* cbk = ws.codebooks + unit * (2 * G * CMAX * DP);
   const int g = lane >> 3, u16 = (2 * lane) & 15;
+  // rotary positions: the pseudo-keys turn at tau_k; lane l holds dims 2l,
+  // 2l + 1, pair index 2 (l % 32) + {0, 1}, its partner in lane l ^ 32
+  const bool rope = ws.rope_inv != nullptr;
+  float rc[2] = {1.f, 1.f}, rs[2] = {0.f, 0.f};
+  if (rope)
+    for (int e = 0; e < 2; ++e) rope_cs((double)m.tau, ws.rope_inv[2 * (lane & 31) + e], rc[e], rs[e]);
   if (lane == 0) {
     const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
     ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
@@ -550,6 +574,25 @@ __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int 
           val.x = c.x + cw.x;
           val.y = c.y + cw.y;
         }
+        if (rope && w == 0) {  // rotate the key as rounded to the KV dtype
+          if (!FP32) {
+            val.x = q_from_bf16(q_to_bf16(val.x));
+            val.y = q_from_bf16(q_to_bf16(val.y));
+          }
+          const float px = __shfl_xor(val.x, 32, 64), py = __shfl_xor(val.y, 32, 64);
+          float lo, hi;
+          if (lane < 32) {
+            rope_pair(val.x, px, rc[0], rs[0], lo, hi);
+            val.x = lo;
+            rope_pair(val.y, py, rc[1], rs[1], lo, hi);
+            val.y = lo;
+          } else {
+            rope_pair(px, val.x, rc[0], rs[0], lo, hi);
+            val.x = hi;
+            rope_pair(py, val.y, rc[1], rs[1], lo, hi);
+            val.y = hi;
+          }
+        }
         if (FP32) {
           reinterpret_cast<float2*>(out + (size_t)s2 * D * 4)[lane] = val;
         } else {
@@ -577,6 +620,15 @@ __global__ __launch_bounds__(256) void k_materialize16(Dims dm, Workspace ws, in
   const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
   const float nf = (float)reinterpret_cast<const RowMeta*>(row + ROW_META)->n;
   const uint32_t* codes = ws.pcodes + (((size_t)u * dm.K + p) * 2) * PCW;
+  // rotary positions: the pseudo-keys turn at tau_k; this lane's dims are
+  // pair indices 8 (dq % 8) + e, the partners in lane dq ^ 8
+  const bool rope = ws.rope_inv != nullptr;
+  float rc[8], rs[8];
+  if (rope) {
+    const double tau = (double)reinterpret_cast<const RowMeta*>(row + ROW_META)->tau;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) rope_cs(tau, ws.rope_inv[8 * (dq & 7) + e], rc[e], rs[e]);
+  }
   const float* cbk = ws.codebooks + unit * (2 * G * CMAX * DP);
   if (lane == 0) {
     const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
@@ -622,6 +674,22 @@ __global__ __launch_bounds__(256) void k_materialize16(Dims dm, Workspace ws, in
           v[0] = c[0] + a.x; v[1] = c[1] + a.y; v[2] = c[2] + a.z; v[3] = c[3] + a.w;
           v[4] = c[4] + b.x; v[5] = c[5] + b.y; v[6] = c[6] + b.z; v[7] = c[7] + b.w;
         }
+        if (rope && w == 0) {  // rotate the key as rounded to bf16
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = q_from_bf16(q_to_bf16(v[e]));
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float pv = __shfl_xor(v[e], 8, 64);
+            float lo, hi;
+            if (dq < 8) {
+              rope_pair(v[e], pv, rc[e], rs[e], lo, hi);
+              v[e] = lo;
+            } else {
+              rope_pair(pv, v[e], rc[e], rs[e], lo, hi);
+              v[e] = hi;
+            }
+          }
+        }
         uint4 o;
         o.x = (uint32_t)q_to_bf16(v[0]) | ((uint32_t)q_to_bf16(v[1]) << 16);
         o.y = (uint32_t)q_to_bf16(v[2]) | ((uint32_t)q_to_bf16(v[3]) << 16);
@@ -648,6 +716,105 @@ hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_act
     hipLaunchKernelGGL((k_decode4<16, LPB>), dim3(nblk), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
     if (wide) hipLaunchKernelGGL(k_decode<16>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
   }
+  return hipGetLastError();
+}
+
+// Eight consecutive KV elements at element offset e of `base` as float, and back.
+template <int FP32>
+__device__ __forceinline__ void ld8kv(const uint8_t* base, size_t e, float (&x)[8]) {
+  if (FP32) {
+    const float4 a = reinterpret_cast<const float4*>(base + e * 4)[0];
+    const float4 b = reinterpret_cast<const float4*>(base + e * 4)[1];
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  } else {
+    const uint4 w = *reinterpret_cast<const uint4*>(base + e * 2);
+    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      x[2 * q] = __uint_as_float(ww[q] << 16);
+      x[2 * q + 1] = __uint_as_float(ww[q] & 0xFFFF0000u);
+    }
+  }
+}
+template <int FP32>
+__device__ __forceinline__ void st8kv(uint8_t* base, size_t e, const float (&x)[8]) {
+  if (FP32) {
+    reinterpret_cast<float4*>(base + e * 4)[0] = make_float4(x[0], x[1], x[2], x[3]);
+    reinterpret_cast<float4*>(base + e * 4)[1] = make_float4(x[4], x[5], x[6], x[7]);
+  } else {
+    uint4 o;
+    o.x = (uint32_t)q_to_bf16(x[0]) | ((uint32_t)q_to_bf16(x[1]) << 16);
+    o.y = (uint32_t)q_to_bf16(x[2]) | ((uint32_t)q_to_bf16(x[3]) << 16);
+    o.z = (uint32_t)q_to_bf16(x[4]) | ((uint32_t)q_to_bf16(x[5]) << 16);
+    o.w = (uint32_t)q_to_bf16(x[6]) | ((uint32_t)q_to_bf16(x[7]) << 16);
+    *reinterpret_cast<uint4*>(base + e * 2) = o;
+  }
+}
+
+// Rotates the rows of one token vector: pair indices [8 c, 8 c + 8) (dims
+// 8c.. and D/2 + 8c..) of the row at element offset `e0`, at position pos.
+template <int FP32>
+__device__ __forceinline__ void rope_row8(const uint8_t* src, uint8_t* dst, size_t e0, int c, double pos,
+                                          const double* inv) {
+  float x1[8], x2[8], y1[8], y2[8];
+  ld8kv<FP32>(src, e0 + 8 * c, x1);
+  ld8kv<FP32>(src, e0 + D / 2 + 8 * c, x2);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float cs, sn;
+    rope_cs(pos, inv[8 * c + e], cs, sn);
+    rope_pair(x1[e], x2[e], cs, sn, y1[e], y2[e]);
+  }
+  st8kv<FP32>(dst, e0 + 8 * c, y1);
+  st8kv<FP32>(dst, e0 + D / 2 + 8 * c, y2);
+}
+
+// Rotary copy of the appended frames' keys (ring_k -> ring_kr): thread =
+// (entry, unit, token j, pair block c); position f * T + j.
+template <int FP32>
+__global__ __launch_bounds__(256) void k_rope_ring(Dims dm, Workspace ws, AppendBatch ab) {
+  const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t per = (size_t)dm.units * dm.T * 8;
+  const int e = (int)(gid / per);
+  if (e >= ab.n) return;
+  const size_t r = gid % per;
+  const int c = (int)(r & 7), j = (int)((r >> 3) % dm.T), u = (int)((r >> 3) / dm.T);
+  const size_t unit = (size_t)ab.sid[e] * dm.units + u;
+  const size_t e0 = ((unit * (dm.W + 1) + ab.slot[e]) * dm.T + j) * (size_t)D;
+  rope_row8<FP32>(ws.ring_k, ws.ring_kr, e0, c, (double)ab.frame[e] * dm.T + j, ws.rope_inv);
+}
+
+// The query [L][tq][Hq][D] rotated into qrot: thread = (row, pair block c);
+// token t at position p0 + t.
+template <int FP32>
+__global__ __launch_bounds__(256) void k_rope_q(Dims dm, Workspace ws, const uint8_t* q, int tq, long long p0) {
+  const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t row = gid >> 3;
+  if (row >= (size_t)dm.L * tq * dm.Hq) return;
+  const int c = (int)(gid & 7);
+  const int t = (int)((row / dm.Hq) % tq);
+  rope_row8<FP32>(q, ws.qrot, row * D, c, (double)(p0 + t), ws.rope_inv);
+}
+
+hipError_t launch_rope_ring(const Dims& dm, const Workspace& ws, const AppendBatch& ab, hipStream_t st) {
+  const size_t n = (size_t)ab.n * dm.units * dm.T * 8;
+  const dim3 grid((unsigned)((n + 255) / 256));
+  if (dm.kv_fp32)
+    hipLaunchKernelGGL(k_rope_ring<1>, grid, dim3(256), 0, st, dm, ws, ab);
+  else
+    hipLaunchKernelGGL(k_rope_ring<0>, grid, dim3(256), 0, st, dm, ws, ab);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_q(const Dims& dm, const Workspace& ws, const void* q, int tq, long long p0,
+                         hipStream_t st) {
+  const size_t n = (size_t)dm.L * tq * dm.Hq * 8;
+  const dim3 grid((unsigned)((n + 255) / 256));
+  const uint8_t* qb = static_cast<const uint8_t*>(q);
+  if (dm.kv_fp32)
+    hipLaunchKernelGGL(k_rope_q<1>, grid, dim3(256), 0, st, dm, ws, qb, tq, p0);
+  else
+    hipLaunchKernelGGL(k_rope_q<0>, grid, dim3(256), 0, st, dm, ws, qb, tq, p0);
   return hipGetLastError();
 }
 
@@ -687,7 +854,7 @@ __device__ __forceinline__ CtxRef ctx_key(const Dims& dm, const Workspace& ws, c
     const int f = aa.f_first + idx / dm.T;
     const int tok = idx - (idx / dm.T) * dm.T;
     const int slot = f % (dm.W + 1);
-    r.base = (values ? ws.ring_v : ws.ring_k) + (((unit * (dm.W + 1) + slot) * dm.T + tok) * (size_t)D) * ES;
+    r.base = (values ? ws.ring_v : aa.near_k) + (((unit * (dm.W + 1) + slot) * dm.T + tok) * (size_t)D) * ES;
   } else {
     const int row = idx - aa.n_near;
     r.base = (values ? ws.pv : ws.pk) + (((size_t)u * dm.K * dm.S + row) * (size_t)D) * ES;
@@ -791,7 +958,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
       const int fo = pos / dm.T;
       const int slot = (aa.f_first + fo) % (dm.W + 1);
       const size_t off = (((unit * (dm.W + 1) + slot) * dm.T + (pos - fo * dm.T)) * (size_t)D) * 2;
-      kp = ws.ring_k + off;
+      kp = aa.near_k + off;
       vp = ws.ring_v + off;
     } else {
       const int prow = pos - aa.n_near;

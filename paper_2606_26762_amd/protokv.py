@@ -30,7 +30,7 @@ EXPORTED = [
 ]
 
 KERNELS = ["ring_insert", "seed", "screen", "aggregate", "decode", "attend", "attend_merge", "pq_encode",
-           "materialize", "maintain"]
+           "materialize", "maintain", "rope_ring", "rope_q"]
 
 
 class ProtoKVError(RuntimeError):
@@ -51,7 +51,7 @@ class Config(ctypes.Structure):
         ("flags", ctypes.c_uint32), ("eta", ctypes.c_float), ("pq_eps", ctypes.c_float),
         ("lambda_sp", ctypes.c_double), ("lambda_idle", ctypes.c_double), ("ridge", ctypes.c_double),
         ("gamma", ctypes.c_double), ("eps_k", ctypes.c_double), ("eps_v", ctypes.c_double),
-        ("alpha", ctypes.c_float), ("beta", ctypes.c_float),
+        ("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("rope_theta", ctypes.c_double),
     ]
 
 

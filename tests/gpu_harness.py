@@ -50,7 +50,7 @@ def gpu_config(wl: W.Workload, p: O.Params, streams: int = 1, max_query_tokens=N
         max_query_tokens=max_query_tokens or wl.query_tokens,
         kv_dtype=pk.KV_FP32 if wl.kv_dtype == "fp32" else pk.KV_BF16, flags=flags,
         eta=p.eta, lambda_sp=p.lambda_sp, lambda_idle=p.lambda_idle, ridge=p.ridge,
-        gamma=p.gamma, eps_k=p.eps_k, eps_v=p.eps_v, alpha=p.alpha, beta=p.beta)
+        gamma=p.gamma, eps_k=p.eps_k, eps_v=p.eps_v, alpha=p.alpha, beta=p.beta, rope_theta=p.rope_theta)
 
 
 def assert_bank_equal(gb, u: int, ob: O.Bank, C: int, where: str, bitwise: bool):
@@ -317,7 +317,19 @@ class Pair:
             ps = pseudo[i]
             n = len(ps.keys)
             assert n == int((self.oracle[stream].banks[i].n > 0).sum()) * S
-            assert np.array_equal(gk[u][:n], ps.keys), f"unit {u}: pseudo keys differ"
+            if self.p.rope_theta > 0:
+                # keys rotated at tau_k: float32 on the GPU, float64 in the
+                # oracle, so within one unit of the KV dtype's last place
+                # (plus cancellation inside a rotated pair)
+                tau = self.oracle[stream].banks[i].tau[ps.slots]
+                want = O.round_kv(O.rope_rotate(ps.keys, tau, self.p.rope_theta).astype(np.float32),
+                                  self.p.kv_dtype).astype(np.float64)
+                ulp = 2.0 ** -7 if self.p.kv_dtype == "bf16" else 2.0 ** -22
+                tol = ulp * np.abs(want) + 2.0 ** -20 * np.linalg.norm(want, axis=1, keepdims=True)
+                err = np.abs(gk[u][:n].astype(np.float64) - want)
+                assert np.all(err <= tol), f"unit {u}: rotated pseudo keys differ by {np.max(err - tol)} beyond tol"
+            else:
+                assert np.array_equal(gk[u][:n], ps.keys), f"unit {u}: pseudo keys differ"
             assert np.array_equal(gv[u][:n], ps.values), f"unit {u}: pseudo values differ"
             slots = ps.slots[::S]
             assert np.allclose(gbias[u][slots], ps.bias[::S], rtol=1e-6, atol=1e-6)

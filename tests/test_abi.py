@@ -56,6 +56,7 @@ def lib_status(c):
     ("window_frames", 0, 1), ("grid_h", 80, 2), ("kv_dtype", 7, 1), ("flags", 16, 1),
     ("eta", 0.0, 1), ("pq_eps", 0.5, 2), ("ridge", 0.0, 1), ("lambda_sp", -1.0, 1),
     ("max_query_tokens", 100, 2), ("max_query_tokens", 0, 1), ("t_idle", -1, 1),
+    ("rope_theta", 0.5, 1), ("rope_theta", -1.0, 1), ("rope_theta", float("inf"), 1),
 ])
 def test_validation_rejects(field, value, status):
     c = pk.default_config(**{field: value})

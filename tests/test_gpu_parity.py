@@ -151,6 +151,38 @@ def test_ema_centres(wl_name, alpha, beta):
     pair.attend(pair.query(np.random.default_rng(13)), pseudo)
 
 
+@pytest.mark.parametrize("wl_name,theta,grid", [("7b", 1e4, 6), ("7b", 1e6, 6), ("7b", 1e4, 24), ("tiny", 1e4, 8)])
+def test_rope_readout(wl_name, theta, grid):
+    """Rotary positions in the readout: near keys at their stream positions,
+    the pseudo-keys of prototype k at tau_k, query token t at frames*T + t.
+    Rows (rotated keys within one unit in the last place) and readout
+    (abs 2e-2) against the oracle's float64 rotation."""
+    h = H()
+    if wl_name == "7b":
+        wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=grid, grid_w=grid,
+                                     frames=12, window_frames=2, capacity=48, query_tokens=4)
+    else:
+        wl = W.WORKLOADS["tiny"].with_(frames=10)
+    h.log(f"case: RoPE {wl.name} theta={theta} T={wl.tokens_per_frame} K={wl.capacity}")
+    pair = h.Pair(wl, rope_theta=theta)
+    for f in range(wl.frames):
+        pair.step()
+    pseudo = pair.synthesize()
+    q = pair.query(np.random.default_rng(17))
+    worst, go, _ = pair.attend(q, pseudo)
+    # the rotation is visible at this tolerance: the unrotated readout of
+    # the same bank is far from the GPU's
+    st = pair.oracle[0]
+    st.p.rope_theta = 0.0
+    try:
+        plain, _ = st.attend(q, wl.num_kv_heads, pseudo)
+    finally:
+        st.p.rope_theta = theta
+    gap = max(float(np.abs(go[u // wl.num_kv_heads] - plain[u // wl.num_kv_heads]).max()) for u in pair.sample)
+    h.log(f"readout abs err {worst:.2e}, distance from the unrotated readout {gap:.2e}")
+    assert gap > 3 * h.READOUT_ATOL
+
+
 def test_capacity_limit_gives_exact_attention():
     """K >= evicted tokens: every token keeps its own slot, and the readout is
     exact attention over the full history with far logits shifted by ln S
