@@ -38,6 +38,15 @@ in DESIGN.md):
   K - c, V - p against those updated centres (Alg. 1 updates the centres
   before R); the screen's cos is unchanged (scale invariant) and synthesis
   uses c, p directly.  Maintenance is not defined for this mode here;
+* with Params.warm_frames > 0 the codebooks are learned from the stream
+  (appendix "PQ codebook initialization", T_warm not given): the first
+  warm_frames folds count no PQ codes (histograms and n_res stay 0) and
+  append their non-seed tokens' residuals against the snapshot centres, in
+  eviction order, to a reservoir of at most warm_tokens per (layer, kv
+  head); after the last of them, mini-batch k-means (minibatch_kmeans: per-
+  centre rates 1/count, batches of consecutive reservoir rows, centres
+  started from rows i * floor(N / C)) learns each subspace's codebook
+  separately for keys and values, fixed thereafter;
 * with Params.rope_theta > 0 the readout applies rotary position
   embeddings (Sec. 3.3, appendix on the RoPE anchor): keys and queries
   arrive unrotated; a near token is rotated at its own stream position
@@ -155,6 +164,13 @@ class Params:
     beta: float = TABLE5_DEFAULTS["beta"]
     # rotary positions in the readout (0 = keys and queries used as given)
     rope_theta: float = 0.0
+    # PQ codebook warm-up: the first warm_frames folds collect residuals (no
+    # PQ counts), then mini-batch k-means learns the codebooks (0 = off: the
+    # given codebooks are used from the start)
+    warm_frames: int = 0
+    warm_tokens: int = 1024      # reservoir capacity per (layer, kv head)
+    kmeans_epochs: int = 4
+    kmeans_batch: int = 64
 
     @property
     def tokens_per_frame(self) -> int:
@@ -315,10 +331,13 @@ class FoldResult:
     assign: np.ndarray      # slot per evicted token (seeded tokens: their slot)
     margin: np.ndarray      # top-2 cost margin (inf for seeded tokens)
     n_seed: int
+    # with collect=True: key and value residuals of the non-seed tokens in
+    # eviction order, against the snapshot centres
+    residuals: Optional[Tuple[np.ndarray, np.ndarray]] = None
 
 
 def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
-               t_frame: int, p: Params, codebooks: np.ndarray) -> FoldResult:
+               t_frame: int, p: Params, codebooks: np.ndarray, collect: bool = False) -> FoldResult:
     """Absorb the evicted frame f_evicted (tokens j = 0..T-1 in raster order)
     into `bank` (modified in place).  t_frame is the frame being appended.
 
@@ -352,7 +371,9 @@ def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
         bank.tau[k] = pos[j]
         assign[j] = k
     if n_seed == T:
-        return FoldResult(assign, margin, n_seed)
+        D = keys.shape[1]
+        empty = (np.zeros((0, D), F32), np.zeros((0, D), F32)) if collect else None
+        return FoldResult(assign, margin, n_seed, empty)
 
     # Assignment (Eq. 1) of the remaining tokens against the post-seed bank.
     snap = bank.copy()
@@ -364,12 +385,13 @@ def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
 
     # Residual codes against the snapshot centres c = f32(sumK / n) (running
     # means; with EMA centres each token is coded after its own update).
-    if p.use_pq and not p.ema:
+    if (p.use_pq or collect) and not p.ema:
         nf = snap.n[idx].astype(F32)[:, None]
         c_snap = (snap.sum_k[idx] / nf).astype(F32)
         p_snap = (snap.sum_v[idx] / nf).astype(F32)
         r_k = (keys[rest].astype(F32) - c_snap).astype(F32)
         r_v = (values[rest].astype(F32) - p_snap).astype(F32)
+    if p.use_pq and not p.ema:
         codes_k = pq_encode(r_k, codebooks[0])
         codes_v = pq_encode(r_v, codebooks[1])
 
@@ -412,7 +434,53 @@ def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
         bank.sigma[k, 1] = F32(F32(keep * sxy) + F32(eta * F32(ddx * ddy)))
         bank.sigma[k, 2] = F32(F32(keep * syy) + F32(eta * F32(ddy * ddy)))
         bank.tau[k] = pos[j]
-    return FoldResult(assign, margin, n_seed)
+    return FoldResult(assign, margin, n_seed, (r_k, r_v) if collect else None)
+
+
+# ---------------------------------------------------------------------------
+# PQ codebook initialization: mini-batch k-means on a warm-up reservoir
+# ---------------------------------------------------------------------------
+
+
+def minibatch_kmeans(x: np.ndarray, centres: np.ndarray, epochs: int, batch: int) -> np.ndarray:
+    """Mini-batch k-means with per-centre rates 1/count on float32 rows
+    x [N][d], from the float32 centres [C][d].  `epochs` passes over x in
+    order, in batches of `batch` consecutive rows (the last one shorter):
+    each row of a batch is assigned to its nearest centre as the batch
+    starts (pq_encode's float32 sequential distance, ties to the lowest
+    index), then the batch's rows update their centres in row order:
+    count += 1, eta = 1 / count, c <- (1 - eta) c + eta x (float32, one
+    rounding per operation).  Counts persist across batches and epochs."""
+    c = np.array(centres, dtype=F32)
+    count = np.zeros(c.shape[0], dtype=np.int64)
+    one = F32(1.0)
+    for _ in range(epochs):
+        for b0 in range(0, len(x), batch):
+            xb = x[b0:b0 + batch].astype(F32)
+            z = pq_encode(xb, c[None])[:, 0]
+            for i, k in enumerate(z):
+                count[k] += 1
+                eta = F32(one / F32(count[k]))
+                c[k] = ((F32(one - eta) * c[k]).astype(F32) + (eta * xb[i]).astype(F32)).astype(F32)
+    return c
+
+
+def learn_codebooks(res_k: np.ndarray, res_v: np.ndarray, codebooks: np.ndarray, p: Params) -> np.ndarray:
+    """Codebooks [2][G][C][D/G] learned from a reservoir of N residuals per
+    side, separately per subspace and per side, each k-means started from
+    the reservoir entries i * floor(N / C), i < C.  With fewer than C
+    residuals the given codebooks are kept."""
+    out = np.array(codebooks, dtype=F32)
+    G, C, Dp = out.shape[1:]
+    N = len(res_k)
+    if N < C:
+        return out
+    for side, res in enumerate((res_k, res_v)):
+        for g in range(G):
+            xg = res[:, g * Dp:(g + 1) * Dp].astype(F32)
+            init = xg[np.arange(C) * (N // C)]
+            out[side, g] = minibatch_kmeans(xg, init, p.kmeans_epochs, p.kmeans_batch)
+    return out
 
 
 # ---------------------------------------------------------------------------
@@ -634,9 +702,14 @@ class OracleStream:
     def __init__(self, p: Params, units: Sequence[int], codebooks: np.ndarray):
         if p.ema and p.maintenance:
             raise ValueError("maintenance is defined for running-mean centres only")
+        if p.ema and p.warm_frames > 0:
+            raise ValueError("the codebook warm-up collects running-mean residuals only")
         self.p = p
+        self.folds = 0          # folds done (the first warm_frames collect residuals)
+        D = p.head_dim
+        self.reservoir = [(np.zeros((0, D), F32), np.zeros((0, D), F32)) for _ in units]
         self.units = list(units)
-        self.codebooks = codebooks
+        self.codebooks = np.array(codebooks, dtype=F32)  # own copy: the warm-up rewrites it
         self.banks = [Bank(p) for _ in self.units]
         self.rings: List[collections.deque] = [collections.deque() for _ in self.units]
         self.frame = 0          # frames appended so far
@@ -651,12 +724,26 @@ class OracleStream:
             self.rings[u].append((t, keys[u].astype(F32), values[u].astype(F32)))
         if len(self.rings[0]) > self.p.window_frames:
             results = []
+            warm = self.folds < self.p.warm_frames
             for u in range(len(self.units)):
                 fe, ke, ve = self.rings[u].popleft()
-                results.append(fold_frame(self.banks[u], ke, ve, fe, t, self.p,
-                                          self.codebooks[u]))
+                if warm:
+                    # warm-up fold: no PQ counts; residuals into the reservoir
+                    r = fold_frame(self.banks[u], ke, ve, fe, t, dataclasses.replace(self.p, use_pq=False),
+                                   self.codebooks[u], collect=True)
+                    room = self.p.warm_tokens - len(self.reservoir[u][0])
+                    rk, rv = r.residuals
+                    self.reservoir[u] = (np.concatenate([self.reservoir[u][0], rk[:room]]),
+                                         np.concatenate([self.reservoir[u][1], rv[:room]]))
+                    results.append(r)
+                else:
+                    results.append(fold_frame(self.banks[u], ke, ve, fe, t, self.p, self.codebooks[u]))
                 if self.p.maintenance:
                     maintain(self.banks[u], self.rings[u], t, self.p)
+            self.folds += 1
+            if warm and self.folds == self.p.warm_frames:
+                for u in range(len(self.units)):
+                    self.codebooks[u] = learn_codebooks(*self.reservoir[u], self.codebooks[u], self.p)
             self.evicted += self.p.tokens_per_frame
         self.frame += 1
         return results

@@ -16,9 +16,20 @@ from tests import test_oracle_ema as E
 from tests import test_oracle_maintenance as M
 from tests import test_oracle_pins as P
 from tests import test_oracle_rope as R
+from tests import test_oracle_warmup as WU
 
 MUTATIONS = [
     # (function, original text, planted mistake, pins expected to catch it)
+    ("minibatch_kmeans", "eta = F32(one / F32(count[k]))", "eta = F32(0.5)",
+     [WU.test_single_centre_tracks_the_running_mean]),
+    ("minibatch_kmeans", "c[k] = ((F32(one - eta) * c[k])", "c[k] = ((F32(one + eta) * c[k])",
+     [WU.test_single_centre_tracks_the_running_mean]),
+    ("learn_codebooks", "init = xg[np.arange(C) * (N // C)]", "init = xg[np.arange(C)]",
+     [WU.test_learned_codebooks_recover_each_subspace_and_side]),
+    ("learn_codebooks", "xg = res[:, g * Dp:(g + 1) * Dp]", "xg = res[:, g:g + Dp]",
+     [WU.test_learned_codebooks_recover_each_subspace_and_side]),
+    ("learn_codebooks", "for side, res in enumerate((res_k, res_v)):", "for side, res in enumerate((res_k, res_k)):",
+     [WU.test_learned_codebooks_recover_each_subspace_and_side]),
     ("rope_rotate", "x1 * c - x2 * s", "x1 * c + x2 * s",
      [R.test_rotation_is_complex_multiplication_and_a_block_rotation_matrix]),
     ("rope_rotate", "(-2.0 * np.arange(h, dtype=np.float64) / D)", "(-1.0 * np.arange(h, dtype=np.float64) / D)",
@@ -143,6 +154,9 @@ def test_stream_eviction_mutation_is_caught(monkeypatch):
 
 STREAM_MUTATIONS = [
     # (original text in OracleStream, planted mistake, pin expected to catch it)
+    ("dataclasses.replace(self.p, use_pq=False)", "self.p",
+     WU.test_warmup_folds_count_no_codes_and_fill_the_reservoir),
+    ("rk[:room]]", "rk[:room][::-1]]", WU.test_reservoir_residuals_use_the_pre_fold_centres),
     ("P + np.repeat(np.arange(Tq), grp)", "np.repeat(np.arange(Tq), grp)",
      lambda: R.test_capacity_limit_with_rope_is_exact_positional_attention(1)),
     ("self.banks[u].tau[pseudo.slots]", "self.banks[u].n[pseudo.slots]",
