@@ -57,6 +57,9 @@ def parse():
                     help="fixed-rate EMA centres (alpha = beta = 0.05) instead of running means")
     ap.add_argument("--rope-theta", type=float, default=0.0,
                     help="rotary positions in the readout with this base (0 = off)")
+    ap.add_argument("--warm-frames", type=int, default=0,
+                    help="PQ codebook warm-up folds (0 = given codebooks); 57..88 puts its end inside "
+                         "the profile pass with the default warm-up and profile frames")
     ap.add_argument("--query-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=32)
@@ -104,6 +107,13 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     if kernel == "rope_ring":
         # the appended frame's keys read and written rotated
         return U * T * D * b * 2
+    if kernel == "warm_collect":
+        # per non-seed token: its K and V, its slot's two sums, the two
+        # residual rows written
+        return U * T * (2 * D * b + 2 * D * 4 + 2 * D * 4)
+    if kernel == "warm_kmeans":
+        # every reservoir row read once per epoch, the codebooks written
+        return U * (cfg.kmeans_epochs * 2 * cfg.warm_tokens * D * 4 + CODEBOOK_BYTES)
     if kernel == "rope_q":
         # the query read and written rotated
         return wl.num_layers * wl.query_tokens * wl.num_q_heads * D * b * 2
@@ -127,10 +137,12 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     return 0
 
 
-FOLD_KERNELS = ("ring_insert", "seed", "screen", "aggregate", "maintain", "rope_ring")
+FOLD_KERNELS = ("ring_insert", "seed", "screen", "aggregate", "maintain", "rope_ring", "warm_collect",
+                "warm_kmeans")
 KERNEL_SOURCES = {k: "fold.hip" for k in FOLD_KERNELS}  # maintain too
 KERNEL_SOURCES.update({k: "query.hip" for k in ("decode", "materialize", "attend", "attend_merge", "rope_ring",
                                                  "rope_q")})
+KERNEL_SOURCES.update({k: "warmup.hip" for k in ("warm_collect", "warm_kmeans")})
 
 
 def kernel_source_hash(kernel):
@@ -241,6 +253,7 @@ def main():
     if args.ema:
         cfg.flags |= pk.FLAG_EMA_CENTRES
     cfg.rope_theta = args.rope_theta
+    cfg.warm_frames = args.warm_frames
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cb = W.make_codebooks_device(wl)
@@ -380,7 +393,8 @@ def main():
                    "window_frames": wl.window_frames, "capacity": wl.capacity,
                    "pseudo_per_proto": cfg.pseudo_per_proto, "query_tokens": tq,
                    "frames_streamed": lo + args.steps, "maintenance": bool(args.maintenance),
-                   "centres": "ema" if args.ema else "mean", "rope_theta": args.rope_theta},
+                   "centres": "ema" if args.ema else "mean", "rope_theta": args.rope_theta,
+                   "warm_frames": args.warm_frames},
         "fold_tokens_per_s": round(args.steps * T / (ms_fold / 1e3), 1),
         "fold_us_per_frame": round(1e3 * ms_fold / args.steps, 2),
         "query_us_in_region": round(1e3 * ms_query_in_region, 2),

@@ -88,11 +88,16 @@ typedef struct {
   double eps_k, eps_v;      /* maintenance: key / value centre merge thresholds (>= 0) */
   float alpha, beta;        /* PROTOKV_FLAG_EMA_CENTRES: key / value centre EMA rates, in [0, 1] */
   double rope_theta;        /* rotary positions in the readout: 0 = off, else the base (> 1) */
+  int32_t warm_frames;      /* codebook warm-up folds T_warm (0 = use the given codebooks throughout) */
+  int32_t warm_tokens;      /* warm-up reservoir capacity per (stream, layer, kv head), 1..65536 */
+  int32_t kmeans_epochs;    /* mini-batch k-means passes over the reservoir, >= 1 */
+  int32_t kmeans_batch;     /* mini-batch size, 1..64 */
 } protokv_config;
 
 /* Table tab:default_config defaults (S=8, lambda_sp=0.1, lambda_idle=0.01,
  * T_idle=120, eta=0.05, alpha=beta=0.05, G=8, C=16, B=32, gamma=0.05,
- * eps_K=0.20, eps_V=0.25; maintenance and EMA centres off) with the 7B-class shape of one
+ * eps_K=0.20, eps_V=0.25; maintenance, EMA centres, RoPE and the codebook
+ * warm-up off, warm_tokens=1024, kmeans_epochs=4, kmeans_batch=64) with the 7B-class shape of one
  * stream: 28 layers, 4 KV heads, 28 query heads, 14x14 tokens per frame,
  * W=8 frames, K=256, bf16 KV, PQ and mass bias on, eps=1, rho=1e-4.
  * Host only. */
@@ -151,6 +156,18 @@ protokv_status protokv_append_frame(protokv_t h, const int32_t* stream_ids, int3
  * beta V in float32 (one rounding per product and per add, 1 - alpha
  * rounded first), then its PQ residual codes are taken against the updated
  * centres (the screen's cosine is unchanged; synthesis uses c, p directly).
+ * With warm_frames > 0 (appendix "PQ codebook initialization") the first
+ * warm_frames folds of a stream count no PQ codes; they append each
+ * non-seed token's key and value residuals against its slot's centre
+ * sum / n before the fold, in eviction order, to a reservoir of at most
+ * warm_tokens per (layer, kv head).  After the last of them, mini-batch
+ * k-means learns each subspace's key and value codebook from the
+ * reservoir (centres started from rows i * floor(N / C); batches of
+ * kmeans_batch consecutive rows assigned with the float32 sequential PQ
+ * distance as each batch starts, then each row in order: count += 1,
+ * eta = 1 / count, c <- (1 - eta) c + eta x in float32; kmeans_epochs
+ * passes), replacing the stream's codebooks from the next fold on (with
+ * fewer than C residuals the given codebooks stay).
  * Invalidates any synthesis.  No-op when nothing is pending. */
 protokv_status protokv_fold(protokv_t h, void* stream);
 
@@ -219,6 +236,12 @@ protokv_status protokv_get_counters(protokv_t h, protokv_counters* out, void* st
 protokv_status protokv_read_assignments(protokv_t h, int32_t stream_id, int32_t* dst,
                                         size_t count, void* stream);
 
+/* Copies the PQ codebooks of `stream_id` (as given at init, or learned by
+ * the warm-up) to dst (host), float32 [num_layers][num_kv_heads][2][G][C][D/G];
+ * count must equal that many floats.  Synchronizes `stream`. */
+protokv_status protokv_read_codebooks(protokv_t h, int32_t stream_id, float* dst, size_t count,
+                                      void* stream);
+
 /* Bank row layout (bytes) of one prototype slot, PROTOKV_ROW_BYTES each,
  * rows ordered [num_layers][num_kv_heads][capacity]:
  *   0     float32 sum_k[128]      sum of absorbed keys (EMA centres: the centre c)
@@ -265,7 +288,9 @@ enum {
   PROTOKV_K_MAINTAIN = 9,        /* prototype maintenance (PROTOKV_FLAG_MAINTENANCE) */
   PROTOKV_K_ROPE_RING = 10,      /* rotated copy of appended keys (rope_theta > 0) */
   PROTOKV_K_ROPE_Q = 11,         /* rotated query (rope_theta > 0) */
-  PROTOKV_K_COUNT = 12
+  PROTOKV_K_WARM_COLLECT = 12,   /* warm-up residuals into the reservoir (warm_frames > 0) */
+  PROTOKV_K_WARM_KMEANS = 13,    /* codebooks learned from the reservoir (warm_frames > 0) */
+  PROTOKV_K_COUNT = 16
 };
 
 typedef struct {

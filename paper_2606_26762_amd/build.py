@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libprotokv.so")
-SOURCES = ["protokv.cpp", "fold.hip", "query.hip"]
+SOURCES = ["protokv.cpp", "fold.hip", "query.hip", "warmup.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -815,8 +815,8 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
   // w / 2 of K (w even) or V; each code bumps its bin of the slot's
   // histogram (integer counts: the order of the increments does not matter).
   // With EMA centres the residuals follow each token's own centre update and
-  // the aggregation codes them.
-  if ((dm.flags & (PROTOKV_FLAG_PQ | PROTOKV_FLAG_EMA_CENTRES)) == PROTOKV_FLAG_PQ) {
+  // the aggregation codes them; codebook warm-up folds count no codes.
+  if ((dm.flags & (PROTOKV_FLAG_PQ | PROTOKV_FLAG_EMA_CENTRES)) == PROTOKV_FLAG_PQ && !fb.warm[b]) {
     __syncthreads();
     const int blk = wave >> 1, kv = wave & 1;
     const int jq = tile * SCREEN_TOK + blk * 32 + col;
@@ -1023,7 +1023,7 @@ __global__ __launch_bounds__(256, EMA ? 3 : 4) void k_aggregate(Dims dm, Workspa
   const int k0 = wgi * AGG_SLOTS;
   if (nseed >= N || k0 >= kact) return;  // uniform
   const size_t unit = (size_t)fb.sid[b] * dm.units + u;
-  const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
+  const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0 && !fb.warm[b];  // warm-up folds count no codes
   const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
   const unsigned long long below = (1ull << lane) - 1ull;
   const int N64 = (N + 63) & ~63;

@@ -61,6 +61,7 @@ struct Dims {
   double gamma, eps_k, eps_v;  // maintenance (PROTOKV_FLAG_MAINTENANCE)
   float alpha, beta;           // centre EMA rates (PROTOKV_FLAG_EMA_CENTRES)
   double rope_theta;           // rotary positions in the readout (0 = off)
+  int warm_frames, warm_tokens, kmeans_epochs, kmeans_batch;  // codebook warm-up
   int max_rows;    // max query rows per kv head (max_query_tokens * Hq / Hkv)
   int max_splits;  // attention context splits (partials storage)
 };
@@ -100,6 +101,8 @@ struct Workspace {
   uint8_t* ring_kr;              // [streams][units][W+1][T][D] kv dtype: ring_k rotated at f * T + j
   uint8_t* qrot;                 // [L][max_query_tokens][Hq][D] kv dtype: the query rotated at P + t
   const double* rope_inv;        // [D/2]: theta^(-2i/D)
+  // codebook warm-up (warm_frames > 0; otherwise null)
+  float* reservoir;              // [streams][units][2][warm_tokens][D]: residuals, eviction order
 };
 
 enum Counter {
@@ -129,6 +132,16 @@ struct FoldBatch {
   int t[MAXB];      // current frame (the one just appended)
   int nact[MAXB];   // active slots before this fold
   int nseed[MAXB];  // tokens of this frame that seed free slots
+  int warm[MAXB];   // warm-up fold: no PQ counts, residuals into the reservoir
+  int rfill[MAXB];  // reservoir rows already filled (warm-up folds)
+};
+
+// Streams whose warm-up ends with this fold: learn their codebooks from
+// `count` reservoir rows.
+struct KmeansBatch {
+  int n;
+  int sid[MAXB];
+  int count[MAXB];
 };
 
 struct AttendArgs {
@@ -187,5 +200,8 @@ hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const Attend
 hipError_t launch_rope_ring(const Dims& dm, const Workspace& ws, const AppendBatch& ab, hipStream_t st);
 hipError_t launch_rope_q(const Dims& dm, const Workspace& ws, const void* q, int tq, long long p0,
                          hipStream_t st);
+// codebook warm-up (warmup.hip)
+hipError_t launch_warm_collect(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st);
+hipError_t launch_warm_kmeans(const Dims& dm, const Workspace& ws, const KmeansBatch& kb, hipStream_t st);
 
 }  // namespace pkv

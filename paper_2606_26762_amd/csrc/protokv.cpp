@@ -23,11 +23,13 @@ struct StreamState {
   int active = 0;
   bool pending = false;
   int pending_fe = -1;
+  int folds = 0;  // folds done (the first warm_frames are the codebook warm-up)
+  int rfill = 0;  // warm-up reservoir rows filled
 };
 
 struct Layout {
   size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codebooks, cbhn, cbmax;
-  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, ring_kr, qrot, rope_inv, total;
+  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, ring_kr, qrot, rope_inv, reservoir, total;
 };
 
 thread_local std::string g_init_err;
@@ -73,6 +75,7 @@ Layout make_layout(const protokv_config& c) {
   ly.ring_kr = take(rope ? U * (c.window_frames + 1) * T * D * es : 0);
   ly.qrot = take(rope ? (size_t)c.num_layers * c.max_query_tokens * c.num_q_heads * D * es : 0);
   ly.rope_inv = take(rope ? (D / 2) * sizeof(double) : 0);
+  ly.reservoir = take(c.warm_frames > 0 ? U * 2 * (size_t)c.warm_tokens * D * 4 : 0);
   ly.total = off;
   return ly;
 }
@@ -111,6 +114,14 @@ protokv_status check_config(const protokv_config* c, std::string& why) {
   }
   if (!(c->rope_theta == 0.0 || (c->rope_theta > 1.0 && std::isfinite(c->rope_theta))))
     return bad("rope_theta must be 0 (off) or a finite base > 1");
+  if (c->warm_frames < 0) return bad("warm_frames must be >= 0");
+  if (c->warm_frames > 0) {
+    if (c->warm_tokens < 1 || c->warm_tokens > 65536) return bad("warm_tokens must be in [1, 65536]");
+    if (c->kmeans_epochs < 1) return bad("kmeans_epochs must be >= 1");
+    if (c->kmeans_batch < 1 || c->kmeans_batch > 64) return bad("kmeans_batch must be in [1, 64]");
+    if (!(c->flags & PROTOKV_FLAG_PQ)) return bad("the codebook warm-up needs PROTOKV_FLAG_PQ");
+    if (c->flags & PROTOKV_FLAG_EMA_CENTRES) return uns("codebook warm-up with EMA centres");
+  }
   if (!(c->eta > 0.f && c->eta < 1.f)) return bad("eta must be in (0, 1)");
   if (c->pq_eps != 1.0f) return uns("pq_eps must be 1");
   if (!(c->lambda_sp >= 0.0) || !(c->lambda_idle >= 0.0) || !std::isfinite(c->lambda_sp) ||
@@ -213,6 +224,9 @@ protokv_status protokv_default_config(protokv_config* c) {
   c->eps_v = 0.25;
   c->alpha = 0.05f;
   c->beta = 0.05f;
+  c->warm_tokens = 1024;
+  c->kmeans_epochs = 4;
+  c->kmeans_batch = 64;
   return PROTOKV_OK;
 }
 
@@ -277,6 +291,10 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   dm.alpha = c->alpha;
   dm.beta = c->beta;
   dm.rope_theta = c->rope_theta;
+  dm.warm_frames = c->warm_frames;
+  dm.warm_tokens = c->warm_tokens;
+  dm.kmeans_epochs = c->kmeans_epochs;
+  dm.kmeans_batch = c->kmeans_batch;
   dm.max_rows = c->max_query_tokens * (c->num_q_heads / c->num_kv_heads);
   dm.max_splits = MAX_SPLITS;
   uint8_t* b = h->base;
@@ -304,6 +322,7 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.ring_kr = rope ? b + ly.ring_kr : nullptr;
   ws.qrot = rope ? b + ly.qrot : nullptr;
   ws.rope_inv = rope ? (const double*)(b + ly.rope_inv) : nullptr;
+  ws.reservoir = c->warm_frames > 0 ? (float*)(b + ly.reservoir) : nullptr;
   h->st.assign(c->num_streams, StreamState());
 
   // codebooks -> [U][2][G][CMAX][DP] with the codeword axis padded to 16
@@ -416,7 +435,7 @@ protokv_status protokv_fold(protokv_t h, void* stream) {
     FoldBatch fb{};
     fb.n = (int)std::min<size_t>(MAXB, pend.size() - b0);
     int max_seed = 0;
-    bool any_assign = false;
+    bool any_assign = false, any_warm = false;
     for (int i = 0; i < fb.n; ++i) {
       const int s = pend[b0 + i];
       const StreamState& ss = h->st[s];
@@ -426,8 +445,11 @@ protokv_status protokv_fold(protokv_t h, void* stream) {
       fb.t[i] = (int)(ss.frames - 1);
       fb.nact[i] = ss.active;
       fb.nseed[i] = std::min(T, K - ss.active);
+      fb.warm[i] = ss.folds < h->dm.warm_frames ? 1 : 0;
+      fb.rfill[i] = ss.rfill;
       max_seed = std::max(max_seed, fb.nseed[i]);
       any_assign |= fb.nseed[i] < T;
+      any_warm |= fb.warm[i] && fb.nseed[i] < T;
     }
     protokv_status st = PROTOKV_OK;
     if (max_seed > 0)
@@ -436,15 +458,35 @@ protokv_status protokv_fold(protokv_t h, void* stream) {
     if (st == PROTOKV_OK && any_assign)
       st = h->dev(h->launch(PROTOKV_K_SCREEN, hs, [&] { return launch_screen(h->dm, h->ws, fb, hs); }),
                   "fold/screen");
+    // warm-up folds: residuals against the centres before this fold
+    if (st == PROTOKV_OK && any_warm)
+      st = h->dev(h->launch(PROTOKV_K_WARM_COLLECT, hs, [&] { return launch_warm_collect(h->dm, h->ws, fb, hs); }),
+                  "fold/warm-up collect");
     if (st == PROTOKV_OK && any_assign)
       st = h->dev(h->launch(PROTOKV_K_AGGREGATE, hs, [&] { return launch_aggregate(h->dm, h->ws, fb, hs); }),
                   "fold/aggregate");
     if (st == PROTOKV_OK && (h->dm.flags & PROTOKV_FLAG_MAINTENANCE))
       st = h->dev(h->launch(PROTOKV_K_MAINTAIN, hs, [&] { return launch_maintain(h->dm, h->ws, fb, hs); }),
                   "fold/maintain");
+    // streams whose warm-up ends with this fold learn their codebooks
+    KmeansBatch kb{};
+    for (int i = 0; i < fb.n; ++i) {
+      if (!fb.warm[i]) continue;
+      const StreamState& ss = h->st[fb.sid[i]];
+      if (ss.folds + 1 == h->dm.warm_frames) {
+        kb.sid[kb.n] = fb.sid[i];
+        kb.count[kb.n] = std::min(h->dm.warm_tokens, ss.rfill + (T - fb.nseed[i]));
+        ++kb.n;
+      }
+    }
+    if (st == PROTOKV_OK && kb.n > 0)
+      st = h->dev(h->launch(PROTOKV_K_WARM_KMEANS, hs, [&] { return launch_warm_kmeans(h->dm, h->ws, kb, hs); }),
+                  "fold/warm-up k-means");
     if (st != PROTOKV_OK) return st;
     for (int i = 0; i < fb.n; ++i) {
       StreamState& ss = h->st[fb.sid[i]];
+      if (fb.warm[i]) ss.rfill = std::min(h->dm.warm_tokens, ss.rfill + (T - fb.nseed[i]));
+      ss.folds += 1;
       ss.active += fb.nseed[i];
       ss.evicted += T;
       ss.pending = false;
@@ -613,6 +655,21 @@ protokv_status protokv_read_assignments(protokv_t h, int32_t sid, int32_t* dst, 
   const size_t n = (size_t)h->dm.units * h->dm.T;
   if (count != n) return h->fail(PROTOKV_E_INVALID, "read_assignments: count must be num_layers*num_kv_heads*T");
   return copy_out(h, dst, h->ws.assign + (size_t)sid * n, n * 4, stream, "read_assignments");
+}
+
+protokv_status protokv_read_codebooks(protokv_t h, int32_t sid, float* dst, size_t count, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (sid < 0 || sid >= h->cfg.num_streams || !dst) return h->fail(PROTOKV_E_INVALID, "read_codebooks: bad stream or dst");
+  const int C = h->dm.C;
+  const size_t blocks = (size_t)h->dm.units * 2 * G;
+  if (count != blocks * C * DP) return h->fail(PROTOKV_E_INVALID, "read_codebooks: count must be L*Hkv*2*G*C*(D/G)");
+  std::vector<float> raw(blocks * CMAX * DP);
+  protokv_status s = copy_out(h, raw.data(), h->ws.codebooks + (size_t)sid * blocks * CMAX * DP,
+                              raw.size() * sizeof(float), stream, "read_codebooks");
+  if (s != PROTOKV_OK) return s;
+  for (size_t blk = 0; blk < blocks; ++blk)
+    std::memcpy(dst + blk * C * DP, raw.data() + blk * CMAX * DP, (size_t)C * DP * sizeof(float));
+  return PROTOKV_OK;
 }
 
 protokv_status protokv_read_bank(protokv_t h, int32_t sid, void* dst, size_t bytes, void* stream) {

@@ -26,11 +26,12 @@ EXPORTED = [
     "protokv_default_config", "protokv_validate_config", "protokv_workspace_size", "protokv_init",
     "protokv_destroy", "protokv_append_frame", "protokv_fold", "protokv_synthesize", "protokv_attend",
     "protokv_stream_info_get", "protokv_get_counters", "protokv_read_assignments", "protokv_read_bank",
-    "protokv_read_pseudo", "protokv_profile", "protokv_profile_read", "protokv_last_error",
+    "protokv_read_pseudo", "protokv_read_codebooks", "protokv_profile", "protokv_profile_read",
+    "protokv_last_error",
 ]
 
 KERNELS = ["ring_insert", "seed", "screen", "aggregate", "decode", "attend", "attend_merge", "pq_encode",
-           "materialize", "maintain", "rope_ring", "rope_q"]
+           "materialize", "maintain", "rope_ring", "rope_q", "warm_collect", "warm_kmeans"]
 
 
 class ProtoKVError(RuntimeError):
@@ -52,6 +53,8 @@ class Config(ctypes.Structure):
         ("lambda_sp", ctypes.c_double), ("lambda_idle", ctypes.c_double), ("ridge", ctypes.c_double),
         ("gamma", ctypes.c_double), ("eps_k", ctypes.c_double), ("eps_v", ctypes.c_double),
         ("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("rope_theta", ctypes.c_double),
+        ("warm_frames", ctypes.c_int32), ("warm_tokens", ctypes.c_int32),
+        ("kmeans_epochs", ctypes.c_int32), ("kmeans_batch", ctypes.c_int32),
     ]
 
 
@@ -69,7 +72,7 @@ class Counters(ctypes.Structure):
 
 
 class KernelTimes(ctypes.Structure):
-    _fields_ = [("ms", ctypes.c_double * 12), ("launches", ctypes.c_uint64 * 12)]
+    _fields_ = [("ms", ctypes.c_double * 16), ("launches", ctypes.c_uint64 * 16)]
 
 
 _lib = None
@@ -97,6 +100,7 @@ def lib() -> ctypes.CDLL:
         L.protokv_read_assignments.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_read_bank.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_read_pseudo.argtypes = [vp, vp, vp, vp, vp]
+        L.protokv_read_codebooks.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_profile.argtypes = [vp, ctypes.c_uint32]
         L.protokv_profile_read.argtypes = [vp, P(KernelTimes)]
         L.protokv_last_error.argtypes = [vp]
@@ -234,6 +238,15 @@ class ProtoKV:
         _check(lib().protokv_read_bank(self.h, stream_id, raw.ctypes.data, raw.size,
                                        _stream_ptr(stream)), self.h)
         return decode_bank(raw, self.units, self.cfg.capacity)
+
+    def read_codebooks(self, stream_id: int, stream=None) -> np.ndarray:
+        """-> float32 [units][2][G][C][D/G]: the stream's PQ codebooks (given, or learned by the warm-up)."""
+        c = self.cfg
+        out = np.zeros((self.units, 2, c.pq_subspaces, c.pq_codewords, c.head_dim // c.pq_subspaces),
+                       dtype=np.float32)
+        _check(lib().protokv_read_codebooks(self.h, stream_id, out.ctypes.data, out.size, _stream_ptr(stream)),
+               self.h)
+        return out
 
     def read_pseudo(self, stream=None):
         """-> keys, values float32 [units][K*S][D] and bias [units][K]."""

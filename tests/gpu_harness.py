@@ -50,7 +50,9 @@ def gpu_config(wl: W.Workload, p: O.Params, streams: int = 1, max_query_tokens=N
         max_query_tokens=max_query_tokens or wl.query_tokens,
         kv_dtype=pk.KV_FP32 if wl.kv_dtype == "fp32" else pk.KV_BF16, flags=flags,
         eta=p.eta, lambda_sp=p.lambda_sp, lambda_idle=p.lambda_idle, ridge=p.ridge,
-        gamma=p.gamma, eps_k=p.eps_k, eps_v=p.eps_v, alpha=p.alpha, beta=p.beta, rope_theta=p.rope_theta)
+        gamma=p.gamma, eps_k=p.eps_k, eps_v=p.eps_v, alpha=p.alpha, beta=p.beta, rope_theta=p.rope_theta,
+        warm_frames=p.warm_frames, warm_tokens=p.warm_tokens, kmeans_epochs=p.kmeans_epochs,
+        kmeans_batch=p.kmeans_batch)
 
 
 def assert_bank_equal(gb, u: int, ob: O.Bank, C: int, where: str, bitwise: bool):

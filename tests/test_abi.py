@@ -57,6 +57,7 @@ def lib_status(c):
     ("eta", 0.0, 1), ("pq_eps", 0.5, 2), ("ridge", 0.0, 1), ("lambda_sp", -1.0, 1),
     ("max_query_tokens", 100, 2), ("max_query_tokens", 0, 1), ("t_idle", -1, 1),
     ("rope_theta", 0.5, 1), ("rope_theta", -1.0, 1), ("rope_theta", float("inf"), 1),
+    ("warm_frames", -1, 1),
 ])
 def test_validation_rejects(field, value, status):
     c = pk.default_config(**{field: value})
@@ -72,6 +73,16 @@ def test_ema_centre_validation(kw, status):
     supported."""
     flags = pk.FLAG_PQ | pk.FLAG_MASS_BIAS | pk.FLAG_EMA_CENTRES | kw.pop("flags", 0)
     assert lib_status(pk.default_config(flags=flags, **kw)) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(warm_tokens=0), 1), (dict(kmeans_epochs=0), 1), (dict(kmeans_batch=65), 1),
+    (dict(flags=pk.FLAG_MASS_BIAS), 1), (dict(flags=pk.FLAG_PQ | pk.FLAG_EMA_CENTRES), 2), ({}, 0),
+])
+def test_warmup_validation(kw, status):
+    """Warm-up sizes must be positive (batch at most 64), it needs PQ and
+    does not combine with EMA centres."""
+    assert lib_status(pk.default_config(warm_frames=2, **kw)) == status
 
 
 def test_workspace_size_scales_with_shape():

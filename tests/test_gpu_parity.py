@@ -183,6 +183,41 @@ def test_rope_readout(wl_name, theta, grid):
     assert gap > 3 * h.READOUT_ATOL
 
 
+@pytest.mark.parametrize("wl_name", ["7b", "tiny"])
+def test_codebook_warmup(wl_name):
+    """PQ codebook warm-up: the warm-up folds count no codes (banks bitwise
+    equal to the oracle's after every fold), the codebooks learned from the
+    reservoir are bitwise the oracle's, and the later folds code with them
+    (banks bitwise), then the readout.  The bf16 case caps the reservoir
+    below the residuals offered."""
+    h = H()
+    if wl_name == "7b":
+        wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=6, grid_w=6,
+                                     frames=12, window_frames=2, capacity=48, query_tokens=4)
+        kw = dict(warm_frames=4, warm_tokens=64, kmeans_epochs=3, kmeans_batch=16)
+    else:
+        wl = W.WORKLOADS["tiny"].with_(frames=10)
+        kw = dict(warm_frames=3, warm_tokens=1024, kmeans_epochs=2, kmeans_batch=64)
+    h.log(f"case: codebook warm-up {wl.name} {kw}")
+    pair = h.Pair(wl, **kw)
+    given = pair.gpu.read_codebooks(0)
+    learned = False
+    for f in range(wl.frames):
+        pair.step()
+        if f >= wl.window_frames:
+            pair.check_bank(bitwise=True)
+            st = pair.oracle[0]
+            if st.folds >= kw["warm_frames"]:
+                cb = pair.gpu.read_codebooks(0)
+                for i, u in enumerate(pair.sample):
+                    assert np.array_equal(cb[u], st.codebooks[i]), f"unit {u}: learned codebooks differ"
+                    assert not np.array_equal(cb[u], given[u])
+                learned = True
+    assert learned
+    pseudo = pair.synthesize()
+    pair.attend(pair.query(np.random.default_rng(19)), pseudo)
+
+
 def test_capacity_limit_gives_exact_attention():
     """K >= evicted tokens: every token keeps its own slot, and the readout is
     exact attention over the full history with far logits shifted by ln S
