@@ -923,9 +923,11 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
 // (mass, sums, sums of squares, residual count, spatial EMA, recency; the
 // screen already counted the PQ codes into the histograms), writes the row
 // back and refreshes the slot's screening copy.  With EMA centres (EMA = 1)
-// the sums are the centres, updated per token at rates alpha, beta, and each
-// token's residuals against its updated centres are coded here (pq_code16)
-// into the slot's histograms, held by the group (two lanes per subspace).
+// the sums are the centres, updated per token at rates alpha, beta; each
+// token's residuals against its updated centres go to the workspace, and
+// once every slot of the workgroup is done, all its threads code every
+// (token, K/V, subspace) in parallel and each group adds its slots' codes
+// to their histograms.
 // ---------------------------------------------------------------------------
 constexpr int AGG_SLOTS = 32;  // slots per workgroup: two per 16-lane group (k0 + g, k0 + g + 16)
 constexpr int AGG_TOK_BYTES = 32768;  // LDS for the workgroup's tokens (64 bf16 or 32 float32 tokens)
@@ -962,52 +964,18 @@ __device__ __forceinline__ void st8f(uint8_t* p, const float (&x)[8]) {
   reinterpret_cast<float4*>(p)[1] = make_float4(x[4], x[5], x[6], x[7]);
 }
 
-// Nearest codeword (ties to the lower index) of one subspace of a residual
-// held by two lanes of a 16-lane group: lane 2g has dims 0..7 of subspace g,
-// lane 2g + 1 dims 8..15.  The float32 distance sum_u (r_u - C[c][u])^2 is
-// accumulated with u ascending, one rounding per operation: lane 2g sums its
-// eight terms, lane 2g + 1 continues from that partial with its own.  cb is
-// the side's codebook [G][CMAX][DP] in LDS.  Returns the code in both lanes.
-__device__ __forceinline__ int pq_code16(const float (&r)[8], const float* cb, int il, int C) {
-  const float* cw = cb + (il >> 1) * CMAX * DP + (il & 1) * 8;
-  float best = INFINITY;
-  int code = 0;
-#pragma unroll 4
-  for (int c = 0; c < CMAX; ++c) {
-    const float4 w0 = *reinterpret_cast<const float4*>(cw + c * DP);
-    const float4 w1 = *reinterpret_cast<const float4*>(cw + c * DP + 4);
-    const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-    float t[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float df = r[e] - w[e];
-      t[e] = df * df;
-    }
-    float acc = t[0];
-#pragma unroll
-    for (int e = 1; e < 8; ++e) acc = acc + t[e];
-    float full = __shfl_xor(acc, 1, 64);  // lane 2g + 1: the partial of dims 0..7
-#pragma unroll
-    for (int e = 0; e < 8; ++e) full = full + t[e];
-    if (c < C && full < best) {
-      best = full;
-      code = c;
-    }
-  }
-  const int other = __shfl_xor(code, 1, 64);
-  return (il & 1) ? code : other;
-}
-
 template <int FP32, int EMA>
-__global__ __launch_bounds__(256, EMA ? 3 : 4) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int wg_per_unit) {
+__global__ __launch_bounds__(256, EMA ? 2 : 4) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int wg_per_unit) {
   __shared__ uint16_t s_asg[TMAX];         // slot of each token (NO_SLOT: seeded / padding)
   __shared__ uint16_t s_tok[TMAX];         // tokens of this workgroup's slots, grouped, eviction order
   __shared__ int s_cnt[AGG_SLOTS];
   __shared__ int s_off[AGG_SLOTS + 1];       // local slot q = group + 16 * pass
   // the workgroup's tokens in list order, [position][K, V][D] KV dtype, when they fit
   __shared__ __attribute__((aligned(16))) uint8_t s_tk[AGG_TOK_BYTES];
-  // EMA centres: the unit's codebooks [K, V][G][CMAX][DP] for the residual codes
+  // EMA centres: the unit's codebooks [K, V][G][CMAX][DP] for the residual
+  // codes, and the code of every (token, K/V, subspace) of the workgroup
   __shared__ __attribute__((aligned(16))) float s_cb[EMA ? 2 * G * CMAX * DP : 4];
+  __shared__ uint8_t s_code[EMA ? TMAX * 2 * G : 4];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // same XCD placement as the screen (consecutive logical blocks share an
@@ -1107,8 +1075,6 @@ __global__ __launch_bounds__(256, EMA ? 3 : 4) void k_aggregate(Dims dm, Workspa
   }
   // the first slot's row (loads in flight with the tokens')
   float sk[8], sv[8], qk[8], qv[8];
-  // EMA centres: this lane's histogram bins H[il / 2][8 (il % 2) ..] (K, V)
-  uint4 hk[2], hv[2];
   RowMeta m;
   auto load_row = [&](int q) {
     const uint8_t* row = ws.bank + (unit * dm.K + k0 + q) * ROW;
@@ -1116,12 +1082,6 @@ __global__ __launch_bounds__(256, EMA ? 3 : 4) void k_aggregate(Dims dm, Workspa
     ld8f(row + ROW_SUMV + il * 32, sv);
     ld8f(row + ROW_SQK + il * 32, qk);
     ld8f(row + ROW_SQV + il * 32, qv);
-    if (EMA && pq) {
-      hk[0] = reinterpret_cast<const uint4*>(row + ROW_HK + il * 32)[0];
-      hk[1] = reinterpret_cast<const uint4*>(row + ROW_HK + il * 32)[1];
-      hv[0] = reinterpret_cast<const uint4*>(row + ROW_HV + il * 32)[0];
-      hv[1] = reinterpret_cast<const uint4*>(row + ROW_HV + il * 32)[1];
-    }
     m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
   };
   const float ak = dm.alpha, av = dm.beta, a1k = 1.0f - dm.alpha, a1v = 1.0f - dm.beta;
@@ -1165,7 +1125,7 @@ __global__ __launch_bounds__(256, EMA ? 3 : 4) void k_aggregate(Dims dm, Workspa
           const int jj = jb[e];
           if (EMA) {
             // c <- (1 - alpha) c + alpha K, p likewise with beta; residuals
-            // against the updated centres, coded into this lane's bins
+            // against the updated centres to the workspace (coded below)
             float rk[8], rv[8];
 #pragma unroll
             for (int d = 0; d < 8; ++d) {
@@ -1178,12 +1138,9 @@ __global__ __launch_bounds__(256, EMA ? 3 : 4) void k_aggregate(Dims dm, Workspa
               rv[d] = xv - sv[d];
             }
             if (pq) {
-              const int zk = pq_code16(rk, s_cb, il, dm.C) - 8 * (il & 1);
-              const int zv = pq_code16(rv, s_cb + G * CMAX * DP, il, dm.C) - 8 * (il & 1);
-              hk[0].x += zk == 0; hk[0].y += zk == 1; hk[0].z += zk == 2; hk[0].w += zk == 3;
-              hk[1].x += zk == 4; hk[1].y += zk == 5; hk[1].z += zk == 6; hk[1].w += zk == 7;
-              hv[0].x += zv == 0; hv[0].y += zv == 1; hv[0].z += zv == 2; hv[0].w += zv == 3;
-              hv[1].x += zv == 4; hv[1].y += zv == 5; hv[1].z += zv == 6; hv[1].w += zv == 7;
+              float* rr = ws.ema_res + ((unit * N + jj) * 2) * (size_t)D + 8 * il;
+              st8f(reinterpret_cast<uint8_t*>(rr), rk);
+              st8f(reinterpret_cast<uint8_t*>(rr + D), rv);
               m.n_res += 1;
             }
           } else {
@@ -1216,16 +1173,67 @@ __global__ __launch_bounds__(256, EMA ? 3 : 4) void k_aggregate(Dims dm, Workspa
     st8f(row + ROW_SUMV + il * 32, sv);
     st8f(row + ROW_SQK + il * 32, qk);
     st8f(row + ROW_SQV + il * 32, qv);
-    if (EMA && pq) {
-      reinterpret_cast<uint4*>(row + ROW_HK + il * 32)[0] = hk[0];
-      reinterpret_cast<uint4*>(row + ROW_HK + il * 32)[1] = hk[1];
-      reinterpret_cast<uint4*>(row + ROW_HV + il * 32)[0] = hv[0];
-      reinterpret_cast<uint4*>(row + ROW_HV + il * 32)[1] = hv[1];
-    }
     if (il == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
     refresh_cache16(dm, sk, m, unit, k, ws, il);
     // per-slot count of folds that touched it (owned by this lane group: no atomics)
     if (il == 0) ws.touched[si] += 1u;
+  }
+  if (EMA && pq) {
+    // every (token, K/V, subspace) of the workgroup coded in parallel from
+    // the residuals written above: the float32 sequential distance over the
+    // subspace's dims, ascending, ties to the lower codeword.  Tasks run
+    // token-fastest, so a wave's lanes share one codebook (broadcast reads).
+    __syncthreads();
+    for (int task = tid; task < ntok * 2 * G; task += 256) {
+      const int pos = task % ntok, sg = task / ntok, side = sg / G, g = sg % G;
+      const float* rr = ws.ema_res + ((unit * N + s_tok[pos]) * 2 + side) * (size_t)D + g * DP;
+      float x[DP];
+#pragma unroll
+      for (int q = 0; q < DP / 4; ++q) {
+        const float4 v = reinterpret_cast<const float4*>(rr)[q];
+        x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
+      }
+      const float* cw = s_cb + (side * G + g) * CMAX * DP;
+      float best = INFINITY;
+      int code = 0;
+      for (int c = 0; c < dm.C; ++c) {
+        float acc = 0.f;
+#pragma unroll
+        for (int d = 0; d < DP; ++d) {
+          const float df = x[d] - cw[c * DP + d];
+          acc = acc + df * df;
+        }
+        if (acc < best) {
+          best = acc;
+          code = c;
+        }
+      }
+      s_code[pos * 2 * G + side * G + g] = (uint8_t)code;
+    }
+    __syncthreads();
+    // each group adds its slots' codes to their histograms: lane il holds
+    // bins H[il / 2][8 (il % 2) ..] of K and of V
+    for (int pass = 0; pass < 2; ++pass) {
+      const int q = gi + 16 * pass;
+      const int t0 = s_off[q], t1 = s_off[q + 1];
+      if (t1 == t0) continue;
+      uint8_t* row = ws.bank + (unit * dm.K + k0 + q) * ROW;
+      uint4* phk = reinterpret_cast<uint4*>(row + ROW_HK + il * 32);
+      uint4* phv = reinterpret_cast<uint4*>(row + ROW_HV + il * 32);
+      uint4 h0 = phk[0], h1 = phk[1], v0 = phv[0], v1 = phv[1];
+      const int sg = il >> 1, base = 8 * (il & 1);
+      for (int pos = t0; pos < t1; ++pos) {
+        const int zk = (int)s_code[pos * 2 * G + sg] - base, zv = (int)s_code[pos * 2 * G + G + sg] - base;
+        h0.x += zk == 0; h0.y += zk == 1; h0.z += zk == 2; h0.w += zk == 3;
+        h1.x += zk == 4; h1.y += zk == 5; h1.z += zk == 6; h1.w += zk == 7;
+        v0.x += zv == 0; v0.y += zv == 1; v0.z += zv == 2; v0.w += zv == 3;
+        v1.x += zv == 4; v1.y += zv == 5; v1.z += zv == 6; v1.w += zv == 7;
+      }
+      phk[0] = h0;
+      phk[1] = h1;
+      phv[0] = v0;
+      phv[1] = v1;
+    }
   }
 }
 

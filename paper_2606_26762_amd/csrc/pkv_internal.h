@@ -103,6 +103,8 @@ struct Workspace {
   const double* rope_inv;        // [D/2]: theta^(-2i/D)
   // codebook warm-up (warm_frames > 0; otherwise null)
   float* reservoir;              // [streams][units][2][warm_tokens][D]: residuals, eviction order
+  // EMA centres (PROTOKV_FLAG_EMA_CENTRES; otherwise null)
+  float* ema_res;                // [streams][units][T][2][D]: residuals of the fold's tokens
 };
 
 enum Counter {

@@ -29,7 +29,7 @@ struct StreamState {
 
 struct Layout {
   size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codebooks, cbhn, cbmax;
-  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, ring_kr, qrot, rope_inv, reservoir, total;
+  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, ring_kr, qrot, rope_inv, reservoir, ema_res, total;
 };
 
 thread_local std::string g_init_err;
@@ -76,6 +76,7 @@ Layout make_layout(const protokv_config& c) {
   ly.qrot = take(rope ? (size_t)c.num_layers * c.max_query_tokens * c.num_q_heads * D * es : 0);
   ly.rope_inv = take(rope ? (D / 2) * sizeof(double) : 0);
   ly.reservoir = take(c.warm_frames > 0 ? U * 2 * (size_t)c.warm_tokens * D * 4 : 0);
+  ly.ema_res = take((c.flags & PROTOKV_FLAG_EMA_CENTRES) ? U * T * 2 * D * 4 : 0);
   ly.total = off;
   return ly;
 }
@@ -323,6 +324,7 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.qrot = rope ? b + ly.qrot : nullptr;
   ws.rope_inv = rope ? (const double*)(b + ly.rope_inv) : nullptr;
   ws.reservoir = c->warm_frames > 0 ? (float*)(b + ly.reservoir) : nullptr;
+  ws.ema_res = (c->flags & PROTOKV_FLAG_EMA_CENTRES) ? (float*)(b + ly.ema_res) : nullptr;
   h->st.assign(c->num_streams, StreamState());
 
   // codebooks -> [U][2][G][CMAX][DP] with the codeword axis padded to 16
