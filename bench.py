@@ -76,6 +76,8 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
     merged and recycled slots per maintenance launch.  `ema`: EMA centres, whose
     residual codes the aggregation computes (the screen only assigns)."""
     U, T, D, K, S = wl.units, wl.tokens_per_frame, wl.head_dim, wl.capacity, cfg.pseudo_per_proto
+    if kernel in FOLD_KERNELS:  # one launch folds every stream's units
+        U *= cfg.num_streams
     b = 4 if wl.kv_dtype == "fp32" else 2
     if kernel == "ring_insert":
         return U * T * D * b * 2 * 2                       # read frame K,V + write ring K,V
@@ -243,7 +245,8 @@ def main():
     assert args.warmup >= wl.window_frames + math.ceil(wl.capacity / wl.tokens_per_frame), \
         "warmup must fill the bank"
     lib = pk.lib()
-    cfg = pk.default_config(num_streams=1, num_layers=wl.num_layers, num_kv_heads=wl.num_kv_heads,
+    NS = wl.streams
+    cfg = pk.default_config(num_streams=NS, num_layers=wl.num_layers, num_kv_heads=wl.num_kv_heads,
                             num_q_heads=wl.num_q_heads, grid_h=wl.grid_h, grid_w=wl.grid_w,
                             window_frames=wl.window_frames, capacity=wl.capacity,
                             max_query_tokens=wl.query_tokens,
@@ -256,11 +259,14 @@ def main():
     cfg.warm_frames = args.warm_frames
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    cb = W.make_codebooks_device(wl)
-    eng = pk.ProtoKV(cfg, cb)
-    gen = W.DeviceStream(wl, n_streams=1)
+    cb = W.make_codebooks_device(wl, n_streams=NS)
+    eng = pk.ProtoKV(cfg, cb.reshape(-1, *cb.shape[2:]))
+    gen = W.DeviceStream(wl, n_streams=NS)
+    # one stream: every frame drawn ahead; several: a pool of POOL frames
+    # (each [streams][L][Hkv][T][D]) taken in turn
+    POOL = 8
     ks, vs = [], []
-    for _ in range(frames_needed):
+    for _ in range(frames_needed if NS == 1 else POOL):
         k, v = gen.next_frame()
         ks.append(k)
         vs.append(v)
@@ -272,7 +278,7 @@ def main():
     stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
     h = eng.h
-    ids = (ctypes.c_int32 * 1)(0)
+    ids = (ctypes.c_int32 * NS)(*range(NS))
     kp = [ctypes.c_void_p(t.data_ptr()) for t in ks]
     vp = [ctypes.c_void_p(t.data_ptr()) for t in vs]
     qp, op, lp = ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(o.data_ptr()), ctypes.c_void_p(lse.data_ptr())
@@ -281,14 +287,21 @@ def main():
     append, fold = lib.protokv_append_frame, lib.protokv_fold
     synth, attend = lib.protokv_synthesize, lib.protokv_attend
 
-    def run_frames(lo, hi):
+    def run_frames(lo, hi, queries=False):
         for i in range(lo, hi):
-            if append(h, ids, 1, kp[i], vp[i], sp) or fold(h, sp):
+            j = i % len(kp)
+            if append(h, ids, NS, kp[j], vp[j], sp) or fold(h, sp):
                 raise RuntimeError(lib.protokv_last_error(h))
+            if queries and i % QEVERY == 0:
+                run_query((i // QEVERY) % NS)
 
-    def run_query():
-        if synth(h, 0, sp) or attend(h, 0, qp, tq, op, lp, sp):
+    def run_query(sid=0):
+        if synth(h, sid, sp) or attend(h, sid, qp, tq, op, lp, sp):
             raise RuntimeError(lib.protokv_last_error(h))
+
+    # several streams: each queries once every query_every frames, so a step
+    # (one frame of every stream) carries NS / query_every queries
+    QEVERY = max(1, wl.query_every // NS) if NS > 1 else 0
 
     # warm-up: fill the window and the bank, compile paths, one query
     run_frames(0, args.warmup)
@@ -335,7 +348,7 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     e0.record(stream)
-    run_frames(lo, lo + args.steps)
+    run_frames(lo, lo + args.steps, queries=NS > 1)
     e1.record(stream)
     run_query()
     e2.record(stream)
@@ -347,7 +360,7 @@ def main():
     ms_total = e0.elapsed_time(e2)
     ms_fold = e0.elapsed_time(e1)
     ms_query_in_region = e1.elapsed_time(e2)
-    value = args.steps * T / (ms_total / 1e3)
+    value = args.steps * T * NS / (ms_total / 1e3)
     touched_live = (c3.touched - c2.touched) / args.steps
 
     # readout latency: median over repeats, synthesize+attend and attend only
@@ -375,7 +388,7 @@ def main():
                 "launches_timed": live["launches"],
                 "traffic_source": traffic["file"] if traffic else None}
     # screen MFMA work, for reference: 2 (hi, lo) x 2 N K D flops per unit
-    scr_flops = wl.units * 2 * 2 * T * wl.capacity * wl.head_dim
+    scr_flops = NS * wl.units * 2 * 2 * T * wl.capacity * wl.head_dim
     if "screen" in kernels:
         kernels["screen"]["mfma_tflops"] = round(scr_flops / (kernels["screen"]["avg_us"] * 1e-6) / 1e12, 2)
     att_flops = wl.units * 4 * rows * ctx * wl.head_dim
@@ -387,15 +400,17 @@ def main():
         "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_total / args.steps, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic (seeded on-device Gaussian-mixture stream, 7B video-LLM shape)",
+        "data": f"synthetic (seeded on-device Gaussian-mixture stream{'s' if NS > 1 else ''}, {wl.name})",
         "config": {"workload": wl.name, "layers": wl.num_layers, "kv_heads": wl.num_kv_heads,
                    "q_heads": wl.num_q_heads, "head_dim": wl.head_dim, "tokens_per_frame": T,
                    "window_frames": wl.window_frames, "capacity": wl.capacity,
                    "pseudo_per_proto": cfg.pseudo_per_proto, "query_tokens": tq,
                    "frames_streamed": lo + args.steps, "maintenance": bool(args.maintenance),
                    "centres": "ema" if args.ema else "mean", "rope_theta": args.rope_theta,
-                   "warm_frames": args.warm_frames},
-        "fold_tokens_per_s": round(args.steps * T / (ms_fold / 1e3), 1),
+                   "warm_frames": args.warm_frames, "streams": NS},
+        # with several streams a step is one frame of every stream, and the
+        # fold figures include the queries issued during the steps
+        "fold_tokens_per_s": round(args.steps * T * NS / (ms_fold / 1e3), 1),
         "fold_us_per_frame": round(1e3 * ms_fold / args.steps, 2),
         "query_us_in_region": round(1e3 * ms_query_in_region, 2),
         "readout_us_per_query": round(1e3 * readout_ms, 2),
@@ -409,7 +424,7 @@ def main():
         "kernels": kernels,
         "roofline": roofline,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and NS == 1:
         result["cpu_baseline"] = cpu_baseline(args, wl)
     print(json.dumps(result), flush=True)
 
