@@ -218,6 +218,35 @@ def test_codebook_warmup(wl_name):
     pair.attend(pair.query(np.random.default_rng(19)), pseudo)
 
 
+@pytest.mark.parametrize("case", ["maintenance+warmup+rope", "ema+rope"])
+def test_combined_options(case):
+    """The optional paths together: banks bitwise equal to the oracle's after
+    every fold (through the warm-up, its k-means and maintenance merges), then
+    the rows and the rotated readout."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=6, grid_w=6,
+                                 frames=14, window_frames=2, capacity=48, query_tokens=4)
+    if case == "ema+rope":
+        kw = dict(ema=True, alpha=0.1, beta=0.2, rope_theta=1e4)
+    else:
+        kw = dict(maintenance=True, t_idle=2, gamma=0.3, eps_k=1.0, eps_v=12.0,
+                  warm_frames=3, warm_tokens=200, kmeans_epochs=2, kmeans_batch=32, rope_theta=1e6)
+    h.log(f"case: combined {case} {kw}")
+    pair = h.Pair(wl, **kw)
+    for f in range(wl.frames):
+        pair.step()
+        if f >= wl.window_frames:
+            pair.check_bank(bitwise=True)
+    if case != "ema+rope":
+        c = pair.gpu.counters()
+        assert c.merged > 0 and c.recycled > 0
+        cb = pair.gpu.read_codebooks(0)
+        for i, u in enumerate(pair.sample):
+            assert np.array_equal(cb[u], pair.oracle[0].codebooks[i])
+    pseudo = pair.synthesize()
+    pair.attend(pair.query(np.random.default_rng(23)), pseudo)
+
+
 def test_capacity_limit_gives_exact_attention():
     """K >= evicted tokens: every token keeps its own slot, and the readout is
     exact attention over the full history with far logits shifted by ln S
