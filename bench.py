@@ -107,8 +107,8 @@ def algorithmic_bytes(kernel, wl, cfg, touched_per_launch=0.0, n_active=0, ctx=0
                 + m.get("merged", 0) * (3 * row + CACHE_BYTES)
                 + m.get("recycled", 0) * (2 * D * b + row + CACHE_BYTES))
     if kernel == "rope_ring":
-        # the appended frame's keys read and written rotated
-        return U * T * D * b * 2
+        # ring insert with the rotated key copy: K, V read; K, V and rotated K written
+        return U * T * D * b * 5
     if kernel == "warm_collect":
         # per non-seed token: its K and V, its slot's two sums, the two
         # residual rows written

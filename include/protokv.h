@@ -286,7 +286,7 @@ enum {
   PROTOKV_K_PQ_ENCODE = 7,       /* reserved: PQ encoding runs inside the screen kernel */
   PROTOKV_K_MATERIALIZE = 8,     /* pseudo-token rows and biases (float32 KV) */
   PROTOKV_K_MAINTAIN = 9,        /* prototype maintenance (PROTOKV_FLAG_MAINTENANCE) */
-  PROTOKV_K_ROPE_RING = 10,      /* rotated copy of appended keys (rope_theta > 0) */
+  PROTOKV_K_ROPE_RING = 10,      /* ring insert with the rotated key copy (rope_theta > 0; replaces RING_INSERT) */
   PROTOKV_K_ROPE_Q = 11,         /* rotated query (rope_theta > 0) */
   PROTOKV_K_WARM_COLLECT = 12,   /* warm-up residuals into the reservoir (warm_frames > 0) */
   PROTOKV_K_WARM_KMEANS = 13,    /* codebooks learned from the reservoir (warm_frames > 0) */

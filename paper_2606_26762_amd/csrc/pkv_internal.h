@@ -197,9 +197,10 @@ hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& 
                          hipStream_t st);
 hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa,
                                hipStream_t st);
-// rotary positions: the appended frames' keys into ring_kr; the query
-// (tq tokens from q, first position p0) into qrot
-hipError_t launch_rope_ring(const Dims& dm, const Workspace& ws, const AppendBatch& ab, hipStream_t st);
+// rotary positions: the query (tq tokens from q, first position p0) into qrot
+// ring insert and the rotated copy in one pass (rope_theta > 0)
+hipError_t launch_ring_insert_rope(const Dims& dm, const Workspace& ws, const AppendBatch& ab, const void* k,
+                                   const void* v, hipStream_t st);
 hipError_t launch_rope_q(const Dims& dm, const Workspace& ws, const void* q, int tq, long long p0,
                          hipStream_t st);
 // codebook warm-up (warmup.hip)

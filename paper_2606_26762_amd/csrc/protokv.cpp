@@ -404,14 +404,14 @@ protokv_status protokv_append_frame(protokv_t h, const int32_t* ids, int32_t n, 
       ab.slot[i] = (int)(ss.frames % (uint64_t)(h->dm.W + 1));
       ab.frame[i] = (int)ss.frames;
     }
-    protokv_status s = h->dev(h->launch(PROTOKV_K_RING_INSERT, hs, [&] {
-                                return launch_ring_insert(h->dm, h->ws, ab, (const uint8_t*)k + b0 * entry_bytes,
-                                                          (const uint8_t*)v + b0 * entry_bytes, hs);
-                              }),
-                              "append");
-    if (s == PROTOKV_OK && h->ws.ring_kr)
-      s = h->dev(h->launch(PROTOKV_K_ROPE_RING, hs, [&] { return launch_rope_ring(h->dm, h->ws, ab, hs); }),
-                 "append/rope");
+    const uint8_t* kb = (const uint8_t*)k + b0 * entry_bytes;
+    const uint8_t* vb = (const uint8_t*)v + b0 * entry_bytes;
+    // with rotary positions the rotated copy of the keys is written in the same pass
+    protokv_status s = h->dev(
+        h->ws.ring_kr
+            ? h->launch(PROTOKV_K_ROPE_RING, hs, [&] { return launch_ring_insert_rope(h->dm, h->ws, ab, kb, vb, hs); })
+            : h->launch(PROTOKV_K_RING_INSERT, hs, [&] { return launch_ring_insert(h->dm, h->ws, ab, kb, vb, hs); }),
+        "append");
     if (s != PROTOKV_OK) return s;
   }
   for (int i = 0; i < n; ++i) {

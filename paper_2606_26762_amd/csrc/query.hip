@@ -769,21 +769,6 @@ __device__ __forceinline__ void rope_row8(const uint8_t* src, uint8_t* dst, size
   st8kv<FP32>(dst, e0 + D / 2 + 8 * c, y2);
 }
 
-// Rotary copy of the appended frames' keys (ring_k -> ring_kr): thread =
-// (entry, unit, token j, pair block c); position f * T + j.
-template <int FP32>
-__global__ __launch_bounds__(256) void k_rope_ring(Dims dm, Workspace ws, AppendBatch ab) {
-  const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const size_t per = (size_t)dm.units * dm.T * 8;
-  const int e = (int)(gid / per);
-  if (e >= ab.n) return;
-  const size_t r = gid % per;
-  const int c = (int)(r & 7), j = (int)((r >> 3) % dm.T), u = (int)((r >> 3) / dm.T);
-  const size_t unit = (size_t)ab.sid[e] * dm.units + u;
-  const size_t e0 = ((unit * (dm.W + 1) + ab.slot[e]) * dm.T + j) * (size_t)D;
-  rope_row8<FP32>(ws.ring_k, ws.ring_kr, e0, c, (double)ab.frame[e] * dm.T + j, ws.rope_inv);
-}
-
 // The query [L][tq][Hq][D] rotated into qrot: thread = (row, pair block c);
 // token t at position p0 + t.
 template <int FP32>
@@ -796,13 +781,62 @@ __global__ __launch_bounds__(256) void k_rope_q(Dims dm, Workspace ws, const uin
   rope_row8<FP32>(q, ws.qrot, row * D, c, (double)(p0 + t), ws.rope_inv);
 }
 
-hipError_t launch_rope_ring(const Dims& dm, const Workspace& ws, const AppendBatch& ab, hipStream_t st) {
+// Ring insert with rotary positions, in one pass: thread = (entry, unit,
+// token j, pair block c) copies the token's K and V chunks [8c, 8c + 8) and
+// [D/2 + 8c, D/2 + 8c + 8) into the ring and writes the K pair rotated at
+// its stream position f * T + j into ring_kr.
+template <int FP32>
+__global__ __launch_bounds__(256) void k_ring_insert_rope(Dims dm, Workspace ws, AppendBatch ab,
+                                                          const uint8_t* k, const uint8_t* v) {
+  const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t per = (size_t)dm.units * dm.T * 8;
+  const int e = (int)(gid / per);
+  if (e >= ab.n) return;
+  const size_t r = gid % per;
+  const int c = (int)(r & 7), j = (int)((r >> 3) % dm.T), u = (int)((r >> 3) / dm.T);
+  const size_t es = FP32 ? 4 : 2;
+  const size_t s0 = (((size_t)e * dm.units + u) * dm.T + j) * (size_t)D;
+  const size_t d0 = ((((size_t)ab.sid[e] * dm.units + u) * (dm.W + 1) + ab.slot[e]) * dm.T + j) * (size_t)D;
+  constexpr int W16 = FP32 ? 2 : 1;  // 16-byte words per 8 elements
+  uint4 ka[W16], kb[W16], va[W16], vb[W16];
+#pragma unroll
+  for (int w = 0; w < W16; ++w) {
+    ka[w] = reinterpret_cast<const uint4*>(k + (s0 + 8 * c) * es)[w];
+    kb[w] = reinterpret_cast<const uint4*>(k + (s0 + D / 2 + 8 * c) * es)[w];
+    va[w] = reinterpret_cast<const uint4*>(v + (s0 + 8 * c) * es)[w];
+    vb[w] = reinterpret_cast<const uint4*>(v + (s0 + D / 2 + 8 * c) * es)[w];
+  }
+#pragma unroll
+  for (int w = 0; w < W16; ++w) {
+    reinterpret_cast<uint4*>(ws.ring_k + (d0 + 8 * c) * es)[w] = ka[w];
+    reinterpret_cast<uint4*>(ws.ring_k + (d0 + D / 2 + 8 * c) * es)[w] = kb[w];
+    reinterpret_cast<uint4*>(ws.ring_v + (d0 + 8 * c) * es)[w] = va[w];
+    reinterpret_cast<uint4*>(ws.ring_v + (d0 + D / 2 + 8 * c) * es)[w] = vb[w];
+  }
+  float x1[8], x2[8], y1[8], y2[8];
+  ld8kv<FP32>(reinterpret_cast<const uint8_t*>(ka), 0, x1);
+  ld8kv<FP32>(reinterpret_cast<const uint8_t*>(kb), 0, x2);
+  const double pos = (double)ab.frame[e] * dm.T + j;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    float cs, sn;
+    rope_cs(pos, ws.rope_inv[8 * c + q], cs, sn);
+    rope_pair(x1[q], x2[q], cs, sn, y1[q], y2[q]);
+  }
+  st8kv<FP32>(ws.ring_kr, d0 + 8 * c, y1);
+  st8kv<FP32>(ws.ring_kr, d0 + D / 2 + 8 * c, y2);
+}
+
+hipError_t launch_ring_insert_rope(const Dims& dm, const Workspace& ws, const AppendBatch& ab, const void* k,
+                                   const void* v, hipStream_t st) {
   const size_t n = (size_t)ab.n * dm.units * dm.T * 8;
   const dim3 grid((unsigned)((n + 255) / 256));
+  const uint8_t* kb = static_cast<const uint8_t*>(k);
+  const uint8_t* vb = static_cast<const uint8_t*>(v);
   if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_rope_ring<1>, grid, dim3(256), 0, st, dm, ws, ab);
+    hipLaunchKernelGGL(k_ring_insert_rope<1>, grid, dim3(256), 0, st, dm, ws, ab, kb, vb);
   else
-    hipLaunchKernelGGL(k_rope_ring<0>, grid, dim3(256), 0, st, dm, ws, ab);
+    hipLaunchKernelGGL(k_ring_insert_rope<0>, grid, dim3(256), 0, st, dm, ws, ab, kb, vb);
   return hipGetLastError();
 }
 
