@@ -63,6 +63,28 @@ def test_7b_shape_one_layer():
           f"+{c.refined_full}, touched {c.touched}, readout err {worst:.2e}")
 
 
+def test_maximum_frame_and_query_sizes():
+    """The largest shapes the library accepts per call: 1024 tokens per frame
+    (32x32 grid), 512 query rows per kv head (64 query tokens x 8 query
+    heads, two row blocks in the readout), with K = 4096 (32 768 pseudo
+    tokens at S = 8, 128 slot tiles per screen workgroup).  Four folds seed
+    the bank exactly to capacity, the next two assign at full K; every
+    assignment, the bank (bitwise), the rows and the readout are checked."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=1, num_q_heads=8, grid_h=32, grid_w=32,
+                                  frames=7, window_frames=1, capacity=4096, query_tokens=64)
+    h.log(f"case: maximum sizes T={wl.tokens_per_frame} K={wl.capacity} rows={wl.query_tokens * 8}")
+    pair = h.Pair(wl)
+    for f in range(wl.frames):
+        pair.step()
+    assert pair.gpu.stream_info(0).active_slots == wl.capacity
+    pair.check_bank(bitwise=True)
+    pseudo = pair.synthesize()
+    worst, *_ = pair.attend(pair.query(np.random.default_rng(23)), pseudo)
+    h.log(f"assignments {pair.assign_checked}, near ties {pair.near_ties}, readout err {worst:.2e}")
+    assert pair.assign_checked == (wl.frames - wl.window_frames) * wl.tokens_per_frame
+
+
 def test_ragged_shapes_seed_and_assign_same_fold():
     """T=35 (5x7, ragged tiles), K=20 < T (seed and assign in one fold),
     2 layers x 2 kv heads x 6 q heads, S=3, C=12, tq=5."""
