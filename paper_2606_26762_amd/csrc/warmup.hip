@@ -63,14 +63,21 @@ __global__ __launch_bounds__(256) void k_warm_collect(Dims dm, Workspace ws, Fol
 // batch of kmeans_batch consecutive rows each lane assigns one row to its
 // nearest centre (float32 sequential distance over the dims, ties to the
 // lower index) with the centres as the batch starts, then the rows update
-// their centres one after another in row order (count += 1, eta = 1 / count,
-// c <- (1 - eta) c + eta x; lane d updates dim d); kmeans_epochs passes.
+// their centres in row order (count += 1, eta = 1 / count,
+// c <- (1 - eta) c + eta x); kmeans_epochs passes.
+// A row's count is known before any update: the count of its centre before
+// the batch plus its rank among the batch's rows of that centre (ballots).
+// So each row lane forms 1 - eta and eta x in parallel, and the row-order
+// chain of a centre is one multiply and one add per row.  In that chain lane
+// (kq, d) = (lane / 16, lane % 16) holds dim d of centres kq, kq + 4, kq + 8,
+// kq + 12 in registers and takes each row's centre and 1 - eta from the row's
+// lane (readlane); the next batch's rows are loaded during this one.
 // The learned codewords replace the codebook, with its |C|^2 / 2 and the
 // bound on max |C| that the PQ encoder uses.
 __global__ __launch_bounds__(64) void k_warm_kmeans(Dims dm, Workspace ws, KmeansBatch kb) {
   __shared__ float s_c[CMAX][DP];
-  __shared__ float s_x[64][DP];
-  __shared__ int s_z[64];
+  __shared__ float s_ex[64][DP];  // eta x of each batch row
+  __shared__ int s_cnt[CMAX];     // count of each centre before the batch
   const int lane = threadIdx.x;
   int id = blockIdx.x;
   const int g = id % G;
@@ -84,47 +91,88 @@ __global__ __launch_bounds__(64) void k_warm_kmeans(Dims dm, Workspace ws, Kmean
   if (N < C) return;  // uniform: too few residuals, the given codebook stays
   const size_t unit = (size_t)kb.sid[e] * dm.units + u;
   const float* res = ws.reservoir + (unit * 2 + side) * (size_t)dm.warm_tokens * D + g * DP;
-  for (int x = lane; x < C * DP; x += 64) s_c[x / DP][x % DP] = res[(size_t)(x / DP) * (N / C) * D + x % DP];
-  int cnt = 0;  // lane k < C: count of centre k
+  for (int x = lane; x < CMAX * DP; x += 64)
+    s_c[x / DP][x % DP] = x < C * DP ? res[(size_t)(x / DP) * (N / C) * D + x % DP] : 0.f;
+  if (lane < CMAX) s_cnt[lane] = 0;
+  const int d = lane & 15, kq = lane >> 4;
+  float cr[CMAX / 4];  // dim d of centres kq + 4 m
   __syncthreads();
+#pragma unroll
+  for (int m = 0; m < CMAX / 4; ++m) cr[m] = s_c[kq + 4 * m][d];
+  const unsigned long long below = (1ull << lane) - 1ull;
   const int B = dm.kmeans_batch;
+  float xn[DP];  // this lane's row of the next batch
+  auto load_row = [&](int b0) {
+    if (lane < min(B, N - b0)) {
+      const float4* src = reinterpret_cast<const float4*>(res + (size_t)(b0 + lane) * D);
+#pragma unroll
+      for (int q = 0; q < DP / 4; ++q) {
+        const float4 v = src[q];
+        xn[4 * q] = v.x; xn[4 * q + 1] = v.y; xn[4 * q + 2] = v.z; xn[4 * q + 3] = v.w;
+      }
+    }
+  };
+  load_row(0);
   for (int ep = 0; ep < dm.kmeans_epochs; ++ep) {
     for (int b0 = 0; b0 < N; b0 += B) {
       const int nb = min(B, N - b0);
-      if (lane < nb) {
-        float x[DP];
-        const float4* src = reinterpret_cast<const float4*>(res + (size_t)(b0 + lane) * D);
+      const bool row = lane < nb;
+      float x[DP];
 #pragma unroll
-        for (int q = 0; q < DP / 4; ++q) {
-          const float4 v = src[q];
-          x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
-        }
-#pragma unroll
-        for (int d = 0; d < DP; ++d) s_x[lane][d] = x[d];
+      for (int q = 0; q < DP; ++q) x[q] = xn[q];
+      if (b0 + B < N) load_row(b0 + B);
+      else if (ep + 1 < dm.kmeans_epochs) load_row(0);
+      int bz = -1;
+      if (row) {
         float best = INFINITY;
-        int bz = 0;
-        for (int k = 0; k < C; ++k) {
-          float acc = 0.f;
+        bz = 0;
 #pragma unroll
-          for (int d = 0; d < DP; ++d) {
-            const float df = x[d] - s_c[k][d];
-            acc = acc + df * df;
-          }
-          if (acc < best) {
-            best = acc;
-            bz = k;
+        for (int k = 0; k < CMAX; ++k) {
+          if (k < C) {
+            float acc = 0.f;
+#pragma unroll
+            for (int q = 0; q < DP; ++q) {
+              const float df = x[q] - s_c[k][q];
+              acc = acc + df * df;
+            }
+            if (acc < best) {
+              best = acc;
+              bz = k;
+            }
           }
         }
-        s_z[lane] = bz;
+      }
+      // rank of this row among the batch's rows of its centre; lane k keeps
+      // the number of rows of centre k
+      int rank = 0, tot = 0;
+      for (int k = 0; k < C; ++k) {
+        const unsigned long long mk = __ballot(bz == k);
+        if (bz == k) rank = __popcll(mk & below);
+        if (lane == k) tot = __popcll(mk);
+      }
+      float om = 0.f;
+      if (row) {
+        const float eta = 1.0f / (float)(s_cnt[bz] + rank + 1);
+        om = 1.0f - eta;
+#pragma unroll
+        for (int q = 0; q < DP; ++q) s_ex[lane][q] = eta * x[q];
       }
       __syncthreads();
+      if (lane < C) s_cnt[lane] += tot;
       for (int i = 0; i < nb; ++i) {
-        const int k = s_z[i];
-        if (lane == k) ++cnt;
-        const int ck = __shfl(cnt, k, 64);
-        const float eta = 1.0f / (float)ck;
-        if (lane < DP) s_c[k][lane] = (1.0f - eta) * s_c[k][lane] + eta * s_x[i][lane];
+        const int z = __builtin_amdgcn_readlane(bz, i);
+        const float omi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(om), i));
+        const float ex = s_ex[i][d];
+        const bool mine = (z & 3) == kq;
+#pragma unroll
+        for (int m = 0; m < CMAX / 4; ++m) {
+          const float v = omi * cr[m] + ex;
+          cr[m] = (mine && (z >> 2) == m) ? v : cr[m];
+        }
       }
+      // the assignments of the next batch read the updated centres
+#pragma unroll
+      for (int m = 0; m < CMAX / 4; ++m) s_c[kq + 4 * m][d] = cr[m];
       __syncthreads();
     }
   }
