@@ -232,8 +232,8 @@ def _cpu_model():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              f"(units are independent and would shard by stream or kv head, see DESIGN.md)",
+        print(f"bench.py: measures one GPU; --gpus {args.gpus} is not supported "
+              f"(units are independent and would shard by stream or kv head)",
               file=sys.stderr)
         sys.exit(2)
     import torch

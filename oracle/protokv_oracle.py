@@ -25,8 +25,7 @@ attn_logit (mass-aware logit); Table tab:default_config for the defaults):
 * readout: softmax attention over [near KV ; pseudo-tokens] with logit bias
   log n_k on the pseudo-tokens of prototype k (Eq. attn_logit).
 
-Readings where the paper is silent or at odds with itself (each is listed
-in DESIGN.md):
+Readings where the paper is silent or at odds with itself:
 
 * centres are running means c_k = sumK_k / n_k (the text's "e.g. via EMA"
   and the merge rule's mass-weighted means), not Alg. 1's fixed-rate EMA;
