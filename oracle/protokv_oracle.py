@@ -504,17 +504,23 @@ def _seed_slot(bank: Bank, k: int, kk: np.ndarray, vv: np.ndarray, coord: np.nda
     bank.tau[k] = pos
 
 
+NEAR_THRESHOLD_REL = 1e-12
+
+
 def _dist2(a: np.ndarray, b: np.ndarray) -> float:
-    """sum_d (a[d] - b[d])^2 for float32 a, b of length 2^m, in float64:
-    each term a rounded difference, then a rounded square; the terms are
-    added as pairs of consecutive dims, then the first half of the partial
-    sums plus the second half, until one is left."""
-    t = (a.astype(np.float64) - b.astype(np.float64)) ** 2
-    s = [t[2 * i] + t[2 * i + 1] for i in range(len(t) // 2)]
-    while len(s) > 1:
-        h = len(s) // 2
-        s = [s[i] + s[i + h] for i in range(h)]
-    return float(s[0])
+    """||a - b||^2 = sum_d (a[d] - b[d])^2 for float32 a, b, in float64 with
+    d ascending (each term a rounded difference, then a rounded square)."""
+    a64, b64 = a.astype(np.float64), b.astype(np.float64)
+    total = 0.0
+    for d in range(len(a64)):
+        diff = a64[d] - b64[d]
+        total += diff * diff
+    return float(total)
+
+
+def _near_threshold(d2: float, eps2: float) -> bool:
+    """The merge test d2 < eps2 is within float64 rounding of flipping."""
+    return abs(d2 - eps2) <= NEAR_THRESHOLD_REL * eps2
 
 
 def maintain(bank: Bank, near: Sequence[Tuple[int, np.ndarray, np.ndarray]], t_frame: int,
@@ -522,14 +528,15 @@ def maintain(bank: Bank, near: Sequence[Tuple[int, np.ndarray, np.ndarray]], t_f
     """One maintenance pass over `bank` (modified in place) at frame t_frame.
 
     near: the near window's frames (frame index, K [T][D], V [T][D]), oldest
-    first.  Returns counts of aged, merged and recycled slots.
+    first.  Returns counts of aged, merged and recycled slots, and of the pair
+    tests that fell within 1e-12 relative of their threshold (near_threshold).
     """
     if p.ema:
         raise ValueError("maintenance is defined for running-mean centres only")
     T = p.tokens_per_frame
     A = int((bank.n > 0).sum())
     assert np.all(bank.n[:A] > 0), "active slots form a prefix"
-    stats = {"aged": 0, "merged": 0, "recycled": 0}
+    stats = {"aged": 0, "merged": 0, "recycled": 0, "near_threshold": 0}
 
     # aging: mass decay of idle prototypes, sums scaled with it
     for k in range(A):
@@ -555,10 +562,14 @@ def maintain(bank: Bank, near: Sequence[Tuple[int, np.ndarray, np.ndarray]], t_f
                 continue
             ni, nj = F32(bank.n[i]), F32(bank.n[j])
             ci, cj = (bank.sum_k[i] / ni).astype(F32), (bank.sum_k[j] / nj).astype(F32)
-            if not _dist2(ci, cj) < ek2:
+            dk = _dist2(ci, cj)
+            stats["near_threshold"] += _near_threshold(dk, ek2)
+            if not dk < ek2:
                 continue
             pi, pj = (bank.sum_v[i] / ni).astype(F32), (bank.sum_v[j] / nj).astype(F32)
-            if not _dist2(pi, pj) < ev2:
+            dv = _dist2(pi, pj)
+            stats["near_threshold"] += _near_threshold(dv, ev2)
+            if not dv < ev2:
                 continue
             wsum = F32(ni + nj)
             for a in range(2):
@@ -713,6 +724,7 @@ class OracleStream:
         self.rings: List[collections.deque] = [collections.deque() for _ in self.units]
         self.frame = 0          # frames appended so far
         self.evicted = 0        # tokens evicted so far (per unit)
+        self.near_threshold = 0  # maintenance pair tests within rounding of a threshold
 
     def append_frame(self, keys: np.ndarray, values: np.ndarray) -> Optional[List[FoldResult]]:
         """Append frame t (keys/values [len(units)][T][D]); if the ring then
@@ -738,7 +750,8 @@ class OracleStream:
                 else:
                     results.append(fold_frame(self.banks[u], ke, ve, fe, t, self.p, self.codebooks[u]))
                 if self.p.maintenance:
-                    maintain(self.banks[u], self.rings[u], t, self.p)
+                    ms = maintain(self.banks[u], self.rings[u], t, self.p)
+                    self.near_threshold += ms["near_threshold"]
             self.folds += 1
             if warm and self.folds == self.p.warm_frames:
                 for u in range(len(self.units)):

@@ -108,7 +108,7 @@ def test_aging_to_zero_recycles_from_the_newest_near_token():
     b = _bank_with(p, rows)
     near = _near(p, t - 1, seed=1) + _near(p, t, seed=2)   # oldest first
     st = O.maintain(b, near, t, p)
-    assert st == {"aged": 1, "merged": 0, "recycled": 1}
+    assert st == {"aged": 1, "merged": 0, "recycled": 1, "near_threshold": 0}
     _, kt, vt = near[-1]
     assert b.n[0] == 1 and b.n_res[0] == 0 and b.tau[0] == t * T
     assert np.array_equal(b.sum_k[0], kt[0]) and np.array_equal(b.sum_v[0], vt[0])
@@ -132,7 +132,7 @@ def test_merge_adds_statistics_and_weights_the_spatial_mean():
     before = b.copy()
     b.sigma[0] = np.array([0.5, 0.125, 0.25], F32)
     st = O.maintain(b, _near(p, t), t, p)
-    assert st == {"aged": 0, "merged": 1, "recycled": 1}
+    assert st == {"aged": 0, "merged": 1, "recycled": 1, "near_threshold": 0}
     assert b.n[0] == 5 and b.n_res[0] == before.n_res[0] + before.n_res[1]
     assert np.array_equal(b.sum_k[0], before.sum_k[0] + before.sum_k[1])
     assert np.array_equal(b.sq_v[0], before.sq_v[0] + before.sq_v[1])
@@ -192,7 +192,7 @@ def test_recycling_takes_near_tokens_newest_frame_first_in_raster_order():
     b = _bank_with(p, rows)
     near = _near(p, t - 1, seed=5) + _near(p, t, seed=6)
     st = O.maintain(b, near, t, p)
-    assert st == {"aged": 0, "merged": 3, "recycled": 3}
+    assert st == {"aged": 0, "merged": 3, "recycled": 3, "near_threshold": 0}
     _, kt, vt = near[-1]
     T = p.tokens_per_frame
     for e, k in enumerate((1, 2, 3)):
