@@ -274,6 +274,83 @@ protokv_status protokv_read_bank(protokv_t h, int32_t stream_id, void* dst, size
 protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float* bias,
                                    void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Stream state (checkpoint / resume).  The state of one stream is what Alg.
+ * "ProtoKV Streaming Update" carries from one token to the next: the near
+ * tier B_near (the ring of the last W frames' exact KV) and the far tier
+ * B_far (the prototype bank), together with the stream's PQ codebooks (the
+ * appendix "PQ codebook initialization" learns them from the stream) and its
+ * position.  A state blob is one contiguous host buffer:
+ *
+ *   offset 0            protokv_state_header
+ *   off_ring_k          kv dtype [units][W+1][T][D]: ring slot f mod (W+1)
+ *                       holds frame f of the last W+1 frames appended
+ *   off_ring_v          likewise for values
+ *   off_bank            [units][capacity] rows of PROTOKV_ROW_BYTES (layout
+ *                       above)
+ *   off_codebooks       float32 [units][2][G][C][D/G] (as protokv_init takes)
+ *   off_reservoir       float32 [units][2][warm_tokens][D]: the warm-up
+ *                       reservoir (present when warm_frames > 0, else 0)
+ *   off_ring_kr         kv dtype [units][W+1][T][D]: the ring's keys rotated
+ *                       at their stream positions (present when
+ *                       rope_theta > 0, else 0)
+ *
+ * units = num_layers * num_kv_heads; every section starts at a multiple of
+ * 256 bytes.  The screening copies of the prototype centres are not part of
+ * the state: protokv_set_state rebuilds them from the bank rows.
+ * --------------------------------------------------------------------------- */
+#define PROTOKV_STATE_MAGIC 0x53564B50u /* "PKVS" */
+#define PROTOKV_STATE_VERSION 1u
+
+typedef struct {
+  uint32_t magic;            /* PROTOKV_STATE_MAGIC */
+  uint32_t version;          /* PROTOKV_STATE_VERSION */
+  uint32_t units;            /* num_layers * num_kv_heads */
+  uint32_t capacity;         /* K */
+  uint32_t tokens_per_frame; /* T */
+  uint32_t window_frames;    /* W */
+  uint32_t kv_bytes;         /* 2 (bf16) or 4 (float32) */
+  uint32_t codewords;        /* C */
+  uint32_t warm_tokens;      /* reservoir rows per unit (0 when warm_frames = 0) */
+  uint32_t rotated;          /* 1 when the rotated-key ring section is present */
+  uint64_t frames;           /* frames appended to the stream */
+  uint64_t evicted_tokens;   /* tokens folded into each unit's bank */
+  int32_t active_slots;      /* slots 0 .. active_slots-1 hold n > 0, the rest n = 0 */
+  int32_t folds;             /* folds done (the first warm_frames are the codebook warm-up) */
+  int32_t reservoir_rows;    /* warm-up reservoir rows filled per unit */
+  int32_t pad;
+  uint64_t off_ring_k, off_ring_v, off_bank, off_codebooks, off_reservoir, off_ring_kr;
+  uint64_t total_bytes;      /* size of the whole blob */
+} protokv_state_header;
+
+/* Size of one stream's state blob for this handle.  Host only. */
+protokv_status protokv_state_size(protokv_t h, size_t* bytes);
+
+/* Copies the state of `stream_id` into host_buf (bytes = protokv_state_size).
+ * Errors: PROTOKV_E_STATE if the stream has an unfolded eviction.
+ * Synchronizes `stream`. */
+protokv_status protokv_get_state(protokv_t h, int32_t stream_id, void* host_buf, size_t bytes,
+                                 void* stream);
+
+/* Replaces the state of `stream_id` with a blob (bytes = protokv_state_size)
+ * made by protokv_get_state on a handle of the same configuration, or built
+ * by the caller to the layout above.  Checked on the host before anything
+ * is copied (PROTOKV_E_INVALID: wrong magic, version or shape, a count out of
+ * range, n > 0 outside the active prefix, a bank inconsistent with the
+ * stream position); the stream must have no unfolded eviction
+ * (PROTOKV_E_STATE).  Rebuilds the screening copies of every slot from the
+ * bank rows and invalidates any synthesis of the stream.  Synchronizes
+ * `stream`. */
+protokv_status protokv_set_state(protokv_t h, int32_t stream_id, const void* host_buf, size_t bytes,
+                                 void* stream);
+
+/* Largest number of evicted tokens per (layer, kv head) a stream may reach:
+ * the exact top-S decode multiplies eight factors H + 1 < 2^24 into a
+ * 192-bit integer, and a residual count H never exceeds the tokens evicted,
+ * so protokv_append_frame rejects (PROTOKV_E_UNSUPPORTED) an append that
+ * would make the stream evict more than this.  Host only. */
+#define PROTOKV_MAX_EVICTED_TOKENS 16777214ull
+
 /* Kernel ids of protokv_kernel_times. */
 enum {
   PROTOKV_K_RING_INSERT = 0,

@@ -325,6 +325,9 @@ def pq_encode(residuals: np.ndarray, codebook: np.ndarray) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 
+NEAR_TIE = 1e-6   # a top-2 cost margin below this is a near tie (counted, either slot valid)
+
+
 @dataclasses.dataclass
 class FoldResult:
     assign: np.ndarray      # slot per evicted token (seeded tokens: their slot)
@@ -333,14 +336,26 @@ class FoldResult:
     # with collect=True: key and value residuals of the non-seed tokens in
     # eviction order, against the snapshot centres
     residuals: Optional[Tuple[np.ndarray, np.ndarray]] = None
+    # Eq. 1 costs of the non-seed tokens (rows: tokens n_seed..T-1, +inf for
+    # inactive slots)
+    cost: Optional[np.ndarray] = None
+
+    @property
+    def near_ties(self) -> int:
+        return int((self.margin < NEAR_TIE).sum())
 
 
 def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
-               t_frame: int, p: Params, codebooks: np.ndarray, collect: bool = False) -> FoldResult:
+               t_frame: int, p: Params, codebooks: np.ndarray, collect: bool = False,
+               choose: Optional[np.ndarray] = None) -> FoldResult:
     """Absorb the evicted frame f_evicted (tokens j = 0..T-1 in raster order)
     into `bank` (modified in place).  t_frame is the frame being appended.
 
     codebooks float32 [2][G][C][D/G] (keys, values) of this (layer, head).
+    choose: optionally a slot for every token of the frame; a non-seed token
+    takes it in place of the lowest argmin, which is allowed only where the
+    two costs lie within NEAR_TIE of each other (a near tie, where either
+    slot is a valid argmin of Eq. 1); any other choice raises ValueError.
     """
     T = keys.shape[0]
     coords = spatial_coords(p.grid_h, p.grid_w)
@@ -379,6 +394,15 @@ def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
     rest = np.arange(n_seed, T)
     cost = assignment_costs(keys[rest], coords[rest], snap, t_frame, p)
     idx, marg = argmin_lowest(cost)
+    if choose is not None:
+        want = np.asarray(choose, dtype=np.int64)[rest]
+        for i, k in enumerate(want):
+            if k == idx[i]:
+                continue
+            if not (0 <= k < p.capacity and np.isfinite(cost[i, k])
+                    and cost[i, k] - cost[i, idx[i]] < NEAR_TIE):
+                raise ValueError(f"token {rest[i]}: slot {k} is not a near-tie argmin of Eq. 1")
+        idx = want
     assign[rest] = idx
     margin[rest] = marg
 
@@ -433,7 +457,7 @@ def fold_frame(bank: Bank, keys: np.ndarray, values: np.ndarray, f_evicted: int,
         bank.sigma[k, 1] = F32(F32(keep * sxy) + F32(eta * F32(ddx * ddy)))
         bank.sigma[k, 2] = F32(F32(keep * syy) + F32(eta * F32(ddy * ddy)))
         bank.tau[k] = pos[j]
-    return FoldResult(assign, margin, n_seed, (r_k, r_v) if collect else None)
+    return FoldResult(assign, margin, n_seed, (r_k, r_v) if collect else None, cost)
 
 
 # ---------------------------------------------------------------------------

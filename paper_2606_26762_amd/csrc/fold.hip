@@ -252,6 +252,28 @@ hipError_t launch_seed(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
 }
 
 // ---------------------------------------------------------------------------
+// Screening copies of every slot of one stream's units rebuilt from their bank
+// rows (after the stream's state was replaced).  One wave per slot.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_refresh_all(Dims dm, Workspace ws, int sid) {
+  const int lane = threadIdx.x & 63;
+  const size_t gs = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (gs >= (size_t)dm.units * dm.K) return;
+  const int u = (int)(gs / dm.K), k = (int)(gs % dm.K);
+  const size_t unit = (size_t)sid * dm.units + u;
+  const uint8_t* row = ws.bank + (unit * dm.K + k) * ROW;
+  const float2 sk = reinterpret_cast<const float2*>(row + ROW_SUMK)[lane];
+  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  refresh_cache(dm, sk, m, unit, k, ws, lane);
+}
+
+hipError_t launch_refresh_all(const Dims& dm, const Workspace& ws, int sid, hipStream_t st) {
+  const size_t slots = (size_t)dm.units * dm.K;
+  hipLaunchKernelGGL(k_refresh_all, dim3((unsigned)((slots + 3) / 4)), dim3(256), 0, st, dm, ws, sid);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Exact cost of Eq. 1 in float64, same formula and operation order as the
 // oracle: cos from sumK, unsquared Mahalanobis with ridge, idle indicator.
 // ---------------------------------------------------------------------------

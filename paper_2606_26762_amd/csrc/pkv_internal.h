@@ -162,13 +162,14 @@ struct AttendArgs {
 };
 
 // 16 bytes per lane from global memory straight into LDS at lds + 16 * lane
-// (global_load_lds_dwordx4; M0 holds the wave-uniform LDS byte address).
-// Issued as inline asm so the compiler does not treat later LDS reads of
-// other buffers as dependent on it: completion is awaited explicitly with
+// (global_load_lds_dwordx4; M0 holds the wave-uniform LDS byte address, passed
+// as an input operand bound to M0 so the compiler sets it and knows it is
+// read).  Issued as inline asm so the compiler does not treat later LDS reads
+// of other buffers as dependent on it: completion is awaited explicitly with
 // wait_vm before the barrier that publishes a tile.
 __device__ __forceinline__ void lds_dma16(const void* g, void* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0) : "memory", "m0");
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(m0) : "memory");
 }
 // s_waitcnt vmcnt(n) (expcnt / lgkmcnt not waited for)
 template <int N>
@@ -187,6 +188,8 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb,
                             hipStream_t st);
 hipError_t launch_maintain(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st);
+// screening copies of every slot of stream sid rebuilt from its bank rows
+hipError_t launch_refresh_all(const Dims& dm, const Workspace& ws, int sid, hipStream_t st);
 // centres: also write the float32 centres (pcen) and biases for the readout's
 // row forming; wide: some slot may hold more than 65534 residuals (the
 // 192-bit path runs too)

@@ -81,6 +81,63 @@ Layout make_layout(const protokv_config& c) {
   return ly;
 }
 
+// One stream's state blob (protokv.h): header, then 256-byte aligned sections.
+struct StateLayout {
+  size_t ring_k, ring_v, bank, codebooks, reservoir, ring_kr, total;
+};
+
+StateLayout state_layout(const protokv_config& c) {
+  StateLayout sl{};
+  size_t off = 256;  // the header, padded
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += (bytes + 255) & ~(size_t)255;
+    return bytes ? o : (size_t)0;
+  };
+  const size_t units = (size_t)c.num_layers * c.num_kv_heads;
+  const size_t T = (size_t)c.grid_h * c.grid_w;
+  const size_t ring = units * (c.window_frames + 1) * T * D * kv_bytes(c);
+  sl.ring_k = take(ring);
+  sl.ring_v = take(ring);
+  sl.bank = take(units * c.capacity * ROW);
+  sl.codebooks = take(units * 2 * G * (size_t)c.pq_codewords * DP * 4);
+  sl.reservoir = take(c.warm_frames > 0 ? units * 2 * (size_t)c.warm_tokens * D * 4 : 0);
+  sl.ring_kr = take(c.rope_theta > 0.0 ? ring : 0);
+  sl.total = off;
+  return sl;
+}
+
+// Per codeword |C|^2 / 2 and per (K/V, subspace) a bound on max |C| of
+// codebooks padded to CMAX codewords, for the PQ encoder's error bound
+// (float32, sequential fused multiply-add).
+void codebook_tables(const std::vector<float>& cb, int C, std::vector<float>& hn, std::vector<float>& cmax) {
+  const size_t blocks = cb.size() / (CMAX * DP);
+  hn.assign(blocks * CMAX, 0.f);
+  cmax.assign(blocks, 0.f);
+  for (size_t blk = 0; blk < blocks; ++blk) {
+    float m = 0.f;
+    for (int cc = 0; cc < CMAX; ++cc) {
+      float n2 = 0.f;
+      for (int q = 0; q < DP; ++q) n2 = std::fma(cb[(blk * CMAX + cc) * DP + q], cb[(blk * CMAX + cc) * DP + q], n2);
+      hn[blk * CMAX + cc] = cc < C ? 0.5f * n2 : INFINITY;
+      if (cc < C) m = std::max(m, n2);
+    }
+    cmax[blk] = std::sqrt(m) * 1.0001f;
+  }
+}
+
+// Codebooks [units][2][G][C][DP] -> the padded device layout [units][2][G][CMAX][DP].
+std::vector<float> pad_codebooks(const float* codebooks, size_t units, int C) {
+  std::vector<float> cb(units * 2 * G * CMAX * DP, 0.f);
+  for (size_t uu = 0; uu < units; ++uu)
+    for (int kv = 0; kv < 2; ++kv)
+      for (int g = 0; g < G; ++g)
+        for (int cc = 0; cc < C; ++cc)
+          std::memcpy(&cb[(((uu * 2 + kv) * G + g) * CMAX + cc) * DP],
+                      &codebooks[(((uu * 2 + kv) * G + g) * C + cc) * DP], DP * sizeof(float));
+  return cb;
+}
+
 protokv_status check_config(const protokv_config* c, std::string& why) {
   if (!c) { why = "config is NULL"; return PROTOKV_E_INVALID; }
   auto bad = [&](const char* m) { why = m; return PROTOKV_E_INVALID; };
@@ -329,27 +386,8 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
 
   // codebooks -> [U][2][G][CMAX][DP] with the codeword axis padded to 16
   const size_t U = (size_t)c->num_streams * dm.units;
-  const int C = c->pq_codewords;
-  std::vector<float> cb(U * 2 * G * CMAX * DP, 0.f);
-  for (size_t uu = 0; uu < U; ++uu)
-    for (int kv = 0; kv < 2; ++kv)
-      for (int g = 0; g < G; ++g)
-        for (int cc = 0; cc < C; ++cc)
-          std::memcpy(&cb[(((uu * 2 + kv) * G + g) * CMAX + cc) * DP],
-                      &codebooks[(((uu * 2 + kv) * G + g) * C + cc) * DP], DP * sizeof(float));
-  // per codeword |C|^2 / 2 and per (K/V, subspace) a bound on max |C|, for the
-  // PQ encoder's error bound (float32, sequential fused multiply-add)
-  std::vector<float> hn(U * 2 * G * CMAX), cmax(U * 2 * G);
-  for (size_t blk = 0; blk < U * 2 * G; ++blk) {
-    float m = 0.f;
-    for (int cc = 0; cc < CMAX; ++cc) {
-      float n2 = 0.f;
-      for (int q = 0; q < DP; ++q) n2 = std::fma(cb[(blk * CMAX + cc) * DP + q], cb[(blk * CMAX + cc) * DP + q], n2);
-      hn[blk * CMAX + cc] = cc < C ? 0.5f * n2 : INFINITY;
-      if (cc < C) m = std::max(m, n2);
-    }
-    cmax[blk] = std::sqrt(m) * 1.0001f;
-  }
+  std::vector<float> cb = pad_codebooks(codebooks, U, c->pq_codewords), hn, cmax;
+  codebook_tables(cb, c->pq_codewords, hn, cmax);
   hipError_t e = hipMemsetAsync(workspace, 0, ly.total, hs);
   if (e == hipSuccess) e = hipMemcpyAsync(ws.codebooks, cb.data(), cb.size() * sizeof(float),
                                           hipMemcpyHostToDevice, hs);
@@ -392,6 +430,11 @@ protokv_status protokv_append_frame(protokv_t h, const int32_t* ids, int32_t n, 
     if (h->st[s].pending) return h->fail(PROTOKV_E_STATE, "append: stream has an unfolded eviction; call protokv_fold");
     if ((h->st[s].frames + 2) * (uint64_t)h->dm.T >= (1ull << 31))
       return h->fail(PROTOKV_E_UNSUPPORTED, "append: stream position exceeds 2^31 tokens");
+    if (h->st[s].frames + 1 > (uint64_t)h->dm.W &&
+        h->st[s].evicted + (uint64_t)h->dm.T > PROTOKV_MAX_EVICTED_TOKENS)
+      return h->fail(PROTOKV_E_UNSUPPORTED,
+                     "append: the stream would evict more than PROTOKV_MAX_EVICTED_TOKENS tokens per unit "
+                     "(the exact decode's 192-bit products)");
   }
   hipStream_t hs = (hipStream_t)stream;
   const size_t entry_bytes = (size_t)h->dm.units * h->dm.T * D * kv_bytes(h->cfg);
@@ -698,6 +741,170 @@ protokv_status protokv_read_pseudo(protokv_t h, void* keys, void* values, float*
   if (s == PROTOKV_OK && values) s = copy_out(h, values, h->ws.pv, n, stream, "read_pseudo");
   if (s == PROTOKV_OK && bias) s = copy_out(h, bias, h->ws.pbias, (size_t)h->dm.units * h->dm.K * 4, stream, "read_pseudo");
   return s;
+}
+
+protokv_status protokv_state_size(protokv_t h, size_t* bytes) {
+  if (!h || !bytes) return PROTOKV_E_INVALID;
+  *bytes = state_layout(h->cfg).total;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_get_state(protokv_t h, int32_t sid, void* buf, size_t bytes, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (sid < 0 || sid >= h->cfg.num_streams || !buf) return h->fail(PROTOKV_E_INVALID, "get_state: bad stream or buffer");
+  const StateLayout sl = state_layout(h->cfg);
+  if (bytes != sl.total) return h->fail(PROTOKV_E_INVALID, "get_state: bytes must equal protokv_state_size");
+  const StreamState& ss = h->st[sid];
+  if (ss.pending) return h->fail(PROTOKV_E_STATE, "get_state: stream has an unfolded eviction");
+  const Dims& dm = h->dm;
+  const size_t units = dm.units, es = kv_bytes(h->cfg);
+  const size_t ring = units * (dm.W + 1) * dm.T * D * es;
+  uint8_t* out = (uint8_t*)buf;
+  std::memset(out, 0, 256);
+  protokv_state_header hd{};
+  hd.magic = PROTOKV_STATE_MAGIC;
+  hd.version = PROTOKV_STATE_VERSION;
+  hd.units = (uint32_t)units;
+  hd.capacity = (uint32_t)dm.K;
+  hd.tokens_per_frame = (uint32_t)dm.T;
+  hd.window_frames = (uint32_t)dm.W;
+  hd.kv_bytes = (uint32_t)es;
+  hd.codewords = (uint32_t)dm.C;
+  hd.warm_tokens = dm.warm_frames > 0 ? (uint32_t)dm.warm_tokens : 0u;
+  hd.rotated = h->ws.ring_kr ? 1u : 0u;
+  hd.frames = ss.frames;
+  hd.evicted_tokens = ss.evicted;
+  hd.active_slots = ss.active;
+  hd.folds = ss.folds;
+  hd.reservoir_rows = ss.rfill;
+  hd.off_ring_k = sl.ring_k;
+  hd.off_ring_v = sl.ring_v;
+  hd.off_bank = sl.bank;
+  hd.off_codebooks = sl.codebooks;
+  hd.off_reservoir = sl.reservoir;
+  hd.off_ring_kr = sl.ring_kr;
+  hd.total_bytes = sl.total;
+  std::memcpy(out, &hd, sizeof(hd));
+  hipStream_t hs = (hipStream_t)stream;
+  std::vector<float> cbp(units * 2 * G * CMAX * DP);
+  hipError_t e = hipMemcpyAsync(out + sl.ring_k, h->ws.ring_k + sid * ring, ring, hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(out + sl.ring_v, h->ws.ring_v + sid * ring, ring, hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(out + sl.bank, h->ws.bank + (size_t)sid * units * dm.K * ROW, units * dm.K * ROW,
+                       hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(cbp.data(), h->ws.codebooks + (size_t)sid * cbp.size(), cbp.size() * 4,
+                       hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess && sl.reservoir) {
+    const size_t rb = units * 2 * (size_t)dm.warm_tokens * D * 4;
+    e = hipMemcpyAsync(out + sl.reservoir, (uint8_t*)h->ws.reservoir + sid * rb, rb, hipMemcpyDeviceToHost, hs);
+  }
+  if (e == hipSuccess && sl.ring_kr)
+    e = hipMemcpyAsync(out + sl.ring_kr, h->ws.ring_kr + sid * ring, ring, hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return h->dev(e, "get_state");
+  float* cbo = (float*)(out + sl.codebooks);
+  for (size_t blk = 0; blk < units * 2 * G; ++blk)
+    std::memcpy(cbo + blk * dm.C * DP, cbp.data() + blk * CMAX * DP, (size_t)dm.C * DP * sizeof(float));
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_set_state(protokv_t h, int32_t sid, const void* buf, size_t bytes, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (sid < 0 || sid >= h->cfg.num_streams || !buf) return h->fail(PROTOKV_E_INVALID, "set_state: bad stream or buffer");
+  const StateLayout sl = state_layout(h->cfg);
+  if (bytes != sl.total) return h->fail(PROTOKV_E_INVALID, "set_state: bytes must equal protokv_state_size");
+  if (h->st[sid].pending) return h->fail(PROTOKV_E_STATE, "set_state: stream has an unfolded eviction");
+  const Dims& dm = h->dm;
+  const size_t units = dm.units, es = kv_bytes(h->cfg);
+  const uint8_t* in = (const uint8_t*)buf;
+  protokv_state_header hd;
+  std::memcpy(&hd, in, sizeof(hd));
+  auto bad = [&](const char* m) { return h->fail(PROTOKV_E_INVALID, std::string("set_state: ") + m); };
+  if (hd.magic != PROTOKV_STATE_MAGIC || hd.version != PROTOKV_STATE_VERSION) return bad("not a state blob");
+  if (hd.units != units || hd.capacity != (uint32_t)dm.K || hd.tokens_per_frame != (uint32_t)dm.T ||
+      hd.window_frames != (uint32_t)dm.W || hd.kv_bytes != es || hd.codewords != (uint32_t)dm.C ||
+      hd.warm_tokens != (dm.warm_frames > 0 ? (uint32_t)dm.warm_tokens : 0u) ||
+      hd.rotated != (h->ws.ring_kr ? 1u : 0u))
+    return bad("shape differs from the handle's configuration");
+  if (hd.off_ring_k != sl.ring_k || hd.off_ring_v != sl.ring_v || hd.off_bank != sl.bank ||
+      hd.off_codebooks != sl.codebooks || hd.off_reservoir != sl.reservoir || hd.off_ring_kr != sl.ring_kr ||
+      hd.total_bytes != sl.total)
+    return bad("section offsets differ from the layout");
+  const uint64_t W = (uint64_t)dm.W, T = (uint64_t)dm.T;
+  const uint64_t folds = hd.frames > W ? hd.frames - W : 0;
+  if ((hd.frames + 1) * T >= (1ull << 31)) return bad("stream position beyond 2^31 tokens");
+  if (hd.evicted_tokens != folds * T || (uint64_t)hd.folds != folds)
+    return bad("evicted_tokens and folds must follow from frames");
+  if (hd.evicted_tokens > PROTOKV_MAX_EVICTED_TOKENS) return bad("evicted_tokens above PROTOKV_MAX_EVICTED_TOKENS");
+  if (hd.active_slots < 0 || (uint64_t)hd.active_slots > std::min<uint64_t>(dm.K, hd.evicted_tokens))
+    return bad("active_slots outside [0, min(capacity, evicted_tokens)]");
+  if (hd.reservoir_rows < 0 || hd.reservoir_rows > (dm.warm_frames > 0 ? dm.warm_tokens : 0))
+    return bad("reservoir_rows outside [0, warm_tokens]");
+  // bank rows: n > 0 exactly on the active prefix, histogram rows summing to
+  // n_res, no counts beyond C codewords, recency within the stream
+  const uint8_t* bank = in + sl.bank;
+  for (size_t u = 0; u < units; ++u)
+    for (int k = 0; k < dm.K; ++k) {
+      const uint8_t* row = bank + (u * dm.K + k) * ROW;
+      RowMeta m;
+      std::memcpy(&m, row + ROW_META, sizeof(m));
+      if ((m.n > 0) != (k < hd.active_slots)) return bad("n > 0 must hold exactly on slots [0, active_slots)");
+      if (m.n == 0) continue;
+      if (m.n_res > hd.evicted_tokens) return bad("n_res above the tokens evicted");
+      if (m.tau < 0 || (uint64_t)m.tau >= hd.evicted_tokens + W * T) return bad("tau outside the stream");
+      for (int side = 0; side < 2; ++side) {
+        const uint32_t* hist = (const uint32_t*)(row + (side ? ROW_HV : ROW_HK));
+        for (int g = 0; g < G; ++g) {
+          uint64_t tot = 0;
+          for (int c = 0; c < CMAX; ++c) {
+            if (c >= dm.C && hist[g * CMAX + c]) return bad("histogram count beyond C codewords");
+            tot += hist[g * CMAX + c];
+          }
+          if ((dm.flags & PROTOKV_FLAG_PQ) && tot != m.n_res) return bad("a histogram row does not sum to n_res");
+        }
+      }
+    }
+  const float* cbi = (const float*)(in + sl.codebooks);
+  for (size_t i = 0; i < units * 2 * G * (size_t)dm.C * DP; ++i)
+    if (!std::isfinite(cbi[i])) return bad("non-finite codebook entry");
+  std::vector<float> cb = pad_codebooks(cbi, units, dm.C), hn, cmax;
+  codebook_tables(cb, dm.C, hn, cmax);
+  hipStream_t hs = (hipStream_t)stream;
+  const size_t ring = units * (dm.W + 1) * dm.T * D * es;
+  hipError_t e = hipMemcpyAsync(h->ws.ring_k + sid * ring, in + sl.ring_k, ring, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(h->ws.ring_v + sid * ring, in + sl.ring_v, ring, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(h->ws.bank + (size_t)sid * units * dm.K * ROW, bank, units * dm.K * ROW,
+                       hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(h->ws.codebooks + (size_t)sid * cb.size(), cb.data(), cb.size() * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(h->ws.cbhn + (size_t)sid * hn.size(), hn.data(), hn.size() * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(h->ws.cbmax + (size_t)sid * cmax.size(), cmax.data(), cmax.size() * 4,
+                       hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess && sl.reservoir) {
+    const size_t rb = units * 2 * (size_t)dm.warm_tokens * D * 4;
+    e = hipMemcpyAsync((uint8_t*)h->ws.reservoir + sid * rb, in + sl.reservoir, rb, hipMemcpyHostToDevice, hs);
+  }
+  if (e == hipSuccess && sl.ring_kr)
+    e = hipMemcpyAsync(h->ws.ring_kr + sid * ring, in + sl.ring_kr, ring, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = launch_refresh_all(dm, h->ws, sid, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return h->dev(e, "set_state");
+  StreamState& ss = h->st[sid];
+  ss.frames = hd.frames;
+  ss.evicted = hd.evicted_tokens;
+  ss.active = hd.active_slots;
+  ss.folds = hd.folds;
+  ss.rfill = hd.reservoir_rows;
+  ss.pending = false;
+  ss.pending_fe = -1;
+  if (h->synth_stream == sid) h->synth_stream = -1;
+  return PROTOKV_OK;
 }
 
 protokv_status protokv_profile(protokv_t h, uint32_t kernel_mask) {

@@ -27,8 +27,11 @@ EXPORTED = [
     "protokv_destroy", "protokv_append_frame", "protokv_fold", "protokv_synthesize", "protokv_attend",
     "protokv_stream_info_get", "protokv_get_counters", "protokv_read_assignments", "protokv_read_bank",
     "protokv_read_pseudo", "protokv_read_codebooks", "protokv_profile", "protokv_profile_read",
-    "protokv_last_error",
+    "protokv_state_size", "protokv_get_state", "protokv_set_state", "protokv_last_error",
 ]
+
+STATE_MAGIC, STATE_VERSION = 0x53564B50, 1
+MAX_EVICTED_TOKENS = 16777214
 
 KERNELS = ["ring_insert", "seed", "screen", "aggregate", "decode", "attend", "attend_merge", "pq_encode",
            "materialize", "maintain", "rope_ring", "rope_q", "warm_collect", "warm_kmeans"]
@@ -71,6 +74,19 @@ class Counters(ctypes.Structure):
                 ("recycled", ctypes.c_uint64)]
 
 
+class StateHeader(ctypes.Structure):
+    _fields_ = [("magic", ctypes.c_uint32), ("version", ctypes.c_uint32), ("units", ctypes.c_uint32),
+                ("capacity", ctypes.c_uint32), ("tokens_per_frame", ctypes.c_uint32),
+                ("window_frames", ctypes.c_uint32), ("kv_bytes", ctypes.c_uint32),
+                ("codewords", ctypes.c_uint32), ("warm_tokens", ctypes.c_uint32), ("rotated", ctypes.c_uint32),
+                ("frames", ctypes.c_uint64), ("evicted_tokens", ctypes.c_uint64),
+                ("active_slots", ctypes.c_int32), ("folds", ctypes.c_int32),
+                ("reservoir_rows", ctypes.c_int32), ("pad", ctypes.c_int32),
+                ("off_ring_k", ctypes.c_uint64), ("off_ring_v", ctypes.c_uint64), ("off_bank", ctypes.c_uint64),
+                ("off_codebooks", ctypes.c_uint64), ("off_reservoir", ctypes.c_uint64),
+                ("off_ring_kr", ctypes.c_uint64), ("total_bytes", ctypes.c_uint64)]
+
+
 class KernelTimes(ctypes.Structure):
     _fields_ = [("ms", ctypes.c_double * 16), ("launches", ctypes.c_uint64 * 16)]
 
@@ -103,6 +119,9 @@ def lib() -> ctypes.CDLL:
         L.protokv_read_codebooks.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_profile.argtypes = [vp, ctypes.c_uint32]
         L.protokv_profile_read.argtypes = [vp, P(KernelTimes)]
+        L.protokv_state_size.argtypes = [vp, P(sz)]
+        L.protokv_get_state.argtypes = [vp, i32, vp, sz, vp]
+        L.protokv_set_state.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_last_error.argtypes = [vp]
         L.protokv_last_error.restype = ctypes.c_char_p
         for name in EXPORTED:
@@ -154,6 +173,76 @@ def decode_bank(raw: np.ndarray, units: int, capacity: int) -> Dict[str, np.ndar
         "mu": meta[:, :, 8:16].view(np.float32), "sigma": meta[:, :, 16:28].view(np.float32),
         "tau": meta[:, :, 28:32].view(np.int32)[..., 0],
     }
+
+
+def encode_bank(bank: Dict[str, np.ndarray], units: int, capacity: int) -> np.ndarray:
+    """The documented bank row layout (uint8 [units*capacity*3200]) from arrays
+    shaped as decode_bank returns them (histograms [units][K][G][C], C <= 16)."""
+    rows = np.zeros((units, capacity, ROW_BYTES), dtype=np.uint8)
+
+    def put(a, b, arr, dt):
+        rows[:, :, a:b] = np.ascontiguousarray(np.asarray(arr, dtype=dt).reshape(units, capacity, -1)).view(np.uint8)
+    put(0, 512, bank["sum_k"], np.float32)
+    put(512, 1024, bank["sum_v"], np.float32)
+    put(1024, 1536, bank["sq_k"], np.float32)
+    put(1536, 2048, bank["sq_v"], np.float32)
+    for name, a in (("hist_k", 2048), ("hist_v", 2560)):
+        h = np.zeros((units, capacity, 8, 16), dtype=np.uint32)
+        src = np.asarray(bank[name])
+        h[..., :src.shape[-1]] = src
+        put(a, a + 512, h, np.uint32)
+    put(3072, 3076, bank["n"], np.uint32)
+    put(3076, 3080, bank["n_res"], np.uint32)
+    put(3080, 3088, bank["mu"], np.float32)
+    put(3088, 3100, bank["sigma"], np.float32)
+    put(3100, 3104, bank["tau"], np.int32)
+    return rows.reshape(-1)
+
+
+class State:
+    """One stream's state blob (protokv.h) with views of its sections."""
+
+    def __init__(self, blob: np.ndarray, kv_dtype: str):
+        self.blob = blob
+        self.header = StateHeader.from_buffer_copy(blob[:ctypes.sizeof(StateHeader)].tobytes())
+        h = self.header
+        if h.magic != STATE_MAGIC:
+            raise ValueError("not a protokv state blob")
+        self.kv_dtype = kv_dtype
+        T, W, U = h.tokens_per_frame, h.window_frames, h.units
+        ring = U * (W + 1) * T * 128 * h.kv_bytes
+        self._ring_shape = (U, W + 1, T, 128)
+        self._ring_bytes = ring
+
+    def _section(self, off, nbytes):
+        return self.blob[off:off + nbytes]
+
+    def ring(self, which: str = "k") -> np.ndarray:
+        """The ring as float32 [units][W+1][T][D] (a copy)."""
+        off = {"k": self.header.off_ring_k, "v": self.header.off_ring_v, "kr": self.header.off_ring_kr}[which]
+        raw = self._section(off, self._ring_bytes)
+        if self.header.kv_bytes == 4:
+            return raw.view(np.float32).reshape(self._ring_shape).copy()
+        return (raw.view(np.uint16).astype(np.uint32) << 16).view(np.float32).reshape(self._ring_shape)
+
+    def bank(self) -> Dict[str, np.ndarray]:
+        h = self.header
+        return decode_bank(self._section(h.off_bank, h.units * h.capacity * ROW_BYTES), h.units, h.capacity)
+
+    def set_bank_rows(self, unit: int, rows: np.ndarray):
+        """Replace the rows of one unit (uint8 [capacity * 3200])."""
+        h = self.header
+        n = h.capacity * ROW_BYTES
+        self.blob[h.off_bank + unit * n:h.off_bank + (unit + 1) * n] = rows
+
+    def set_active_slots(self, n: int):
+        self.header.active_slots = n
+        self.blob[:ctypes.sizeof(StateHeader)] = np.frombuffer(bytes(self.header), dtype=np.uint8)
+
+    def codebooks(self) -> np.ndarray:
+        h = self.header
+        n = h.units * 2 * 8 * h.codewords * 16
+        return self._section(h.off_codebooks, n * 4).view(np.float32).reshape(h.units, 2, 8, h.codewords, 16)
 
 
 class ProtoKV:
@@ -261,6 +350,20 @@ class ProtoKV:
             (lambda r: (r.astype(np.uint32) << 16).view(np.float32))
         shape = (self.units, self.cfg.capacity * self.cfg.pseudo_per_proto, self.cfg.head_dim)
         return conv(raw_k).reshape(shape), conv(raw_v).reshape(shape), bias.reshape(self.units, -1)
+
+    def state_size(self) -> int:
+        n = ctypes.c_size_t()
+        _check(lib().protokv_state_size(self.h, ctypes.byref(n)), self.h)
+        return n.value
+
+    def get_state(self, stream_id: int, stream=None) -> State:
+        blob = np.zeros(self.state_size(), dtype=np.uint8)
+        _check(lib().protokv_get_state(self.h, stream_id, blob.ctypes.data, blob.size, _stream_ptr(stream)), self.h)
+        return State(blob, "fp32" if self.cfg.kv_dtype == KV_FP32 else "bf16")
+
+    def set_state(self, stream_id: int, state, stream=None):
+        blob = np.ascontiguousarray(state.blob if isinstance(state, State) else state, dtype=np.uint8)
+        _check(lib().protokv_set_state(self.h, stream_id, blob.ctypes.data, blob.size, _stream_ptr(stream)), self.h)
 
     def profile(self, enable, kernels=None):
         """Time every launch (enable=True), only the named kernels, or stop (False)."""

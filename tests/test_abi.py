@@ -94,3 +94,37 @@ def test_workspace_size_scales_with_shape():
     assert full > 112 * (9 * 196 * 128 * 4 + 256 * 3200)
     with pytest.raises(pk.ProtoKVError):
         pk.workspace_size(pk.default_config(head_dim=96))
+
+
+def test_state_header_and_bank_encoding_round_trip():
+    """The state header is 128 bytes with the documented field order, and the
+    bank encoder writes the documented row layout that decode_bank reads."""
+    import ctypes
+    import numpy as np
+    assert ctypes.sizeof(pk.StateHeader) == 128
+    assert pk.StateHeader.off_ring_k.offset == 72 and pk.StateHeader.total_bytes.offset == 120
+    rng = np.random.default_rng(0)
+    U, K = 3, 5
+    bank = {"sum_k": rng.standard_normal((U, K, 128)).astype(np.float32),
+            "sum_v": rng.standard_normal((U, K, 128)).astype(np.float32),
+            "sq_k": rng.random((U, K, 128)).astype(np.float32),
+            "sq_v": rng.random((U, K, 128)).astype(np.float32),
+            "hist_k": rng.integers(0, 9, (U, K, 8, 12)).astype(np.uint32),
+            "hist_v": rng.integers(0, 9, (U, K, 8, 12)).astype(np.uint32),
+            "n": rng.integers(0, 99, (U, K)).astype(np.uint32),
+            "n_res": rng.integers(0, 99, (U, K)).astype(np.uint32),
+            "mu": rng.random((U, K, 2)).astype(np.float32),
+            "sigma": rng.random((U, K, 3)).astype(np.float32),
+            "tau": rng.integers(0, 999, (U, K)).astype(np.int32)}
+    raw = pk.encode_bank(bank, U, K)
+    assert raw.size == U * K * 3200
+    back = pk.decode_bank(raw, U, K)
+    for name, want in bank.items():
+        got = back[name][..., :want.shape[-1]] if name.startswith("hist") else back[name]
+        assert np.array_equal(got, want), name
+    assert not back["hist_k"][..., 12:].any()
+    # field offsets of the documented row
+    row = raw.reshape(U, K, 3200)[1, 2]
+    assert row[3072:3076].view(np.uint32)[0] == bank["n"][1, 2]
+    assert row[3100:3104].view(np.int32)[0] == bank["tau"][1, 2]
+    assert np.array_equal(row[512:1024].view(np.float32), bank["sum_v"][1, 2])

@@ -44,6 +44,7 @@ def test_tiny_stream_fp32_full():
     h.log(f"assignments checked {pair.assign_checked}, near ties {pair.near_ties}, "
           f"refined {c.refined}+{c.refined_full}, readout max abs err {worst:.2e}")
     assert pair.assign_checked == (wl.frames - wl.window_frames) * wl.tokens_per_frame
+    pair.check_near_tie_counter()
 
 
 def test_7b_shape_one_layer():
@@ -61,6 +62,7 @@ def test_7b_shape_one_layer():
     c = pair.gpu.counters()
     h.log(f"assignments {pair.assign_checked}, near ties {pair.near_ties}, refined {c.refined}"
           f"+{c.refined_full}, touched {c.touched}, readout err {worst:.2e}")
+    pair.check_near_tie_counter()
 
 
 def test_maximum_frame_and_query_sizes():
@@ -99,6 +101,7 @@ def test_ragged_shapes_seed_and_assign_same_fold():
         if f == wl.window_frames:
             pair.check_bank(bitwise=True)
     pair.check_bank(bitwise=True)
+    pair.check_near_tie_counter()
     pseudo = pair.synthesize()
     for tq in (5, 1):
         pair.attend(pair.query(np.random.default_rng(3), tq=tq), pseudo)
@@ -334,7 +337,9 @@ def test_duplicate_tokens_force_exact_ties():
     for f in range(wl.frames - wl.window_frames - 1):
         pair.step()
     pair.check_bank()
-    h.log(f"near ties {pair.near_ties}, gpu counter {pair.gpu.counters().near_ties}")
+    h.log(f"near ties {pair.near_ties}, gpu counter {pair.gpu.counters().near_ties}, resyncs {pair.resyncs}")
+    assert pair.near_ties > 0
+    pair.check_near_tie_counter()
 
 
 @pytest.mark.parametrize("use_pq,mass_bias", [(False, True), (True, False)])
@@ -364,6 +369,7 @@ def test_multi_stream_round_robin():
         pair.step()
     pair.step(streams=[1])
     pair.step(streams=[2, 0])
+    pair.check_near_tie_counter()
     for s in range(3):
         pair.check_bank(stream=s, bitwise=True)
         pseudo = pair.synthesize(stream=s)

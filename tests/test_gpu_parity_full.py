@@ -2,10 +2,15 @@
 
 Every unit of every stream runs on the GPU in the launch configuration that
 bench.py times (default config, one batched append + fold per frame).  The
-oracle follows sampled units: over the whole stream where it can afford it
-(7B workload), else by per-frame re-sync (the oracle folds a sampled unit
-starting from the GPU's own pre-fold bank and must reproduce the GPU's fold
-exactly).  Each test prints its case before any GPU step.
+oracle follows sampled units free-running (it is authoritative: after an
+excused near tie the device's state of those units is replaced by the
+oracle's) over the whole 7B stream and over the first hundreds of frames of
+the long-delay, high-resolution and 64-stream workloads.  Over the full
+length of those three the device runs alone; single folds are checked
+against the oracle from the device's own pre-fold state at chosen frames,
+and at the end every unit of every stream must satisfy the mass, histogram
+and residual-count identities.  Each test prints its case before any GPU
+step.
 """
 import numpy as np
 import pytest
@@ -57,13 +62,96 @@ def _resync_run(h, wl, sample, check_frames, frames=None, streams=1, readout_str
     r = h.Resync(wl, sample, streams=streams, **kw)
     for f in range(frames):
         r.step(check=f in check_frames)
+        if f % 512 == 511:
+            h.log(f"frame {f + 1}")
     worst = max(r.check_readout(s) for s in readout_streams)
+    r.check_invariants()
     c = r.gpu.counters()
-    h.log(f"folds re-checked {r.folds_checked}, near ties {r.near_ties}, "
+    h.log(f"folds re-checked {r.folds_checked}, near ties {r.near_ties} (excused {r.excused}), "
           f"refined {c.refined}+{c.refined_full}, readout max abs err {worst:.2e}")
     expect = len(sample) * sum(1 for f in check_frames if wl.window_frames <= f < frames)
     assert r.folds_checked == expect
     return r
+
+
+def test_long_delay_free_running_through_the_cue():
+    """Long-delay workload (K=1024, W=16), one unit followed by the oracle from
+    the first frame through frame 320: seeding, the rare cue cluster in frames
+    100-102 and its eviction at frames 116-118, then 200 more folds.  Every
+    assignment is checked, banks bitwise at the cue's eviction and at the end,
+    and a query whose last half is aligned with the cue cluster's mean is
+    read out."""
+    h = H()
+    wl = W.WORKLOADS["long"].with_(frames=320)
+    h.log(f"case: {wl.name} free-running through frame 320, unit 57")
+    pair = h.Pair(wl, sample=[57])
+    for f in range(wl.frames):
+        pair.step()
+        if f in (119, 319):
+            pair.check_bank(bitwise=True)
+        if f % 100 == 99:
+            h.log(f"frame {f + 1}")
+    pseudo = pair.synthesize()
+    q = pair.query(np.random.default_rng(31))
+    l, hk = divmod(57, wl.num_kv_heads)
+    grp = wl.num_q_heads // wl.num_kv_heads
+    cue = pair.host[0]._heads[57].means[0]
+    q[l, wl.query_tokens // 2:, hk * grp:(hk + 1) * grp] += 4.0 * np.sqrt(wl.head_dim) * cue
+    q = W.quantize(q, wl.kv_dtype)
+    worst, *_ = pair.attend(q, pseudo)
+    b = pair.oracle[0].banks[0]
+    h.log(f"assignments {pair.assign_checked}, near ties {pair.near_ties} (excused {pair.excused}, "
+          f"resyncs {pair.resyncs}), active {(b.n > 0).sum()}, readout err {worst:.2e}")
+    assert pair.assign_checked == (wl.frames - wl.window_frames) * wl.tokens_per_frame
+
+
+def test_hires_free_running():
+    """High-resolution workload (576 tokens/frame, K=2048, W=8), one unit
+    followed by the oracle over 40 frames: the bank fills on the 4th fold, then
+    28 folds assign 576 tokens against 2048 slots; banks bitwise, readout."""
+    h = H()
+    wl = W.WORKLOADS["hires"].with_(frames=40)
+    h.log(f"case: {wl.name} free-running 40 frames, unit 200")
+    pair = h.Pair(wl, sample=[200])
+    for f in range(wl.frames):
+        pair.step()
+    pair.check_bank(bitwise=True)
+    pseudo = pair.synthesize()
+    worst, *_ = pair.attend(pair.query(np.random.default_rng(32)), pseudo)
+    h.log(f"assignments {pair.assign_checked}, near ties {pair.near_ties} (excused {pair.excused}), "
+          f"readout err {worst:.2e}")
+
+
+def test_multistream_free_running_with_queries():
+    """The 64-stream workload (K=512, W=8) in its launch pattern: one batched
+    append of every stream and one fold per round, for 136 rounds, and the
+    queries of the schedule (stream b at rounds r with (r - 2b) mod 128 = 127).
+    The oracle follows unit 90 of streams 0 and 37 from the first frame; the
+    queries of those streams (rounds 73 and 127) are checked against it."""
+    h = H()
+    wl = W.WORKLOADS["multi"]
+    tracked = [0, 37]
+    h.log(f"case: {wl.name} 136 rounds, oracle on unit 90 of streams {tracked}")
+    pair = h.Pair(wl, sample=[90], streams=wl.streams, oracle_streams=tracked, cb_samples=256, cb_iters=4)
+    checked = 0
+    for r in range(136):
+        pair.step()
+        b = (r - 127) % 128
+        if b % 2 == 0 and b // 2 < wl.streams:
+            s = b // 2
+            if s in tracked:
+                pair.check_bank(stream=s, bitwise=True)
+                pseudo = pair.synthesize(stream=s)
+                worst, *_ = pair.attend(pair.query(np.random.default_rng(r)), pseudo, stream=s)
+                h.log(f"round {r}: stream {s} readout err {worst:.2e}")
+                checked += 1
+            else:
+                pair.gpu.synthesize(s)
+                pair.gpu.attend(s, pair.torch.zeros((wl.num_layers, wl.query_tokens, wl.num_q_heads, 128),
+                                                    dtype=pair.dtype, device="cuda"))
+    assert checked == 2
+    h.log(f"assignments {pair.assign_checked}, near ties {pair.near_ties} (excused {pair.excused})")
+    assert pair.assign_checked == len(tracked) * (136 - wl.window_frames) * wl.tokens_per_frame
 
 
 def test_long_delay_full_stream_resync():

@@ -198,3 +198,30 @@ def test_recycling_takes_near_tokens_newest_frame_first_in_raster_order():
     for e, k in enumerate((1, 2, 3)):
         assert np.array_equal(b.sum_k[k], kt[e]) and b.tau[k] == t * T + e
     assert b.n[0] == 4
+
+
+def test_merge_distance_is_the_squared_euclidean_distance():
+    """The merge test's ||a - b||^2 against scipy's sqeuclidean on random float32
+    centres (float64 sums agree to rounding), and a 3-4-5 case exactly."""
+    import scipy.spatial.distance as ssd
+    rng = np.random.default_rng(5)
+    for _ in range(200):
+        scale = 10.0 ** rng.uniform(-3, 2)
+        a = (rng.standard_normal(D) * scale).astype(F32)
+        b = (a + rng.standard_normal(D) * scale * rng.uniform(0, 1)).astype(F32)
+        ref = ssd.sqeuclidean(a.astype(np.float64), b.astype(np.float64))
+        assert abs(O._dist2(a, b) - ref) <= 1e-13 * ref
+    assert O._dist2(_vec((0, 3.0)), _vec((1, 4.0))) == 25.0
+    assert O._dist2(_vec((127, 0.5)), _vec()) == 0.25
+
+
+def test_pair_on_the_threshold_is_counted_and_not_merged():
+    """Key centres exactly eps_K apart (0.25^2 = 0.0625 is exact): the strict
+    test keeps them apart, and the pair is counted as near-threshold."""
+    p = _params(eps_k=0.25, eps_v=10.0, t_idle=100)
+    rows = [(2, _vec((0, 0.5)), _vec((0, 1.0)), (0.25, 0.25), 0),
+            (2, _vec((0, 0.75)), _vec((0, 1.0)), (0.25, 0.25), 0)]
+    b = _bank_with(p, rows)
+    st = O.maintain(b, _near(p, 1), 1, p)
+    assert st["merged"] == 0 and st["near_threshold"] == 1
+    assert b.n[0] == 2 and b.n[1] == 2

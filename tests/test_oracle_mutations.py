@@ -101,9 +101,9 @@ MUTATIONS = [
     ("maintain", "> p.t_idle", ">= p.t_idle", [M.test_aging_floors_the_mass_and_keeps_the_centre]),
     ("maintain", "ci, cj = (bank.sum_k[i] / ni)", "ci, cj = (bank.sum_k[i] / F32(1))",
      [lambda: M.test_merge_uses_the_centre_updated_by_earlier_merges(0.3, 1)]),
-    ("maintain", "if not _dist2(ci, cj) < ek2", "if not _dist2(ci, cj) <= ek2",
+    ("maintain", "if not dk < ek2", "if not dk <= ek2",
      [M.test_merge_thresholds_are_strict_and_need_both_centres]),
-    ("maintain", "if not _dist2(pi, pj) < ev2", "if False",
+    ("maintain", "if not dv < ev2", "if False",
      [M.test_merge_thresholds_are_strict_and_need_both_centres]),
     ("maintain", "F32(ni * bank.mu[i, a])", "F32(nj * bank.mu[i, a])",
      [M.test_merge_adds_statistics_and_weights_the_spatial_mean]),
@@ -115,6 +115,22 @@ MUTATIONS = [
      [M.test_recycling_takes_near_tokens_newest_frame_first_in_raster_order]),
     ("maintain", "bank.n[j] = 0", "bank.n[j] = bank.n[j]",
      [M.test_merge_adds_statistics_and_weights_the_spatial_mean]),
+    ("_dist2", "for d in range(len(a64)):", "for d in range(len(a64) - 1):",
+     [M.test_merge_distance_is_the_squared_euclidean_distance]),
+    ("_dist2", "diff = a64[d] - b64[d]", "diff = a64[d] - b64[d - 1]",
+     [M.test_merge_distance_is_the_squared_euclidean_distance]),
+    ("_near_threshold", "return abs(d2 - eps2) <= NEAR_THRESHOLD_REL * eps2", "return False",
+     [M.test_pair_on_the_threshold_is_counted_and_not_merged]),
+    ("argmin_lowest", "margin = part[:, 1] - part[:, 0]", "margin = 0 * (part[:, 1] - part[:, 0])",
+     [P.test_margin_is_second_best_minus_best_of_an_independent_cost_matrix]),
+    ("argmin_lowest", "margin = part[:, 1] - part[:, 0]", "margin = 10 * (part[:, 1] - part[:, 0])",
+     [P.test_margin_is_second_best_minus_best_of_an_independent_cost_matrix]),
+    ("argmin_lowest", "margin = part[:, 1] - part[:, 0]", "margin = part[:, 2] - part[:, 0]",
+     [P.test_margin_is_second_best_minus_best_of_an_independent_cost_matrix]),
+    ("round_kv", "top = ((bits + 0x7FFF + lsb) >> 16)", "top = ((bits + 0 * lsb) >> 16)",
+     [P.test_round_kv_bf16_is_torch_round_to_nearest_even]),
+    ("round_kv", "top = ((bits + 0x7FFF + lsb) >> 16)", "top = ((bits + 0x8000 + 0 * lsb) >> 16)",
+     [P.test_round_kv_bf16_is_torch_round_to_nearest_even]),
 ]
 
 

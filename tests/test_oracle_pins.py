@@ -557,3 +557,181 @@ def test_pseudo_tokens_from_brute_force_modes():
             assert np.allclose(ps.keys[row], ck + rk, rtol=1e-6, atol=1e-6)
             assert np.allclose(ps.values[row], cv + rv, rtol=1e-6, atol=1e-6)
             assert ps.bias[row] == pytest.approx(math.log(bank.n[k]))
+
+
+# ---------------------------------------------------------------------------
+# Eq. 1 argmin: the top-2 margin that decides a near tie
+# ---------------------------------------------------------------------------
+
+
+def test_margin_is_second_best_minus_best_of_an_independent_cost_matrix():
+    """The argmin's margin equals (second smallest - smallest) of the cost
+    matrix built from scipy's cosine and Mahalanobis distances, row by row."""
+    p = tiny_params(grid_h=6, grid_w=6, capacity=40)
+    rng = np.random.default_rng(7)
+    bank = _random_bank(p, rng, 33)
+    keys = rng.standard_normal((36, p.head_dim)).astype(F32)
+    coords = O.spatial_coords(p.grid_h, p.grid_w)
+    t = 300
+    idx, margin = O.argmin_lowest(O.assignment_costs(keys, coords, bank, t, p))
+    cosd = ssd.cdist(keys.astype(np.float64), bank.sum_k[:33].astype(np.float64), "cosine")
+    for i in range(len(keys)):
+        row = []
+        for k in range(33):
+            sig = bank.sigma[k].astype(np.float64)
+            vi = np.linalg.inv(np.array([[sig[0] + p.ridge, sig[1]], [sig[1], sig[2] + p.ridge]]))
+            mah = ssd.mahalanobis(coords[i].astype(np.float64), bank.mu[k].astype(np.float64), vi)
+            idle = 1.0 if t - bank.tau[k] // p.tokens_per_frame > p.t_idle else 0.0
+            row.append(-(1.0 - cosd[i, k]) + p.lambda_sp * mah + p.lambda_idle * idle)
+        first, second = sorted(row)[:2]
+        assert idx[i] == row.index(first)
+        assert abs(margin[i] - (second - first)) < 1e-9, (i, margin[i], second - first)
+
+
+def test_margin_hand_worked_tie_and_single_slot():
+    """lambda = 0, key e0, centres e0 and (e0 + e1)/sqrt 2: cost -1 and -1/sqrt 2,
+    so the margin is 1 - 1/sqrt 2.  Two equal centres: margin 0, lowest slot.
+    One active slot: no second candidate, margin +inf."""
+    p = tiny_params(capacity=4, lambda_sp=0.0, lambda_idle=0.0)
+    b = O.Bank(p)
+    e0, e1 = np.eye(p.head_dim, dtype=F32)[:2]
+    b.n[:2] = 1
+    b.sum_k[0] = e0
+    b.sum_k[1] = (e0 + e1).astype(F32)
+    key = e0[None, :]
+    idx, m = O.argmin_lowest(O.assignment_costs(key, O.spatial_coords(4, 4)[:1], b, 0, p))
+    assert idx[0] == 0 and abs(m[0] - (1.0 - 1.0 / math.sqrt(2.0))) < 1e-15
+    b.sum_k[1] = (3 * e0).astype(F32)      # same direction: cos 1 for both
+    idx, m = O.argmin_lowest(O.assignment_costs(key, O.spatial_coords(4, 4)[:1], b, 0, p))
+    assert idx[0] == 0 and m[0] == 0.0
+    b.n[1] = 0
+    idx, m = O.argmin_lowest(O.assignment_costs(key, O.spatial_coords(4, 4)[:1], b, 0, p))
+    assert idx[0] == 0 and m[0] == np.inf
+
+
+# ---------------------------------------------------------------------------
+# rounding to the KV dtype
+# ---------------------------------------------------------------------------
+
+
+def test_round_kv_bf16_is_torch_round_to_nearest_even():
+    """bf16 rounding against torch's float32 -> bfloat16 conversion, on random
+    values over the whole exponent range and on exact halfway cases (both
+    parities of the kept bit, both signs), their neighbours and subnormals."""
+    rng = np.random.default_rng(11)
+    hi = rng.integers(0, 0x7F7F, 4000, dtype=np.uint32)
+    lows = np.array([0x8000, 0x7FFF, 0x8001, 0x0000, 0xFFFF, 0x0001], dtype=np.uint32)
+    bits = ((hi[:, None] << 16) | lows[None, :]).reshape(-1)
+    bits = np.concatenate([bits, bits | 0x80000000, rng.integers(0, 0x7F800000, 20000, dtype=np.uint32)])
+    x = bits.view(F32)
+    ref = torch.from_numpy(x.copy()).to(torch.bfloat16).to(torch.float32).numpy()
+    got = O.round_kv(x, "bf16")
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    # halfway: 1 + 2^-8 is between 1 and 1 + 2^-7 -> even (1); 1 + 3 * 2^-8 -> 1 + 2^-6
+    assert O.round_kv(np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8], F32), "bf16").tolist() == [1.0, 1 + 2.0 ** -6]
+    assert np.array_equal(O.round_kv(x, "fp32"), x)
+
+
+# ---------------------------------------------------------------------------
+# P12: with one token per frame the frame-batched fold is Alg. 1's per-token loop
+# ---------------------------------------------------------------------------
+
+
+def _sequential_alg1(p, tokens, codebooks):
+    """Alg. "ProtoKV Streaming Update" token by token (running-mean centres,
+    residual against the centre before the token's update): seed the lowest
+    free slot while one is free, else assign by Eq. 1 (scipy distances, ties
+    to the lowest slot) and accumulate.  tokens: (key, value, frame) in
+    stream order; the token evicted by the append of frame t is scored at t."""
+    K, Dd = p.capacity, p.head_dim
+    n = np.zeros(K, np.int64)
+    sk, sv, qk, qv = (np.zeros((K, Dd), F32) for _ in range(4))
+    hk, hv = np.zeros((K, p.G, p.C), np.int64), np.zeros((K, p.G, p.C), np.int64)
+    nres, tau = np.zeros(K, np.int64), np.zeros(K, np.int64)
+    mu, sig = np.zeros((K, 2), F32), np.zeros((K, 3), F32)
+    s = np.array([0.5, 0.5], F32)
+    log = []
+    for key, val, f in tokens:
+        t = f + p.window_frames           # the frame whose append evicts this one
+        free = [k for k in range(K) if n[k] == 0]
+        if free:
+            k = free[0]
+            n[k], sk[k], sv[k], qk[k], qv[k] = 1, key, val, key * key, val * val
+            mu[k], sig[k], tau[k] = s, (1.0, 0.0, 1.0), f
+            log.append(k)
+            continue
+        cosd = ssd.cdist(key[None].astype(np.float64), sk.astype(np.float64), "cosine")[0]
+        cost = []
+        for j in range(K):
+            sg = sig[j].astype(np.float64)
+            vi = np.linalg.inv(np.array([[sg[0] + p.ridge, sg[1]], [sg[1], sg[2] + p.ridge]]))
+            mah = ssd.mahalanobis(s.astype(np.float64), mu[j].astype(np.float64), vi)
+            idle = 1.0 if t - tau[j] > p.t_idle else 0.0
+            cost.append(-(1.0 - cosd[j]) + p.lambda_sp * mah + p.lambda_idle * idle)
+        k = int(np.argmin(cost))
+        log.append(k)
+        ck = (sk[k] / F32(n[k])).astype(F32)
+        cv = (sv[k] / F32(n[k])).astype(F32)
+        zk = O.pq_encode((key - ck).astype(F32)[None], codebooks[0])[0]
+        zv = O.pq_encode((val - cv).astype(F32)[None], codebooks[1])[0]
+        n[k] += 1
+        sk[k] = (sk[k] + key).astype(F32)
+        sv[k] = (sv[k] + val).astype(F32)
+        qk[k] = (qk[k] + (key * key).astype(F32)).astype(F32)
+        qv[k] = (qv[k] + (val * val).astype(F32)).astype(F32)
+        hk[k, np.arange(p.G), zk] += 1
+        hv[k, np.arange(p.G), zv] += 1
+        nres[k] += 1
+        eta = F32(p.eta)
+        keep = F32(F32(1) - eta)
+        m = [F32(F32(keep * mu[k, a]) + F32(eta * s[a])) for a in range(2)]
+        mu[k] = m
+        dx, dy = F32(s[0] - m[0]), F32(s[1] - m[1])
+        sig[k] = [F32(F32(keep * sig[k, 0]) + F32(eta * F32(dx * dx))),
+                  F32(F32(keep * sig[k, 1]) + F32(eta * F32(dx * dy))),
+                  F32(F32(keep * sig[k, 2]) + F32(eta * F32(dy * dy)))]
+        tau[k] = f
+    return dict(n=n, sum_k=sk, sum_v=sv, sq_k=qk, sq_v=qv, hist_k=hk, hist_v=hv, n_res=nres, mu=mu,
+                sigma=sig, tau=tau), log
+
+
+def test_one_token_per_frame_batching_is_the_sequential_loop():
+    """With T = 1 every fold holds one token, so seeding, the post-seed
+    snapshot and the in-order aggregation reduce to Alg. 1's per-token loop:
+    the bank and the assignment log are identical."""
+    p = tiny_params(grid_h=1, grid_w=1, window_frames=3, capacity=10, t_idle=4)
+    wl = tiny_stream(p, 70, seed=21, clusters=4)
+    st, log, _ = run_stream(p, wl, 70)
+    tokens = [(ke[0], ve[0], f) for f, (_, ke, ve, _) in enumerate(log)]
+    ref, ref_log = _sequential_alg1(p, tokens, st.codebooks[0])
+    assert [int(r.assign[0]) for *_, r in log] == ref_log
+    b = st.banks[0]
+    for name, want in ref.items():
+        assert np.array_equal(getattr(b, name), want), name
+    assert (b.n_res > 0).sum() > 3 and len(set(ref_log[p.capacity:])) > 3
+
+
+def test_a_chosen_slot_must_be_a_near_tie_argmin():
+    """fold_frame(choose=...) accepts another slot only where Eq. 1 gives it a
+    cost within 1e-6 of the minimum (an exact tie here: two equal centres),
+    and refuses a slot whose cost is clearly larger."""
+    p = tiny_params(grid_h=1, grid_w=2, capacity=3, lambda_sp=0.0, lambda_idle=0.0, use_pq=False)
+    e0, e1 = np.eye(p.head_dim, dtype=F32)[:2]
+    cb = np.zeros((2, p.G, p.C, p.head_dim // p.G), F32)
+
+    def bank():
+        b = O.Bank(p)
+        b.n[:3] = 1
+        b.sum_k[0], b.sum_k[1], b.sum_k[2] = e0, e0, e1
+        b.mu[:] = 0.25
+        b.sigma[:] = (1.0, 0.0, 1.0)
+        return b
+    keys = np.stack([e0, e1]).astype(F32)
+    vals = np.zeros_like(keys)
+    r = O.fold_frame(bank(), keys, vals, 0, 1, p, cb)
+    assert r.assign.tolist() == [0, 2] and r.margin[0] == 0.0 and r.near_ties == 1
+    b = bank()
+    r = O.fold_frame(b, keys, vals, 0, 1, p, cb, choose=np.array([1, 2]))
+    assert r.assign.tolist() == [1, 2] and b.n.tolist() == [1, 2, 2]
+    with pytest.raises(ValueError):
+        O.fold_frame(bank(), keys, vals, 0, 1, p, cb, choose=np.array([2, 2]))
