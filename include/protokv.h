@@ -203,6 +203,30 @@ protokv_status protokv_synthesize(protokv_t h, int32_t stream_id, void* stream);
 protokv_status protokv_attend(protokv_t h, int32_t stream_id, const void* q, int32_t tq,
                               void* o, float* lse, void* stream);
 
+/* Bytes of the fixed device array behind protokv_attend_static (64 MiB). */
+#define PROTOKV_STATIC_SCRATCH_BYTES (64u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * readout as protokv_attend, same arguments, same result up to the readout
+ * tolerance (bitwise equal when the split count is the same), whose
+ * kernels keep their scratch -- the per-split partial outputs and (m, l)
+ * pairs, and with rope_theta > 0 the rotated query -- in a fixed device
+ * array of PROTOKV_STATIC_SCRATCH_BYTES compiled into the library instead of
+ * the workspace.  Each device holds its own copy until the process ends
+ * (its address is looked up once per device, by protokv_init).  No device
+ * memory is allocated or freed and nothing needs clearing: every partial is
+ * written before it is read.  The context split count is that of
+ * protokv_attend, lowered if needed until units * splits * rows * (D + 2) * 4
+ * bytes (rows = tq * Hq / Hkv), plus L * tq * Hq * D * kv bytes with rotary
+ * positions, fit the array.
+ * Errors: as protokv_attend; PROTOKV_E_UNSUPPORTED when even one split does
+ * not fit.  All calls on one device share the array: calls that overlap in
+ * time on one device (other streams, other handles, other threads) race and
+ * must be serialized by the caller. */
+protokv_status protokv_attend_static(protokv_t h, int32_t stream_id, const void* q, int32_t tq,
+                                     void* o, float* lse, void* stream);
+
 typedef struct {
   uint64_t frames;          /* frames appended to the stream */
   uint64_t evicted_tokens;  /* tokens folded into the bank, per (layer, kv head) */

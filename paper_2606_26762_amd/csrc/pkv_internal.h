@@ -206,6 +206,10 @@ hipError_t launch_ring_insert_rope(const Dims& dm, const Workspace& ws, const Ap
                                    const void* v, hipStream_t st);
 hipError_t launch_rope_q(const Dims& dm, const Workspace& ws, const void* q, int tq, long long p0,
                          hipStream_t st);
+// device address of protokv_attend_static's scratch array on the current
+// device (looked up once per device, then cached)
+constexpr int MAX_DEVICES = 64;
+hipError_t static_scratch_ptr(void** out);
 // codebook warm-up (warmup.hip)
 hipError_t launch_warm_collect(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st);
 hipError_t launch_warm_kmeans(const Dims& dm, const Workspace& ws, const KmeansBatch& kb, hipStream_t st);

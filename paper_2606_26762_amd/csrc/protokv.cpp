@@ -204,6 +204,7 @@ struct protokv_ctx {
   Layout ly;
   uint8_t* base = nullptr;
   std::vector<StreamState> st;
+  void* scratch = nullptr;  // this device's protokv_attend_static array
   int synth_stream = -1;
   int synth_active = 0;
   bool synth_rows = false;  // pseudo-token rows written (else only centres, biases, codes)
@@ -401,6 +402,8 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   if (e == hipSuccess && ws.rope_inv)
     e = hipMemcpyAsync(const_cast<double*>(ws.rope_inv), inv.data(), inv.size() * sizeof(double),
                        hipMemcpyHostToDevice, hs);
+  // the address of this device's protokv_attend_static scratch (once per device)
+  if (e == hipSuccess) e = static_scratch_ptr(&h->scratch);
   if (e == hipSuccess) e = hipStreamSynchronize(hs);
   if (e != hipSuccess) {
     g_init_err = std::string("init: ") + hipGetErrorString(e);
@@ -570,16 +573,19 @@ protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
   return PROTOKV_OK;
 }
 
-protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t tq, void* o, float* lse,
-                              void* stream) {
-  if (!h) return PROTOKV_E_INVALID;
-  if (sid < 0 || sid >= h->cfg.num_streams) return h->fail(PROTOKV_E_INVALID, "attend: stream id out of range");
-  if (!q || !o) return h->fail(PROTOKV_E_INVALID, "attend: q and o must be non-NULL");
-  if (tq < 1 || tq > h->cfg.max_query_tokens) return h->fail(PROTOKV_E_INVALID, "attend: tq outside [1, max_query_tokens]");
+// Checks a readout of stream sid and plans its context splits (at most
+// max_splits); no launches.
+static protokv_status plan_attend(protokv_t h, int32_t sid, const void* q, int32_t tq, void* o, float* lse,
+                                  int max_splits, AttendArgs& aa, const char* who) {
+  if (sid < 0 || sid >= h->cfg.num_streams) return h->fail(PROTOKV_E_INVALID, std::string(who) + ": stream id out of range");
+  if (!q || !o) return h->fail(PROTOKV_E_INVALID, std::string(who) + ": q and o must be non-NULL");
+  if (tq < 1 || tq > h->cfg.max_query_tokens)
+    return h->fail(PROTOKV_E_INVALID, std::string(who) + ": tq outside [1, max_query_tokens]");
   const StreamState& ss = h->st[sid];
-  if (ss.pending) return h->fail(PROTOKV_E_STATE, "attend: stream has an unfolded eviction");
-  if (h->synth_stream != sid) return h->fail(PROTOKV_E_STATE, "attend: no synthesis of this stream since its last fold");
-  AttendArgs aa{};
+  if (ss.pending) return h->fail(PROTOKV_E_STATE, std::string(who) + ": stream has an unfolded eviction");
+  if (h->synth_stream != sid)
+    return h->fail(PROTOKV_E_STATE, std::string(who) + ": no synthesis of this stream since its last fold");
+  aa = AttendArgs{};
   aa.sid = sid;
   const int T = h->dm.T, W = h->dm.W;
   const uint64_t nf = std::min<uint64_t>(ss.frames, (uint64_t)W);
@@ -589,30 +595,18 @@ protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t t
   aa.gen = h->synth_rows ? 0 : 1;
   aa.tq = tq;
   aa.q = q;
-  aa.near_k = h->ws.ring_k;
-  if (h->ws.ring_kr) {
-    // rotary positions: near keys from the rotated ring, the query rotated
-    // at P + t with P = frames appended * T
-    aa.near_k = h->ws.ring_kr;
-    aa.q = h->ws.qrot;
-    const long long p0 = (long long)ss.frames * T;
-    protokv_status sr = h->dev(
-        h->launch(PROTOKV_K_ROPE_Q, (hipStream_t)stream,
-                  [&] { return launch_rope_q(h->dm, h->ws, q, tq, p0, (hipStream_t)stream); }),
-        "attend/rope");
-    if (sr != PROTOKV_OK) return sr;
-  }
+  aa.near_k = h->ws.ring_kr ? h->ws.ring_kr : h->ws.ring_k;
   aa.o = o;
   aa.lse = lse;
   const int ctx = aa.n_near + aa.n_far;
-  if (ctx == 0) return h->fail(PROTOKV_E_STATE, "attend: empty context (no frames appended)");
+  if (ctx == 0) return h->fail(PROTOKV_E_STATE, std::string(who) + ": empty context (no frames appended)");
   const int rows = tq * (h->dm.Hq / h->dm.Hkv);
   int splits;
-  if (h->dm.kv_fp32) splits = std::max(1, std::min(MAX_SPLITS, (1024 + h->dm.units * rows - 1) / (h->dm.units * rows)));
+  if (h->dm.kv_fp32) splits = std::max(1, std::min(max_splits, (1024 + h->dm.units * rows - 1) / (h->dm.units * rows)));
   else {
     const int rblocks = (rows + 255) / 256;
     // about one workgroup per compute unit (256 on MI355X)
-    splits = std::max(1, std::min(MAX_SPLITS, (256 + h->dm.units * rblocks / 2) / (h->dm.units * rblocks)));
+    splits = std::max(1, std::min(max_splits, (256 + h->dm.units * rblocks / 2) / (h->dm.units * rblocks)));
   }
   int chunk = (ctx + splits - 1) / splits;
   chunk = (chunk + 63) / 64 * 64;
@@ -639,15 +633,71 @@ protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t t
     }
     chunk = best_chunk;
   }
-  splits = (ctx + chunk - 1) / chunk;
-  aa.splits = splits;
+  aa.splits = (ctx + chunk - 1) / chunk;
   aa.chunk = chunk;
-  hipStream_t hs = (hipStream_t)stream;
-  protokv_status s = h->dev(h->launch(PROTOKV_K_ATTEND, hs, [&] { return launch_attend(h->dm, h->ws, aa, hs); }),
+  return PROTOKV_OK;
+}
+
+// Enqueues a planned readout: the rotated query (rotary positions), the
+// split readout and the merge, with the scratch of `ws` and the partial
+// strides of `dm`.
+static protokv_status run_attend(protokv_t h, const Dims& dm, const Workspace& ws, AttendArgs& aa, hipStream_t hs) {
+  if (ws.qrot) {
+    // rotary positions: the query rotated at P + t with P = frames appended * T
+    const void* q = aa.q;
+    const long long p0 = (long long)h->st[aa.sid].frames * dm.T;
+    protokv_status sr = h->dev(
+        h->launch(PROTOKV_K_ROPE_Q, hs, [&] { return launch_rope_q(dm, ws, q, aa.tq, p0, hs); }), "attend/rope");
+    if (sr != PROTOKV_OK) return sr;
+    aa.q = ws.qrot;
+  }
+  protokv_status s = h->dev(h->launch(PROTOKV_K_ATTEND, hs, [&] { return launch_attend(dm, ws, aa, hs); }),
                             "attend");
   if (s != PROTOKV_OK) return s;
-  return h->dev(h->launch(PROTOKV_K_ATTEND_MERGE, hs, [&] { return launch_attend_merge(h->dm, h->ws, aa, hs); }),
+  return h->dev(h->launch(PROTOKV_K_ATTEND_MERGE, hs, [&] { return launch_attend_merge(dm, ws, aa, hs); }),
                 "attend/merge");
+}
+
+protokv_status protokv_attend(protokv_t h, int32_t sid, const void* q, int32_t tq, void* o, float* lse,
+                              void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  AttendArgs aa;
+  protokv_status s = plan_attend(h, sid, q, tq, o, lse, MAX_SPLITS, aa, "attend");
+  if (s != PROTOKV_OK) return s;
+  return run_attend(h, h->dm, h->ws, aa, (hipStream_t)stream);
+}
+
+protokv_status protokv_attend_static(protokv_t h, int32_t sid, const void* q, int32_t tq, void* o, float* lse,
+                                     void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (!h->scratch) return h->fail(PROTOKV_E_DEVICE, "attend_static: no scratch address for this device");
+  const int rows = tq * (h->dm.Hq / h->dm.Hkv);
+  const size_t es = kv_bytes(h->cfg);
+  const size_t qrot = h->ws.qrot ? ((size_t)h->dm.L * std::max(tq, 1) * h->dm.Hq * D * es + 255) / 256 * 256 : 0;
+  // partial outputs [units][splits][rows][D] and (m, l) [units][splits][rows][2], float32
+  auto part_bytes = [&](int sp) {
+    const size_t po = ((size_t)h->dm.units * sp * std::max(rows, 1) * D * 4 + 255) / 256 * 256;
+    const size_t pm = ((size_t)h->dm.units * sp * std::max(rows, 1) * 2 * 4 + 255) / 256 * 256;
+    return po + pm;
+  };
+  int max_splits = MAX_SPLITS;
+  while (max_splits > 1 && part_bytes(max_splits) + qrot > PROTOKV_STATIC_SCRATCH_BYTES) --max_splits;
+  if (part_bytes(1) + qrot > PROTOKV_STATIC_SCRATCH_BYTES)
+    return h->fail(PROTOKV_E_UNSUPPORTED, "attend_static: the partials of one context split (units * rows * (D + 2) "
+                                          "* 4 bytes) and the rotated query exceed PROTOKV_STATIC_SCRATCH_BYTES");
+  AttendArgs aa;
+  protokv_status s = plan_attend(h, sid, q, tq, o, lse, max_splits, aa, "attend_static");
+  if (s != PROTOKV_OK) return s;
+  // the same kernels with compact partial strides and the scratch pointers
+  Dims dm = h->dm;
+  dm.max_splits = aa.splits;
+  dm.max_rows = rows;
+  Workspace ws = h->ws;
+  uint8_t* base = (uint8_t*)h->scratch;
+  ws.part_o = (float*)base;
+  ws.part_ml = (float*)(base + ((size_t)dm.units * aa.splits * rows * D * 4 + 255) / 256 * 256);
+  if (ws.qrot) ws.qrot = base + part_bytes(aa.splits);
+  return run_attend(h, dm, ws, aa, (hipStream_t)stream);
 }
 
 protokv_status protokv_stream_info_get(protokv_t h, int32_t sid, protokv_stream_info* out) {

@@ -5,6 +5,7 @@
 // tokens, mass-aware bias, Eq. attn_logit), Eq. pq and Appendix Algorithms
 // "DecodeTopSResidualModes" and "ProtoKV Query-Time Pseudo-Token Decoding
 // and Attention".
+#include <mutex>
 #include <type_traits>
 
 #include "pkv_internal.h"
@@ -1485,6 +1486,33 @@ hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& 
       hipLaunchKernelGGL(k_attend_bf16<4>, dim3(dm.units * aa.splits), dim3(256), 0, st, dm, ws, aa, rows, 1);
   }
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of protokv_attend_static (callers that cannot allocate): the split
+// partials and the rotated query live in this file-scope device array instead
+// of the workspace.  Every device the library runs on holds its own copy
+// until the process ends; host code must use the address from
+// static_scratch_ptr, never the array's name.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) uint8_t scratch[PROTOKV_STATIC_SCRATCH_BYTES];
+
+hipError_t static_scratch_ptr(void** out) {
+  static std::mutex mu;
+  static void* per_device[MAX_DEVICES] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!per_device[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    per_device[dev] = p;
+  }
+  *out = per_device[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa, hipStream_t st) {

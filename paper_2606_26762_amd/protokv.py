@@ -27,11 +27,13 @@ EXPORTED = [
     "protokv_destroy", "protokv_append_frame", "protokv_fold", "protokv_synthesize", "protokv_attend",
     "protokv_stream_info_get", "protokv_get_counters", "protokv_read_assignments", "protokv_read_bank",
     "protokv_read_pseudo", "protokv_read_codebooks", "protokv_profile", "protokv_profile_read",
-    "protokv_state_size", "protokv_get_state", "protokv_set_state", "protokv_last_error",
+    "protokv_state_size", "protokv_get_state", "protokv_set_state", "protokv_attend_static",
+    "protokv_last_error",
 ]
 
 STATE_MAGIC, STATE_VERSION = 0x53564B50, 1
 MAX_EVICTED_TOKENS = 16777214
+STATIC_SCRATCH_BYTES = 64 << 20
 
 KERNELS = ["ring_insert", "seed", "screen", "aggregate", "decode", "attend", "attend_merge", "pq_encode",
            "materialize", "maintain", "rope_ring", "rope_q", "warm_collect", "warm_kmeans"]
@@ -111,6 +113,7 @@ def lib() -> ctypes.CDLL:
         L.protokv_fold.argtypes = [vp, vp]
         L.protokv_synthesize.argtypes = [vp, i32, vp]
         L.protokv_attend.argtypes = [vp, i32, vp, i32, vp, vp, vp]
+        L.protokv_attend_static.argtypes = [vp, i32, vp, i32, vp, vp, vp]
         L.protokv_stream_info_get.argtypes = [vp, i32, P(StreamInfo)]
         L.protokv_get_counters.argtypes = [vp, P(Counters), vp]
         L.protokv_read_assignments.argtypes = [vp, i32, vp, sz, vp]
@@ -303,6 +306,21 @@ class ProtoKV:
         _check(lib().protokv_attend(self.h, stream_id, q.data_ptr(), tq, out.data_ptr(),
                                     lse.data_ptr() if lse is not False else None,
                                     _stream_ptr(stream)), self.h)
+        return out, lse
+
+    def attend_static(self, stream_id: int, q, out=None, lse=None, stream=None):
+        """protokv_attend_static: the readout with its scratch in the library's
+        fixed device array (no allocation by the library)."""
+        torch = self.torch
+        tq = q.shape[1]
+        self._check_tensor(q, (self.cfg.num_layers, tq, self.cfg.num_q_heads, self.cfg.head_dim))
+        if out is None:
+            out = torch.empty_like(q)
+        if lse is None:
+            lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+        _check(lib().protokv_attend_static(self.h, stream_id, q.data_ptr(), tq, out.data_ptr(),
+                                           lse.data_ptr() if lse is not False else None,
+                                           _stream_ptr(stream)), self.h)
         return out, lse
 
     # -- introspection -----------------------------------------------------
