@@ -951,7 +951,8 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
 // (token, K/V, subspace) in parallel and each group adds its slots' codes
 // to their histograms.
 // ---------------------------------------------------------------------------
-constexpr int AGG_SLOTS = 32;  // slots per workgroup: two per 16-lane group (k0 + g, k0 + g + 16)
+// slots per workgroup: NP per 16-lane group (k0 + g + 16 p, p < NP), 16 NP in all
+constexpr int AGG_NP = 2;
 constexpr int AGG_TOK_BYTES = 32768;  // LDS for the workgroup's tokens (64 bf16 or 32 float32 tokens)
 constexpr int TOK_BATCH = 2;
 constexpr uint16_t NO_SLOT = 0xFFFF;
@@ -986,8 +987,11 @@ __device__ __forceinline__ void st8f(uint8_t* p, const float (&x)[8]) {
   reinterpret_cast<float4*>(p)[1] = make_float4(x[4], x[5], x[6], x[7]);
 }
 
-template <int FP32, int EMA>
-__global__ __launch_bounds__(256, EMA ? 2 : 4) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb, int wg_per_unit) {
+template <int FP32, int EMA, int NP>
+__global__ __launch_bounds__(256, EMA ? 2 : (NP > 2 ? 3 : 4)) void k_aggregate(Dims dm, Workspace ws, FoldBatch fb,
+                                                                            int wg_per_unit) {
+  constexpr int AGG_SLOTS = 16 * NP;
+  constexpr int NGW = 4 * NP;              // (group, pass) pairs of one wave
   __shared__ uint16_t s_asg[TMAX];         // slot of each token (NO_SLOT: seeded / padding)
   __shared__ uint16_t s_tok[TMAX];         // tokens of this workgroup's slots, grouped, eviction order
   __shared__ int s_cnt[AGG_SLOTS];
@@ -1021,36 +1025,44 @@ __global__ __launch_bounds__(256, EMA ? 2 : 4) void k_aggregate(Dims dm, Workspa
   for (int j = tid; j < N64; j += 256)
     s_asg[j] = (j >= nseed && j < N) ? (uint16_t)ws.assign[unit * N + j] : NO_SLOT;
   __syncthreads();
-  // wave w sweeps for the local slots of its lane groups: q = 4 w + g and
-  // q + 16 (slot k0 + q), g = 0..3
-  int kw[8];
+  // wave w sweeps for the local slots of its lane groups: q = 4 w + g + 16 p
+  // (slot k0 + q), g = 0..3, p < NP
+  int kw[NGW];
 #pragma unroll
-  for (int g = 0; g < 8; ++g) {
+  for (int g = 0; g < NGW; ++g) {
     const int q = 4 * wave + (g & 3) + 16 * (g >> 2);
     kw[g] = (k0 + q < kact) ? k0 + q : -1;
   }
-  int cw[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  int cw[NGW];
+#pragma unroll
+  for (int g = 0; g < NGW; ++g) cw[g] = 0;
   for (int c = 0; c < N64; c += 64) {
     const int a = s_asg[c + lane];
 #pragma unroll
-    for (int g = 0; g < 8; ++g) cw[g] += __popcll(__ballot(a == kw[g]));
+    for (int g = 0; g < NGW; ++g) cw[g] += __popcll(__ballot(a == kw[g]));
   }
-  if (lane < 8) {
+  if (lane < NGW) {
     int v = cw[0];
 #pragma unroll
-    for (int g = 1; g < 8; ++g) v = lane == g ? cw[g] : v;
+    for (int g = 1; g < NGW; ++g) v = lane == g ? cw[g] : v;
     s_cnt[4 * wave + (lane & 3) + 16 * (lane >> 2)] = v;
   }
   __syncthreads();
   if (wave == 0) {
-    const int v = lane < AGG_SLOTS ? s_cnt[lane] : 0;
-    int incl = v;
+    // inclusive scan of the counts, entries lane and lane + 64
+    int carry = 0;
 #pragma unroll
-    for (int o = 1; o < AGG_SLOTS; o <<= 1) {
-      const int y = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += y;
+    for (int h = 0; h < (AGG_SLOTS + 63) / 64; ++h) {
+      const int e = h * 64 + lane;
+      int incl = e < AGG_SLOTS ? s_cnt[e] : 0;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      if (e < AGG_SLOTS) s_off[e + 1] = carry + incl;
+      carry += __shfl(incl, 63, 64);
     }
-    if (lane < AGG_SLOTS) s_off[lane + 1] = incl;
     if (lane == 0) s_off[0] = 0;
   }
   __syncthreads();
@@ -1059,13 +1071,13 @@ __global__ __launch_bounds__(256, EMA ? 2 : 4) void k_aggregate(Dims dm, Workspa
     const float4* src = reinterpret_cast<const float4*>(ws.codebooks + unit * (2 * G * CMAX * DP));
     for (int x = tid; x < 2 * G * CMAX * DP / 4; x += 256) reinterpret_cast<float4*>(s_cb)[x] = src[x];
   }
-  int ow[8];
+  int ow[NGW];
 #pragma unroll
-  for (int g = 0; g < 8; ++g) ow[g] = s_off[4 * wave + (g & 3) + 16 * (g >> 2)];
+  for (int g = 0; g < NGW; ++g) ow[g] = s_off[4 * wave + (g & 3) + 16 * (g >> 2)];
   for (int c = 0; c < N64; c += 64) {
     const int a = s_asg[c + lane];
 #pragma unroll
-    for (int g = 0; g < 8; ++g) {
+    for (int g = 0; g < NGW; ++g) {
       const unsigned long long mk = __ballot(a == kw[g]);
       if (a == kw[g]) s_tok[ow[g] + __popcll(mk & below)] = (uint16_t)(c + lane);
       ow[g] += __popcll(mk);
@@ -1095,31 +1107,40 @@ __global__ __launch_bounds__(256, EMA ? 2 : 4) void k_aggregate(Dims dm, Workspa
       lds_dma16(src, s_tk + i * 1024);
     }
   }
-  // the first slot's row (loads in flight with the tokens')
+  // the group's first touched slot's row (loads in flight with the
+  // tokens'); each later touched slot's row is loaded while the one before
+  // it absorbs its tokens
   float sk[8], sv[8], qk[8], qv[8];
-  RowMeta m;
-  auto load_row = [&](int q) {
+  float nk[8], nv[8], nqk[8], nqv[8];
+  RowMeta m, nm;
+  auto load_row = [&](int q, float (&a)[8], float (&b)[8], float (&c)[8], float (&d)[8], RowMeta& mm) {
     const uint8_t* row = ws.bank + (unit * dm.K + k0 + q) * ROW;
-    ld8f(row + ROW_SUMK + il * 32, sk);
-    ld8f(row + ROW_SUMV + il * 32, sv);
-    ld8f(row + ROW_SQK + il * 32, qk);
-    ld8f(row + ROW_SQV + il * 32, qv);
-    m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+    ld8f(row + ROW_SUMK + il * 32, a);
+    ld8f(row + ROW_SUMV + il * 32, b);
+    ld8f(row + ROW_SQK + il * 32, c);
+    ld8f(row + ROW_SQV + il * 32, d);
+    mm = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  };
+  // next pass >= p with tokens for this group (NP if none)
+  auto next_pass = [&](int p) {
+    while (p < NP && s_off[gi + 16 * p + 1] == s_off[gi + 16 * p]) ++p;
+    return p;
   };
   const float ak = dm.alpha, av = dm.beta, a1k = 1.0f - dm.alpha, a1v = 1.0f - dm.beta;
-  if (s_off[gi + 1] > s_off[gi]) load_row(gi);
+  int pnext = next_pass(0);
+  if (pnext < NP) load_row(gi + 16 * pnext, sk, sv, qk, qv, m);
   if (staged) {
     wait_vm<0>();  // this wave's token loads (and its row loads) have landed
     __syncthreads();
   }
-  for (int pass = 0; pass < 2; ++pass) {  // uniform per lane group; no barrier below
+  for (int pass = pnext; pass < NP; pass = pnext) {  // uniform per lane group; no barrier below
     const int q = gi + 16 * pass;
     const int t0 = s_off[q], t1 = s_off[q + 1];
-    if (t1 == t0) continue;
     const int k = k0 + q;
     const size_t si = unit * dm.K + k;
     uint8_t* row = ws.bank + si * ROW;
-    if (pass == 1) load_row(q);
+    pnext = next_pass(pass + 1);
+    if (NP > 2 && pnext < NP) load_row(gi + 16 * pnext, nk, nv, nqk, nqv, nm);
     for (int tb = t0; tb < t1; tb += TOK_BATCH) {  // uniform per lane group
       // a batch's loads all in flight together (indices clamped into the list)
       int jb[TOK_BATCH];
@@ -1199,6 +1220,20 @@ __global__ __launch_bounds__(256, EMA ? 2 : 4) void k_aggregate(Dims dm, Workspa
     refresh_cache16(dm, sk, m, unit, k, ws, il);
     // per-slot count of folds that touched it (owned by this lane group: no atomics)
     if (il == 0) ws.touched[si] += 1u;
+    if (pnext < NP) {
+      if (NP > 2) {
+#pragma unroll
+        for (int d = 0; d < 8; ++d) {
+          sk[d] = nk[d];
+          sv[d] = nv[d];
+          qk[d] = nqk[d];
+          qv[d] = nqv[d];
+        }
+        m = nm;
+      } else {
+        load_row(gi + 16 * pnext, sk, sv, qk, qv, m);
+      }
+    }
   }
   if (EMA && pq) {
     // every (token, K/V, subspace) of the workgroup coded in parallel from
@@ -1235,7 +1270,7 @@ __global__ __launch_bounds__(256, EMA ? 2 : 4) void k_aggregate(Dims dm, Workspa
     __syncthreads();
     // each group adds its slots' codes to their histograms: lane il holds
     // bins H[il / 2][8 (il % 2) ..] of K and of V
-    for (int pass = 0; pass < 2; ++pass) {
+    for (int pass = 0; pass < NP; ++pass) {
       const int q = gi + 16 * pass;
       const int t0 = s_off[q], t1 = s_off[q + 1];
       if (t1 == t0) continue;
@@ -1260,12 +1295,16 @@ __global__ __launch_bounds__(256, EMA ? 2 : 4) void k_aggregate(Dims dm, Workspa
 }
 
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
-  const int wpu = (dm.K + AGG_SLOTS - 1) / AGG_SLOTS;
-  dim3 grid(fb.n * dm.units * wpu);
   const bool ema = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) != 0;
+  // running means: AGG_NP slots per lane group (16 AGG_NP per workgroup);
+  // EMA centres code their residuals in the workgroup: two per group
+  constexpr int NPM = AGG_NP;
+  const int slots = ema ? 32 : 16 * NPM;
+  const int wpu = (dm.K + slots - 1) / slots;
+  dim3 grid(fb.n * dm.units * wpu);
   using KFn = void (*)(Dims, Workspace, FoldBatch, int);
-  const KFn fn = dm.kv_fp32 ? (ema ? k_aggregate<1, 1> : k_aggregate<1, 0>)
-                            : (ema ? k_aggregate<0, 1> : k_aggregate<0, 0>);
+  const KFn fn = dm.kv_fp32 ? (ema ? k_aggregate<1, 1, 2> : k_aggregate<1, 0, NPM>)
+                            : (ema ? k_aggregate<0, 1, 2> : k_aggregate<0, 0, NPM>);
   hipLaunchKernelGGL(fn, grid, dim3(256), 0, st, dm, ws, fb, wpu);
   return hipGetLastError();
 }
