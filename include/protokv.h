@@ -59,7 +59,9 @@ enum {
   PROTOKV_FLAG_PQ = 1u,        /* residual statistics on (off = "w/o residual stats" ablation) */
   PROTOKV_FLAG_MASS_BIAS = 2u, /* log-mass bias on (off = "b_k = 0" ablation) */
   PROTOKV_FLAG_MAINTENANCE = 4u, /* Alg. "Prototype Maintenance" after every fold (capacity <= 2048) */
-  PROTOKV_FLAG_EMA_CENTRES = 8u  /* Alg. "ProtoKV Streaming Update" fixed-rate EMA centres (not with maintenance) */
+  PROTOKV_FLAG_EMA_CENTRES = 8u, /* Alg. "ProtoKV Streaming Update" fixed-rate EMA centres (not with maintenance) */
+  PROTOKV_FLAG_MAH_SQUARED = 16u /* Eq. 1's spatial term as the squared Mahalanobis distance d^T (Sigma + rho I)^-1 d
+                                    (default: its square root, the distance) */
 };
 
 typedef struct {

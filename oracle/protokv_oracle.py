@@ -61,7 +61,9 @@ Readings where the paper is silent or at odds with itself:
 * ties in the argmin of Eq. 1 go to the lowest slot; cos is 0 when either
   vector is zero;
 * d_Mah is the (unsquared) distance sqrt(d^T (Sigma + rho I)^-1 d) with a
-  ridge rho = 1e-4; coordinates are cell centres ((col+.5)/W, (row+.5)/H);
+  ridge rho = 1e-4 (Params.mah_squared: the squared form d^T (Sigma + rho
+  I)^-1 d, the gating distance of the tracker the paper cites for this
+  term); coordinates are cell centres ((col+.5)/W, (row+.5)/H);
 * tau is the stream position of the most recently absorbed source token; a
   prototype is idle when (current frame) - (frame of tau) > T_idle frames;
 * PQ residuals are taken against the centre before this fold's updates
@@ -149,6 +151,9 @@ class Params:
     kv_dtype: str = "bf16"
     use_pq: bool = True
     mass_bias: bool = True
+    # Eq. 1's spatial term as the squared Mahalanobis distance (default: the
+    # distance itself)
+    mah_squared: bool = False
     # Alg. "Prototype Maintenance" (off unless asked for); gamma and the
     # thresholds are float64, so (1 - 0.05) n lands on the integers the paper
     # means (a float32 gamma = 0.0500000007 would floor 0.95 * 40 to 37)
@@ -274,7 +279,7 @@ def assignment_costs(keys: np.ndarray, coords: np.ndarray, bank: Bank, t_frame: 
     Cc = bank.sigma[:, 2].astype(np.float64) + p.ridge
     det = A * Cc - Bxy * Bxy
     q = (Cc[None, :] * dx * dx - 2.0 * Bxy[None, :] * dx * dy + A[None, :] * dy * dy) / det[None, :]
-    d_mah = np.sqrt(np.maximum(q, 0.0))
+    d_mah = np.maximum(q, 0.0) if p.mah_squared else np.sqrt(np.maximum(q, 0.0))
 
     T = p.tokens_per_frame
     idle = ((t_frame - bank.tau // T) > p.t_idle).astype(np.float64)

@@ -287,7 +287,7 @@ __device__ double cost_from_meta(const Dims& dm, double dot, double knorm, doubl
   double A = (double)m.sxx + dm.ridge, B = (double)m.sxy, Cc = (double)m.syy + dm.ridge;
   double det = A * Cc - B * B;
   double q = (Cc * dx * dx - 2.0 * B * dx * dy + A * dy * dy) / det;
-  double dm_ = sqrt(q > 0.0 ? q : 0.0);
+  double dm_ = (dm.flags & PROTOKV_FLAG_MAH_SQUARED) ? (q > 0.0 ? q : 0.0) : sqrt(q > 0.0 ? q : 0.0);
   double idle = (t_frame - m.tau / dm.T) > dm.t_idle ? 1.0 : 0.0;
   return -cosv + dm.lambda_sp * dm_ + dm.lambda_idle * idle;
 }
@@ -521,7 +521,9 @@ __device__ __forceinline__ void top3_merge(Top3& a, const Top3& b) {
 
 // Approximate cost of one (token, slot) pair folded into the token's running
 // top-3.  a = (mu_x, mu_y, qa, 2 qb), c = (qc, lambda_idle * idle), with c.y =
-// +inf for rows past the active slots.
+// +inf for rows past the active slots.  SQ: the spatial term is q itself
+// (the squared distance), whose error is eq.
+template <int SQ>
 __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, float ty, const float4& a,
                                             const float2& c, int k, float lsp, Top3& top) {
   const float dx = tx - a.x, dy = ty - a.y;
@@ -536,6 +538,14 @@ __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, flo
   // (|sqrt a - sqrt b| <= |a - b| / sqrt(max(a, b)) and <= sqrt|a - b|; raw
   // v_rsq_f32 is accurate to ~1 ulp for the normal arguments >= 1e-30 used here)
   const float qp = fmaxf(q, 0.f);
+  if (SQ) {
+    // |max(q, 0) - q_exact| <= eq (q_exact >= 0); the assembly's rounding
+    // relative to the term is covered as for the distance
+    const float cost = fmaf(lsp, qp, fmaf(-dot, invn, c.y));
+    top.emax = fmaxf(top.emax, fmaf(6.5e-7f, qp, eq));
+    top3_push(top, cost, k);
+    return;
+  }
   const float rq = __builtin_amdgcn_rsqf(fmaxf(qp, eq));
   const float dd = qp * rq;
   const float cost = fmaf(lsp, dd, fmaf(-dot, invn, c.y));
@@ -545,7 +555,7 @@ __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, flo
 
 constexpr int SCREEN_WAVES = 4;
 
-template <int FP32>
+template <int FP32, int SQ>
 __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
   // token operands of the workgroup in MFMA B order [token half][k-step][lane]
   __shared__ bf16x8 s_bk[2][8][64];
@@ -700,8 +710,8 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
       const float4 a = s_ma[wave][m];
       const float2 c = s_mb[wave][m];
       const int k = t * 32 + m;
-      screen_pair(acc0[r], invn[0], tx[0], ty[0], a, c, k, lsp, top[0]);
-      screen_pair(acc1[r], invn[1], tx[1], ty[1], a, c, k, lsp, top[1]);
+      screen_pair<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, k, lsp, top[0]);
+      screen_pair<SQ>(acc1[r], invn[1], tx[1], ty[1], a, c, k, lsp, top[1]);
       if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -927,10 +937,10 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
 hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
   int tpu = (dm.T + SCREEN_TOK - 1) / SCREEN_TOK;
   dim3 grid(fb.n * dm.units * tpu);
-  if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_screen<1>, grid, dim3(64 * SCREEN_WAVES), 0, st, dm, ws, fb, tpu);
-  else
-    hipLaunchKernelGGL(k_screen<0>, grid, dim3(64 * SCREEN_WAVES), 0, st, dm, ws, fb, tpu);
+  using KFn = void (*)(Dims, Workspace, FoldBatch, int);
+  const bool sq = (dm.flags & PROTOKV_FLAG_MAH_SQUARED) != 0;
+  const KFn fn = dm.kv_fp32 ? (sq ? k_screen<1, 1> : k_screen<1, 0>) : (sq ? k_screen<0, 1> : k_screen<0, 0>);
+  hipLaunchKernelGGL(fn, grid, dim3(64 * SCREEN_WAVES), 0, st, dm, ws, fb, tpu);
   return hipGetLastError();
 }
 

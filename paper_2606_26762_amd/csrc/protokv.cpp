@@ -163,7 +163,7 @@ protokv_status check_config(const protokv_config* c, std::string& why) {
     return uns("max_query_tokens * (num_q_heads/num_kv_heads) above 512");
   if (c->kv_dtype != PROTOKV_KV_BF16 && c->kv_dtype != PROTOKV_KV_FP32) return bad("kv_dtype unknown");
   if (c->flags & ~(uint32_t)(PROTOKV_FLAG_PQ | PROTOKV_FLAG_MASS_BIAS | PROTOKV_FLAG_MAINTENANCE |
-                             PROTOKV_FLAG_EMA_CENTRES))
+                             PROTOKV_FLAG_EMA_CENTRES | PROTOKV_FLAG_MAH_SQUARED))
     return bad("unknown flag bits");
   if (c->flags & PROTOKV_FLAG_EMA_CENTRES) {
     if (!(c->alpha >= 0.f && c->alpha <= 1.f) || !(c->beta >= 0.f && c->beta <= 1.f))

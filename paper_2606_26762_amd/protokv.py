@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "libprotokv.so")
 
 ROW_BYTES = 3200
 KV_BF16, KV_FP32 = 0, 1
-FLAG_PQ, FLAG_MASS_BIAS, FLAG_MAINTENANCE, FLAG_EMA_CENTRES = 1, 2, 4, 8
+FLAG_PQ, FLAG_MASS_BIAS, FLAG_MAINTENANCE, FLAG_EMA_CENTRES, FLAG_MAH_SQUARED = 1, 2, 4, 8, 16
 
 STATUS = {0: "OK", 1: "E_INVALID", 2: "E_UNSUPPORTED", 3: "E_WORKSPACE", 4: "E_STATE", 5: "E_DEVICE"}
 

@@ -54,7 +54,8 @@ def oracle_params(wl: W.Workload, **kw) -> O.Params:
 
 def gpu_config(wl: W.Workload, p: O.Params, streams: int = 1, max_query_tokens=None) -> pk.Config:
     flags = ((pk.FLAG_PQ if p.use_pq else 0) | (pk.FLAG_MASS_BIAS if p.mass_bias else 0)
-             | (pk.FLAG_MAINTENANCE if p.maintenance else 0) | (pk.FLAG_EMA_CENTRES if p.ema else 0))
+             | (pk.FLAG_MAINTENANCE if p.maintenance else 0) | (pk.FLAG_EMA_CENTRES if p.ema else 0)
+             | (pk.FLAG_MAH_SQUARED if p.mah_squared else 0))
     return pk.default_config(
         num_streams=streams, num_layers=wl.num_layers, num_kv_heads=wl.num_kv_heads,
         num_q_heads=wl.num_q_heads, head_dim=wl.head_dim, grid_h=wl.grid_h, grid_w=wl.grid_w,

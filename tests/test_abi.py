@@ -53,7 +53,7 @@ def lib_status(c):
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 64, 2), ("num_q_heads", 30, 1), ("num_streams", 0, 1), ("pq_subspaces", 4, 2),
     ("pq_codewords", 17, 2), ("pseudo_per_proto", 17, 2), ("beam", 4, 1), ("capacity", 0, 1),
-    ("window_frames", 0, 1), ("grid_h", 80, 2), ("kv_dtype", 7, 1), ("flags", 16, 1),
+    ("window_frames", 0, 1), ("grid_h", 80, 2), ("kv_dtype", 7, 1), ("flags", 32, 1),
     ("eta", 0.0, 1), ("pq_eps", 0.5, 2), ("ridge", 0.0, 1), ("lambda_sp", -1.0, 1),
     ("max_query_tokens", 100, 2), ("max_query_tokens", 0, 1), ("t_idle", -1, 1),
     ("rope_theta", 0.5, 1), ("rope_theta", -1.0, 1), ("rope_theta", float("inf"), 1),

@@ -65,6 +65,29 @@ def test_7b_shape_one_layer():
     pair.check_near_tie_counter()
 
 
+@pytest.mark.parametrize("wl_name", ["7b", "hires"])
+def test_squared_mahalanobis(wl_name):
+    """Eq. 1 with the squared spatial term (PROTOKV_FLAG_MAH_SQUARED): the 7B
+    frame shape (persistent layout) and the high-resolution one (per-position
+    spatial bias), one layer, every unit followed: assignments, banks bitwise,
+    the near-tie counter, then the readout."""
+    h = H()
+    base = W.WORKLOADS[wl_name]
+    wl = base.with_(num_layers=1, num_kv_heads=2, num_q_heads=2 * (base.num_q_heads // base.num_kv_heads),
+                    frames=24 if wl_name == "hires" else 40)
+    h.log(f"case: squared Mahalanobis {wl.name} L=1 Hkv=2 frames={wl.frames}")
+    pair = h.Pair(wl, mah_squared=True)
+    for f in range(wl.frames):
+        pair.step()
+    pair.check_bank(bitwise=True)
+    pair.check_near_tie_counter()
+    pseudo = pair.synthesize()
+    worst, *_ = pair.attend(pair.query(np.random.default_rng(17)), pseudo)
+    c = pair.gpu.counters()
+    h.log(f"assignments {pair.assign_checked}, near ties {pair.near_ties}, refined {c.refined}+{c.refined_full}, "
+          f"readout err {worst:.2e}")
+
+
 def test_maximum_frame_and_query_sizes():
     """The largest shapes the library accepts per call: 1024 tokens per frame
     (32x32 grid), 512 query rows per kv head (64 query tokens x 8 query

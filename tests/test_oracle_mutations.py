@@ -59,6 +59,8 @@ MUTATIONS = [
     ("assignment_costs", "> p.t_idle", ">= p.t_idle", [P.test_idle_term_counts_frames]),
     ("assignment_costs", "p.lambda_sp * d_mah", "p.lambda_sp * d_mah * d_mah",
      [P.test_cost_matches_scipy_cosine_and_mahalanobis]),
+    ("assignment_costs", "d_mah = np.maximum(q, 0.0) if p.mah_squared", "d_mah = np.sqrt(np.maximum(q, 0.0)) if p.mah_squared",
+     [P.test_squared_mahalanobis_cost_matches_scipy]),
     ("argmin_lowest", "idx = np.argmin(cost, axis=1)", "idx = np.argmax(cost, axis=1)",
      [P.test_zero_lambdas_is_spherical_kmeans_assignment]),
     ("spatial_coords", "F32(col + 0.5) / F32(grid_w)", "F32(row + 0.5) / F32(grid_w)",

@@ -174,7 +174,16 @@ def _random_bank(p, rng, n_active):
 
 
 def test_cost_matches_scipy_cosine_and_mahalanobis():
-    p = tiny_params(grid_h=6, grid_w=6, capacity=40)
+    _cost_vs_scipy(False)
+
+
+def test_squared_mahalanobis_cost_matches_scipy():
+    """The squared reading of the spatial term: scipy's distance, squared."""
+    _cost_vs_scipy(True)
+
+
+def _cost_vs_scipy(squared):
+    p = tiny_params(grid_h=6, grid_w=6, capacity=40, mah_squared=squared)
     rng = np.random.default_rng(0)
     bank = _random_bank(p, rng, 33)
     keys = rng.standard_normal((36, p.head_dim)).astype(F32)
@@ -190,7 +199,7 @@ def test_cost_matches_scipy_cosine_and_mahalanobis():
         idle = 1.0 if t - bank.tau[k] // p.tokens_per_frame > p.t_idle else 0.0
         for i in range(len(keys)):
             mah = ssd.mahalanobis(coords[i].astype(np.float64), bank.mu[k].astype(np.float64), vi)
-            ref = -(1.0 - cosd[i, k]) + p.lambda_sp * mah + p.lambda_idle * idle
+            ref = -(1.0 - cosd[i, k]) + p.lambda_sp * (mah * mah if squared else mah) + p.lambda_idle * idle
             assert abs(cost[i, k] - ref) < 1e-9
 
 
