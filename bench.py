@@ -80,7 +80,7 @@ SUB_WORKLOADS = ("7b", "long", "hires")
 def parse(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=128, help="timed rounds of the headline workload")
+    ap.add_argument("--steps", type=int, default=64, help="timed rounds of the headline workload")
     ap.add_argument("--warmup", type=int, default=8,
                     help="untimed steady-state rounds after the windows and banks are filled")
     ap.add_argument("--workload", default="multi")
@@ -89,7 +89,9 @@ def parse(argv=None):
                     help="comma-separated workloads reported as sub-objects ('' = none)")
     ap.add_argument("--sub-steps", type=int, default=32)
     ap.add_argument("--query-reps", type=int, default=20)
-    ap.add_argument("--pool", type=int, default=16, help="distinct device frames cycled per multi-stream run")
+    ap.add_argument("--pool", type=int, default=0,
+                    help="distinct device frames cycled per multi-stream run (0: every frame distinct, "
+                         "up to 100 GB of frames)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=16)
     ap.add_argument("--cpu-frames", type=int, default=32)
@@ -313,9 +315,10 @@ def run_workload(wl, args, steps, warmup, profile_frames, query_reps, headline):
     eng = pk.ProtoKV(cfg, cb.reshape(-1, *cb.shape[2:]))
     del cb
     gen = W.DeviceStream(wl, n_streams=NS)
-    # one stream: every frame drawn ahead; several: a pool of distinct frames
-    # (each [streams][L][Hkv][T][D]) taken in turn
-    nframes = pl["total"] if NS == 1 else min(args.pool, pl["total"])
+    # every frame drawn ahead (each [streams][L][Hkv][T][D]), up to 100 GB of
+    # them; beyond that (or --pool) a pool of distinct frames taken in turn
+    frame_bytes = 2 * NS * wl.units * wl.tokens_per_frame * D * kv_bytes(wl)
+    nframes = min(pl["total"], args.pool or pl["total"], max(1, int(100e9 // frame_bytes)))
     ks, vs = [], []
     for _ in range(nframes):
         k, v = gen.next_frame()
@@ -492,6 +495,7 @@ def run_workload(wl, args, steps, warmup, profile_frames, query_reps, headline):
         "attend_us_per_query": round(1e3 * attend_ms, 2),
         "wall_s_timed_region": round(t_wall, 4),
         "touched_per_unit_fold": round(touched_live, 2), "active_slots": n_active, "context_tokens": ctx,
+        "distinct_frames": nframes,
         "refined_fraction": round((c3.refined + c3.refined_full) / max(1, c3.tokens_assigned), 5),
         "near_ties": c3.near_ties, "frames_per_stream": r,
         "kernels": kernels, "query_kernels_us": query_kernels,
