@@ -75,6 +75,23 @@ Readings where the paper is silent or at odds with itself:
   between equal scores go to the lexicographically smaller code tuple;
 * pseudo-tokens are rounded to the KV dtype from the float32 sum c + r;
   centres are float32(sumK / n);
+* with Params.var_alloc (appendix "Dynamic Pseudo-Token Allocation") each
+  active prototype k gets S_k pseudo-tokens, its top-S_k code tuples, in
+  place of S.  Var(H_k) is the total variance of the residual distribution
+  the PQ statistics describe: per side (K, V) and subspace g the empirical
+  code distribution H[g][c] / n_res places mass on the codewords C_g[c];
+  Var(H_k) sums, over sides and subspaces, sum_c P(c) |C_g[c]|^2 -
+  |sum_c P(c) C_g[c]|^2 (0 without residuals).  The total S_tot = A * S
+  over the A active prototypes (the paper's K_max * S once the bank is
+  full) is kept; every prototype keeps one pseudo-token (with Var = 0 the
+  proportional share would remove it, and its mass, from the readout) and
+  the other S_tot - A are shared in proportion to Var(H_k), capped at s_max
+  (the excess re-shared among the uncapped, repeatedly; with no variance
+  left they share equally; with no variance at all every S_k = S); the
+  real shares x_k become integers by cumulative rounding,
+  S_k = floor(X_k + 1/2) - floor(X_(k-1) + 1/2) with X_k the sum of
+  x_1..x_k in slot order, which keeps the total and each S_k within one of
+  x_k.  All of it in float64, sums in slot order;
 * maintenance (Alg. "Prototype Maintenance", when enabled) runs once per
   fold, after the evicted frame is absorbed, at the current frame t, over
   the active prefix of A slots (the slots seeded so far).  Aging: an idle
@@ -168,6 +185,11 @@ class Params:
     beta: float = TABLE5_DEFAULTS["beta"]
     # rotary positions in the readout (0 = keys and queries used as given)
     rope_theta: float = 0.0
+    # variance-aware pseudo-token allocation (appendix "Dynamic Pseudo-Token
+    # Allocation"): S_k per prototype under the fixed total A * S, at most
+    # s_max each (off: S for every prototype)
+    var_alloc: bool = False
+    s_max: int = 16
     # PQ codebook warm-up: the first warm_frames folds collect residuals (no
     # PQ counts), then mini-batch k-means learns the codebooks (0 = off: the
     # given codebooks are used from the start)
@@ -675,12 +697,99 @@ class Pseudo:
     slots: np.ndarray    # slot k of each pseudo-token
 
 
+def residual_variance(bank: Bank, codebooks: np.ndarray) -> np.ndarray:
+    """Var(H_k) of every slot, float64 [K]: over sides (K then V) and
+    subspaces g ascending, sum_c P(c) |C[c]|^2 - |sum_c P(c) C[c]|^2 with
+    P(c) = H[g][c] / n_res (clamped at 0), where |C[c]|^2 and the mean are
+    summed over the subspace's dims ascending and over codewords ascending;
+    0 for slots without residuals."""
+    K = len(bank.n)
+    G, C, Dp = codebooks.shape[1:]
+    nres = bank.n_res.astype(np.float64)
+    has = nres > 0
+    denom = np.where(has, nres, 1.0)
+    total = np.zeros(K)
+    for side, hist in ((0, bank.hist_k), (1, bank.hist_v)):
+        for g in range(G):
+            cw = codebooks[side, g].astype(np.float64)         # [C][Dp]
+            n2 = np.zeros(C)
+            for u in range(Dp):
+                n2 = n2 + cw[:, u] * cw[:, u]
+            e2 = np.zeros(K)
+            mean = np.zeros((K, Dp))
+            for c in range(C):
+                pc = hist[:, g, c].astype(np.float64) / denom
+                e2 = e2 + pc * n2[c]
+                mean = mean + pc[:, None] * cw[c][None, :]
+            m2 = np.zeros(K)
+            for u in range(Dp):
+                m2 = m2 + mean[:, u] * mean[:, u]
+            total = total + np.maximum(e2 - m2, 0.0)
+    return np.where(has, total, 0.0)
+
+
+def allocate_pseudo(var: Sequence[float], S: int, s_max: int) -> List[int]:
+    """S_k for the A = len(var) active prototypes under the total A * S."""
+    A = len(var)
+    if A == 0:
+        return []
+    wsum = 0.0
+    for v in var:
+        wsum += float(v)
+    if wsum == 0.0:
+        return [S] * A
+    total = A * S
+    capped = [False] * A
+    while True:
+        ncap = sum(capped)
+        rest = float(total - A - ncap * (s_max - 1))    # beyond one per uncapped prototype
+        w = 0.0
+        for k in range(A):
+            if not capped[k]:
+                w += float(var[k])
+        nunc = A - ncap
+        x = []
+        for k in range(A):
+            if capped[k]:
+                x.append(float(s_max))
+            elif w > 0.0:
+                x.append(1.0 + rest * float(var[k]) / w)
+            else:
+                x.append(1.0 + rest / nunc)
+        over = [k for k in range(A) if not capped[k] and x[k] > s_max]
+        if not over:
+            break
+        for k in over:
+            capped[k] = True
+    out, X, prev = [], 0.0, 0
+    for k in range(A):
+        X += x[k]
+        cur = math.floor(X + 0.5)
+        out.append(cur - prev)
+        prev = cur
+    return out
+
+
+def pseudo_counts(bank: Bank, codebooks: np.ndarray, p: Params) -> np.ndarray:
+    """Pseudo-tokens per slot: S for every active slot, or the variance-aware
+    S_k; 0 for inactive slots.  Active slots form a prefix of the bank."""
+    A = int((bank.n > 0).sum())
+    out = np.zeros(p.capacity, dtype=np.int64)
+    if not p.var_alloc:
+        out[:A] = p.S
+        return out
+    out[:A] = allocate_pseudo(residual_variance(bank, codebooks)[:A], p.S, p.s_max)
+    return out
+
+
 def synthesize(bank: Bank, codebooks: np.ndarray, p: Params) -> Pseudo:
     ks, vs, bs, sl = [], [], [], []
     zero = np.zeros(p.head_dim, dtype=F32)
+    counts = pseudo_counts(bank, codebooks, p)
     for k in range(p.capacity):
         if bank.n[k] == 0:
             continue
+        Sk = int(counts[k])
         if p.ema:  # the fields hold the centres
             c, pv = bank.sum_k[k].copy(), bank.sum_v[k].copy()
         else:
@@ -688,15 +797,15 @@ def synthesize(bank: Bank, codebooks: np.ndarray, p: Params) -> Pseudo:
             c = (bank.sum_k[k] / nf).astype(F32)
             pv = (bank.sum_v[k] / nf).astype(F32)
         if bank.n_res[k] == 0 or not p.use_pq:
-            rk = [zero] * p.S
-            rv = [zero] * p.S
+            rk = [zero] * Sk
+            rv = [zero] * Sk
         else:
-            zk = decode_top_s(bank.hist_k[k], p.S, p.B)
-            zv = decode_top_s(bank.hist_v[k], p.S, p.B)
+            zk = decode_top_s(bank.hist_k[k], Sk, max(p.B, Sk))
+            zv = decode_top_s(bank.hist_v[k], Sk, max(p.B, Sk))
             rk = [residual_from_codes(z, codebooks[0]) for z in zk]
             rv = [residual_from_codes(z, codebooks[1]) for z in zv]
         b = math.log(bank.n[k]) if p.mass_bias else 0.0
-        for s in range(p.S):
+        for s in range(Sk):
             ks.append(round_kv((c + rk[s]).astype(F32), p.kv_dtype))
             vs.append(round_kv((pv + rv[s]).astype(F32), p.kv_dtype))
             bs.append(b)

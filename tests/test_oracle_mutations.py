@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 from oracle import protokv_oracle as O
+from tests import test_oracle_alloc as AL
 from tests import test_oracle_ema as E
 from tests import test_oracle_maintenance as M
 from tests import test_oracle_pins as P
@@ -117,6 +118,22 @@ MUTATIONS = [
      [M.test_recycling_takes_near_tokens_newest_frame_first_in_raster_order]),
     ("maintain", "bank.n[j] = 0", "bank.n[j] = bank.n[j]",
      [M.test_merge_adds_statistics_and_weights_the_spatial_mean]),
+    ("residual_variance", "total = total + np.maximum(e2 - m2, 0.0)", "total = total + np.maximum(e2, 0.0)",
+     [AL.test_residual_variance_is_numpys_weighted_variance_of_the_codewords]),
+    ("residual_variance", "mean = mean + pc[:, None] * cw[c][None, :]", "mean = mean + pc[:, None] * cw[0][None, :]",
+     [AL.test_residual_variance_is_numpys_weighted_variance_of_the_codewords]),
+    ("residual_variance", "for side, hist in ((0, bank.hist_k), (1, bank.hist_v)):",
+     "for side, hist in ((0, bank.hist_k), (1, bank.hist_k)):",
+     [AL.test_residual_variance_is_numpys_weighted_variance_of_the_codewords]),
+    ("allocate_pseudo", "x.append(1.0 + rest * float(var[k]) / w)", "x.append(rest * float(var[k]) / w)",
+     [lambda: AL.test_allocation_keeps_the_total_and_follows_the_exact_shares(2, 8, 16)]),
+    ("allocate_pseudo", "cur = math.floor(X + 0.5)", "cur = math.floor(X)",
+     [AL.test_allocation_special_cases]),
+    ("allocate_pseudo", "over = [k for k in range(A) if not capped[k] and x[k] > s_max]",
+     "over = [k for k in range(A) if not capped[k] and x[k] > s_max + 4]",
+     [AL.test_allocation_special_cases]),
+    ("synthesize", "Sk = int(counts[k])", "Sk = p.S",
+     [AL.test_synthesis_gives_each_prototype_its_top_sk_modes]),
     ("_dist2", "for d in range(len(a64)):", "for d in range(len(a64) - 1):",
      [M.test_merge_distance_is_the_squared_euclidean_distance]),
     ("_dist2", "diff = a64[d] - b64[d]", "diff = a64[d] - b64[d - 1]",
