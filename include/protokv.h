@@ -60,8 +60,11 @@ enum {
   PROTOKV_FLAG_MASS_BIAS = 2u, /* log-mass bias on (off = "b_k = 0" ablation) */
   PROTOKV_FLAG_MAINTENANCE = 4u, /* Alg. "Prototype Maintenance" after every fold (capacity <= 2048) */
   PROTOKV_FLAG_EMA_CENTRES = 8u, /* Alg. "ProtoKV Streaming Update" fixed-rate EMA centres (not with maintenance) */
-  PROTOKV_FLAG_MAH_SQUARED = 16u /* Eq. 1's spatial term as the squared Mahalanobis distance d^T (Sigma + rho I)^-1 d
+  PROTOKV_FLAG_MAH_SQUARED = 16u, /* Eq. 1's spatial term as the squared Mahalanobis distance d^T (Sigma + rho I)^-1 d
                                     (default: its square root, the distance) */
+  PROTOKV_FLAG_VAR_ALLOC = 32u    /* appendix "Dynamic Pseudo-Token Allocation": S_k pseudo-tokens per prototype
+                                     in proportion to its residual variance (capacity <= 4096); see
+                                     protokv_synthesize */
 };
 
 typedef struct {
@@ -94,12 +97,14 @@ typedef struct {
   int32_t warm_tokens;      /* warm-up reservoir capacity per (stream, layer, kv head), 1..65536 */
   int32_t kmeans_epochs;    /* mini-batch k-means passes over the reservoir, >= 1 */
   int32_t kmeans_batch;     /* mini-batch size, 1..64 */
+  int32_t pseudo_max;       /* PROTOKV_FLAG_VAR_ALLOC: largest S_k, pseudo_per_proto..16 */
 } protokv_config;
 
 /* Table tab:default_config defaults (S=8, lambda_sp=0.1, lambda_idle=0.01,
  * T_idle=120, eta=0.05, alpha=beta=0.05, G=8, C=16, B=32, gamma=0.05,
  * eps_K=0.20, eps_V=0.25; maintenance, EMA centres, RoPE and the codebook
- * warm-up off, warm_tokens=1024, kmeans_epochs=4, kmeans_batch=64) with the 7B-class shape of one
+ * warm-up off, warm_tokens=1024, kmeans_epochs=4, kmeans_batch=64; variance-aware
+ * allocation off, pseudo_max=16) with the 7B-class shape of one
  * stream: 28 layers, 4 KV heads, 28 query heads, 14x14 tokens per frame,
  * W=8 frames, K=256, bf16 KV, PQ and mass bias on, eps=1, rho=1e-4.
  * Host only. */
@@ -186,6 +191,27 @@ protokv_status protokv_fold(protokv_t h, void* stream);
  * rounded to kv_dtype, is rotated at tau_k in float32 (angle reduced in
  * float64) and rounded again. */
 protokv_status protokv_synthesize(protokv_t h, int32_t stream_id, void* stream);
+/* With PROTOKV_FLAG_VAR_ALLOC (appendix "Dynamic Pseudo-Token Allocation")
+ * prototype k of each (layer, kv head) is exposed as S_k pseudo-tokens, its
+ * top-S_k code tuples (all with bias log n_k), in place of S: the A active
+ * prototypes keep the total A * S; each keeps one and the other A * (S - 1)
+ * are shared in proportion to Var(H_k), at most pseudo_max each (the excess
+ * re-shared among the others, repeatedly; with no variance left they share
+ * equally, with no variance at all every S_k = S), and the real shares x_k
+ * become integers as floor(X_k + 1/2) - floor(X_(k-1) + 1/2), X_k the sum of
+ * x_1..x_k in slot order.  Var(H_k) = sum over K and V and subspaces g of
+ * sum_c P(c) |C_g[c]|^2 - |sum_c P(c) C_g[c]|^2 (clamped at 0), P(c) =
+ * H[g][c] / n_res, 0 without residuals: the variance of the residual
+ * distribution the histograms describe.  All of it in float64 with sums in
+ * slot, subspace, codeword and dim order.  The rows are written, slot k's
+ * from row sum_(j<k) S_j of its (layer, kv head). */
+
+/* Copies the pseudo-token count of every slot of the current synthesis:
+ * int32 [num_layers][num_kv_heads][capacity] (S_k, or S for every active
+ * slot without PROTOKV_FLAG_VAR_ALLOC; 0 for inactive slots); count = that
+ * many elements.  Errors: PROTOKV_E_STATE when no synthesis was made since
+ * the last fold.  Synchronizes `stream`. */
+protokv_status protokv_read_pseudo_counts(protokv_t h, int32_t* dst, size_t count, void* stream);
 
 /* Mass-aware readout (Eq. attn_logit): for every layer l, query token t and
  * query head h, with kv head g = h / (Hq/Hkv):
@@ -393,6 +419,7 @@ enum {
   PROTOKV_K_ROPE_Q = 11,         /* rotated query (rope_theta > 0) */
   PROTOKV_K_WARM_COLLECT = 12,   /* warm-up residuals into the reservoir (warm_frames > 0) */
   PROTOKV_K_WARM_KMEANS = 13,    /* codebooks learned from the reservoir (warm_frames > 0) */
+  PROTOKV_K_ALLOC = 14,          /* variance-aware pseudo-token counts (PROTOKV_FLAG_VAR_ALLOC) */
   PROTOKV_K_COUNT = 16
 };
 

@@ -26,6 +26,7 @@ constexpr int PCW = SMAX + 2;   // words per (slot, K/V) decode record: S tuples
 constexpr int PS_SLOTS = 14;
 constexpr int PS_MIN_S = 5;
 constexpr int MT_KMAX = 2048;   // largest capacity the maintenance pass supports (its LDS)
+constexpr int AL_KMAX = 4096;   // largest capacity of the variance-aware allocation (its LDS)
 
 // Bank row (one prototype slot), byte offsets; see protokv.h.
 constexpr int ROW = PROTOKV_ROW_BYTES;
@@ -62,6 +63,7 @@ struct Dims {
   float alpha, beta;           // centre EMA rates (PROTOKV_FLAG_EMA_CENTRES)
   double rope_theta;           // rotary positions in the readout (0 = off)
   int warm_frames, warm_tokens, kmeans_epochs, kmeans_batch;  // codebook warm-up
+  int pseudo_max;  // variance-aware allocation: largest S_k
   int max_rows;    // max query rows per kv head (max_query_tokens * Hq / Hkv)
   int max_splits;  // attention context splits (partials storage)
 };
@@ -105,6 +107,10 @@ struct Workspace {
   float* reservoir;              // [streams][units][2][warm_tokens][D]: residuals, eviction order
   // EMA centres (PROTOKV_FLAG_EMA_CENTRES; otherwise null)
   float* ema_res;                // [streams][units][T][2][D]: residuals of the fold's tokens
+  // variance-aware allocation (PROTOKV_FLAG_VAR_ALLOC; otherwise null), synthesis of one stream
+  int32_t* ps_count;             // [units][K]: S_k (0 for inactive slots)
+  int32_t* ps_off;               // [units][K]: first row of slot k, sum of S_j over j < k
+  float* prow_bias;              // [units][K*S]: bias of every pseudo-token row
 };
 
 enum Counter {
@@ -156,6 +162,7 @@ struct AttendArgs {
   int chunk;        // context tokens per split (multiple of 32)
   int gen;          // bf16: pseudo-token rows are formed from centres, codes and codebooks (else read from pk, pv)
   const uint8_t* near_k;  // near-window keys: ring_k, or ring_kr with rotary positions
+  const float* rowbias;   // bias per pseudo-token row [units][K*S] (variance-aware allocation), else null
   const void* q;
   void* o;
   float* lse;
@@ -196,6 +203,8 @@ hipError_t launch_refresh_all(const Dims& dm, const Workspace& ws, int sid, hipS
 hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, bool centres, bool wide,
                          hipStream_t st);
 hipError_t launch_materialize(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st);
+// variance-aware allocation: S_k and row offsets of stream sid's slots from their histograms
+hipError_t launch_alloc(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st);
 hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& aa,
                          hipStream_t st);
 hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const AttendArgs& aa,

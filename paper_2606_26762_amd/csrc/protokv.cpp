@@ -29,7 +29,8 @@ struct StreamState {
 
 struct Layout {
   size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codebooks, cbhn, cbmax;
-  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, ring_kr, qrot, rope_inv, reservoir, ema_res, total;
+  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, ring_kr, qrot, rope_inv, reservoir, ema_res;
+  size_t ps_count, ps_off, prow_bias, total;
 };
 
 thread_local std::string g_init_err;
@@ -77,6 +78,10 @@ Layout make_layout(const protokv_config& c) {
   ly.rope_inv = take(rope ? (D / 2) * sizeof(double) : 0);
   ly.reservoir = take(c.warm_frames > 0 ? U * 2 * (size_t)c.warm_tokens * D * 4 : 0);
   ly.ema_res = take((c.flags & PROTOKV_FLAG_EMA_CENTRES) ? U * T * 2 * D * 4 : 0);
+  const bool va = (c.flags & PROTOKV_FLAG_VAR_ALLOC) != 0;
+  ly.ps_count = take(va ? units * K * 4 : 0);
+  ly.ps_off = take(va ? units * K * 4 : 0);
+  ly.prow_bias = take(va ? units * K * S * 4 : 0);
   ly.total = off;
   return ly;
 }
@@ -163,8 +168,14 @@ protokv_status check_config(const protokv_config* c, std::string& why) {
     return uns("max_query_tokens * (num_q_heads/num_kv_heads) above 512");
   if (c->kv_dtype != PROTOKV_KV_BF16 && c->kv_dtype != PROTOKV_KV_FP32) return bad("kv_dtype unknown");
   if (c->flags & ~(uint32_t)(PROTOKV_FLAG_PQ | PROTOKV_FLAG_MASS_BIAS | PROTOKV_FLAG_MAINTENANCE |
-                             PROTOKV_FLAG_EMA_CENTRES | PROTOKV_FLAG_MAH_SQUARED))
+                             PROTOKV_FLAG_EMA_CENTRES | PROTOKV_FLAG_MAH_SQUARED | PROTOKV_FLAG_VAR_ALLOC))
     return bad("unknown flag bits");
+  if (c->flags & PROTOKV_FLAG_VAR_ALLOC) {
+    if (c->pseudo_max < c->pseudo_per_proto) return bad("pseudo_max must be >= pseudo_per_proto");
+    if (c->pseudo_max > SMAX) return uns("pseudo_max above 16");
+    if (c->beam < c->pseudo_max) return bad("beam must be >= pseudo_max");
+    if (c->capacity > AL_KMAX) return uns("the variance-aware allocation supports capacity up to 4096");
+  }
   if (c->flags & PROTOKV_FLAG_EMA_CENTRES) {
     if (!(c->alpha >= 0.f && c->alpha <= 1.f) || !(c->beta >= 0.f && c->beta <= 1.f))
       return bad("alpha and beta must be in [0, 1]");
@@ -286,6 +297,7 @@ protokv_status protokv_default_config(protokv_config* c) {
   c->warm_tokens = 1024;
   c->kmeans_epochs = 4;
   c->kmeans_batch = 64;
+  c->pseudo_max = 16;
   return PROTOKV_OK;
 }
 
@@ -354,6 +366,7 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   dm.warm_tokens = c->warm_tokens;
   dm.kmeans_epochs = c->kmeans_epochs;
   dm.kmeans_batch = c->kmeans_batch;
+  dm.pseudo_max = c->pseudo_max;
   dm.max_rows = c->max_query_tokens * (c->num_q_heads / c->num_kv_heads);
   dm.max_splits = MAX_SPLITS;
   uint8_t* b = h->base;
@@ -383,6 +396,10 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.rope_inv = rope ? (const double*)(b + ly.rope_inv) : nullptr;
   ws.reservoir = c->warm_frames > 0 ? (float*)(b + ly.reservoir) : nullptr;
   ws.ema_res = (c->flags & PROTOKV_FLAG_EMA_CENTRES) ? (float*)(b + ly.ema_res) : nullptr;
+  const bool va = (c->flags & PROTOKV_FLAG_VAR_ALLOC) != 0;
+  ws.ps_count = va ? (int32_t*)(b + ly.ps_count) : nullptr;
+  ws.ps_off = va ? (int32_t*)(b + ly.ps_off) : nullptr;
+  ws.prow_bias = va ? (float*)(b + ly.prow_bias) : nullptr;
   h->st.assign(c->num_streams, StreamState());
 
   // codebooks -> [U][2][G][CMAX][DP] with the codeword axis padded to 16
@@ -553,16 +570,24 @@ protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
   if (h->st[sid].pending) return h->fail(PROTOKV_E_STATE, "synthesize: stream has an unfolded eviction");
   hipStream_t hs = (hipStream_t)stream;
   const int na = h->st[sid].active;
+  const bool va = h->ws.ps_count != nullptr;
   // bf16 with S >= PS_MIN_S: the decode also writes the float32 centres and
   // the readout forms the rows from them as it loads them; otherwise the rows
   // are written here
-  // (with rotary positions the rows are written, pseudo-keys rotated at tau_k)
-  const bool rows = h->dm.kv_fp32 != 0 || h->dm.S < PS_MIN_S || h->ws.ring_kr != nullptr;
+  // (with rotary positions the rows are written, pseudo-keys rotated at tau_k;
+  // with the variance-aware allocation each slot's S_k rows are written)
+  const bool rows = h->dm.kv_fp32 != 0 || h->dm.S < PS_MIN_S || h->ws.ring_kr != nullptr || va;
   // a slot's residual count is at most the tokens its stream has evicted
   const bool wide = h->st[sid].evicted > 65534u;
+  // the allocation decodes every slot's top pseudo_max tuples; slot k keeps its first S_k
+  Dims dd = h->dm;
+  if (va) dd.S = h->dm.pseudo_max;
   protokv_status s = h->dev(
-      h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] { return launch_decode(h->dm, h->ws, sid, na, !rows, wide, hs); }),
+      h->launch(PROTOKV_K_SYNTHESIZE, hs, [&] { return launch_decode(dd, h->ws, sid, na, !rows, wide, hs); }),
       "synthesize/decode");
+  if (s == PROTOKV_OK && va)
+    s = h->dev(h->launch(PROTOKV_K_ALLOC, hs, [&] { return launch_alloc(h->dm, h->ws, sid, na, hs); }),
+               "synthesize/allocate");
   if (s == PROTOKV_OK && rows)
     s = h->dev(h->launch(PROTOKV_K_MATERIALIZE, hs, [&] { return launch_materialize(h->dm, h->ws, sid, na, hs); }),
                "synthesize/materialize");
@@ -596,6 +621,7 @@ static protokv_status plan_attend(protokv_t h, int32_t sid, const void* q, int32
   aa.tq = tq;
   aa.q = q;
   aa.near_k = h->ws.ring_kr ? h->ws.ring_kr : h->ws.ring_k;
+  aa.rowbias = h->ws.prow_bias;
   aa.o = o;
   aa.lse = lse;
   const int ctx = aa.n_near + aa.n_far;
@@ -954,6 +980,17 @@ protokv_status protokv_set_state(protokv_t h, int32_t sid, const void* buf, size
   ss.pending = false;
   ss.pending_fe = -1;
   if (h->synth_stream == sid) h->synth_stream = -1;
+  return PROTOKV_OK;
+}
+
+protokv_status protokv_read_pseudo_counts(protokv_t h, int32_t* dst, size_t count, void* stream) {
+  if (!h) return PROTOKV_E_INVALID;
+  if (!dst) return h->fail(PROTOKV_E_INVALID, "read_pseudo_counts: dst is NULL");
+  if (h->synth_stream < 0) return h->fail(PROTOKV_E_STATE, "read_pseudo_counts: no synthesis since the last fold");
+  const size_t n = (size_t)h->dm.units * h->dm.K;
+  if (count != n) return h->fail(PROTOKV_E_INVALID, "read_pseudo_counts: count must be num_layers*num_kv_heads*capacity");
+  if (h->ws.ps_count) return copy_out(h, dst, h->ws.ps_count, n * 4, stream, "read_pseudo_counts");
+  for (size_t i = 0; i < n; ++i) dst[i] = (int)(i % h->dm.K) < h->synth_active ? h->dm.S : 0;
   return PROTOKV_OK;
 }
 

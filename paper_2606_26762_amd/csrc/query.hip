@@ -528,7 +528,10 @@ __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int 
   const int u = gw / dm.K, p = gw % dm.K;
   if (u >= dm.units || p >= n_active) return;
   const size_t unit = (size_t)sid * dm.units + u;
-  const int S = dm.S;
+  // S_k rows from row rb of the unit (variance-aware allocation), else S from p S
+  const bool var = ws.ps_count != nullptr;
+  const int S = var ? ws.ps_count[(size_t)u * dm.K + p] : dm.S;
+  const size_t rb = var ? (size_t)ws.ps_off[(size_t)u * dm.K + p] : (size_t)p * dm.S;
   const size_t es = FP32 ? 4 : 2;
   const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
   const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
@@ -543,9 +546,11 @@ __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int 
   float rc[2] = {1.f, 1.f}, rs[2] = {0.f, 0.f};
   if (rope)
     for (int e = 0; e < 2; ++e) rope_cs((double)m.tau, ws.rope_inv[2 * (lane & 31) + e], rc[e], rs[e]);
-  if (lane == 0) {
+  {
     const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
-    ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
+    const float bias = mb ? logf(nf) : 0.f;
+    if (lane == 0) ws.pbias[(size_t)u * dm.K + p] = bias;
+    if (var && lane < S) ws.prow_bias[(size_t)u * dm.K * dm.S + rb + lane] = bias;
   }
   // the decoded tuples of K and V first (all loads in flight together)
   const uint32_t* codes_k = ws.pcodes + (((size_t)u * dm.K + p) * 2) * PCW;
@@ -564,7 +569,7 @@ __global__ __launch_bounds__(256) void k_materialize(Dims dm, Workspace ws, int 
     const float2 c = w ? make_float2(sv.x / cd, sv.y / cd) : make_float2(sk.x / cd, sk.y / cd);
     const bool nores = w ? nores_v : nores_k;
     const float* cbw = cbk + ((size_t)w * G + g) * CMAX * DP + u16;
-    uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * S + (size_t)p * S) * D * es;
+    uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * dm.S + rb) * D * es;
 #pragma unroll
     for (int s2 = 0; s2 < SMAX; ++s2) {
       if (s2 < S) {
@@ -615,7 +620,10 @@ __global__ __launch_bounds__(256) void k_materialize16(Dims dm, Workspace ws, in
   const int u = gw / dm.K, p = gw % dm.K;
   if (u >= dm.units || p >= n_active) return;
   const size_t unit = (size_t)sid * dm.units + u;
-  const int S = dm.S;
+  // S_k rows from row rb of the unit (variance-aware allocation), else S from p S
+  const bool var = ws.ps_count != nullptr;
+  const int S = var ? ws.ps_count[(size_t)u * dm.K + p] : dm.S;
+  const size_t rb = var ? (size_t)ws.ps_off[(size_t)u * dm.K + p] : (size_t)p * dm.S;
   const int dq = lane & 15, r0 = lane >> 4;
   const int g = dq >> 1, hsub = (dq & 1) * 8;  // subspace of these 8 dims, offset inside it
   const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
@@ -631,9 +639,11 @@ __global__ __launch_bounds__(256) void k_materialize16(Dims dm, Workspace ws, in
     for (int e = 0; e < 8; ++e) rope_cs(tau, ws.rope_inv[8 * (dq & 7) + e], rc[e], rs[e]);
   }
   const float* cbk = ws.codebooks + unit * (2 * G * CMAX * DP);
-  if (lane == 0) {
+  {
     const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
-    ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
+    const float bias = mb ? logf(nf) : 0.f;
+    if (lane == 0) ws.pbias[(size_t)u * dm.K + p] = bias;
+    if (var && lane < S) ws.prow_bias[(size_t)u * dm.K * dm.S + rb + lane] = bias;
   }
   // everything this lane needs first: its 8 dims of both sums, the no-residual
   // flags and the tuples of its rows
@@ -660,7 +670,7 @@ __global__ __launch_bounds__(256) void k_materialize16(Dims dm, Workspace ws, in
     const float c[8] = {sr[w][0].x / cd, sr[w][0].y / cd, sr[w][0].z / cd, sr[w][0].w / cd,
                         sr[w][1].x / cd, sr[w][1].y / cd, sr[w][1].z / cd, sr[w][1].w / cd};
     const float* cbw = cbk + ((size_t)w * G + g) * CMAX * DP + hsub;
-    uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * S + (size_t)p * S) * D * 2 + dq * 16;
+    uint8_t* out = (w ? ws.pv : ws.pk) + ((size_t)u * dm.K * dm.S + rb) * D * 2 + dq * 16;
 #pragma unroll
     for (int i = 0; i < SMAX / 4; ++i) {
       const int s2 = r0 + 4 * i;
@@ -853,6 +863,145 @@ hipError_t launch_rope_q(const Dims& dm, const Workspace& ws, const void* q, int
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Variance-aware pseudo-token counts (appendix "Dynamic Pseudo-Token
+// Allocation").  Workgroup = one (layer, kv head) of stream sid.  Every
+// thread computes Var(H_k) of its slots in float64, in the order the
+// definition sums (sides, subspaces, codewords, dims ascending); one thread
+// takes the sums over slots in slot order (water-filling of the shares over
+// the cap, then cumulative rounding), the others compute the shares.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_alloc(Dims dm, Workspace ws, int sid, int A) {
+  __shared__ double s_var[AL_KMAX];
+  __shared__ double s_x[AL_KMAX];
+  __shared__ uint8_t s_cap[AL_KMAX];
+  __shared__ float s_cb[2 * G * CMAX * DP];
+  __shared__ double s_n2[2 * G * CMAX];
+  __shared__ double s_par[2];   // remaining budget, variance sum of the uncapped
+  __shared__ int s_flag;
+  const int tid = threadIdx.x, u = blockIdx.x;
+  const size_t unit = (size_t)sid * dm.units + u;
+  const int C = dm.C, S = dm.S, smax = dm.pseudo_max;
+  const float* cbk = ws.codebooks + unit * (2 * G * CMAX * DP);
+  for (int i = tid; i < 2 * G * CMAX * DP; i += 256) s_cb[i] = cbk[i];
+  __syncthreads();
+  if (tid < 2 * G * CMAX) {
+    double n2 = 0.0;
+    for (int d = 0; d < DP; ++d) {
+      const double c = (double)s_cb[tid * DP + d];
+      n2 = n2 + c * c;
+    }
+    s_n2[tid] = n2;
+  }
+  __syncthreads();
+  for (int k = tid; k < A; k += 256) {
+    const uint8_t* row = ws.bank + (unit * dm.K + k) * ROW;
+    const uint32_t nres = reinterpret_cast<const RowMeta*>(row + ROW_META)->n_res;
+    double total = 0.0;
+    if (nres > 0) {
+      const double den = (double)nres;
+      for (int side = 0; side < 2; ++side) {
+        const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (side ? ROW_HV : ROW_HK));
+        for (int g = 0; g < G; ++g) {
+          double e2 = 0.0, mean[DP];
+#pragma unroll
+          for (int d = 0; d < DP; ++d) mean[d] = 0.0;
+          for (int c = 0; c < C; ++c) {
+            const double pc = (double)hist[g * CMAX + c] / den;
+            e2 = e2 + pc * s_n2[(side * G + g) * CMAX + c];
+            const float* cw = s_cb + ((side * G + g) * CMAX + c) * DP;
+#pragma unroll
+            for (int d = 0; d < DP; ++d) mean[d] = mean[d] + pc * (double)cw[d];
+          }
+          double m2 = 0.0;
+#pragma unroll
+          for (int d = 0; d < DP; ++d) m2 = m2 + mean[d] * mean[d];
+          const double v = e2 - m2;
+          total = total + (v > 0.0 ? v : 0.0);
+        }
+      }
+    }
+    s_var[k] = total;
+    s_cap[k] = 0;
+  }
+  __syncthreads();
+  const int tot = A * S;
+  __shared__ int s_novar;
+  if (tid == 0) {
+    double w = 0.0;
+    for (int k = 0; k < A; ++k) w += s_var[k];
+    s_novar = w == 0.0 ? 1 : 0;  // no variance at all: every S_k = S
+  }
+  __syncthreads();
+  if (!s_novar) {
+    int ncap = 0;
+    for (;;) {  // uniform: every thread sees the same ncap and flags
+      if (tid == 0) {
+        double w = 0.0;
+        for (int k = 0; k < A; ++k)
+          if (!s_cap[k]) w += s_var[k];
+        s_par[0] = (double)(tot - A - ncap * (smax - 1));
+        s_par[1] = w;
+        s_flag = 0;
+      }
+      __syncthreads();
+      const double rest = s_par[0], w = s_par[1];
+      const double nunc = (double)(A - ncap);
+      for (int k = tid; k < A; k += 256) {
+        double x;
+        if (s_cap[k]) x = (double)smax;
+        else if (w > 0.0) x = 1.0 + rest * s_var[k] / w;
+        else x = 1.0 + rest / nunc;
+        s_x[k] = x;
+        if (!s_cap[k] && x > (double)smax) s_flag = 1;  // every writer stores 1
+      }
+      __syncthreads();
+      const int again = s_flag;
+      __syncthreads();
+      if (!again) break;
+      for (int k = tid; k < A; k += 256)
+        if (!s_cap[k] && s_x[k] > (double)smax) s_cap[k] = 1;
+      __syncthreads();
+      if (tid == 0) {
+        int n = 0;
+        for (int k = 0; k < A; ++k) n += s_cap[k];
+        s_par[0] = (double)n;
+      }
+      __syncthreads();
+      ncap = (int)s_par[0];
+      __syncthreads();
+    }
+  }
+  if (tid == 0) {
+    int32_t* cnt = ws.ps_count + (size_t)u * dm.K;
+    int32_t* off = ws.ps_off + (size_t)u * dm.K;
+    // cumulative rounding: S_k = floor(X_k + 1/2) - floor(X_(k-1) + 1/2)
+    double X = 0.0;
+    long long prev = 0;
+    for (int k = 0; k < A; ++k) {
+      off[k] = (int32_t)prev;
+      if (s_novar) {
+        cnt[k] = S;
+        prev += S;
+        continue;
+      }
+      X += s_x[k];
+      const long long cur = (long long)floor(X + 0.5);
+      cnt[k] = (int32_t)(cur - prev);
+      prev = cur;
+    }
+    for (int k = A; k < dm.K; ++k) {
+      cnt[k] = 0;
+      off[k] = (int32_t)prev;
+    }
+  }
+}
+
+hipError_t launch_alloc(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st) {
+  hipLaunchKernelGGL(k_alloc, dim3(dm.units), dim3(256), 0, st, dm, ws, sid, n_active);
+  return hipGetLastError();
+}
+
 hipError_t launch_materialize(const Dims& dm, const Workspace& ws, int sid, int n_active, hipStream_t st) {
   if (n_active <= 0) return hipSuccess;
   const int waves = dm.units * dm.K;
@@ -893,7 +1042,7 @@ __device__ __forceinline__ CtxRef ctx_key(const Dims& dm, const Workspace& ws, c
   } else {
     const int row = idx - aa.n_near;
     r.base = (values ? ws.pv : ws.pk) + (((size_t)u * dm.K * dm.S + row) * (size_t)D) * ES;
-    r.bias = ws.pbias[(size_t)u * dm.K + row / dm.S];
+    r.bias = aa.rowbias ? aa.rowbias[(size_t)u * dm.K * dm.S + row] : ws.pbias[(size_t)u * dm.K + row / dm.S];
   }
   return r;
 }
@@ -1000,10 +1149,14 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
       const size_t off = (((size_t)u * dm.K * dm.S + prow) * (size_t)D) * 2;
       kp = ws.pk + off;
       vp = ws.pv + off;
-      int k = (int)((float)prow * invS);
-      k -= k * dm.S > prow ? 1 : 0;
-      k += (k + 1) * dm.S <= prow ? 1 : 0;
-      if (idx < c1n) bv = pb_lds ? s_pb[k] : ws.pbias[(size_t)u * dm.K + k] * LOG2E;
+      if (aa.rowbias) {
+        if (idx < c1n) bv = aa.rowbias[(size_t)u * dm.K * dm.S + prow] * LOG2E;
+      } else {
+        int k = (int)((float)prow * invS);
+        k -= k * dm.S > prow ? 1 : 0;
+        k += (k + 1) * dm.S <= prow ? 1 : 0;
+        if (idx < c1n) bv = pb_lds ? s_pb[k] : ws.pbias[(size_t)u * dm.K + k] * LOG2E;
+      }
     }
   };
   auto publish = [&](int t, const uint8_t* kp, const uint8_t* vp, float bv) {

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "libprotokv.so")
 
 ROW_BYTES = 3200
 KV_BF16, KV_FP32 = 0, 1
-FLAG_PQ, FLAG_MASS_BIAS, FLAG_MAINTENANCE, FLAG_EMA_CENTRES, FLAG_MAH_SQUARED = 1, 2, 4, 8, 16
+FLAG_PQ, FLAG_MASS_BIAS, FLAG_MAINTENANCE, FLAG_EMA_CENTRES, FLAG_MAH_SQUARED, FLAG_VAR_ALLOC = 1, 2, 4, 8, 16, 32
 
 STATUS = {0: "OK", 1: "E_INVALID", 2: "E_UNSUPPORTED", 3: "E_WORKSPACE", 4: "E_STATE", 5: "E_DEVICE"}
 
@@ -28,6 +28,7 @@ EXPORTED = [
     "protokv_stream_info_get", "protokv_get_counters", "protokv_read_assignments", "protokv_read_bank",
     "protokv_read_pseudo", "protokv_read_codebooks", "protokv_profile", "protokv_profile_read",
     "protokv_state_size", "protokv_get_state", "protokv_set_state", "protokv_attend_static",
+    "protokv_read_pseudo_counts",
     "protokv_last_error",
 ]
 
@@ -36,7 +37,7 @@ MAX_EVICTED_TOKENS = 16777214
 STATIC_SCRATCH_BYTES = 64 << 20
 
 KERNELS = ["ring_insert", "seed", "screen", "aggregate", "decode", "attend", "attend_merge", "pq_encode",
-           "materialize", "maintain", "rope_ring", "rope_q", "warm_collect", "warm_kmeans"]
+           "materialize", "maintain", "rope_ring", "rope_q", "warm_collect", "warm_kmeans", "alloc"]
 
 
 class ProtoKVError(RuntimeError):
@@ -59,7 +60,7 @@ class Config(ctypes.Structure):
         ("gamma", ctypes.c_double), ("eps_k", ctypes.c_double), ("eps_v", ctypes.c_double),
         ("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("rope_theta", ctypes.c_double),
         ("warm_frames", ctypes.c_int32), ("warm_tokens", ctypes.c_int32),
-        ("kmeans_epochs", ctypes.c_int32), ("kmeans_batch", ctypes.c_int32),
+        ("kmeans_epochs", ctypes.c_int32), ("kmeans_batch", ctypes.c_int32), ("pseudo_max", ctypes.c_int32),
     ]
 
 
@@ -120,6 +121,7 @@ def lib() -> ctypes.CDLL:
         L.protokv_read_bank.argtypes = [vp, i32, vp, sz, vp]
         L.protokv_read_pseudo.argtypes = [vp, vp, vp, vp, vp]
         L.protokv_read_codebooks.argtypes = [vp, i32, vp, sz, vp]
+        L.protokv_read_pseudo_counts.argtypes = [vp, vp, sz, vp]
         L.protokv_profile.argtypes = [vp, ctypes.c_uint32]
         L.protokv_profile_read.argtypes = [vp, P(KernelTimes)]
         L.protokv_state_size.argtypes = [vp, P(sz)]
@@ -382,6 +384,12 @@ class ProtoKV:
     def set_state(self, stream_id: int, state, stream=None):
         blob = np.ascontiguousarray(state.blob if isinstance(state, State) else state, dtype=np.uint8)
         _check(lib().protokv_set_state(self.h, stream_id, blob.ctypes.data, blob.size, _stream_ptr(stream)), self.h)
+
+    def read_pseudo_counts(self, stream=None) -> np.ndarray:
+        """-> int32 [units][K]: pseudo-tokens per slot of the current synthesis."""
+        out = np.zeros((self.units, self.cfg.capacity), dtype=np.int32)
+        _check(lib().protokv_read_pseudo_counts(self.h, out.ctypes.data, out.size, _stream_ptr(stream)), self.h)
+        return out
 
     def profile(self, enable, kernels=None):
         """Time every launch (enable=True), only the named kernels, or stop (False)."""

@@ -55,7 +55,7 @@ def oracle_params(wl: W.Workload, **kw) -> O.Params:
 def gpu_config(wl: W.Workload, p: O.Params, streams: int = 1, max_query_tokens=None) -> pk.Config:
     flags = ((pk.FLAG_PQ if p.use_pq else 0) | (pk.FLAG_MASS_BIAS if p.mass_bias else 0)
              | (pk.FLAG_MAINTENANCE if p.maintenance else 0) | (pk.FLAG_EMA_CENTRES if p.ema else 0)
-             | (pk.FLAG_MAH_SQUARED if p.mah_squared else 0))
+             | (pk.FLAG_MAH_SQUARED if p.mah_squared else 0) | (pk.FLAG_VAR_ALLOC if p.var_alloc else 0))
     return pk.default_config(
         num_streams=streams, num_layers=wl.num_layers, num_kv_heads=wl.num_kv_heads,
         num_q_heads=wl.num_q_heads, head_dim=wl.head_dim, grid_h=wl.grid_h, grid_w=wl.grid_w,
@@ -66,7 +66,7 @@ def gpu_config(wl: W.Workload, p: O.Params, streams: int = 1, max_query_tokens=N
         eta=p.eta, lambda_sp=p.lambda_sp, lambda_idle=p.lambda_idle, ridge=p.ridge,
         gamma=p.gamma, eps_k=p.eps_k, eps_v=p.eps_v, alpha=p.alpha, beta=p.beta, rope_theta=p.rope_theta,
         warm_frames=p.warm_frames, warm_tokens=p.warm_tokens, kmeans_epochs=p.kmeans_epochs,
-        kmeans_batch=p.kmeans_batch)
+        kmeans_batch=p.kmeans_batch, pseudo_max=p.s_max)
 
 
 def assert_bank_equal(gb, u: int, ob: O.Bank, C: int, where: str, bitwise: bool):
@@ -254,8 +254,8 @@ class Resync:
             assert n == int((ob.n > 0).sum()) * self.p.S
             assert np.array_equal(gk[u][:n], ps.keys), f"stream {s} unit {u}: pseudo keys differ"
             assert np.array_equal(gv[u][:n], ps.values), f"stream {s} unit {u}: pseudo values differ"
-            slots = ps.slots[::self.p.S]
-            assert np.allclose(gbias[u][slots], ps.bias[::self.p.S], rtol=1e-6, atol=1e-6)
+            slots, first = np.unique(ps.slots, return_index=True)
+            assert np.allclose(gbias[u][slots], ps.bias[first], rtol=1e-6, atol=1e-6)
             kn = np.concatenate([f[1][i] for f in near])
             vn = np.concatenate([f[2][i] for f in near])
             k_ctx = np.concatenate([kn, ps.keys])
@@ -410,6 +410,7 @@ class Pair:
         stream, pseudo = self._rows_pending
         self._rows_pending = None
         gk, gv, gbias = self.gpu.read_pseudo()
+        gcounts = self.gpu.read_pseudo_counts() if self.p.var_alloc else None
         S = self.p.S
         for i, u in enumerate(self.sample):
             ps = pseudo[i]
@@ -429,8 +430,11 @@ class Pair:
             else:
                 assert np.array_equal(gk[u][:n], ps.keys), f"unit {u}: pseudo keys differ"
             assert np.array_equal(gv[u][:n], ps.values), f"unit {u}: pseudo values differ"
-            slots = ps.slots[::S]
-            assert np.allclose(gbias[u][slots], ps.bias[::S], rtol=1e-6, atol=1e-6)
+            slots, first = np.unique(ps.slots, return_index=True)
+            assert np.allclose(gbias[u][slots], ps.bias[first], rtol=1e-6, atol=1e-6)
+            if self.p.var_alloc:
+                want = O.pseudo_counts(self.oracle[stream].banks[i], self.oracle[stream].codebooks[i], self.p)
+                assert np.array_equal(gcounts[u].astype(np.int64), want), f"unit {u}: pseudo-token counts differ"
 
     def query(self, rng: np.random.Generator, tq: Optional[int] = None) -> np.ndarray:
         wl = self.wl

@@ -53,7 +53,7 @@ def lib_status(c):
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 64, 2), ("num_q_heads", 30, 1), ("num_streams", 0, 1), ("pq_subspaces", 4, 2),
     ("pq_codewords", 17, 2), ("pseudo_per_proto", 17, 2), ("beam", 4, 1), ("capacity", 0, 1),
-    ("window_frames", 0, 1), ("grid_h", 80, 2), ("kv_dtype", 7, 1), ("flags", 32, 1),
+    ("window_frames", 0, 1), ("grid_h", 80, 2), ("kv_dtype", 7, 1), ("flags", 64, 1),
     ("eta", 0.0, 1), ("pq_eps", 0.5, 2), ("ridge", 0.0, 1), ("lambda_sp", -1.0, 1),
     ("max_query_tokens", 100, 2), ("max_query_tokens", 0, 1), ("t_idle", -1, 1),
     ("rope_theta", 0.5, 1), ("rope_theta", -1.0, 1), ("rope_theta", float("inf"), 1),
@@ -128,3 +128,14 @@ def test_state_header_and_bank_encoding_round_trip():
     assert row[3072:3076].view(np.uint32)[0] == bank["n"][1, 2]
     assert row[3100:3104].view(np.int32)[0] == bank["tau"][1, 2]
     assert np.array_equal(row[512:1024].view(np.float32), bank["sum_v"][1, 2])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(pseudo_max=7), 1), (dict(pseudo_max=17), 2), (dict(capacity=5000), 2), (dict(beam=12), 1), ({}, 0),
+    (dict(pseudo_max=8), 0), (dict(capacity=4096), 0)])
+def test_variance_allocation_validation(kw, status):
+    """The variance-aware allocation needs S <= pseudo_max <= 16, a beam of at
+    least pseudo_max, and a capacity of at most 4096."""
+    flags = pk.FLAG_PQ | pk.FLAG_MASS_BIAS | pk.FLAG_VAR_ALLOC
+    assert lib_status(pk.default_config(flags=flags, **kw)) == status
+    assert pk.default_config().pseudo_max == 16

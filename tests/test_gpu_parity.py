@@ -88,6 +88,38 @@ def test_squared_mahalanobis(wl_name):
           f"readout err {worst:.2e}")
 
 
+@pytest.mark.parametrize("case", ["7b", "tiny", "7b+rope", "ragged"])
+def test_variance_aware_allocation(case):
+    """PROTOKV_FLAG_VAR_ALLOC (appendix "Dynamic Pseudo-Token Allocation"):
+    every slot's S_k equal to the oracle's allocation, the rows (top-S_k
+    tuples at the running offsets) bitwise, then the readout; bf16 K=256
+    S=8 up to 16, float32 S=3 up to 6, with rotary positions, and a ragged
+    shape with C=12."""
+    h = H()
+    if case == "tiny":
+        wl = W.WORKLOADS["tiny"].with_(frames=20)
+        kw = dict(S=3, s_max=6)
+    elif case == "ragged":
+        wl = W.WORKLOADS["7b"].with_(num_layers=2, num_kv_heads=2, num_q_heads=6, grid_h=5, grid_w=7,
+                                     frames=16, window_frames=2, capacity=20, query_tokens=5, clusters=6)
+        kw = dict(S=5, s_max=9, C=12)
+    else:
+        wl = W.WORKLOADS["7b"].with_(num_layers=1, num_q_heads=28, frames=30)
+        kw = dict(s_max=16)
+        if case == "7b+rope":
+            kw["rope_theta"] = 1e4
+    h.log(f"case: variance-aware allocation {case} {wl.name} {kw}")
+    pair = h.Pair(wl, var_alloc=True, **kw)
+    for f in range(wl.frames):
+        pair.step()
+    pair.check_bank(bitwise=True)
+    pseudo = pair.synthesize()
+    worst, *_ = pair.attend(pair.query(np.random.default_rng(19)), pseudo)
+    counts = [int(v) for v in np.bincount(pseudo[0].slots)]
+    h.log(f"S_k range {min(counts)}..{max(counts)} over {len(counts)} slots, readout err {worst:.2e}")
+    assert max(counts) > min(counts)
+
+
 def test_maximum_frame_and_query_sizes():
     """The largest shapes the library accepts per call: 1024 tokens per frame
     (32x32 grid), 512 query rows per kv head (64 query tokens x 8 query
