@@ -187,9 +187,10 @@ protokv_status protokv_fold(protokv_t h, void* stream);
  * there it holds the float32 centres c_k, p_k instead and protokv_attend
  * forms each row, with the same rounding, as it reads it.  With
  * rope_theta > 0 (Sec. 3.3: the S pseudo-tokens of prototype k share the
- * rotary position tau_k) the rows are always written, and each pseudo-key,
- * rounded to kv_dtype, is rotated at tau_k in float32 (angle reduced in
- * float64) and rounded again. */
+ * rotary position tau_k) each pseudo-key, rounded to kv_dtype, is rotated at
+ * tau_k in float32 (angle reduced in float64) and rounded again: written
+ * that way when the rows are written, turned that way inside protokv_attend
+ * when it forms them (the same values either way). */
 protokv_status protokv_synthesize(protokv_t h, int32_t stream_id, void* stream);
 /* With PROTOKV_FLAG_VAR_ALLOC (appendix "Dynamic Pseudo-Token Allocation")
  * prototype k of each (layer, kv head) is exposed as S_k pseudo-tokens, its

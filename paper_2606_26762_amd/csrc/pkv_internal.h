@@ -19,7 +19,7 @@ constexpr int MAXB = 64;   // streams per launch batch
 constexpr int MAX_SPLITS = 16;  // attention context splits (partials storage)
 constexpr int MAX_RBLOCKS = 2;  // query-row blocks of 256 per kv head
 constexpr int KMAX = 65535;     // prototype slots per unit (slot ids fit 16 bits)
-constexpr int PCW = SMAX + 2;   // words per (slot, K/V) decode record: S tuples, no-residual flag, pad
+constexpr int PCW = SMAX + 2;   // words per (slot, K/V) decode record: S tuples, no-residual flag, tau (key record) / pad
 // The bf16 readout forms pseudo-token rows in LDS from at most PS_SLOTS slots
 // per 64-row tile, which holds for S >= PS_MIN_S (64 consecutive rows span
 // floor(63 / S) + 2 slots at most); below that the synthesis writes the rows.
@@ -94,7 +94,7 @@ struct Workspace {
   uint8_t* pv;
   float* pbias;               // [units][K]
   float* pcen;                // [units][K][2][D]: float32 centres (sum / n) of K and V (synthesis, bf16 path)
-  uint32_t* pcodes;           // [units][K][2][PCW]: decoded top-S code tuples, no-residual flag (word SMAX), pad
+  uint32_t* pcodes;           // [units][K][2][PCW]: decoded top-S code tuples, no-residual flag (word SMAX), tau_k (word SMAX + 1 of the key record, written with the centres)
   float* part_o;              // [units][max_splits][max_rows][D]
   float* part_ml;             // [units][max_splits][max_rows][2]  (max, sum)
   unsigned long long* counters;  // [16]

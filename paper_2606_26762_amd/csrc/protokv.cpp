@@ -574,9 +574,9 @@ protokv_status protokv_synthesize(protokv_t h, int32_t sid, void* stream) {
   // bf16 with S >= PS_MIN_S: the decode also writes the float32 centres and
   // the readout forms the rows from them as it loads them; otherwise the rows
   // are written here
-  // (with rotary positions the rows are written, pseudo-keys rotated at tau_k;
+  // (with rotary positions the readout turns the formed pseudo-keys at tau_k;
   // with the variance-aware allocation each slot's S_k rows are written)
-  const bool rows = h->dm.kv_fp32 != 0 || h->dm.S < PS_MIN_S || h->ws.ring_kr != nullptr || va;
+  const bool rows = h->dm.kv_fp32 != 0 || h->dm.S < PS_MIN_S || va;
   // a slot's residual count is at most the tokens its stream has evicted
   const bool wide = h->st[sid].evicted > 65534u;
   // the allocation decodes every slot's top pseudo_max tuples; slot k keeps its first S_k

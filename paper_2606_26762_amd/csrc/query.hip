@@ -261,6 +261,9 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
     if (kv == 0 && q == 0) {
       const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
       ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
+      // tau_k in the key record's spare word: the readout rotates the
+      // slot's formed pseudo-keys at it
+      out[SMAX + 1] = (uint32_t)m.tau;
     }
   }
   // this path decodes the beam (uniform within the beam's lanes)
@@ -1079,7 +1082,7 @@ __device__ __forceinline__ void lds_barrier() {
 }
 constexpr int AT_NBUF = 4;        // tile buffers: tile t computes while t+1..t+3 load
 constexpr int AT_NTAB = 5;        // row-table entries (written 3 tiles ahead)
-constexpr int AT_PB_MAX = 4096;   // pseudo-token biases staged in LDS up to this capacity
+constexpr int AT_PB_MAX = 2048;   // pseudo-token biases staged in LDS up to this capacity
 
 template <int NW>
 __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims dm, Workspace ws, AttendArgs aa, int rows, int rblocks) {
@@ -1088,6 +1091,9 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
   __shared__ __attribute__((aligned(16))) float s_bias[AT_NTAB][AT_KEYS];           // log2(e) * bias, -inf past the context
   __shared__ const uint8_t* s_rowp[AT_NTAB][2][AT_KEYS];                             // K and V address of each tile row
   __shared__ float s_pb[AT_PB_MAX];                                                  // log2(e) * ln n_k of this unit
+  // rotary positions: (cos, sin) of tau_k * theta^(-2i/D) for the slots of
+  // a formed tile, two tiles' tables (the next one's is written ahead)
+  __shared__ float2 s_rtab[2][PS_SLOTS][D / 2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // blocks of one kv head land on one XCD (dispatch is round-robin over 8)
@@ -1410,13 +1416,38 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
     // tiles.  A thread forms the 16-byte store units q = tid + e * NW * 64 of
     // K (row q % 64, chunk q / 64) and of V (row q / 4 % 64, chunk
     // 4 (q / 256) + q % 4): one K row and one V row per thread, and each
-    // store instruction writes 1 KiB contiguous.
+    // store instruction writes 1 KiB contiguous.  The K chunks of a thread
+    // come in rotate-half pairs (chunk c and c + 8 hold dims i and i + D/2),
+    // so with rotary positions each formed key, rounded to bf16 as written,
+    // is turned at tau_k in registers (float32, the roundings of
+    // k_materialize16) and rounded again.
+    const bool rope = ws.rope_inv != nullptr;  // uniform
     auto form = [&](int t) {
       constexpr int UPT = 1024 / (NW * 64);  // units per thread of K (and of V)
       const int r0 = ps0 + t * AT_KEYS;
       const int kA = divS(r0);
       const uint8_t* sb = s_stage + (t % 3) * PS_STAGE;
       const int pb = t & 1;
+      // the 8 values c + m w of 16-byte unit q (chunk cl) of the row of slot
+      // j, tuple tup, as float
+      auto unit8 = [&](int kv, int q, int cl, int j, uint32_t tup, float m, const float4* cen, float (&x)[8]) {
+        const float4 ca = cen[(2 * cl + 2 * j) & 31], cb = cen[(2 * cl + 1 + 2 * j) & 31];
+        const int g = cl >> 1;
+        const int z = (tup >> (4 * (G - 1 - g))) & 15;
+        const float4* cw = reinterpret_cast<const float4*>(s_cbb) + ((kv * G + g) * CMAX + z) * 4;
+        const int zr = z >> 2;
+        const float4 wa = cw[(2 * (cl & 1) + zr) & 3], wb = cw[(2 * (cl & 1) + 1 + zr) & 3];
+        // w * m + c is exactly c + w (m = 1) or c (m = 0)
+        x[0] = fmaf(wa.x, m, ca.x); x[1] = fmaf(wa.y, m, ca.y); x[2] = fmaf(wa.z, m, ca.z); x[3] = fmaf(wa.w, m, ca.w);
+        x[4] = fmaf(wb.x, m, cb.x); x[5] = fmaf(wb.y, m, cb.y); x[6] = fmaf(wb.z, m, cb.z); x[7] = fmaf(wb.w, m, cb.w);
+      };
+      auto store8 = [&](int kv, int q, const float (&x)[8]) {
+        const bf16x2 o0 = {(__bf16)x[0], (__bf16)x[1]}, o1 = {(__bf16)x[2], (__bf16)x[3]};
+        const bf16x2 o2 = {(__bf16)x[4], (__bf16)x[5]}, o3 = {(__bf16)x[6], (__bf16)x[7]};
+        *reinterpret_cast<uint4*>(s_kv[pb][kv] + q * 16) =
+            make_uint4(__builtin_bit_cast(uint32_t, o0), __builtin_bit_cast(uint32_t, o1),
+                       __builtin_bit_cast(uint32_t, o2), __builtin_bit_cast(uint32_t, o3));
+      };
 #pragma unroll
       for (int kv = 0; kv < 2; ++kv) {
         const int row = kv ? (tid >> 2) & 63 : tid & 63;
@@ -1428,27 +1459,62 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
         const uint32_t tup = rec[s2];
         const float m = rec[SMAX] != 0u ? 0.f : 1.f;  // no residual: the centre alone
         const float4* cen = reinterpret_cast<const float4*>(sb + j * 1024 + kv * 512);
+        if (kv == 0 && rope) {
+          // K units e and e + UPT/2: chunks cl < 8 and cl + 8
 #pragma unroll
-        for (int e = 0; e < UPT; ++e) {
-          const int q = tid + e * NW * 64;
-          const int cl = kv ? (q >> 8) * 4 + (q & 3) : q >> 6;
-          const float4 ca = cen[(2 * cl + 2 * j) & 31], cb = cen[(2 * cl + 1 + 2 * j) & 31];
-          const int g = cl >> 1;
-          const int z = (tup >> (4 * (G - 1 - g))) & 15;
-          const float4* cw = reinterpret_cast<const float4*>(s_cbb) + ((kv * G + g) * CMAX + z) * 4;
-          const int zr = z >> 2;
-          const float4 wa = cw[(2 * (cl & 1) + zr) & 3], wb = cw[(2 * (cl & 1) + 1 + zr) & 3];
-          // w * m + c is exactly c + w (m = 1) or c (m = 0)
-          const bf16x2 o0 = {(__bf16)fmaf(wa.x, m, ca.x), (__bf16)fmaf(wa.y, m, ca.y)};
-          const bf16x2 o1 = {(__bf16)fmaf(wa.z, m, ca.z), (__bf16)fmaf(wa.w, m, ca.w)};
-          const bf16x2 o2 = {(__bf16)fmaf(wb.x, m, cb.x), (__bf16)fmaf(wb.y, m, cb.y)};
-          const bf16x2 o3 = {(__bf16)fmaf(wb.z, m, cb.z), (__bf16)fmaf(wb.w, m, cb.w)};
-          *reinterpret_cast<uint4*>(s_kv[pb][kv] + q * 16) =
-              make_uint4(__builtin_bit_cast(uint32_t, o0), __builtin_bit_cast(uint32_t, o1),
-                         __builtin_bit_cast(uint32_t, o2), __builtin_bit_cast(uint32_t, o3));
+          for (int e = 0; e < UPT / 2; ++e) {
+            const int ql = tid + e * NW * 64, qh = ql + (UPT / 2) * NW * 64;
+            const int cl = ql >> 6;
+            float xl[8], xh[8];
+            unit8(0, ql, cl, j, tup, m, cen, xl);
+            unit8(0, qh, cl + 8, j, tup, m, cen, xh);
+            const float4* cs = reinterpret_cast<const float4*>(&s_rtab[pb][j][8 * cl]);
+#pragma unroll
+            for (int i2 = 0; i2 < 4; ++i2) {
+              const float4 a = cs[i2];  // (cos, sin) of pair indices 8 cl + 2 i2, + 1
+#pragma unroll
+              for (int h = 0; h < 2; ++h) {
+                const int i = 2 * i2 + h;
+                const float c = h ? a.z : a.x, sn = h ? a.w : a.y;
+                const float x1 = (float)(__bf16)xl[i], x2 = (float)(__bf16)xh[i];
+                float lo, hi;
+                rope_pair(x1, x2, c, sn, lo, hi);
+                xl[i] = lo;
+                xh[i] = hi;
+              }
+            }
+            store8(0, ql, xl);
+            store8(0, qh, xh);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < UPT; ++e) {
+            const int q = tid + e * NW * 64;
+            const int cl = kv ? (q >> 8) * 4 + (q & 3) : q >> 6;
+            float x[8];
+            unit8(kv, q, cl, j, tup, m, cen, x);
+            store8(kv, q, x);
+          }
         }
         if (kv == 0 && tid < AT_KEYS)  // row == tid
           s_bias[pb][row] = valid ? (pb_lds ? s_pb[k] : ws.pbias[ubase + k] * LOG2E) : -INFINITY;
+      }
+    };
+    // (cos, sin) table of tile t's slots from tau_k in the staged key
+    // records (stage t % 3), into table t % 2: a thread's pair index i =
+    // tid % 64 is the same for every entry it computes
+    const double rinv = rope ? ws.rope_inv[tid & 63] : 0.0;
+    auto rtab = [&](int t) {
+      const int r0 = ps0 + t * AT_KEYS;
+      const int kA = divS(r0), kB = divS(min(r0 + AT_KEYS, ps1) - 1);
+      const int nk = kB - kA + 1;
+      const uint32_t* recs = reinterpret_cast<const uint32_t*>(s_stage + (t % 3) * PS_STAGE + PS_REC);
+      for (int x = tid; x < nk * 64; x += NW * 64) {
+        const int jj = x >> 6;
+        const double tau = (double)(int32_t)recs[jj * 2 * PCW + SMAX + 1];
+        float c, sn;
+        rope_cs(tau, rinv, c, sn);
+        s_rtab[t & 1][jj][tid & 63] = make_float2(c, sn);
       }
     };
 
@@ -1468,20 +1534,29 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
     stage(0);
     if (npt > 1) stage(1);
     if (npt > 2) stage(2);
-    // codebooks and tile 0's inputs have landed (tiles 1, 2 may be in flight)
-    if (npt > 2) wait_vm<2 * IPW>();
-    else if (npt > 1) wait_vm<IPW>();
+    // codebooks and tile 0's inputs have landed (tiles 1, 2 may be in flight;
+    // with rotary positions tile 1's have landed too, for its table)
+    if (npt > 2 && !rope) wait_vm<2 * IPW>();
+    else if (npt > 1 && !rope) wait_vm<IPW>();
     else wait_vm<0>();
     lds_barrier();
+    if (rope) {
+      rtab(0);
+      if (npt > 1) rtab(1);
+      lds_barrier();
+    }
     form(0);
     for (int t = 0; t < npt; ++t) {
-      // this wave's loads of tile t+1's inputs have landed (tile t+2's may be in flight)
-      if (t + 2 < npt) wait_vm<IPW>();
+      // this wave's loads of tile t+1's inputs have landed (tile t+2's may be
+      // in flight, except with rotary positions: its table is made now)
+      if (t + 2 < npt && !rope) wait_vm<IPW>();
       else wait_vm<0>();
-      // tile t formed everywhere; stage t % 3 (read by form(t)) and formed
-      // buffer (t+1) % 2 (read by compute(t-1)) are free
+      // tile t formed everywhere; stage t % 3 (read by form(t)), formed
+      // buffer (t+1) % 2 (read by compute(t-1)) and table t % 2 (read by
+      // form(t)) are free
       lds_barrier();
       if (t + 3 < npt) stage(t + 3);
+      if (rope && t + 2 < npt) rtab(t + 2);
       // waves w and w + 4 share a SIMD: one forms before computing, the other
       // after, so the forming overlaps the partner's matrix work
       const bool form_first = wave < 4 || !wvalid;  // uniform

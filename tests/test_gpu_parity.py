@@ -120,16 +120,22 @@ def test_variance_aware_allocation(case):
     assert max(counts) > min(counts)
 
 
-def test_maximum_frame_and_query_sizes():
-    """The largest shapes the library accepts per call: 1024 tokens per frame
-    (32x32 grid), 512 query rows per kv head (64 query tokens x 8 query
-    heads, two row blocks in the readout), with K = 4096 (32 768 pseudo
-    tokens at S = 8, 128 slot tiles per screen workgroup).  Four folds seed
-    the bank exactly to capacity, the next two assign at full K; every
-    assignment, the bank (bitwise), the rows and the readout are checked."""
+@pytest.mark.parametrize("cap", [4096, 4160])
+def test_maximum_frame_and_query_sizes(cap):
+    """The largest per-call shapes: 1024 tokens per frame (32x32 grid), 512
+    query rows per kv head (64 query tokens x 8 query heads, two row blocks
+    in the readout), with K = 4096 (32 768 pseudo tokens at S = 8, 128 slot
+    tiles per screen workgroup) and K = 4160 (130 slot tiles, a seeding
+    fold that leaves a partial tile).  Both read the pseudo-token biases from
+    global memory in the readout (K above the 2048 staged in LDS).  The
+    folds seed the bank to capacity, the last two assign at full K; every
+    assignment, the bank (bitwise), the rows and the readout are checked.
+    The library accepts capacities up to 65535; these are the largest the
+    parity tests run."""
     h = H()
+    frames = 1 + (cap + 1023) // 1024 + 2
     wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=1, num_q_heads=8, grid_h=32, grid_w=32,
-                                  frames=7, window_frames=1, capacity=4096, query_tokens=64)
+                                  frames=frames, window_frames=1, capacity=cap, query_tokens=64)
     h.log(f"case: maximum sizes T={wl.tokens_per_frame} K={wl.capacity} rows={wl.query_tokens * 8}")
     pair = h.Pair(wl)
     for f in range(wl.frames):
@@ -249,7 +255,14 @@ def test_rope_readout(wl_name, theta, grid):
         pair.step()
     pseudo = pair.synthesize()
     q = pair.query(np.random.default_rng(17))
+    # bf16 KV: the first readout forms the pseudo-keys in LDS and turns them
+    # at tau_k there; the rows are then written (and checked against the
+    # oracle) and the second readout reads them.  Both are checked against
+    # the oracle; the written keys carry the same roundings as the formed
+    # ones, so the two readouts differ only by their context splits.
     worst, go, _ = pair.attend(q, pseudo)
+    w2, go2, _ = pair.attend(q, pseudo)
+    h.log(f"readout err formed {worst:.2e} written {w2:.2e}, max diff {np.abs(go - go2).max():.2e}")
     # the rotation is visible at this tolerance: the unrotated readout of
     # the same bank is far from the GPU's
     st = pair.oracle[0]
