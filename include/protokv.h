@@ -308,7 +308,7 @@ protokv_status protokv_read_codebooks(protokv_t h, int32_t stream_id, float* dst
  *   3080  float32 mu_x, mu_y      running spatial mean
  *   3088  float32 sig_xx, sig_xy, sig_yy
  *   3100  int32   tau             stream position of the last absorbed token
- *   3104  padding to 3200 */
+ *   3104  padding to 3200 (the library writes bytes 3104..3135 as zeros) */
 #define PROTOKV_ROW_BYTES 3200
 
 /* Copies the bank of `stream_id` (num_layers*num_kv_heads*capacity rows) to

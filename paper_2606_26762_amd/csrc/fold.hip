@@ -112,8 +112,9 @@ __device__ void refresh_cache(const Dims& dm, float2 sk, const RowMeta& m, size_
     c.last_frame = m.tau / dm.T;
     c.active = m.n > 0 ? 1u : 0u;
     c.pad = 0.f;
-    ws.cmeta[slot_index] = c;
+    ws.cmeta[slot_index * CMETA_STRIDE] = c;
   }
+  if (lane == 1) ws.cmeta[slot_index * CMETA_STRIDE + 1] = CacheMeta{};
 }
 
 // As refresh_cache, for a slot owned by a 16-lane group: s = this lane's
@@ -149,8 +150,9 @@ __device__ void refresh_cache16(const Dims& dm, const float (&s)[8], const RowMe
     c.last_frame = m.tau / dm.T;
     c.active = m.n > 0 ? 1u : 0u;
     c.pad = 0.f;
-    ws.cmeta[unit * dm.K + k] = c;
+    ws.cmeta[(unit * dm.K + k) * CMETA_STRIDE] = c;
   }
+  if (il == 1) ws.cmeta[(unit * dm.K + k) * CMETA_STRIDE + 1] = CacheMeta{};
 }
 
 // ---------------------------------------------------------------------------
@@ -590,26 +592,27 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
 
   const int ntiles = (kact + 31) / 32;
   const size_t K32 = (size_t)cap32(dm.K);
-  const uint16_t* ghi = ws.chat_hi + unit * K32 * D + lane * 8;
-  const uint16_t* glo = ws.chat_lo + unit * K32 * D + lane * 8;
-  const CacheMeta* gmeta = ws.cmeta + unit * dm.K;
+  const uint16_t* ghi = ws.chat_hi + unit * K32 * D + col * 32 + half * 8;
+  const uint16_t* glo = ws.chat_lo + unit * K32 * D + col * 32 + half * 8;
+  const CacheMeta* gmeta = ws.cmeta + unit * dm.K * CMETA_STRIDE;
 
-  // operands of slot tile t: k-step kk of lane l is 16 contiguous bytes at
-  // ((t * 8 + kk) * 64 + l) * 8 elements; half-0 lanes also fetch their row's meta
+  // operands of slot tile t: k-step kk of lane (col, half) is the 16 bytes
+  // of slot 32 t + col at dims 16 kk + 8 half (chat_offset); half-0 lanes
+  // also fetch their row's meta
   u16x8 ah[8], al[8];
   float4 ma = make_float4(0.f, 0.f, 0.f, 0.f);
   float2 mb = make_float2(0.f, INFINITY);
   auto load_tile = [&](int t) {
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
-      ah[kk] = *reinterpret_cast<const u16x8*>(ghi + ((size_t)t * 8 + kk) * 512);
-      al[kk] = *reinterpret_cast<const u16x8*>(glo + ((size_t)t * 8 + kk) * 512);
+      ah[kk] = *reinterpret_cast<const u16x8*>(ghi + (size_t)t * 32 * D + (kk >> 1) * 1024 + (kk & 1) * 16);
+      al[kk] = *reinterpret_cast<const u16x8*>(glo + (size_t)t * 32 * D + (kk >> 1) * 1024 + (kk & 1) * 16);
     }
     const int krow = t * 32 + col;
     ma = make_float4(0.f, 0.f, 0.f, 0.f);
     mb = make_float2(0.f, INFINITY);
     if (half == 0 && krow < kact) {
-      const CacheMeta cm = gmeta[krow];
+      const CacheMeta cm = gmeta[(size_t)krow * CMETA_STRIDE];
       ma = make_float4(cm.mu_x, cm.mu_y, cm.qa, 2.0f * cm.qb);
       mb = make_float2(cm.qc, (t_frame - cm.last_frame) > dm.t_idle ? lidle : 0.f);
     }
@@ -1226,7 +1229,9 @@ __global__ __launch_bounds__(256, EMA ? 2 : (NP > 2 ? 3 : 4)) void k_aggregate(D
     st8f(row + ROW_SUMV + il * 32, sv);
     st8f(row + ROW_SQK + il * 32, qk);
     st8f(row + ROW_SQV + il * 32, qv);
+    // the meta and the padding after it: one whole 64-byte sector
     if (il == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
+    if (il == 1) *reinterpret_cast<RowMeta*>(row + ROW_META + sizeof(RowMeta)) = RowMeta{};
     refresh_cache16(dm, sk, m, unit, k, ws, il);
     // per-slot count of folds that touched it (owned by this lane group: no atomics)
     if (il == 0) ws.touched[si] += 1u;
@@ -1304,8 +1309,206 @@ __global__ __launch_bounds__(256, EMA ? 2 : (NP > 2 ? 3 : 4)) void k_aggregate(D
   }
 }
 
+// ---------------------------------------------------------------------------
+// Aggregation over the touched slots only (running means, K <= AGC_KMAX).
+// A fold touches a fraction of the K slots (about 100 of 512 on a 7B-shaped
+// stream), so workgroups over fixed ranges of slots spend most of their lane
+// groups on slots without tokens.  Here each of the P workgroups of a unit
+// buckets the unit's evicted tokens by slot in LDS (per-slot counts by LDS
+// atomics, one exclusive scan that also numbers the touched slots, a scatter
+// and a stable re-ranking, so every slot's tokens are in eviction order),
+// then its 16 lane groups take touched slots gi + 16 (p + P r): the row's
+// four sums go to registers (lane il: dims [8 il, 8 il + 8)), the slot's
+// tokens are absorbed in order TOK_BATCH at a time with their loads in
+// flight, the row and the slot's screening copy are written back, and the
+// next touched slot's row is loaded before the current one's stores.  The
+// arithmetic is k_aggregate's: the same float32 operation sequence per slot.
+// ---------------------------------------------------------------------------
+constexpr int AGC_KMAX = 4096;  // slot counters held in LDS
+
+template <int FP32>
+__global__ __launch_bounds__(256) void k_aggregate_c(Dims dm, Workspace ws, FoldBatch fb, int wg_per_unit) {
+  // per slot: token count | touched flag << 16, then the exclusive prefix of
+  // both (list offset | touched index << 16); entry K holds the totals
+  __shared__ uint32_t s_cnt[AGC_KMAX + 1];
+  __shared__ uint16_t s_asg[TMAX];     // slot of token j
+  __shared__ uint16_t s_pos[TMAX];     // arrival index of token j among its slot's tokens
+  __shared__ uint16_t s_list[TMAX];    // tokens grouped by slot, arrival order
+  __shared__ uint16_t s_tok[TMAX];     // the same groups in eviction order
+  __shared__ uint16_t s_tslot[TMAX];   // touched slots, ascending
+  __shared__ uint16_t s_tstart[TMAX + 1];
+  __shared__ uint32_t s_wsum[4];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nblk = (int)gridDim.x, per = nblk >> 3, bid = (int)blockIdx.x;
+  const int lb = bid < per * 8 ? (bid & 7) * per + (bid >> 3) : bid;
+  const int wgi = lb % wg_per_unit;
+  const int bu = lb / wg_per_unit;
+  const int b = bu / dm.units, u = bu % dm.units;
+  const int N = dm.T, K = dm.K;
+  const int nseed = fb.nseed[b];
+  if (nseed >= N) return;  // uniform
+  const size_t unit = (size_t)fb.sid[b] * dm.units + u;
+  const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0 && !fb.warm[b];  // warm-up folds count no codes
+  const size_t fbase = ((unit * (dm.W + 1) + fb.slot[b]) * N) * (size_t)D;
+
+  // 1. counts per slot
+  for (int k = tid; k <= K; k += 256) s_cnt[k] = 0u;
+  __syncthreads();
+  for (int j = nseed + tid; j < N; j += 256) {
+    const int k = ws.assign[unit * N + j];
+    s_asg[j] = (uint16_t)k;
+    s_pos[j] = (uint16_t)atomicAdd(&s_cnt[k], 1u);
+  }
+  __syncthreads();
+  // 2. exclusive scan of (count | touched << 16): thread tid owns slots
+  // [tid E, tid E + E); counts stay below 2^16, so the two fields add apart
+  const int E = (K + 255) >> 8;
+  const int ka = min(K, tid * E), kb = min(K, ka + E);
+  uint32_t own = 0u;
+  for (int k = ka; k < kb; ++k) {
+    const uint32_t c = s_cnt[k];
+    own += c + (c ? 0x10000u : 0u);
+  }
+  uint32_t incl = own;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) s_wsum[wave] = incl;
+  __syncthreads();
+  uint32_t base = 0u;
+  for (int w = 0; w < wave; ++w) base += s_wsum[w];
+  uint32_t run = base + incl - own;
+  for (int k = ka; k < kb; ++k) {
+    const uint32_t c = s_cnt[k];
+    s_cnt[k] = run;
+    if (c) {
+      s_tslot[run >> 16] = (uint16_t)k;
+      s_tstart[run >> 16] = (uint16_t)(run & 0xFFFFu);
+    }
+    run += c + (c ? 0x10000u : 0u);
+  }
+  const uint32_t total = s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
+  const int ntouched = (int)(total >> 16), ntok = (int)(total & 0xFFFFu);
+  if (tid == 0) {
+    s_cnt[K] = total;
+    s_tstart[ntouched] = (uint16_t)ntok;
+  }
+  __syncthreads();
+  // 3. scatter (arrival order), then each token's rank among its slot's
+  // tokens by index: the eviction order
+  for (int j = nseed + tid; j < N; j += 256) s_list[(s_cnt[s_asg[j]] & 0xFFFFu) + s_pos[j]] = (uint16_t)j;
+  __syncthreads();
+  for (int j = nseed + tid; j < N; j += 256) {
+    const int k = s_asg[j];
+    const int a = (int)(s_cnt[k] & 0xFFFFu), e = (int)(s_cnt[k + 1] & 0xFFFFu);
+    int rank = 0;
+    for (int m = a; m < e; ++m) rank += s_list[m] < j ? 1 : 0;
+    s_tok[a + rank] = (uint16_t)j;
+  }
+  __syncthreads();
+
+  // 4. the lane groups' touched slots
+  const int gi = tid >> 4, il = tid & 15;
+  const int step = 16 * wg_per_unit;
+  int ti = gi + 16 * wgi;
+  if (ti >= ntouched) return;  // uniform per lane group; no barrier below
+  const float eta = dm.eta, keep = 1.0f - dm.eta;
+  float sk[8], sv[8], qk[8], qv[8];
+  float nk[8], nv[8], nqk[8], nqv[8];
+  RowMeta m, nm;
+  auto load_row = [&](int k, float (&a)[8], float (&b2)[8], float (&c)[8], float (&d)[8], RowMeta& mm) {
+    const uint8_t* row = ws.bank + (unit * K + k) * ROW;
+    ld8f(row + ROW_SUMK + il * 32, a);
+    ld8f(row + ROW_SUMV + il * 32, b2);
+    ld8f(row + ROW_SQK + il * 32, c);
+    ld8f(row + ROW_SQV + il * 32, d);
+    mm = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  };
+  load_row(s_tslot[ti], sk, sv, qk, qv, m);
+  for (; ti < ntouched; ti += step) {
+    const int k = s_tslot[ti];
+    const int t0 = s_tstart[ti], t1 = s_tstart[ti + 1];
+    const size_t si = unit * K + k;
+    uint8_t* row = ws.bank + si * ROW;
+    const int tn = ti + step;
+    for (int tb = t0; tb < t1; tb += TOK_BATCH) {
+      int jb[TOK_BATCH];
+      Raw8<FP32> kb2[TOK_BATCH], vb2[TOK_BATCH];
+#pragma unroll
+      for (int e = 0; e < TOK_BATCH; ++e) {
+        jb[e] = s_tok[min(tb + e, t1 - 1)];
+        load8<FP32>(ws.ring_k, fbase + (size_t)jb[e] * D + 8 * il, kb2[e]);
+        load8<FP32>(ws.ring_v, fbase + (size_t)jb[e] * D + 8 * il, vb2[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < TOK_BATCH; ++e) {
+        if (tb + e < t1) {
+          const int jj = jb[e];
+#pragma unroll
+          for (int d = 0; d < 8; ++d) {
+            const float xk = raw_at<FP32>(kb2[e], d), xv = raw_at<FP32>(vb2[e], d);
+            sk[d] = sk[d] + xk;
+            sv[d] = sv[d] + xv;
+            qk[d] = qk[d] + xk * xk;
+            qv[d] = qv[d] + xv * xv;
+          }
+          if (pq) m.n_res += 1;
+          float sx, sy;
+          token_xy(jj, dm.grid_w, dm.grid_h, sx, sy);
+          const float mx = keep * m.mu_x + eta * sx;
+          const float my = keep * m.mu_y + eta * sy;
+          m.mu_x = mx;
+          m.mu_y = my;
+          const float ddx = sx - mx, ddy = sy - my;
+          m.sxx = keep * m.sxx + eta * (ddx * ddx);
+          m.sxy = keep * m.sxy + eta * (ddx * ddy);
+          m.syy = keep * m.syy + eta * (ddy * ddy);
+          m.tau = fb.fe[b] * N + jj;
+          m.n += 1;
+        }
+      }
+    }
+    // the next touched slot's row in flight before this one's stores
+    if (tn < ntouched) load_row(s_tslot[tn], nk, nv, nqk, nqv, nm);
+    st8f(row + ROW_SUMK + il * 32, sk);
+    st8f(row + ROW_SUMV + il * 32, sv);
+    st8f(row + ROW_SQK + il * 32, qk);
+    st8f(row + ROW_SQV + il * 32, qv);
+    // the meta and the padding after it: one whole 64-byte sector
+    if (il == 0) *reinterpret_cast<RowMeta*>(row + ROW_META) = m;
+    if (il == 1) *reinterpret_cast<RowMeta*>(row + ROW_META + sizeof(RowMeta)) = RowMeta{};
+    refresh_cache16(dm, sk, m, unit, k, ws, il);
+    if (il == 0) ws.touched[si] += 1u;
+    if (tn < ntouched) {
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        sk[d] = nk[d];
+        sv[d] = nv[d];
+        qk[d] = nqk[d];
+        qv[d] = nqv[d];
+      }
+      m = nm;
+    }
+  }
+}
+
 hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
   const bool ema = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) != 0;
+  if (!ema && dm.K <= AGC_KMAX) {
+    // touched slots only: P workgroups per unit, enough to put about 2048
+    // workgroups in flight, at most one per 16 slots a fold can touch
+    const int units = fb.n * dm.units;
+    const int pmax = (std::min(dm.T, dm.K) + 15) / 16;
+    const int P = std::max(1, std::min(pmax, (2048 + units - 1) / units));
+    dim3 grid(units * P);
+    using KFn = void (*)(Dims, Workspace, FoldBatch, int);
+    const KFn fn = dm.kv_fp32 ? k_aggregate_c<1> : k_aggregate_c<0>;
+    hipLaunchKernelGGL(fn, grid, dim3(256), 0, st, dm, ws, fb, P);
+    return hipGetLastError();
+  }
   // running means: AGG_NP slots per lane group (16 AGG_NP per workgroup);
   // EMA centres code their residuals in the workgroup: two per group
   constexpr int NPM = AGG_NP;

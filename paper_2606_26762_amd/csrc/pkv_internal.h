@@ -68,24 +68,29 @@ struct Dims {
   int max_splits;  // attention context splits (partials storage)
 };
 
-// Screening copy of the unit centres, stored in the operand order of
-// v_mfma_f32_32x32x16_bf16 so that one wave reads 1 KiB contiguous per
-// k-step: slot k of a unit sits in slot tile k / 32 at column k % 32; element
-// d in k-step d / 16, lane (d / 8 % 2) * 32 + k % 32, position d % 8.
-// Capacity is padded to K32 = 32 * ceil(K / 32) slots per unit.
+// Screening copy of the unit centres in 64-byte pieces: for slot tile
+// t = k / 32 and dim chunk c = d / 32, the 32 bf16 components of slot k
+// sit together, [t][c][k % 32][d % 32].  The aggregation rewrites a touched
+// slot in whole 64-byte sectors (partial sectors cost a read-modify-write
+// in memory), and the screen's operand load of one k-step (32 slots x 16
+// dims) touches 16 cache lines.  Capacity is padded to K32 = 32 * ceil(K /
+// 32) slots per unit.
 __host__ __device__ inline int cap32(int K) { return (K + 31) & ~31; }
 __host__ __device__ inline size_t chat_offset(int k, int d) {
-  return ((((size_t)(k >> 5) * 8 + (d >> 4)) * 64 + ((d >> 3) & 1) * 32 + (k & 31)) * 8) + (d & 7);
+  return (((size_t)(k >> 5) * 4 + (d >> 5)) * 32 + (k & 31)) * 32 + (d & 31);
 }
+// Slot k's CacheMeta sits at cmeta[k * CMETA_STRIDE] (the second half of its
+// 64 bytes is zero), so its rewrite is a whole sector too.
+constexpr int CMETA_STRIDE = 2;
 
 // Device pointers into the caller's workspace.
 struct Workspace {
   uint8_t* ring_k;            // [streams][units][W+1][T][D] kv dtype
   uint8_t* ring_v;
   uint8_t* bank;              // [streams][units][K] rows of ROW bytes
-  uint16_t* chat_hi;          // [streams][units][K32 / 32][8][64][8] bf16 bits (chat_offset)
+  uint16_t* chat_hi;          // [streams][units][K32 / 32][4][32][32] bf16 bits (chat_offset)
   uint16_t* chat_lo;
-  CacheMeta* cmeta;           // [streams][units][K]
+  CacheMeta* cmeta;           // [streams][units][K][CMETA_STRIDE] (entry 0 used)
   int32_t* assign;            // [streams][units][T]
   float* codebooks;           // [streams][units][2][G][CMAX][DP]
   float* cbhn;                // [streams][units][2][G][CMAX]: |C|^2 / 2 (+inf for codewords >= C)

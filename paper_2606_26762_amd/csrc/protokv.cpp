@@ -58,7 +58,7 @@ Layout make_layout(const protokv_config& c) {
   const size_t K32 = (size_t)cap32(c.capacity);
   ly.chat_hi = take(U * K32 * D * 2);
   ly.chat_lo = take(U * K32 * D * 2);
-  ly.cmeta = take(U * K * sizeof(CacheMeta));
+  ly.cmeta = take(U * K * CMETA_STRIDE * sizeof(CacheMeta));
   ly.assign = take(U * T * 4);
   ly.codebooks = take(U * 2 * G * CMAX * DP * 4);
   ly.cbhn = take(U * 2 * G * CMAX * 4);
