@@ -223,60 +223,41 @@ __device__ __forceinline__ uint32_t sel32(bool t, uint32_t a, uint32_t b) {
   return (a & m) | (b & ~m);
 }
 
-template <int SM, int LPB>
-__global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid, int n_active, int centres) {
-  static_assert(LPB == 2 || LPB == 4, "lanes per beam");
-  constexpr int E = SM / LPB;        // prefixes per lane
-  constexpr int BPW = 64 / LPB;      // beams per wave
-  constexpr int KPL = CMAX / LPB;    // codewords per lane
-  __shared__ uint32_t s_rank[4][BPW][CMAX];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int q = lane & (LPB - 1), bq = lane / LPB;
-  const int beam = (blockIdx.x * 4 + wave) * BPW + bq;  // ((unit * n_active + slot) * 2 + K/V)
-  const bool bvalid = beam < dm.units * n_active * 2;
-  const int kv = beam & 1, up = bvalid ? beam >> 1 : 0;
-  const int u = up / n_active, p = up % n_active;
-  const size_t unit = (size_t)sid * dm.units + u;
-  const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
-  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
-  uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * PCW;
-  const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
-  const int S = dm.S, C = dm.C;
-  const bool nores = !pq || m.n_res == 0;
-  if (bvalid && q == 0 && nores) out[SMAX] = 1u;
-  if (bvalid && centres) {
-    // lane q takes float4s q, q + LPB, ...
-    // centre = sum / n (EMA centres: the stored centre, divided by 1)
-    const float nf = (float)m.n, cd = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) ? 1.f : nf;
-    const float4* sums = reinterpret_cast<const float4*>(row + (kv ? ROW_SUMV : ROW_SUMK));
-    float4* cen = reinterpret_cast<float4*>(ws.pcen + (((size_t)u * dm.K + p) * 2 + kv) * D);
-    // every load issued before the first store (the stores may alias them
-    // as far as the compiler knows)
-    float4 v[D / 4 / LPB];
-#pragma unroll
-    for (int i = 0; i < D / 4 / LPB; ++i) v[i] = sums[q + LPB * i];
-#pragma unroll
-    for (int i = 0; i < D / 4 / LPB; ++i)
-      cen[q + LPB * i] = make_float4(v[i].x / cd, v[i].y / cd, v[i].z / cd, v[i].w / cd);
-    if (kv == 0 && q == 0) {
-      const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
-      ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
-      // tau_k in the key record's spare word: the readout rotates the
-      // slot's formed pseudo-keys at it
-      out[SMAX + 1] = (uint32_t)m.tau;
-    }
-  }
-  // this path decodes the beam (uniform within the beam's lanes)
-  const bool mine = bvalid && !nores && m.n_res <= 65534u && S <= SM;
-  const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
-  const int R = S < C ? S : C;
+// Product helpers of the decode merge: 64-bit or 128-bit unsigned products.
+template <typename P> __device__ __forceinline__ P pt_from(uint32_t x);
+template <> __device__ __forceinline__ uint64_t pt_from<uint64_t>(uint32_t x) { return x; }
+template <> __device__ __forceinline__ U128 pt_from<U128>(uint32_t x) { return U128{x, 0ull}; }
+__device__ __forceinline__ uint64_t pt_mul(uint64_t a, uint32_t f) { return a * f; }
+__device__ __forceinline__ U128 pt_mul(const U128& a, uint32_t f) { return mul_u128_u32(a, f); }
+__device__ __forceinline__ bool pt_before(uint64_t pa, uint32_t ca, uint64_t pb, uint32_t cb) {
+  return (pa > pb) | ((pa == pb) & (ca < cb));
+}
+__device__ __forceinline__ bool pt_before(const U128& pa, uint32_t ca, const U128& pb, uint32_t cb) {
+  return before128b(pa, ca, pb, cb);
+}
+__device__ __forceinline__ uint64_t pt_sel(bool t, uint64_t a, uint64_t b) { return sel64(t, a, b); }
+__device__ __forceinline__ U128 pt_sel(bool t, const U128& a, const U128& b) {
+  return U128{sel64(t, a.lo, b.lo), sel64(t, a.hi, b.hi)};
+}
+template <int CTRL> __device__ __forceinline__ uint64_t pt_perm(uint64_t x) { return qperm64<CTRL>(x); }
+template <int CTRL> __device__ __forceinline__ U128 pt_perm(const U128& x) {
+  return U128{qperm64<CTRL>(x.lo), qperm64<CTRL>(x.hi)};
+}
 
-  U128 pp[E];
+// The beam merge of k_decode4 for one product type P (uint64_t when every
+// product of the wave's beams fits in 64 bits, else U128): products of the
+// factors H+1 compare exactly either way.
+template <int SM, int LPB, typename P>
+__device__ __forceinline__ void decode_beam(uint32_t (*s_rank)[CMAX], const uint32_t* hist, bool mine, int S,
+                                            int C, int q, int bq, uint32_t* out) {
+  constexpr int E = SM / LPB;        // prefixes per lane
+  constexpr int KPL = CMAX / LPB;    // codewords per lane
+  const int R = S < C ? S : C;
+  P pp[E];
   uint32_t pc[E];
 #pragma unroll
   for (int j = 0; j < E; ++j) {
-    pp[j].lo = (q == 0 && j == 0) ? 1u : 0u;
-    pp[j].hi = 0;
+    pp[j] = pt_from<P>((q == 0 && j == 0) ? 1u : 0u);
     pc[j] = 0;
   }
   int nb = 1;
@@ -341,7 +322,7 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
           if ((i ^ j) > i) cx(i, i ^ j, true);
 #pragma unroll
       for (int i = 0; i < KPL; ++i)
-        if (key[i] != 0u && q * KPL + i < R) s_rank[wave][bq][q * KPL + i] = key[i];
+        if (key[i] != 0u && q * KPL + i < R) s_rank[bq][q * KPL + i] = key[i];
     } else {
       int rk[KPL];
 #pragma unroll
@@ -357,7 +338,7 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
       }
 #pragma unroll
       for (int i = 0; i < KPL; ++i)
-        if (key[i] != 0u && rk[i] < R) s_rank[wave][bq][rk[i]] = key[i];
+        if (key[i] != 0u && rk[i] < R) s_rank[bq][rk[i]] = key[i];
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -368,8 +349,8 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
 #pragma unroll
       for (int j = 0; j < E; ++j) {
         const int e = q + LPB * j;
-        const uint32_t ke = s_rank[wave][bq][e < R ? e : 0];
-        pp[j] = e < R ? U128{((ke - 1u) >> 4) + 1u, 0ull} : U128{0ull, 0ull};
+        const uint32_t ke = s_rank[bq][e < R ? e : 0];
+        pp[j] = pt_from<P>(e < R ? ((ke - 1u) >> 4) + 1u : 0u);
         pc[j] = e < R ? (15u - ((ke - 1u) & 15u)) << shift : 0u;
       }
       nb = S < R ? S : R;
@@ -378,35 +359,34 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       continue;
     }
-    const uint32_t k0 = s_rank[wave][bq][0];
+    const uint32_t k0 = s_rank[bq][0];
     // row heads: prefix e = q + LPB j times rank ptr[j]
     int ptr[E];
-    U128 hp[E];
+    P hp[E];
     uint32_t hc[E];
 #pragma unroll
     for (int j = 0; j < E; ++j) {
       ptr[j] = 0;
       const bool ok = q + LPB * j < nb;
-      hp[j] = ok ? mul_u128_u32(pp[j], ((k0 - 1u) >> 4) + 1u) : U128{0, 0};
+      hp[j] = ok ? pt_mul(pp[j], ((k0 - 1u) >> 4) + 1u) : pt_from<P>(0u);
       hc[j] = ok ? (pc[j] | ((15u - ((k0 - 1u) & 15u)) << shift)) : 0xFFFFFFFFu;
     }
     const int nout = S < nb * R ? S : nb * R;
-    U128 np[E];
+    P np[E];
     uint32_t nc[E];
 #pragma unroll
-    for (int j = 0; j < E; ++j) { np[j] = U128{0, 0}; nc[j] = 0; }
+    for (int j = 0; j < E; ++j) { np[j] = pt_from<P>(0u); nc[j] = 0; }
 #pragma unroll
     for (int o = 0; o < SM; ++o) {
       if (o < nout) {
         // best head of this lane (product 0 = exhausted row)
-        U128 bv = hp[0];
+        P bv = hp[0];
         uint32_t bc = hc[0];
         int bj = 0;
 #pragma unroll
         for (int j = 1; j < E; ++j) {
-          const bool t = before128b(hp[j], hc[j], bv, bc);
-          bv.lo = sel64(t, hp[j].lo, bv.lo);
-          bv.hi = sel64(t, hp[j].hi, bv.hi);
+          const bool t = pt_before(hp[j], hc[j], bv, bc);
+          bv = pt_sel(t, hp[j], bv);
           bc = sel32(t, hc[j], bc);
           bj = t ? j : bj;
         }
@@ -414,54 +394,48 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
         // best of the beam's lanes
 #pragma unroll
         for (int x = 0; x < (LPB == 4 ? 2 : 1); ++x) {
-          U128 ov;
+          P ov;
           uint32_t oc, ow;
           if (x == 0) {
-            ov.lo = qperm64<QP_XOR1>(bv.lo); ov.hi = qperm64<QP_XOR1>(bv.hi);
+            ov = pt_perm<QP_XOR1>(bv);
             oc = qperm<QP_XOR1>(bc); ow = qperm<QP_XOR1>(who);
           } else {
-            ov.lo = qperm64<QP_XOR2>(bv.lo); ov.hi = qperm64<QP_XOR2>(bv.hi);
+            ov = pt_perm<QP_XOR2>(bv);
             oc = qperm<QP_XOR2>(bc); ow = qperm<QP_XOR2>(who);
           }
-          const bool t = before128b(ov, oc, bv, bc);
-          bv.lo = sel64(t, ov.lo, bv.lo);
-          bv.hi = sel64(t, ov.hi, bv.hi);
+          const bool t = pt_before(ov, oc, bv, bc);
+          bv = pt_sel(t, ov, bv);
           bc = sel32(t, oc, bc);
           who = sel32(t, ow, who);
         }
         {
           const bool rec = (o % LPB) == q;
-          np[o / LPB].lo = sel64(rec, bv.lo, np[o / LPB].lo);
-          np[o / LPB].hi = sel64(rec, bv.hi, np[o / LPB].hi);
+          np[o / LPB] = pt_sel(rec, bv, np[o / LPB]);
           nc[o / LPB] = sel32(rec, bc, nc[o / LPB]);
         }
         // the winning row moves to its next rank: one product, then selects
         const bool iwin = (int)(who / E) == q;
         const int j = (int)(who % E);
         int pj = ptr[0];
-        U128 base = pp[0];
+        P base = pp[0];
         uint32_t bcode = pc[0];
 #pragma unroll
         for (int jj = 1; jj < E; ++jj) {
           const bool t = jj == j;
           pj = t ? ptr[jj] : pj;
-          base.lo = sel64(t, pp[jj].lo, base.lo);
-          base.hi = sel64(t, pp[jj].hi, base.hi);
+          base = pt_sel(t, pp[jj], base);
           bcode = sel32(t, pc[jj], bcode);
         }
         pj += 1;
         const bool more = pj < R;
-        const uint32_t kk = s_rank[wave][bq][more ? pj : 0];
-        U128 nh = mul_u128_u32(base, ((kk - 1u) >> 4) + 1u);
-        nh.lo = more ? nh.lo : 0ull;
-        nh.hi = more ? nh.hi : 0ull;
+        const uint32_t kk = s_rank[bq][more ? pj : 0];
+        const P nh = pt_sel(more, pt_mul(base, ((kk - 1u) >> 4) + 1u), pt_from<P>(0u));
         const uint32_t ncode = more ? (bcode | ((15u - ((kk - 1u) & 15u)) << shift)) : 0xFFFFFFFFu;
 #pragma unroll
         for (int jj = 0; jj < E; ++jj) {
           const bool t = iwin && jj == j;
           ptr[jj] = t ? pj : ptr[jj];
-          hp[jj].lo = sel64(t, nh.lo, hp[jj].lo);
-          hp[jj].hi = sel64(t, nh.hi, hp[jj].hi);
+          hp[jj] = pt_sel(t, nh, hp[jj]);
           hc[jj] = sel32(t, ncode, hc[jj]);
         }
       }
@@ -481,6 +455,79 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
     }
     if (q == 0) out[SMAX] = 0u;
   }
+}
+
+template <int SM, int LPB>
+__global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid, int n_active, int centres) {
+  static_assert(LPB == 2 || LPB == 4, "lanes per beam");
+  constexpr int E = SM / LPB;        // prefixes per lane
+  constexpr int BPW = 64 / LPB;      // beams per wave
+  constexpr int KPL = CMAX / LPB;    // codewords per lane
+  __shared__ uint32_t s_rank[4][BPW][CMAX];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane & (LPB - 1), bq = lane / LPB;
+  const int beam = (blockIdx.x * 4 + wave) * BPW + bq;  // ((unit * n_active + slot) * 2 + K/V)
+  const bool bvalid = beam < dm.units * n_active * 2;
+  const int kv = beam & 1, up = bvalid ? beam >> 1 : 0;
+  const int u = up / n_active, p = up % n_active;
+  const size_t unit = (size_t)sid * dm.units + u;
+  const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
+  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * PCW;
+  const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
+  const int S = dm.S, C = dm.C;
+  const bool nores = !pq || m.n_res == 0;
+  if (bvalid && q == 0 && nores) out[SMAX] = 1u;
+  if (bvalid && centres) {
+    // lane q takes float4s q, q + LPB, ...
+    // centre = sum / n (EMA centres: the stored centre, divided by 1)
+    const float nf = (float)m.n, cd = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) ? 1.f : nf;
+    const float4* sums = reinterpret_cast<const float4*>(row + (kv ? ROW_SUMV : ROW_SUMK));
+    float4* cen = reinterpret_cast<float4*>(ws.pcen + (((size_t)u * dm.K + p) * 2 + kv) * D);
+    // every load issued before the first store (the stores may alias them
+    // as far as the compiler knows)
+    float4 v[D / 4 / LPB];
+#pragma unroll
+    for (int i = 0; i < D / 4 / LPB; ++i) v[i] = sums[q + LPB * i];
+#pragma unroll
+    for (int i = 0; i < D / 4 / LPB; ++i)
+      cen[q + LPB * i] = make_float4(v[i].x / cd, v[i].y / cd, v[i].z / cd, v[i].w / cd);
+    if (kv == 0 && q == 0) {
+      const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
+      ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
+      // tau_k in the key record's spare word: the readout rotates the
+      // slot's formed pseudo-keys at it
+      out[SMAX + 1] = (uint32_t)m.tau;
+    }
+  }
+  // this path decodes the beam (uniform within the beam's lanes)
+  const bool mine = bvalid && !nores && m.n_res <= 65534u && S <= SM;
+  const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
+  // every product the merge forms is at most prod_g max_c (H[g][c] + 1) (the
+  // beam's top tuple); when that fits in 64 bits for all of the wave's
+  // beams the merge runs on 64-bit products
+  bool fits = true;
+  if (mine) {
+    uint64_t bound = 1;
+    bool ovf = false;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      uint32_t mx = 0;
+#pragma unroll
+      for (int v4 = 0; v4 < KPL / 4; ++v4) {
+        const uint4 h4 = reinterpret_cast<const uint4*>(hist + g * CMAX)[q * (KPL / 4) + v4];
+        mx = max(mx, max(max(h4.x, h4.y), max(h4.z, h4.w)));
+      }
+      mx = max(mx, qperm<QP_XOR1>(mx));
+      if (LPB == 4) mx = max(mx, qperm<QP_XOR2>(mx));
+      ovf |= __builtin_mul_overflow(bound, (uint64_t)mx + 1u, &bound);
+    }
+    fits = !ovf;
+  }
+  if (__all(fits))
+    decode_beam<SM, LPB, uint64_t>(s_rank[wave], hist, mine, S, C, q, bq, out);
+  else
+    decode_beam<SM, LPB, U128>(s_rank[wave], hist, mine, S, C, q, bq, out);
 }
 
 // Decoding, wide path (prototypes with more than 65534 residuals, whose
