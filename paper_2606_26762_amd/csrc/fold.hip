@@ -412,8 +412,8 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
       v1 = fmaxf(v1, v);
       i1 = (cw & mk) | (i1 & ~mk);
     }
-    const float o1 = __shfl_xor(v1, 32, 64), o2 = __shfl_xor(v2, 32, 64);
-    const int oi = __shfl_xor(i1, 32, 64);
+    const float o1 = xor32(v1), o2 = xor32(v2);
+    const int oi = xor32(i1);
     const bool take = o1 > v1 || (o1 == v1 && oi < i1);
     bst2[sub] = fmaxf(fminf(v1, o1), fmaxf(v2, o2));
     bst1[sub] = fmaxf(v1, o1);
@@ -423,7 +423,7 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
   const int g = half ? g1 : g0;
   const float v1 = half ? bst1[1] : bst1[0], v2 = half ? bst2[1] : bst2[0];
   float rn2 = half ? n1 : n0;
-  rn2 += __shfl_xor(half ? n0 : n1, 32, 64);  // the partner's half of subspace g
+  rn2 += xor32(half ? n0 : n1);  // the partner's half of subspace g
   // |score - exact| <= F for every codeword: the hi + lo split of both
   // operands leaves <= 3 * 2^-16 |r_u| |C_u| per product (the dropped
   // lo * lo and the two split remainders), summed <= 4.6e-5 |r| |C|; the
@@ -433,7 +433,7 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
   // D <= |r|^2 - 2 score of the runner-up (dlead).  Each term is taken with
   // margin.
   float cn2 = half ? cn2h1 : cn2h0;
-  cn2 += __shfl_xor(half ? cn2h0 : cn2h1, 32, 64);
+  cn2 += xor32(half ? cn2h0 : cn2h1);
   const float rn = sqrtf(rn2) * 1.0001f, cm = cmx[g];
   const float dlead = fmaxf(rn * rn - 2.0f * v2, 0.f) + 1e-30f;
   // ... and <= 3.1 u |c| |C| from the centre c' (taken as 2e-7 |c'| |C|)
@@ -726,12 +726,12 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     Top3 o;
-    o.c1 = __shfl_xor(top[h].c1, 32, 64);
-    o.c2 = __shfl_xor(top[h].c2, 32, 64);
-    o.c3 = __shfl_xor(top[h].c3, 32, 64);
-    o.i1 = __shfl_xor(top[h].i1, 32, 64);
-    o.i2 = __shfl_xor(top[h].i2, 32, 64);
-    o.emax = __shfl_xor(top[h].emax, 32, 64);
+    o.c1 = xor32(top[h].c1);
+    o.c2 = xor32(top[h].c2);
+    o.c3 = xor32(top[h].c3);
+    o.i1 = xor32(top[h].i1);
+    o.i2 = xor32(top[h].i2);
+    o.emax = xor32(top[h].emax);
     top3_merge(top[h], o);
     if (half == 0) s_top[wave][h * 32 + col] = top[h];
   }

@@ -183,6 +183,17 @@ __device__ __forceinline__ void lds_dma16(const void* g, void* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(m0) : "memory");
 }
+// The value of lane l ^ 32 (the other half of the wave) without an LDS
+// round trip: v_permlane32_swap exchanges the upper half of one register
+// with the lower half of another, so swapping a register with itself
+// gives each half the other's value.  Every lane of the wave takes part.
+__device__ __forceinline__ uint32_t xor32_u(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return (__lane_id() & 32) ? r[0] : r[1];
+}
+__device__ __forceinline__ float xor32(float v) { return __uint_as_float(xor32_u(__float_as_uint(v))); }
+__device__ __forceinline__ int xor32(int v) { return (int)xor32_u((uint32_t)v); }
+
 // s_waitcnt vmcnt(n) (expcnt / lgkmcnt not waited for)
 template <int N>
 __device__ __forceinline__ void wait_vm() {

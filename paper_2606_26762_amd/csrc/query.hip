@@ -1303,7 +1303,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
           tmax = fmaxf(tmax, x);
         }
     }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    tmax = fmaxf(tmax, xor32(tmax));
     // the reference moves up only when a row's max exceeds it by more than 8
     const bool grow = BIAS ? tmax > mref + 8.0f : tmax > 8.0f;
     if (__ballot(grow)) {  // uniform
@@ -1348,7 +1348,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
       sum1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 6, 7), ones2, sum1, false);
     }
     float psum = sum0 + sum1;
-    psum += __shfl_xor(psum, 32, 64);
+    psum += xor32(psum);
     lrun += psum;
     // O^T = V^T P.  k positions half*8 + i of step st <-> keys 16 st + 4 half + {0..3}
     // (i < 4) and 16 st + 8 + 4 half + {0..3} (i >= 4), matching P's layout.  Each
