@@ -1646,17 +1646,20 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
 // Combines the splits of each query row: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
 // Combines the splits' partials of output row r, dims 4 d4 .. 4 d4 + 3, of
 // kv head u: O = sum_s w_s O_s / sum_s w_s l_s with w_s = 2^(m_s - max m).
-template <int FP32>
+// NSP: the number of splits when known at compile time (0: aa.splits).
+template <int FP32, int NSP>
 __device__ __forceinline__ void merge_row4(const Dims& dm, const Workspace& ws, const AttendArgs& aa, int u, int r,
                                            int d4) {
+  constexpr int NS = NSP ? NSP : MAX_SPLITS;
+  const int nsplit = NSP ? NSP : aa.splits;
   const int grp = dm.Hq / dm.Hkv;
   const int l = u / dm.Hkv, kvh = u % dm.Hkv;
-  float ms[MAX_SPLITS], ls[MAX_SPLITS];
-  float4 ov[MAX_SPLITS];
+  float ms[NS], ls[NS];
+  float4 ov[NS];
   float M = -INFINITY;
 #pragma unroll
-  for (int s2 = 0; s2 < MAX_SPLITS; ++s2) {
-    if (s2 < aa.splits) {
+  for (int s2 = 0; s2 < NS; ++s2) {
+    if (s2 < nsplit) {
       const size_t pr = ((size_t)u * dm.max_splits + s2) * dm.max_rows + r;
       ms[s2] = ws.part_ml[pr * 2];
       ls[s2] = ws.part_ml[pr * 2 + 1];
@@ -1667,8 +1670,8 @@ __device__ __forceinline__ void merge_row4(const Dims& dm, const Workspace& ws, 
   float Lsum = 0.f;
   float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int s2 = 0; s2 < MAX_SPLITS; ++s2) {
-    if (s2 < aa.splits) {
+  for (int s2 = 0; s2 < NS; ++s2) {
+    if (s2 < nsplit) {
       const float w = ms[s2] == -INFINITY ? 0.f : exp2f(ms[s2] - M);
       Lsum += w * ls[s2];
       o.x += w * ov[s2].x;
@@ -1691,16 +1694,17 @@ __device__ __forceinline__ void merge_row4(const Dims& dm, const Workspace& ws, 
   if (d4 == 0 && aa.lse) aa.lse[((size_t)l * aa.tq + t) * dm.Hq + kvh * grp + gg] = (M + log2f(Lsum)) * LN2;
 }
 
-template <int FP32>
+template <int FP32, int NSP>
 __global__ __launch_bounds__(256) void k_attend_merge(Dims dm, Workspace ws, AttendArgs aa, int rows) {
   // thread = (kv head, query row, 4 output dims); every split's (m, l) and
-  // partial O are loaded together
-  const size_t gt = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (gt >= (size_t)dm.units * rows * (D / 4)) return;
-  const int d4 = (int)(gt % (D / 4));
-  const int r = (int)((gt / (D / 4)) % rows);
-  const int u = (int)(gt / ((size_t)(D / 4) * rows));
-  merge_row4<FP32>(dm, ws, aa, u, r, d4);
+  // partial O are loaded together (units * rows * D / 4 < 2^31)
+  const int gt = (int)blockIdx.x * 256 + (int)threadIdx.x;
+  if (gt >= dm.units * rows * (D / 4)) return;
+  const int d4 = gt & (D / 4 - 1);
+  const int rr = gt / (D / 4);
+  const int r = rr % rows;
+  const int u = rr / rows;
+  merge_row4<FP32, NSP>(dm, ws, aa, u, r, d4);
 }
 
 // float32 path (small fp32 streams): one wave per (kv head, query row, split),
@@ -1795,9 +1799,11 @@ hipError_t launch_attend_merge(const Dims& dm, const Workspace& ws, const Attend
   const int rows = aa.tq * (dm.Hq / dm.Hkv);
   const int nb = (int)(((size_t)dm.units * rows * (D / 4) + 255) / 256);
   if (dm.kv_fp32)
-    hipLaunchKernelGGL(k_attend_merge<1>, dim3(nb), dim3(256), 0, st, dm, ws, aa, rows);
+    hipLaunchKernelGGL((k_attend_merge<1, 0>), dim3(nb), dim3(256), 0, st, dm, ws, aa, rows);
+  else if (aa.splits == 2)
+    hipLaunchKernelGGL((k_attend_merge<0, 2>), dim3(nb), dim3(256), 0, st, dm, ws, aa, rows);
   else
-    hipLaunchKernelGGL(k_attend_merge<0>, dim3(nb), dim3(256), 0, st, dm, ws, aa, rows);
+    hipLaunchKernelGGL((k_attend_merge<0, 0>), dim3(nb), dim3(256), 0, st, dm, ws, aa, rows);
   return hipGetLastError();
 }
 
