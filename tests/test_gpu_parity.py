@@ -148,6 +148,31 @@ def test_maximum_frame_and_query_sizes(cap):
     assert pair.assign_checked == (wl.frames - wl.window_frames) * wl.tokens_per_frame
 
 
+@pytest.mark.parametrize("cap,clusters", [(8, 4), (24, 3)])
+def test_many_tokens_per_slot(cap, clusters):
+    """Few slots, many tokens: T = 1024 (32x32) folded into K = 8 or 24
+    slots over 3 or 4 clusters, so a fold gives one slot up to several
+    hundred tokens.  The touched-slot aggregation buckets them by slot and
+    absorbs each slot's tokens in eviction order: banks bitwise equal to the
+    oracle's after every fold (the float32 sums depend on that order), then
+    the rows and the readout."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=4, grid_h=32, grid_w=32,
+                                 frames=6, window_frames=1, capacity=cap, query_tokens=4, clusters=clusters)
+    h.log(f"case: many tokens per slot T=1024 K={cap} clusters={clusters}")
+    pair = h.Pair(wl)
+    for f in range(wl.frames):
+        pair.step()
+        if f >= wl.window_frames:
+            pair.check_bank(bitwise=True)
+    pseudo = pair.synthesize()
+    pair.attend(pair.query(np.random.default_rng(29)), pseudo)
+    st = pair.oracle[0]
+    most = max(int(b.n.max()) for b in st.banks)
+    h.log(f"largest slot mass {most}, near ties {pair.near_ties}")
+    assert most > 4 * 1024 // cap
+
+
 def test_ragged_shapes_seed_and_assign_same_fold():
     """T=35 (5x7, ragged tiles), K=20 < T (seed and assign in one fold),
     2 layers x 2 kv heads x 6 q heads, S=3, C=12, tq=5."""
