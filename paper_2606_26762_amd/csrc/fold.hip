@@ -158,11 +158,13 @@ __device__ void refresh_cache16(const Dims& dm, const float (&s)[8], const RowMe
 // ---------------------------------------------------------------------------
 // Near ring insert: frame -> ring slot (f mod (W+1)) of each listed stream.
 // Workgroup = one part of one (batch entry, unit): its frame of K and of V is
-// one contiguous block on both sides, split into parts of at most 1024
-// 16-byte chunks so that every thread issues all of its (up to 4 + 4) loads
-// before its first store.
+// one contiguous block on both sides, split into `parts` equal parts of at
+// most 1024 16-byte chunks so that every thread issues all of its (up to
+// 4 + 4) loads before its first store.  The frame is read once and the ring
+// is read again only W frames later, so both go through nontemporal
+// accesses that do not keep the lines in L2.
 // ---------------------------------------------------------------------------
-constexpr int RING_CHUNKS = 1024;  // 16-byte chunks of K (and of V) per workgroup
+constexpr int RING_CHUNKS = 1024;  // 16-byte chunks of K (and of V) per workgroup, at most
 
 __global__ __launch_bounds__(256) void k_ring_insert(Dims dm, Workspace ws, AppendBatch ab,
                                                      const uint8_t* k, const uint8_t* v,
@@ -171,22 +173,26 @@ __global__ __launch_bounds__(256) void k_ring_insert(Dims dm, Workspace ws, Appe
   const int e = eu / dm.units, unit = eu % dm.units;
   const size_t dst = (((size_t)ab.sid[e] * dm.units + unit) * (dm.W + 1) + ab.slot[e]) * unit_bytes;
   const size_t src = ((size_t)e * dm.units + unit) * unit_bytes;
-  const uint4* ks = reinterpret_cast<const uint4*>(k + src);
-  const uint4* vs = reinterpret_cast<const uint4*>(v + src);
-  uint4* kd = reinterpret_cast<uint4*>(ws.ring_k + dst);
-  uint4* vd = reinterpret_cast<uint4*>(ws.ring_v + dst);
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4* ks = reinterpret_cast<const u32x4*>(k + src);
+  const u32x4* vs = reinterpret_cast<const u32x4*>(v + src);
+  u32x4* kd = reinterpret_cast<u32x4*>(ws.ring_k + dst);
+  u32x4* vd = reinterpret_cast<u32x4*>(ws.ring_v + dst);
   const int n16 = (int)(unit_bytes / 16);
-  const int lo = part * RING_CHUNKS, hi = min(n16, lo + RING_CHUNKS);
+  const int per = (n16 + parts - 1) / parts;  // <= RING_CHUNKS
+  const int lo = part * per, hi = min(n16, lo + per);
   // loads unconditional (index clamped into the part, which is never empty)
   // so that all eight are in flight together; stores predicated
   // (named registers, not an array: a private array here gets promoted to LDS)
   const int i0 = lo + (int)threadIdx.x, i1 = i0 + 256, i2 = i0 + 512, i3 = i0 + 768;
-  const uint4 a0 = ks[min(i0, hi - 1)], a1 = ks[min(i1, hi - 1)], a2 = ks[min(i2, hi - 1)], a3 = ks[min(i3, hi - 1)];
-  const uint4 c0 = vs[min(i0, hi - 1)], c1 = vs[min(i1, hi - 1)], c2 = vs[min(i2, hi - 1)], c3 = vs[min(i3, hi - 1)];
-  if (i0 < hi) { kd[i0] = a0; vd[i0] = c0; }
-  if (i1 < hi) { kd[i1] = a1; vd[i1] = c1; }
-  if (i2 < hi) { kd[i2] = a2; vd[i2] = c2; }
-  if (i3 < hi) { kd[i3] = a3; vd[i3] = c3; }
+  const u32x4 a0 = __builtin_nontemporal_load(ks + min(i0, hi - 1)), a1 = __builtin_nontemporal_load(ks + min(i1, hi - 1));
+  const u32x4 a2 = __builtin_nontemporal_load(ks + min(i2, hi - 1)), a3 = __builtin_nontemporal_load(ks + min(i3, hi - 1));
+  const u32x4 c0 = __builtin_nontemporal_load(vs + min(i0, hi - 1)), c1 = __builtin_nontemporal_load(vs + min(i1, hi - 1));
+  const u32x4 c2 = __builtin_nontemporal_load(vs + min(i2, hi - 1)), c3 = __builtin_nontemporal_load(vs + min(i3, hi - 1));
+  if (i0 < hi) { __builtin_nontemporal_store(a0, kd + i0); __builtin_nontemporal_store(c0, vd + i0); }
+  if (i1 < hi) { __builtin_nontemporal_store(a1, kd + i1); __builtin_nontemporal_store(c1, vd + i1); }
+  if (i2 < hi) { __builtin_nontemporal_store(a2, kd + i2); __builtin_nontemporal_store(c2, vd + i2); }
+  if (i3 < hi) { __builtin_nontemporal_store(a3, kd + i3); __builtin_nontemporal_store(c3, vd + i3); }
 }
 
 hipError_t launch_ring_insert(const Dims& dm, const Workspace& ws, const AppendBatch& ab,
