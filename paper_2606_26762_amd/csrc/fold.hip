@@ -983,10 +983,15 @@ struct Raw8 {
   uint4 w[FP32 ? 2 : 1];
 };
 template <int FP32>
+// (nontemporal: an evicted token is absorbed once, so its lines need not stay in L2)
 __device__ __forceinline__ void load8(const uint8_t* base, size_t e, Raw8<FP32>& x) {
-  const uint4* p = reinterpret_cast<const uint4*>(base + e * (FP32 ? 4 : 2));
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4* p = reinterpret_cast<const u32x4*>(base + e * (FP32 ? 4 : 2));
 #pragma unroll
-  for (int q = 0; q < (FP32 ? 2 : 1); ++q) x.w[q] = p[q];
+  for (int q = 0; q < (FP32 ? 2 : 1); ++q) {
+    const u32x4 t = __builtin_nontemporal_load(p + q);
+    x.w[q] = make_uint4(t.x, t.y, t.z, t.w);
+  }
 }
 template <int FP32>
 __device__ __forceinline__ float raw_at(const Raw8<FP32>& x, int q) {
@@ -1001,9 +1006,12 @@ __device__ __forceinline__ void ld8f(const uint8_t* p, float (&x)[8]) {
   const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
   x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
 }
+// (nontemporal: a rewritten bank row is read again only when a later fold
+// touches the slot, long after it has left L2)
 __device__ __forceinline__ void st8f(uint8_t* p, const float (&x)[8]) {
-  reinterpret_cast<float4*>(p)[0] = make_float4(x[0], x[1], x[2], x[3]);
-  reinterpret_cast<float4*>(p)[1] = make_float4(x[4], x[5], x[6], x[7]);
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store((f32x4){x[0], x[1], x[2], x[3]}, reinterpret_cast<f32x4*>(p));
+  __builtin_nontemporal_store((f32x4){x[4], x[5], x[6], x[7]}, reinterpret_cast<f32x4*>(p) + 1);
 }
 
 template <int FP32, int EMA, int NP>
@@ -1201,8 +1209,11 @@ __global__ __launch_bounds__(256, EMA ? 2 : (NP > 2 ? 3 : 4)) void k_aggregate(D
             }
             if (pq) {
               float* rr = ws.ema_res + ((unit * N + jj) * 2) * (size_t)D + 8 * il;
-              st8f(reinterpret_cast<uint8_t*>(rr), rk);
-              st8f(reinterpret_cast<uint8_t*>(rr + D), rv);
+              // read back by this workgroup below: ordinary stores
+              *reinterpret_cast<float4*>(rr) = make_float4(rk[0], rk[1], rk[2], rk[3]);
+              *reinterpret_cast<float4*>(rr + 4) = make_float4(rk[4], rk[5], rk[6], rk[7]);
+              *reinterpret_cast<float4*>(rr + D) = make_float4(rv[0], rv[1], rv[2], rv[3]);
+              *reinterpret_cast<float4*>(rr + D + 4) = make_float4(rv[4], rv[5], rv[6], rv[7]);
               m.n_res += 1;
             }
           } else {
