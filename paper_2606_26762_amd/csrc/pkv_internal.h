@@ -164,7 +164,9 @@ struct AttendArgs {
   int n_far;        // pseudo-tokens (active slots * S)
   int tq;
   int splits;       // context splits per kv head
-  int chunk;        // context tokens per split (multiple of 32)
+  int chunk;        // context tokens per split (multiple of 64; rows written, gen 0)
+  int near_chunk;   // gen 1: near-window tokens per split (multiple of 64) ...
+  int far_chunk;    // ... and pseudo-token rows per split (multiple of 64)
   int gen;          // bf16: pseudo-token rows are formed from centres, codes and codebooks (else read from pk, pv)
   const uint8_t* near_k;  // near-window keys: ring_k, or ring_kr with rotary positions
   const float* rowbias;   // bias per pseudo-token row [units][K*S] (variance-aware allocation), else null

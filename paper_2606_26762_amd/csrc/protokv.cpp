@@ -634,31 +634,19 @@ static protokv_status plan_attend(protokv_t h, int32_t sid, const void* q, int32
     // about one workgroup per compute unit (256 on MI355X)
     splits = std::max(1, std::min(max_splits, (256 + h->dm.units * rblocks / 2) / (h->dm.units * rblocks)));
   }
-  int chunk = (ctx + splits - 1) / splits;
-  chunk = (chunk + 63) / 64 * 64;
-  if (!h->dm.kv_fp32 && splits > 1) {
-    // Split i covers context rows [i * chunk, min(ctx, (i + 1) * chunk)).
-    // Pseudo-token tiles formed in LDS cost more than near-window tiles, so
-    // the chunk is the multiple of 64 (>= ctx / splits) that minimises the
-    // largest split's cost in tiles, a formed tile weighing kFormed.
-    const double kFormed = aa.gen ? 1.4 : 1.0;
-    auto tiles = [](int n) { return (n + 63) / 64; };
-    double best = 1e300;
-    int best_chunk = chunk;
-    for (int ch = chunk; ch < ctx + 64; ch += 64) {
-      double worst = 0.0;
-      for (int lo = 0; lo < ctx; lo += ch) {
-        const int hi = std::min(ctx, lo + ch);
-        const int nn = std::max(0, std::min(hi, aa.n_near) - lo);
-        worst = std::max(worst, tiles(nn) + kFormed * tiles(hi - lo - nn));
-      }
-      if (worst < best) {
-        best = worst;
-        best_chunk = ch;
-      }
-    }
-    chunk = best_chunk;
+  auto up64 = [](int x) { return (x + 63) / 64 * 64; };
+  if (aa.gen) {
+    // pseudo-token rows formed in LDS (bf16): every split takes an equal
+    // share of the near-window tiles and of the formed tiles, which cost
+    // more than the tiles loaded directly
+    aa.near_chunk = std::max(64, up64((aa.n_near + splits - 1) / splits));
+    aa.far_chunk = std::max(64, up64((aa.n_far + splits - 1) / splits));
+    aa.splits = std::max((aa.n_near + aa.near_chunk - 1) / aa.near_chunk,
+                         (aa.n_far + aa.far_chunk - 1) / aa.far_chunk);
+    aa.chunk = 0;
+    return PROTOKV_OK;
   }
+  const int chunk = up64((ctx + splits - 1) / splits);
   aa.splits = (ctx + chunk - 1) / chunk;
   aa.chunk = chunk;
   return PROTOKV_OK;

@@ -1153,13 +1153,13 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
   const int grp = dm.Hq / dm.Hkv;
   const int l = u / dm.Hkv, kvh = u % dm.Hkv;
   const int ctx = aa.n_near + aa.n_far;
-  const int c0 = split * aa.chunk;
-  const int c1 = min(ctx, c0 + aa.chunk);
-  // rows [c0, c1n) stream through LDS by DMA (near-window rows, and the
-  // written pseudo-token rows when aa.gen is 0); with aa.gen the pseudo-token
-  // rows [max(c0, n_near), c1) are formed in LDS from the synthesized centres,
-  // decode records and codebooks
-  const int c1n = aa.gen ? min(c1, aa.n_near) : c1;
+  // rows [c0, c1n) stream through LDS by DMA: with aa.gen the split's share
+  // of the near window (the pseudo-token rows [ps0, ps1) of its share are
+  // formed in LDS from the synthesized centres, decode records and
+  // codebooks), else context rows [c0, c1) of the near window followed by
+  // the written pseudo-token rows
+  const int c0 = aa.gen ? min(aa.n_near, split * aa.near_chunk) : split * aa.chunk;
+  const int c1n = aa.gen ? min(aa.n_near, c0 + aa.near_chunk) : min(ctx, c0 + aa.chunk);
   const int ntiles = c1n > c0 ? (c1n - c0 + AT_KEYS - 1) / AT_KEYS : 0;
   const bool pb_lds = dm.K <= AT_PB_MAX;
   if (pb_lds)
@@ -1413,7 +1413,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
   // forming of the next tile overlaps the MFMA work of the current one.
   // LDS: buffers 0, 1 the formed tiles, s_kv[2][0] the unit's codebooks (16
   // KiB), s_kv[2][1] .. s_kv[3][1] the staging buffers.
-  const int ps0 = max(c0, aa.n_near) - aa.n_near, ps1 = c1 - aa.n_near;
+  const int ps0 = min(aa.n_far, split * aa.far_chunk), ps1 = min(aa.n_far, ps0 + aa.far_chunk);
   const int npt = aa.gen && ps1 > ps0 ? (ps1 - ps0 + AT_KEYS - 1) / AT_KEYS : 0;
   if (npt > 0) {  // uniform
     constexpr int PS_INSTR = 16;                        // PS_SLOTS centre loads + 2 record loads
