@@ -1097,8 +1097,11 @@ __device__ __forceinline__ CtxRef ctx_key(const Dims& dm, const Workspace& ws, c
   return r;
 }
 
-// bf16 path.  Workgroup = one (kv head, context split, block of up to 256
-// query rows), one wave per 32 rows (at least 4 waves).  A context tile of 64
+// bf16 path.  Workgroup = eight waves for one (kv head, context split,
+// block of query rows): one wave per 32 rows for up to 256 rows (KH = 1), or
+// for at most 128 rows two waves per 32 rows, each taking one 32-key half
+// of every tile, their results merged at the end (KH = 2), so each SIMD
+// runs two waves either way.  A context tile of 64
 // keys sits in LDS in two layouts under which every operand read is a per-lane
 // base plus compile-time offsets and touches distinct banks:
 //   K chunk-major: 16-byte chunk c (dims 8c .. 8c+7) of row r at c * 1024 + r * 16;
@@ -1131,9 +1134,10 @@ constexpr int AT_NBUF = 4;        // tile buffers: tile t computes while t+1..t+
 constexpr int AT_NTAB = 5;        // row-table entries (written 3 tiles ahead)
 constexpr int AT_PB_MAX = 2048;   // pseudo-token biases staged in LDS up to this capacity
 
-template <int NW>
-__global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims dm, Workspace ws, AttendArgs aa, int rows, int rblocks) {
+template <int NW, int KH>
+__global__ __launch_bounds__(NW * 64, 1) void k_attend_bf16(Dims dm, Workspace ws, AttendArgs aa, int rows, int rblocks) {
   constexpr int LPT = 32 / NW;  // load instructions per wave per tile
+  constexpr int RPW = NW * 32 / KH;  // query rows per workgroup
   __shared__ __attribute__((aligned(16))) uint8_t s_kv[AT_NBUF][2][AT_TILE_BYTES];   // [buffer][K,V]
   __shared__ __attribute__((aligned(16))) float s_bias[AT_NTAB][AT_KEYS];           // log2(e) * bias, -inf past the context
   __shared__ const uint8_t* s_rowp[AT_NTAB][2][AT_KEYS];                             // K and V address of each tile row
@@ -1166,9 +1170,12 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
     for (int k = tid; k < dm.K; k += NW * 64) s_pb[k] = ws.pbias[(size_t)u * dm.K + k] * LOG2E;
 
   const int col = lane & 31, half = lane >> 5;
-  const int r = rb * (NW * 32) + wave * 32 + col;  // query row of this lane
+  // KH = 2: waves w and w + NW / 2 take the same 32 query rows and the two
+  // 32-key halves of every tile
+  const int rblk = KH == 2 ? wave % (NW / 2) : wave, kh = KH == 2 ? wave / (NW / 2) : 0;
+  const int r = rb * RPW + rblk * 32 + col;  // query row of this lane
   const bool rvalid = r < rows;
-  const bool wvalid = rb * (NW * 32) + wave * 32 < rows;  // uniform: the wave has query rows
+  const bool wvalid = rb * RPW + rblk * 32 < rows;  // uniform: the wave has query rows
   bf16x8 bq[8];
   {
     const int t = rvalid ? r / grp : 0, gg = rvalid ? r % grp : 0;
@@ -1264,15 +1271,17 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
     constexpr bool BIAS = decltype(bias_tag)::value;
     const uint8_t* kl = kt + koff;
     const uint8_t* vl = vt + voff;
-    // S^T for the two 32-key halves of the tile
-    f32x16 sacc[2];
+    // S^T for the wave's 32-key halves of the tile (both, or half kh)
+    constexpr int NH = 2 / KH;
+    f32x16 sacc[NH];
   #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      sacc[h] = (f32x16){0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int hh = 0; hh < NH; ++hh) {
+      const int h = KH == 2 ? kh : hh;
+      sacc[hh] = (f32x16){0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   #pragma unroll
       for (int kk = 0; kk < 8; ++kk) {
         const bf16x8 ak = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(kl + kk * 2048 + h * 512));
-        sacc[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bq[kk], sacc[h], 0, 0, 0);
+        sacc[hh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bq[kk], sacc[hh], 0, 0, 0);
       }
     }
     // scores x = s * scale + bias (key m = h*32 + (i/4)*8 + half*4 + i%4),
@@ -1280,26 +1289,28 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
     float tmax = -1e30f;
     if constexpr (BIAS) {
   #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int hh = 0; hh < NH; ++hh) {
+        const int h = KH == 2 ? kh : hh;
   #pragma unroll
         for (int i4 = 0; i4 < 4; ++i4) {
           const float4 bb = *reinterpret_cast<const float4*>(&s_bias[tb][h * 32 + i4 * 8 + half * 4]);
           const float bv[4] = {bb.x, bb.y, bb.z, bb.w};
   #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float x = fmaf(sacc[h][i4 * 4 + e], scale, bv[e]);
-            sacc[h][i4 * 4 + e] = x;
+            const float x = fmaf(sacc[hh][i4 * 4 + e], scale, bv[e]);
+            sacc[hh][i4 * 4 + e] = x;
             tmax = fmaxf(tmax, x);
           }
         }
+      }
     } else {
       const float nm = -mref;
   #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int hh = 0; hh < NH; ++hh)
   #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const float x = fmaf(sacc[h][i], scale, nm);
-          sacc[h][i] = x;
+          const float x = fmaf(sacc[hh][i], scale, nm);
+          sacc[hh][i] = x;
           tmax = fmaxf(tmax, x);
         }
     }
@@ -1326,22 +1337,22 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
   #pragma unroll
           for (int i = 0; i < 16; ++i) oacc[b][i] *= alpha;
   #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int hh = 0; hh < NH; ++hh)
   #pragma unroll
-          for (int i = 0; i < 16; ++i) sacc[h][i] -= delta;
+          for (int i = 0; i < 16; ++i) sacc[hh][i] -= delta;
         mref = mnew;
       }
     }
     // P in bf16; the row sum is taken over the rounded values the products use
-    bf16x8 pb[4];
+    bf16x8 pb[2 * NH];
   #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int hh = 0; hh < NH; ++hh)
   #pragma unroll
       for (int i = 0; i < 16; ++i)
-        pb[2 * h + (i >> 3)][i & 7] = (__bf16)__builtin_amdgcn_exp2f(BIAS ? sacc[h][i] - mref : sacc[h][i]);
+        pb[2 * hh + (i >> 3)][i & 7] = (__bf16)__builtin_amdgcn_exp2f(BIAS ? sacc[hh][i] - mref : sacc[hh][i]);
     float sum0 = 0.f, sum1 = 0.f;
   #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 2 * NH; ++j) {
       sum0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 0, 1), ones2, sum0, false);
       sum1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 2, 3), ones2, sum1, false);
       sum0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 4, 5), ones2, sum0, false);
@@ -1358,9 +1369,10 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
   #pragma unroll
     for (int b = 0; b < 4; ++b) {
   #pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vl + b * 4096 + st * 1024));
-        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vl + b * 4096 + st * 1024 + 512));
+      for (int st = 0; st < 2 * NH; ++st) {
+        const int sk = KH == 2 ? 2 * kh + st : st;  // 16-key step of the tile
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vl + b * 4096 + sk * 1024));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vl + b * 4096 + sk * 1024 + 512));
         const v8i16 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), pb[st], oacc[b], 0, 0, 0);
       }
@@ -1612,6 +1624,32 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attend_bf16(Dims d
       if (!form_first && t + 1 < npt) form(t + 1);
     }
   }
+  if constexpr (KH == 2) {
+    // waves of key half 1 hand (reference, sum, O) to their half-0 partner
+    // through LDS; both are relative to their own reference, so
+    // O = 2^(m1 - m) O1 + 2^(m2 - m) O2, l likewise, m = max(m1, m2)
+    __syncthreads();  // every wave is done with the tiles (LDS reused)
+    float* s_part = reinterpret_cast<float*>(&s_kv[0][0][0]) + (size_t)rblk * 66 * 64;
+    if (kh == 1) {
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s_part[(b * 16 + i) * 64 + lane] = oacc[b][i];
+      s_part[64 * 64 + lane] = mref;
+      s_part[65 * 64 + lane] = lrun;
+    }
+    __syncthreads();
+    if (kh == 1) return;
+    const float m2 = s_part[64 * 64 + lane], l2 = s_part[65 * 64 + lane];
+    const float m = fmaxf(mref, m2);
+    const float a1 = __builtin_amdgcn_exp2f(mref - m), a2 = __builtin_amdgcn_exp2f(m2 - m);
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) oacc[b][i] = oacc[b][i] * a1 + s_part[(b * 16 + i) * 64 + lane] * a2;
+    lrun = lrun * a1 + l2 * a2;
+    mref = m;
+  }
   const float mrun = mref;
 
   const size_t orow_t = rvalid ? (size_t)(r / grp) : 0;
@@ -1755,14 +1793,14 @@ hipError_t launch_attend(const Dims& dm, const Workspace& ws, const AttendArgs& 
   if (dm.kv_fp32) {
     hipLaunchKernelGGL(k_attend_f32, dim3(dm.units * rows * aa.splits), dim3(64), 0, st, dm, ws, aa, rows);
   } else {
-    // 8 waves (256 query rows) per workgroup, or 4 waves for at most 128 rows:
-    // every wave issues 32 / waves loads per tile
+    // 8 waves per workgroup: 256 query rows, or at most 128 rows with the
+    // tiles' key halves split between wave pairs
     const int rblocks = (rows + AT_ROWS - 1) / AT_ROWS;
     if (rows > 128)
-      hipLaunchKernelGGL(k_attend_bf16<8>, dim3(dm.units * aa.splits * rblocks), dim3(512), 0, st, dm, ws, aa,
+      hipLaunchKernelGGL((k_attend_bf16<8, 1>), dim3(dm.units * aa.splits * rblocks), dim3(512), 0, st, dm, ws, aa,
                          rows, rblocks);
     else
-      hipLaunchKernelGGL(k_attend_bf16<4>, dim3(dm.units * aa.splits), dim3(256), 0, st, dm, ws, aa, rows, 1);
+      hipLaunchKernelGGL((k_attend_bf16<8, 2>), dim3(dm.units * aa.splits), dim3(512), 0, st, dm, ws, aa, rows, 1);
   }
   return hipGetLastError();
 }
