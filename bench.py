@@ -452,8 +452,12 @@ def run_workload(wl, args, steps, warmup, profile_frames, query_reps, headline):
         dom_bytes = readout_bytes(wl, wl.units, ctx, n_active, rows) * live["avg_us"] / max(query_dev_us, 1e-9)
     achieved = dom_bytes / (live["avg_us"] * 1e-6) / 1e9
     traffic = recorded_traffic(dom, wl)
+    # a plain copy of known size measured in the same run (the ring insert:
+    # the frame read once and written once) as the practical bandwidth
+    copy_gbs = kernels.get("ring_insert", {}).get("gbs")
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "copy_gbs": copy_gbs, "frac_of_copy": round(achieved / copy_gbs, 4) if copy_gbs else None,
                 "traffic": traffic["traffic_bytes_per_launch"] if traffic else None,
                 "alg_bytes_per_launch": int(dom_bytes), "avg_us": round(live["avg_us"], 3),
                 "launches_timed": live["launches"],
@@ -465,6 +469,7 @@ def run_workload(wl, args, steps, warmup, profile_frames, query_reps, headline):
     roof_fold = {"kernels": fold_names, "alg_bytes_per_frame": int(fold_b), "device_us_per_frame": round(fold_us, 2),
                  "achieved": round(fold_b / (fold_us * 1e-6) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                  "frac": round(fold_b / (fold_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                 "frac_of_copy": round(fold_b / (fold_us * 1e-6) / 1e9 / copy_gbs, 4) if copy_gbs else None,
                  "touched_per_unit": round(touched, 2)}
     rb = readout_bytes(wl, wl.units, ctx, n_active, rows)
     rf = readout_flops(wl.units, ctx, rows)
@@ -472,6 +477,7 @@ def run_workload(wl, args, steps, warmup, profile_frames, query_reps, headline):
                  "alg_bytes_per_query": int(rb), "flops_per_query": int(rf),
                  "hbm_achieved": round(rb / (query_dev_us * 1e-6) / 1e9, 1), "hbm_peak": HBM_PEAK_GBS,
                  "hbm_frac": round(rb / (query_dev_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                 "hbm_frac_of_copy": round(rb / (query_dev_us * 1e-6) / 1e9 / copy_gbs, 4) if copy_gbs else None,
                  "mfma_tflops": round(rf / (query_dev_us * 1e-6) / 1e12, 2), "mfma_peak": MFMA_BF16_PEAK_TF,
                  "mfma_frac": round(rf / (query_dev_us * 1e-6) / 1e12 / MFMA_BF16_PEAK_TF, 4),
                  "roof_us": round(1e6 * max(rb / (HBM_PEAK_GBS * 1e9), rf / (MFMA_BF16_PEAK_TF * 1e12)), 2),
