@@ -457,9 +457,13 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
     const int cw = lane & 15;
     const float* wc = cbk + gs * CBW + cw * DP;
     // the exact residual x - float32(s / n) of subspace gs, this lane's half
+    // (n passes through an empty asm so that the divisions stay in this
+    // rarely taken loop rather than being hoisted onto the common path)
+    float nfl = nf;
+    asm volatile("" : "+v"(nfl));
     float rex[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) rex[i] = (gs == g0) ? x[0][i] - sv[0][i] / nf : x[1][i] - sv[1][i] / nf;
+    for (int i = 0; i < 8; ++i) rex[i] = (gs == g0) ? x[0][i] - sv[0][i] / nfl : x[1][i] - sv[1][i] / nfl;
     float a = 0.f;
 #pragma unroll
     for (int q = 0; q < DP; ++q) {
