@@ -214,6 +214,27 @@ def test_formed_rows_across_s(S):
     h.log(f"readout err formed {w1:.2e} written {w2:.2e}, max diff {np.abs(o1 - o2).max():.2e}")
 
 
+@pytest.mark.parametrize("grp,tq", [(8, 5), (7, 13), (4, 32), (3, 43)])
+def test_readout_row_blocks(grp, tq):
+    """bf16 readout over 40, 91, 128 and 129 query rows per kv head: up to
+    128 rows two waves share each 32-row block (one per 32-key half of every
+    tile) and merge at the end, partial blocks included; 129 rows take one
+    wave per block.  T=49, W=3, K=40, S=8 (rows formed in LDS), 2 kv heads;
+    readout against the oracle, formed and written rows."""
+    h = H()
+    wl = W.WORKLOADS["7b"].with_(num_layers=1, num_kv_heads=2, num_q_heads=2 * grp, grid_h=7, grid_w=7,
+                                 frames=12, window_frames=3, capacity=40, query_tokens=tq)
+    h.log(f"case: readout rows {grp * tq} (grp {grp}, tq {tq})")
+    pair = h.Pair(wl)
+    for f in range(wl.frames):
+        pair.step()
+    pseudo = pair.synthesize()
+    q = pair.query(np.random.default_rng(70 + grp))
+    w1, o1, _ = pair.attend(q, pseudo)      # formed rows
+    w2, o2, _ = pair.attend(q, pseudo)      # rows written by read_pseudo
+    h.log(f"readout err formed {w1:.2e} written {w2:.2e}")
+
+
 # K = 48: one row block, the exactly tested pairs all listed, 16-dim filter;
 # K = 600: 8-dim filter, more filter pairs than the list holds (rows scanned);
 # K = 1100: 4-dim filter, two row blocks (the first overflows, the second
