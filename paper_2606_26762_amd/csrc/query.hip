@@ -530,6 +530,267 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
     decode_beam<SM, LPB, U128>(s_rank[wave], hist, mine, S, C, q, bq, out);
 }
 
+// Decoding, one lane per (slot, K/V) beam (S <= 8): the same beam search
+// as decode_beam, with each subspace's merge done by sorting networks in
+// registers.  For S <= 8, the top S of the (prefix i, rank j) products can
+// only come from pairs with (i + 1)(j + 1) <= 8 (every pair (i', j') with
+// i' <= i, j' <= j ranks at least as high: both lists are sorted, and equal
+// products fall back to the packed tuple, whose prefix nibbles lead): the
+// column j = 0 (8 prefixes), j = 1 (4), j = 2 and 3 (2 each), and prefix 0
+// with ranks 4..7.  These sorted lists are merged into the running top 8 by
+// a half-cleaner and a bitonic merger each.
+
+// (pa, ca) and (pb, cb) in rank order (product desc, packed tuple asc)
+template <typename P>
+__device__ __forceinline__ void cx_rank(P& pa, uint32_t& ca, P& pb, uint32_t& cb) {
+  const bool sw = pt_before(pb, cb, pa, ca);
+  const P tp = pa;
+  const uint32_t tc = ca;
+  pa = pt_sel(sw, pb, pa);
+  ca = sel32(sw, cb, ca);
+  pb = pt_sel(sw, tp, pb);
+  cb = sel32(sw, tc, cb);
+}
+// (pa, ca) becomes the first in rank order of a and b
+template <typename P>
+__device__ __forceinline__ void keep_first(P& pa, uint32_t& ca, const P& pb, uint32_t cb) {
+  const bool sw = pt_before(pb, cb, pa, ca);
+  pa = pt_sel(sw, pb, pa);
+  ca = sel32(sw, cb, ca);
+}
+// bitonic sequence of 8 -> rank order
+template <typename P>
+__device__ __forceinline__ void bmerge8(P (&p)[8], uint32_t (&c)[8]) {
+#pragma unroll
+  for (int j = 4; j > 0; j >>= 1)
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if ((i & j) == 0) cx_rank(p[i], c[i], p[i + j], c[i + j]);
+}
+// (p, c) <- the first 8 in rank order of (p, c) and (lp, lc), both sorted
+template <int K, typename P>
+__device__ __forceinline__ void merge_top8(P (&p)[8], uint32_t (&c)[8], const P (&lp)[K], const uint32_t (&lc)[K]) {
+#pragma unroll
+  for (int i = 8 - K; i < 8; ++i) keep_first(p[i], c[i], lp[7 - i], lc[7 - i]);
+  bmerge8(p, c);
+}
+// 32-bit keys (unique, larger first): a[0..7] sorted descending
+__device__ __forceinline__ void sort8_desc(uint32_t* a) {
+#pragma unroll
+  for (int k = 2; k <= 8; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if ((i ^ j) > i) {
+          const uint32_t x = a[i], y = a[i ^ j];
+          const uint32_t hi = x > y ? x : y, lo = x > y ? y : x;
+          const bool desc = (i & k) == 0;
+          a[i] = desc ? hi : lo;
+          a[i ^ j] = desc ? lo : hi;
+        }
+}
+
+template <typename P>
+__device__ __forceinline__ void decode_beam1(const uint32_t* hist, bool mine, int S, int C, uint32_t* out) {
+  const int R = S < C ? S : C;
+  P pp[8];
+  uint32_t pc[8];
+  int nb = 0;
+  uint4 hnext[4];
+#pragma unroll
+  for (int v4 = 0; v4 < 4; ++v4) hnext[v4] = mine ? reinterpret_cast<const uint4*>(hist)[v4] : make_uint4(0, 0, 0, 0);
+  for (int g = 0; g < G; ++g) {
+    uint4 hcur[4];
+#pragma unroll
+    for (int v4 = 0; v4 < 4; ++v4) {
+      hcur[v4] = hnext[v4];
+      hnext[v4] = mine && g + 1 < G ? reinterpret_cast<const uint4*>(hist + (g + 1) * CMAX)[v4] : make_uint4(0, 0, 0, 0);
+    }
+    // keys (count << 4 | (15 - c)) + 1, larger = better, 0 = absent; the
+    // first 8 in order: both halves sorted, then a half-cleaner and a merger
+    uint32_t key[16];
+#pragma unroll
+    for (int v4 = 0; v4 < 4; ++v4) {
+      const uint32_t hv[4] = {hcur[v4].x, hcur[v4].y, hcur[v4].z, hcur[v4].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = 4 * v4 + i;
+        key[c] = c < C ? ((hv[i] << 4) | (uint32_t)(15 - c)) + 1u : 0u;
+      }
+    }
+    sort8_desc(key);
+    sort8_desc(key + 8);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) key[i] = key[i] > key[15 - i] ? key[i] : key[15 - i];
+#pragma unroll
+    for (int j = 4; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if ((i & j) == 0) {
+          const uint32_t x = key[i], y = key[i + j];
+          key[i] = x > y ? x : y;
+          key[i + j] = x > y ? y : x;
+        }
+    // rank j: factor H + 1 (0 past the R ranks) and codeword
+    uint32_t f[8], z[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool ok = j < R && key[j] != 0u;
+      f[j] = ok ? ((key[j] - 1u) >> 4) + 1u : 0u;
+      z[j] = 15u - ((key[j] - 1u) & 15u);
+    }
+    const int shift = 4 * (G - 1 - g);
+    if (g == 0) {
+      // one prefix (the empty tuple): the ranks themselves
+      nb = S < R ? S : R;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const bool ok = i < nb;
+        pp[i] = pt_from<P>(ok ? f[i] : 0u);
+        pc[i] = ok ? z[i] << shift : 0xFFFFFFFFu;
+      }
+      continue;
+    }
+    // candidate (i, j): product pp[i] f[j] (0 when either is absent),
+    // tuple pc[i] | z[j] << shift
+    auto cand = [&](int i, int j, P& cp, uint32_t& cc) {
+      const bool ok = i < nb && j < R;
+      cp = ok ? pt_mul(pp[i], f[j]) : pt_from<P>(0u);
+      cc = ok ? (pc[i] | (z[j] << shift)) : 0xFFFFFFFFu;
+    };
+    P rp[8];
+    uint32_t rc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cand(i, 0, rp[i], rc[i]);
+    {
+      P lp[4];
+      uint32_t lc[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cand(i, 1, lp[i], lc[i]);
+      merge_top8<4>(rp, rc, lp, lc);
+    }
+    {
+      // columns 2 and 3 (prefixes 0, 1 each) merged into one sorted list
+      P lp[4];
+      uint32_t lc[4];
+      cand(0, 2, lp[0], lc[0]);
+      cand(1, 2, lp[1], lc[1]);
+      cand(1, 3, lp[2], lc[2]);
+      cand(0, 3, lp[3], lc[3]);
+      cx_rank(lp[0], lc[0], lp[2], lc[2]);
+      cx_rank(lp[1], lc[1], lp[3], lc[3]);
+      cx_rank(lp[0], lc[0], lp[1], lc[1]);
+      cx_rank(lp[2], lc[2], lp[3], lc[3]);
+      merge_top8<4>(rp, rc, lp, lc);
+    }
+    {
+      P lp[4];
+      uint32_t lc[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cand(0, 4 + j, lp[j], lc[j]);
+      merge_top8<4>(rp, rc, lp, lc);
+    }
+    const int nout = S < nb * R ? S : nb * R;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const bool ok = i < nout;
+      pp[i] = ok ? rp[i] : pt_from<P>(0u);
+      pc[i] = ok ? rc[i] : 0xFFFFFFFFu;
+    }
+    nb = nout;
+  }
+  if (mine) {
+#pragma unroll
+    for (int o = 0; o < 8; ++o)
+      if (o < S) out[o] = o < nb ? pc[o] : 0u;
+    out[SMAX] = 0u;
+  }
+}
+
+// One lane per (slot, K/V) beam, 64 beams (32 slots) per wave, S <= 8.  With
+// `centres` the wave also writes its 32 slots' float32 centres sum / n
+// (IEEE division), one slot's K and V halves (1 KiB) per instruction, and
+// each slot's bias.
+__global__ __launch_bounds__(256) void k_decode1(Dims dm, Workspace ws, int sid, int n_active, int centres) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int beam0 = (blockIdx.x * 4 + wave) * 64;
+  const int beam = beam0 + lane;  // (unit * n_active + slot) * 2 + K/V
+  const int nbeams = dm.units * n_active * 2;
+  if (beam0 >= nbeams) return;  // uniform
+  const bool bvalid = beam < nbeams;
+  const int kv = beam & 1, up = bvalid ? beam >> 1 : 0;
+  const int u = up / n_active, p = up % n_active;
+  const size_t unit = (size_t)sid * dm.units + u;
+  const uint8_t* row = ws.bank + (unit * dm.K + p) * ROW;
+  const RowMeta m = *reinterpret_cast<const RowMeta*>(row + ROW_META);
+  uint32_t* out = ws.pcodes + (((size_t)u * dm.K + p) * 2 + kv) * PCW;
+  const bool pq = (dm.flags & PROTOKV_FLAG_PQ) != 0;
+  const int S = dm.S, C = dm.C;
+  const bool nores = !pq || m.n_res == 0;
+  if (bvalid && nores) out[SMAX] = 1u;
+  if (centres) {  // uniform
+    const bool ema = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) != 0;
+    if (bvalid && kv == 0) {
+      const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
+      ws.pbias[(size_t)u * dm.K + p] = mb ? logf((float)m.n) : 0.f;
+      // tau_k in the key record's spare word: the readout rotates the
+      // slot's formed pseudo-keys at it
+      out[SMAX + 1] = (uint32_t)m.tau;
+    }
+    // slot i of the wave (beams 2i, 2i + 1): lane l moves float4 l of its
+    // [sum K | sum V] (the two are adjacent in the row) to the centres
+    const uint32_t nself = m.n;
+    for (int i0 = 0; i0 < 32; i0 += 8) {
+      float4 v[8];
+      float cd[8];
+      bool ok[8];
+      float4* dst[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int i = i0 + e;
+        const int bi = beam0 + 2 * i;
+        ok[e] = bi < nbeams;  // uniform
+        const int upi = ok[e] ? bi >> 1 : 0;
+        const int ui = upi / n_active, pi = upi % n_active;
+        const uint8_t* ri = ws.bank + (((size_t)sid * dm.units + ui) * dm.K + pi) * ROW;
+        v[e] = reinterpret_cast<const float4*>(ri + ROW_SUMK)[lane];
+        const uint32_t ni = (uint32_t)__shfl((int)nself, 2 * i, 64);
+        cd[e] = ema ? 1.f : (float)ni;
+        dst[e] = reinterpret_cast<float4*>(ws.pcen + ((size_t)ui * dm.K + pi) * 2 * D) + lane;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (ok[e]) *dst[e] = make_float4(v[e].x / cd[e], v[e].y / cd[e], v[e].z / cd[e], v[e].w / cd[e]);
+    }
+  }
+  const bool mine = bvalid && !nores && m.n_res <= 65534u && S <= 8;
+  const uint32_t* hist = reinterpret_cast<const uint32_t*>(row + (kv ? ROW_HV : ROW_HK));
+  // every product the merge forms is at most prod_g max_c (H[g][c] + 1);
+  // when that fits in 64 bits for all of the wave's beams the merge runs on
+  // 64-bit products
+  bool fits = true;
+  if (mine) {
+    uint64_t bound = 1;
+    bool ovf = false;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      uint32_t mx = 0;
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const uint4 h4 = reinterpret_cast<const uint4*>(hist + g * CMAX)[v4];
+        mx = max(mx, max(max(h4.x, h4.y), max(h4.z, h4.w)));
+      }
+      ovf |= __builtin_mul_overflow(bound, (uint64_t)mx + 1u, &bound);
+    }
+    fits = !ovf;
+  }
+  if (__all(fits))
+    decode_beam1<uint64_t>(hist, mine, S, C, out);
+  else
+    decode_beam1<U128>(hist, mine, S, C, out);
+}
+
 // Decoding, wide path (prototypes with more than 65534 residuals, whose
 // products need 192 bits): one thread per (slot, K/V) of one (layer, kv
 // head), 32 slots per
@@ -771,7 +1032,8 @@ hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_act
   constexpr int LPB = 2;  // lanes per beam
   const int nblk = (nbeams + 4 * (64 / LPB) - 1) / (4 * (64 / LPB));
   if (dm.S <= 8) {
-    hipLaunchKernelGGL((k_decode4<8, LPB>), dim3(nblk), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
+    const int nblk1 = (nbeams + 255) / 256;
+    hipLaunchKernelGGL(k_decode1, dim3(nblk1), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
     if (wide) hipLaunchKernelGGL(k_decode<8>, dim3(dm.units * bpu), dim3(64), lds, st, dm, ws, sid, n_active, bpu);
   } else {
     hipLaunchKernelGGL((k_decode4<16, LPB>), dim3(nblk), dim3(256), 0, st, dm, ws, sid, n_active, centres ? 1 : 0);
