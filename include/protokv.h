@@ -184,8 +184,9 @@ protokv_status protokv_fold(protokv_t h, void* stream);
  * kv_dtype, bias log n_k (Algorithms "DecodeTopSResidualModes" and
  * "Pseudo-Token Decoding and Attention").  The buffer holds the top-S code
  * tuples, the biases and the rows themselves, except for bf16 KV with S >= 5:
- * there it holds the float32 centres c_k, p_k instead and protokv_attend
- * forms each row, with the same rounding, as it reads it.  With
+ * there it holds no rows, and protokv_attend forms each row from the bank's
+ * sums (the centre sum / n, IEEE division) and the code tuples, with the
+ * same rounding, as it reads it.  With
  * rope_theta > 0 (Sec. 3.3: the S pseudo-tokens of prototype k share the
  * rotary position tau_k) each pseudo-key, rounded to kv_dtype, is rotated at
  * tau_k in float32 (angle reduced in float64) and rounded again: written

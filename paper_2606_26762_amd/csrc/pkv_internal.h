@@ -19,7 +19,7 @@ constexpr int MAXB = 64;   // streams per launch batch
 constexpr int MAX_SPLITS = 16;  // attention context splits (partials storage)
 constexpr int MAX_RBLOCKS = 2;  // query-row blocks of 256 per kv head
 constexpr int KMAX = 65535;     // prototype slots per unit (slot ids fit 16 bits)
-constexpr int PCW = SMAX + 2;   // words per (slot, K/V) decode record: S tuples, no-residual flag, tau (key record) / pad
+constexpr int PCW = SMAX + 2;   // words per (slot, K/V) decode record: S tuples, no-residual flag, tau (key record) / n (value record)
 // The bf16 readout forms pseudo-token rows in LDS from at most PS_SLOTS slots
 // per 64-row tile, which holds for S >= PS_MIN_S (64 consecutive rows span
 // floor(63 / S) + 2 slots at most); below that the synthesis writes the rows.
@@ -98,8 +98,7 @@ struct Workspace {
   uint8_t* pk;                // [units][K*S][D] kv dtype (synthesis of one stream)
   uint8_t* pv;
   float* pbias;               // [units][K]
-  float* pcen;                // [units][K][2][D]: float32 centres (sum / n) of K and V (synthesis, bf16 path)
-  uint32_t* pcodes;           // [units][K][2][PCW]: decoded top-S code tuples, no-residual flag (word SMAX), tau_k (word SMAX + 1 of the key record, written with the centres)
+  uint32_t* pcodes;           // [units][K][2][PCW]: decoded top-S code tuples, no-residual flag (word SMAX), tau_k and n (word SMAX + 1 of the key and value record, for the readout's row forming)
   float* part_o;              // [units][max_splits][max_rows][D]
   float* part_ml;             // [units][max_splits][max_rows][2]  (max, sum)
   unsigned long long* counters;  // [16]
@@ -215,8 +214,8 @@ hipError_t launch_aggregate(const Dims& dm, const Workspace& ws, const FoldBatch
 hipError_t launch_maintain(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st);
 // screening copies of every slot of stream sid rebuilt from its bank rows
 hipError_t launch_refresh_all(const Dims& dm, const Workspace& ws, int sid, hipStream_t st);
-// centres: also write the float32 centres (pcen) and biases for the readout's
-// row forming; wide: some slot may hold more than 65534 residuals (the
+// centres: also write the biases and the words the readout's row forming
+// reads (tau_k, n) into the decode records; wide: some slot may hold more than 65534 residuals (the
 // 192-bit path runs too)
 hipError_t launch_decode(const Dims& dm, const Workspace& ws, int sid, int n_active, bool centres, bool wide,
                          hipStream_t st);

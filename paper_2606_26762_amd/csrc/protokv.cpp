@@ -29,7 +29,7 @@ struct StreamState {
 
 struct Layout {
   size_t ring_k, ring_v, bank, chat_hi, chat_lo, cmeta, assign, codebooks, cbhn, cbmax;
-  size_t pk, pv, pbias, pcen, pcodes, part_o, part_ml, counters, touched, ring_kr, qrot, rope_inv, reservoir, ema_res;
+  size_t pk, pv, pbias, pcodes, part_o, part_ml, counters, touched, ring_kr, qrot, rope_inv, reservoir, ema_res;
   size_t ps_count, ps_off, prow_bias, total;
 };
 
@@ -66,7 +66,6 @@ Layout make_layout(const protokv_config& c) {
   ly.pk = take(units * K * S * D * es);
   ly.pv = take(units * K * S * D * es);
   ly.pbias = take(units * K * 4);
-  ly.pcen = take(units * K * 2 * D * 4);
   ly.pcodes = take(units * K * 2 * PCW * 4);
   ly.part_o = take(units * MAX_SPLITS * rows * D * 4);
   ly.part_ml = take(units * MAX_SPLITS * rows * 2 * 4);
@@ -384,7 +383,6 @@ protokv_status protokv_init(const protokv_config* c, const float* codebooks, voi
   ws.pk = b + ly.pk;
   ws.pv = b + ly.pv;
   ws.pbias = (float*)(b + ly.pbias);
-  ws.pcen = (float*)(b + ly.pcen);
   ws.pcodes = (uint32_t*)(b + ly.pcodes);
   ws.part_o = (float*)(b + ly.part_o);
   ws.part_ml = (float*)(b + ly.part_ml);

@@ -478,26 +478,17 @@ __global__ __launch_bounds__(256) void k_decode4(Dims dm, Workspace ws, int sid,
   const int S = dm.S, C = dm.C;
   const bool nores = !pq || m.n_res == 0;
   if (bvalid && q == 0 && nores) out[SMAX] = 1u;
-  if (bvalid && centres) {
-    // lane q takes float4s q, q + LPB, ...
-    // centre = sum / n (EMA centres: the stored centre, divided by 1)
-    const float nf = (float)m.n, cd = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) ? 1.f : nf;
-    const float4* sums = reinterpret_cast<const float4*>(row + (kv ? ROW_SUMV : ROW_SUMK));
-    float4* cen = reinterpret_cast<float4*>(ws.pcen + (((size_t)u * dm.K + p) * 2 + kv) * D);
-    // every load issued before the first store (the stores may alias them
-    // as far as the compiler knows)
-    float4 v[D / 4 / LPB];
-#pragma unroll
-    for (int i = 0; i < D / 4 / LPB; ++i) v[i] = sums[q + LPB * i];
-#pragma unroll
-    for (int i = 0; i < D / 4 / LPB; ++i)
-      cen[q + LPB * i] = make_float4(v[i].x / cd, v[i].y / cd, v[i].z / cd, v[i].w / cd);
-    if (kv == 0 && q == 0) {
+  if (bvalid && centres && q == 0) {
+    if (kv == 0) {
       const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
-      ws.pbias[(size_t)u * dm.K + p] = mb ? logf(nf) : 0.f;
+      ws.pbias[(size_t)u * dm.K + p] = mb ? logf((float)m.n) : 0.f;
       // tau_k in the key record's spare word: the readout rotates the
       // slot's formed pseudo-keys at it
       out[SMAX + 1] = (uint32_t)m.tau;
+    } else {
+      // n in the value record's spare word: the readout divides the slot's
+      // sums by it
+      out[SMAX + 1] = m.n;
     }
   }
   // this path decodes the beam (uniform within the beam's lanes)
@@ -709,9 +700,8 @@ __device__ __forceinline__ void decode_beam1(const uint32_t* hist, bool mine, in
 }
 
 // One lane per (slot, K/V) beam, 64 beams (32 slots) per wave, S <= 8.  With
-// `centres` the wave also writes its 32 slots' float32 centres sum / n
-// (IEEE division), one slot's K and V halves (1 KiB) per instruction, and
-// each slot's bias.
+// `centres` (rows formed by the readout) it also writes each slot's bias,
+// tau_k into the key record's spare word and n into the value record's.
 __global__ __launch_bounds__(256) void k_decode1(Dims dm, Workspace ws, int sid, int n_active, int centres) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int beam0 = (blockIdx.x * 4 + wave) * 64;
@@ -729,39 +719,17 @@ __global__ __launch_bounds__(256) void k_decode1(Dims dm, Workspace ws, int sid,
   const int S = dm.S, C = dm.C;
   const bool nores = !pq || m.n_res == 0;
   if (bvalid && nores) out[SMAX] = 1u;
-  if (centres) {  // uniform
-    const bool ema = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) != 0;
-    if (bvalid && kv == 0) {
+  if (centres && bvalid) {  // centres: uniform
+    if (kv == 0) {
       const bool mb = (dm.flags & PROTOKV_FLAG_MASS_BIAS) != 0;
       ws.pbias[(size_t)u * dm.K + p] = mb ? logf((float)m.n) : 0.f;
       // tau_k in the key record's spare word: the readout rotates the
       // slot's formed pseudo-keys at it
       out[SMAX + 1] = (uint32_t)m.tau;
-    }
-    // slot i of the wave (beams 2i, 2i + 1): lane l moves float4 l of its
-    // [sum K | sum V] (the two are adjacent in the row) to the centres
-    const uint32_t nself = m.n;
-    for (int i0 = 0; i0 < 32; i0 += 8) {
-      float4 v[8];
-      float cd[8];
-      bool ok[8];
-      float4* dst[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int i = i0 + e;
-        const int bi = beam0 + 2 * i;
-        ok[e] = bi < nbeams;  // uniform
-        const int upi = ok[e] ? bi >> 1 : 0;
-        const int ui = upi / n_active, pi = upi % n_active;
-        const uint8_t* ri = ws.bank + (((size_t)sid * dm.units + ui) * dm.K + pi) * ROW;
-        v[e] = reinterpret_cast<const float4*>(ri + ROW_SUMK)[lane];
-        const uint32_t ni = (uint32_t)__shfl((int)nself, 2 * i, 64);
-        cd[e] = ema ? 1.f : (float)ni;
-        dst[e] = reinterpret_cast<float4*>(ws.pcen + ((size_t)ui * dm.K + pi) * 2 * D) + lane;
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (ok[e]) *dst[e] = make_float4(v[e].x / cd[e], v[e].y / cd[e], v[e].z / cd[e], v[e].w / cd[e]);
+    } else {
+      // n in the value record's spare word: the readout divides the slot's
+      // sums by it
+      out[SMAX + 1] = m.n;
     }
   }
   const bool mine = bvalid && !nores && m.n_res <= 65534u && S <= 8;
@@ -1678,13 +1646,15 @@ __global__ __launch_bounds__(NW * 64, 1) void k_attend_bf16(Dims dm, Workspace w
   // Pseudo-token tiles formed in LDS (aa.gen): row (k, s) of K is
   // bf16(c_k + concat_g C^K_g[z_{s,g}]) (c_k alone when the slot has no
   // residual), the values k_materialize writes; likewise V.  The inputs of a
-  // tile (float32 centres, 1 KiB per slot, and decode records of its <=
-  // PS_SLOTS slots) go by DMA into one of three 16 KiB staging buffers three
-  // tiles ahead, with PS_INSTR load instructions per tile spread evenly over
-  // the waves (unused ones repeat a valid slot), so every wave's outstanding
-  // count is known.  Iteration t: wait for tile t+1's inputs, barrier, issue
-  // tile t+3's, form tile t+1 into buffer (t+1) % 2, compute tile t: the
-  // forming of the next tile overlaps the MFMA work of the current one.
+  // tile (the bank rows' float32 sums, 1 KiB per slot, and decode records of
+  // its <= PS_SLOTS slots) go by DMA into one of three 16 KiB staging buffers
+  // three tiles ahead, with PS_INSTR load instructions per tile spread evenly
+  // over the waves (unused ones repeat a valid slot), so every wave's
+  // outstanding count is known; two tiles ahead the sums are turned into
+  // centres in place.  Iteration t: wait for tile t+2's inputs, barrier,
+  // issue tile t+3's, convert tile t+2's, form tile t+1 into buffer
+  // (t+1) % 2, compute tile t: the forming of the next tile overlaps the
+  // MFMA work of the current one.
   // LDS: buffers 0, 1 the formed tiles, s_kv[2][0] the unit's codebooks (16
   // KiB), s_kv[2][1] .. s_kv[3][1] the staging buffers.
   const int ps0 = min(aa.n_far, split * aa.far_chunk), ps1 = min(aa.n_far, ps0 + aa.far_chunk);
@@ -1723,7 +1693,7 @@ __global__ __launch_bounds__(NW * 64, 1) void k_attend_bf16(Dims dm, Workspace w
         uint8_t* dst;
         if (i < PS_SLOTS) {
           const int part = (lane & 32) + (((lane & 31) - 2 * i) & 31);
-          src = reinterpret_cast<const uint8_t*>(ws.pcen + (ubase + kA + min(i, nk - 1)) * 2 * D) + part * 16;
+          src = ws.bank + (unit * dm.K + kA + min(i, nk - 1)) * ROW + ROW_SUMK + part * 16;
           dst = sb + i * 1024;
         } else {
           const int ch = min((i - PS_SLOTS) * 64 + lane, nk * (2 * PCW / 4) - 1);
@@ -1731,6 +1701,24 @@ __global__ __launch_bounds__(NW * 64, 1) void k_attend_bf16(Dims dm, Workspace w
           dst = sb + PS_REC + (i - PS_SLOTS) * 1024;
         }
         lds_dma16(src, dst);
+      }
+    };
+    // The staged sums of tile t's slots become their float32 centres
+    // sum / n (IEEE division; EMA centres are stored as such) in place, n
+    // from the staged value records.
+    const bool ema = (dm.flags & PROTOKV_FLAG_EMA_CENTRES) != 0;
+    auto convert = [&](int t) {
+      const int r0 = ps0 + t * AT_KEYS;
+      const int kA = divS(r0), kB = divS(min(r0 + AT_KEYS, ps1) - 1);
+      const int nk = kB - kA + 1;
+      uint8_t* sb = s_stage + (t % 3) * PS_STAGE;
+      const uint32_t* recs = reinterpret_cast<const uint32_t*>(sb + PS_REC);
+      for (int x = tid; x < nk * 64; x += NW * 64) {
+        const int i = x >> 6;
+        float4* c4 = reinterpret_cast<float4*>(sb + i * 1024) + (x & 63);
+        const float nf = ema ? 1.f : (float)recs[(i * 2 + 1) * PCW + SMAX + 1];
+        const float4 v = *c4;
+        *c4 = make_float4(v.x / nf, v.y / nf, v.z / nf, v.w / nf);
       }
     };
     // Tile t from stage t % 3 into buffer t % 2, in the layouts of the near
@@ -1855,28 +1843,31 @@ __global__ __launch_bounds__(NW * 64, 1) void k_attend_bf16(Dims dm, Workspace w
     stage(0);
     if (npt > 1) stage(1);
     if (npt > 2) stage(2);
-    // codebooks and tile 0's inputs have landed (tiles 1, 2 may be in flight;
-    // with rotary positions tile 1's have landed too, for its table)
-    if (npt > 2 && !rope) wait_vm<2 * IPW>();
-    else if (npt > 1 && !rope) wait_vm<IPW>();
+    // codebooks and tiles 0 and 1's inputs have landed (tile 2's may be in
+    // flight): both are converted (and with rotary positions get their
+    // tables) before tile 0 is formed
+    if (npt > 2) wait_vm<IPW>();
     else wait_vm<0>();
     lds_barrier();
+    convert(0);
+    if (npt > 1) convert(1);
     if (rope) {
       rtab(0);
       if (npt > 1) rtab(1);
-      lds_barrier();
     }
+    lds_barrier();
     form(0);
     for (int t = 0; t < npt; ++t) {
-      // this wave's loads of tile t+1's inputs have landed (tile t+2's may be
-      // in flight, except with rotary positions: its table is made now)
-      if (t + 2 < npt && !rope) wait_vm<IPW>();
-      else wait_vm<0>();
+      // this wave's loads of tile t+2's inputs have landed (converted, and
+      // with rotary positions tabled, now; tile t+1's were converted in the
+      // previous iteration)
+      wait_vm<0>();
       // tile t formed everywhere; stage t % 3 (read by form(t)), formed
       // buffer (t+1) % 2 (read by compute(t-1)) and table t % 2 (read by
       // form(t)) are free
       lds_barrier();
       if (t + 3 < npt) stage(t + 3);
+      if (t + 2 < npt) convert(t + 2);
       if (rope && t + 2 < npt) rtab(t + 2);
       // waves w and w + 4 share a SIMD: one forms before computing, the other
       // after, so the forming overlaps the partner's matrix work
