@@ -488,8 +488,8 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
 
 // ---------------------------------------------------------------------------
 // Screen + argmin.  Workgroup = 64 evicted tokens of one unit (two 32-token
-// columns per lane, keys staged once in LDS); its 4 waves split the slot
-// tiles (t = wave, wave + 4, ...) and score them with v_mfma_f32_32x32x16_bf16 (slots = rows, tokens =
+// columns per lane, keys staged once in LDS); its SW waves split the slot
+// tiles (t = wave, wave + SW, ...) and score them with v_mfma_f32_32x32x16_bf16 (slots = rows, tokens =
 // columns; unit centres as a hi + lo bf16 split read in MFMA operand order,
 // so each k-step is one contiguous 1 KiB load per wave, and the next tile's
 // loads are in flight during this tile's epilogue).  The float32 epilogue
@@ -565,10 +565,14 @@ __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, flo
   top3_push(top, cost, k);
 }
 
-constexpr int SCREEN_WAVES = 4;
-
-template <int FP32, int SQ>
-__global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
+// SW waves per workgroup, two waves per SIMD either way: four for small
+// grids, two (four workgroups per CU, whose phases overlap better) for
+// launches of many thousand workgroups.  Waves 0 and 1 decide the two
+// 32-token halves, so SW >= 2.
+template <int FP32, int SQ, int SW>
+__global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
+  static_assert(SW == 2 || SW == 4, "waves per workgroup");
+  constexpr int SCREEN_WAVES = SW;
   // token operands of the workgroup in MFMA B order [token half][k-step][lane]
   __shared__ bf16x8 s_bk[2][8][64];
   __shared__ bf16x8 s_bkl[FP32 ? 2 : 1][FP32 ? 8 : 1][64];  // low part of float32 keys
@@ -856,14 +860,15 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
   }
   }  // waves 0 and 1
 
-  // PQ codes of the tile's assigned tokens: wave w encodes the 32-token block
-  // w / 2 of K (w even) or V; each code bumps its bin of the slot's
+  // PQ codes of the tile's assigned tokens: job j = 0..3 (taken by waves
+  // j, j + SW, ...) encodes the 32-token block j / 2 of K (j even) or V; each code bumps its bin of the slot's
   // histogram (integer counts: the order of the increments does not matter).
   // With EMA centres the residuals follow each token's own centre update and
   // the aggregation codes them; codebook warm-up folds count no codes.
   if ((dm.flags & (PROTOKV_FLAG_PQ | PROTOKV_FLAG_EMA_CENTRES)) == PROTOKV_FLAG_PQ && !fb.warm[b]) {
     __syncthreads();
-    const int blk = wave >> 1, kv = wave & 1;
+    for (int job = wave; job < 4; job += SCREEN_WAVES) {  // uniform
+    const int blk = job >> 1, kv = job & 1;
     const int jq = tile * SCREEN_TOK + blk * 32 + col;
     const bool qv = jq >= nseed && jq < N;
     if (__ballot(qv)) {  // uniform per wave
@@ -944,16 +949,23 @@ __global__ __launch_bounds__(64 * SCREEN_WAVES, 2) void k_screen(Dims dm, Worksp
         if (qv) atomicAdd(hist + (2 * p + half) * CMAX + z, 1u);
       }
     }
+    }
   }
 }
 
 hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& fb, hipStream_t st) {
   int tpu = (dm.T + SCREEN_TOK - 1) / SCREEN_TOK;
-  dim3 grid(fb.n * dm.units * tpu);
+  const int nwg = fb.n * dm.units * tpu;
+  dim3 grid(nwg);
   using KFn = void (*)(Dims, Workspace, FoldBatch, int);
   const bool sq = (dm.flags & PROTOKV_FLAG_MAH_SQUARED) != 0;
-  const KFn fn = dm.kv_fp32 ? (sq ? k_screen<1, 1> : k_screen<1, 0>) : (sq ? k_screen<0, 1> : k_screen<0, 0>);
-  hipLaunchKernelGGL(fn, grid, dim3(64 * SCREEN_WAVES), 0, st, dm, ws, fb, tpu);
+  if (nwg >= 8192) {
+    const KFn fn = dm.kv_fp32 ? (sq ? k_screen<1, 1, 2> : k_screen<1, 0, 2>) : (sq ? k_screen<0, 1, 2> : k_screen<0, 0, 2>);
+    hipLaunchKernelGGL(fn, grid, dim3(128), 0, st, dm, ws, fb, tpu);
+  } else {
+    const KFn fn = dm.kv_fp32 ? (sq ? k_screen<1, 1, 4> : k_screen<1, 0, 4>) : (sq ? k_screen<0, 1, 4> : k_screen<0, 0, 4>);
+    hipLaunchKernelGGL(fn, grid, dim3(256), 0, st, dm, ws, fb, tpu);
+  }
   return hipGetLastError();
 }
 
