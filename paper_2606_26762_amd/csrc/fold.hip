@@ -566,12 +566,11 @@ __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, flo
 }
 
 // SW waves per workgroup, two waves per SIMD either way: four for small
-// grids, two (four workgroups per CU, whose phases overlap better) for
-// launches of many thousand workgroups.  Waves 0 and 1 decide the two
-// 32-token halves, so SW >= 2.
+// grids, one (eight workgroups per CU, whose phases overlap better) for
+// launches of many thousand workgroups.
 template <int FP32, int SQ, int SW>
 __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, FoldBatch fb, int tiles_per_unit) {
-  static_assert(SW == 2 || SW == 4, "waves per workgroup");
+  static_assert(SW == 1 || SW == 4, "waves per workgroup");
   constexpr int SCREEN_WAVES = SW;
   // token operands of the workgroup in MFMA B order [token half][k-step][lane]
   __shared__ bf16x8 s_bk[2][8][64];
@@ -750,9 +749,9 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     if (half == 0) s_top[wave][h * 32 + col] = top[h];
   }
   __syncthreads();
-  // waves 0 and 1 decide for token columns 0..31 and 32..63
-  if (wave < 2) {
-  const int hsel = wave;
+  // waves 0 and 1 decide for token columns 0..31 and 32..63 (one wave: both)
+  constexpr int HSTEP = SCREEN_WAVES >= 2 ? 2 : 1;
+  for (int hsel = wave; hsel < 2; hsel += HSTEP) {  // uniform
   Top3 tp = s_top[0][hsel * 32 + col];
 #pragma unroll
   for (int w = 1; w < SCREEN_WAVES; ++w) top3_merge(tp, s_top[w][hsel * 32 + col]);
@@ -858,7 +857,7 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     if (n_full) atomicAdd(&ws.counters[CNT_REFINED_FULL], (unsigned long long)n_full);
     if (n_tie) atomicAdd(&ws.counters[CNT_NEAR_TIES], (unsigned long long)n_tie);
   }
-  }  // waves 0 and 1
+  }  // token halves
 
   // PQ codes of the tile's assigned tokens: job j = 0..3 (taken by waves
   // j, j + SW, ...) encodes the 32-token block j / 2 of K (j even) or V; each code bumps its bin of the slot's
@@ -960,8 +959,8 @@ hipError_t launch_screen(const Dims& dm, const Workspace& ws, const FoldBatch& f
   using KFn = void (*)(Dims, Workspace, FoldBatch, int);
   const bool sq = (dm.flags & PROTOKV_FLAG_MAH_SQUARED) != 0;
   if (nwg >= 8192) {
-    const KFn fn = dm.kv_fp32 ? (sq ? k_screen<1, 1, 2> : k_screen<1, 0, 2>) : (sq ? k_screen<0, 1, 2> : k_screen<0, 0, 2>);
-    hipLaunchKernelGGL(fn, grid, dim3(128), 0, st, dm, ws, fb, tpu);
+    const KFn fn = dm.kv_fp32 ? (sq ? k_screen<1, 1, 1> : k_screen<1, 0, 1>) : (sq ? k_screen<0, 1, 1> : k_screen<0, 0, 1>);
+    hipLaunchKernelGGL(fn, grid, dim3(64), 0, st, dm, ws, fb, tpu);
   } else {
     const KFn fn = dm.kv_fp32 ? (sq ? k_screen<1, 1, 4> : k_screen<1, 0, 4>) : (sq ? k_screen<0, 1, 4> : k_screen<0, 0, 4>);
     hipLaunchKernelGGL(fn, grid, dim3(256), 0, st, dm, ws, fb, tpu);
