@@ -206,3 +206,87 @@ def test_malformed_states_are_refused_and_the_eviction_limit_holds():
         g.append_frame([0], k, k)
     assert e.value.status == 2
     assert g.stream_info(0).frames == frames and g.stream_info(0).pending == 0
+
+
+@pytest.mark.parametrize("S", [8, 5])
+def test_decode_on_crafted_histograms(S):
+    """The decode (exact top-S residual tuples, Alg. "DecodeTopSResidualModes")
+    on histograms made for ties, loaded through protokv_set_state: every
+    codeword with the same count (all products equal: the packed tuple
+    decides), one count vector permuted per subspace (products collide
+    across tuples), random counts up to 3, and counts whose top products
+    pass 2^64 (the 128-bit merge).  Pseudo-token rows bitwise against the
+    oracle's, and the readout."""
+    import torch
+    from oracle import protokv_oracle as O
+    h = H()
+    wl = _small()
+    h.log(f"case: crafted histograms, S={S}, T=49 K=64 W=2")
+    p = h.oracle_params(wl, S=S)
+    cb = W.make_codebooks(wl, samples=512, iters=6)
+    gen = W.HostStream(wl)
+    ora = O.OracleStream(p, list(range(wl.units)), cb)
+    frames = [gen.next_frame() for _ in range(8)]
+    for k, v in frames:
+        ora.append_frame(k, v)
+    rng = np.random.default_rng(90 + S)
+    C, G = p.C, 8
+    for u in range(wl.units):
+        b = ora.banks[u]
+        for k in np.nonzero(b.n > 0)[0]:
+            kind = k % 4
+            for hist in (b.hist_k, b.hist_v):
+                if kind == 0:
+                    nres = 3 * C
+                    hist[k] = 3
+                elif kind == 1:
+                    base = np.array([6, 4, 4, 3, 3, 2, 2, 1, 1, 1, 1, 0, 0, 0, 0, 0], dtype=np.int64)[:C]
+                    nres = int(base.sum())
+                    for g in range(G):
+                        hist[k, g] = base[rng.permutation(C)]
+                elif kind == 2:
+                    nres = 20
+                    for g in range(G):
+                        hist[k, g] = rng.multinomial(nres, np.full(C, 1.0 / C))
+                else:
+                    nres = 60000
+                    for g in range(G):
+                        hist[k, g] = rng.multinomial(nres, rng.dirichlet(np.full(C, 0.5)))
+            b.n_res[k] = nres
+            b.n[k] = max(int(b.n[k]), nres + 1)
+    gpu = h.pk.ProtoKV(h.gpu_config(wl, p), cb)
+    st = gpu.get_state(0)
+    hd = st.header
+    T, Wf = wl.tokens_per_frame, wl.window_frames
+    hd.frames = 1300   # enough evicted tokens for n_res = 60000
+    hd.folds = hd.frames - Wf
+    hd.evicted_tokens = hd.folds * T
+    hd.active_slots = int((ora.banks[0].n > 0).sum())
+    assert all(int((b.n > 0).sum()) == hd.active_slots for b in ora.banks)
+    st.blob[:128] = np.frombuffer(bytes(hd), dtype=np.uint8)
+    ring = wl.units * (Wf + 1) * T * 128 * 2
+    ring_k = st.blob[hd.off_ring_k:hd.off_ring_k + ring].view(np.uint16).reshape(wl.units, Wf + 1, T, 128)
+    ring_v = st.blob[hd.off_ring_v:hd.off_ring_v + ring].view(np.uint16).reshape(wl.units, Wf + 1, T, 128)
+    # the oracle's near window (its last W frames) as the device's last W frames
+    for i, f in enumerate(range(hd.frames - Wf, hd.frames)):
+        k, v = frames[8 - Wf + i]
+        ring_k[:, f % (Wf + 1)] = W.to_bf16_bits(k)
+        ring_v[:, f % (Wf + 1)] = W.to_bf16_bits(v)
+    for u in range(wl.units):
+        st.set_bank_rows(u, h.rows_from_bank(ora.banks[u]))
+    gpu.set_state(0, st)
+    gpu.synthesize(0)
+    pseudo = ora.synthesize()
+    q = W.quantize(np.random.default_rng(9).standard_normal((1, wl.query_tokens, 4, 128)), "bf16")
+    o, _ = gpu.attend(0, torch.from_numpy(q).to("cuda", torch.bfloat16).contiguous())  # rows formed in LDS
+    torch.cuda.synchronize()
+    oo, _ = ora.attend(q, wl.num_kv_heads, pseudo)
+    err = float(np.abs(o.float().cpu().numpy() - oo).max())
+    gk, gv, gbias = gpu.read_pseudo()
+    for u in range(wl.units):
+        ps = pseudo[u]
+        n = len(ps.keys)
+        assert np.array_equal(gk[u][:n], ps.keys), f"unit {u}: pseudo keys differ"
+        assert np.array_equal(gv[u][:n], ps.values), f"unit {u}: pseudo values differ"
+    h.log(f"readout err {err:.2e}, rows bitwise")
+    assert err <= h.READOUT_ATOL
