@@ -581,7 +581,11 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   __shared__ Top3 s_top[SCREEN_WAVES][SCREEN_TOK];
   __shared__ int s_asg[SCREEN_TOK];                           // final slot of each token of the tile
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // wave is a compile-time 0 for one-wave workgroups: the loops over a
+  // wave's share of k-steps, token halves and jobs then unroll with their
+  // loads issued together (a wave index the compiler cannot bound turns
+  // each step into a guarded load and a wait of its own)
+  const int tid = threadIdx.x, lane = tid & 63, wave = SCREEN_WAVES == 1 ? 0 : tid >> 6;
   // Workgroups are dealt to the 8 XCDs round-robin; logical block lb runs on
   // XCD lb / per, so consecutive logical blocks (the tiles of one unit) share
   // an L2.
@@ -610,70 +614,89 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   const CacheMeta* gmeta = ws.cmeta + unit * dm.K * CMETA_STRIDE;
 
   // operands of slot tile t: k-step kk of lane (col, half) is the 16 bytes
-  // of slot 32 t + col at dims 16 kk + 8 half (chat_offset); half-0 lanes
-  // also fetch their row's meta
+  // of slot 32 t + col at dims 16 kk + 8 half (chat_offset), and the first
+  // 24 bytes of that row's meta (mu_x, mu_y, qa, qb | qc, last_frame), read
+  // unconditionally from a row clamped into range (kact >= 1 whenever a tile
+  // exists) and converted only where it is used: a load under a divergent
+  // branch would be waited for at once, with every operand load before it
   u16x8 ah[8], al[8];
-  float4 ma = make_float4(0.f, 0.f, 0.f, 0.f);
-  float2 mb = make_float2(0.f, INFINITY);
+  float4 mr0 = make_float4(0.f, 0.f, 0.f, 0.f);
+  float2 mr1 = make_float2(0.f, 0.f);
   auto load_tile = [&](int t) {
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
       ah[kk] = *reinterpret_cast<const u16x8*>(ghi + (size_t)t * 32 * D + (kk >> 1) * 1024 + (kk & 1) * 16);
       al[kk] = *reinterpret_cast<const u16x8*>(glo + (size_t)t * 32 * D + (kk >> 1) * 1024 + (kk & 1) * 16);
     }
-    const int krow = t * 32 + col;
-    ma = make_float4(0.f, 0.f, 0.f, 0.f);
-    mb = make_float2(0.f, INFINITY);
-    if (half == 0 && krow < kact) {
-      const CacheMeta cm = gmeta[(size_t)krow * CMETA_STRIDE];
-      ma = make_float4(cm.mu_x, cm.mu_y, cm.qa, 2.0f * cm.qb);
-      mb = make_float2(cm.qc, (t_frame - cm.last_frame) > dm.t_idle ? lidle : 0.f);
-    }
+    const float* mp = reinterpret_cast<const float*>(gmeta + (size_t)min(t * 32 + col, kact - 1) * CMETA_STRIDE);
+    mr0 = *reinterpret_cast<const float4*>(mp);
+    mr1 = *reinterpret_cast<const float2*>(mp + 4);
   };
+  static_assert(offsetof(CacheMeta, qc) == 16 && offsetof(CacheMeta, last_frame) == 20, "meta layout");
   if (wave < ntiles) load_tile(wave);  // in flight while the keys are staged
 
-  // Stage the keys: wave w loads k-steps w, w + SCREEN_WAVES, ... of both 32-token halves
+  // Stage the keys: wave w (< SCREEN_WAVES by the launch) loads k-steps w, w + SCREEN_WAVES, ... of both 32-token halves
   // (tokens tile*64 + h*32 + col, dims 16 kk + 8 half .. + 8) and its partial norms.
   int jt[2];
   bool vt[2];
+  const uint8_t* krow[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int j = tile * SCREEN_TOK + h * 32 + col;
     const bool valid = (j >= nseed) && (j < N);
     jt[h] = j;
     vt[h] = valid;
-    const uint8_t* kr = kframe + (size_t)(valid ? j : 0) * D * es;
-    float nsq = 0.f;
+    krow[h] = kframe + (size_t)(valid ? j : 0) * D * es;
+  }
+  if (FP32) {
 #pragma unroll
-    for (int kk = wave; kk < 8; kk += SCREEN_WAVES) {
-    const int d0 = kk * 16 + half * 8;
-    if (FP32) {
-      const float4 a0 = *reinterpret_cast<const float4*>(kr + (size_t)d0 * 4);
-      const float4 a1 = *reinterpret_cast<const float4*>(kr + (size_t)(d0 + 4) * 4);
-      float f[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-      u16x8 hh, ll;
+    for (int h = 0; h < 2; ++h) {
+      float nsq = 0.f;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        float x = valid ? f[i] : 0.f;
-        nsq += x * x;
-        uint16_t hb = to_bf16(x);
-        hh[i] = hb;
-        ll[i] = to_bf16(x - from_bf16(hb));
+      for (int ks = 0; ks < 8 / SCREEN_WAVES; ++ks) {
+        const int kk = wave + ks * SCREEN_WAVES;
+        const int d0 = kk * 16 + half * 8;
+        const float4 a0 = *reinterpret_cast<const float4*>(krow[h] + (size_t)d0 * 4);
+        const float4 a1 = *reinterpret_cast<const float4*>(krow[h] + (size_t)(d0 + 4) * 4);
+        float f[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        u16x8 hh, ll;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float x = vt[h] ? f[i] : 0.f;
+          nsq += x * x;
+          uint16_t hb = to_bf16(x);
+          hh[i] = hb;
+          ll[i] = to_bf16(x - from_bf16(hb));
+        }
+        s_bk[h][kk][lane] = __builtin_bit_cast(bf16x8, hh);
+        s_bkl[FP32 ? h : 0][FP32 ? kk : 0][lane] = __builtin_bit_cast(bf16x8, ll);
       }
-      s_bk[h][kk][lane] = __builtin_bit_cast(bf16x8, hh);
-      s_bkl[FP32 ? h : 0][FP32 ? kk : 0][lane] = __builtin_bit_cast(bf16x8, ll);
-    } else {
-      u16x8 hh = *reinterpret_cast<const u16x8*>(kr + (size_t)d0 * 2);
-      if (!valid) hh = (u16x8)0;
+      s_nsq[wave][h][lane] = nsq;
+    }
+  } else {
+    // every key load of the wave in flight before the first is used
+    u16x8 kraw[2][8 / SCREEN_WAVES];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        float x = from_bf16(hh[i]);
-        nsq += x * x;
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int ks = 0; ks < 8 / SCREEN_WAVES; ++ks)
+        kraw[h][ks] = *reinterpret_cast<const u16x8*>(krow[h] + (size_t)((wave + ks * SCREEN_WAVES) * 16 + half * 8) * 2);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float nsq = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 8 / SCREEN_WAVES; ++ks) {
+        u16x8 hh = kraw[h][ks];
+        if (!vt[h]) hh = (u16x8)0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float x = from_bf16(hh[i]);
+          nsq += x * x;
+        }
+        s_bk[h][wave + ks * SCREEN_WAVES][lane] = __builtin_bit_cast(bf16x8, hh);
       }
-      s_bk[h][kk][lane] = __builtin_bit_cast(bf16x8, hh);
+      s_nsq[wave][h][lane] = nsq;
     }
-    }
-    s_nsq[wave][h][lane] = nsq;
   }
   __syncthreads();
   float invn[2], tx[2], ty[2];
@@ -696,8 +719,11 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
 
   for (int t = wave; t < ntiles; t += SCREEN_WAVES) {
     if (half == 0) {
-      s_ma[wave][col] = ma;
-      s_mb[wave][col] = mb;
+      // rows past the active slots: +inf idle term, never selected
+      const bool mv = t * 32 + col < kact;
+      const bool idle = (t_frame - __float_as_int(mr1.y)) > dm.t_idle;
+      s_ma[wave][col] = mv ? make_float4(mr0.x, mr0.y, mr0.z, 2.0f * mr0.w) : make_float4(0.f, 0.f, 0.f, 0.f);
+      s_mb[wave][col] = mv ? make_float2(mr1.x, idle ? lidle : 0.f) : make_float2(0.f, INFINITY);
     }
     f32x16 acc0 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     f32x16 acc1 = acc0;
