@@ -364,7 +364,9 @@ __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
 // a multiply: |c' - c| <= 3.01 u |c| against c = float32(sum / n)); the
 // bound carries that difference through cn (the norm of c' over the
 // subspace, from both halves), and the exact fallback forms its residual
-// from x, the sums s and n with the IEEE division.
+// from x, the sums s and n with the IEEE division.  hnp (|C|^2 / 2 of the
+// side's codewords, [G][CMAX]) and cmx (max norms, [G]) are the workgroup's
+// LDS copies.
 __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const float* hnp, const float* cmx,
                                        const float (&r)[2][8], const float (&w)[8], const float (&x)[2][8],
                                        const float (&sv)[2][8], float nf, float cn2h0, float cn2h1, int p,
@@ -761,6 +763,17 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 
+  // The PQ tail's per-unit constants (both sides' codeword half norms and
+  // max norms), fetched now so that the decision covers their latency and
+  // staged in LDS once the decision is done.
+  const bool pq_on = (dm.flags & (PROTOKV_FLAG_PQ | PROTOKV_FLAG_EMA_CENTRES)) == PROTOKV_FLAG_PQ && !fb.warm[b];
+  static_assert(2 * G * CMAX == 64 * 4 && 2 * G <= 4 * 4, "one float4 of half norms per lane, max norms in 4");
+  float4 pq_hn = make_float4(0.f, 0.f, 0.f, 0.f), pq_cm = pq_hn;
+  if (pq_on && wave == 0) {  // uniform
+    pq_hn = reinterpret_cast<const float4*>(ws.cbhn + unit * 2 * G * CMAX)[lane];
+    pq_cm = reinterpret_cast<const float4*>(ws.cbmax + unit * 2 * G)[lane & 3];
+  }
+
   // merge with the partner lane (other 16 rows of each slot tile), then across waves
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -890,7 +903,16 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   // histogram (integer counts: the order of the increments does not matter).
   // With EMA centres the residuals follow each token's own centre update and
   // the aggregation codes them; codebook warm-up folds count no codes.
-  if ((dm.flags & (PROTOKV_FLAG_PQ | PROTOKV_FLAG_EMA_CENTRES)) == PROTOKV_FLAG_PQ && !fb.warm[b]) {
+  if (pq_on) {
+    __syncthreads();
+    // the decision no longer reads s_top: it holds the unit's half norms
+    // [kv][g][CMAX], then its max norms [kv][g]
+    static_assert(sizeof(s_top) >= (2 * G * CMAX + 2 * G) * sizeof(float), "PQ constants fit s_top");
+    float* s_pqc = reinterpret_cast<float*>(&s_top[0][0]);
+    if (wave == 0) {
+      reinterpret_cast<float4*>(s_pqc)[lane] = pq_hn;
+      if (lane < 4) reinterpret_cast<float4*>(s_pqc + 2 * G * CMAX)[lane] = pq_cm;
+    }
     __syncthreads();
     for (int job = wave; job < 4; job += SCREEN_WAVES) {  // uniform
     const int blk = job >> 1, kv = job & 1;
@@ -969,7 +991,7 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
         }
         w[0] = wr[p][0].x; w[1] = wr[p][0].y; w[2] = wr[p][0].z; w[3] = wr[p][0].w;
         w[4] = wr[p][1].x; w[5] = wr[p][1].y; w[6] = wr[p][1].z; w[7] = wr[p][1].w;
-        const int z = pq_pair(dm, cbk, ws.cbhn + ub * G * CMAX, ws.cbmax + ub * G, r, w, xs, ss, nf, cn2[0], cn2[1],
+        const int z = pq_pair(dm, cbk, s_pqc + kv * G * CMAX, s_pqc + 2 * G * CMAX + kv * G, r, w, xs, ss, nf, cn2[0], cn2[1],
                               p, qv, lane);
         if (qv) atomicAdd(hist + (2 * p + half) * CMAX + z, 1u);
       }
