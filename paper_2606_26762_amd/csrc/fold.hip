@@ -719,6 +719,10 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     top[h].emax = 0.f;
   }
 
+  // a second token half with no token to screen (the ragged end of a frame:
+  // tokens [tile * 64 + 32, tile * 64 + 64) all below nseed or past N)
+  // skips its MFMAs and epilogue rows
+  const bool live1 = max(tile * SCREEN_TOK + 32, nseed) < min(tile * SCREEN_TOK + SCREEN_TOK, N);  // uniform
   for (int t = wave; t < ntiles; t += SCREEN_WAVES) {
     if (half == 0) {
       // rows past the active slots: +inf idle term, never selected
@@ -729,34 +733,61 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     }
     f32x16 acc0 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     f32x16 acc1 = acc0;
+    // the two halves' products (a half's MFMA chain depends only on itself)
+    auto products = [&](int h, f32x16& acc) {
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const bf16x8 xh = __builtin_bit_cast(bf16x8, ah[kk]), xl = __builtin_bit_cast(bf16x8, al[kk]);
-      const bf16x8 b0 = s_bk[0][kk][lane], b1 = s_bk[1][kk][lane];
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, b0, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, b1, acc1, 0, 0, 0);
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xl, b0, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xl, b1, acc1, 0, 0, 0);
-      if (FP32) {
-        const bf16x8 c0 = s_bkl[FP32 ? 0 : 0][FP32 ? kk : 0][lane];
-        const bf16x8 c1 = s_bkl[FP32 ? 1 : 0][FP32 ? kk : 0][lane];
-        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, c0, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, c1, acc1, 0, 0, 0);
+      for (int kk = 0; kk < 8; ++kk) {
+        const bf16x8 xh = __builtin_bit_cast(bf16x8, ah[kk]), xl = __builtin_bit_cast(bf16x8, al[kk]);
+        const bf16x8 bk = s_bk[h][kk][lane];
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, bk, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xl, bk, acc, 0, 0, 0);
+        if (FP32) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, s_bkl[FP32 ? h : 0][FP32 ? kk : 0][lane], acc, 0, 0, 0);
       }
+    };
+    if (live1) {
+      // both chains interleaved
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) {
+        const bf16x8 xh = __builtin_bit_cast(bf16x8, ah[kk]), xl = __builtin_bit_cast(bf16x8, al[kk]);
+        const bf16x8 b0 = s_bk[0][kk][lane], b1 = s_bk[1][kk][lane];
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, b1, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xl, b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xl, b1, acc1, 0, 0, 0);
+        if (FP32) {
+          const bf16x8 c0 = s_bkl[FP32 ? 0 : 0][FP32 ? kk : 0][lane];
+          const bf16x8 c1 = s_bkl[FP32 ? 1 : 0][FP32 ? kk : 0][lane];
+          acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, c0, acc0, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, c1, acc1, 0, 0, 0);
+        }
+      }
+    } else {
+      products(0, acc0);
     }
     if (t + SCREEN_WAVES < ntiles) load_tile(t + SCREEN_WAVES);  // in flight during the epilogue
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (live1) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = (r >> 2) * 8 + half * 4 + (r & 3);
-      const float4 a = s_ma[wave][m];
-      const float2 c = s_mb[wave][m];
-      const int k = t * 32 + m;
-      screen_pair<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, k, lsp, top[0]);
-      screen_pair<SQ>(acc1[r], invn[1], tx[1], ty[1], a, c, k, lsp, top[1]);
-      if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+      for (int r = 0; r < 16; ++r) {
+        const int m = (r >> 2) * 8 + half * 4 + (r & 3);
+        const float4 a = s_ma[wave][m];
+        const float2 c = s_mb[wave][m];
+        const int k = t * 32 + m;
+        screen_pair<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, k, lsp, top[0]);
+        screen_pair<SQ>(acc1[r], invn[1], tx[1], ty[1], a, c, k, lsp, top[1]);
+        if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = (r >> 2) * 8 + half * 4 + (r & 3);
+        const float4 a = s_ma[wave][m];
+        const float2 c = s_mb[wave][m];
+        screen_pair<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, t * 32 + m, lsp, top[0]);
+        if ((r & 7) == 7) __builtin_amdgcn_sched_barrier(0);
+      }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
