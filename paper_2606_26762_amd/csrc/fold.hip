@@ -577,10 +577,18 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   // token operands of the workgroup in MFMA B order [token half][k-step][lane]
   __shared__ bf16x8 s_bk[2][8][64];
   __shared__ bf16x8 s_bkl[FP32 ? 2 : 1][FP32 ? 8 : 1][64];  // low part of float32 keys
-  __shared__ float s_nsq[SCREEN_WAVES][2][64];                // partial squared key norms
-  __shared__ float4 s_ma[SCREEN_WAVES][32];                   // mu_x, mu_y, qa, 2 qb
-  __shared__ float2 s_mb[SCREEN_WAVES][32];                   // qc, lambda_idle * idle (+inf past the active slots)
-  __shared__ Top3 s_top[SCREEN_WAVES][SCREEN_TOK];
+  // The staging and slot-tile arrays (partial squared key norms; per slot
+  // row mu_x, mu_y, qa, 2 qb and qc, lambda_idle * idle, +inf past the
+  // active slots) share their LDS with the per-wave top-3 of the decision,
+  // which is written only after every wave has left the slot tiles: 18 KiB
+  // per one-wave workgroup lets eight of them share a CU.
+  constexpr int NSQ_B = SCREEN_WAVES * 2 * 64 * 4, MA_B = SCREEN_WAVES * 32 * 16, MB_B = SCREEN_WAVES * 32 * 8;
+  constexpr int TOP_B = SCREEN_WAVES * SCREEN_TOK * (int)sizeof(Top3);
+  __shared__ __align__(16) unsigned char s_u[TOP_B > NSQ_B + MA_B + MB_B ? TOP_B : NSQ_B + MA_B + MB_B];
+  float(*s_nsq)[2][64] = reinterpret_cast<float(*)[2][64]>(s_u);
+  float4(*s_ma)[32] = reinterpret_cast<float4(*)[32]>(s_u + NSQ_B);
+  float2(*s_mb)[32] = reinterpret_cast<float2(*)[32]>(s_u + NSQ_B + MA_B);
+  Top3(*s_top)[SCREEN_TOK] = reinterpret_cast<Top3(*)[SCREEN_TOK]>(s_u);
   __shared__ int s_asg[SCREEN_TOK];                           // final slot of each token of the tile
 
   // wave is a compile-time 0 for one-wave workgroups: the loops over a
@@ -590,11 +598,14 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   const int tid = threadIdx.x, lane = tid & 63, wave = SCREEN_WAVES == 1 ? 0 : tid >> 6;
   // Workgroups are dealt to the 8 XCDs round-robin; logical block lb runs on
   // XCD lb / per, so consecutive logical blocks (the tiles of one unit) share
-  // an L2.
+  // an L2.  Within an XCD the workgroups are dealt round-robin to its four
+  // shader engines as well: the tile of logical block lb is rotated by its
+  // unit so that an engine is not always handed the same tile of every unit
+  // (the ragged last tile costs about half a full one).
   const int nblk = (int)gridDim.x, per = nblk >> 3, bid = (int)blockIdx.x;
   const int lb = bid < per * 8 ? (bid & 7) * per + (bid >> 3) : bid;
-  const int tile = lb % tiles_per_unit;
   const int bu = lb / tiles_per_unit;
+  const int tile = (lb % tiles_per_unit + bu) % tiles_per_unit;
   const int b = bu / dm.units, u = bu % dm.units;
   const int N = dm.T;
   const int nseed = fb.nseed[b];
@@ -805,7 +816,10 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     pq_cm = reinterpret_cast<const float4*>(ws.cbmax + unit * 2 * G)[lane & 3];
   }
 
-  // merge with the partner lane (other 16 rows of each slot tile), then across waves
+  // merge with the partner lane (other 16 rows of each slot tile), then
+  // across waves (s_top reuses the slot-tile arrays: every wave leaves the
+  // slot tiles first)
+  if (SCREEN_WAVES > 1) __syncthreads();
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     Top3 o;
@@ -938,8 +952,8 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     __syncthreads();
     // the decision no longer reads s_top: it holds the unit's half norms
     // [kv][g][CMAX], then its max norms [kv][g]
-    static_assert(sizeof(s_top) >= (2 * G * CMAX + 2 * G) * sizeof(float), "PQ constants fit s_top");
-    float* s_pqc = reinterpret_cast<float*>(&s_top[0][0]);
+    static_assert(TOP_B >= (2 * G * CMAX + 2 * G) * (int)sizeof(float), "PQ constants fit s_top");
+    float* s_pqc = reinterpret_cast<float*>(s_u);
     if (wave == 0) {
       reinterpret_cast<float4*>(s_pqc)[lane] = pq_hn;
       if (lane < 4) reinterpret_cast<float4*>(s_pqc + 2 * G * CMAX)[lane] = pq_cm;
