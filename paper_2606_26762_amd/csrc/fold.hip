@@ -86,6 +86,44 @@ __device__ __forceinline__ void token_xy(int j, int gw, int gh, float& x, float&
   y = ((float)row + 0.5f) / (float)gh;
 }
 
+// Screening meta of a slot from its row meta, in float64.  With
+// A = sxx + rho, B = sxy, Cc = syy + rho and det = A Cc - B^2 (> 0), the
+// quadratic form of Eq. 1's Mahalanobis distance,
+// q = (Cc dx^2 - 2 B dx dy + A dy^2) / det, is (la dx + lb dy)^2 + (lc dy)^2
+// with la = sqrt(Cc / det), lb = -(B / Cc) la, lc = 1 / sqrt(Cc).
+//
+// The screen evaluates it in float32 as dx = tx - mu_x, dy = ty - mu_y,
+// u = fma(lb, dy, la dx), q' = fma(u, u, (lc dy)^2), from la, lb, lc rounded
+// to float32.  Writing U = la X + lb Y and V = lc Y for the exact
+// differences X, Y: |lb Y| <= rho |V| <= rho sqrt(q) with rho = |lb| / lc =
+// |B| / sqrt(det), so |la X| <= (1 + rho) sqrt(q).  Every rounding is
+// relative (u = 2^-24 each: dx, dy, the three factors, two products, the
+// fma), which gives |u' - U| <= (4 + 5 rho) u sqrt(q), |(lc dy)'^2 - V^2| <=
+// 7 u V^2 and |q' - q| <= (16 + 10 rho) u q to first order.  The distance
+// q' rsq(q') then carries half of that plus 2.5e-7 for the rsq and the
+// multiply; q' < 1e-30 is handled as an absolute 2e-15 in the screen.
+__device__ __forceinline__ CacheMeta cache_meta(const Dims& dm, const RowMeta& m) {
+  const double A = (double)m.sxx + dm.ridge, B = (double)m.sxy, Cc = (double)m.syy + dm.ridge;
+  const double det = A * Cc - B * B;
+  // la = Cc / sqrt(Cc det), lb = -B / sqrt(Cc det), lc = 1 / sqrt(Cc): two
+  // square roots and two divisions (a few float64 roundings, far below the
+  // float32 rounding of the factors)
+  const double rd = 1.0 / sqrt(det), rc = 1.0 / sqrt(Cc);
+  const double rho = fabs(B) * rd;
+  const double u = 0x1p-24;
+  const double eq = (16.0 + 10.0 * rho) * u * 1.02;
+  CacheMeta c;
+  c.mu_x = m.mu_x;
+  c.mu_y = m.mu_y;
+  c.la = (float)(Cc * rc * rd);
+  c.lb = (float)(-B * rc * rd);
+  c.lc = (float)rc;
+  c.last_frame = m.tau / dm.T;
+  c.active = m.n > 0 ? 1u : 0u;
+  c.eps = (float)(((dm.flags & PROTOKV_FLAG_MAH_SQUARED) ? eq : 0.5 * eq + 2.5e-7) * 1.001);
+  return c;
+}
+
 // Rewrites the screening copy of one slot from its (updated) statistics.
 // sk = this lane's two components (2*lane, 2*lane+1) of sum_k.
 __device__ void refresh_cache(const Dims& dm, float2 sk, const RowMeta& m, size_t unit, int k,
@@ -101,17 +139,7 @@ __device__ void refresh_cache(const Dims& dm, float2 sk, const RowMeta& m, size_
   *reinterpret_cast<uint32_t*>(ws.chat_hi + off) = (uint32_t)hx | ((uint32_t)hy << 16);
   *reinterpret_cast<uint32_t*>(ws.chat_lo + off) = (uint32_t)lx | ((uint32_t)ly << 16);
   if (lane == 0) {
-    double A = (double)m.sxx + dm.ridge, B = (double)m.sxy, Cc = (double)m.syy + dm.ridge;
-    double det = A * Cc - B * B;
-    CacheMeta c;
-    c.mu_x = m.mu_x;
-    c.mu_y = m.mu_y;
-    c.qa = (float)(Cc / det);
-    c.qb = (float)(-B / det);
-    c.qc = (float)(A / det);
-    c.last_frame = m.tau / dm.T;
-    c.active = m.n > 0 ? 1u : 0u;
-    c.pad = 0.f;
+    const CacheMeta c = cache_meta(dm, m);
     ws.cmeta[slot_index * CMETA_STRIDE] = c;
   }
   if (lane == 1) ws.cmeta[slot_index * CMETA_STRIDE + 1] = CacheMeta{};
@@ -139,17 +167,7 @@ __device__ void refresh_cache16(const Dims& dm, const float (&s)[8], const RowMe
   *reinterpret_cast<u16x8*>(ws.chat_hi + off) = hi;
   *reinterpret_cast<u16x8*>(ws.chat_lo + off) = lo;
   if (il == 0) {
-    double A = (double)m.sxx + dm.ridge, B = (double)m.sxy, Cc = (double)m.syy + dm.ridge;
-    double det = A * Cc - B * B;
-    CacheMeta c;
-    c.mu_x = m.mu_x;
-    c.mu_y = m.mu_y;
-    c.qa = (float)(Cc / det);
-    c.qb = (float)(-B / det);
-    c.qc = (float)(A / det);
-    c.last_frame = m.tau / dm.T;
-    c.active = m.n > 0 ? 1u : 0u;
-    c.pad = 0.f;
+    const CacheMeta c = cache_meta(dm, m);
     ws.cmeta[(unit * dm.K + k) * CMETA_STRIDE] = c;
   }
   if (il == 1) ws.cmeta[(unit * dm.K + k) * CMETA_STRIDE + 1] = CacheMeta{};
@@ -508,7 +526,7 @@ constexpr int SCREEN_TOK = 64;
 struct Top3 {
   float c1, c2, c3;  // three smallest approximate costs
   int i1, i2;        // slots of c1 and c2
-  float emax;        // largest spatial error term (in units of d_Mah)
+  float emax;        // largest relative error bound (eps) of the spatial term over the slots screened
 };
 
 __device__ __forceinline__ void top3_push(Top3& a, float c, int k) {
@@ -534,36 +552,21 @@ __device__ __forceinline__ void top3_merge(Top3& a, const Top3& b) {
 }
 
 // Approximate cost of one (token, slot) pair folded into the token's running
-// top-3.  a = (mu_x, mu_y, qa, 2 qb), c = (qc, lambda_idle * idle), with c.y =
-// +inf for rows past the active slots.  SQ: the spatial term is q itself
-// (the squared distance), whose error is eq.
+// top-3.  a = (mu_x, mu_y, la, lb), c = (lc, lambda_idle * idle), with c.y =
+// +inf for rows past the active slots.  The spatial term's error is the
+// slot's eps relative to the term (cache_meta); SQ: the term is q itself.
 template <int SQ>
 __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, float ty, const float4& a,
                                             const float2& c, int k, float lsp, Top3& top) {
   const float dx = tx - a.x, dy = ty - a.y;
-  // q = qa dx^2 + 2 qb dx dy + qc dy^2; Sigma + rho I is positive definite,
-  // so |2 qb dx dy| <= qa dx^2 + qc dy^2 = t13 and
-  // |q - q_exact| <= 16 u (t13 + |t2|) <= 33 u t13 =: eq
-  const float t13 = fmaf(a.z * dx, dx, (c.x * dy) * dy);
-  const float t2 = (a.w * dx) * dy;
-  const float q = t13 + t2;
-  const float eq = fmaf(33.0f * U32, t13, 1e-30f);
-  // d = q rsq(max(q, eq)), |d - d_exact| <= eq rsq(max(q, eq)) + 2.5e-7 d
-  // (|sqrt a - sqrt b| <= |a - b| / sqrt(max(a, b)) and <= sqrt|a - b|; raw
-  // v_rsq_f32 is accurate to ~1 ulp for the normal arguments >= 1e-30 used here)
-  const float qp = fmaxf(q, 0.f);
-  if (SQ) {
-    // |max(q, 0) - q_exact| <= eq (q_exact >= 0); the assembly's rounding
-    // relative to the term is covered as for the distance
-    const float cost = fmaf(lsp, qp, fmaf(-dot, invn, c.y));
-    top.emax = fmaxf(top.emax, fmaf(6.5e-7f, qp, eq));
-    top3_push(top, cost, k);
-    return;
-  }
-  const float rq = __builtin_amdgcn_rsqf(fmaxf(qp, eq));
-  const float dd = qp * rq;
-  const float cost = fmaf(lsp, dd, fmaf(-dot, invn, c.y));
-  top.emax = fmaxf(top.emax, fmaf(eq, rq, 6.5e-7f * dd));
+  const float u = fmaf(a.w, dy, a.z * dx);
+  const float v = c.x * dy;
+  const float q = fmaf(u, u, v * v);  // >= 0: a sum of squares
+  float term = q;
+  // raw v_rsq_f32 is accurate to ~1 ulp for the normal arguments >= 1e-30
+  // used here; below that the distance is < 2e-15
+  if (!SQ) term = q * __builtin_amdgcn_rsqf(fmaxf(q, 1e-30f));
+  const float cost = fmaf(lsp, term, fmaf(-dot, invn, c.y));
   top3_push(top, cost, k);
 }
 
@@ -627,14 +630,14 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   const CacheMeta* gmeta = ws.cmeta + unit * dm.K * CMETA_STRIDE;
 
   // operands of slot tile t: k-step kk of lane (col, half) is the 16 bytes
-  // of slot 32 t + col at dims 16 kk + 8 half (chat_offset), and the first
-  // 24 bytes of that row's meta (mu_x, mu_y, qa, qb | qc, last_frame), read
+  // of slot 32 t + col at dims 16 kk + 8 half (chat_offset), and that row's
+  // meta (mu_x, mu_y, la, lb | lc, last_frame, active, eps), read
   // unconditionally from a row clamped into range (kact >= 1 whenever a tile
   // exists) and converted only where it is used: a load under a divergent
   // branch would be waited for at once, with every operand load before it
   u16x8 ah[8], al[8];
   float4 mr0 = make_float4(0.f, 0.f, 0.f, 0.f);
-  float2 mr1 = make_float2(0.f, 0.f);
+  float4 mr1 = make_float4(0.f, 0.f, 0.f, 0.f);
   auto load_tile = [&](int t) {
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
@@ -643,9 +646,10 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     }
     const float* mp = reinterpret_cast<const float*>(gmeta + (size_t)min(t * 32 + col, kact - 1) * CMETA_STRIDE);
     mr0 = *reinterpret_cast<const float4*>(mp);
-    mr1 = *reinterpret_cast<const float2*>(mp + 4);
+    mr1 = *reinterpret_cast<const float4*>(mp + 4);
   };
-  static_assert(offsetof(CacheMeta, qc) == 16 && offsetof(CacheMeta, last_frame) == 20, "meta layout");
+  static_assert(offsetof(CacheMeta, lc) == 16 && offsetof(CacheMeta, last_frame) == 20 &&
+                offsetof(CacheMeta, eps) == 28, "meta layout");
   if (wave < ntiles) load_tile(wave);  // in flight while the keys are staged
 
   // Stage the keys: wave w (< SCREEN_WAVES by the launch) loads k-steps w, w + SCREEN_WAVES, ... of both 32-token halves
@@ -734,13 +738,15 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   // tokens [tile * 64 + 32, tile * 64 + 64) all below nseed or past N)
   // skips its MFMAs and epilogue rows
   const bool live1 = max(tile * SCREEN_TOK + 32, nseed) < min(tile * SCREEN_TOK + SCREEN_TOK, N);  // uniform
+  float emx = 0.f;  // largest eps of this lane's rows
   for (int t = wave; t < ntiles; t += SCREEN_WAVES) {
     if (half == 0) {
       // rows past the active slots: +inf idle term, never selected
       const bool mv = t * 32 + col < kact;
       const bool idle = (t_frame - __float_as_int(mr1.y)) > dm.t_idle;
-      s_ma[wave][col] = mv ? make_float4(mr0.x, mr0.y, mr0.z, 2.0f * mr0.w) : make_float4(0.f, 0.f, 0.f, 0.f);
+      s_ma[wave][col] = mv ? mr0 : make_float4(0.f, 0.f, 0.f, 0.f);
       s_mb[wave][col] = mv ? make_float2(mr1.x, idle ? lidle : 0.f) : make_float2(0.f, INFINITY);
+      emx = fmaxf(emx, mv ? mr1.w : 0.f);
     }
     f32x16 acc0 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     f32x16 acc1 = acc0;
@@ -805,6 +811,11 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 
+  // every token's spatial error bound: the largest eps over the wave's rows
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) emx = fmaxf(emx, __shfl_xor(emx, o, 64));
+  top[0].emax = top[1].emax = emx;
+
   // The PQ tail's per-unit constants (both sides' codeword half norms and
   // max norms), fetched now so that the decision covers their latency and
   // staged in LDS once the decision is done.
@@ -842,13 +853,21 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   const int j = hsel ? jt[1] : jt[0];
   const bool valid = hsel ? vt[1] : vt[0];
 
-  // |cost - cost_exact| <= E for every slot: ECOS for the dot product,
-  // 4e-7 (|cost| + 1) for rounding the assembly (|cost| <= 1 + lsp d +
-  // lambda_idle), and lsp * 1.01 * emax for the spatial term.  Slot k can
-  // be the exact argmin only if cost_k - E <= c1 + E.
-  const float E = ECOS + 4e-7f * (2.0f + lidle) + 1.01f * lsp * tp.emax;
-  const float thr = tp.c1 + 2.0f * E + 2e-6f;
-  const int nc = 1 + (tp.c2 <= thr) + (tp.c3 <= thr);
+  // |cost - cost_exact| <= E(cost) for every slot, with
+  // E(c) = E0 + ee max(c + 1.001, 0): ECOS for the dot product, 4e-7
+  // (2 + lambda_idle) for rounding the rest of the assembly, lsp 1e-14 for
+  // q' < 1e-30, and for the spatial term lsp eps_k s_k <= ee (cost + 1.001)
+  // (s_k the term: cost >= -1 + lsp s_k, since cos <= 1 and the idle term
+  // is >= 0), ee covering eps_k and the rounding of lsp s_k.  c - E(c) is
+  // increasing, so slot k can be the exact argmin only if
+  // c_k - E(c_k) <= c1 + E(c1), and if the third smallest fails that
+  // test, so does every slot after it.
+  const float E0 = ECOS + 4e-7f * (2.0f + lidle) + 1e-14f * lsp;
+  const float ee = 1.02f * tp.emax + 2.0f * U32;
+  const float thr = tp.c1 + E0 + ee * fmaxf(tp.c1 + 1.001f, 0.f) + 2e-6f;
+  const bool cand2 = tp.c2 < INFINITY && tp.c2 - (E0 + ee * fmaxf(tp.c2 + 1.001f, 0.f)) <= thr;
+  const bool cand3 = tp.c3 < INFINITY && tp.c3 - (E0 + ee * fmaxf(tp.c3 + 1.001f, 0.f)) <= thr;
+  const int nc = 1 + cand2 + cand3;
   const bool mine = valid && half == 0;
   if (mine && nc <= 1) {
     ws.assign[unit * N + j] = tp.i1;
@@ -1452,7 +1471,7 @@ __global__ __launch_bounds__(256, EMA ? 2 : (NP > 2 ? 3 : 4)) void k_aggregate(D
 constexpr int AGC_KMAX = 4096;  // slot counters held in LDS
 
 template <int FP32>
-__global__ __launch_bounds__(256) void k_aggregate_c(Dims dm, Workspace ws, FoldBatch fb, int wg_per_unit) {
+__global__ __launch_bounds__(256, 4) void k_aggregate_c(Dims dm, Workspace ws, FoldBatch fb, int wg_per_unit) {
   // per slot: token count | touched flag << 16, then the exclusive prefix of
   // both (list offset | touched index << 16); entry K holds the totals
   __shared__ uint32_t s_cnt[AGC_KMAX + 1];

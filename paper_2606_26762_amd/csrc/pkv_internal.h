@@ -41,14 +41,17 @@ struct RowMeta {
 static_assert(sizeof(RowMeta) == 32, "row meta is 32 bytes");
 
 // Screening copy of a slot (derived from its row after every update):
-// spatial mean, the inverse of (Sigma + rho I) as q = qa dx^2 + 2 qb dx dy + qc dy^2,
-// the frame index of tau and an active flag.  The unit key centre sumK/|sumK|
-// lives beside it as a two-term bf16 split (hi + lo).
+// spatial mean; the quadratic form of (Sigma + rho I)^-1 as a sum of two
+// squares, q = (la dx + lb dy)^2 + (lc dy)^2; the frame index of tau; an
+// active flag; and eps, a bound on the relative error of the screen's
+// float32 spatial term (of d_Mah, or of q itself with squared distances).
+// The unit key centre sumK/|sumK| lives beside it as a two-term bf16 split
+// (hi + lo).
 struct CacheMeta {
-  float mu_x, mu_y, qa, qb, qc;
+  float mu_x, mu_y, la, lb, lc;
   int32_t last_frame;
   uint32_t active;
-  float pad;
+  float eps;
 };
 static_assert(sizeof(CacheMeta) == 32, "cache meta is 32 bytes");
 
