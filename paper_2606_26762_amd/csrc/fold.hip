@@ -551,13 +551,18 @@ __device__ __forceinline__ void top3_merge(Top3& a, const Top3& b) {
   a.emax = fmaxf(a.emax, b.emax);
 }
 
-// Approximate cost of one (token, slot) pair folded into the token's running
-// top-3.  a = (mu_x, mu_y, la, lb), c = (lc, lambda_idle * idle), with c.y =
-// +inf for rows past the active slots.  The spatial term's error is the
-// slot's eps relative to the term (cache_meta); SQ: the term is q itself.
+// Approximate cost of one (token, slot) pair, with the slot's row m in the
+// slot tile (0..31) in its five low mantissa bits: a change of at most 31
+// ulp, which the decision's bound covers, and it lets the three smallest of
+// a tile's rows be kept by three min / median operations.  a = (mu_x, mu_y,
+// la, lb), c = (lc, lambda_idle * idle), with c.y = 3e38 (finite: the row
+// bits must not turn it into a NaN) for rows past the active slots.  The
+// spatial term's error is the slot's eps relative to the term (cache_meta);
+// SQ: the term is q itself.
+constexpr float PAST_ACTIVE = 3e38f;
 template <int SQ>
-__device__ __forceinline__ void screen_pair(float dot, float invn, float tx, float ty, const float4& a,
-                                            const float2& c, int k, float lsp, Top3& top) {
+__device__ __forceinline__ float screen_cost(float dot, float invn, float tx, float ty, const float4& a,
+                                             const float2& c, int m, float lsp) {
   const float dx = tx - a.x, dy = ty - a.y;
   const float u = fmaf(a.w, dy, a.z * dx);
   const float v = c.x * dy;
@@ -567,7 +572,23 @@ __device__ __forceinline__ void screen_pair(float dot, float invn, float tx, flo
   // used here; below that the distance is < 2e-15
   if (!SQ) term = q * __builtin_amdgcn_rsqf(fmaxf(q, 1e-30f));
   const float cost = fmaf(lsp, term, fmaf(-dot, invn, c.y));
-  top3_push(top, cost, k);
+  return __uint_as_float((__float_as_uint(cost) & ~31u) | (uint32_t)m);
+}
+
+// Three smallest row-tagged costs of a slot tile.
+struct Low3 {
+  float c1, c2, c3;
+};
+__device__ __forceinline__ void low3_push(Low3& a, float c) {
+  a.c3 = __builtin_amdgcn_fmed3f(c, a.c2, a.c3);
+  a.c2 = __builtin_amdgcn_fmed3f(c, a.c1, a.c2);
+  a.c1 = fminf(a.c1, c);
+}
+// ... folded into the token's running top-3 with their slot ids
+__device__ __forceinline__ void low3_fold(Top3& top, const Low3& l, int k0) {
+  top3_push(top, l.c1, k0 + (int)(__float_as_uint(l.c1) & 31u));
+  top3_push(top, l.c2, k0 + (int)(__float_as_uint(l.c2) & 31u));
+  top3_push(top, l.c3, k0 + (int)(__float_as_uint(l.c3) & 31u));
 }
 
 // SW waves per workgroup, two waves per SIMD either way: four for small
@@ -745,7 +766,7 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
       const bool mv = t * 32 + col < kact;
       const bool idle = (t_frame - __float_as_int(mr1.y)) > dm.t_idle;
       s_ma[wave][col] = mv ? mr0 : make_float4(0.f, 0.f, 0.f, 0.f);
-      s_mb[wave][col] = mv ? make_float2(mr1.x, idle ? lidle : 0.f) : make_float2(0.f, INFINITY);
+      s_mb[wave][col] = mv ? make_float2(mr1.x, idle ? lidle : 0.f) : make_float2(0.f, PAST_ACTIVE);
       emx = fmaxf(emx, mv ? mr1.w : 0.f);
     }
     f32x16 acc0 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -785,26 +806,29 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    Low3 l0 = {INFINITY, INFINITY, INFINITY}, l1 = l0;
     if (live1) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = (r >> 2) * 8 + half * 4 + (r & 3);
         const float4 a = s_ma[wave][m];
         const float2 c = s_mb[wave][m];
-        const int k = t * 32 + m;
-        screen_pair<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, k, lsp, top[0]);
-        screen_pair<SQ>(acc1[r], invn[1], tx[1], ty[1], a, c, k, lsp, top[1]);
+        low3_push(l0, screen_cost<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, m, lsp));
+        low3_push(l1, screen_cost<SQ>(acc1[r], invn[1], tx[1], ty[1], a, c, m, lsp));
         if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
       }
+      low3_fold(top[0], l0, t * 32);
+      low3_fold(top[1], l1, t * 32);
     } else {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = (r >> 2) * 8 + half * 4 + (r & 3);
         const float4 a = s_ma[wave][m];
         const float2 c = s_mb[wave][m];
-        screen_pair<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, t * 32 + m, lsp, top[0]);
+        low3_push(l0, screen_cost<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, m, lsp));
         if ((r & 7) == 7) __builtin_amdgcn_sched_barrier(0);
       }
+      low3_fold(top[0], l0, t * 32);
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -858,15 +882,17 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   // (2 + lambda_idle) for rounding the rest of the assembly, lsp 1e-14 for
   // q' < 1e-30, and for the spatial term lsp eps_k s_k <= ee (cost + 1.001)
   // (s_k the term: cost >= -1 + lsp s_k, since cos <= 1 and the idle term
-  // is >= 0), ee covering eps_k and the rounding of lsp s_k.  c - E(c) is
-  // increasing, so slot k can be the exact argmin only if
+  // is >= 0), ee covering eps_k and the rounding of lsp s_k; the row tag
+  // (<= 31 ulp = 3.7e-6 |c|) adds 4.2e-6 to E0 and 3.8e-6 to ee.  c - E(c)
+  // is increasing, so slot k can be the exact argmin only if
   // c_k - E(c_k) <= c1 + E(c1), and if the third smallest fails that
-  // test, so does every slot after it.
-  const float E0 = ECOS + 4e-7f * (2.0f + lidle) + 1e-14f * lsp;
-  const float ee = 1.02f * tp.emax + 2.0f * U32;
+  // test, so does every slot after it.  Costs of 1e38 and more are rows
+  // past the active slots.
+  const float E0 = ECOS + 4e-7f * (2.0f + lidle) + 1e-14f * lsp + 4.2e-6f;
+  const float ee = 1.02f * tp.emax + 2.0f * U32 + 3.8e-6f;
   const float thr = tp.c1 + E0 + ee * fmaxf(tp.c1 + 1.001f, 0.f) + 2e-6f;
-  const bool cand2 = tp.c2 < INFINITY && tp.c2 - (E0 + ee * fmaxf(tp.c2 + 1.001f, 0.f)) <= thr;
-  const bool cand3 = tp.c3 < INFINITY && tp.c3 - (E0 + ee * fmaxf(tp.c3 + 1.001f, 0.f)) <= thr;
+  const bool cand2 = tp.c2 < 1e38f && tp.c2 - (E0 + ee * fmaxf(tp.c2 + 1.001f, 0.f)) <= thr;
+  const bool cand3 = tp.c3 < 1e38f && tp.c3 - (E0 + ee * fmaxf(tp.c3 + 1.001f, 0.f)) <= thr;
   const int nc = 1 + cand2 + cand3;
   const bool mine = valid && half == 0;
   if (mine && nc <= 1) {
