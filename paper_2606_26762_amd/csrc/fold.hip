@@ -365,13 +365,21 @@ __device__ __forceinline__ bool better(double c1, int k1, double c2, int k2) {
 // ---------------------------------------------------------------------------
 constexpr int CBW = CMAX * DP;  // floats per (K/V, subspace) codebook block
 
-// v -> hi + lo with hi = bf16(v), lo = bf16(v - hi), both round to nearest even
+// v -> hi + lo with hi = bf16(v), lo = bf16(v - hi), both round to nearest
+// even; two values per packed conversion, hi read back from its bits
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const __bf16 h = (__bf16)v[i];
-    hi[i] = h;
-    lo[i] = (__bf16)(v[i] - (float)h);
+  for (int i = 0; i < 8; i += 2) {
+    const bf16x2 h = __builtin_convertvector((f32x2){v[i], v[i + 1]}, bf16x2);
+    const uint32_t hb = __builtin_bit_cast(uint32_t, h);
+    const bf16x2 l = __builtin_convertvector(
+        (f32x2){v[i] - __uint_as_float(hb << 16), v[i + 1] - __uint_as_float(hb & 0xFFFF0000u)}, bf16x2);
+    hi[i] = h[0];
+    hi[i + 1] = h[1];
+    lo[i] = l[0];
+    lo[i + 1] = l[1];
   }
 }
 
@@ -422,28 +430,24 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
   acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1h, b1l, acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1l, b1h, acc, 0, 0, 0);
 
-  // best two scores per subspace: 8 codewords here, 8 in the partner lane
+  // best two scores per subspace: 8 codewords here, 8 in the partner lane.
+  // Each score carries its codeword in its four low mantissa bits (at most
+  // 15 ulp, covered by F below), so max / med3 keep the winner's id too;
+  // unused codewords start from -3e38, finite, so no tag makes a NaN.
   float bst1[2], bst2[2];
-  int bid[2];
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub) {
     float v1 = -INFINITY, v2 = -INFINITY;
-    int i1 = 0;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      const float v = acc[sub * 8 + q];
-      const int cw = (q >> 2) * 8 + half * 4 + (q & 3);
-      const int mk = -(int)(v > v1);
+      const uint32_t cw = (q >> 2) * 8 + half * 4 + (q & 3);
+      const float v = __uint_as_float((__float_as_uint(acc[sub * 8 + q]) & ~15u) | cw);
       v2 = __builtin_amdgcn_fmed3f(v, v1, v2);
       v1 = fmaxf(v1, v);
-      i1 = (cw & mk) | (i1 & ~mk);
     }
     const float o1 = xor32(v1), o2 = xor32(v2);
-    const int oi = xor32(i1);
-    const bool take = o1 > v1 || (o1 == v1 && oi < i1);
     bst2[sub] = fmaxf(fminf(v1, o1), fmaxf(v2, o2));
     bst1[sub] = fmaxf(v1, o1);
-    bid[sub] = take ? oi : i1;
   }
   // lane half 0 settles g0, half 1 settles g1
   const int g = half ? g1 : g0;
@@ -454,7 +458,8 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
   // operands leaves <= 3 * 2^-16 |r_u| |C_u| per product (the dropped
   // lo * lo and the two split remainders), summed <= 4.6e-5 |r| |C|; the
   // float32 accumulation over three MFMAs adds <= 51 u (|C|^2 / 2 +
-  // |r| |C|), the rounded |C|^2 / 2 <= 9 u |C|^2.  The float32 sequential
+  // |r| |C|), the rounded |C|^2 / 2 <= 9 u |C|^2, the codeword tag <= 15 ulp
+  // = 1.8e-6 (|C|^2 / 2 + |r| |C|).  The float32 sequential
   // distances of the codewords differ from the exact ones by <= 19 u D,
   // D <= |r|^2 - 2 score of the runner-up (dlead).  Each term is taken with
   // margin.
@@ -463,9 +468,9 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
   const float rn = sqrtf(rn2) * 1.0001f, cm = cmx[g];
   const float dlead = fmaxf(rn * rn - 2.0f * v2, 0.f) + 1e-30f;
   // ... and <= 3.1 u |c| |C| from the centre c' (taken as 2e-7 |c'| |C|)
-  const float F = fmaf(fmaf(5.2e-5f, rn, 2e-7f * sqrtf(cn2) * 1.0001f), cm,
-                       fmaf(2.5e-6f, cm * cm, 1.2e-6f * dlead));
-  int z = half ? bid[1] : bid[0];
+  const float F = fmaf(fmaf(5.4e-5f, rn, 2e-7f * sqrtf(cn2) * 1.0001f), cm,
+                       fmaf(3.5e-6f, cm * cm, 1.2e-6f * dlead));
+  int z = (int)(__float_as_uint(v1) & 15u);
   // not separated: the float32 sequential distances decide, one flagged
   // (token, subspace) at a time for the whole wave (lane % 16 = codeword)
   unsigned long long fm = __ballot(valid && !(v1 - v2 > 2.0f * F));
@@ -1073,11 +1078,11 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
           for (int i = 0; i < 8; ++i) {
             const float c = sv[i] * inv;
             c2 = fmaf(c, c, c2);
-            r[q][i] = qv ? x[i] - c : 0.f;
+            r[q][i] = x[i] - c;  // garbage for lanes past the frame, which code nothing
             xs[q][i] = x[i];
             ss[q][i] = sv[i];
           }
-          cn2[q] = qv ? c2 : 0.f;
+          cn2[q] = c2;
         }
         w[0] = wr[p][0].x; w[1] = wr[p][0].y; w[2] = wr[p][0].z; w[3] = wr[p][0].w;
         w[4] = wr[p][1].x; w[5] = wr[p][1].y; w[6] = wr[p][1].z; w[7] = wr[p][1].w;

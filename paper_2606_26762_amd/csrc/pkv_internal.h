@@ -96,7 +96,7 @@ struct Workspace {
   CacheMeta* cmeta;           // [streams][units][K][CMETA_STRIDE] (entry 0 used)
   int32_t* assign;            // [streams][units][T]
   float* codebooks;           // [streams][units][2][G][CMAX][DP]
-  float* cbhn;                // [streams][units][2][G][CMAX]: |C|^2 / 2 (+inf for codewords >= C)
+  float* cbhn;                // [streams][units][2][G][CMAX]: |C|^2 / 2 (3e38 for codewords >= C)
   float* cbmax;               // [streams][units][2][G]: an upper bound of max_c |C|
   uint8_t* pk;                // [units][K*S][D] kv dtype (synthesis of one stream)
   uint8_t* pv;

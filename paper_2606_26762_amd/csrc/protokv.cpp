@@ -123,7 +123,7 @@ void codebook_tables(const std::vector<float>& cb, int C, std::vector<float>& hn
     for (int cc = 0; cc < CMAX; ++cc) {
       float n2 = 0.f;
       for (int q = 0; q < DP; ++q) n2 = std::fma(cb[(blk * CMAX + cc) * DP + q], cb[(blk * CMAX + cc) * DP + q], n2);
-      hn[blk * CMAX + cc] = cc < C ? 0.5f * n2 : INFINITY;
+      hn[blk * CMAX + cc] = cc < C ? 0.5f * n2 : 3e38f;  // finite: the encoder tags scores
       if (cc < C) m = std::max(m, n2);
     }
     cmax[blk] = std::sqrt(m) * 1.0001f;

@@ -183,7 +183,7 @@ __global__ __launch_bounds__(64) void k_warm_kmeans(Dims dm, Workspace ws, Kmean
   float n2 = 0.f;
   if (lane < C)
     for (int d = 0; d < DP; ++d) n2 = fmaf(s_c[lane][d], s_c[lane][d], n2);
-  if (lane < CMAX) ws.cbhn[((unit * 2 + side) * G + g) * CMAX + lane] = lane < C ? 0.5f * n2 : INFINITY;
+  if (lane < CMAX) ws.cbhn[((unit * 2 + side) * G + g) * CMAX + lane] = lane < C ? 0.5f * n2 : 3e38f;
   float m = lane < C ? n2 : 0.f;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
