@@ -393,7 +393,7 @@ __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
 // from x, the sums s and n with the IEEE division.  hnp (|C|^2 / 2 of the
 // side's codewords, [G][CMAX]) and cmx (max norms, [G]) are the workgroup's
 // LDS copies.
-__device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const float* hnp, const float* cmx,
+__device__ __forceinline__ int pq_pair(const Dims& dm, float pinf, float ninf, const float* cbk, const float* hnp, const float* cmx,
                                        const float (&r)[2][8], const float (&w)[8], const float (&x)[2][8],
                                        const float (&sv)[2][8], float nf, float cn2h0, float cn2h1, int p,
                                        bool valid, int lane) {
@@ -443,11 +443,11 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, const float* cbk, const f
       const uint32_t cw = (q >> 2) * 8 + half * 4 + (q & 3);
       const float v = __uint_as_float((__float_as_uint(acc[sub * 8 + q]) & ~15u) | cw);
       v2 = __builtin_amdgcn_fmed3f(v, v1, v2);
-      v1 = fmaxf(v1, v);
+      v1 = __builtin_amdgcn_fmed3f(v, v1, pinf);  // max without quieting the tagged value (as low3_push)
     }
     const float o1 = xor32(v1), o2 = xor32(v2);
-    bst2[sub] = fmaxf(fminf(v1, o1), fmaxf(v2, o2));
-    bst1[sub] = fmaxf(v1, o1);
+    bst2[sub] = __builtin_amdgcn_fmed3f(__builtin_amdgcn_fmed3f(v1, o1, ninf), __builtin_amdgcn_fmed3f(v2, o2, pinf), pinf);
+    bst1[sub] = __builtin_amdgcn_fmed3f(v1, o1, pinf);
   }
   // lane half 0 settles g0, half 1 settles g1
   const int g = half ? g1 : g0;
@@ -584,10 +584,18 @@ __device__ __forceinline__ float screen_cost(float dot, float invn, float tx, fl
 struct Low3 {
   float c1, c2, c3;
 };
-__device__ __forceinline__ void low3_push(Low3& a, float c) {
+// The minimum is taken as a median with -inf, held in a register the
+// compiler cannot see into: fminf, or a median with a constant infinity that
+// it folds back into one, would first quiet the tagged operand (one more
+// instruction per pair).
+__device__ __forceinline__ float opaque(float x) {
+  asm("" : "+v"(x));
+  return x;
+}
+__device__ __forceinline__ void low3_push(Low3& a, float ninf, float c) {
   a.c3 = __builtin_amdgcn_fmed3f(c, a.c2, a.c3);
   a.c2 = __builtin_amdgcn_fmed3f(c, a.c1, a.c2);
-  a.c1 = fminf(a.c1, c);
+  a.c1 = __builtin_amdgcn_fmed3f(c, a.c1, ninf);
 }
 // ... folded into the token's running top-3 with their slot ids
 __device__ __forceinline__ void low3_fold(Top3& top, const Low3& l, int k0) {
@@ -765,6 +773,7 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   // skips its MFMAs and epilogue rows
   const bool live1 = max(tile * SCREEN_TOK + 32, nseed) < min(tile * SCREEN_TOK + SCREEN_TOK, N);  // uniform
   float emx = 0.f;  // largest eps of this lane's rows
+  const float ninf = opaque(-INFINITY);
   for (int t = wave; t < ntiles; t += SCREEN_WAVES) {
     if (half == 0) {
       // rows past the active slots: +inf idle term, never selected
@@ -818,8 +827,8 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
         const int m = (r >> 2) * 8 + half * 4 + (r & 3);
         const float4 a = s_ma[wave][m];
         const float2 c = s_mb[wave][m];
-        low3_push(l0, screen_cost<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, m, lsp));
-        low3_push(l1, screen_cost<SQ>(acc1[r], invn[1], tx[1], ty[1], a, c, m, lsp));
+        low3_push(l0, ninf, screen_cost<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, m, lsp));
+        low3_push(l1, ninf, screen_cost<SQ>(acc1[r], invn[1], tx[1], ty[1], a, c, m, lsp));
         if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
       }
       low3_fold(top[0], l0, t * 32);
@@ -830,7 +839,7 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
         const int m = (r >> 2) * 8 + half * 4 + (r & 3);
         const float4 a = s_ma[wave][m];
         const float2 c = s_mb[wave][m];
-        low3_push(l0, screen_cost<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, m, lsp));
+        low3_push(l0, ninf, screen_cost<SQ>(acc0[r], invn[0], tx[0], ty[0], a, c, m, lsp));
         if ((r & 7) == 7) __builtin_amdgcn_sched_barrier(0);
       }
       low3_fold(top[0], l0, t * 32);
@@ -1050,6 +1059,7 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
       const float nf = (float)*reinterpret_cast<const uint32_t*>(srow + ROW_META);
       const float inv = 1.0f / nf;
       uint32_t* hist = reinterpret_cast<uint32_t*>(ws.bank + (unit * dm.K + slot) * ROW + (kv ? ROW_HV : ROW_HK));
+      const float pinf = opaque(INFINITY);
 #pragma unroll
       for (int p = 0; p < G / 2; ++p) {
         float r[2][8], w[8], xs[2][8], ss[2][8], cn2[2];
@@ -1086,7 +1096,7 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
         }
         w[0] = wr[p][0].x; w[1] = wr[p][0].y; w[2] = wr[p][0].z; w[3] = wr[p][0].w;
         w[4] = wr[p][1].x; w[5] = wr[p][1].y; w[6] = wr[p][1].z; w[7] = wr[p][1].w;
-        const int z = pq_pair(dm, cbk, s_pqc + kv * G * CMAX, s_pqc + 2 * G * CMAX + kv * G, r, w, xs, ss, nf, cn2[0], cn2[1],
+        const int z = pq_pair(dm, pinf, ninf, cbk, s_pqc + kv * G * CMAX, s_pqc + 2 * G * CMAX + kv * G, r, w, xs, ss, nf, cn2[0], cn2[1],
                               p, qv, lane);
         if (qv) atomicAdd(hist + (2 * p + half) * CMAX + z, 1u);
       }
