@@ -100,8 +100,8 @@ __device__ __forceinline__ void token_xy(int j, int gw, int gh, float& x, float&
 // relative (u = 2^-24 each: dx, dy, the three factors, two products, the
 // fma), which gives |u' - U| <= (4 + 5 rho) u sqrt(q), |(lc dy)'^2 - V^2| <=
 // 7 u V^2 and |q' - q| <= (16 + 10 rho) u q to first order.  The distance
-// q' rsq(q') then carries half of that plus 2.5e-7 for the rsq and the
-// multiply; q' < 1e-30 is handled as an absolute 2e-15 in the screen.
+// sqrt(q') (the raw v_sqrt_f32, about 1 ulp) then carries half of that plus
+// 2.5e-7; q' < 1e-30 is handled as an absolute 2e-15 in the screen.
 __device__ __forceinline__ CacheMeta cache_meta(const Dims& dm, const RowMeta& m) {
   const double A = (double)m.sxx + dm.ridge, B = (double)m.sxy, Cc = (double)m.syy + dm.ridge;
   const double det = A * Cc - B * B;
@@ -573,9 +573,9 @@ __device__ __forceinline__ float screen_cost(float dot, float invn, float tx, fl
   const float v = c.x * dy;
   const float q = fmaf(u, u, v * v);  // >= 0: a sum of squares
   float term = q;
-  // raw v_rsq_f32 is accurate to ~1 ulp for the normal arguments >= 1e-30
-  // used here; below that the distance is < 2e-15
-  if (!SQ) term = q * __builtin_amdgcn_rsqf(fmaxf(q, 1e-30f));
+  // raw v_sqrt_f32 (about 1 ulp; the bound allows 2.5e-7 relative, and
+  // q' < 1e-30 an absolute 2e-15)
+  if (!SQ) term = __builtin_amdgcn_sqrtf(q);
   const float cost = fmaf(lsp, term, fmaf(-dot, invn, c.y));
   return __uint_as_float((__float_as_uint(cost) & ~31u) | (uint32_t)m);
 }

@@ -3,13 +3,13 @@ Mahalanobis distance).
 
 The screen writes the quadratic form of (Sigma + rho I)^-1 as
 q = (la dx + lb dy)^2 + (lc dy)^2, evaluates it in float32 as
-u = fma(lb, dy, la * dx), q' = fma(u, u, (lc * dy)^2), d' = q' rsq(max(q', 1e-30)),
+u = fma(lb, dy, la * dx), q' = fma(u, u, (lc * dy)^2), d' = sqrt(q') (raw, ~1 ulp),
 and bounds the error by eps_k * d + 2e-15 with
 eps_k = 1.02 (8 + 5 rho) 2^-24 + 2.5e-7 (squared distances:
 1.02 (16 + 10 rho) 2^-24 on q), rho = |B| / sqrt(det), stored rounded up by
 0.1%.  This test replays that float32 sequence in numpy (a fused multiply-add
-as one rounding of the exact float64 value, the hardware rsq as the correctly
-rounded reciprocal square root moved one ulp either way) on random
+as one rounding of the exact float64 value, the hardware square root as the
+correctly rounded one moved one ulp either way) on random
 covariances from isotropic to nearly singular and positions from the centre
 itself to far away, and checks every result against the float64 distance
 from the same float32 positions.  It pins the derivation, not the kernel: the
@@ -42,7 +42,7 @@ def meta(sxx, sxy, syy, ridge, squared):
     return f32(Cc * rc * rd), f32(-B * rc * rd), f32(rc), f32(eps), (A, B, Cc, det)
 
 
-def screen_term(tx, ty, mx, my, la, lb, lc, squared, rsq_shift):
+def screen_term(tx, ty, mx, my, la, lb, lc, squared, sqrt_shift):
     dx = f32(tx - mx)  # float32 subtraction: exact difference, one rounding
     dy = f32(ty - my)
     u = fma32(lb, dy, f32(la * dx))
@@ -50,11 +50,9 @@ def screen_term(tx, ty, mx, my, la, lb, lc, squared, rsq_shift):
     q = fma32(u, u, f32(v * v))
     if squared:
         return q
-    qm = np.maximum(q, np.float32(1e-30))
-    r = f32(1.0 / np.sqrt(qm.astype(np.float64)))
-    r = np.where(rsq_shift > 0, np.nextafter(r, np.float32(np.inf)),
-                 np.where(rsq_shift < 0, np.nextafter(r, np.float32(0)), r)).astype(np.float32)
-    return f32(q * r)
+    d = f32(np.sqrt(q.astype(np.float64)))
+    return np.where(sqrt_shift > 0, np.nextafter(d, np.float32(np.inf)),
+                    np.where((sqrt_shift < 0) & (d > 0), np.nextafter(d, np.float32(0)), d)).astype(np.float32)
 
 
 def exact_term(tx, ty, mx, my, A, B, Cc, det, squared):
