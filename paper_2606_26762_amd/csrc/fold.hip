@@ -518,9 +518,11 @@ __device__ __forceinline__ int pq_pair(const Dims& dm, float pinf, float ninf, c
 // columns; unit centres as a hi + lo bf16 split read in MFMA operand order,
 // so each k-step is one contiguous 1 KiB load per wave, and the next tile's
 // loads are in flight during this tile's epilogue).  The float32 epilogue
-// approximates Eq. 1 per (token, slot) with a rigorous bound on its error;
-// each lane keeps, per token, the three smallest approximate costs (slots of
-// the first two) and the largest spatial error term.  A token whose interval
+// approximates Eq. 1 per (token, slot) with a rigorous bound on its error
+// (relative to the cost, from the largest per-slot bound of the spatial
+// term over the unit's slots); each lane keeps, per token, the three
+// smallest approximate costs (slots of the first two), folded in from each
+// slot tile's three smallest row-tagged costs.  A token whose interval
 // admits one slot is assigned directly; two candidates are re-scored exactly
 // in float64; three or more send the token to an exact float64 pass over
 // every slot.  Workgroups are placed so that the tiles of one unit run on the
@@ -615,7 +617,7 @@ __global__ __launch_bounds__(64 * SW, 2) void k_screen(Dims dm, Workspace ws, Fo
   __shared__ bf16x8 s_bk[2][8][64];
   __shared__ bf16x8 s_bkl[FP32 ? 2 : 1][FP32 ? 8 : 1][64];  // low part of float32 keys
   // The staging and slot-tile arrays (partial squared key norms; per slot
-  // row mu_x, mu_y, qa, 2 qb and qc, lambda_idle * idle, +inf past the
+  // row mu_x, mu_y, la, lb and lc, lambda_idle * idle, 3e38 past the
   // active slots) share their LDS with the per-wave top-3 of the decision,
   // which is written only after every wave has left the slot tiles: 18 KiB
   // per one-wave workgroup lets eight of them share a CU.
