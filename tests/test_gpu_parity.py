@@ -88,6 +88,34 @@ def test_squared_mahalanobis(wl_name):
           f"readout err {worst:.2e}")
 
 
+@pytest.mark.parametrize("kv,squared", [("bf16", True), ("fp32", False)])
+def test_one_wave_screen_options(kv, squared):
+    """The one-wave screen form (launches of 8 192 tiles or more: here 64
+    streams x 32 units x 4 tiles of a 16x16 frame) with squared distances on
+    bf16 keys and with float32 keys; K = 80, so the last slot tile is half
+    rows past the active slots.  Two units of two streams are
+    followed from the first frame: assignments every fold, banks bitwise,
+    then the readout of each followed stream."""
+    h = H()
+    wl = W.WORKLOADS["multi"].with_(num_layers=1, num_kv_heads=32, num_q_heads=32, grid_h=16, grid_w=16,
+                                    frames=12, window_frames=2, capacity=80, query_tokens=4, kv_dtype=kv)
+    tracked, sample = [0, 63], [0, 31]
+    h.log(f"case: one-wave screen {wl.name} kv={kv} squared={squared} streams={wl.streams} "
+          f"units={wl.units} T={wl.tokens_per_frame} K={wl.capacity}")
+    assert wl.streams * wl.units * ((wl.tokens_per_frame + 63) // 64) >= 8192
+    pair = h.Pair(wl, sample=sample, streams=wl.streams, oracle_streams=tracked, cb_samples=256, cb_iters=4,
+                  mah_squared=squared)
+    for f in range(wl.frames):
+        pair.step()
+    for s in tracked:
+        pair.check_bank(stream=s, bitwise=True)
+        pseudo = pair.synthesize(stream=s)
+        worst, *_ = pair.attend(pair.query(np.random.default_rng(40 + s)), pseudo, stream=s)
+        h.log(f"stream {s}: readout err {worst:.2e}")
+    h.log(f"assignments {pair.assign_checked}, near ties {pair.near_ties} (excused {pair.excused})")
+    assert pair.assign_checked == len(tracked) * len(sample) * (wl.frames - wl.window_frames) * wl.tokens_per_frame
+
+
 @pytest.mark.parametrize("case", ["7b", "tiny", "7b+rope", "ragged"])
 def test_variance_aware_allocation(case):
     """PROTOKV_FLAG_VAR_ALLOC (appendix "Dynamic Pseudo-Token Allocation"):
